@@ -1,0 +1,342 @@
+"""Pins for the CPU oracle: hand-worked values, brute force, library special cases, exact adjoint
+identities and invariants. None of these re-run the oracle's own formula."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.signal
+
+from oracle import oracle as O
+from tests import bruteforce as BF
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def gold(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+MODES = {"floor": O.FLOOR, "trunc": O.TRUNC}
+
+
+# ---------------------------------------------------------------- hand-worked tables
+
+def test_division_table():
+    g = gold("division.json")
+    for z, fl, tr in g["rows"]:
+        assert int(O.nitro_scaling(z, g["sf"], O.FLOOR)) == fl
+        assert int(O.nitro_scaling(z, g["sf"], O.TRUNC)) == tr
+
+
+def test_division_against_python_semantics():
+    # Python's // is floor division by language definition; int(a / b) is not used.
+    rng = np.random.default_rng(1)
+    a = np.concatenate([rng.integers(-(1 << 40), 1 << 40, 2000), np.arange(-50, 51)])
+    for d in (1, 2, 3, 7, 10, 512, 2304, 589824, 327680, 8192000000):
+        q = O.idiv(a, d, O.FLOOR)
+        t = O.idiv(a, d, O.TRUNC)
+        for ai, qi, ti in zip(a.tolist(), q.tolist(), t.tolist()):
+            assert qi == ai // d
+            assert qi * d <= ai < (qi + 1) * d
+            # truncation: |t| = floor(|a| / d) with the sign of a
+            assert ti == (abs(ai) // d) * (1 if ai >= 0 else -1)
+
+
+def test_relu_table():
+    g = gold("relu.json")
+    for mode in ("floor", "trunc"):
+        m = MODES[mode]
+        assert O.relu_mu(g["alpha_inv"], m) == g[mode]["mu"]
+        out = O.nitro_relu(np.array(g[mode]["x"]), g["alpha_inv"], m)
+        assert out.tolist() == g[mode]["out"]
+
+
+def test_mu_table():
+    t = gold("relu.json")["mu_table"]
+    for a, fl, tr in zip(t["alpha_inv"], t["floor"], t["trunc"]):
+        assert O.relu_mu(a, O.FLOOR) == fl
+        assert O.relu_mu(a, O.TRUNC) == tr
+
+
+def test_relu_grad_table():
+    g = gold("relu_grad.json")
+    for zs, d, fl, tr in g["rows"]:
+        assert int(O.nitro_relu_grad(d, zs, g["alpha_inv"], O.FLOOR)) == fl
+        assert int(O.nitro_relu_grad(d, zs, g["alpha_inv"], O.TRUNC)) == tr
+
+
+def test_sgd_table():
+    g = gold("sgd.json")
+    for w, d, gam, lam, fl, tr in g["rows"]:
+        assert int(O.integer_sgd(np.array(w), np.array(d), gam, lam, O.FLOOR)) == fl
+        assert int(O.integer_sgd(np.array(w), np.array(d), gam, lam, O.TRUNC)) == tr
+
+
+def test_kaiming_table():
+    g = gold("kaiming.json")
+    for f, isq, b in zip(g["fan_in"], g["isqrt"], g["bound"]):
+        assert math.isqrt(f) == isq
+        assert O.kaiming_bound(f) == b
+
+
+def test_scaling_factors_and_af():
+    # SF = 2^8 * fan_in (section 3.2.1); AF = 2^6 * G (Eq. 6)
+    assert O.scaling_factor_conv(3, 1) == 2304
+    assert O.scaling_factor_conv(3, 256) == 589824
+    assert O.scaling_factor_linear(784) == 200704
+    assert O.amplification_factor(10) == 640
+    assert O.amplification_factor(100) == 6400
+
+
+@pytest.mark.parametrize("mode", ["floor", "trunc"])
+def test_mini_step(mode):
+    """A complete iteration on a hand-worked one-block integer MLP."""
+    g = gold("mini_step.json")
+    exp = g[mode]
+    m = MODES[mode]
+    hp = O.Hyper(gamma_inv=g["gamma_inv"], lambda_inv_fw=g["lambda_inv_fw"],
+                 lambda_inv_lr=g["lambda_inv_lr"], alpha_inv=g["alpha_inv"], n_classes=g["G"], mode=m)
+    net = O.OracleNet([(1, False, True)], False,
+                      [np.array(g["W1"], np.int32), np.array(g["Wlr"], np.int32)], hp)
+    st = net.train_step(np.array(g["x"], np.int8), np.array(g["label"], np.int32))
+    b = st.blocks[0]
+    assert b.layers[0].zs.tolist() == exp["zs"]
+    assert b.out.tolist() == exp["a"]
+    assert b.yhat.tolist() == exp["yhat"]
+    assert b.e.tolist() == exp["e"]
+    assert b.dw_lr.tolist() == exp["dWlr"]
+    assert b.delta_fw.tolist() == exp["delta_fw"]
+    assert b.g[0].tolist() == exp["g"]
+    assert b.dw[0].tolist() == exp["dW1"]
+    assert net.w[1].tolist() == exp["Wlr_new"]
+    assert net.w[0].tolist() == exp["W1_new"]
+
+
+# ---------------------------------------------------------------- brute force, tiny shapes
+
+def _rand(rng, shape, lo, hi, dtype=np.int64):
+    return rng.integers(lo, hi, size=shape, endpoint=True).astype(dtype)
+
+
+@pytest.mark.parametrize("N,H,W,C,CO", [(1, 1, 1, 1, 1), (1, 3, 4, 2, 3), (2, 5, 3, 3, 2),
+                                        (2, 4, 4, 4, 5), (1, 6, 6, 1, 2)])
+def test_conv_against_bruteforce(N, H, W, C, CO):
+    rng = np.random.default_rng(N * 1000 + H * 100 + W * 10 + C)
+    x = _rand(rng, (N, H, W, C), -127, 127, np.int8)
+    w = _rand(rng, (CO, 3, 3, C), -40000, 40000, np.int32)
+    g = _rand(rng, (N, H, W, CO), -70000, 70000)
+    assert O.conv3x3_fwd(x, w).tolist() == BF.conv_fwd(x.tolist(), w.tolist())
+    assert O.conv3x3_dx(g, w).tolist() == BF.conv_dx(g.tolist(), w.tolist())
+    assert O.conv3x3_dw(g, x).tolist() == BF.conv_dw(g.tolist(), x.tolist())
+
+
+@pytest.mark.parametrize("N,K,M", [(1, 1, 1), (3, 7, 2), (4, 5, 10), (2, 16, 3)])
+def test_linear_against_bruteforce(N, K, M):
+    rng = np.random.default_rng(N * 100 + K * 10 + M)
+    x = _rand(rng, (N, K), -127, 127, np.int8)
+    w = _rand(rng, (M, K), -(1 << 20), 1 << 20, np.int32)
+    e = _rand(rng, (N, M), -(1 << 20), 1 << 20)
+    assert O.linear_fwd(x, w).tolist() == BF.linear_fwd(x.tolist(), w.tolist())
+    assert O.linear_dx(e, w).tolist() == BF.linear_dx(e.tolist(), w.tolist())
+    assert O.linear_dw(e, x).tolist() == BF.linear_dw(e.tolist(), x.tolist())
+
+
+def test_maxpool_against_bruteforce_with_ties():
+    rng = np.random.default_rng(7)
+    a = _rand(rng, (2, 6, 4, 3), -3, 3, np.int8)        # a narrow range forces many ties
+    a[0, 0:2, 0:2, 0] = 5                                  # all four equal: index 0 must win
+    a[0, 0, 2, 1] = -1
+    a[0, 0, 3, 1] = 2
+    a[0, 1, 2, 1] = 2
+    a[0, 1, 3, 1] = 2                                      # tie among (0,1),(1,0),(1,1): index 1
+    p, i = O.maxpool2(a)
+    bp, bi = BF.maxpool(a.tolist())
+    assert p.tolist() == bp and i.tolist() == bi
+    assert i[0, 0, 0, 0] == 0 and i[0, 0, 1, 1] == 1
+
+
+# ---------------------------------------------------------------- library special cases
+
+def test_conv_matches_scipy_correlate():
+    """With SF = 1 the forward conv is a plain cross-correlation summed over input channels;
+    scipy.signal.correlate2d ('same', zero fill) computes exactly that for a 3x3 kernel."""
+    rng = np.random.default_rng(3)
+    N, H, W, C, CO = 2, 9, 7, 4, 3
+    x = _rand(rng, (N, H, W, C), -127, 127, np.int8)
+    w = _rand(rng, (CO, 3, 3, C), -127, 127, np.int32)
+    z = O.conv3x3_fwd(x, w)
+    for n in range(N):
+        for co in range(CO):
+            ref = sum(scipy.signal.correlate2d(x[n, :, :, ci].astype(np.int64),
+                                               w[co, :, :, ci].astype(np.int64), mode="same")
+                      for ci in range(C))
+            assert np.array_equal(z[n, :, :, co], ref)
+
+
+def test_conv_matches_float64_im2col_blas():
+    """An im2col matrix product in float64 is exact while every partial sum stays below 2^53."""
+    rng = np.random.default_rng(4)
+    N, H, W, C, CO = 3, 8, 8, 16, 24
+    x = _rand(rng, (N, H, W, C), -127, 127, np.int8)
+    w = _rand(rng, (CO, 3, 3, C), -30000, 30000, np.int32)
+    xp = np.zeros((N, H + 2, W + 2, C), np.float64)
+    xp[:, 1:-1, 1:-1, :] = x
+    cols = np.stack([xp[:, r:r + H, s:s + W, :] for r in range(3) for s in range(3)], axis=3)
+    cols = cols.reshape(N * H * W, 9 * C)
+    ref = cols @ w.reshape(CO, 9 * C).astype(np.float64).T
+    assert np.abs(ref).max() < 2.0 ** 52
+    assert np.array_equal(O.conv3x3_fwd(x, w).reshape(-1, CO), ref.astype(np.int64))
+
+
+def test_linear_matches_float64_blas():
+    rng = np.random.default_rng(5)
+    x = _rand(rng, (33, 300), -127, 127, np.int8)
+    w = _rand(rng, (17, 300), -(1 << 20), 1 << 20, np.int32)
+    e = _rand(rng, (33, 17), -(1 << 15), 1 << 15)
+    assert np.array_equal(O.linear_fwd(x, w), (x.astype(np.float64) @ w.T.astype(np.float64)).astype(np.int64))
+    assert np.array_equal(O.linear_dx(e, w), (e.astype(np.float64) @ w.astype(np.float64)).astype(np.int64))
+    assert np.array_equal(O.linear_dw(e, x), (e.T.astype(np.float64) @ x.astype(np.float64)).astype(np.int64))
+
+
+# ---------------------------------------------------------------- exact identities
+
+def test_conv_adjoint_identities():
+    """<conv(x, W), g> = <x, dX(g, W)> = <W, dW(g, x)>, exactly in integers."""
+    rng = np.random.default_rng(6)
+    N, H, W, C, CO = 2, 8, 6, 5, 7
+    x = _rand(rng, (N, H, W, C), -127, 127, np.int8)
+    w = _rand(rng, (CO, 3, 3, C), -1000, 1000, np.int32)
+    g = _rand(rng, (N, H, W, CO), -1000, 1000)
+    lhs = int(np.sum(O.conv3x3_fwd(x, w) * g))
+    mid = int(np.sum(x.astype(np.int64) * O.conv3x3_dx(g, w)))
+    rhs = int(np.sum(w.astype(np.int64) * O.conv3x3_dw(g, x)))
+    assert lhs == mid == rhs
+
+
+def test_linear_adjoint_identities():
+    rng = np.random.default_rng(8)
+    x = _rand(rng, (9, 31), -127, 127, np.int8)
+    w = _rand(rng, (11, 31), -5000, 5000, np.int32)
+    e = _rand(rng, (9, 11), -5000, 5000)
+    lhs = int(np.sum(O.linear_fwd(x, w) * e))
+    assert lhs == int(np.sum(x.astype(np.int64) * O.linear_dx(e, w)))
+    assert lhs == int(np.sum(w.astype(np.int64) * O.linear_dw(e, x)))
+
+
+def test_conv_delta_kernel_is_a_shift():
+    """A kernel that is 1 at tap (r, s) and channel c copies x shifted by (r-1, s-1)."""
+    rng = np.random.default_rng(9)
+    x = _rand(rng, (1, 5, 6, 2), -127, 127, np.int8)
+    for r in range(3):
+        for s in range(3):
+            w = np.zeros((1, 3, 3, 2), np.int32)
+            w[0, r, s, 1] = 1
+            z = O.conv3x3_fwd(x, w)[0, :, :, 0]
+            ref = np.zeros((5, 6), np.int64)
+            for h in range(5):
+                for q in range(6):
+                    if 0 <= h + r - 1 < 5 and 0 <= q + s - 1 < 6:
+                        ref[h, q] = x[0, h + r - 1, q + s - 1, 1]
+            assert np.array_equal(z, ref)
+
+
+# ---------------------------------------------------------------- invariants
+
+def test_scaled_preactivation_range_with_int8_operands():
+    """With |x|, |W| <= 127 and SF = 2^8 fan_in: |z| <= 16129 fan_in, so floor(z/SF) in [-64, 63]."""
+    for C in (1, 3, 64):
+        x = np.full((1, 4, 4, C), 127, np.int8)
+        w = np.full((2, 3, 3, C), 127, np.int32)
+        w[1] = -127
+        zs = O.nitro_scaling(O.conv3x3_fwd(x, w), O.scaling_factor_conv(3, C))
+        assert zs.max() <= 63 and zs.min() >= -64
+        assert zs[0, 1, 1, 0] == 63 and zs[0, 1, 1, 1] == -64
+
+
+@pytest.mark.parametrize("alpha", [2, 3, 4, 10, 100, 127, 128])
+@pytest.mark.parametrize("mode", ["floor", "trunc"])
+def test_relu_monotone_and_range(alpha, mode):
+    m = MODES[mode]
+    xs = np.arange(-2000, 2001)
+    out = O.nitro_relu(xs, alpha, m)
+    assert np.all(np.diff(out) >= 0)
+    mu = O.relu_mu(alpha, m)
+    assert out.min() == int(O.idiv(-127, alpha, m)) - mu
+    assert out.max() == 127 - mu
+    assert -128 <= out.min() and out.max() <= 127            # fits int8 for alpha_inv >= 2
+
+
+def test_relu_alpha1_leaves_int8():
+    """alpha_inv = 1 under floor gives mu = -1 and a maximum output of 128, outside int8."""
+    assert O.relu_mu(1, O.FLOOR) == -1
+    assert int(O.nitro_relu(np.array([127]), 1, O.FLOOR)[0]) == 128
+
+
+def test_relu_grad_shrinks():
+    rng = np.random.default_rng(10)
+    d = rng.integers(-(1 << 20), 1 << 20, 5000)
+    zs = rng.integers(-300, 300, 5000)
+    for m in (O.FLOOR, O.TRUNC):
+        g = O.nitro_relu_grad(d, zs, 10, m)
+        assert np.all(np.abs(g) <= np.abs(d) + (m == O.FLOOR))
+
+
+def test_maxpool_backward_conserves_sum():
+    rng = np.random.default_rng(11)
+    a = _rand(rng, (2, 8, 6, 5), -100, 100, np.int8)
+    p, idx = O.maxpool2(a)
+    dp = _rand(rng, p.shape, -(1 << 20), 1 << 20)
+    full = O.maxpool2_bwd(dp, idx, a.shape)
+    assert full.sum() == dp.sum()
+    # exactly one non-zero target per window, at the argmax
+    assert np.count_nonzero(full) == np.count_nonzero(dp)
+    n, i, j, c = 1, 2, 1, 3
+    k = idx[n, i, j, c]
+    assert full[n, 2 * i + k // 2, 2 * j + k % 2, c] == dp[n, i, j, c]
+
+
+def test_sgd_special_cases():
+    rng = np.random.default_rng(12)
+    w = rng.integers(-(1 << 20), 1 << 20, 1000)
+    g = rng.integers(-(1 << 20), 1 << 20, 1000)
+    # gamma = 1 and no decay: plain W - g
+    assert np.array_equal(O.integer_sgd(w, g, 1, 0), w - g)
+    # decay threshold: with zero gradient, trunc leaves every |W| < eta untouched
+    ws = np.arange(-30, 31)
+    assert np.array_equal(O.integer_sgd(ws, np.zeros_like(ws), 5, 7, O.TRUNC)[np.abs(ws) < 35],
+                          ws[np.abs(ws) < 35])
+    # floor leaves 0 <= W < eta untouched and moves -eta <= W < 0 up by one
+    out = O.integer_sgd(ws, np.zeros_like(ws), 5, 7, O.FLOOR)
+    assert np.array_equal(out[ws >= 0], ws[ws >= 0])
+    assert np.array_equal(out[ws < 0], ws[ws < 0] + 1)
+
+
+def test_int32_guard():
+    with pytest.raises(OverflowError):
+        O.integer_sgd(np.array([(1 << 31) - 1]), np.array([-1]), 1, 0)
+
+
+def test_one_hot_and_labels():
+    y = O.one_hot32([2, 0], 3)
+    assert y.tolist() == [[0, 0, 32], [32, 0, 0]]
+    with pytest.raises(ValueError):
+        O.one_hot32([3], 3)
+
+
+def test_oracle_step_is_repeatable():
+    """Two oracle nets fed the same draws end in identical weights."""
+    from paper_2407_11698_amd import workloads as WL
+    wl = WL.scaled(WL.SMALL_CNN, 4)
+    dr = WL.draw_workload(wl, O.kaiming_bound, steps=2)
+    hp = O.Hyper(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr, wl.alpha_inv, wl.n_classes)
+    specs = [(len(b.layers), b.maxpool, b.learning) for b in wl.blocks]
+    a = O.OracleNet(specs, wl.head, dr.weights, hp)
+    b = O.OracleNet(specs, wl.head, dr.weights, hp)
+    for (x, y) in dr.batches:
+        a.train_step(x, y)
+        b.train_step(x, y)
+    for wa, wb in zip(a.w, b.w):
+        assert np.array_equal(wa, wb)
