@@ -1,0 +1,237 @@
+/*
+ * nitro.h -- C ABI of the MI355X (gfx950) library for the hot path of NITRO-D integer-only
+ * training (Pirillo, Colombo, Roveri, "NITRO-D: Native Integer-only Training of Deep
+ * Convolutional Neural Networks", arXiv 2407.11698).
+ *
+ * What the library computes, per integer local-loss block (section 3.2):
+ *   forward layers  IntConv2D 3x3 / IntLinear (section 3.2.1, Tab. 1: stride 1, zero padding 1,
+ *                   no bias) -> NITRO-Scaling z* = floor(z / SF), SF = 2^8 * fan_in (Eq. 1 and
+ *                   the scaling-factor rule of section 3.2.1) -> NITRO-ReLU (section 3.2.2)
+ *                   -> optional 2x2/2 max-pool after the last layer (Tab. 1);
+ *   learning layer  IntLinear(d -> G) + NITRO-Scaling on the block output (section 3.2, the
+ *                   training procedure of section 3.3), RSS loss gradient yhat - y with the
+ *                   32-valued one-hot target (Eq. 4, section 3.3.4, Appendix A);
+ *   backward        delta^fw = grad * W^il (section 3.3.5) routed back through pool, NITRO-ReLU
+ *                   and the forward layers of the block only; int64 weight gradients;
+ *   IntegerSGD      Alg. 1, with gamma^fw = AF * gamma, AF = 2^6 * G (Eq. 6).
+ * Everything is integer arithmetic; results are bit-exact.
+ *
+ * Readings of passages the paper leaves open (the same ones the test-side checker uses):
+ *   - division rounds toward minus infinity (the paper's floor macro) unless NITRO_ROUND_TRUNC
+ *     is chosen, which rounds every division of the step toward zero;
+ *   - the NITRO-ReLU mean is (s1 + s2 + 63 + 127) / 4 with s1 = -127/alpha_inv and
+ *     s2 = -127/(2 alpha_inv), every division by the chosen rounding;
+ *   - the NITRO-ReLU backward is the derivative of its piecewise map at z*: identity for
+ *     0 <= z* <= 127, division by alpha_inv for -127 <= z* < 0, zero where the map saturates
+ *     (NITRO-Scaling itself passes gradients unchanged, section 3.2.1);
+ *   - the loss gradient is per sample; max-pool routes the gradient to the first maximum of the
+ *     2x2 window in row-major order; delta^fw uses the learning weights from before the update;
+ *   - every layer (learning and output layers included) is rescaled by 2^8 times its own fan-in;
+ *     learning and output layers have no NITRO-ReLU.
+ *
+ * Conventions
+ *   - Tensor arguments are DEVICE pointers owned by the caller. The library never frees them and
+ *     keeps no reference to them after the work it enqueued has run.
+ *   - Layouts: images NHWC (channels innermost); conv weights KRSC [C_out][3][3][C_in];
+ *     linear weights [out][in]; the learning layer's input index d runs over the block output in
+ *     (h, w, c) order. Activations are int8, weights int32, weight gradients int64,
+ *     predictions and gradients int32.
+ *   - Every call validates its arguments on the host and returns NITRO_EINVAL before enqueuing
+ *     anything when they are wrong. Work is then enqueued asynchronously on the context's stream.
+ *   - Data-dependent errors are sticky device flags, read and cleared by nitro_sync_status():
+ *     NITRO_EOVERFLOW when a value does not fit its int32 destination (or a weight or gradient
+ *     operand exceeds what the kernels can represent), NITRO_ELABEL when a label is outside
+ *     [0, G). A kernel that raises a flag still writes its outputs (then unspecified).
+ *   - A context is used by one host thread at a time. Calls that overlap on one stream are
+ *     ordered by the stream.
+ */
+#ifndef NITRO_H
+#define NITRO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    NITRO_OK = 0,
+    NITRO_EINVAL = -1,        /* bad argument: null pointer, zero divisor, bad shape ...     */
+    NITRO_EOVERFLOW = -2,     /* a result does not fit its declared integer type             */
+    NITRO_ELABEL = -3,        /* a label outside [0, G)                                       */
+    NITRO_EHIP = -4,          /* a HIP runtime call failed                                    */
+    NITRO_ENOMEM = -5,        /* a device allocation failed                                   */
+    NITRO_EUNSUPPORTED = -6   /* valid but not supported by this build (e.g. too many blocks)*/
+} nitro_status;
+
+typedef enum { NITRO_ROUND_FLOOR = 0, NITRO_ROUND_TRUNC = 1 } nitro_round;
+typedef enum { NITRO_CONV3X3 = 0, NITRO_LINEAR = 1 } nitro_layer_kind;
+
+#define NITRO_MAX_LAYERS 4
+#define NITRO_MAX_BLOCKS 8
+
+typedef struct nitro_ctx nitro_ctx;
+
+/* Create a context on HIP device `device` that enqueues on `hip_stream` (a hipStream_t; NULL
+ * means the null stream). Allocates a few bytes of device memory for the status flags. */
+nitro_status nitro_create(nitro_ctx **out, int device, void *hip_stream);
+/* Destroy a context (synchronises its stream first). NULL is ignored. */
+void nitro_destroy(nitro_ctx *ctx);
+/* Change the stream later calls enqueue on. */
+nitro_status nitro_set_stream(nitro_ctx *ctx, void *hip_stream);
+/* Synchronise the stream, then return and clear the sticky device flags: NITRO_OK, or the first
+ * of NITRO_EOVERFLOW, NITRO_ELABEL that was raised. */
+nitro_status nitro_sync_status(nitro_ctx *ctx);
+/* Static description of a status code. */
+const char *nitro_status_str(nitro_status s);
+
+/* ------------------------------------------------------------------------------------------ */
+/* One integer local-loss block                                                               */
+/* ------------------------------------------------------------------------------------------ */
+
+typedef struct {
+    int32_t kind;      /* nitro_layer_kind                                                  */
+    int32_t c_in;      /* conv: input channels; linear: input features                      */
+    int32_t c_out;     /* conv: output channels; linear: output features                    */
+} nitro_layer;
+
+typedef struct {
+    int32_t n, h, w;                       /* batch; input height and width (1, 1 for linear)  */
+    int32_t n_layers;                      /* 1..NITRO_MAX_LAYERS forward layers               */
+    nitro_layer layer[NITRO_MAX_LAYERS];   /* all conv or all linear; c_in[j] = c_out[j-1]     */
+    int32_t maxpool;                       /* 1: 2x2/2 max-pool after the last NITRO-ReLU      */
+    int32_t n_classes;                     /* G of the learning layer; 0: no learning layer,
+                                              the caller supplies the output gradient          */
+    int32_t alpha_inv;                     /* NITRO-ReLU inverse slope, >= 2                    */
+    int32_t round;                         /* nitro_round                                       */
+} nitro_block_desc;
+
+typedef struct {
+    const int32_t *w[NITRO_MAX_LAYERS];    /* forward-layer weights                            */
+    const int32_t *w_lr;                   /* learning layer [G][d]; NULL iff n_classes == 0    */
+} nitro_block_params;
+
+typedef struct {
+    int64_t *dw[NITRO_MAX_LAYERS];         /* weight gradients of the forward layers (required) */
+    int64_t *dw_lr;                        /* learning-layer gradient [G][d] (if n_classes > 0) */
+} nitro_block_grads;
+
+/* Optional extra outputs of the backward pass; every pointer may be NULL. */
+typedef struct {
+    int32_t *yhat;                         /* [n][G] learning-layer prediction                 */
+    int32_t *e;                            /* [n][G] loss gradient yhat - y                     */
+    int32_t *delta;                        /* gradient at the block output (pooled), NHWC      */
+    int32_t *g[NITRO_MAX_LAYERS];          /* gradient at layer j's pre-activation z_j, NHWC   */
+    int32_t *dx;                           /* input gradient of the first layer, NHWC          */
+} nitro_block_taps;
+
+/* Size in bytes of the block's state buffer: what the forward pass saves for the backward pass
+ * plus the backward pass's scratch. The caller allocates it (any device allocation, 256-byte
+ * aligned) and passes the same buffer to nitro_block_forward and nitro_block_backward. */
+nitro_status nitro_block_query(const nitro_block_desc *desc, size_t *state_bytes);
+
+/* Forward layers of one block (section 3.2; training procedure of section 3.3).
+ *   x      int8 NHWC [n][h][w][c_in] (or [n][c_in] for linear blocks); must stay unchanged
+ *          until the matching nitro_block_backward has run;
+ *   a_out  int8 NHWC block output, [n][h/2][w/2][c_out] when maxpool, else [n][h][w][c_out];
+ *   state  the block's state buffer (nitro_block_query). */
+nitro_status nitro_block_forward(nitro_ctx *ctx, const nitro_block_desc *desc,
+                                 const nitro_block_params *params, const int8_t *x,
+                                 int8_t *a_out, void *state);
+
+/* Local training of one block, with the weights from before any update (section 3.3):
+ * learning layer -> yhat, loss gradient e = yhat - 32*onehot(labels), dW^il = e^T a_out,
+ * delta^fw = e W^il, then back through pool, NITRO-ReLU and the forward layers: dW per layer.
+ *   x, a_out  the same buffers as the forward call;
+ *   labels    int32 [n] in [0, G) (NITRO_ELABEL otherwise); used iff n_classes > 0;
+ *   delta_out int32 gradient at the block output, same shape as a_out; used iff n_classes == 0;
+ *   grads     int64 outputs (overwritten);
+ *   taps      optional extra outputs (may be NULL). */
+nitro_status nitro_block_backward(nitro_ctx *ctx, const nitro_block_desc *desc,
+                                  const nitro_block_params *params, const int8_t *x,
+                                  const int8_t *a_out, const int32_t *labels,
+                                  const int32_t *delta_out, void *state,
+                                  const nitro_block_grads *grads, const nitro_block_taps *taps);
+
+/* Output layer on f [n][d] int8: yhat = floor(f W^T / (2^8 d)), e = yhat - 32*onehot(labels),
+ * dW = e^T f (int64 [G][d]) -- the global loss gradient of section 3.3. yhat, e may be NULL. */
+nitro_status nitro_head_backward(nitro_ctx *ctx, int32_t n, int32_t d, int32_t n_classes,
+                                 const int8_t *f, const int32_t *w, const int32_t *labels,
+                                 int32_t round, int64_t *dw, int32_t *yhat, int32_t *e);
+
+/* IntegerSGD with weight decay (Alg. 1) on `count` int32 weights, in place:
+ *   eta = gamma_inv * lambda_inv (or eta_override when >= 0);
+ *   d = dw / gamma_inv; if eta != 0: d += w / eta; w -= d.
+ * gamma_inv >= 1, lambda_inv >= 0 (EINVAL otherwise). A result outside int32 raises
+ * NITRO_EOVERFLOW (the weight is then left unchanged). */
+nitro_status nitro_integer_sgd_step(nitro_ctx *ctx, int32_t *w, const int64_t *dw, int64_t count,
+                                    int64_t gamma_inv, int64_t lambda_inv, int64_t eta_override,
+                                    int32_t round);
+
+/* ------------------------------------------------------------------------------------------ */
+/* A whole network: one training iteration                                                    */
+/* ------------------------------------------------------------------------------------------ */
+
+typedef struct {
+    int32_t n_blocks;                          /* 1..NITRO_MAX_BLOCKS                           */
+    nitro_block_desc block[NITRO_MAX_BLOCKS];  /* shapes must chain: block b+1 reads block b's
+                                                  output; every block has n_classes = G > 0    */
+    int32_t head;                              /* 1: output layer IntLinear(d_L -> G)           */
+} nitro_net_desc;
+
+typedef struct {
+    int32_t *w[NITRO_MAX_BLOCKS][NITRO_MAX_LAYERS];   /* forward-layer weights (updated)        */
+    int32_t *w_lr[NITRO_MAX_BLOCKS];                  /* learning-layer weights (updated)       */
+    int32_t *w_head;                                  /* output layer [G][d_L] (if head)        */
+} nitro_net_params;
+
+typedef struct {
+    int64_t gamma_inv;        /* gamma_inv of learning and output layers (>= 1)                 */
+    int64_t lambda_inv_fw;    /* lambda_inv of forward layers (>= 0, 0: no decay)               */
+    int64_t lambda_inv_lr;    /* lambda_inv of learning and output layers                       */
+    int64_t af;               /* amplification factor; 0 means 2^6 * G (Eq. 6)                 */
+    int64_t eta_fw;           /* < 0: eta = (AF * gamma_inv) * lambda_inv_fw; else this eta     */
+    int64_t eta_lr;           /* < 0: eta = gamma_inv * lambda_inv_lr; else this eta           */
+} nitro_hparams;
+
+/* Size in bytes of the network workspace: every block's state and output, and every weight
+ * gradient. */
+nitro_status nitro_net_query(const nitro_net_desc *net, size_t *workspace_bytes);
+
+/* One training iteration (section 3.3): forward through every block, output layer and its
+ * IntegerSGD update, then each block's local training and the IntegerSGD update of its learning
+ * layer (gamma_inv) and forward layers (AF * gamma_inv). All gradients are taken at the weights
+ * from before the iteration. Weights in `params` are updated in place.
+ *   x       int8 input batch (NHWC, or [n][d] for an MLP);
+ *   labels  int32 [n] in [0, G). */
+nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
+                              const nitro_net_params *params, void *workspace,
+                              const int8_t *x, const int32_t *labels, const nitro_hparams *hp);
+
+/* Device pointer, inside a workspace laid out by nitro_net_query, of block b's output a_b
+ * (int8), so that callers can inspect the forward activations after nitro_train_step. */
+nitro_status nitro_net_block_output(const nitro_net_desc *net, void *workspace, int32_t b,
+                                    int8_t **a_out);
+
+/* ------------------------------------------------------------------------------------------ */
+/* Host-side helpers (no device work)                                                         */
+/* ------------------------------------------------------------------------------------------ */
+
+/* The division the kernels use (multiply by a precomputed reciprocal of the invariant
+ * divisor), evaluated on the host: n / d with d >= 1 and |n| < 2^62, rounded per `round`. */
+int64_t nitro_host_div(int64_t n, int64_t d, int32_t round);
+/* NITRO-ReLU mean for alpha_inv (section 3.2.2) under `round`. */
+int32_t nitro_host_relu_mu(int32_t alpha_inv, int32_t round);
+
+/* Per-kernel timing for profiling: when enabled, the library records HIP events around every
+ * launch of the kernel class `cls` (0: conv forward, 1: conv input gradient, 2: conv weight
+ * gradient) on the context stream; nitro_kernel_time returns the accumulated milliseconds and
+ * launch count since the last reset (synchronises the stream). */
+nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable);
+nitro_status nitro_kernel_time(nitro_ctx *ctx, int32_t cls, double *ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NITRO_H */

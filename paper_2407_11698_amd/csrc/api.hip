@@ -1,0 +1,606 @@
+// C ABI of the NITRO-D HIP library: argument validation, state layout, and the enqueueing of
+// the kernels that make up one block's forward pass, one block's local training, the output
+// layer, IntegerSGD and a whole training iteration (section 3.3).
+#include <string.h>
+
+#include <utility>
+#include <vector>
+
+#include "nitro_internal.h"
+
+using namespace nitro;
+
+struct nitro_ctx {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    uint32_t *flags = nullptr;                  // device: sticky status bits
+    bool timing = false;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[3];
+    size_t used[3] = {0, 0, 0};
+};
+
+namespace {
+
+struct DeviceGuard {
+    int prev = -1;
+    explicit DeviceGuard(int dev)
+    {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        if (prev != dev) (void)hipSetDevice(dev);
+    }
+    ~DeviceGuard()
+    {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+nitro_status hip_status()
+{
+    return hipGetLastError() == hipSuccess ? NITRO_OK : NITRO_EHIP;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// Kernel classes for the optional per-kernel timing.
+enum { CLS_CONV_FWD = 0, CLS_CONV_DX = 1, CLS_CONV_DW = 2 };
+
+struct TimedLaunch {
+    nitro_ctx *ctx;
+    int cls;
+    hipEvent_t stop = nullptr;
+    TimedLaunch(nitro_ctx *c, int k) : ctx(c), cls(k)
+    {
+        if (!ctx->timing) return;
+        if (ctx->used[cls] == ctx->ev[cls].size()) {
+            hipEvent_t a, b;
+            if (hipEventCreate(&a) != hipSuccess) return;
+            if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+            ctx->ev[cls].push_back({a, b});
+        }
+        auto &p = ctx->ev[cls][ctx->used[cls]++];
+        (void)hipEventRecord(p.first, ctx->stream);
+        stop = p.second;
+    }
+    ~TimedLaunch()
+    {
+        if (stop) (void)hipEventRecord(stop, ctx->stream);
+    }
+};
+
+// ------------------------------------------------------------------------------------------
+// Per-layer shapes of a block.
+struct LayerGeom {
+    bool conv;
+    ConvShape sh;             // conv: input NHWC and c_out; linear: n, c = in, co = out, h=w=1
+    int64_t in_elems;         // per batch
+    int64_t out_elems;        // full resolution, per batch
+    int64_t sf;               // 2^8 * fan_in
+};
+
+struct BlockGeom {
+    int J;
+    LayerGeom L[NITRO_MAX_LAYERS];
+    int64_t out_elems;        // block output (pooled if maxpool), whole batch
+    int64_t d;                // per-sample block output size (learning layer input)
+    // state buffer offsets
+    size_t act[NITRO_MAX_LAYERS];
+    size_t code[NITRO_MAX_LAYERS];
+    size_t yhat, e, delta, g0, g1;
+    size_t total;
+};
+
+nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
+{
+    if (!d || !g) return NITRO_EINVAL;
+    if (d->n < 1 || d->n_layers < 1 || d->n_layers > NITRO_MAX_LAYERS) return NITRO_EINVAL;
+    if (d->alpha_inv < 2) return NITRO_EINVAL;
+    if (d->round != NITRO_ROUND_FLOOR && d->round != NITRO_ROUND_TRUNC) return NITRO_EINVAL;
+    if (d->n_classes < 0 || (d->maxpool != 0 && d->maxpool != 1)) return NITRO_EINVAL;
+    const int kind = d->layer[0].kind;
+    if (kind != NITRO_CONV3X3 && kind != NITRO_LINEAR) return NITRO_EINVAL;
+    const bool conv = kind == NITRO_CONV3X3;
+    if (conv) {
+        if (d->h < 1 || d->w < 1) return NITRO_EINVAL;
+        if (d->maxpool && ((d->h & 1) || (d->w & 1))) return NITRO_EINVAL;
+    } else {
+        if (d->h != 1 || d->w != 1 || d->maxpool) return NITRO_EINVAL;
+    }
+    g->J = d->n_layers;
+    int c = d->layer[0].c_in;
+    const int64_t hw = (int64_t)d->h * d->w;
+    for (int j = 0; j < g->J; j++) {
+        const nitro_layer &ly = d->layer[j];
+        if (ly.kind != kind || ly.c_in < 1 || ly.c_out < 1 || ly.c_in != c) return NITRO_EINVAL;
+        LayerGeom &L = g->L[j];
+        L.conv = conv;
+        L.sh = ConvShape{d->n, conv ? d->h : 1, conv ? d->w : 1, ly.c_in, ly.c_out};
+        L.in_elems = hw * ly.c_in;
+        L.out_elems = hw * ly.c_out;
+        L.sf = 256 * (int64_t)(conv ? 9 * ly.c_in : ly.c_in);
+        c = ly.c_out;
+    }
+    // keep every flattened index far from overflow
+    for (int j = 0; j < g->J; j++)
+        if ((int64_t)d->n * (g->L[j].out_elems > g->L[j].in_elems ? g->L[j].out_elems : g->L[j].in_elems) > ((int64_t)1 << 40))
+            return NITRO_EUNSUPPORTED;
+    g->d = d->maxpool ? (int64_t)(d->h / 2) * (d->w / 2) * c : hw * c;
+    g->out_elems = (int64_t)d->n * g->d;
+    // state buffer layout
+    size_t off = 0;
+    int64_t gmax = 0;
+    for (int j = 0; j < g->J; j++) {
+        const int64_t full = (int64_t)d->n * g->L[j].out_elems;
+        const bool last = j == g->J - 1;
+        g->act[j] = off;
+        if (!last) off = align256(off + (size_t)full);
+        g->code[j] = off;
+        off = align256(off + (size_t)(last ? (d->maxpool ? g->out_elems : full) : full));
+        if (full > gmax) gmax = full;
+    }
+    const int64_t G = d->n_classes;
+    g->yhat = off;  off = align256(off + (size_t)(d->n * G) * 4);
+    g->e = off;     off = align256(off + (size_t)(d->n * G) * 4);
+    g->delta = off; off = align256(off + (size_t)(G > 0 ? g->out_elems : 0) * 4);
+    g->g0 = off;    off = align256(off + (size_t)gmax * 4);
+    g->g1 = off;    off = align256(off + (size_t)(g->J > 1 ? gmax : 0) * 4);
+    g->total = off;
+    return NITRO_OK;
+}
+
+Relu make_relu(int alpha_inv, int round)
+{
+    Relu r;
+    r.alpha = make_div(alpha_inv, round);
+    r.mu = nitro_host_relu_mu(alpha_inv, round);
+    return r;
+}
+
+inline uint8_t *at(void *base, size_t off) { return (uint8_t *)base + off; }
+
+nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, const BlockGeom &g,
+                                const nitro_block_params *p, const int8_t *x, int8_t *a_out,
+                                void *state)
+{
+    hipStream_t s = ctx->stream;
+    const Relu rp = make_relu(desc->alpha_inv, desc->round);
+    const int8_t *cur = x;
+    for (int j = 0; j < g.J; j++) {
+        const LayerGeom &L = g.L[j];
+        const bool last = j == g.J - 1;
+        int8_t *out = last ? a_out : (int8_t *)at(state, g.act[j]);
+        uint8_t *code = at(state, g.code[j]);
+        const Div sf = make_div(L.sf, desc->round);
+        if (L.conv) {
+            TimedLaunch t(ctx, CLS_CONV_FWD);
+            launch_conv_fwd(s, L.sh, cur, p->w[j], sf, rp, last && desc->maxpool, out, code);
+        } else {
+            launch_linear_fwd_relu(s, L.sh.n, L.sh.c, L.sh.co, cur, p->w[j], sf, rp, out, code);
+        }
+        cur = out;
+    }
+    return hip_status();
+}
+
+nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, const BlockGeom &g,
+                                 const nitro_block_params *p, const int8_t *x, const int8_t *a_out,
+                                 const int32_t *labels, const int32_t *delta_out, void *state,
+                                 const nitro_block_grads *gr, const nitro_block_taps *taps)
+{
+    hipStream_t s = ctx->stream;
+    const Relu rp = make_relu(desc->alpha_inv, desc->round);
+    const int n = desc->n;
+    const int G = desc->n_classes;
+    const int32_t *delta = delta_out;
+    if (G > 0) {
+        int32_t *yhat = (int32_t *)at(state, g.yhat);
+        int32_t *e = (int32_t *)at(state, g.e);
+        int32_t *dl = (int32_t *)at(state, g.delta);
+        const Div sf = make_div(256 * g.d, desc->round);
+        launch_linear_fwd_loss(s, n, (int)g.d, G, a_out, p->w_lr, sf, labels, yhat, e, ctx->flags);
+        launch_linear_dw(s, n, (int)g.d, G, e, a_out, gr->dw_lr);
+        launch_linear_dx(s, n, (int)g.d, G, e, p->w_lr, nullptr, rp, dl, ctx->flags);
+        if (taps) {
+            if (taps->yhat) (void)hipMemcpyAsync(taps->yhat, yhat, (size_t)n * G * 4, hipMemcpyDeviceToDevice, s);
+            if (taps->e) (void)hipMemcpyAsync(taps->e, e, (size_t)n * G * 4, hipMemcpyDeviceToDevice, s);
+            if (taps->delta) (void)hipMemcpyAsync(taps->delta, dl, (size_t)g.out_elems * 4, hipMemcpyDeviceToDevice, s);
+        }
+        delta = dl;
+    }
+    int32_t *gb[2] = {(int32_t *)at(state, g.g0), (int32_t *)at(state, g.g1)};
+    const int J = g.J;
+    {
+        const LayerGeom &L = g.L[J - 1];
+        launch_unpool_relu_bwd(s, n, L.sh.h, L.sh.w, L.sh.co, desc->maxpool != 0, delta,
+                               at(state, g.code[J - 1]), rp, gb[0], ctx->flags);
+    }
+    int cur = 0;
+    for (int j = J - 1; j >= 0; j--) {
+        const LayerGeom &L = g.L[j];
+        const int8_t *xin = j == 0 ? x : (const int8_t *)at(state, g.act[j - 1]);
+        const int32_t *gj = gb[cur];
+        if (L.conv) {
+            TimedLaunch t(ctx, CLS_CONV_DW);
+            launch_conv_dw(s, L.sh, gj, xin, gr->dw[j]);
+        } else {
+            launch_linear_dw(s, n, L.sh.c, L.sh.co, gj, xin, gr->dw[j]);
+        }
+        if (taps && taps->g[j])
+            (void)hipMemcpyAsync(taps->g[j], gj, (size_t)n * L.out_elems * 4, hipMemcpyDeviceToDevice, s);
+        int32_t *dst = nullptr;
+        const uint8_t *code = nullptr;
+        if (j > 0) {
+            dst = gb[cur ^ 1];
+            code = at(state, g.code[j - 1]);
+        } else if (taps && taps->dx) {
+            dst = taps->dx;
+        }
+        if (dst) {
+            if (L.conv) {
+                TimedLaunch t(ctx, CLS_CONV_DX);
+                launch_conv_dx(s, L.sh, gj, p->w[j], code, rp, dst, ctx->flags);
+            } else {
+                launch_linear_dx(s, n, L.sh.c, L.sh.co, gj, p->w[j], code, rp, dst, ctx->flags);
+            }
+        }
+        cur ^= 1;
+    }
+    return hip_status();
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t *out)
+{
+    return !__builtin_mul_overflow(a, b, out);
+}
+
+nitro_status sgd_impl(nitro_ctx *ctx, int32_t *w, const int64_t *dw, int64_t count,
+                      int64_t gamma_inv, int64_t lambda_inv, int64_t eta_override, int32_t round)
+{
+    if (!w || !dw || count < 0 || gamma_inv < 1 || lambda_inv < 0) return NITRO_EINVAL;
+    if (round != NITRO_ROUND_FLOOR && round != NITRO_ROUND_TRUNC) return NITRO_EINVAL;
+    int64_t eta = eta_override;
+    if (eta < 0 && !mul_ok(gamma_inv, lambda_inv, &eta)) return NITRO_EINVAL;
+    const Div dg = make_div(gamma_inv, round);
+    const Div de = make_div(eta > 0 ? eta : 1, round);
+    launch_sgd(ctx->stream, w, dw, count, dg, de, eta != 0, ctx->flags);
+    return hip_status();
+}
+
+// ------------------------------------------------------------------------------------------
+// Network workspace layout.
+struct NetGeom {
+    BlockGeom b[NITRO_MAX_BLOCKS];
+    size_t state[NITRO_MAX_BLOCKS], aout[NITRO_MAX_BLOCKS];
+    size_t dw[NITRO_MAX_BLOCKS][NITRO_MAX_LAYERS], dwlr[NITRO_MAX_BLOCKS];
+    size_t hyhat, he, hdw;
+    int64_t hd;            // head input size
+    size_t total;
+};
+
+int64_t weight_count(const nitro_layer &ly)
+{
+    return ly.kind == NITRO_CONV3X3 ? (int64_t)ly.c_out * 9 * ly.c_in : (int64_t)ly.c_out * ly.c_in;
+}
+
+nitro_status net_geom(const nitro_net_desc *net, NetGeom *g)
+{
+    if (!net || !g) return NITRO_EINVAL;
+    if (net->n_blocks < 1) return NITRO_EINVAL;
+    if (net->n_blocks > NITRO_MAX_BLOCKS) return NITRO_EUNSUPPORTED;
+    if (net->head != 0 && net->head != 1) return NITRO_EINVAL;
+    const int G = net->block[0].n_classes;
+    if (G < 1) return NITRO_EINVAL;
+    size_t off = 0;
+    for (int b = 0; b < net->n_blocks; b++) {
+        const nitro_block_desc &d = net->block[b];
+        nitro_status st = block_geom(&d, &g->b[b]);
+        if (st != NITRO_OK) return st;
+        if (d.n_classes != G || d.n != net->block[0].n || d.alpha_inv != net->block[0].alpha_inv ||
+            d.round != net->block[0].round)
+            return NITRO_EINVAL;
+        if (b > 0) {
+            const nitro_block_desc &pd = net->block[b - 1];
+            const nitro_layer &pl = pd.layer[pd.n_layers - 1];
+            const bool pconv = pl.kind == NITRO_CONV3X3;
+            const bool conv = d.layer[0].kind == NITRO_CONV3X3;
+            if (pconv != conv) return NITRO_EINVAL;
+            if (conv) {
+                const int ph = pd.maxpool ? pd.h / 2 : pd.h, pw = pd.maxpool ? pd.w / 2 : pd.w;
+                if (d.h != ph || d.w != pw || d.layer[0].c_in != pl.c_out) return NITRO_EINVAL;
+            } else if (d.layer[0].c_in != pl.c_out) {
+                return NITRO_EINVAL;
+            }
+        }
+        g->state[b] = off; off = align256(off + g->b[b].total);
+        g->aout[b] = off;  off = align256(off + (size_t)g->b[b].out_elems);
+        for (int j = 0; j < d.n_layers; j++) {
+            g->dw[b][j] = off;
+            off = align256(off + (size_t)weight_count(d.layer[j]) * 8);
+        }
+        g->dwlr[b] = off; off = align256(off + (size_t)G * g->b[b].d * 8);
+    }
+    const int L = net->n_blocks - 1;
+    const int n = net->block[0].n;
+    g->hd = g->b[L].d;
+    g->hyhat = off; off = align256(off + (size_t)(net->head ? n * G : 0) * 4);
+    g->he = off;    off = align256(off + (size_t)(net->head ? n * G : 0) * 4);
+    g->hdw = off;   off = align256(off + (size_t)(net->head ? G * g->hd : 0) * 8);
+    g->total = off;
+    return NITRO_OK;
+}
+
+}  // namespace
+
+// ============================================================================================
+extern "C" {
+
+const char *nitro_status_str(nitro_status s)
+{
+    switch (s) {
+    case NITRO_OK: return "ok";
+    case NITRO_EINVAL: return "invalid argument";
+    case NITRO_EOVERFLOW: return "integer overflow: a value does not fit its declared type";
+    case NITRO_ELABEL: return "label outside [0, G)";
+    case NITRO_EHIP: return "HIP runtime error";
+    case NITRO_ENOMEM: return "out of device memory";
+    case NITRO_EUNSUPPORTED: return "unsupported by this build";
+    }
+    return "unknown status";
+}
+
+int64_t nitro_host_div(int64_t n, int64_t d, int32_t round)
+{
+    if (d < 1) return 0;
+    return idiv(n, make_div(d, round));
+}
+
+int32_t nitro_host_relu_mu(int32_t alpha_inv, int32_t round)
+{
+    if (alpha_inv < 1) return 0;
+    const int64_t s1 = idiv(-127, make_div(alpha_inv, round));
+    const int64_t s2 = idiv(-127, make_div(2 * (int64_t)alpha_inv, round));
+    return (int32_t)idiv(s1 + s2 + 63 + 127, make_div(4, round));
+}
+
+nitro_status nitro_create(nitro_ctx **out, int device, void *hip_stream)
+{
+    if (!out) return NITRO_EINVAL;
+    *out = nullptr;
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || device < 0 || device >= count) return NITRO_EINVAL;
+    DeviceGuard guard(device);
+    nitro_ctx *c = new nitro_ctx();
+    c->device = device;
+    c->stream = (hipStream_t)hip_stream;
+    if (hipMalloc((void **)&c->flags, 256) != hipSuccess) { delete c; return NITRO_ENOMEM; }
+    if (hipMemset(c->flags, 0, 256) != hipSuccess) { (void)hipFree(c->flags); delete c; return NITRO_EHIP; }
+    *out = c;
+    return NITRO_OK;
+}
+
+void nitro_destroy(nitro_ctx *ctx)
+{
+    if (!ctx) return;
+    DeviceGuard guard(ctx->device);
+    (void)hipStreamSynchronize(ctx->stream);
+    for (auto &v : ctx->ev)
+        for (auto &p : v) { (void)hipEventDestroy(p.first); (void)hipEventDestroy(p.second); }
+    (void)hipFree(ctx->flags);
+    delete ctx;
+}
+
+nitro_status nitro_set_stream(nitro_ctx *ctx, void *hip_stream)
+{
+    if (!ctx) return NITRO_EINVAL;
+    ctx->stream = (hipStream_t)hip_stream;
+    return NITRO_OK;
+}
+
+nitro_status nitro_sync_status(nitro_ctx *ctx)
+{
+    if (!ctx) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+    if (hipStreamSynchronize(ctx->stream) != hipSuccess) return NITRO_EHIP;
+    uint32_t f = 0;
+    if (hipMemcpy(&f, ctx->flags, 4, hipMemcpyDeviceToHost) != hipSuccess) return NITRO_EHIP;
+    if (f && hipMemset(ctx->flags, 0, 4) != hipSuccess) return NITRO_EHIP;
+    if (f & FLAG_OVERFLOW) return NITRO_EOVERFLOW;
+    if (f & FLAG_LABEL) return NITRO_ELABEL;
+    return NITRO_OK;
+}
+
+nitro_status nitro_block_query(const nitro_block_desc *desc, size_t *state_bytes)
+{
+    if (!state_bytes) return NITRO_EINVAL;
+    BlockGeom g;
+    nitro_status st = block_geom(desc, &g);
+    if (st != NITRO_OK) return st;
+    *state_bytes = g.total;
+    return NITRO_OK;
+}
+
+nitro_status nitro_block_forward(nitro_ctx *ctx, const nitro_block_desc *desc,
+                                 const nitro_block_params *params, const int8_t *x,
+                                 int8_t *a_out, void *state)
+{
+    if (!ctx || !params || !x || !a_out || !state) return NITRO_EINVAL;
+    BlockGeom g;
+    nitro_status st = block_geom(desc, &g);
+    if (st != NITRO_OK) return st;
+    for (int j = 0; j < g.J; j++)
+        if (!params->w[j]) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+    return block_forward_impl(ctx, desc, g, params, x, a_out, state);
+}
+
+nitro_status nitro_block_backward(nitro_ctx *ctx, const nitro_block_desc *desc,
+                                  const nitro_block_params *params, const int8_t *x,
+                                  const int8_t *a_out, const int32_t *labels,
+                                  const int32_t *delta_out, void *state,
+                                  const nitro_block_grads *grads, const nitro_block_taps *taps)
+{
+    if (!ctx || !params || !x || !a_out || !state || !grads) return NITRO_EINVAL;
+    BlockGeom g;
+    nitro_status st = block_geom(desc, &g);
+    if (st != NITRO_OK) return st;
+    for (int j = 0; j < g.J; j++)
+        if (!params->w[j] || !grads->dw[j]) return NITRO_EINVAL;
+    if (desc->n_classes > 0) {
+        if (!labels || !params->w_lr || !grads->dw_lr) return NITRO_EINVAL;
+    } else if (!delta_out) {
+        return NITRO_EINVAL;
+    }
+    DeviceGuard guard(ctx->device);
+    return block_backward_impl(ctx, desc, g, params, x, a_out, labels, delta_out, state, grads, taps);
+}
+
+nitro_status nitro_head_backward(nitro_ctx *ctx, int32_t n, int32_t d, int32_t n_classes,
+                                 const int8_t *f, const int32_t *w, const int32_t *labels,
+                                 int32_t round, int64_t *dw, int32_t *yhat, int32_t *e)
+{
+    if (!ctx || n < 1 || d < 1 || n_classes < 1 || !f || !w || !labels || !dw || !yhat || !e)
+        return NITRO_EINVAL;
+    if (round != NITRO_ROUND_FLOOR && round != NITRO_ROUND_TRUNC) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+    const Div sf = make_div(256 * (int64_t)d, round);
+    launch_linear_fwd_loss(ctx->stream, n, d, n_classes, f, w, sf, labels, yhat, e, ctx->flags);
+    launch_linear_dw(ctx->stream, n, d, n_classes, e, f, dw);
+    return hip_status();
+}
+
+nitro_status nitro_integer_sgd_step(nitro_ctx *ctx, int32_t *w, const int64_t *dw, int64_t count,
+                                    int64_t gamma_inv, int64_t lambda_inv, int64_t eta_override,
+                                    int32_t round)
+{
+    if (!ctx) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+    return sgd_impl(ctx, w, dw, count, gamma_inv, lambda_inv, eta_override, round);
+}
+
+nitro_status nitro_net_query(const nitro_net_desc *net, size_t *workspace_bytes)
+{
+    if (!workspace_bytes) return NITRO_EINVAL;
+    NetGeom g;
+    nitro_status st = net_geom(net, &g);
+    if (st != NITRO_OK) return st;
+    *workspace_bytes = g.total;
+    return NITRO_OK;
+}
+
+nitro_status nitro_net_block_output(const nitro_net_desc *net, void *workspace, int32_t b,
+                                    int8_t **a_out)
+{
+    if (!workspace || !a_out) return NITRO_EINVAL;
+    NetGeom g;
+    nitro_status st = net_geom(net, &g);
+    if (st != NITRO_OK) return st;
+    if (b < 0 || b >= net->n_blocks) return NITRO_EINVAL;
+    *a_out = (int8_t *)at(workspace, g.aout[b]);
+    return NITRO_OK;
+}
+
+nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
+                              const nitro_net_params *params, void *workspace,
+                              const int8_t *x, const int32_t *labels, const nitro_hparams *hp)
+{
+    if (!ctx || !params || !workspace || !x || !labels || !hp) return NITRO_EINVAL;
+    NetGeom g;
+    nitro_status st = net_geom(net, &g);
+    if (st != NITRO_OK) return st;
+    const int G = net->block[0].n_classes;
+    const int round = net->block[0].round;
+    if (hp->gamma_inv < 1 || hp->lambda_inv_fw < 0 || hp->lambda_inv_lr < 0 || hp->af < 0)
+        return NITRO_EINVAL;
+    int64_t af = hp->af ? hp->af : 64 * (int64_t)G;
+    int64_t gamma_fw;
+    if (!mul_ok(af, hp->gamma_inv, &gamma_fw)) return NITRO_EINVAL;
+    int64_t eta_fw = hp->eta_fw, eta_lr = hp->eta_lr;
+    if (eta_fw < 0 && !mul_ok(gamma_fw, hp->lambda_inv_fw, &eta_fw)) return NITRO_EINVAL;
+    if (eta_lr < 0 && !mul_ok(hp->gamma_inv, hp->lambda_inv_lr, &eta_lr)) return NITRO_EINVAL;
+    for (int b = 0; b < net->n_blocks; b++) {
+        for (int j = 0; j < net->block[b].n_layers; j++)
+            if (!params->w[b][j]) return NITRO_EINVAL;
+        if (!params->w_lr[b]) return NITRO_EINVAL;
+    }
+    if (net->head && !params->w_head) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+
+    // 1. forward through every block (pre-update weights)
+    const int8_t *cur = x;
+    for (int b = 0; b < net->n_blocks; b++) {
+        nitro_block_params bp{};
+        for (int j = 0; j < net->block[b].n_layers; j++) bp.w[j] = params->w[b][j];
+        bp.w_lr = params->w_lr[b];
+        int8_t *aout = (int8_t *)at(workspace, g.aout[b]);
+        st = block_forward_impl(ctx, &net->block[b], g.b[b], &bp, cur, aout, at(workspace, g.state[b]));
+        if (st != NITRO_OK) return st;
+        cur = aout;
+    }
+    // 2. output layer: global gradient, then its IntegerSGD update
+    const int n = net->block[0].n;
+    if (net->head) {
+        const int64_t d = g.hd;
+        const Div sf = make_div(256 * d, round);
+        int64_t *hdw = (int64_t *)at(workspace, g.hdw);
+        launch_linear_fwd_loss(ctx->stream, n, (int)d, G, cur, params->w_head, sf, labels,
+                               (int32_t *)at(workspace, g.hyhat), (int32_t *)at(workspace, g.he),
+                               ctx->flags);
+        launch_linear_dw(ctx->stream, n, (int)d, G, (const int32_t *)at(workspace, g.he), cur, hdw);
+        st = sgd_impl(ctx, params->w_head, hdw, (int64_t)G * d, hp->gamma_inv, hp->lambda_inv_lr,
+                      eta_lr, round);
+        if (st != NITRO_OK) return st;
+    }
+    // 3. local training of every block, then its updates
+    for (int b = 0; b < net->n_blocks; b++) {
+        const nitro_block_desc &d = net->block[b];
+        const int8_t *xin = b == 0 ? x : (const int8_t *)at(workspace, g.aout[b - 1]);
+        nitro_block_params bp{};
+        nitro_block_grads gr{};
+        for (int j = 0; j < d.n_layers; j++) {
+            bp.w[j] = params->w[b][j];
+            gr.dw[j] = (int64_t *)at(workspace, g.dw[b][j]);
+        }
+        bp.w_lr = params->w_lr[b];
+        gr.dw_lr = (int64_t *)at(workspace, g.dwlr[b]);
+        st = block_backward_impl(ctx, &d, g.b[b], &bp, xin, (const int8_t *)at(workspace, g.aout[b]),
+                                 labels, nullptr, at(workspace, g.state[b]), &gr, nullptr);
+        if (st != NITRO_OK) return st;
+        st = sgd_impl(ctx, params->w_lr[b], gr.dw_lr, (int64_t)G * g.b[b].d, hp->gamma_inv,
+                      hp->lambda_inv_lr, eta_lr, round);
+        if (st != NITRO_OK) return st;
+        for (int j = 0; j < d.n_layers; j++) {
+            st = sgd_impl(ctx, params->w[b][j], gr.dw[j], weight_count(d.layer[j]), gamma_fw,
+                          hp->lambda_inv_fw, eta_fw, round);
+            if (st != NITRO_OK) return st;
+        }
+    }
+    return NITRO_OK;
+}
+
+nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable)
+{
+    if (!ctx) return NITRO_EINVAL;
+    ctx->timing = enable != 0;
+    for (auto &u : ctx->used) u = 0;
+    return NITRO_OK;
+}
+
+nitro_status nitro_kernel_time(nitro_ctx *ctx, int32_t cls, double *ms, int64_t *launches)
+{
+    if (!ctx || cls < 0 || cls > 2 || !ms || !launches) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+    if (hipStreamSynchronize(ctx->stream) != hipSuccess) return NITRO_EHIP;
+    double tot = 0.0;
+    for (size_t i = 0; i < ctx->used[cls]; i++) {
+        float t = 0.f;
+        if (hipEventElapsedTime(&t, ctx->ev[cls][i].first, ctx->ev[cls][i].second) != hipSuccess)
+            return NITRO_EHIP;
+        tot += t;
+    }
+    *ms = tot;
+    *launches = (int64_t)ctx->used[cls];
+    ctx->used[cls] = 0;
+    return NITRO_OK;
+}
+
+}  // extern "C"

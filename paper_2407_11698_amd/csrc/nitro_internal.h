@@ -1,0 +1,142 @@
+// Internal declarations of the NITRO-D HIP library (gfx950). Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "nitro.h"
+
+namespace nitro {
+
+// ------------------------------------------------------------------------------------------
+// Division by an invariant positive divisor.
+//
+// Every division in the method has a divisor fixed for the whole launch (SF, alpha_inv,
+// gamma_inv, eta). The kernels multiply by a precomputed reciprocal instead of dividing:
+// the round-up method of Granlund and Montgomery, "Division by invariant integers using
+// multiplication" (PLDI 1994, section 4), for unsigned 64-bit numerators below 2^63:
+//   l = ceil(log2 d), m = floor(2^64 (2^l - d) / d) + 1,  q = (mulhi(m, n) + n) >> l.
+// (t = mulhi(m, n) <= n < 2^63, so t + n cannot wrap.) Signed numerators are reduced to that
+// case: floor(n/d) = n >= 0 ? q(n) : ~q(~n)  and  trunc(n/d) = n >= 0 ? q(n) : -q(-n).
+// ------------------------------------------------------------------------------------------
+struct Div {
+    int64_t d;        // the divisor, >= 1
+    uint64_t m;       // magic multiplier
+    int32_t l;        // shift
+    int32_t trunc;    // 0: round toward minus infinity, 1: toward zero
+};
+
+inline Div make_div(int64_t d, int round)
+{
+    Div r;
+    r.d = d;
+    int l = 0;
+    while (l < 63 && ((int64_t)1 << l) < d) l++;
+    unsigned __int128 num = ((unsigned __int128)(((uint64_t)1 << l) - (uint64_t)d)) << 64;
+    r.m = (uint64_t)(num / (uint64_t)d) + 1;
+    r.l = l;
+    r.trunc = round == NITRO_ROUND_TRUNC;
+    return r;
+}
+
+__host__ __device__ inline uint64_t mulhi_u64(uint64_t a, uint64_t b)
+{
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __umul64hi(a, b);
+#else
+    return (uint64_t)(((unsigned __int128)a * b) >> 64);
+#endif
+}
+
+__host__ __device__ inline uint64_t udiv_magic(uint64_t n, const Div &v)
+{
+    uint64_t t = mulhi_u64(v.m, n);
+    return (t + n) >> v.l;
+}
+
+__host__ __device__ inline int64_t idiv(int64_t n, const Div &v)
+{
+    if (n >= 0) return (int64_t)udiv_magic((uint64_t)n, v);
+    if (v.trunc) return -(int64_t)udiv_magic((uint64_t)(-n), v);
+    return ~(int64_t)udiv_magic((uint64_t)(~n), v);
+}
+
+// ------------------------------------------------------------------------------------------
+// NITRO-ReLU parameters and region codes.
+// Region of a rescaled pre-activation z*: 0 = identity segment (0 <= z* <= 127),
+// 1 = leaky segment (-127 <= z* < 0), 2 = saturated (z* > 127 or z* < -127).
+// ------------------------------------------------------------------------------------------
+struct Relu {
+    Div alpha;        // alpha_inv
+    int32_t mu;
+};
+
+enum : uint8_t { REG_PASS = 0, REG_SLOPE = 1, REG_ZERO = 2 };
+
+__device__ inline int32_t relu_fwd(int64_t zs, const Relu &rp, uint8_t &region)
+{
+    if (zs < 0) {
+        region = zs >= -127 ? REG_SLOPE : REG_ZERO;
+        int64_t c = zs < -127 ? -127 : zs;
+        return (int32_t)(idiv(c, rp.alpha) - rp.mu);
+    }
+    region = zs <= 127 ? REG_PASS : REG_ZERO;
+    int64_t c = zs > 127 ? 127 : zs;
+    return (int32_t)(c - rp.mu);
+}
+
+__device__ inline int64_t relu_bwd(int64_t delta, uint8_t region, const Relu &rp)
+{
+    if (region == REG_PASS) return delta;
+    if (region == REG_SLOPE) return idiv(delta, rp.alpha);
+    return 0;
+}
+
+// Sticky status flags written by kernels (bit or).
+enum : uint32_t { FLAG_OVERFLOW = 1u, FLAG_LABEL = 2u };
+
+__device__ inline bool fits_i32(int64_t v) { return v >= INT32_MIN && v <= INT32_MAX; }
+
+__device__ inline void raise_flag(uint32_t *flags, uint32_t f) { atomicOr(flags, f); }
+
+// ------------------------------------------------------------------------------------------
+// Kernel launchers (each enqueues on `s`; shapes are validated by the caller).
+// ------------------------------------------------------------------------------------------
+struct ConvShape {
+    int n, h, w, c, co;    // input NHWC [n][h][w][c], output channels co
+};
+
+void launch_fill_i64(hipStream_t s, int64_t *p, int64_t count);
+
+// forward conv + Scaling + ReLU; POOL variant writes the pooled output and per pooled element
+// code = argmax | region << 2; the plain variant writes the full-resolution output and region.
+void launch_conv_fwd(hipStream_t s, const ConvShape &sh, const int8_t *x, const int32_t *w,
+                     const Div &sf, const Relu &rp, bool pool, int8_t *out, uint8_t *code);
+// forward linear + Scaling + ReLU: x [n][k], w [m][k] -> a [n][m], region codes [n][m].
+void launch_linear_fwd_relu(hipStream_t s, int n, int k, int m, const int8_t *x, const int32_t *w,
+                            const Div &sf, const Relu &rp, int8_t *out, uint8_t *code);
+// learning / output layer: yhat = x w^T / sf, e = yhat - 32 onehot(labels).
+void launch_linear_fwd_loss(hipStream_t s, int n, int k, int g, const int8_t *x, const int32_t *w,
+                            const Div &sf, const int32_t *labels, int32_t *yhat, int32_t *e,
+                            uint32_t *flags);
+// dx[n][k] = sum_m e[n][m] w[m][k]; optional ReLU' with `code` -> int32 out (overflow flagged).
+void launch_linear_dx(hipStream_t s, int n, int k, int m, const int32_t *e, const int32_t *w,
+                      const uint8_t *code, const Relu &rp, int32_t *out, uint32_t *flags);
+// dw[m][k] = sum_n e[n][m] x[n][k], int64, overwritten.
+void launch_linear_dw(hipStream_t s, int n, int k, int m, const int32_t *e, const int8_t *x,
+                      int64_t *dw);
+// gradient at the block output -> gradient at the last layer's pre-activation.
+void launch_unpool_relu_bwd(hipStream_t s, int n, int h, int w, int c, bool pool,
+                            const int32_t *delta, const uint8_t *code, const Relu &rp,
+                            int32_t *g, uint32_t *flags);
+// conv input gradient; with `code` applies ReLU' of the previous layer.
+void launch_conv_dx(hipStream_t s, const ConvShape &sh, const int32_t *g, const int32_t *w,
+                    const uint8_t *code, const Relu &rp, int32_t *out, uint32_t *flags);
+// conv weight gradient, int64 KRSC, overwritten.
+void launch_conv_dw(hipStream_t s, const ConvShape &sh, const int32_t *g, const int8_t *x,
+                    int64_t *dw);
+// IntegerSGD (Alg. 1) in place.
+void launch_sgd(hipStream_t s, int32_t *w, const int64_t *dw, int64_t count, const Div &gamma,
+                const Div &eta, bool decay, uint32_t *flags);
+
+}  // namespace nitro

@@ -1,0 +1,275 @@
+"""ctypes binding of libnitro.so, the HIP library behind include/nitro.h.
+
+Argument marshalling only: every function hands torch tensors' device pointers to the C ABI and
+turns non-zero status codes into exceptions. No arithmetic of the method happens here; if the
+library is not built this module raises on import instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libnitro.so")
+
+MAX_LAYERS = 4
+MAX_BLOCKS = 8
+CONV3X3 = 0
+LINEAR = 1
+ROUND_FLOOR = 0
+ROUND_TRUNC = 1
+
+OK, EINVAL, EOVERFLOW, ELABEL, EHIP, ENOMEM, EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
+
+I32 = ctypes.c_int32
+I64 = ctypes.c_int64
+VP = ctypes.c_void_p
+
+
+class NitroError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__("%s: %s (%d)" % (what, status_str(code), code))
+        self.code = code
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("kind", I32), ("c_in", I32), ("c_out", I32)]
+
+
+class BlockDesc(ctypes.Structure):
+    _fields_ = [("n", I32), ("h", I32), ("w", I32), ("n_layers", I32),
+                ("layer", Layer * MAX_LAYERS), ("maxpool", I32), ("n_classes", I32),
+                ("alpha_inv", I32), ("round", I32)]
+
+
+class BlockParams(ctypes.Structure):
+    _fields_ = [("w", VP * MAX_LAYERS), ("w_lr", VP)]
+
+
+class BlockGrads(ctypes.Structure):
+    _fields_ = [("dw", VP * MAX_LAYERS), ("dw_lr", VP)]
+
+
+class BlockTaps(ctypes.Structure):
+    _fields_ = [("yhat", VP), ("e", VP), ("delta", VP), ("g", VP * MAX_LAYERS), ("dx", VP)]
+
+
+class NetDesc(ctypes.Structure):
+    _fields_ = [("n_blocks", I32), ("block", BlockDesc * MAX_BLOCKS), ("head", I32)]
+
+
+class NetParams(ctypes.Structure):
+    _fields_ = [("w", (VP * MAX_LAYERS) * MAX_BLOCKS), ("w_lr", VP * MAX_BLOCKS), ("w_head", VP)]
+
+
+class HParams(ctypes.Structure):
+    _fields_ = [("gamma_inv", I64), ("lambda_inv_fw", I64), ("lambda_inv_lr", I64), ("af", I64),
+                ("eta_fw", I64), ("eta_lr", I64)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libnitro.so is not built (run `python -m paper_2407_11698_amd.build`); "
+                          "there is no fallback path")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    sig = {
+        "nitro_create": (I32, [P(VP), ctypes.c_int, VP]),
+        "nitro_destroy": (None, [VP]),
+        "nitro_set_stream": (I32, [VP, VP]),
+        "nitro_sync_status": (I32, [VP]),
+        "nitro_status_str": (ctypes.c_char_p, [I32]),
+        "nitro_block_query": (I32, [P(BlockDesc), P(ctypes.c_size_t)]),
+        "nitro_block_forward": (I32, [VP, P(BlockDesc), P(BlockParams), VP, VP, VP]),
+        "nitro_block_backward": (I32, [VP, P(BlockDesc), P(BlockParams), VP, VP, VP, VP, VP,
+                                       P(BlockGrads), P(BlockTaps)]),
+        "nitro_head_backward": (I32, [VP, I32, I32, I32, VP, VP, VP, I32, VP, VP, VP]),
+        "nitro_integer_sgd_step": (I32, [VP, VP, VP, I64, I64, I64, I64, I32]),
+        "nitro_net_query": (I32, [P(NetDesc), P(ctypes.c_size_t)]),
+        "nitro_net_block_output": (I32, [P(NetDesc), VP, I32, P(VP)]),
+        "nitro_train_step": (I32, [VP, P(NetDesc), P(NetParams), VP, VP, VP, P(HParams)]),
+        "nitro_host_div": (I64, [I64, I64, I32]),
+        "nitro_host_relu_mu": (I32, [I32, I32]),
+        "nitro_kernel_timing": (I32, [VP, I32]),
+        "nitro_kernel_time": (I32, [VP, I32, P(ctypes.c_double), P(I64)]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+LIB = _load()
+
+# every symbol the header declares (checked by the ABI tests)
+EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_sync_status",
+           "nitro_status_str", "nitro_block_query", "nitro_block_forward", "nitro_block_backward",
+           "nitro_head_backward", "nitro_integer_sgd_step", "nitro_net_query",
+           "nitro_net_block_output", "nitro_train_step", "nitro_host_div", "nitro_host_relu_mu",
+           "nitro_kernel_timing", "nitro_kernel_time")
+
+
+def status_str(code: int) -> str:
+    return LIB.nitro_status_str(code).decode()
+
+
+def check(code: int, what: str) -> None:
+    if code != OK:
+        raise NitroError(code, what)
+
+
+def _p(t) -> Optional[int]:
+    """Device pointer of a tensor (None stays NULL)."""
+    return None if t is None else t.data_ptr()
+
+
+# ----------------------------------------------------------------------------- descriptors
+
+def layer(kind: int, c_in: int, c_out: int) -> Layer:
+    return Layer(kind, c_in, c_out)
+
+
+def block_desc(n: int, h: int, w: int, layers: Sequence[Layer], maxpool: bool, n_classes: int,
+               alpha_inv: int, round_mode: int = ROUND_FLOOR) -> BlockDesc:
+    d = BlockDesc()
+    d.n, d.h, d.w = n, h, w
+    d.n_layers = len(layers)
+    for j, ly in enumerate(layers):
+        d.layer[j] = ly
+    d.maxpool = 1 if maxpool else 0
+    d.n_classes = n_classes
+    d.alpha_inv = alpha_inv
+    d.round = round_mode
+    return d
+
+
+def block_query(desc: BlockDesc) -> int:
+    out = ctypes.c_size_t(0)
+    check(LIB.nitro_block_query(ctypes.byref(desc), ctypes.byref(out)), "nitro_block_query")
+    return out.value
+
+
+def net_desc(blocks: Sequence[BlockDesc], head: bool) -> NetDesc:
+    nd = NetDesc()
+    nd.n_blocks = len(blocks)
+    for b, d in enumerate(blocks):
+        nd.block[b] = d
+    nd.head = 1 if head else 0
+    return nd
+
+
+def net_query(nd: NetDesc) -> int:
+    out = ctypes.c_size_t(0)
+    check(LIB.nitro_net_query(ctypes.byref(nd), ctypes.byref(out)), "nitro_net_query")
+    return out.value
+
+
+def host_div(n: int, d: int, round_mode: int = ROUND_FLOOR) -> int:
+    return int(LIB.nitro_host_div(n, d, round_mode))
+
+
+def host_relu_mu(alpha_inv: int, round_mode: int = ROUND_FLOOR) -> int:
+    return int(LIB.nitro_host_relu_mu(alpha_inv, round_mode))
+
+
+# ----------------------------------------------------------------------------- context
+
+class Context:
+    """A library context bound to one device and one HIP stream (torch's current stream by
+    default)."""
+
+    def __init__(self, device: int = 0, stream=None):
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream(device)
+        self.device = device
+        self.stream = stream
+        h = VP()
+        check(LIB.nitro_create(ctypes.byref(h), device, VP(stream.cuda_stream)), "nitro_create")
+        self.h = h
+
+    def close(self):
+        if self.h:
+            LIB.nitro_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_stream(self, stream):
+        self.stream = stream
+        check(LIB.nitro_set_stream(self.h, VP(stream.cuda_stream)), "nitro_set_stream")
+
+    def sync_status(self) -> int:
+        return int(LIB.nitro_sync_status(self.h))
+
+    def sync(self) -> None:
+        check(self.sync_status(), "device status")
+
+    # -- block level --------------------------------------------------------------------
+    def block_forward(self, desc: BlockDesc, ws, x, a_out, state) -> None:
+        bp = BlockParams()
+        for j, w in enumerate(ws):
+            bp.w[j] = _p(w)
+        check(LIB.nitro_block_forward(self.h, ctypes.byref(desc), ctypes.byref(bp), _p(x),
+                                      _p(a_out), _p(state)), "nitro_block_forward")
+
+    def block_backward(self, desc: BlockDesc, ws, w_lr, x, a_out, labels, delta_out, state,
+                       dws, dw_lr, taps: Optional[dict] = None) -> None:
+        bp = BlockParams()
+        for j, w in enumerate(ws):
+            bp.w[j] = _p(w)
+        bp.w_lr = _p(w_lr)
+        gr = BlockGrads()
+        for j, d in enumerate(dws):
+            gr.dw[j] = _p(d)
+        gr.dw_lr = _p(dw_lr)
+        tp = None
+        if taps:
+            tp = BlockTaps()
+            tp.yhat = _p(taps.get("yhat"))
+            tp.e = _p(taps.get("e"))
+            tp.delta = _p(taps.get("delta"))
+            for j, g in enumerate(taps.get("g", [])):
+                tp.g[j] = _p(g)
+            tp.dx = _p(taps.get("dx"))
+        check(LIB.nitro_block_backward(self.h, ctypes.byref(desc), ctypes.byref(bp), _p(x),
+                                       _p(a_out), _p(labels), _p(delta_out), _p(state),
+                                       ctypes.byref(gr), ctypes.byref(tp) if tp else None),
+              "nitro_block_backward")
+
+    def head_backward(self, n, d, G, f, w, labels, round_mode, dw, yhat, e) -> None:
+        check(LIB.nitro_head_backward(self.h, n, d, G, _p(f), _p(w), _p(labels), round_mode,
+                                      _p(dw), _p(yhat), _p(e)), "nitro_head_backward")
+
+    def integer_sgd_step(self, w, dw, gamma_inv: int, lambda_inv: int, eta: int = -1,
+                         round_mode: int = ROUND_FLOOR) -> None:
+        check(LIB.nitro_integer_sgd_step(self.h, _p(w), _p(dw), w.numel(), gamma_inv, lambda_inv,
+                                         eta, round_mode), "nitro_integer_sgd_step")
+
+    # -- network level ------------------------------------------------------------------
+    def train_step(self, nd: NetDesc, params: NetParams, workspace, x, labels, hp: HParams) -> None:
+        check(LIB.nitro_train_step(self.h, ctypes.byref(nd), ctypes.byref(params), _p(workspace),
+                                   _p(x), _p(labels), ctypes.byref(hp)), "nitro_train_step")
+
+    def net_block_output_ptr(self, nd: NetDesc, workspace, b: int) -> int:
+        out = VP()
+        check(LIB.nitro_net_block_output(ctypes.byref(nd), _p(workspace), b, ctypes.byref(out)),
+              "nitro_net_block_output")
+        return out.value
+
+    # -- profiling ----------------------------------------------------------------------
+    def kernel_timing(self, enable: bool) -> None:
+        check(LIB.nitro_kernel_timing(self.h, 1 if enable else 0), "nitro_kernel_timing")
+
+    def kernel_time(self, cls: int):
+        ms = ctypes.c_double(0)
+        n = I64(0)
+        check(LIB.nitro_kernel_time(self.h, cls, ctypes.byref(ms), ctypes.byref(n)),
+              "nitro_kernel_time")
+        return ms.value, n.value

@@ -1,0 +1,269 @@
+"""GPU parity: the HIP library (through the C ABI) against the CPU oracle, element by element and
+bit-exact, on seeded inputs. Block-level calls at shapes that span several tiles and ragged
+tails, the edge cases of the method, IntegerSGD, the output layer and whole training steps."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2407_11698_amd import nitro as N
+from paper_2407_11698_amd import runner
+from paper_2407_11698_amd import workloads as WL
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda", 0)
+MODES = [(N.ROUND_FLOOR, O.FLOOR), (N.ROUND_TRUNC, O.TRUNC)]
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    c = N.Context(0)
+    yield c
+    c.close()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def rand(rng, shape, lo, hi, dtype):
+    return rng.integers(lo, hi, size=shape, endpoint=True).astype(dtype)
+
+
+def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dmax=1 << 15,
+              conv=True):
+    """One nitro_block_forward + nitro_block_backward against the oracle's block functions."""
+    print("block case", dict(n=n, h=h, w=w, chans=chans, pool=maxpool, G=G, alpha=alpha,
+                             mode=nm, wmax=wmax, conv=conv), flush=True)
+    J = len(chans) - 1
+    if conv:
+        x = rand(rng, (n, h, w, chans[0]), -127, 127, np.int8)
+        ws = [rand(rng, (chans[j + 1], 3, 3, chans[j]), -wmax, wmax, np.int32) for j in range(J)]
+        layers = [N.layer(N.CONV3X3, chans[j], chans[j + 1]) for j in range(J)]
+        hh, ww = h, w
+    else:
+        x = rand(rng, (n, chans[0]), -127, 127, np.int8)
+        ws = [rand(rng, (chans[j + 1], chans[j]), -wmax, wmax, np.int32) for j in range(J)]
+        layers = [N.layer(N.LINEAR, chans[j], chans[j + 1]) for j in range(J)]
+        hh = ww = 1
+    desc = N.block_desc(n, hh, ww, layers, maxpool, G, alpha, nm)
+    # oracle
+    rec = O.block_forward(x, ws, maxpool, alpha, om)
+    out_shape = rec.out.shape
+    d = int(np.prod(out_shape[1:]))
+    labels = rng.integers(0, max(G, 1), n).astype(np.int32)
+    if G > 0:
+        w_lr = rand(rng, (G, d), -wmax, wmax, np.int32)
+        f = rec.out.reshape(n, d)
+        rec.yhat = O.learning_forward(f, w_lr, om)
+        rec.e = O.loss_grad(rec.yhat, labels, G)
+        rec.dw_lr = O.linear_dw(rec.e, f)
+        rec.delta_fw = O.check_int32(O.linear_dx(rec.e, w_lr), "delta")
+        delta = rec.delta_fw.reshape(out_shape)
+    else:
+        w_lr = None
+        delta = rand(rng, out_shape, -dmax, dmax, np.int32)
+    O.block_backward(rec, ws, delta, maxpool, alpha, om, want_dx=True)
+    # GPU
+    xd = dev(x)
+    wd = [dev(a) for a in ws]
+    a_out = torch.empty(out_shape, dtype=torch.int8, device=DEV)
+    state = torch.empty(N.block_query(desc), dtype=torch.uint8, device=DEV)
+    ctx.block_forward(desc, wd, xd, a_out, state)
+    dws = [torch.empty(a.shape, dtype=torch.int64, device=DEV) for a in ws]
+    dw_lr = torch.empty((G, d), dtype=torch.int64, device=DEV) if G else None
+    taps = {"g": [torch.empty(l.zs.shape, dtype=torch.int32, device=DEV) for l in rec.layers],
+            "dx": torch.empty(x.shape, dtype=torch.int32, device=DEV)}
+    if G:
+        taps["yhat"] = torch.empty((n, G), dtype=torch.int32, device=DEV)
+        taps["e"] = torch.empty((n, G), dtype=torch.int32, device=DEV)
+        taps["delta"] = torch.empty(out_shape, dtype=torch.int32, device=DEV)
+    ctx.block_backward(desc, wd, dev(w_lr) if G else None, xd, a_out,
+                       dev(labels) if G else None, None if G else dev(delta), state, dws, dw_lr,
+                       taps)
+    ctx.sync()
+    assert np.array_equal(host(a_out), rec.out), "block output"
+    if G:
+        assert np.array_equal(host(taps["yhat"]), rec.yhat), "yhat"
+        assert np.array_equal(host(taps["e"]), rec.e), "e"
+        assert np.array_equal(host(dw_lr), rec.dw_lr), "dW learning"
+        assert np.array_equal(host(taps["delta"]), rec.delta_fw.reshape(out_shape)), "delta_fw"
+    for j in range(J):
+        assert np.array_equal(host(taps["g"][j]), rec.g[j]), "g layer %d" % j
+        assert np.array_equal(host(dws[j]), rec.dw[j]), "dW layer %d" % j
+    assert np.array_equal(host(taps["dx"]), rec.dx), "dx"
+
+
+CONV_CASES = [
+    # n, h, w, chans, pool, G, alpha, wmax
+    (2, 6, 6, [1, 16], True, 10, 10, 127),
+    (3, 10, 6, [3, 32], True, 10, 10, 127),
+    (2, 4, 4, [5, 7, 9], True, 3, 10, 127),
+    (2, 8, 8, [16, 32, 16], False, 0, 10, 127),
+    (1, 2, 2, [4, 4], True, 2, 2, 2000),
+    (2, 5, 7, [6, 5], False, 4, 3, 30000),
+    (2, 6, 10, [64, 64], True, 10, 10, 127),
+    (1, 4, 4, [128, 256], True, 100, 10, 9),
+    (2, 8, 8, [64, 128, 128], True, 100, 16, 6000),
+    (1, 32, 32, [3, 64, 64], True, 100, 10, 44),
+]
+
+
+@pytest.mark.parametrize("case", CONV_CASES)
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_conv_block(ctx, case, modes):
+    n, h, w, chans, pool, G, alpha, wmax = case
+    rng = np.random.default_rng(hash((n, h, w, tuple(chans), G)) % (1 << 31))
+    run_block(ctx, rng, n, h, w, chans, pool, G, alpha, modes[0], modes[1], wmax=wmax)
+
+
+@pytest.mark.parametrize("chans,G,wmax", [([784, 100], 10, 7), ([100, 50, 30], 10, 300),
+                                          ([37, 5], 3, 100000), ([64, 65], 0, 127)])
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_linear_block(ctx, chans, G, wmax, modes):
+    rng = np.random.default_rng(len(chans) * 1000 + chans[0])
+    run_block(ctx, rng, 64 if chans[0] == 784 else 5, 1, 1, chans, False, G, 10, modes[0],
+              modes[1], wmax=wmax, conv=False)
+
+
+@pytest.mark.parametrize("alpha", [2, 3, 4, 5, 8, 64, 100, 127, 128])
+def test_relu_alphas(ctx, alpha):
+    """Every NITRO-ReLU segment, for many alpha_inv: int16-range weights saturate both ends."""
+    rng = np.random.default_rng(alpha)
+    run_block(ctx, rng, 2, 6, 6, [8, 12], False, 0, alpha, N.ROUND_FLOOR, O.FLOOR, wmax=20000)
+
+
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_sgd(ctx, modes):
+    rng = np.random.default_rng(5)
+    w = rand(rng, (100003,), -(1 << 24), 1 << 24, np.int32)
+    dw = rand(rng, (100003,), -(1 << 40), 1 << 40, np.int64)
+    for gamma, lam, eta in [(512, 3000, -1), (327680, 25000, -1), (1, 0, -1), (4, 3, -1),
+                            (3276800, 25000, 1000)]:
+        ref = O.integer_sgd(w, dw, gamma, lam, modes[1], eta)
+        wd = dev(w)
+        ctx.integer_sgd_step(wd, dev(dw), gamma, lam, eta, modes[0])
+        ctx.sync()
+        assert np.array_equal(host(wd), ref), (gamma, lam, eta)
+
+
+def test_sgd_overflow_flag(ctx):
+    w = np.array([(1 << 31) - 1, 5], np.int32)
+    dw = np.array([-1, 0], np.int64)
+    wd = dev(w)
+    ctx.integer_sgd_step(wd, dev(dw), 1, 0)
+    assert ctx.sync_status() == N.EOVERFLOW
+    assert host(wd)[0] == (1 << 31) - 1
+    assert ctx.sync_status() == N.OK                   # the flag is cleared by reading it
+
+
+def test_label_flag(ctx):
+    n, d, G = 4, 8, 3
+    f = dev(np.ones((n, d), np.int8))
+    w = dev(np.ones((G, d), np.int32))
+    labels = dev(np.array([0, 1, 3, 2], np.int32))
+    dw = torch.empty((G, d), dtype=torch.int64, device=DEV)
+    yhat = torch.empty((n, G), dtype=torch.int32, device=DEV)
+    e = torch.empty((n, G), dtype=torch.int32, device=DEV)
+    ctx.head_backward(n, d, G, f, w, labels, N.ROUND_FLOOR, dw, yhat, e)
+    assert ctx.sync_status() == N.ELABEL
+
+
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_head(ctx, modes):
+    rng = np.random.default_rng(9)
+    n, d, G = 64, 2048, 10
+    f = rand(rng, (n, d), -87, 104, np.int8)
+    w = rand(rng, (G, d), -3000, 3000, np.int32)
+    labels = rng.integers(0, G, n).astype(np.int32)
+    yhat = O.learning_forward(f, w, modes[1])
+    e = O.loss_grad(yhat, labels, G)
+    dw_ref = O.linear_dw(e, f)
+    dw = torch.empty((G, d), dtype=torch.int64, device=DEV)
+    yd = torch.empty((n, G), dtype=torch.int32, device=DEV)
+    ed = torch.empty((n, G), dtype=torch.int32, device=DEV)
+    ctx.head_backward(n, d, G, dev(f), dev(w), dev(labels), modes[0], dw, yd, ed)
+    ctx.sync()
+    assert np.array_equal(host(yd), yhat)
+    assert np.array_equal(host(ed), e)
+    assert np.array_equal(host(dw), dw_ref)
+
+
+# ------------------------------------------------------------------ whole training iterations
+
+def oracle_net(wl, weights, om):
+    hp = O.Hyper(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr, wl.alpha_inv, wl.n_classes,
+                 mode=om, af_classes=wl.af_classes)
+    specs = [(len(b.layers), b.maxpool, b.learning) for b in wl.blocks]
+    return O.OracleNet(specs, wl.head, weights, hp)
+
+
+def check_training(ctx, wl, steps, nm, om):
+    print("training case", wl.name, "batch", wl.batch, "steps", steps, "mode", nm, flush=True)
+    dr = WL.draw_workload(wl, O.kaiming_bound, steps=steps)
+    ref = oracle_net(wl, dr.weights, om)
+    net = runner.GpuNet(wl, dr.weights, nm, ctx=ctx)
+    for s, (x, y) in enumerate(dr.batches):
+        st = ref.train_step(x, y)
+        net.step(dev(x), dev(y))
+        ctx.sync()
+        for b, rec in enumerate(st.blocks):
+            assert np.array_equal(host(net.block_output(b)), rec.out), "step %d block %d output" % (s, b)
+        for k, (wg, wo) in enumerate(zip(net.weights_np(), ref.w)):
+            assert np.array_equal(wg, wo), "step %d weight tensor %d" % (s, k)
+
+
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_train_tiny_cnn(ctx, modes):
+    check_training(ctx, WL.TINY_CNN, 10, *modes)
+
+
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_train_mlp(ctx, modes):
+    check_training(ctx, WL.MLP, 10, *modes)
+
+
+def test_train_small_cnn(ctx):
+    check_training(ctx, WL.SMALL_CNN, 10, N.ROUND_FLOOR, O.FLOOR)
+
+
+def test_train_vgg_reduced_batch(ctx):
+    check_training(ctx, WL.scaled(WL.VGG_CNN, 4), 10, N.ROUND_FLOOR, O.FLOOR)
+
+
+def test_conv_stress_reduced_batch(ctx):
+    wl = WL.scaled(WL.CONV_STRESS, 2)
+    print("stress case batch", wl.batch, flush=True)
+    dr = WL.draw_workload(wl, O.kaiming_bound)
+    ref = oracle_net(wl, dr.weights, O.FLOOR)
+    st = runner.GpuConvStress(wl, dr.weights[0], ctx=ctx)
+    x, _ = dr.batches[0]
+    xd, dd = dev(x), dev(dr.delta)
+    for r in range(3):
+        rec = ref.stress_repeat(x, dr.delta)
+        st.repeat(xd, dd)
+        ctx.sync()
+        assert np.array_equal(host(st.a), rec.out), "repeat %d output" % r
+        assert np.array_equal(host(st.dw), rec.dw[0]), "repeat %d dW" % r
+        assert np.array_equal(host(st.dx), rec.dx), "repeat %d dx" % r
+        assert np.array_equal(host(st.w), ref.w[0]), "repeat %d W" % r
+
+
+def test_deterministic(ctx):
+    wl = WL.scaled(WL.SMALL_CNN, 8)
+    dr = WL.draw_workload(wl, O.kaiming_bound, steps=3)
+    outs = []
+    for _ in range(2):
+        net = runner.GpuNet(wl, dr.weights, ctx=ctx)
+        for x, y in dr.batches:
+            net.step(dev(x), dev(y))
+        ctx.sync()
+        outs.append(net.weights_np())
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
