@@ -376,12 +376,12 @@ def block_backward(rec: BlockRecord, ws: list, delta_out, maxpool: bool, alpha_i
                 dx = conv3x3_dx(g, ws[j])
             else:
                 dx = linear_dx(g, ws[j])
-            dx = check_int32(dx, "input gradient")
             if j > 0:
+                dx = check_int32(dx, "input gradient")
                 g = check_int32(nitro_relu_grad(dx, rec.layers[j - 1].zs, alpha_inv, mode),
                                 "ReLU gradient")
             else:
-                rec.dx = dx
+                rec.dx = dx       # leaves the block: never used by the method, kept in int64
     rec.g = gs
     rec.dw = dws
 
