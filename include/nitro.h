@@ -123,7 +123,9 @@ typedef struct {
     int32_t *e;                            /* [n][G] loss gradient yhat - y                     */
     int32_t *delta;                        /* gradient at the block output (pooled), NHWC      */
     int32_t *g[NITRO_MAX_LAYERS];          /* gradient at layer j's pre-activation z_j, NHWC   */
-    int32_t *dx;                           /* input gradient of the first layer, NHWC          */
+    int64_t *dx;                           /* input gradient of the first layer, NHWC; int64
+                                              since no gradient leaves a block in the method,
+                                              so nothing bounds it to int32                    */
 } nitro_block_taps;
 
 /* Size in bytes of the block's state buffer: what the forward pass saves for the backward pass

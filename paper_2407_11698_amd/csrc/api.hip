@@ -199,7 +199,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         const Div sf = make_div(256 * g.d, desc->round);
         launch_linear_fwd_loss(s, n, (int)g.d, G, a_out, p->w_lr, sf, labels, yhat, e, ctx->flags);
         launch_linear_dw(s, n, (int)g.d, G, e, a_out, gr->dw_lr);
-        launch_linear_dx(s, n, (int)g.d, G, e, p->w_lr, nullptr, rp, dl, ctx->flags);
+        launch_linear_dx(s, n, (int)g.d, G, e, p->w_lr, nullptr, rp, dl, nullptr, ctx->flags);
         if (taps) {
             if (taps->yhat) (void)hipMemcpyAsync(taps->yhat, yhat, (size_t)n * G * 4, hipMemcpyDeviceToDevice, s);
             if (taps->e) (void)hipMemcpyAsync(taps->e, e, (size_t)n * G * 4, hipMemcpyDeviceToDevice, s);
@@ -228,19 +228,21 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         if (taps && taps->g[j])
             (void)hipMemcpyAsync(taps->g[j], gj, (size_t)n * L.out_elems * 4, hipMemcpyDeviceToDevice, s);
         int32_t *dst = nullptr;
+        int64_t *dst64 = nullptr;
         const uint8_t *code = nullptr;
         if (j > 0) {
             dst = gb[cur ^ 1];
             code = at(state, g.code[j - 1]);
         } else if (taps && taps->dx) {
-            dst = taps->dx;
+            dst64 = taps->dx;
         }
-        if (dst) {
+        if (dst || dst64) {
             if (L.conv) {
                 TimedLaunch t(ctx, CLS_CONV_DX);
-                launch_conv_dx(s, L.sh, gj, p->w[j], code, rp, dst, ctx->flags);
+                launch_conv_dx(s, L.sh, gj, p->w[j], code, rp, dst, dst64, ctx->flags);
             } else {
-                launch_linear_dx(s, n, L.sh.c, L.sh.co, gj, p->w[j], code, rp, dst, ctx->flags);
+                launch_linear_dx(s, n, L.sh.c, L.sh.co, gj, p->w[j], code, rp, dst, dst64,
+                                 ctx->flags);
             }
         }
         cur ^= 1;

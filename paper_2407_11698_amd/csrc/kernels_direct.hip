@@ -178,7 +178,8 @@ void launch_linear_fwd_loss(hipStream_t s, int n, int k, int g, const int8_t *x,
 // dx[n][k] = sum_m e[n][m] w[m][k]: one thread per (n, k); lanes along k read w coalesced.
 __global__ void k_linear_dx(int n, int k, int m, const int32_t *__restrict__ e,
                             const int32_t *__restrict__ w, const uint8_t *__restrict__ code,
-                            Relu rp, int32_t *__restrict__ out, uint32_t *flags)
+                            Relu rp, int32_t *__restrict__ out, int64_t *__restrict__ out64,
+                            uint32_t *flags)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)n * k) return;
@@ -186,6 +187,10 @@ __global__ void k_linear_dx(int n, int k, int m, const int32_t *__restrict__ e,
     const int32_t *er = e + (int64_t)row * m;
     int64_t acc = 0;
     for (int t = 0; t < m; t++) acc += (int64_t)er[t] * (int64_t)w[(int64_t)t * k + col];
+    if (out64) {
+        out64[i] = acc;
+        return;
+    }
     bool bad = !fits_i32(acc);
     if (code) {
         acc = relu_bwd(acc, code[i], rp);
@@ -196,11 +201,12 @@ __global__ void k_linear_dx(int n, int k, int m, const int32_t *__restrict__ e,
 }
 
 void launch_linear_dx(hipStream_t s, int n, int k, int m, const int32_t *e, const int32_t *w,
-                      const uint8_t *code, const Relu &rp, int32_t *out, uint32_t *flags)
+                      const uint8_t *code, const Relu &rp, int32_t *out, int64_t *out64,
+                      uint32_t *flags)
 {
     int64_t total = (int64_t)n * k;
     hipLaunchKernelGGL(k_linear_dx, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                       n, k, m, e, w, code, rp, out, flags);
+                       n, k, m, e, w, code, rp, out, out64, flags);
 }
 
 // dw[m][k] = sum_n e[n][m] x[n][k]: one thread per (m, k).
@@ -278,7 +284,8 @@ void launch_unpool_relu_bwd(hipStream_t s, int n, int h, int w, int c, bool pool
 // One thread per (pixel, ci): lanes along ci read W coalesced and g as a broadcast.
 __global__ void k_conv_dx_direct(ConvShape sh, const int32_t *__restrict__ g,
                                  const int32_t *__restrict__ w, const uint8_t *__restrict__ code,
-                                 Relu rp, int32_t *__restrict__ out, uint32_t *flags)
+                                 Relu rp, int32_t *__restrict__ out, int64_t *__restrict__ out64,
+                                 uint32_t *flags)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)sh.n * sh.h * sh.w * sh.c) return;
@@ -300,6 +307,10 @@ __global__ void k_conv_dx_direct(ConvShape sh, const int32_t *__restrict__ g,
                 acc += (int64_t)gp[co] * (int64_t)wp[(int64_t)co * 9 * sh.c];
         }
     }
+    if (out64) {
+        out64[i] = acc;
+        return;
+    }
     bool bad = !fits_i32(acc);
     if (code) {
         acc = relu_bwd(acc, code[i], rp);
@@ -310,11 +321,12 @@ __global__ void k_conv_dx_direct(ConvShape sh, const int32_t *__restrict__ g,
 }
 
 void launch_conv_dx(hipStream_t s, const ConvShape &sh, const int32_t *g, const int32_t *w,
-                    const uint8_t *code, const Relu &rp, int32_t *out, uint32_t *flags)
+                    const uint8_t *code, const Relu &rp, int32_t *out, int64_t *out64,
+                    uint32_t *flags)
 {
     int64_t total = (int64_t)sh.n * sh.h * sh.w * sh.c;
     hipLaunchKernelGGL(k_conv_dx_direct, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                       sh, g, w, code, rp, out, flags);
+                       sh, g, w, code, rp, out, out64, flags);
 }
 
 // ---------------------------------------------------------------------------------------------

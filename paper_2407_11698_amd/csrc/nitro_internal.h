@@ -119,9 +119,11 @@ void launch_linear_fwd_relu(hipStream_t s, int n, int k, int m, const int8_t *x,
 void launch_linear_fwd_loss(hipStream_t s, int n, int k, int g, const int8_t *x, const int32_t *w,
                             const Div &sf, const int32_t *labels, int32_t *yhat, int32_t *e,
                             uint32_t *flags);
-// dx[n][k] = sum_m e[n][m] w[m][k]; optional ReLU' with `code` -> int32 out (overflow flagged).
+// dx[n][k] = sum_m e[n][m] w[m][k]; optional ReLU' with `code` -> int32 out (overflow flagged),
+// or the raw sum into out64 (int64) when out64 is not null.
 void launch_linear_dx(hipStream_t s, int n, int k, int m, const int32_t *e, const int32_t *w,
-                      const uint8_t *code, const Relu &rp, int32_t *out, uint32_t *flags);
+                      const uint8_t *code, const Relu &rp, int32_t *out, int64_t *out64,
+                      uint32_t *flags);
 // dw[m][k] = sum_n e[n][m] x[n][k], int64, overwritten.
 void launch_linear_dw(hipStream_t s, int n, int k, int m, const int32_t *e, const int8_t *x,
                       int64_t *dw);
@@ -129,9 +131,11 @@ void launch_linear_dw(hipStream_t s, int n, int k, int m, const int32_t *e, cons
 void launch_unpool_relu_bwd(hipStream_t s, int n, int h, int w, int c, bool pool,
                             const int32_t *delta, const uint8_t *code, const Relu &rp,
                             int32_t *g, uint32_t *flags);
-// conv input gradient; with `code` applies ReLU' of the previous layer.
+// conv input gradient; with `code` applies ReLU' of the previous layer and writes int32 `out`
+// (overflow flagged); with out64 writes the raw int64 sum instead.
 void launch_conv_dx(hipStream_t s, const ConvShape &sh, const int32_t *g, const int32_t *w,
-                    const uint8_t *code, const Relu &rp, int32_t *out, uint32_t *flags);
+                    const uint8_t *code, const Relu &rp, int32_t *out, int64_t *out64,
+                    uint32_t *flags);
 // conv weight gradient, int64 KRSC, overwritten.
 void launch_conv_dw(hipStream_t s, const ConvShape &sh, const int32_t *g, const int8_t *x,
                     int64_t *dw);

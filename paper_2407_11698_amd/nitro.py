@@ -10,6 +10,10 @@ import ctypes
 import os
 from typing import Optional, Sequence
 
+# torch ships its own HIP runtime with the same soname as /opt/rocm's. Importing torch first makes
+# libnitro.so bind to that one runtime; loading the library first would pull in a second one.
+import torch  # noqa: F401
+
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libnitro.so")
 

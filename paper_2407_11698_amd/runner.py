@@ -96,7 +96,7 @@ class GpuConvStress:
         self.state = torch.empty(N.block_query(self.desc), dtype=torch.uint8, device=self.dev)
         self.a = torch.empty((wl.batch, h, w, ly.c_out), dtype=torch.int8, device=self.dev)
         self.dw = torch.empty((ly.c_out, 3, 3, ly.c_in), dtype=torch.int64, device=self.dev)
-        self.dx = torch.empty((wl.batch, h, w, ly.c_in), dtype=torch.int32, device=self.dev)
+        self.dx = torch.empty((wl.batch, h, w, ly.c_in), dtype=torch.int64, device=self.dev)
         self.gamma_fw = (1 << 6) * wl.af_classes * wl.gamma_inv
 
     def repeat(self, x: torch.Tensor, delta: torch.Tensor, want_dx: bool = True) -> None:

@@ -58,18 +58,24 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
     out_shape = rec.out.shape
     d = int(np.prod(out_shape[1:]))
     labels = rng.integers(0, max(G, 1), n).astype(np.int32)
-    if G > 0:
-        w_lr = rand(rng, (G, d), -wmax, wmax, np.int32)
-        f = rec.out.reshape(n, d)
-        rec.yhat = O.learning_forward(f, w_lr, om)
-        rec.e = O.loss_grad(rec.yhat, labels, G)
-        rec.dw_lr = O.linear_dw(rec.e, f)
-        rec.delta_fw = O.check_int32(O.linear_dx(rec.e, w_lr), "delta")
-        delta = rec.delta_fw.reshape(out_shape)
-    else:
-        w_lr = None
-        delta = rand(rng, out_shape, -dmax, dmax, np.int32)
-    O.block_backward(rec, ws, delta, maxpool, alpha, om, want_dx=True)
+    want_dx, expect_overflow = True, False
+    w_lr = rand(rng, (G, d), -wmax, wmax, np.int32) if G else None
+    delta = None if G else rand(rng, out_shape, -dmax, dmax, np.int32)
+    try:
+        if G > 0:
+            f = rec.out.reshape(n, d)
+            rec.yhat = O.learning_forward(f, w_lr, om)
+            rec.e = O.check_int32(O.loss_grad(rec.yhat, labels, G), "e")
+            rec.dw_lr = O.linear_dw(rec.e, f)
+            rec.delta_fw = O.check_int32(O.linear_dx(rec.e, w_lr), "delta")
+            delta = rec.delta_fw.reshape(out_shape)
+        try:
+            O.block_backward(rec, ws, delta, maxpool, alpha, om, want_dx=True)
+        except OverflowError:
+            want_dx = False              # only the optional input gradient may be out of range
+            O.block_backward(rec, ws, delta, maxpool, alpha, om, want_dx=False)
+    except OverflowError:
+        expect_overflow = True
     # GPU
     xd = dev(x)
     wd = [dev(a) for a in ws]
@@ -79,7 +85,7 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
     dws = [torch.empty(a.shape, dtype=torch.int64, device=DEV) for a in ws]
     dw_lr = torch.empty((G, d), dtype=torch.int64, device=DEV) if G else None
     taps = {"g": [torch.empty(l.zs.shape, dtype=torch.int32, device=DEV) for l in rec.layers],
-            "dx": torch.empty(x.shape, dtype=torch.int32, device=DEV)}
+            "dx": torch.empty(x.shape, dtype=torch.int64, device=DEV) if want_dx else None}
     if G:
         taps["yhat"] = torch.empty((n, G), dtype=torch.int32, device=DEV)
         taps["e"] = torch.empty((n, G), dtype=torch.int32, device=DEV)
@@ -87,6 +93,9 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
     ctx.block_backward(desc, wd, dev(w_lr) if G else None, xd, a_out,
                        dev(labels) if G else None, None if G else dev(delta), state, dws, dw_lr,
                        taps)
+    if expect_overflow:
+        assert ctx.sync_status() == N.EOVERFLOW
+        return
     ctx.sync()
     assert np.array_equal(host(a_out), rec.out), "block output"
     if G:
@@ -97,7 +106,8 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
     for j in range(J):
         assert np.array_equal(host(taps["g"][j]), rec.g[j]), "g layer %d" % j
         assert np.array_equal(host(dws[j]), rec.dw[j]), "dW layer %d" % j
-    assert np.array_equal(host(taps["dx"]), rec.dx), "dx"
+    if want_dx:
+        assert np.array_equal(host(taps["dx"]), rec.dx), "dx"
 
 
 CONV_CASES = [
@@ -124,12 +134,19 @@ def test_conv_block(ctx, case, modes):
 
 
 @pytest.mark.parametrize("chans,G,wmax", [([784, 100], 10, 7), ([100, 50, 30], 10, 300),
-                                          ([37, 5], 3, 100000), ([64, 65], 0, 127)])
+                                          ([37, 5], 3, 20000), ([64, 65], 0, 127)])
 @pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
 def test_linear_block(ctx, chans, G, wmax, modes):
     rng = np.random.default_rng(len(chans) * 1000 + chans[0])
     run_block(ctx, rng, 64 if chans[0] == 784 else 5, 1, 1, chans, False, G, 10, modes[0],
               modes[1], wmax=wmax, conv=False)
+
+
+def test_gradient_overflow_is_flagged(ctx):
+    """A block whose error signal cannot fit int32: the oracle raises, the GPU flags it."""
+    rng = np.random.default_rng(77)
+    run_block(ctx, rng, 2, 6, 6, [32, 32, 32], False, 0, 10, N.ROUND_FLOOR, O.FLOOR,
+              wmax=1 << 20, dmax=1 << 15)
 
 
 @pytest.mark.parametrize("alpha", [2, 3, 4, 5, 8, 64, 100, 127, 128])
@@ -143,9 +160,9 @@ def test_relu_alphas(ctx, alpha):
 def test_sgd(ctx, modes):
     rng = np.random.default_rng(5)
     w = rand(rng, (100003,), -(1 << 24), 1 << 24, np.int32)
-    dw = rand(rng, (100003,), -(1 << 40), 1 << 40, np.int64)
     for gamma, lam, eta in [(512, 3000, -1), (327680, 25000, -1), (1, 0, -1), (4, 3, -1),
                             (3276800, 25000, 1000)]:
+        dw = rand(rng, (100003,), -gamma << 20, gamma << 20, np.int64)
         ref = O.integer_sgd(w, dw, gamma, lam, modes[1], eta)
         wd = dev(w)
         ctx.integer_sgd_step(wd, dev(dw), gamma, lam, eta, modes[0])
