@@ -1,0 +1,169 @@
+"""Benchmark: images/s of the NITRO-D integer training iteration on one MI355X.
+
+Workload: the VGG-style integer CNN (3x32x32 int8 inputs, batch 256, four blocks of two 3x3
+convolutions 3-64-64, 64-128-128, 128-256-256, 256-512-512, 2x2 max-pool and a learning layer to
+100 classes per block), trained with nitro_train_step. Inputs are seeded synthetic data already
+resident in HBM. The timed loop replays the ten-step trajectory the parity tests check: every ten
+steps the weights are reset to their initial values, so each timed step is one of those ten
+verified iterations.
+
+Prints one JSON line with the throughput, the roofline position of the dominant kernel (its own
+HIP-event time inside the timed region) and the CPU oracle's throughput on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# MI355X published peaks
+PEAK_INT8_TOPS = 5000.0          # dense int8 MFMA, TOP/s
+PEAK_HBM_GBS = 8000.0
+
+KERNEL_CLASSES = {0: "conv_fwd", 1: "conv_dx", 2: "conv_dw"}
+
+
+def conv_layer_ops(wl):
+    """Algorithmic ops (2 x MACs) per training iteration of every conv GEMM, by class.
+
+    forward: N*H*W*C_out*9*C_in MACs per layer; weight gradient: the same count; input gradient:
+    the same count, for every layer but the first of a block (whose input gradient the method
+    never needs)."""
+    from paper_2407_11698_amd.workloads import Conv3x3
+    ops = {"conv_fwd": 0, "conv_dx": 0, "conv_dw": 0}
+    for (inp, _), blk in zip(wl.block_shapes(), wl.blocks):
+        if not isinstance(blk.layers[0], Conv3x3):
+            continue
+        _, h, w = inp
+        for j, ly in enumerate(blk.layers):
+            macs = wl.batch * h * w * ly.c_out * 9 * ly.c_in
+            ops["conv_fwd"] += 2 * macs
+            ops["conv_dw"] += 2 * macs
+            if j > 0:
+                ops["conv_dx"] += 2 * macs
+    return ops
+
+
+def cpu_baseline(wl, budget_s: float = 20.0):
+    """The CPU oracle, untuned, on a bounded sample of the same workload: full training
+    iterations at a reduced batch, repeated until about `budget_s` seconds have passed."""
+    from oracle import oracle as O
+    from paper_2407_11698_amd import workloads as WL
+    batch = 16
+    sample = WL.scaled(wl, batch)
+    dr = WL.draw_workload(sample, O.kaiming_bound, steps=sample.steps)
+    hp = O.Hyper(sample.gamma_inv, sample.lambda_inv_fw, sample.lambda_inv_lr, sample.alpha_inv,
+                 sample.n_classes)
+    net = O.OracleNet([(len(b.layers), b.maxpool, b.learning) for b in sample.blocks],
+                      sample.head, dr.weights, hp)
+    t0 = time.perf_counter()
+    steps = 0
+    while steps < len(dr.batches):
+        net.train_step(*dr.batches[steps])
+        steps += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": round(batch * steps / el, 3), "unit": "images/s", "cores": O.num_threads(),
+            "kind": "oracle",
+            "sample": "%d training iterations of the same workload at batch %d (%.1f s); "
+                      "host %s" % (steps, batch, el, platform.processor() or platform.machine())}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only; --gpus %d is not supported" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2407_11698_amd import nitro as N
+    from paper_2407_11698_amd import runner
+    from paper_2407_11698_amd import workloads as WL
+
+    wl = WL.VGG_CNN
+    dev = torch.device("cuda", 0)
+    dr = WL.draw_workload(wl, runner.kaiming_bound)
+    w0 = [torch.from_numpy(w).to(dev) for w in dr.weights]
+    xs = [torch.from_numpy(x).to(dev) for x, _ in dr.batches]
+    ys = [torch.from_numpy(y).to(dev) for _, y in dr.batches]
+    net = runner.GpuNet(wl, dr.weights)
+    period = len(xs)
+
+    def run(k0, k):
+        for i in range(k0, k0 + k):
+            if i % period == 0:
+                for a, b in zip(net.w, w0):
+                    a.copy_(b)
+            net.step(xs[i % period], ys[i % period])
+
+    run(0, args.warmup)
+    net.ctx.sync()
+    net.ctx.kernel_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(args.warmup, args.steps)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    net.ctx.sync()                        # raises if any kernel flagged overflow or a bad label
+    ktime = {KERNEL_CLASSES[c]: net.ctx.kernel_time(c) for c in KERNEL_CLASSES}
+    net.ctx.kernel_timing(False)
+
+    ops = conv_layer_ops(wl)
+    per_class = {}
+    for name, (ms, launches) in ktime.items():
+        tops = ops[name] * args.steps / (ms * 1e-3) / 1e12 if ms > 0 else 0.0
+        per_class[name] = {"ms_per_step": round(ms / args.steps, 4), "launches": launches,
+                           "algorithmic_TOPs": round(tops, 3)}
+    dom = max(per_class, key=lambda k: per_class[k]["ms_per_step"])
+    achieved = per_class[dom]["algorithmic_TOPs"]
+    conv_ms = sum(v["ms_per_step"] for v in per_class.values())
+    conv_tops = sum(ops.values()) / (conv_ms * 1e-3) / 1e12 if conv_ms > 0 else 0.0
+
+    out = {
+        "metric": "images/s per IntegerSGD training step; int8 conv TOPS as % of MFMA peak",
+        "value": round(wl.batch * args.steps / el, 2),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(el * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "input": "3x32x32 int8",
+                   "blocks": "conv 3-64-64, 64-128-128, 128-256-256, 256-512-512, pool, "
+                             "learning layer to 100 classes", "gamma_inv": wl.gamma_inv,
+                   "lambda_inv_fw": wl.lambda_inv_fw, "lambda_inv_lr": wl.lambda_inv_lr,
+                   "alpha_inv": wl.alpha_inv, "rounding": "floor"},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved,
+                     "peak": PEAK_INT8_TOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_INT8_TOPS, 5), "traffic": None},
+        "conv": {"algorithmic_TOPs": round(conv_tops, 3),
+                 "frac_of_int8_peak": round(conv_tops / PEAK_INT8_TOPS, 5),
+                 "per_kernel_class": per_class},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

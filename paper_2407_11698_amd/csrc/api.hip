@@ -86,6 +86,9 @@ struct BlockGeom {
     // state buffer offsets
     size_t act[NITRO_MAX_LAYERS];
     size_t code[NITRO_MAX_LAYERS];
+    size_t wf[NITRO_MAX_LAYERS];   // conv: 4 int8 limb planes of W, [co][9 ci]
+    size_t wt[NITRO_MAX_LAYERS];   // conv: 4 int8 limb planes of W, [ci][9 co]
+    size_t slots;                  // uint32 [8]: max|W_j| (0..3), max|g_j| (4..7)
     size_t yhat, e, delta, g0, g1;
     size_t total;
 };
@@ -138,6 +141,12 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
         off = align256(off + (size_t)(last ? (d->maxpool ? g->out_elems : full) : full));
         if (full > gmax) gmax = full;
     }
+    for (int j = 0; j < g->J; j++) {
+        const int64_t nw = conv ? 9 * (int64_t)d->layer[j].c_in * d->layer[j].c_out : 0;
+        g->wf[j] = off; off = align256(off + (size_t)(4 * nw));
+        g->wt[j] = off; off = align256(off + (size_t)(4 * nw));
+    }
+    g->slots = off; off = align256(off + 8 * 4);
     const int64_t G = d->n_classes;
     g->yhat = off;  off = align256(off + (size_t)(d->n * G) * 4);
     g->e = off;     off = align256(off + (size_t)(d->n * G) * 4);
@@ -164,16 +173,26 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
 {
     hipStream_t s = ctx->stream;
     const Relu rp = make_relu(desc->alpha_inv, desc->round);
+    uint32_t *slots = (uint32_t *)at(state, g.slots);
+    if (hipMemsetAsync(slots, 0, 8 * 4, s) != hipSuccess) return NITRO_EHIP;
     const int8_t *cur = x;
     for (int j = 0; j < g.J; j++) {
         const LayerGeom &L = g.L[j];
         const bool last = j == g.J - 1;
+        const bool pool = last && desc->maxpool;
         int8_t *out = last ? a_out : (int8_t *)at(state, g.act[j]);
         uint8_t *code = at(state, g.code[j]);
         const Div sf = make_div(L.sf, desc->round);
         if (L.conv) {
+            // limb planes for this call's forward and input-gradient GEMMs, and max|W_j|
+            launch_pack_conv_weights(s, p->w[j], L.sh.co, L.sh.c, (int8_t *)at(state, g.wf[j]),
+                                     (int8_t *)at(state, g.wt[j]), &slots[j]);
             TimedLaunch t(ctx, CLS_CONV_FWD);
-            launch_conv_fwd(s, L.sh, cur, p->w[j], sf, rp, last && desc->maxpool, out, code);
+            if (mfma_conv_fwd_ok(L.sh, pool))
+                launch_conv_fwd_mfma(s, L.sh, cur, (const int8_t *)at(state, g.wf[j]), &slots[j],
+                                     sf, rp, pool, out, code, ctx->flags);
+            else
+                launch_conv_fwd(s, L.sh, cur, p->w[j], sf, rp, pool, out, code);
         } else {
             launch_linear_fwd_relu(s, L.sh.n, L.sh.c, L.sh.co, cur, p->w[j], sf, rp, out, code);
         }
@@ -209,10 +228,12 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
     }
     int32_t *gb[2] = {(int32_t *)at(state, g.g0), (int32_t *)at(state, g.g1)};
     const int J = g.J;
+    uint32_t *slots = (uint32_t *)at(state, g.slots);
+    if (hipMemsetAsync(slots + 4, 0, 4 * 4, s) != hipSuccess) return NITRO_EHIP;
     {
         const LayerGeom &L = g.L[J - 1];
         launch_unpool_relu_bwd(s, n, L.sh.h, L.sh.w, L.sh.co, desc->maxpool != 0, delta,
-                               at(state, g.code[J - 1]), rp, gb[0], ctx->flags);
+                               at(state, g.code[J - 1]), rp, gb[0], &slots[4 + J - 1], ctx->flags);
     }
     int cur = 0;
     for (int j = J - 1; j >= 0; j--) {
@@ -237,9 +258,14 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
             dst64 = taps->dx;
         }
         if (dst || dst64) {
+            uint32_t *gmax_out = j > 0 ? &slots[4 + j - 1] : nullptr;
             if (L.conv) {
                 TimedLaunch t(ctx, CLS_CONV_DX);
-                launch_conv_dx(s, L.sh, gj, p->w[j], code, rp, dst, dst64, ctx->flags);
+                if (mfma_conv_dx_ok(L.sh))
+                    launch_conv_dx_mfma(s, L.sh, gj, &slots[4 + j], (const int8_t *)at(state, g.wt[j]),
+                                        &slots[j], code, rp, dst, dst64, gmax_out, ctx->flags);
+                else
+                    launch_conv_dx(s, L.sh, gj, p->w[j], code, rp, dst, dst64, gmax_out, ctx->flags);
             } else {
                 launch_linear_dx(s, n, L.sh.c, L.sh.co, gj, p->w[j], code, rp, dst, dst64,
                                  ctx->flags);

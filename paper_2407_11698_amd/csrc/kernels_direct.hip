@@ -230,14 +230,27 @@ void launch_linear_dw(hipStream_t s, int n, int k, int m, const int32_t *e, cons
 }
 
 // ---------------------------------------------------------------------------------------------
+// max|v| over the wave, then one atomic per wave (the slot must be zeroed first).
+__device__ inline void wave_abs_max_to(uint32_t *gmax, int64_t v)
+{
+    uint32_t m = fits_i32(v) ? (v < 0 ? (uint32_t)(-v) : (uint32_t)v) : 0xFFFFFFFFu;
+    for (int off = 32; off > 0; off >>= 1) {
+        uint32_t o = __shfl_xor(m, off, 64);
+        m = o > m ? o : m;
+    }
+    if ((threadIdx.x & 63) == 0 && m) atomicMax(gmax, m);
+}
+
 // Gradient at the block output -> gradient at the last layer's z (un-pool + ReLU').
 __global__ void k_unpool_relu_bwd(int n, int h, int w, int c, const int32_t *__restrict__ delta,
                                   const uint8_t *__restrict__ code, Relu rp,
-                                  int32_t *__restrict__ g, uint32_t *flags)
+                                  int32_t *__restrict__ g, uint32_t *gmax, uint32_t *flags)
 {
     int H2 = h / 2, W2 = w / 2;
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (int64_t)n * H2 * W2 * c) return;
+    const bool live = i < (int64_t)n * H2 * W2 * c;
+    if (gmax) wave_abs_max_to(gmax, live ? relu_bwd(delta[i], (uint8_t)(code[i] >> 2), rp) : 0);
+    if (!live) return;
     int ch = (int)(i % c);
     int64_t p = i / c;
     int q2 = (int)(p % W2);
@@ -255,27 +268,29 @@ __global__ void k_unpool_relu_bwd(int n, int h, int w, int c, const int32_t *__r
 
 __global__ void k_relu_bwd(int64_t count, const int32_t *__restrict__ delta,
                            const uint8_t *__restrict__ code, Relu rp, int32_t *__restrict__ g,
-                           uint32_t *flags)
+                           uint32_t *gmax, uint32_t *flags)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= count) return;
-    int64_t v = relu_bwd(delta[i], code[i], rp);
+    const bool live = i < count;
+    int64_t v = live ? relu_bwd(delta[i], code[i], rp) : 0;
+    if (gmax) wave_abs_max_to(gmax, v);
+    if (!live) return;
     if (!fits_i32(v)) raise_flag(flags, FLAG_OVERFLOW);
     g[i] = (int32_t)v;
 }
 
 void launch_unpool_relu_bwd(hipStream_t s, int n, int h, int w, int c, bool pool,
                             const int32_t *delta, const uint8_t *code, const Relu &rp,
-                            int32_t *g, uint32_t *flags)
+                            int32_t *g, uint32_t *gmax, uint32_t *flags)
 {
     if (pool) {
         int64_t total = (int64_t)n * (h / 2) * (w / 2) * c;
         hipLaunchKernelGGL(k_unpool_relu_bwd, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                           n, h, w, c, delta, code, rp, g, flags);
+                           n, h, w, c, delta, code, rp, g, gmax, flags);
     } else {
         int64_t total = (int64_t)n * h * w * c;
         hipLaunchKernelGGL(k_relu_bwd, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                           total, delta, code, rp, g, flags);
+                           total, delta, code, rp, g, gmax, flags);
     }
 }
 
@@ -285,10 +300,14 @@ void launch_unpool_relu_bwd(hipStream_t s, int n, int h, int w, int c, bool pool
 __global__ void k_conv_dx_direct(ConvShape sh, const int32_t *__restrict__ g,
                                  const int32_t *__restrict__ w, const uint8_t *__restrict__ code,
                                  Relu rp, int32_t *__restrict__ out, int64_t *__restrict__ out64,
-                                 uint32_t *flags)
+                                 uint32_t *gmax, uint32_t *flags)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (int64_t)sh.n * sh.h * sh.w * sh.c) return;
+    const bool live = i < (int64_t)sh.n * sh.h * sh.w * sh.c;
+    if (!live) {
+        if (gmax) wave_abs_max_to(gmax, 0);
+        return;
+    }
     int ci = (int)(i % sh.c);
     int64_t p = i / sh.c;
     int q = (int)(p % sh.w);
@@ -316,17 +335,18 @@ __global__ void k_conv_dx_direct(ConvShape sh, const int32_t *__restrict__ g,
         acc = relu_bwd(acc, code[i], rp);
         bad |= !fits_i32(acc);
     }
+    if (gmax) wave_abs_max_to(gmax, acc);
     if (bad) raise_flag(flags, FLAG_OVERFLOW);
     out[i] = (int32_t)acc;
 }
 
 void launch_conv_dx(hipStream_t s, const ConvShape &sh, const int32_t *g, const int32_t *w,
                     const uint8_t *code, const Relu &rp, int32_t *out, int64_t *out64,
-                    uint32_t *flags)
+                    uint32_t *gmax, uint32_t *flags)
 {
     int64_t total = (int64_t)sh.n * sh.h * sh.w * sh.c;
     hipLaunchKernelGGL(k_conv_dx_direct, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                       sh, g, w, code, rp, out, out64, flags);
+                       sh, g, w, code, rp, out, out64, gmax, flags);
 }
 
 // ---------------------------------------------------------------------------------------------

@@ -127,15 +127,31 @@ void launch_linear_dx(hipStream_t s, int n, int k, int m, const int32_t *e, cons
 // dw[m][k] = sum_n e[n][m] x[n][k], int64, overwritten.
 void launch_linear_dw(hipStream_t s, int n, int k, int m, const int32_t *e, const int8_t *x,
                       int64_t *dw);
-// gradient at the block output -> gradient at the last layer's pre-activation.
+// gradient at the block output -> gradient at the last layer's pre-activation; max|g| -> *gmax
+// (when not null).
 void launch_unpool_relu_bwd(hipStream_t s, int n, int h, int w, int c, bool pool,
                             const int32_t *delta, const uint8_t *code, const Relu &rp,
-                            int32_t *g, uint32_t *flags);
+                            int32_t *g, uint32_t *gmax, uint32_t *flags);
 // conv input gradient; with `code` applies ReLU' of the previous layer and writes int32 `out`
-// (overflow flagged); with out64 writes the raw int64 sum instead.
+// (overflow flagged, max|out| -> *gmax when not null); with out64 writes the raw int64 sum.
 void launch_conv_dx(hipStream_t s, const ConvShape &sh, const int32_t *g, const int32_t *w,
                     const uint8_t *code, const Relu &rp, int32_t *out, int64_t *out64,
-                    uint32_t *flags);
+                    uint32_t *gmax, uint32_t *flags);
+
+// ---- int8 MFMA implicit-GEMM path (conv_mfma.hip)
+bool mfma_conv_fwd_ok(const ConvShape &sh, bool pool);
+bool mfma_conv_dx_ok(const ConvShape &sh);
+// W int32 KRSC -> 4 balanced int8 limb planes [co][9 ci] (wf) and [ci][9 co] (wt, optional);
+// max|W| -> *wmax (atomic max: the slot must be zeroed first).
+void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,
+                              int8_t *wt, uint32_t *wmax);
+void launch_conv_fwd_mfma(hipStream_t s, const ConvShape &sh, const int8_t *x, const int8_t *wf,
+                          const uint32_t *wmax, const Div &sf, const Relu &rp, bool pool,
+                          int8_t *out, uint8_t *code, uint32_t *flags);
+void launch_conv_dx_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g, const uint32_t *gmax_in,
+                         const int8_t *wt, const uint32_t *wmax, const uint8_t *prev_code,
+                         const Relu &rp, int32_t *gout, int64_t *out64, uint32_t *gmax_out,
+                         uint32_t *flags);
 // conv weight gradient, int64 KRSC, overwritten.
 void launch_conv_dw(hipStream_t s, const ConvShape &sh, const int32_t *g, const int8_t *x,
                     int64_t *dw);
