@@ -242,7 +242,10 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         const int32_t *gj = gb[cur];
         if (L.conv) {
             TimedLaunch t(ctx, CLS_CONV_DW);
-            launch_conv_dw(s, L.sh, gj, xin, gr->dw[j]);
+            if (mfma_conv_dw_ok(L.sh))
+                launch_conv_dw_mfma(s, L.sh, gj, &slots[4 + j], xin, gr->dw[j], ctx->flags);
+            else
+                launch_conv_dw(s, L.sh, gj, xin, gr->dw[j]);
         } else {
             launch_linear_dw(s, n, L.sh.c, L.sh.co, gj, xin, gr->dw[j]);
         }

@@ -77,7 +77,7 @@ __global__ void k_pack_conv_weights(const int32_t *__restrict__ w, int co, int c
         }
     }
     m = wave_max_u32(m);
-    if ((threadIdx.x & 63) == 0 && m) atomicMax(wmax, m);
+    if ((threadIdx.x & 63) == 0) slot_max(wmax, m);
 }
 
 void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,
@@ -312,7 +312,7 @@ __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
         if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
         if (p.gmax) {
             mx = wave_max_u32(mx);
-            if (lane == 0 && mx) atomicMax(p.gmax, mx);
+            if (lane == 0) slot_max(p.gmax, mx);
         }
     }
 }
@@ -332,12 +332,14 @@ static void launch_igemm(hipStream_t s, const IgemmArgs &a)
     }
 }
 
+// K = 9 * ck <= 9 * 8192 keeps 128 * 128 * K below 2^31 (one limb pass in int32).
 bool mfma_conv_fwd_ok(const ConvShape &sh, bool pool)
 {
-    return sh.c % 16 == 0 && (!pool || (sh.w % 2 == 0 && sh.h % 2 == 0 && 128 % (2 * sh.w) == 0));
+    return sh.c % 16 == 0 && sh.c <= 8192 &&
+           (!pool || (sh.w % 2 == 0 && sh.h % 2 == 0 && 128 % (2 * sh.w) == 0));
 }
 
-bool mfma_conv_dx_ok(const ConvShape &sh) { return sh.co % 16 == 0; }
+bool mfma_conv_dx_ok(const ConvShape &sh) { return sh.co % 16 == 0 && sh.co <= 8192; }
 
 void launch_conv_fwd_mfma(hipStream_t s, const ConvShape &sh, const int8_t *x, const int8_t *wf,
                           const uint32_t *wmax, const Div &sf, const Relu &rp, bool pool,
@@ -368,6 +370,170 @@ void launch_conv_dx_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g, c
     a.prev_code = prev_code; a.gout = gout; a.out64 = out64; a.gmax = gmax_out;
     a.flags = flags;
     launch_igemm<IG_DX>(s, a);
+}
+
+
+// =============================================================================================
+// Weight gradient: dW[co][r][s][ci] = sum_p g[p][co] * x[p + (r-1, s-1)][ci]  (int64 result)
+//
+// GEMM with M = co, N = (tap, ci), K = pixels. Both operands are stored channel-contiguous
+// (NHWC), so each 4 pixel x 4 channel byte block is transposed in registers (v_perm_b32) on its
+// way into LDS, where rows are K(pixel)-contiguous as the MFMA lanes read them. One workgroup owns
+// 64 output channels x 16 input channels x all 9 taps over a chunk of pixels; the x tile of each
+// tap is staged with its shift applied and zeros outside the image. All limbs of g are staged in
+// the same pass (one accumulator set per limb). Chunks are combined with int64 atomics (integer
+// addition commutes, so the result does not depend on their order). A chunk has at most 2^17
+// pixels, so a limb's int32 accumulator cannot overflow (|x d| <= 128 * 128).
+// =============================================================================================
+struct DwArgs {
+    int n, h, w, ci, co;
+    const int32_t *g;            // NHWC [P][co]
+    const uint32_t *gmax;        // max|g|
+    const int8_t *x;             // NHWC [P][ci]
+    int64_t *dw;                 // [co][9][ci], zeroed before the launch
+    int kc;                      // pixels per chunk (multiple of 64, <= 2^17)
+    uint32_t *flags;
+};
+
+// 4x4 byte transpose: in a[i] byte j -> out[j] byte i.
+__device__ inline void transpose4x4(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3,
+                                    uint32_t &o0, uint32_t &o1, uint32_t &o2, uint32_t &o3)
+{
+    const uint32_t t0 = __builtin_amdgcn_perm(a1, a0, 0x05010400u);   // a0.b0 a1.b0 a0.b1 a1.b1
+    const uint32_t t1 = __builtin_amdgcn_perm(a1, a0, 0x07030602u);   // a0.b2 a1.b2 a0.b3 a1.b3
+    const uint32_t t2 = __builtin_amdgcn_perm(a3, a2, 0x05010400u);   // a2.b0 a3.b0 a2.b1 a3.b1
+    const uint32_t t3 = __builtin_amdgcn_perm(a3, a2, 0x07030602u);   // a2.b2 a3.b2 a2.b3 a3.b3
+    o0 = __builtin_amdgcn_perm(t2, t0, 0x05040100u);                   // a0.b0 a1.b0 a2.b0 a3.b0
+    o1 = __builtin_amdgcn_perm(t2, t0, 0x07060302u);
+    o2 = __builtin_amdgcn_perm(t3, t1, 0x05040100u);
+    o3 = __builtin_amdgcn_perm(t3, t1, 0x07060302u);
+}
+
+constexpr int DW_BM = 64;          // output channels per workgroup (4 waves x 16)
+constexpr int DW_BC = 16;          // input channels per workgroup
+constexpr int DW_BK = 64;          // pixels per step
+constexpr int DW_LDS = 80;         // LDS row stride (64 + 16 pad)
+// largest chunk: 128 * 128 * DW_KC_MAX < 2^31, so a limb's int32 accumulator cannot overflow
+constexpr int DW_KC_MAX = 131008;
+
+__global__ __launch_bounds__(256) void k_conv_dw_mfma(DwArgs p)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t As[4][DW_BM][DW_LDS];
+    __shared__ __attribute__((aligned(16))) uint8_t Bs[9][DW_BC][DW_LDS];
+    __shared__ int pix_p[DW_BK];
+    __shared__ int pix_hw[DW_BK];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int LA = limbs_for(*p.gmax);
+    if (LA > 4) {
+        if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
+        return;
+    }
+    const int HW = p.h * p.w;
+    const int P = p.n * HW;
+    const int co0 = blockIdx.x * DW_BM, ci0 = blockIdx.y * DW_BC;
+    const int pb = blockIdx.z * p.kc;
+    const int pe = pb + p.kc < P ? pb + p.kc : P;
+
+    v4i acc[4][9];
+    for (int l = 0; l < 4; l++)
+        for (int t = 0; t < 9; t++) acc[l][t] = v4i{0, 0, 0, 0};
+
+    for (int k0 = pb; k0 < pe; k0 += DW_BK) {
+        __syncthreads();                                   // previous step done with LDS
+        if (tid < DW_BK) {
+            const int pp = k0 + tid;
+            const int rem = pp % HW;
+            pix_p[tid] = pp < pe ? pp : -1;
+            pix_hw[tid] = ((rem / p.w) << 16) | (rem % p.w);
+        }
+        __syncthreads();
+        // ---- A: g[p][co0 + 4cq .. +4] for 4 pixels -> all limbs, transposed to [co][pixel]
+        {
+            const int cq = tid & 15, pq = tid >> 4;        // 16 x 16 tasks = 256 threads
+            const int co = co0 + 4 * cq;
+            v4i q[4];
+            for (int i = 0; i < 4; i++) {
+                const int pp = pix_p[4 * pq + i];
+                q[i] = (pp >= 0 && co < p.co) ? *(const v4i *)(p.g + (int64_t)pp * p.co + co)
+                                              : v4i{0, 0, 0, 0};
+            }
+            for (int l = 0; l < 4; l++) {
+                if (l >= LA) break;
+                uint32_t d[4], o[4];
+                for (int i = 0; i < 4; i++) d[i] = limb4(q[i][0], q[i][1], q[i][2], q[i][3], l);
+                transpose4x4(d[0], d[1], d[2], d[3], o[0], o[1], o[2], o[3]);
+                for (int c = 0; c < 4; c++) *(uint32_t *)&As[l][4 * cq + c][4 * pq] = o[c];
+            }
+        }
+        // ---- B: for each tap, x[p + shift][ci0 + 4cq .. +4] for 4 pixels, transposed
+        for (int task = tid; task < 9 * 64; task += 256) {
+            const int t = task >> 6, rem = task & 63;
+            const int pq = rem >> 2, cq = rem & 3;
+            const int dr = t / 3 - 1, ds = t % 3 - 1;
+            const int ci = ci0 + 4 * cq;
+            uint32_t d[4];
+            for (int i = 0; i < 4; i++) {
+                const int pp = pix_p[4 * pq + i];
+                const int hw = pix_hw[4 * pq + i];
+                const int hh = (hw >> 16) + dr, ww = (hw & 0xFFFF) + ds;
+                const bool ok = pp >= 0 && ci < p.ci && hh >= 0 && hh < p.h && ww >= 0 && ww < p.w;
+                d[i] = ok ? *(const uint32_t *)(p.x + (int64_t)(pp + dr * p.w + ds) * p.ci + ci) : 0u;
+            }
+            uint32_t o[4];
+            transpose4x4(d[0], d[1], d[2], d[3], o[0], o[1], o[2], o[3]);
+            for (int c = 0; c < 4; c++) *(uint32_t *)&Bs[t][4 * cq + c][4 * pq] = o[c];
+        }
+        __syncthreads();
+        v4i bf[9];
+        for (int t = 0; t < 9; t++) bf[t] = *(const v4i *)&Bs[t][lane & 15][(lane >> 4) * 16];
+        for (int l = 0; l < 4; l++) {
+            if (l >= LA) break;
+            const v4i af = *(const v4i *)&As[l][wave * 16 + (lane & 15)][(lane >> 4) * 16];
+            for (int t = 0; t < 9; t++)
+                acc[l][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, bf[t], acc[l][t], 0, 0, 0);
+        }
+    }
+    // ---- combine limbs, add this chunk's partial tile into dW
+    for (int t = 0; t < 9; t++)
+        for (int i = 0; i < 4; i++) {
+            const int co = co0 + wave * 16 + (lane >> 4) * 4 + i;
+            const int ci = ci0 + (lane & 15);
+            if (co >= p.co || ci >= p.ci) continue;
+            int64_t v = 0;
+            for (int l = 0; l < 4; l++) v += (int64_t)acc[l][t][i] << (8 * l);
+            if (v != 0)
+                atomicAdd((unsigned long long *)&p.dw[((int64_t)co * 9 + t) * p.ci + ci],
+                          (unsigned long long)v);
+        }
+}
+
+bool mfma_conv_dw_ok(const ConvShape &sh)
+{
+    return sh.c % 4 == 0 && sh.co % 4 == 0 && (int64_t)sh.n * sh.h * sh.w < ((int64_t)1 << 31) &&
+           sh.w < 65536 && sh.h < 65536;
+}
+
+void launch_conv_dw_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g,
+                         const uint32_t *gmax, const int8_t *x, int64_t *dw, uint32_t *flags)
+{
+    launch_fill_i64(s, dw, (int64_t)sh.co * 9 * sh.c);
+    DwArgs a{};
+    a.n = sh.n; a.h = sh.h; a.w = sh.w; a.ci = sh.c; a.co = sh.co;
+    a.g = g; a.gmax = gmax; a.x = x; a.dw = dw; a.flags = flags;
+    const int64_t P = (int64_t)sh.n * sh.h * sh.w;
+    const int tiles = ((sh.co + DW_BM - 1) / DW_BM) * ((sh.c + DW_BC - 1) / DW_BC);
+    // about 512 workgroups in total; chunks of whole 64-pixel steps, at most 2^17 pixels
+    int64_t nz = (512 + tiles - 1) / tiles;
+    const int64_t steps = (P + DW_BK - 1) / DW_BK;
+    if (nz > steps) nz = steps;
+    int64_t kc = ((steps + nz - 1) / nz) * DW_BK;
+    if (kc > DW_KC_MAX) kc = DW_KC_MAX;
+    nz = (P + kc - 1) / kc;
+    a.kc = (int)kc;
+    dim3 grid((unsigned)((sh.co + DW_BM - 1) / DW_BM), (unsigned)((sh.c + DW_BC - 1) / DW_BC),
+              (unsigned)nz);
+    hipLaunchKernelGGL(k_conv_dw_mfma, grid, dim3(256), 0, s, a);
 }
 
 }  // namespace nitro

@@ -238,7 +238,7 @@ __device__ inline void wave_abs_max_to(uint32_t *gmax, int64_t v)
         uint32_t o = __shfl_xor(m, off, 64);
         m = o > m ? o : m;
     }
-    if ((threadIdx.x & 63) == 0 && m) atomicMax(gmax, m);
+    if ((threadIdx.x & 63) == 0) slot_max(gmax, m);
 }
 
 // Gradient at the block output -> gradient at the last layer's z (un-pool + ReLU').

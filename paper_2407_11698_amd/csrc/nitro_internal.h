@@ -99,6 +99,14 @@ __device__ inline bool fits_i32(int64_t v) { return v >= INT32_MIN && v <= INT32
 
 __device__ inline void raise_flag(uint32_t *flags, uint32_t f) { atomicOr(flags, f); }
 
+// Running maximum in a device slot. The plain read first skips the atomic whenever the slot
+// already holds a value at least as large (a stale read only costs an extra atomic).
+__device__ inline void slot_max(uint32_t *slot, uint32_t m)
+{
+    if (m && m > __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+        atomicMax(slot, m);
+}
+
 // ------------------------------------------------------------------------------------------
 // Kernel launchers (each enqueues on `s`; shapes are validated by the caller).
 // ------------------------------------------------------------------------------------------
@@ -148,6 +156,10 @@ void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, i
 void launch_conv_fwd_mfma(hipStream_t s, const ConvShape &sh, const int8_t *x, const int8_t *wf,
                           const uint32_t *wmax, const Div &sf, const Relu &rp, bool pool,
                           int8_t *out, uint8_t *code, uint32_t *flags);
+bool mfma_conv_dw_ok(const ConvShape &sh);
+// dW (int64, zeroed here) from g int32 NHWC (max|g| in *gmax) and x int8 NHWC.
+void launch_conv_dw_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g,
+                         const uint32_t *gmax, const int8_t *x, int64_t *dw, uint32_t *flags);
 void launch_conv_dx_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g, const uint32_t *gmax_in,
                          const int8_t *wt, const uint32_t *wmax, const uint8_t *prev_code,
                          const Relu &rp, int32_t *gout, int64_t *out64, uint32_t *gmax_out,
