@@ -89,6 +89,10 @@ struct BlockGeom {
     size_t wf[NITRO_MAX_LAYERS];   // conv: 4 int8 limb planes of W, [co][9 ci]
     size_t wt[NITRO_MAX_LAYERS];   // conv: 4 int8 limb planes of W, [ci][9 co]
     size_t slots;                  // uint32 [8]: max|W_j| (0..3), max|g_j| (4..7)
+    size_t gt;                     // weight-gradient scratch: pixel-contiguous limb planes of g
+    size_t part;                   // weight-gradient scratch: split-K partial sums (int64)
+    bool lr_mfma;                  // learning layer on the MFMA path
+    size_t lwf, lwt, lft, lpart, lepad, let;   // its scratch
     size_t yhat, e, delta, g0, g1;
     size_t total;
 };
@@ -123,10 +127,12 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
         L.sf = 256 * (int64_t)(conv ? 9 * ly.c_in : ly.c_in);
         c = ly.c_out;
     }
-    // keep every flattened index far from overflow
-    for (int j = 0; j < g->J; j++)
-        if ((int64_t)d->n * (g->L[j].out_elems > g->L[j].in_elems ? g->L[j].out_elems : g->L[j].in_elems) > ((int64_t)1 << 40))
-            return NITRO_EUNSUPPORTED;
+    // the elementwise kernels index activations and weights with 32-bit arithmetic
+    for (int j = 0; j < g->J; j++) {
+        const int64_t big = g->L[j].out_elems > g->L[j].in_elems ? g->L[j].out_elems : g->L[j].in_elems;
+        if ((int64_t)d->n * big >= ((int64_t)1 << 31)) return NITRO_EUNSUPPORTED;
+        if (9 * (int64_t)g->L[j].sh.c * g->L[j].sh.co >= ((int64_t)1 << 31)) return NITRO_EUNSUPPORTED;
+    }
     g->d = d->maxpool ? (int64_t)(d->h / 2) * (d->w / 2) * c : hw * c;
     g->out_elems = (int64_t)d->n * g->d;
     // state buffer layout
@@ -146,7 +152,34 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
         g->wf[j] = off; off = align256(off + (size_t)(4 * nw));
         g->wt[j] = off; off = align256(off + (size_t)(4 * nw));
     }
-    g->slots = off; off = align256(off + 8 * 4);
+    g->slots = off; off = align256(off + 16 * 4);
+    g->lr_mfma = d->n_classes > 0 && mfma_learning_ok(d->n, g->d, d->n_classes);
+    {
+        LearningScratch ls{};
+        if (g->lr_mfma) ls = learning_scratch(d->n, g->d, d->n_classes);
+        g->lwf = off;   off = align256(off + (size_t)ls.wf_bytes);
+        g->lwt = off;   off = align256(off + (size_t)ls.wt_bytes);
+        g->lft = off;   off = align256(off + (size_t)ls.ft_bytes);
+        g->lpart = off; off = align256(off + (size_t)ls.part_bytes);
+        g->lepad = off; off = align256(off + (size_t)ls.epad_bytes);
+        g->let = off;   off = align256(off + (size_t)ls.et_bytes);
+    }
+    int64_t gtb = 0;
+    for (int j = 0; j < g->J; j++)
+        if (conv && mfma_conv_dw_ok(g->L[j].sh)) {
+            const int64_t b = 4 * (int64_t)g->L[j].sh.co * dw_plane_stride(g->L[j].sh);
+            if (b > gtb) gtb = b;
+        }
+    g->gt = off; off = align256(off + (size_t)gtb);
+    int64_t parts = 0;
+    for (int j = 0; j < g->J; j++) {
+        if (!conv) continue;
+        int64_t c = 0;
+        if (mfma_conv_dw_ok(g->L[j].sh)) c = dw_partial_count(g->L[j].sh);
+        else if (smallc_dw_ok(g->L[j].sh)) c = smallc_dw_partial_count(g->L[j].sh);
+        if (c > parts) parts = c;
+    }
+    g->part = off; off = align256(off + (size_t)parts * 8);
     const int64_t G = d->n_classes;
     g->yhat = off;  off = align256(off + (size_t)(d->n * G) * 4);
     g->e = off;     off = align256(off + (size_t)(d->n * G) * 4);
@@ -191,6 +224,8 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
             if (mfma_conv_fwd_ok(L.sh, pool))
                 launch_conv_fwd_mfma(s, L.sh, cur, (const int8_t *)at(state, g.wf[j]), &slots[j],
                                      sf, rp, pool, out, code, ctx->flags);
+            else if (smallc_fwd_ok(L.sh))
+                launch_conv_fwd_smallc(s, L.sh, cur, p->w[j], sf, rp, pool, out, code);
             else
                 launch_conv_fwd(s, L.sh, cur, p->w[j], sf, rp, pool, out, code);
         } else {
@@ -211,30 +246,50 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
     const int n = desc->n;
     const int G = desc->n_classes;
     const int32_t *delta = delta_out;
+    int32_t *gb[2] = {(int32_t *)at(state, g.g0), (int32_t *)at(state, g.g1)};
+    const int J = g.J;
+    const LayerGeom &LJ = g.L[J - 1];
+    uint32_t *slots = (uint32_t *)at(state, g.slots);
+    // max|g_j| (4..7), max|W_lr| (8), max|e| (9) are produced by this call
+    if (hipMemsetAsync(slots + 4, 0, 6 * 4, s) != hipSuccess) return NITRO_EHIP;
+    bool have_g = false;
     if (G > 0) {
         int32_t *yhat = (int32_t *)at(state, g.yhat);
         int32_t *e = (int32_t *)at(state, g.e);
-        int32_t *dl = (int32_t *)at(state, g.delta);
         const Div sf = make_div(256 * g.d, desc->round);
-        launch_linear_fwd_loss(s, n, (int)g.d, G, a_out, p->w_lr, sf, labels, yhat, e, ctx->flags);
-        launch_linear_dw(s, n, (int)g.d, G, e, a_out, gr->dw_lr);
-        launch_linear_dx(s, n, (int)g.d, G, e, p->w_lr, nullptr, rp, dl, nullptr, ctx->flags);
+        if (g.lr_mfma) {
+            LearningBuffers lb;
+            lb.wf = (int8_t *)at(state, g.lwf);
+            lb.wt = (int8_t *)at(state, g.lwt);
+            lb.ft = (int8_t *)at(state, g.lft);
+            lb.part = (int64_t *)at(state, g.lpart);
+            lb.epad = (int32_t *)at(state, g.lepad);
+            lb.et = (int32_t *)at(state, g.let);
+            lb.wmax = &slots[8];
+            lb.emax = &slots[9];
+            lb.gmax = &slots[4 + J - 1];
+            launch_learning_mfma(s, n, g.d, G, a_out, p->w_lr, sf, labels, lb,
+                                 at(state, g.code[J - 1]), rp, LJ.sh.h, LJ.sh.w, LJ.sh.co,
+                                 desc->maxpool != 0, gb[0], taps ? taps->delta : nullptr, yhat, e,
+                                 gr->dw_lr, ctx->flags);
+            have_g = true;
+        } else {
+            int32_t *dl = (int32_t *)at(state, g.delta);
+            launch_linear_fwd_loss(s, n, (int)g.d, G, a_out, p->w_lr, sf, labels, yhat, e, ctx->flags);
+            launch_linear_dw(s, n, (int)g.d, G, e, a_out, gr->dw_lr);
+            launch_linear_dx(s, n, (int)g.d, G, e, p->w_lr, nullptr, rp, dl, nullptr, ctx->flags);
+            if (taps && taps->delta)
+                (void)hipMemcpyAsync(taps->delta, dl, (size_t)g.out_elems * 4, hipMemcpyDeviceToDevice, s);
+            delta = dl;
+        }
         if (taps) {
             if (taps->yhat) (void)hipMemcpyAsync(taps->yhat, yhat, (size_t)n * G * 4, hipMemcpyDeviceToDevice, s);
             if (taps->e) (void)hipMemcpyAsync(taps->e, e, (size_t)n * G * 4, hipMemcpyDeviceToDevice, s);
-            if (taps->delta) (void)hipMemcpyAsync(taps->delta, dl, (size_t)g.out_elems * 4, hipMemcpyDeviceToDevice, s);
         }
-        delta = dl;
     }
-    int32_t *gb[2] = {(int32_t *)at(state, g.g0), (int32_t *)at(state, g.g1)};
-    const int J = g.J;
-    uint32_t *slots = (uint32_t *)at(state, g.slots);
-    if (hipMemsetAsync(slots + 4, 0, 4 * 4, s) != hipSuccess) return NITRO_EHIP;
-    {
-        const LayerGeom &L = g.L[J - 1];
-        launch_unpool_relu_bwd(s, n, L.sh.h, L.sh.w, L.sh.co, desc->maxpool != 0, delta,
+    if (!have_g)
+        launch_unpool_relu_bwd(s, n, LJ.sh.h, LJ.sh.w, LJ.sh.co, desc->maxpool != 0, delta,
                                at(state, g.code[J - 1]), rp, gb[0], &slots[4 + J - 1], ctx->flags);
-    }
     int cur = 0;
     for (int j = J - 1; j >= 0; j--) {
         const LayerGeom &L = g.L[j];
@@ -243,7 +298,10 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         if (L.conv) {
             TimedLaunch t(ctx, CLS_CONV_DW);
             if (mfma_conv_dw_ok(L.sh))
-                launch_conv_dw_mfma(s, L.sh, gj, &slots[4 + j], xin, gr->dw[j], ctx->flags);
+                launch_conv_dw_mfma(s, L.sh, gj, &slots[4 + j], xin, (int8_t *)at(state, g.gt),
+                                    (int64_t *)at(state, g.part), gr->dw[j], ctx->flags);
+            else if (smallc_dw_ok(L.sh))
+                launch_conv_dw_smallc(s, L.sh, gj, xin, (int64_t *)at(state, g.part), gr->dw[j]);
             else
                 launch_conv_dw(s, L.sh, gj, xin, gr->dw[j]);
         } else {

@@ -12,80 +12,54 @@
 //   input grad  dx[p][ci] = sum_{r,s,co} g[p - (r-1, s-1)][co] * W[co][r][s][ci]
 // The B operand is a packed limb plane [N][9*CK] (int8), K-contiguous, produced per call by
 // k_pack_conv_weights (forward: W itself; input gradient: W with its two channel axes swapped).
-#include "nitro_internal.h"
+#include <type_traits>
+
+#include "mfma_common.h"
 
 namespace nitro {
-
-typedef int v4i __attribute__((ext_vector_type(4)));
-
-__host__ __device__ inline int limbs_for(uint32_t m)
-{
-    return m <= 127u ? 1 : m <= 32639u ? 2 : m <= 8355711u ? 3 : m <= 2139062143u ? 4 : 5;
-}
-
-__device__ inline uint32_t abs_u32(int32_t v) { return v < 0 ? (uint32_t)(-(int64_t)v) : (uint32_t)v; }
-
-// Limb l of four int32 values, packed into one dword (value i in byte i). Digit l of
-// v + sum_{i<=l} 128*256^i is d_l + 128; xor 0x80 turns it back into the signed digit.
-__device__ inline uint32_t limb4(int32_t v0, int32_t v1, int32_t v2, int32_t v3, int l)
-{
-    const uint32_t bias = 0x80808080u >> (24 - 8 * l);
-    const int sh = 8 * l;
-    uint32_t t0 = (((uint32_t)v0 + bias) >> sh) & 0xFFu;
-    uint32_t t1 = (((uint32_t)v1 + bias) >> sh) & 0xFFu;
-    uint32_t t2 = (((uint32_t)v2 + bias) >> sh) & 0xFFu;
-    uint32_t t3 = (((uint32_t)v3 + bias) >> sh) & 0xFFu;
-    return (t0 | (t1 << 8) | (t2 << 16) | (t3 << 24)) ^ 0x80808080u;
-}
-
-__device__ inline int8_t limb1(int32_t v, int l)
-{
-    const uint32_t bias = 0x80808080u >> (24 - 8 * l);
-    return (int8_t)(((((uint32_t)v + bias) >> (8 * l)) & 0xFFu) ^ 0x80u);
-}
-
-__device__ inline uint32_t wave_max_u32(uint32_t v)
-{
-    for (int off = 32; off > 0; off >>= 1) {
-        uint32_t o = __shfl_xor(v, off, 64);
-        v = o > v ? o : v;
-    }
-    return v;
-}
 
 // ---------------------------------------------------------------------------------------------
 // Weight packing: W int32 KRSC [co][3][3][ci] -> 4 limb planes of [co][9 ci] (forward) and,
 // when wt != null, of [ci][9 co] with the same tap order (input gradient); max|W| -> *wmax.
-__global__ void k_pack_conv_weights(const int32_t *__restrict__ w, int co, int ci,
-                                    int8_t *__restrict__ wf, int8_t *__restrict__ wt,
-                                    uint32_t *wmax)
+// Two passes, each with coalesced stores: the forward planes in W's own order, the swapped
+// planes in their order (gathering W through the cache).
+__global__ void k_pack_conv_weights(const int32_t *__restrict__ w, uint32_t total,
+                                    int8_t *__restrict__ wf, uint32_t *wmax)
 {
-    const int64_t total = (int64_t)co * 9 * ci;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     uint32_t m = 0;
-    if (i < total) {
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
         const int32_t v = w[i];
-        m = abs_u32(v);
-        const int o = (int)(i / (9 * ci));
-        const int rem = (int)(i % (9 * ci));
-        const int rs = rem / ci, c = rem % ci;
-        const int64_t ti = (int64_t)c * 9 * co + (int64_t)rs * co + o;
-        for (int l = 0; l < 4; l++) {
-            const int8_t d = limb1(v, l);
-            wf[l * total + i] = d;
-            if (wt) wt[l * total + ti] = d;
-        }
+        const uint32_t a = abs_u32(v);
+        m = a > m ? a : m;
+#pragma unroll
+        for (int l = 0; l < 4; l++) wf[(int64_t)l * total + i] = limb1(v, l);
     }
-    m = wave_max_u32(m);
-    if ((threadIdx.x & 63) == 0) slot_max(wmax, m);
+    block_slot_max(wmax, m);
+}
+
+__global__ void k_pack_conv_weights_t(const int32_t *__restrict__ w, uint32_t co, uint32_t ci,
+                                      int8_t *__restrict__ wt)
+{
+    const uint32_t total = co * 9 * ci;
+    const uint32_t ti = blockIdx.x * blockDim.x + threadIdx.x;   // = (c * 9 + rs) * co + o
+    if (ti >= total) return;
+    const uint32_t o = ti % co, crs = ti / co;
+    const uint32_t rs = crs % 9, c = crs / 9;
+    const int32_t v = w[(o * 9 + rs) * ci + c];
+#pragma unroll
+    for (int l = 0; l < 4; l++) wt[(int64_t)l * total + ti] = limb1(v, l);
 }
 
 void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,
                               int8_t *wt, uint32_t *wmax)
 {
-    const int64_t total = (int64_t)co * 9 * ci;
-    hipLaunchKernelGGL(k_pack_conv_weights, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
-                       s, w, co, ci, wf, wt, wmax);
+    const uint32_t total = (uint32_t)co * 9 * (uint32_t)ci;
+    const dim3 grid((total + 255) / 256);
+    hipLaunchKernelGGL(k_pack_conv_weights, dim3(grid_stride_blocks(total)), dim3(256), 0, s, w,
+                       total, wf, wmax);
+    if (wt)
+        hipLaunchKernelGGL(k_pack_conv_weights_t, grid, dim3(256), 0, s, w, (uint32_t)co,
+                           (uint32_t)ci, wt);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -117,6 +91,8 @@ constexpr int IG_BK = 64;            // K per step = one MFMA K
 constexpr int IG_LDS_STRIDE = 80;    // bytes per LDS row (64 + 16 pad)
 
 // BM x BN tile per 256-thread workgroup; 4 waves in a 2 x 2 grid, each (BM/2) x (BN/2).
+// K steps are software-pipelined: the global loads of step k+1 are issued before the MFMAs of
+// step k, and LDS is double-buffered so each step needs one barrier.
 template <int MODE, int BM, int BN>
 __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
 {
@@ -125,12 +101,11 @@ __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
     constexpr int A_CHUNKS = BM * 4 / 256;       // 16-byte chunks of A per thread per step
     constexpr int B_CHUNKS = BN * 4 / 256;
     static_assert(A_CHUNKS >= 1 && B_CHUNKS >= 1, "tile too small");
-    constexpr int SMEM_AB = (BM + BN) * IG_LDS_STRIDE;
+    constexpr int STAGE = (BM + BN) * IG_LDS_STRIDE;
+    constexpr int SMEM_AB = 2 * STAGE;
     constexpr int SMEM_EPI = 2 * BM * BN;
     constexpr int SMEM = SMEM_AB > SMEM_EPI ? SMEM_AB : SMEM_EPI;
     __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
-    uint8_t *As = smem;
-    uint8_t *Bs = smem + BM * IG_LDS_STRIDE;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -151,17 +126,22 @@ __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
 
     // rows this thread stages: row = tid/4 + 64 i, chunk kc = tid % 4 (fixed over K)
     const int kc = tid & 3;
-    int a_n[A_CHUNKS], a_h[A_CHUNKS], a_w[A_CHUNKS];
-    bool a_ok[A_CHUNKS];
+    int a_h[A_CHUNKS], a_w[A_CHUNKS];
+    int64_t a_pix[A_CHUNKS];                      // flattened pixel index of the output row
     for (int i = 0; i < A_CHUNKS; i++) {
         const int64_t m = m0 + (tid >> 2) + 64 * i;
-        a_ok[i] = m < M;
-        const int64_t mm = a_ok[i] ? m : 0;
-        a_n[i] = (int)(mm / HW);
+        const bool ok = m < M;
+        const int64_t mm = ok ? m : 0;
         const int rem = (int)(mm % HW);
-        a_h[i] = rem / p.w;
+        a_h[i] = ok ? rem / p.w : -100000;        // out-of-range rows never pass the bound test
         a_w[i] = rem % p.w;
+        a_pix[i] = mm;
     }
+    const int sgn = MODE == IG_FWD ? 1 : -1;
+
+    typedef typename std::conditional<MODE == IG_FWD, v4i[1], v4i[4]>::type ARaw;
+    ARaw ar[A_CHUNKS];
+    v4i br[B_CHUNKS];
 
     int64_t acc64[TM][TN][4];
     for (int i = 0; i < TM; i++)
@@ -171,46 +151,63 @@ __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
     const int64_t plane = (int64_t)p.no * K;
     for (int la = 0; la < LA; la++) {
         for (int lb = 0; lb < LB; lb++) {
-            v4i acc[TM][TN];
-            for (int i = 0; i < TM; i++)
-                for (int j = 0; j < TN; j++) acc[i][j] = v4i{0, 0, 0, 0};
             const int8_t *bpl = p.b + lb * plane;
-            for (int ks = 0; ks < ksteps; ks++) {
+            // position of this thread's 16-value chunk in K: tap and channel, advanced by 64 a step
+            int ktap = 0, kci = kc * 16;
+            while (kci >= p.ck) { kci -= p.ck; ktap++; }
+            auto load = [&](int ks) {
                 const int k = ks * IG_BK + kc * 16;
                 const bool kin = k < K;
-                const int tap = kin ? k / p.ck : 0;
-                const int ci = kin ? k - tap * p.ck : 0;
-                const int dr = tap / 3 - 1, ds = tap % 3 - 1;
-                // ---- stage A
+                const int dr = sgn * (ktap / 3 - 1), ds = sgn * (ktap % 3 - 1);
                 for (int i = 0; i < A_CHUNKS; i++) {
-                    int hh, ww;
-                    if (MODE == IG_FWD) { hh = a_h[i] + dr; ww = a_w[i] + ds; }
-                    else { hh = a_h[i] - dr; ww = a_w[i] - ds; }
-                    const bool ok = kin && a_ok[i] && hh >= 0 && hh < p.h && ww >= 0 && ww < p.w;
-                    v4i v = {0, 0, 0, 0};
-                    if (ok) {
-                        const int64_t pix = ((int64_t)a_n[i] * p.h + hh) * p.w + ww;
-                        if (MODE == IG_FWD) {
-                            v = *(const v4i *)((const int8_t *)p.a + pix * p.ck + ci);
-                        } else {
-                            const v4i *src = (const v4i *)((const int32_t *)p.a + pix * p.ck + ci);
-                            v4i q0 = src[0], q1 = src[1], q2 = src[2], q3 = src[3];
-                            v[0] = (int)limb4(q0[0], q0[1], q0[2], q0[3], la);
-                            v[1] = (int)limb4(q1[0], q1[1], q1[2], q1[3], la);
-                            v[2] = (int)limb4(q2[0], q2[1], q2[2], q2[3], la);
-                            v[3] = (int)limb4(q3[0], q3[1], q3[2], q3[3], la);
-                        }
+                    const int hh = a_h[i] + dr, ww = a_w[i] + ds;
+                    const bool ok = kin && hh >= 0 && hh < p.h && ww >= 0 && ww < p.w;
+                    const int64_t pix = a_pix[i] + (int64_t)dr * p.w + ds;
+                    if (MODE == IG_FWD) {
+                        ar[i][0] = ok ? *(const v4i *)((const int8_t *)p.a + pix * p.ck + kci)
+                                      : v4i{0, 0, 0, 0};
+                    } else {
+                        const v4i *src = (const v4i *)((const int32_t *)p.a + pix * p.ck + kci);
+                        for (int u = 0; u < 4; u++) ar[i][u] = ok ? src[u] : v4i{0, 0, 0, 0};
+                    }
+                }
+                for (int i = 0; i < B_CHUNKS; i++) {
+                    const int nn = n0 + (tid >> 2) + 64 * i;
+                    br[i] = (kin && nn < p.no) ? *(const v4i *)(bpl + (int64_t)nn * K + k)
+                                               : v4i{0, 0, 0, 0};
+                }
+                kci += IG_BK;
+                while (kci >= p.ck) { kci -= p.ck; ktap++; }
+            };
+            auto store = [&](int buf) {
+                uint8_t *As = smem + buf * STAGE;
+                uint8_t *Bs = As + BM * IG_LDS_STRIDE;
+                for (int i = 0; i < A_CHUNKS; i++) {
+                    v4i v;
+                    if (MODE == IG_FWD) {
+                        v = ar[i][0];
+                    } else {
+                        for (int u = 0; u < 4; u++)
+                            v[u] = (int)limb4(ar[i][u][0], ar[i][u][1], ar[i][u][2], ar[i][u][3], la);
                     }
                     *(v4i *)(As + ((tid >> 2) + 64 * i) * IG_LDS_STRIDE + kc * 16) = v;
                 }
-                // ---- stage B (packed limb plane lb)
-                for (int i = 0; i < B_CHUNKS; i++) {
-                    const int nn = n0 + (tid >> 2) + 64 * i;
-                    v4i v = {0, 0, 0, 0};
-                    if (kin && nn < p.no) v = *(const v4i *)(bpl + (int64_t)nn * K + k);
-                    *(v4i *)(Bs + ((tid >> 2) + 64 * i) * IG_LDS_STRIDE + kc * 16) = v;
-                }
-                __syncthreads();
+                for (int i = 0; i < B_CHUNKS; i++)
+                    *(v4i *)(Bs + ((tid >> 2) + 64 * i) * IG_LDS_STRIDE + kc * 16) = br[i];
+            };
+
+            v4i acc[TM][TN];
+            for (int i = 0; i < TM; i++)
+                for (int j = 0; j < TN; j++) acc[i][j] = v4i{0, 0, 0, 0};
+            load(0);
+            store(0);
+            __syncthreads();
+            for (int ks = 0; ks < ksteps; ks++) {
+                const int cur = ks & 1;
+                const bool more = ks + 1 < ksteps;
+                if (more) load(ks + 1);
+                const uint8_t *As = smem + cur * STAGE;
+                const uint8_t *Bs = As + BM * IG_LDS_STRIDE;
                 v4i af[TM], bf[TN];
                 for (int i = 0; i < TM; i++)
                     af[i] = *(const v4i *)(As + (wm * WM + i * 16 + (lane & 15)) * IG_LDS_STRIDE + (lane >> 4) * 16);
@@ -219,6 +216,7 @@ __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
                 for (int i = 0; i < TM; i++)
                     for (int j = 0; j < TN; j++)
                         acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
+                if (more) store(cur ^ 1);
                 __syncthreads();
             }
             const int sh = 8 * (la + lb);
@@ -233,8 +231,11 @@ __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
         // NITRO-Scaling + NITRO-ReLU per element into LDS, then coalesced (and pooled) stores.
         uint8_t *Os = smem;             // [BM][BN] int8 activations
         uint8_t *Rs = smem + BM * BN;   // [BM][BN] region codes
+#pragma unroll
         for (int i = 0; i < TM; i++)
+#pragma unroll
             for (int j = 0; j < TN; j++)
+#pragma unroll
                 for (int t = 0; t < 4; t++) {
                     const int row = wm * WM + i * 16 + (lane >> 4) * 4 + t;
                     const int col = wn * WN + j * 16 + (lane & 15);
@@ -272,12 +273,13 @@ __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
                 const int q = 2 * wr * W + 2 * wc;            // top-left local pixel
                 const int64_t m = m0 + q;
                 if (m >= M || n0 + col >= p.no) continue;
-                const int idx[4] = {q, q + 1, q + W, q + W + 1};
                 int best = -1000, arg = 0;
                 uint8_t breg = 0;
+#pragma unroll
                 for (int t = 0; t < 4; t++) {
-                    const int v = (int)(int8_t)Os[idx[t] * BN + col];
-                    if (v > best) { best = v; arg = t; breg = Rs[idx[t] * BN + col]; }
+                    const int at = q + (t >> 1) * W + (t & 1);
+                    const int v = (int)(int8_t)Os[at * BN + col];
+                    if (v > best) { best = v; arg = t; breg = Rs[at * BN + col]; }
                 }
                 const int64_t grow = m / W;                   // global image row (all images)
                 const int64_t pp = (grow / 2) * W2 + (m % W) / 2;
@@ -289,8 +291,11 @@ __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
     } else {
         uint32_t mx = 0;
         bool bad = false;
+#pragma unroll
         for (int i = 0; i < TM; i++)
+#pragma unroll
             for (int j = 0; j < TN; j++)
+#pragma unroll
                 for (int t = 0; t < 4; t++) {
                     const int64_t m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + t;
                     const int col = n0 + wn * WN + j * 16 + (lane & 15);
@@ -310,26 +315,18 @@ __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
                     mx = ag > mx ? ag : mx;
                 }
         if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
-        if (p.gmax) {
-            mx = wave_max_u32(mx);
-            if (lane == 0) slot_max(p.gmax, mx);
-        }
+        if (p.gmax) block_slot_max(p.gmax, mx);
     }
 }
 
-// Tile choice: BN covers the GEMM's N when it is small (64), else 128.
+// One tile shape: 128 output pixels x 64 GEMM columns per workgroup.
 template <int MODE>
 static void launch_igemm(hipStream_t s, const IgemmArgs &a)
 {
     const int64_t M = (int64_t)a.n * a.h * a.w;
-    constexpr int BM = 128;
-    if (a.no <= 64) {
-        dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.no + 63) / 64));
-        hipLaunchKernelGGL((k_igemm_conv<MODE, BM, 64>), grid, dim3(256), 0, s, a);
-    } else {
-        dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.no + 127) / 128));
-        hipLaunchKernelGGL((k_igemm_conv<MODE, BM, 128>), grid, dim3(256), 0, s, a);
-    }
+    constexpr int BM = 128, BN = 64;
+    dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.no + BN - 1) / BN));
+    hipLaunchKernelGGL((k_igemm_conv<MODE, BM, BN>), grid, dim3(256), 0, s, a);
 }
 
 // K = 9 * ck <= 9 * 8192 keeps 128 * 128 * K below 2^31 (one limb pass in int32).
@@ -387,28 +384,54 @@ void launch_conv_dx_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g, c
 // =============================================================================================
 struct DwArgs {
     int n, h, w, ci, co;
-    const int32_t *g;            // NHWC [P][co]
+    const int8_t *gt;            // limb planes of g, [4][co][pstride] (pixel-contiguous rows)
+    int64_t pstride;             // row length of a plane (>= P, multiple of 64)
     const uint32_t *gmax;        // max|g|
     const int8_t *x;             // NHWC [P][ci]
-    int64_t *dw;                 // [co][9][ci], zeroed before the launch
-    int kc;                      // pixels per chunk (multiple of 64, <= 2^17)
+    int64_t *part;               // [chunks][co][9][ci]: this chunk's partial sums
+    int kc;                      // pixels per chunk (multiple of 64)
     uint32_t *flags;
 };
 
-// 4x4 byte transpose: in a[i] byte j -> out[j] byte i.
-__device__ inline void transpose4x4(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3,
-                                    uint32_t &o0, uint32_t &o1, uint32_t &o2, uint32_t &o3)
+// ---------------------------------------------------------------------------------------------
+// g int32 NHWC [P][C] -> limb planes [l][C][pstride] for l < limbs(max|g|), rows pixel-contiguous
+// (pixels P..pstride-1 are written as zeros). One thread: 4 pixels x 4 channels.
+__global__ __launch_bounds__(256) void k_grad_limb_planes(const int32_t *__restrict__ g, int P,
+                                                          int C, int64_t pstride,
+                                                          const uint32_t *gmax,
+                                                          int8_t *__restrict__ gt)
 {
-    const uint32_t t0 = __builtin_amdgcn_perm(a1, a0, 0x05010400u);   // a0.b0 a1.b0 a0.b1 a1.b1
-    const uint32_t t1 = __builtin_amdgcn_perm(a1, a0, 0x07030602u);   // a0.b2 a1.b2 a0.b3 a1.b3
-    const uint32_t t2 = __builtin_amdgcn_perm(a3, a2, 0x05010400u);   // a2.b0 a3.b0 a2.b1 a3.b1
-    const uint32_t t3 = __builtin_amdgcn_perm(a3, a2, 0x07030602u);   // a2.b2 a3.b2 a2.b3 a3.b3
-    o0 = __builtin_amdgcn_perm(t2, t0, 0x05040100u);                   // a0.b0 a1.b0 a2.b0 a3.b0
-    o1 = __builtin_amdgcn_perm(t2, t0, 0x07060302u);
-    o2 = __builtin_amdgcn_perm(t3, t1, 0x05040100u);
-    o3 = __builtin_amdgcn_perm(t3, t1, 0x07060302u);
+    const int LA = limbs_for(*gmax);
+    const int cq4 = (C + 3) / 4;
+    const int64_t pq4 = pstride / 4;
+    const int64_t task = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t ntask = pq4 * cq4;
+    if (task >= ntask || LA > 4) return;
+    // pixel quads vary fastest: the plane stores of a wave are contiguous
+    const int cq = (int)(task / pq4);
+    const int64_t p0 = (task % pq4) * 4;
+    const int c0 = cq * 4;
+    int32_t v[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+            v[i][j] = (p0 + i < P && c0 + j < C) ? g[(p0 + i) * C + c0 + j] : 0;
+#pragma unroll
+    for (int l = 0; l < 4; l++) {
+        if (l < LA) {
+            uint32_t d[4], o[4];
+#pragma unroll
+            for (int i = 0; i < 4; i++) d[i] = limb4(v[i][0], v[i][1], v[i][2], v[i][3], l);
+            transpose4x4(d[0], d[1], d[2], d[3], o[0], o[1], o[2], o[3]);
+#pragma unroll
+            for (int j = 0; j < 4; j++)
+                if (c0 + j < C) *(uint32_t *)(gt + ((int64_t)l * C + c0 + j) * pstride + p0) = o[j];
+        }
+    }
 }
 
+// ---------------------------------------------------------------------------------------------
 constexpr int DW_BM = 64;          // output channels per workgroup (4 waves x 16)
 constexpr int DW_BC = 16;          // input channels per workgroup
 constexpr int DW_BK = 64;          // pixels per step
@@ -416,12 +439,13 @@ constexpr int DW_LDS = 80;         // LDS row stride (64 + 16 pad)
 // largest chunk: 128 * 128 * DW_KC_MAX < 2^31, so a limb's int32 accumulator cannot overflow
 constexpr int DW_KC_MAX = 131008;
 
+// One workgroup: 64 output channels x 16 input channels x 9 taps over a chunk of pixels.
+// A fragments (g limbs) come straight from the pixel-contiguous planes: each wave owns 16
+// output channels. The x tile of each tap is staged in LDS (double-buffered, next step's global
+// loads issued before this step's MFMAs).
 __global__ __launch_bounds__(256) void k_conv_dw_mfma(DwArgs p)
 {
-    __shared__ __attribute__((aligned(16))) uint8_t As[4][DW_BM][DW_LDS];
-    __shared__ __attribute__((aligned(16))) uint8_t Bs[9][DW_BC][DW_LDS];
-    __shared__ int pix_p[DW_BK];
-    __shared__ int pix_hw[DW_BK];
+    __shared__ __attribute__((aligned(16))) uint8_t Bs[2][9][DW_BC][DW_LDS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int LA = limbs_for(*p.gmax);
@@ -434,77 +458,112 @@ __global__ __launch_bounds__(256) void k_conv_dw_mfma(DwArgs p)
     const int co0 = blockIdx.x * DW_BM, ci0 = blockIdx.y * DW_BC;
     const int pb = blockIdx.z * p.kc;
     const int pe = pb + p.kc < P ? pb + p.kc : P;
+    const int nsteps = (pe - pb + DW_BK - 1) / DW_BK;
+
+    // A: this lane's row (output channel) and 16-pixel group within a step
+    const int arow = co0 + wave * 16 + (lane & 15);
+    const bool arow_ok = arow < p.co;
+    const int8_t *abase = p.gt + (int64_t)(arow_ok ? arow : 0) * p.pstride + pb + (lane >> 4) * 16;
+    const int64_t aplane = (int64_t)p.co * p.pstride;
+
+    // B staging: tasks (tap t = wave + 4 i, pixel quad pq, channel quad cq); pq, cq fixed
+    const int pq = (tid & 63) >> 2, cq = tid & 3;
+    const int ci = ci0 + 4 * cq;
+    const bool ci_ok = ci < p.ci;
+    // coordinates of this thread's 4 pixels in the current step (tracked incrementally)
+    int ph[4], pw[4], pidx[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const int pp = pb + 4 * pq + i;
+        const int rem = pp % HW;
+        pidx[i] = pp;
+        ph[i] = rem / p.w;
+        pw[i] = rem % p.w;
+    }
 
     v4i acc[4][9];
+#pragma unroll
     for (int l = 0; l < 4; l++)
+#pragma unroll
         for (int t = 0; t < 9; t++) acc[l][t] = v4i{0, 0, 0, 0};
 
-    for (int k0 = pb; k0 < pe; k0 += DW_BK) {
-        __syncthreads();                                   // previous step done with LDS
-        if (tid < DW_BK) {
-            const int pp = k0 + tid;
-            const int rem = pp % HW;
-            pix_p[tid] = pp < pe ? pp : -1;
-            pix_hw[tid] = ((rem / p.w) << 16) | (rem % p.w);
-        }
-        __syncthreads();
-        // ---- A: g[p][co0 + 4cq .. +4] for 4 pixels -> all limbs, transposed to [co][pixel]
-        {
-            const int cq = tid & 15, pq = tid >> 4;        // 16 x 16 tasks = 256 threads
-            const int co = co0 + 4 * cq;
-            v4i q[4];
-            for (int i = 0; i < 4; i++) {
-                const int pp = pix_p[4 * pq + i];
-                q[i] = (pp >= 0 && co < p.co) ? *(const v4i *)(p.g + (int64_t)pp * p.co + co)
+    v4i af[2][4];
+    uint32_t braw[3][4];
+    auto load = [&](int ks, int slot) {
+        const int k0 = ks * DW_BK;
+#pragma unroll
+        for (int l = 0; l < 4; l++)
+            af[slot][l] = (l < LA && arow_ok) ? *(const v4i *)(abase + l * aplane + k0)
                                               : v4i{0, 0, 0, 0};
-            }
-            for (int l = 0; l < 4; l++) {
-                if (l >= LA) break;
-                uint32_t d[4], o[4];
-                for (int i = 0; i < 4; i++) d[i] = limb4(q[i][0], q[i][1], q[i][2], q[i][3], l);
-                transpose4x4(d[0], d[1], d[2], d[3], o[0], o[1], o[2], o[3]);
-                for (int c = 0; c < 4; c++) *(uint32_t *)&As[l][4 * cq + c][4 * pq] = o[c];
-            }
-        }
-        // ---- B: for each tap, x[p + shift][ci0 + 4cq .. +4] for 4 pixels, transposed
-        for (int task = tid; task < 9 * 64; task += 256) {
-            const int t = task >> 6, rem = task & 63;
-            const int pq = rem >> 2, cq = rem & 3;
+#pragma unroll
+        for (int i = 0; i < 3; i++) {
+            const int t = wave + 4 * i;
             const int dr = t / 3 - 1, ds = t % 3 - 1;
-            const int ci = ci0 + 4 * cq;
-            uint32_t d[4];
-            for (int i = 0; i < 4; i++) {
-                const int pp = pix_p[4 * pq + i];
-                const int hw = pix_hw[4 * pq + i];
-                const int hh = (hw >> 16) + dr, ww = (hw & 0xFFFF) + ds;
-                const bool ok = pp >= 0 && ci < p.ci && hh >= 0 && hh < p.h && ww >= 0 && ww < p.w;
-                d[i] = ok ? *(const uint32_t *)(p.x + (int64_t)(pp + dr * p.w + ds) * p.ci + ci) : 0u;
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                const int hh = ph[u] + dr, ww = pw[u] + ds;
+                const bool ok = t < 9 && ci_ok && pidx[u] < pe && hh >= 0 && hh < p.h &&
+                                ww >= 0 && ww < p.w;
+                braw[i][u] = ok ? *(const uint32_t *)(p.x + (int64_t)(pidx[u] + dr * p.w + ds) * p.ci + ci)
+                                : 0u;
             }
-            uint32_t o[4];
-            transpose4x4(d[0], d[1], d[2], d[3], o[0], o[1], o[2], o[3]);
-            for (int c = 0; c < 4; c++) *(uint32_t *)&Bs[t][4 * cq + c][4 * pq] = o[c];
         }
-        __syncthreads();
+        // advance the tracked pixels by one step
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            pidx[u] += DW_BK;
+            pw[u] += DW_BK;
+            while (pw[u] >= p.w) { pw[u] -= p.w; ph[u]++; }
+            while (ph[u] >= p.h) ph[u] -= p.h;
+        }
+    };
+    auto store = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < 3; i++) {
+            const int t = wave + 4 * i;
+            if (t < 9) {
+                uint32_t o[4];
+                transpose4x4(braw[i][0], braw[i][1], braw[i][2], braw[i][3], o[0], o[1], o[2], o[3]);
+#pragma unroll
+                for (int c = 0; c < 4; c++) *(uint32_t *)&Bs[buf][t][4 * cq + c][4 * pq] = o[c];
+            }
+        }
+    };
+
+    load(0, 0);
+    store(0);
+    __syncthreads();
+    for (int ks = 0; ks < nsteps; ks++) {
+        const int cur = ks & 1;
+        const bool more = ks + 1 < nsteps;
+        if (more) load(ks + 1, cur ^ 1);
         v4i bf[9];
-        for (int t = 0; t < 9; t++) bf[t] = *(const v4i *)&Bs[t][lane & 15][(lane >> 4) * 16];
+#pragma unroll
+        for (int t = 0; t < 9; t++) bf[t] = *(const v4i *)&Bs[cur][t][lane & 15][(lane >> 4) * 16];
+#pragma unroll
         for (int l = 0; l < 4; l++) {
-            if (l >= LA) break;
-            const v4i af = *(const v4i *)&As[l][wave * 16 + (lane & 15)][(lane >> 4) * 16];
-            for (int t = 0; t < 9; t++)
-                acc[l][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af, bf[t], acc[l][t], 0, 0, 0);
+            if (l < LA) {
+#pragma unroll
+                for (int t = 0; t < 9; t++)
+                    acc[l][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[cur][l], bf[t], acc[l][t], 0, 0, 0);
+            }
         }
+        if (more) store(cur ^ 1);
+        __syncthreads();
     }
-    // ---- combine limbs, add this chunk's partial tile into dW
+    // ---- combine limbs, store this chunk's partial tile
+    int64_t *part = p.part + (int64_t)blockIdx.z * p.co * 9 * p.ci;
+#pragma unroll
     for (int t = 0; t < 9; t++)
+#pragma unroll
         for (int i = 0; i < 4; i++) {
             const int co = co0 + wave * 16 + (lane >> 4) * 4 + i;
-            const int ci = ci0 + (lane & 15);
-            if (co >= p.co || ci >= p.ci) continue;
+            const int cin = ci0 + (lane & 15);
+            if (co >= p.co || cin >= p.ci) continue;
             int64_t v = 0;
+#pragma unroll
             for (int l = 0; l < 4; l++) v += (int64_t)acc[l][t][i] << (8 * l);
-            if (v != 0)
-                atomicAdd((unsigned long long *)&p.dw[((int64_t)co * 9 + t) * p.ci + ci],
-                          (unsigned long long)v);
+            part[((int64_t)co * 9 + t) * p.ci + cin] = v;
         }
 }
 
@@ -514,26 +573,54 @@ bool mfma_conv_dw_ok(const ConvShape &sh)
            sh.w < 65536 && sh.h < 65536;
 }
 
-void launch_conv_dw_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g,
-                         const uint32_t *gmax, const int8_t *x, int64_t *dw, uint32_t *flags)
+int64_t dw_plane_stride(const ConvShape &sh)
 {
-    launch_fill_i64(s, dw, (int64_t)sh.co * 9 * sh.c);
-    DwArgs a{};
-    a.n = sh.n; a.h = sh.h; a.w = sh.w; a.ci = sh.c; a.co = sh.co;
-    a.g = g; a.gmax = gmax; a.x = x; a.dw = dw; a.flags = flags;
+    const int64_t P = (int64_t)sh.n * sh.h * sh.w;
+    return (P + DW_BK - 1) / DW_BK * DW_BK;
+}
+
+// Split of the pixel dimension: about 512 workgroups in total, chunks of whole 64-pixel steps.
+static void dw_split(const ConvShape &sh, int64_t *nz_out, int64_t *kc_out)
+{
     const int64_t P = (int64_t)sh.n * sh.h * sh.w;
     const int tiles = ((sh.co + DW_BM - 1) / DW_BM) * ((sh.c + DW_BC - 1) / DW_BC);
-    // about 512 workgroups in total; chunks of whole 64-pixel steps, at most 2^17 pixels
     int64_t nz = (512 + tiles - 1) / tiles;
     const int64_t steps = (P + DW_BK - 1) / DW_BK;
     if (nz > steps) nz = steps;
     int64_t kc = ((steps + nz - 1) / nz) * DW_BK;
     if (kc > DW_KC_MAX) kc = DW_KC_MAX;
-    nz = (P + kc - 1) / kc;
-    a.kc = (int)kc;
+    *kc_out = kc;
+    *nz_out = (P + kc - 1) / kc;
+}
+
+int64_t dw_partial_count(const ConvShape &sh)
+{
+    int64_t nz, kc;
+    dw_split(sh, &nz, &kc);
+    return nz * sh.co * 9 * sh.c;
+}
+
+void launch_conv_dw_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g,
+                         const uint32_t *gmax, const int8_t *x, int8_t *gt, int64_t *part,
+                         int64_t *dw, uint32_t *flags)
+{
+    const int64_t P = (int64_t)sh.n * sh.h * sh.w;
+    const int64_t ps = dw_plane_stride(sh);
+    {
+        const int64_t ntask = (ps / 4) * ((sh.co + 3) / 4);
+        hipLaunchKernelGGL(k_grad_limb_planes, dim3((unsigned)((ntask + 255) / 256)), dim3(256), 0,
+                           s, g, (int)P, sh.co, ps, gmax, gt);
+    }
+    int64_t nz, kc;
+    dw_split(sh, &nz, &kc);
+    DwArgs a{};
+    a.n = sh.n; a.h = sh.h; a.w = sh.w; a.ci = sh.c; a.co = sh.co;
+    a.gt = gt; a.pstride = ps; a.gmax = gmax; a.x = x; a.part = part; a.kc = (int)kc;
+    a.flags = flags;
     dim3 grid((unsigned)((sh.co + DW_BM - 1) / DW_BM), (unsigned)((sh.c + DW_BC - 1) / DW_BC),
               (unsigned)nz);
     hipLaunchKernelGGL(k_conv_dw_mfma, grid, dim3(256), 0, s, a);
+    launch_sum_partials(s, part, (int)nz, (int64_t)sh.co * 9 * sh.c, dw);
 }
 
 }  // namespace nitro

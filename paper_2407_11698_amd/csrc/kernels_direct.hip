@@ -23,6 +23,24 @@ void launch_fill_i64(hipStream_t s, int64_t *p, int64_t count)
     hipLaunchKernelGGL(k_fill_i64, dim3(g), dim3(256), 0, s, p, count);
 }
 
+__global__ void k_sum_partials(const int64_t *__restrict__ part, int nz, int64_t count,
+                               int64_t *__restrict__ out)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t v = 0;
+        for (int z = 0; z < nz; z++) v += part[(int64_t)z * count + i];
+        out[i] = v;
+    }
+}
+
+void launch_sum_partials(hipStream_t s, const int64_t *part, int nz, int64_t count, int64_t *out)
+{
+    if (count <= 0) return;
+    hipLaunchKernelGGL(k_sum_partials, dim3(grid_stride_blocks(count, 256, 8192)), dim3(256), 0, s,
+                       part, nz, count, out);
+}
+
 // ---------------------------------------------------------------------------------------------
 // Direct 3x3 conv, stride 1, zero padding 1: z[n][h][w][co] = sum_{r,s,ci} x[..][h+r-1][w+s-1][ci]
 // * W[co][r][s][ci], then NITRO-Scaling and NITRO-ReLU.
@@ -230,53 +248,50 @@ void launch_linear_dw(hipStream_t s, int n, int k, int m, const int32_t *e, cons
 }
 
 // ---------------------------------------------------------------------------------------------
-// max|v| over the wave, then one atomic per wave (the slot must be zeroed first).
-__device__ inline void wave_abs_max_to(uint32_t *gmax, int64_t v)
-{
-    uint32_t m = fits_i32(v) ? (v < 0 ? (uint32_t)(-v) : (uint32_t)v) : 0xFFFFFFFFu;
-    for (int off = 32; off > 0; off >>= 1) {
-        uint32_t o = __shfl_xor(m, off, 64);
-        m = o > m ? o : m;
-    }
-    if ((threadIdx.x & 63) == 0) slot_max(gmax, m);
-}
-
 // Gradient at the block output -> gradient at the last layer's z (un-pool + ReLU').
 __global__ void k_unpool_relu_bwd(int n, int h, int w, int c, const int32_t *__restrict__ delta,
                                   const uint8_t *__restrict__ code, Relu rp,
                                   int32_t *__restrict__ g, uint32_t *gmax, uint32_t *flags)
 {
-    int H2 = h / 2, W2 = w / 2;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const bool live = i < (int64_t)n * H2 * W2 * c;
-    if (gmax) wave_abs_max_to(gmax, live ? relu_bwd(delta[i], (uint8_t)(code[i] >> 2), rp) : 0);
-    if (!live) return;
-    int ch = (int)(i % c);
-    int64_t p = i / c;
-    int q2 = (int)(p % W2);
-    int h2 = (int)((p / W2) % H2);
-    int nn = (int)(p / ((int64_t)W2 * H2));
-    uint8_t cd = code[i];
-    int arg = cd & 3;
-    int64_t v = relu_bwd(delta[i], (uint8_t)(cd >> 2), rp);
-    if (!fits_i32(v)) raise_flag(flags, FLAG_OVERFLOW);
-    for (int t = 0; t < 4; t++) {
-        int hh = 2 * h2 + (t >> 1), ww = 2 * q2 + (t & 1);
-        g[(((int64_t)nn * h + hh) * w + ww) * c + ch] = t == arg ? (int32_t)v : 0;
+    // pooled element i = (r * W2 + q2) * c + ch with r = n * H2 + h2 (all indices < 2^31)
+    const uint32_t W2 = (uint32_t)w / 2;
+    const uint32_t total = (uint32_t)n * ((uint32_t)h / 2) * W2 * (uint32_t)c;
+    uint32_t mx = 0;
+    bool bad = false;
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const uint8_t cd = code[i];
+        const int64_t v = relu_bwd(delta[i], (uint8_t)(cd >> 2), rp);
+        const uint32_t a = abs_i64_sat(v);
+        mx = a > mx ? a : mx;
+        bad |= !fits_i32(v);
+        const uint32_t ch = i % (uint32_t)c, pp = i / (uint32_t)c;
+        const uint32_t q2 = pp % W2, r = pp / W2;
+        const int arg = cd & 3;
+#pragma unroll
+        for (int t = 0; t < 4; t++) {
+            const uint32_t pix = (2 * r + (t >> 1)) * (uint32_t)w + 2 * q2 + (t & 1);
+            g[(int64_t)pix * c + ch] = t == arg ? (int32_t)v : 0;
+        }
     }
+    if (bad) raise_flag(flags, FLAG_OVERFLOW);
+    if (gmax) block_slot_max(gmax, mx);
 }
 
-__global__ void k_relu_bwd(int64_t count, const int32_t *__restrict__ delta,
+__global__ void k_relu_bwd(uint32_t count, const int32_t *__restrict__ delta,
                            const uint8_t *__restrict__ code, Relu rp, int32_t *__restrict__ g,
                            uint32_t *gmax, uint32_t *flags)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const bool live = i < count;
-    int64_t v = live ? relu_bwd(delta[i], code[i], rp) : 0;
-    if (gmax) wave_abs_max_to(gmax, v);
-    if (!live) return;
-    if (!fits_i32(v)) raise_flag(flags, FLAG_OVERFLOW);
-    g[i] = (int32_t)v;
+    uint32_t mx = 0;
+    bool bad = false;
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < count; i += gridDim.x * blockDim.x) {
+        const int64_t v = relu_bwd(delta[i], code[i], rp);
+        const uint32_t a = abs_i64_sat(v);
+        mx = a > mx ? a : mx;
+        bad |= !fits_i32(v);
+        g[i] = (int32_t)v;
+    }
+    if (bad) raise_flag(flags, FLAG_OVERFLOW);
+    if (gmax) block_slot_max(gmax, mx);
 }
 
 void launch_unpool_relu_bwd(hipStream_t s, int n, int h, int w, int c, bool pool,
@@ -285,12 +300,12 @@ void launch_unpool_relu_bwd(hipStream_t s, int n, int h, int w, int c, bool pool
 {
     if (pool) {
         int64_t total = (int64_t)n * (h / 2) * (w / 2) * c;
-        hipLaunchKernelGGL(k_unpool_relu_bwd, dim3(blocks_for(total, 256)), dim3(256), 0, s,
+        hipLaunchKernelGGL(k_unpool_relu_bwd, dim3(grid_stride_blocks(total)), dim3(256), 0, s,
                            n, h, w, c, delta, code, rp, g, gmax, flags);
     } else {
         int64_t total = (int64_t)n * h * w * c;
-        hipLaunchKernelGGL(k_relu_bwd, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                           total, delta, code, rp, g, gmax, flags);
+        hipLaunchKernelGGL(k_relu_bwd, dim3(grid_stride_blocks(total)), dim3(256), 0, s,
+                           (uint32_t)total, delta, code, rp, g, gmax, flags);
     }
 }
 
@@ -302,42 +317,44 @@ __global__ void k_conv_dx_direct(ConvShape sh, const int32_t *__restrict__ g,
                                  Relu rp, int32_t *__restrict__ out, int64_t *__restrict__ out64,
                                  uint32_t *gmax, uint32_t *flags)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const bool live = i < (int64_t)sh.n * sh.h * sh.w * sh.c;
-    if (!live) {
-        if (gmax) wave_abs_max_to(gmax, 0);
-        return;
-    }
-    int ci = (int)(i % sh.c);
-    int64_t p = i / sh.c;
-    int q = (int)(p % sh.w);
-    int h = (int)((p / sh.w) % sh.h);
-    int n = (int)(p / ((int64_t)sh.w * sh.h));
-    int64_t acc = 0;
-    for (int r = 0; r < 3; r++) {
-        int ho = h - r + 1;
-        if (ho < 0 || ho >= sh.h) continue;
-        for (int s = 0; s < 3; s++) {
-            int wo = q - s + 1;
-            if (wo < 0 || wo >= sh.w) continue;
-            const int32_t *gp = g + (((int64_t)n * sh.h + ho) * sh.w + wo) * sh.co;
-            const int32_t *wp = w + ((int64_t)r * 3 + s) * sh.c + ci;
-            for (int co = 0; co < sh.co; co++)
-                acc += (int64_t)gp[co] * (int64_t)wp[(int64_t)co * 9 * sh.c];
+    const int64_t total = (int64_t)sh.n * sh.h * sh.w * sh.c;
+    uint32_t mx = 0;
+    bool bad = false;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int ci = (int)(i % sh.c);
+        const int64_t p = i / sh.c;
+        const int q = (int)(p % sh.w);
+        const int h = (int)((p / sh.w) % sh.h);
+        const int n = (int)(p / ((int64_t)sh.w * sh.h));
+        int64_t acc = 0;
+        for (int r = 0; r < 3; r++) {
+            const int ho = h - r + 1;
+            if (ho < 0 || ho >= sh.h) continue;
+            for (int s = 0; s < 3; s++) {
+                const int wo = q - s + 1;
+                if (wo < 0 || wo >= sh.w) continue;
+                const int32_t *gp = g + (((int64_t)n * sh.h + ho) * sh.w + wo) * sh.co;
+                const int32_t *wp = w + ((int64_t)r * 3 + s) * sh.c + ci;
+                for (int co = 0; co < sh.co; co++)
+                    acc += (int64_t)gp[co] * (int64_t)wp[(int64_t)co * 9 * sh.c];
+            }
         }
-    }
-    if (out64) {
-        out64[i] = acc;
-        return;
-    }
-    bool bad = !fits_i32(acc);
-    if (code) {
-        acc = relu_bwd(acc, code[i], rp);
+        if (out64) {
+            out64[i] = acc;
+            continue;
+        }
         bad |= !fits_i32(acc);
+        if (code) {
+            acc = relu_bwd(acc, code[i], rp);
+            bad |= !fits_i32(acc);
+        }
+        const uint32_t a = abs_i64_sat(acc);
+        mx = a > mx ? a : mx;
+        out[i] = (int32_t)acc;
     }
-    if (gmax) wave_abs_max_to(gmax, acc);
     if (bad) raise_flag(flags, FLAG_OVERFLOW);
-    out[i] = (int32_t)acc;
+    if (gmax) block_slot_max(gmax, mx);
 }
 
 void launch_conv_dx(hipStream_t s, const ConvShape &sh, const int32_t *g, const int32_t *w,
@@ -345,8 +362,8 @@ void launch_conv_dx(hipStream_t s, const ConvShape &sh, const int32_t *g, const 
                     uint32_t *gmax, uint32_t *flags)
 {
     int64_t total = (int64_t)sh.n * sh.h * sh.w * sh.c;
-    hipLaunchKernelGGL(k_conv_dx_direct, dim3(blocks_for(total, 256)), dim3(256), 0, s,
-                       sh, g, w, code, rp, out, out64, gmax, flags);
+    hipLaunchKernelGGL(k_conv_dx_direct, dim3(grid_stride_blocks(total, 256, 8192)), dim3(256), 0,
+                       s, sh, g, w, code, rp, out, out64, gmax, flags);
 }
 
 // ---------------------------------------------------------------------------------------------

@@ -1,0 +1,380 @@
+// The learning layer of a block (an IntLinear d -> G with NITRO-Scaling, trained on the RSS
+// loss) on int8 MFMA, exact:
+//   forward    yhat[n][g] = floor(sum_k f[n][k] W[g][k] / 2^8 d),  e = yhat - 32 onehot(label)
+//   delta      delta[n][k] = sum_g e[n][g] W[g][k]   (pre-update W), fused with the max-pool
+//              routing and NITRO-ReLU backward of the block's last layer
+//   gradient   dW[g][k] = sum_n e[n][g] f[n][k]
+// All three are C[m][j] = sum_k A[m][k] B[j][k] with K-contiguous rows: one kernel, three
+// epilogues. Wide operands use balanced int8 limbs as in the convolution kernels.
+#include "mfma_common.h"
+
+namespace nitro {
+
+enum { LIN_PART = 0, LIN_UNPOOL = 1, LIN_DW = 2 };
+
+struct LgemmArgs {
+    int M, N, K;                  // K: a multiple of 16 (zero padded rows)
+    const void *a;                // A rows [M][lda]: int8 or int32
+    int64_t lda;
+    const uint32_t *a_max;        // int32 A: max|A|
+    const int8_t *b;              // B limb planes [4][N][ldb] (one plane when b_max is null)
+    int64_t ldb, bplane;
+    const uint32_t *b_max;
+    int kchunk;                   // K per split (multiple of 64); grid.z = number of splits
+    // LIN_PART: part[z][M][N]; LIN_DW: out64[m * ldc + j] for m < m_valid
+    int64_t *out64;
+    int64_t ldc;
+    int m_valid;
+    // LIN_UNPOOL: block output geometry (full resolution h x w, c channels, pooled or not)
+    const uint8_t *code;
+    Relu rp;
+    int h, w, c, pool;
+    int32_t *g;                   // gradient at the last layer's pre-activation, NHWC
+    int32_t *delta;               // optional copy of delta (int32, pooled NHWC)
+    uint32_t *gmax;
+    uint32_t *flags;
+};
+
+constexpr int LG_BM = 128, LG_BN = 64, LG_BK = 64, LG_LDS = 80;
+
+template <bool A32, int MODE>
+__global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
+{
+    constexpr int WM = LG_BM / 2, WN = LG_BN / 2;
+    constexpr int TM = WM / 16, TN = WN / 16;
+    constexpr int A_CHUNKS = LG_BM * 4 / 256, B_CHUNKS = LG_BN * 4 / 256;
+    constexpr int STAGE = (LG_BM + LG_BN) * LG_LDS;
+    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int m0 = blockIdx.x * LG_BM, n0 = blockIdx.y * LG_BN;
+    const int kb = blockIdx.z * p.kchunk;
+    const int ke = kb + p.kchunk < p.K ? kb + p.kchunk : p.K;
+    const int ksteps = (ke - kb + LG_BK - 1) / LG_BK;
+    const int LA = A32 ? limbs_for(*p.a_max) : 1;
+    const int LB = p.b_max ? limbs_for(*p.b_max) : 1;
+    if (LA > 4 || LB > 4) {
+        if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
+        return;
+    }
+    const int kc = tid & 3;
+
+    typedef typename std::conditional<A32, v4i[4], v4i[1]>::type ARaw;
+    ARaw ar[A_CHUNKS];
+    v4i br[B_CHUNKS];
+    int64_t acc64[TM][TN][4];
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++)
+#pragma unroll
+            for (int t = 0; t < 4; t++) acc64[i][j][t] = 0;
+
+    for (int la = 0; la < LA; la++) {
+        for (int lb = 0; lb < LB; lb++) {
+            const int8_t *bpl = p.b + lb * p.bplane;
+            auto load = [&](int ks) {
+                const int k = kb + ks * LG_BK + kc * 16;
+                const bool kin = k < ke;
+#pragma unroll
+                for (int i = 0; i < A_CHUNKS; i++) {
+                    const int m = m0 + (tid >> 2) + 64 * i;
+                    const bool ok = kin && m < p.M;
+                    if (A32) {
+                        const v4i *src = (const v4i *)((const int32_t *)p.a + (int64_t)m * p.lda + k);
+#pragma unroll
+                        for (int u = 0; u < 4; u++) ar[i][u] = ok ? src[u] : v4i{0, 0, 0, 0};
+                    } else {
+                        ar[i][0] = ok ? *(const v4i *)((const int8_t *)p.a + (int64_t)m * p.lda + k)
+                                      : v4i{0, 0, 0, 0};
+                    }
+                }
+#pragma unroll
+                for (int i = 0; i < B_CHUNKS; i++) {
+                    const int nn = n0 + (tid >> 2) + 64 * i;
+                    br[i] = (kin && nn < p.N) ? *(const v4i *)(bpl + (int64_t)nn * p.ldb + k)
+                                              : v4i{0, 0, 0, 0};
+                }
+            };
+            auto store = [&](int buf) {
+                uint8_t *As = smem + buf * STAGE;
+                uint8_t *Bs = As + LG_BM * LG_LDS;
+#pragma unroll
+                for (int i = 0; i < A_CHUNKS; i++) {
+                    v4i v;
+                    if (A32) {
+#pragma unroll
+                        for (int u = 0; u < 4; u++)
+                            v[u] = (int)limb4(ar[i][u][0], ar[i][u][1], ar[i][u][2], ar[i][u][3], la);
+                    } else {
+                        v = ar[i][0];
+                    }
+                    *(v4i *)(As + ((tid >> 2) + 64 * i) * LG_LDS + kc * 16) = v;
+                }
+#pragma unroll
+                for (int i = 0; i < B_CHUNKS; i++)
+                    *(v4i *)(Bs + ((tid >> 2) + 64 * i) * LG_LDS + kc * 16) = br[i];
+            };
+            v4i acc[TM][TN];
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++) acc[i][j] = v4i{0, 0, 0, 0};
+            if (ksteps > 0) {
+                load(0);
+                store(0);
+            }
+            __syncthreads();
+            for (int ks = 0; ks < ksteps; ks++) {
+                const int cur = ks & 1;
+                const bool more = ks + 1 < ksteps;
+                if (more) load(ks + 1);
+                const uint8_t *As = smem + cur * STAGE;
+                const uint8_t *Bs = As + LG_BM * LG_LDS;
+                v4i af[TM], bf[TN];
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+                    af[i] = *(const v4i *)(As + (wm * WM + i * 16 + (lane & 15)) * LG_LDS + (lane >> 4) * 16);
+#pragma unroll
+                for (int j = 0; j < TN; j++)
+                    bf[j] = *(const v4i *)(Bs + (wn * WN + j * 16 + (lane & 15)) * LG_LDS + (lane >> 4) * 16);
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int j = 0; j < TN; j++)
+                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
+                if (more) store(cur ^ 1);
+                __syncthreads();
+            }
+            const int sh = 8 * (la + lb);
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++)
+#pragma unroll
+                    for (int t = 0; t < 4; t++) acc64[i][j][t] += (int64_t)acc[i][j][t] << sh;
+        }
+    }
+
+    uint32_t mx = 0;
+    bool bad = false;
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++)
+#pragma unroll
+            for (int t = 0; t < 4; t++) {
+                const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + t;
+                const int col = n0 + wn * WN + j * 16 + (lane & 15);
+                if (m >= p.M || col >= p.N) continue;
+                const int64_t v = acc64[i][j][t];
+                if (MODE == LIN_PART) {
+                    p.out64[((int64_t)blockIdx.z * p.M + m) * p.N + col] = v;
+                } else if (MODE == LIN_DW) {
+                    if (m < p.m_valid) p.out64[(int64_t)m * p.ldc + col] = v;
+                } else {
+                    // m = sample, col = index in the block output; delta leaves no int32 range
+                    bad |= !fits_i32(v);
+                    const int64_t o = (int64_t)m * p.N + col;
+                    if (p.delta) p.delta[o] = (int32_t)v;
+                    if (p.pool) {
+                        const uint8_t cd = p.code[o];
+                        const int64_t gv = relu_bwd(v, (uint8_t)(cd >> 2), p.rp);
+                        bad |= !fits_i32(gv);
+                        const uint32_t a = abs_i64_sat(gv);
+                        mx = a > mx ? a : mx;
+                        const uint32_t W2 = (uint32_t)p.w / 2;
+                        const uint32_t ch = (uint32_t)col % (uint32_t)p.c, pp = (uint32_t)col / (uint32_t)p.c;
+                        const uint32_t q2 = pp % W2, h2 = pp / W2;
+                        const int arg = cd & 3;
+                        int32_t *gb = p.g + (int64_t)m * p.h * p.w * p.c;
+#pragma unroll
+                        for (int u = 0; u < 4; u++) {
+                            const uint32_t pix = (2 * h2 + (u >> 1)) * (uint32_t)p.w + 2 * q2 + (u & 1);
+                            gb[(int64_t)pix * p.c + ch] = u == arg ? (int32_t)gv : 0;
+                        }
+                    } else {
+                        const int64_t gv = relu_bwd(v, p.code[o], p.rp);
+                        bad |= !fits_i32(gv);
+                        const uint32_t a = abs_i64_sat(gv);
+                        mx = a > mx ? a : mx;
+                        p.g[o] = (int32_t)gv;
+                    }
+                }
+            }
+    if (MODE == LIN_UNPOOL) {
+        if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
+        block_slot_max(p.gmax, mx);
+    }
+}
+
+template <bool A32, int MODE>
+static void launch_lgemm(hipStream_t s, const LgemmArgs &a, int splits)
+{
+    dim3 grid((unsigned)((a.M + LG_BM - 1) / LG_BM), (unsigned)((a.N + LG_BN - 1) / LG_BN),
+              (unsigned)splits);
+    hipLaunchKernelGGL((k_lgemm<A32, MODE>), grid, dim3(256), 0, s, a);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Learning weights W [G][d] int32 -> limb planes [4][G][d] and [4][d][gp] (zero rows g >= G);
+// max|W| -> *wmax.
+__global__ void k_pack_learning_weights(const int32_t *__restrict__ w, uint32_t G, uint32_t d,
+                                        uint32_t gp, int8_t *__restrict__ wf,
+                                        int8_t *__restrict__ wt, uint32_t *wmax)
+{
+    const uint32_t total = G * d;
+    uint32_t m = 0;
+    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const int32_t v = w[i];
+        const uint32_t a = abs_u32(v);
+        m = a > m ? a : m;
+#pragma unroll
+        for (int l = 0; l < 4; l++) wf[(int64_t)l * total + i] = limb1(v, l);
+    }
+    // transposed planes in their own order (coalesced stores)
+    const uint32_t ttotal = d * gp;
+    for (uint32_t ti = blockIdx.x * blockDim.x + threadIdx.x; ti < ttotal; ti += gridDim.x * blockDim.x) {
+        const uint32_t g = ti % gp, k = ti / gp;
+        const int32_t v = g < G ? w[g * d + k] : 0;
+#pragma unroll
+        for (int l = 0; l < 4; l++) wt[(int64_t)l * ttotal + ti] = limb1(v, l);
+    }
+    block_slot_max(wmax, m);
+}
+
+// f [n][d] int8 -> fT [d][np] (zero columns n >= N): 64 x 64 tiles through LDS.
+__global__ __launch_bounds__(256) void k_transpose_i8(const int8_t *__restrict__ f, int N, int d,
+                                                      int np, int8_t *__restrict__ ft)
+{
+    __shared__ int8_t t[64][65];
+    const int n0 = blockIdx.y * 64, k0 = blockIdx.x * 64;
+    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+        const int r = e / 64, c = e % 64;                 // r: sample, c: feature
+        t[r][c] = (n0 + r < N && k0 + c < d) ? f[(int64_t)(n0 + r) * d + k0 + c] : 0;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+        const int r = e / 64, c = e % 64;                 // r: feature, c: sample
+        if (k0 + r < d && n0 + c < np) ft[(int64_t)(k0 + r) * np + n0 + c] = t[c][r];
+    }
+}
+
+// yhat and e from the split-K partial sums; also e padded to [n][gp] and transposed to [gp][np]
+// (zeros in the padding), max|e| -> *emax.
+__global__ void k_loss_from_partials(const int64_t *__restrict__ part, int nz, int N, int G, int gp,
+                                     int np, Div sf, const int32_t *__restrict__ labels,
+                                     int32_t *__restrict__ yhat, int32_t *__restrict__ e,
+                                     int32_t *__restrict__ epad, int32_t *__restrict__ et,
+                                     uint32_t *emax, uint32_t *flags)
+{
+    uint32_t m = 0;
+    bool bad = false, badlab = false;
+    const int total = np * gp;
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+        const int n = i / gp, g = i % gp;
+        int64_t ev = 0;
+        if (n < N && g < G) {
+            int64_t z = 0;
+            for (int s = 0; s < nz; s++) z += part[((int64_t)s * N + n) * G + g];
+            const int64_t y = idiv(z, sf);
+            const int lab = labels[n];
+            badlab |= lab < 0 || lab >= G;
+            ev = y - (lab == g ? 32 : 0);
+            bad |= !fits_i32(y) || !fits_i32(ev);
+            yhat[n * G + g] = (int32_t)y;
+            e[n * G + g] = (int32_t)ev;
+            const uint32_t a = abs_i64_sat(ev);
+            m = a > m ? a : m;
+        }
+        if (n < N) epad[n * gp + g] = (int32_t)ev;
+        et[(int64_t)g * np + n] = (int32_t)ev;
+    }
+    if (bad) raise_flag(flags, FLAG_OVERFLOW);
+    if (badlab) raise_flag(flags, FLAG_LABEL);
+    block_slot_max(emax, m);
+}
+
+// ---------------------------------------------------------------------------------------------
+bool mfma_learning_ok(int n, int64_t d, int G)
+{
+    return d % 16 == 0 && n >= 1 && G >= 1 && (int64_t)n * d < ((int64_t)1 << 31) &&
+           (int64_t)G * d < ((int64_t)1 << 31) && G <= 4096;
+}
+
+LearningScratch learning_scratch(int n, int64_t d, int G)
+{
+    LearningScratch s{};
+    s.gp = (G + 15) / 16 * 16;
+    s.np = (n + 15) / 16 * 16;
+    int splits = (int)((d + 1023) / 1024);
+    if (splits < 1) splits = 1;
+    const int tiles = ((n + LG_BM - 1) / LG_BM) * ((G + LG_BN - 1) / LG_BN);
+    if (splits * tiles > 1024) splits = (1024 + tiles - 1) / tiles;
+    int64_t kchunk = (d + splits - 1) / splits;
+    kchunk = (kchunk + LG_BK - 1) / LG_BK * LG_BK;
+    s.kchunk = kchunk;
+    s.splits = (int)((d + kchunk - 1) / kchunk);
+    s.wf_bytes = 4 * (int64_t)G * d;
+    s.wt_bytes = 4 * d * s.gp;
+    s.part_bytes = 8 * (int64_t)s.splits * n * G;
+    s.epad_bytes = 4 * (int64_t)s.np * s.gp;
+    s.et_bytes = 4 * (int64_t)s.gp * s.np;
+    s.ft_bytes = d * s.np;
+    return s;
+}
+
+void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *f,
+                          const int32_t *w, const Div &sf, const int32_t *labels,
+                          const LearningBuffers &b, const uint8_t *code, const Relu &rp, int h,
+                          int wdt, int c, bool pool, int32_t *g, int32_t *delta_copy,
+                          int32_t *yhat, int32_t *e, int64_t *dw, uint32_t *flags)
+{
+    const LearningScratch sc = learning_scratch(n, d, G);
+    // operands: learning-weight limb planes, the transposed block output
+    hipLaunchKernelGGL(k_pack_learning_weights, dim3(grid_stride_blocks((int64_t)G * d, 256, 1024)),
+                       dim3(256), 0, s, w, (uint32_t)G, (uint32_t)d, (uint32_t)sc.gp, b.wf, b.wt,
+                       b.wmax);
+    hipLaunchKernelGGL(k_transpose_i8, dim3((unsigned)((d + 63) / 64), (unsigned)((sc.np + 63) / 64)),
+                       dim3(256), 0, s, f, n, (int)d, sc.np, b.ft);
+    // forward: split-K partials, then yhat / e
+    {
+        LgemmArgs a{};
+        a.M = n; a.N = G; a.K = (int)d;
+        a.a = f; a.lda = d;
+        a.b = b.wf; a.ldb = d; a.bplane = (int64_t)G * d; a.b_max = b.wmax;
+        a.kchunk = (int)sc.kchunk;
+        a.out64 = b.part;
+        a.flags = flags;
+        launch_lgemm<false, LIN_PART>(s, a, sc.splits);
+        hipLaunchKernelGGL(k_loss_from_partials, dim3(grid_stride_blocks((int64_t)sc.np * sc.gp, 256, 256)),
+                           dim3(256), 0, s, b.part, sc.splits, n, G, sc.gp, sc.np, sf, labels, yhat,
+                           e, b.epad, b.et, b.emax, flags);
+    }
+    // weight gradient: dW[g][k] = sum_n e[n][g] f[n][k]   (M = gp, N = d, K = np)
+    {
+        LgemmArgs a{};
+        a.M = sc.gp; a.N = (int)d; a.K = sc.np;
+        a.a = b.et; a.lda = sc.np; a.a_max = b.emax;
+        a.b = b.ft; a.ldb = sc.np; a.bplane = 0; a.b_max = nullptr;
+        a.kchunk = sc.np;
+        a.out64 = dw; a.ldc = d; a.m_valid = G;
+        a.flags = flags;
+        launch_lgemm<true, LIN_DW>(s, a, 1);
+    }
+    // delta = e W (pre-update), routed through the pool and NITRO-ReLU backward into g
+    {
+        LgemmArgs a{};
+        a.M = n; a.N = (int)d; a.K = sc.gp;
+        a.a = b.epad; a.lda = sc.gp; a.a_max = b.emax;
+        a.b = b.wt; a.ldb = sc.gp; a.bplane = d * sc.gp; a.b_max = b.wmax;
+        a.kchunk = sc.gp;
+        a.code = code; a.rp = rp; a.h = h; a.w = wdt; a.c = c; a.pool = pool ? 1 : 0;
+        a.g = g; a.delta = delta_copy; a.gmax = b.gmax;
+        a.flags = flags;
+        launch_lgemm<true, LIN_UNPOOL>(s, a, 1);
+    }
+}
+
+}  // namespace nitro

@@ -107,6 +107,47 @@ __device__ inline void slot_max(uint32_t *slot, uint32_t m)
         atomicMax(slot, m);
 }
 
+__device__ inline uint32_t wave_max_u32(uint32_t v)
+{
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t o = __shfl_xor(v, off, 64);
+        v = o > v ? o : v;
+    }
+    return v;
+}
+
+// Workgroup-wide maximum folded into a device slot with one atomic per workgroup. Every thread
+// of the workgroup must call it (it contains a barrier); at most 1024 threads.
+__device__ inline void block_slot_max(uint32_t *slot, uint32_t m)
+{
+    __shared__ uint32_t red[16];
+    m = wave_max_u32(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t r = 0;
+        for (unsigned w = 0; w < (blockDim.x + 63) / 64; w++) r = red[w] > r ? red[w] : r;
+        slot_max(slot, r);
+    }
+}
+
+__device__ inline uint32_t abs_u32(int32_t v) { return v < 0 ? (uint32_t)(-(int64_t)v) : (uint32_t)v; }
+
+// |v| for a value meant for int32 (anything outside int32 maps to the largest code, which no
+// limb count accepts)
+__device__ inline uint32_t abs_i64_sat(int64_t v)
+{
+    return (v >= INT32_MIN && v <= INT32_MAX) ? abs_u32((int32_t)v) : 0xFFFFFFFFu;
+}
+
+// Grid size for a grid-stride elementwise kernel: enough workgroups to fill the GPU, few
+// enough that per-workgroup reductions stay cheap.
+inline unsigned grid_stride_blocks(int64_t n, int per = 256, unsigned cap = 2048)
+{
+    const int64_t b = (n + per - 1) / per;
+    return (unsigned)(b < 1 ? 1 : (b > cap ? cap : b));
+}
+
 // ------------------------------------------------------------------------------------------
 // Kernel launchers (each enqueues on `s`; shapes are validated by the caller).
 // ------------------------------------------------------------------------------------------
@@ -115,6 +156,8 @@ struct ConvShape {
 };
 
 void launch_fill_i64(hipStream_t s, int64_t *p, int64_t count);
+// out[i] = sum_{z < nz} part[z * count + i]  (split-K partial sums, fixed order)
+void launch_sum_partials(hipStream_t s, const int64_t *part, int nz, int64_t count, int64_t *out);
 
 // forward conv + Scaling + ReLU; POOL variant writes the pooled output and per pooled element
 // code = argmax | region << 2; the plain variant writes the full-resolution output and region.
@@ -146,6 +189,37 @@ void launch_conv_dx(hipStream_t s, const ConvShape &sh, const int32_t *g, const 
                     const uint8_t *code, const Relu &rp, int32_t *out, int64_t *out64,
                     uint32_t *gmax, uint32_t *flags);
 
+// ---- learning layer on int8 MFMA (linear_mfma.hip)
+struct LearningScratch {
+    int gp, np, splits;            // G and n rounded up to 16; split-K count of the forward GEMM
+    int64_t kchunk;
+    int64_t wf_bytes, wt_bytes, part_bytes, epad_bytes, et_bytes, ft_bytes;
+};
+struct LearningBuffers {
+    int8_t *wf, *wt, *ft;          // weight limb planes [4][G][d], [4][d][gp]; f^T [d][np]
+    int64_t *part;                 // forward split-K partial sums
+    int32_t *epad, *et;            // e as [np][gp] and [gp][np] (zero padded)
+    uint32_t *wmax, *emax, *gmax;  // max|W|, max|e|, max|g| slots (zeroed before the call)
+};
+bool mfma_learning_ok(int n, int64_t d, int G);
+LearningScratch learning_scratch(int n, int64_t d, int G);
+// yhat, e, dW of the learning layer on f = the block output [n][d], and the gradient g at the
+// last forward layer's pre-activation (un-pool and NITRO-ReLU backward of delta = e W).
+void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *f,
+                          const int32_t *w, const Div &sf, const int32_t *labels,
+                          const LearningBuffers &b, const uint8_t *code, const Relu &rp, int h,
+                          int wdt, int c, bool pool, int32_t *g, int32_t *delta_copy,
+                          int32_t *yhat, int32_t *e, int64_t *dw, uint32_t *flags);
+
+// ---- few input channels (conv_smallc.hip)
+bool smallc_fwd_ok(const ConvShape &sh);
+bool smallc_dw_ok(const ConvShape &sh);
+void launch_conv_fwd_smallc(hipStream_t s, const ConvShape &sh, const int8_t *x, const int32_t *w,
+                            const Div &sf, const Relu &rp, bool pool, int8_t *out, uint8_t *code);
+int64_t smallc_dw_partial_count(const ConvShape &sh);
+void launch_conv_dw_smallc(hipStream_t s, const ConvShape &sh, const int32_t *g, const int8_t *x,
+                           int64_t *part, int64_t *dw);
+
 // ---- int8 MFMA implicit-GEMM path (conv_mfma.hip)
 bool mfma_conv_fwd_ok(const ConvShape &sh, bool pool);
 bool mfma_conv_dx_ok(const ConvShape &sh);
@@ -157,9 +231,15 @@ void launch_conv_fwd_mfma(hipStream_t s, const ConvShape &sh, const int8_t *x, c
                           const uint32_t *wmax, const Div &sf, const Relu &rp, bool pool,
                           int8_t *out, uint8_t *code, uint32_t *flags);
 bool mfma_conv_dw_ok(const ConvShape &sh);
-// dW (int64, zeroed here) from g int32 NHWC (max|g| in *gmax) and x int8 NHWC.
+// Row length of the pixel-contiguous gradient limb planes used by the weight gradient; the
+// scratch `gt` holds 4 * sh.co * dw_plane_stride(sh) bytes.
+int64_t dw_plane_stride(const ConvShape &sh);
+// int64 words of split-K partial sums the weight gradient needs as scratch
+int64_t dw_partial_count(const ConvShape &sh);
+// dW (int64) from g int32 NHWC (max|g| in *gmax) and x int8 NHWC; `gt`, `part` are scratch.
 void launch_conv_dw_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g,
-                         const uint32_t *gmax, const int8_t *x, int64_t *dw, uint32_t *flags);
+                         const uint32_t *gmax, const int8_t *x, int8_t *gt, int64_t *part,
+                         int64_t *dw, uint32_t *flags);
 void launch_conv_dx_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g, const uint32_t *gmax_in,
                          const int8_t *wt, const uint32_t *wmax, const uint8_t *prev_code,
                          const Relu &rp, int32_t *gout, int64_t *out64, uint32_t *gmax_out,
