@@ -10,8 +10,8 @@
  *                   -> optional 2x2/2 max-pool after the last layer (Tab. 1);
  *   learning layer  IntLinear(d -> G) + NITRO-Scaling on the block output (section 3.2, the
  *                   training procedure of section 3.3), RSS loss gradient yhat - y with the
- *                   32-valued one-hot target (Eq. 4, section 3.3.4, Appendix A);
- *   backward        delta^fw = grad * W^il (section 3.3.5) routed back through pool, NITRO-ReLU
+ *                   32-valued one-hot target (Eq. 4; section 3.3.4, Appendix A);
+ *   backward        delta^fw = grad * W^il (section 3.3.4) routed back through pool, NITRO-ReLU
  *                   and the forward layers of the block only; int64 weight gradients;
  *   IntegerSGD      Alg. 1, with gamma^fw = AF * gamma, AF = 2^6 * G (Eq. 6).
  * Everything is integer arithmetic; results are bit-exact.
@@ -133,6 +133,14 @@ typedef struct {
  * aligned) and passes the same buffer to nitro_block_forward and nitro_block_backward. */
 nitro_status nitro_block_query(const nitro_block_desc *desc, size_t *state_bytes);
 
+/* Device pointers, inside a block state buffer, of what the forward pass saved for forward layer
+ * j: its int8 NHWC output activations (*act; NULL for the last layer, whose output is the
+ * caller's a_out) and its NITRO-ReLU region codes (*code; one uint8 per output element: 0 for
+ * 0 <= z* <= 127, 1 for -127 <= z* < 0, 2 where the map saturates; for a pooled last layer, one
+ * per pooled element: argmax index in the 2x2 window | region << 2). For inspection. */
+nitro_status nitro_block_saved(const nitro_block_desc *desc, void *state, int32_t j,
+                               int8_t **act, uint8_t **code);
+
 /* Forward layers of one block (section 3.2; training procedure of section 3.3).
  *   x      int8 NHWC [n][h][w][c_in] (or [n][c_in] for linear blocks); must stay unchanged
  *          until the matching nitro_block_backward has run;
@@ -226,10 +234,11 @@ int64_t nitro_host_div(int64_t n, int64_t d, int32_t round);
 /* NITRO-ReLU mean for alpha_inv (section 3.2.2) under `round`. */
 int32_t nitro_host_relu_mu(int32_t alpha_inv, int32_t round);
 
-/* Per-kernel timing for profiling: when enabled, the library records HIP events around every
- * launch of the kernel class `cls` (0: conv forward, 1: conv input gradient, 2: conv weight
- * gradient) on the context stream; nitro_kernel_time returns the accumulated milliseconds and
- * launch count since the last reset (synchronises the stream). */
+/* Per-kernel timing for profiling: when enabled, the library records HIP events on the context
+ * stream around every launch of one kernel of class `cls`: 0 the int8 MFMA conv forward kernel,
+ * 1 the int8 MFMA conv input-gradient kernel, 2 the int8 MFMA conv weight-gradient kernel
+ * (layers that take other kernels are not timed). nitro_kernel_time synchronises the stream and
+ * returns the accumulated milliseconds and launch count since the last read or enable. */
 nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable);
 nitro_status nitro_kernel_time(nitro_ctx *ctx, int32_t cls, double *ms, int64_t *launches);
 

@@ -400,7 +400,7 @@ class Hyper:
 
     @property
     def gamma_fw(self) -> int:
-        """gamma_inv^fw = AF * gamma_inv^lr (section 3.3.5)."""
+        """gamma_inv^fw = AF * gamma_inv^lr (section 3.3.4, Eq. 6)."""
         return amplification_factor(self.n_classes or self.af_classes) * self.gamma_inv
 
 

@@ -10,13 +10,37 @@
 
 using namespace nitro;
 
-struct nitro_ctx {
+namespace nitro {
+thread_local LaunchTimer *g_timer = nullptr;
+}
+
+struct nitro_ctx : public LaunchTimer {
     int device = 0;
     hipStream_t stream = nullptr;
     uint32_t *flags = nullptr;                  // device: sticky status bits
     bool timing = false;
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[3];
-    size_t used[3] = {0, 0, 0};
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[TIMED_CLASSES];
+    size_t used[TIMED_CLASSES] = {0, 0, 0};
+    hipEvent_t pending_stop = nullptr;
+
+    // HIP events around one launch of a timed kernel class, on the context's stream
+    void begin(int cls) override
+    {
+        if (used[cls] == ev[cls].size()) {
+            hipEvent_t a, b;
+            if (hipEventCreate(&a) != hipSuccess) return;
+            if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+            ev[cls].push_back({a, b});
+        }
+        auto &p = ev[cls][used[cls]++];
+        (void)hipEventRecord(p.first, stream);
+        pending_stop = p.second;
+    }
+    void end(int) override
+    {
+        if (pending_stop) (void)hipEventRecord(pending_stop, stream);
+        pending_stop = nullptr;
+    }
 };
 
 namespace {
@@ -42,30 +66,11 @@ nitro_status hip_status()
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-// Kernel classes for the optional per-kernel timing.
-enum { CLS_CONV_FWD = 0, CLS_CONV_DX = 1, CLS_CONV_DW = 2 };
-
-struct TimedLaunch {
-    nitro_ctx *ctx;
-    int cls;
-    hipEvent_t stop = nullptr;
-    TimedLaunch(nitro_ctx *c, int k) : ctx(c), cls(k)
-    {
-        if (!ctx->timing) return;
-        if (ctx->used[cls] == ctx->ev[cls].size()) {
-            hipEvent_t a, b;
-            if (hipEventCreate(&a) != hipSuccess) return;
-            if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
-            ctx->ev[cls].push_back({a, b});
-        }
-        auto &p = ctx->ev[cls][ctx->used[cls]++];
-        (void)hipEventRecord(p.first, ctx->stream);
-        stop = p.second;
-    }
-    ~TimedLaunch()
-    {
-        if (stop) (void)hipEventRecord(stop, ctx->stream);
-    }
+// Installs the context's launch timer for the duration of an API call.
+struct TimerScope {
+    LaunchTimer *prev;
+    explicit TimerScope(nitro_ctx *ctx) : prev(g_timer) { g_timer = ctx->timing ? ctx : nullptr; }
+    ~TimerScope() { g_timer = prev; }
 };
 
 // ------------------------------------------------------------------------------------------
@@ -166,7 +171,7 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     }
     int64_t gtb = 0;
     for (int j = 0; j < g->J; j++)
-        if (conv && mfma_conv_dw_ok(g->L[j].sh)) {
+        if (conv && (mfma_conv_dw_ok(g->L[j].sh) || mfma_conv_dw_smallc_ok(g->L[j].sh))) {
             const int64_t b = 4 * (int64_t)g->L[j].sh.co * dw_plane_stride(g->L[j].sh);
             if (b > gtb) gtb = b;
         }
@@ -175,7 +180,8 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     for (int j = 0; j < g->J; j++) {
         if (!conv) continue;
         int64_t c = 0;
-        if (mfma_conv_dw_ok(g->L[j].sh)) c = dw_partial_count(g->L[j].sh);
+        if (mfma_conv_dw_ok(g->L[j].sh) || mfma_conv_dw_smallc_ok(g->L[j].sh))
+            c = dw_partial_count(g->L[j].sh);
         else if (smallc_dw_ok(g->L[j].sh)) c = smallc_dw_partial_count(g->L[j].sh);
         if (c > parts) parts = c;
     }
@@ -220,7 +226,6 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
             // limb planes for this call's forward and input-gradient GEMMs, and max|W_j|
             launch_pack_conv_weights(s, p->w[j], L.sh.co, L.sh.c, (int8_t *)at(state, g.wf[j]),
                                      (int8_t *)at(state, g.wt[j]), &slots[j]);
-            TimedLaunch t(ctx, CLS_CONV_FWD);
             if (mfma_conv_fwd_ok(L.sh, pool))
                 launch_conv_fwd_mfma(s, L.sh, cur, (const int8_t *)at(state, g.wf[j]), &slots[j],
                                      sf, rp, pool, out, code, ctx->flags);
@@ -296,8 +301,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         const int8_t *xin = j == 0 ? x : (const int8_t *)at(state, g.act[j - 1]);
         const int32_t *gj = gb[cur];
         if (L.conv) {
-            TimedLaunch t(ctx, CLS_CONV_DW);
-            if (mfma_conv_dw_ok(L.sh))
+            if (mfma_conv_dw_ok(L.sh) || mfma_conv_dw_smallc_ok(L.sh))
                 launch_conv_dw_mfma(s, L.sh, gj, &slots[4 + j], xin, (int8_t *)at(state, g.gt),
                                     (int64_t *)at(state, g.part), gr->dw[j], ctx->flags);
             else if (smallc_dw_ok(L.sh))
@@ -321,7 +325,6 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         if (dst || dst64) {
             uint32_t *gmax_out = j > 0 ? &slots[4 + j - 1] : nullptr;
             if (L.conv) {
-                TimedLaunch t(ctx, CLS_CONV_DX);
                 if (mfma_conv_dx_ok(L.sh))
                     launch_conv_dx_mfma(s, L.sh, gj, &slots[4 + j], (const int8_t *)at(state, g.wt[j]),
                                         &slots[j], code, rp, dst, dst64, gmax_out, ctx->flags);
@@ -508,6 +511,19 @@ nitro_status nitro_block_query(const nitro_block_desc *desc, size_t *state_bytes
     return NITRO_OK;
 }
 
+nitro_status nitro_block_saved(const nitro_block_desc *desc, void *state, int32_t j,
+                               int8_t **act, uint8_t **code)
+{
+    if (!state || !act || !code) return NITRO_EINVAL;
+    BlockGeom g;
+    nitro_status st = block_geom(desc, &g);
+    if (st != NITRO_OK) return st;
+    if (j < 0 || j >= g.J) return NITRO_EINVAL;
+    *act = j == g.J - 1 ? nullptr : (int8_t *)at(state, g.act[j]);
+    *code = at(state, g.code[j]);
+    return NITRO_OK;
+}
+
 nitro_status nitro_block_forward(nitro_ctx *ctx, const nitro_block_desc *desc,
                                  const nitro_block_params *params, const int8_t *x,
                                  int8_t *a_out, void *state)
@@ -519,6 +535,7 @@ nitro_status nitro_block_forward(nitro_ctx *ctx, const nitro_block_desc *desc,
     for (int j = 0; j < g.J; j++)
         if (!params->w[j]) return NITRO_EINVAL;
     DeviceGuard guard(ctx->device);
+    TimerScope timer(ctx);
     return block_forward_impl(ctx, desc, g, params, x, a_out, state);
 }
 
@@ -540,6 +557,7 @@ nitro_status nitro_block_backward(nitro_ctx *ctx, const nitro_block_desc *desc,
         return NITRO_EINVAL;
     }
     DeviceGuard guard(ctx->device);
+    TimerScope timer(ctx);
     return block_backward_impl(ctx, desc, g, params, x, a_out, labels, delta_out, state, grads, taps);
 }
 
@@ -613,6 +631,7 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     }
     if (net->head && !params->w_head) return NITRO_EINVAL;
     DeviceGuard guard(ctx->device);
+    TimerScope timer(ctx);
 
     // 1. forward through every block (pre-update weights)
     const int8_t *cur = x;
@@ -676,7 +695,7 @@ nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable)
 
 nitro_status nitro_kernel_time(nitro_ctx *ctx, int32_t cls, double *ms, int64_t *launches)
 {
-    if (!ctx || cls < 0 || cls > 2 || !ms || !launches) return NITRO_EINVAL;
+    if (!ctx || cls < 0 || cls >= TIMED_CLASSES || !ms || !launches) return NITRO_EINVAL;
     DeviceGuard guard(ctx->device);
     if (hipStreamSynchronize(ctx->stream) != hipSuccess) return NITRO_EHIP;
     double tot = 0.0;

@@ -326,7 +326,10 @@ static void launch_igemm(hipStream_t s, const IgemmArgs &a)
     const int64_t M = (int64_t)a.n * a.h * a.w;
     constexpr int BM = 128, BN = 64;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.no + BN - 1) / BN));
+    const int cls = MODE == IG_FWD ? TIMED_IGEMM_FWD : TIMED_IGEMM_DX;
+    timer_begin(cls);
     hipLaunchKernelGGL((k_igemm_conv<MODE, BM, BN>), grid, dim3(256), 0, s, a);
+    timer_end(cls);
 }
 
 // K = 9 * ck <= 9 * 8192 keeps 128 * 128 * K below 2^31 (one limb pass in int32).
@@ -442,7 +445,8 @@ constexpr int DW_KC_MAX = 131008;
 // One workgroup: 64 output channels x 16 input channels x 9 taps over a chunk of pixels.
 // A fragments (g limbs) come straight from the pixel-contiguous planes: each wave owns 16
 // output channels. The x tile of each tap is staged in LDS (double-buffered, next step's global
-// loads issued before this step's MFMAs).
+// loads issued before this step's MFMAs). Limbs are taken two at a time: a second pass over the
+// chunk handles limbs 2 and 3 when g needs them.
 __global__ __launch_bounds__(256) void k_conv_dw_mfma(DwArgs p)
 {
     __shared__ __attribute__((aligned(16))) uint8_t Bs[2][9][DW_BC][DW_LDS];
@@ -459,118 +463,258 @@ __global__ __launch_bounds__(256) void k_conv_dw_mfma(DwArgs p)
     const int pb = blockIdx.z * p.kc;
     const int pe = pb + p.kc < P ? pb + p.kc : P;
     const int nsteps = (pe - pb + DW_BK - 1) / DW_BK;
+    // one step advances every tracked pixel by DW_BK = adv_h rows + adv_w columns
+    const int adv_h = DW_BK / p.w, adv_w = DW_BK % p.w;
 
-    // A: this lane's row (output channel) and 16-pixel group within a step
     const int arow = co0 + wave * 16 + (lane & 15);
     const bool arow_ok = arow < p.co;
     const int8_t *abase = p.gt + (int64_t)(arow_ok ? arow : 0) * p.pstride + pb + (lane >> 4) * 16;
     const int64_t aplane = (int64_t)p.co * p.pstride;
 
-    // B staging: tasks (tap t = wave + 4 i, pixel quad pq, channel quad cq); pq, cq fixed
     const int pq = (tid & 63) >> 2, cq = tid & 3;
     const int ci = ci0 + 4 * cq;
     const bool ci_ok = ci < p.ci;
-    // coordinates of this thread's 4 pixels in the current step (tracked incrementally)
-    int ph[4], pw[4], pidx[4];
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-        const int pp = pb + 4 * pq + i;
-        const int rem = pp % HW;
-        pidx[i] = pp;
-        ph[i] = rem / p.w;
-        pw[i] = rem % p.w;
-    }
+    const int8_t *xci = p.x + ci;
 
-    v4i acc[4][9];
-#pragma unroll
-    for (int l = 0; l < 4; l++)
-#pragma unroll
-        for (int t = 0; t < 9; t++) acc[l][t] = v4i{0, 0, 0, 0};
-
-    v4i af[2][4];
-    uint32_t braw[3][4];
-    auto load = [&](int ks, int slot) {
-        const int k0 = ks * DW_BK;
-#pragma unroll
-        for (int l = 0; l < 4; l++)
-            af[slot][l] = (l < LA && arow_ok) ? *(const v4i *)(abase + l * aplane + k0)
-                                              : v4i{0, 0, 0, 0};
-#pragma unroll
-        for (int i = 0; i < 3; i++) {
-            const int t = wave + 4 * i;
-            const int dr = t / 3 - 1, ds = t % 3 - 1;
-#pragma unroll
-            for (int u = 0; u < 4; u++) {
-                const int hh = ph[u] + dr, ww = pw[u] + ds;
-                const bool ok = t < 9 && ci_ok && pidx[u] < pe && hh >= 0 && hh < p.h &&
-                                ww >= 0 && ww < p.w;
-                braw[i][u] = ok ? *(const uint32_t *)(p.x + (int64_t)(pidx[u] + dr * p.w + ds) * p.ci + ci)
-                                : 0u;
-            }
-        }
-        // advance the tracked pixels by one step
-#pragma unroll
-        for (int u = 0; u < 4; u++) {
-            pidx[u] += DW_BK;
-            pw[u] += DW_BK;
-            while (pw[u] >= p.w) { pw[u] -= p.w; ph[u]++; }
-            while (ph[u] >= p.h) ph[u] -= p.h;
-        }
-    };
-    auto store = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < 3; i++) {
-            const int t = wave + 4 * i;
-            if (t < 9) {
-                uint32_t o[4];
-                transpose4x4(braw[i][0], braw[i][1], braw[i][2], braw[i][3], o[0], o[1], o[2], o[3]);
-#pragma unroll
-                for (int c = 0; c < 4; c++) *(uint32_t *)&Bs[buf][t][4 * cq + c][4 * pq] = o[c];
-            }
-        }
-    };
-
-    load(0, 0);
-    store(0);
-    __syncthreads();
-    for (int ks = 0; ks < nsteps; ks++) {
-        const int cur = ks & 1;
-        const bool more = ks + 1 < nsteps;
-        if (more) load(ks + 1, cur ^ 1);
-        v4i bf[9];
-#pragma unroll
-        for (int t = 0; t < 9; t++) bf[t] = *(const v4i *)&Bs[cur][t][lane & 15][(lane >> 4) * 16];
-#pragma unroll
-        for (int l = 0; l < 4; l++) {
-            if (l < LA) {
-#pragma unroll
-                for (int t = 0; t < 9; t++)
-                    acc[l][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[cur][l], bf[t], acc[l][t], 0, 0, 0);
-            }
-        }
-        if (more) store(cur ^ 1);
-        __syncthreads();
-    }
-    // ---- combine limbs, store this chunk's partial tile
     int64_t *part = p.part + (int64_t)blockIdx.z * p.co * 9 * p.ci;
-#pragma unroll
-    for (int t = 0; t < 9; t++)
+    for (int lp = 0; lp < LA; lp += 2) {
+        const bool two = lp + 1 < LA;
+        int ph[4], pw[4], pidx[4];
 #pragma unroll
         for (int i = 0; i < 4; i++) {
-            const int co = co0 + wave * 16 + (lane >> 4) * 4 + i;
-            const int cin = ci0 + (lane & 15);
-            if (co >= p.co || cin >= p.ci) continue;
-            int64_t v = 0;
-#pragma unroll
-            for (int l = 0; l < 4; l++) v += (int64_t)acc[l][t][i] << (8 * l);
-            part[((int64_t)co * 9 + t) * p.ci + cin] = v;
+            const int pp = pb + 4 * pq + i;
+            const int rem = pp % HW;
+            pidx[i] = pp;
+            ph[i] = rem / p.w;
+            pw[i] = rem % p.w;
         }
+        v4i acc[2][9];
+#pragma unroll
+        for (int l = 0; l < 2; l++)
+#pragma unroll
+            for (int t = 0; t < 9; t++) acc[l][t] = v4i{0, 0, 0, 0};
+
+        v4i af[2][2];
+        uint32_t braw[3][4];
+        auto load = [&](int ks, int slot) {
+            const int k0 = ks * DW_BK;
+#pragma unroll
+            for (int l = 0; l < 2; l++)
+                af[slot][l] = (arow_ok && (l == 0 || two))
+                                  ? *(const v4i *)(abase + (lp + l) * aplane + k0)
+                                  : v4i{0, 0, 0, 0};
+#pragma unroll
+            for (int i = 0; i < 3; i++) {
+                const int t = wave + 4 * i;
+                const int dr = t / 3 - 1, ds = t % 3 - 1;
+#pragma unroll
+                for (int u = 0; u < 4; u++) {
+                    const int hh = ph[u] + dr, ww = pw[u] + ds;
+                    const bool ok = t < 9 && ci_ok && pidx[u] < pe && hh >= 0 && hh < p.h &&
+                                    ww >= 0 && ww < p.w;
+                    braw[i][u] = ok ? *(const uint32_t *)(xci + (pidx[u] + dr * p.w + ds) * p.ci) : 0u;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                pidx[u] += DW_BK;
+                pw[u] += adv_w;
+                ph[u] += adv_h;
+                if (pw[u] >= p.w) { pw[u] -= p.w; ph[u]++; }
+                if (ph[u] >= p.h) ph[u] %= p.h;
+            }
+        };
+        auto store = [&](int buf) {
+#pragma unroll
+            for (int i = 0; i < 3; i++) {
+                const int t = wave + 4 * i;
+                if (t < 9) {
+                    uint32_t o[4];
+                    transpose4x4(braw[i][0], braw[i][1], braw[i][2], braw[i][3], o[0], o[1], o[2], o[3]);
+#pragma unroll
+                    for (int c = 0; c < 4; c++) *(uint32_t *)&Bs[buf][t][4 * cq + c][4 * pq] = o[c];
+                }
+            }
+        };
+
+        load(0, 0);
+        store(0);
+        __syncthreads();
+        for (int ks = 0; ks < nsteps; ks++) {
+            const int cur = ks & 1;
+            const bool more = ks + 1 < nsteps;
+            if (more) load(ks + 1, cur ^ 1);
+            v4i bf[9];
+#pragma unroll
+            for (int t = 0; t < 9; t++) bf[t] = *(const v4i *)&Bs[cur][t][lane & 15][(lane >> 4) * 16];
+#pragma unroll
+            for (int t = 0; t < 9; t++)
+                acc[0][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[cur][0], bf[t], acc[0][t], 0, 0, 0);
+            if (two) {
+#pragma unroll
+                for (int t = 0; t < 9; t++)
+                    acc[1][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[cur][1], bf[t], acc[1][t], 0, 0, 0);
+            }
+            if (more) store(cur ^ 1);
+            __syncthreads();
+        }
+        // this chunk's partial tile: the first pass stores, a second pass (limbs 2, 3) adds
+#pragma unroll
+        for (int t = 0; t < 9; t++)
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const int co = co0 + wave * 16 + (lane >> 4) * 4 + i;
+                const int cin = ci0 + (lane & 15);
+                if (co < p.co && cin < p.ci) {
+                    const int64_t v = ((int64_t)acc[0][t][i] << (8 * lp)) +
+                                      ((int64_t)acc[1][t][i] << (8 * lp + 8));
+                    int64_t *dst = part + ((int64_t)co * 9 + t) * p.ci + cin;
+                    *dst = lp == 0 ? v : *dst + v;
+                }
+            }
+    }
+}
+
+// Weight gradient for few input channels (9 * C_in <= 64): the N dimension is the flattened
+// (tap, channel) column index of the KRSC weight row. Same A operand as k_conv_dw_mfma; the B tile
+// [column][pixel] is gathered byte by byte (each thread: one column, four pixels).
+__global__ __launch_bounds__(256) void k_conv_dw_mfma_smallc(DwArgs p)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t Bs[2][64][DW_LDS];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int LA = limbs_for(*p.gmax);
+    if (LA > 4) {
+        if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
+        return;
+    }
+    const int HW = p.h * p.w;
+    const int P = p.n * HW;
+    const int ncols = 9 * p.ci;
+    const int co0 = blockIdx.x * DW_BM;
+    const int pb = blockIdx.z * p.kc;
+    const int pe = pb + p.kc < P ? pb + p.kc : P;
+    const int nsteps = (pe - pb + DW_BK - 1) / DW_BK;
+    const int adv_h = DW_BK / p.w, adv_w = DW_BK % p.w;
+
+    const int arow = co0 + wave * 16 + (lane & 15);
+    const bool arow_ok = arow < p.co;
+    const int8_t *abase = p.gt + (int64_t)(arow_ok ? arow : 0) * p.pstride + pb + (lane >> 4) * 16;
+    const int64_t aplane = (int64_t)p.co * p.pstride;
+
+    // B tasks: column tid/16 + 16 i (i = 0..3), pixel quad tid % 16
+    const int pq = tid & 15;
+    int c_t[4], c_ci[4];
+    bool c_ok[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const int col = (tid >> 4) + 16 * i;
+        c_ok[i] = col < ncols;
+        c_t[i] = c_ok[i] ? col / p.ci : 0;
+        c_ci[i] = c_ok[i] ? col % p.ci : 0;
+    }
+
+    int64_t *part = p.part + (int64_t)blockIdx.z * p.co * ncols;
+    for (int lp = 0; lp < LA; lp += 2) {
+        const bool two = lp + 1 < LA;
+        int ph[4], pw[4], pidx[4];
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            const int pp = pb + 4 * pq + u;
+            const int rem = pp % HW;
+            pidx[u] = pp;
+            ph[u] = rem / p.w;
+            pw[u] = rem % p.w;
+        }
+        v4i acc[2][4];
+#pragma unroll
+        for (int l = 0; l < 2; l++)
+#pragma unroll
+            for (int j = 0; j < 4; j++) acc[l][j] = v4i{0, 0, 0, 0};
+        v4i af[2][2];
+        uint32_t braw[4];
+        auto load = [&](int ks, int slot) {
+            const int k0 = ks * DW_BK;
+#pragma unroll
+            for (int l = 0; l < 2; l++)
+                af[slot][l] = (arow_ok && (l == 0 || two))
+                                  ? *(const v4i *)(abase + (lp + l) * aplane + k0)
+                                  : v4i{0, 0, 0, 0};
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const int dr = c_t[i] / 3 - 1, ds = c_t[i] % 3 - 1;
+                uint32_t v = 0;
+#pragma unroll
+                for (int u = 0; u < 4; u++) {
+                    const int hh = ph[u] + dr, ww = pw[u] + ds;
+                    const bool ok = c_ok[i] && pidx[u] < pe && hh >= 0 && hh < p.h && ww >= 0 &&
+                                    ww < p.w;
+                    const uint32_t b = ok ? (uint32_t)(uint8_t)p.x[(pidx[u] + dr * p.w + ds) * p.ci + c_ci[i]] : 0u;
+                    v |= b << (8 * u);
+                }
+                braw[i] = v;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                pidx[u] += DW_BK;
+                pw[u] += adv_w;
+                ph[u] += adv_h;
+                if (pw[u] >= p.w) { pw[u] -= p.w; ph[u]++; }
+                if (ph[u] >= p.h) ph[u] %= p.h;
+            }
+        };
+        auto store = [&](int buf) {
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+                *(uint32_t *)&Bs[buf][(tid >> 4) + 16 * i][4 * pq] = braw[i];
+        };
+        load(0, 0);
+        store(0);
+        __syncthreads();
+        const int ntile = (ncols + 15) / 16;
+        for (int ks = 0; ks < nsteps; ks++) {
+            const int cur = ks & 1;
+            const bool more = ks + 1 < nsteps;
+            if (more) load(ks + 1, cur ^ 1);
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                if (j < ntile) {
+                    const v4i bf = *(const v4i *)&Bs[cur][16 * j + (lane & 15)][(lane >> 4) * 16];
+                    acc[0][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[cur][0], bf, acc[0][j], 0, 0, 0);
+                    if (two)
+                        acc[1][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[cur][1], bf, acc[1][j], 0, 0, 0);
+                }
+            }
+            if (more) store(cur ^ 1);
+            __syncthreads();
+        }
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const int co = co0 + wave * 16 + (lane >> 4) * 4 + i;
+                const int col = 16 * j + (lane & 15);
+                if (co < p.co && col < ncols) {
+                    const int64_t v = ((int64_t)acc[0][j][i] << (8 * lp)) +
+                                      ((int64_t)acc[1][j][i] << (8 * lp + 8));
+                    int64_t *dst = part + (int64_t)co * ncols + col;
+                    *dst = lp == 0 ? v : *dst + v;
+                }
+            }
+    }
+}
+
+bool mfma_conv_dw_smallc_ok(const ConvShape &sh)
+{
+    return 9 * sh.c <= 64 && sh.co % 4 == 0 &&
+           ((int64_t)sh.n * sh.h * sh.w + 2 * sh.w + 2) * sh.c < ((int64_t)1 << 31);
 }
 
 bool mfma_conv_dw_ok(const ConvShape &sh)
 {
-    return sh.c % 4 == 0 && sh.co % 4 == 0 && (int64_t)sh.n * sh.h * sh.w < ((int64_t)1 << 31) &&
-           sh.w < 65536 && sh.h < 65536;
+    // 32-bit pixel arithmetic: every x offset (pixel * channels) stays below 2^31
+    return sh.c % 4 == 0 && sh.co % 4 == 0 &&
+           ((int64_t)sh.n * sh.h * sh.w + 2 * sh.w + 2) * sh.c < ((int64_t)1 << 31);
 }
 
 int64_t dw_plane_stride(const ConvShape &sh)
@@ -579,12 +723,14 @@ int64_t dw_plane_stride(const ConvShape &sh)
     return (P + DW_BK - 1) / DW_BK * DW_BK;
 }
 
-// Split of the pixel dimension: about 512 workgroups in total, chunks of whole 64-pixel steps.
+// Split of the pixel dimension: about 512 workgroups in total (128 for few input channels,
+// whose partial tiles are few and short), chunks of whole 64-pixel steps.
 static void dw_split(const ConvShape &sh, int64_t *nz_out, int64_t *kc_out)
 {
     const int64_t P = (int64_t)sh.n * sh.h * sh.w;
-    const int tiles = ((sh.co + DW_BM - 1) / DW_BM) * ((sh.c + DW_BC - 1) / DW_BC);
-    int64_t nz = (512 + tiles - 1) / tiles;
+    const bool smallc = !mfma_conv_dw_ok(sh);
+    const int tiles = ((sh.co + DW_BM - 1) / DW_BM) * (smallc ? 1 : (sh.c + DW_BC - 1) / DW_BC);
+    int64_t nz = ((smallc ? 128 : 512) + tiles - 1) / tiles;
     const int64_t steps = (P + DW_BK - 1) / DW_BK;
     if (nz > steps) nz = steps;
     int64_t kc = ((steps + nz - 1) / nz) * DW_BK;
@@ -617,9 +763,16 @@ void launch_conv_dw_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g,
     a.n = sh.n; a.h = sh.h; a.w = sh.w; a.ci = sh.c; a.co = sh.co;
     a.gt = gt; a.pstride = ps; a.gmax = gmax; a.x = x; a.part = part; a.kc = (int)kc;
     a.flags = flags;
-    dim3 grid((unsigned)((sh.co + DW_BM - 1) / DW_BM), (unsigned)((sh.c + DW_BC - 1) / DW_BC),
-              (unsigned)nz);
-    hipLaunchKernelGGL(k_conv_dw_mfma, grid, dim3(256), 0, s, a);
+    if (mfma_conv_dw_ok(sh)) {
+        dim3 grid((unsigned)((sh.co + DW_BM - 1) / DW_BM), (unsigned)((sh.c + DW_BC - 1) / DW_BC),
+                  (unsigned)nz);
+        timer_begin(TIMED_DW_MFMA);
+        hipLaunchKernelGGL(k_conv_dw_mfma, grid, dim3(256), 0, s, a);
+        timer_end(TIMED_DW_MFMA);
+    } else {
+        dim3 grid((unsigned)((sh.co + DW_BM - 1) / DW_BM), 1, (unsigned)nz);
+        hipLaunchKernelGGL(k_conv_dw_mfma_smallc, grid, dim3(256), 0, s, a);
+    }
     launch_sum_partials(s, part, (int)nz, (int64_t)sh.co * 9 * sh.c, dw);
 }
 

@@ -173,7 +173,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_smallc(ConvShape sh, int chunk,
 static void smallc_dw_split(const ConvShape &sh, int64_t *nb_out, int64_t *chunk_out)
 {
     const int64_t P = (int64_t)sh.n * sh.h * sh.w;
-    int64_t nb = 512;
+    int64_t nb = 128;
     int64_t chunk = (P + nb - 1) / nb;
     chunk = (chunk + SC_PIX - 1) / SC_PIX * SC_PIX;
     *chunk_out = chunk;

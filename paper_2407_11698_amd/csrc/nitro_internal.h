@@ -149,6 +149,20 @@ inline unsigned grid_stride_blocks(int64_t n, int per = 256, unsigned cap = 2048
 }
 
 // ------------------------------------------------------------------------------------------
+// Optional per-kernel timing: launchers bracket the launches of the timed kernel classes with
+// begin/end; the API entry points install the calling context's timer for the duration of a
+// call (thread-local, so concurrent contexts on other threads are not affected).
+enum { TIMED_IGEMM_FWD = 0, TIMED_IGEMM_DX = 1, TIMED_DW_MFMA = 2, TIMED_CLASSES = 3 };
+struct LaunchTimer {
+    virtual void begin(int cls) = 0;
+    virtual void end(int cls) = 0;
+    virtual ~LaunchTimer() {}
+};
+extern thread_local LaunchTimer *g_timer;
+inline void timer_begin(int cls) { if (g_timer) g_timer->begin(cls); }
+inline void timer_end(int cls) { if (g_timer) g_timer->end(cls); }
+
+// ------------------------------------------------------------------------------------------
 // Kernel launchers (each enqueues on `s`; shapes are validated by the caller).
 // ------------------------------------------------------------------------------------------
 struct ConvShape {
@@ -231,6 +245,7 @@ void launch_conv_fwd_mfma(hipStream_t s, const ConvShape &sh, const int8_t *x, c
                           const uint32_t *wmax, const Div &sf, const Relu &rp, bool pool,
                           int8_t *out, uint8_t *code, uint32_t *flags);
 bool mfma_conv_dw_ok(const ConvShape &sh);
+bool mfma_conv_dw_smallc_ok(const ConvShape &sh);   // few input channels (9 C_in <= 64)
 // Row length of the pixel-contiguous gradient limb planes used by the weight gradient; the
 // scratch `gt` holds 4 * sh.co * dw_plane_stride(sh) bytes.
 int64_t dw_plane_stride(const ConvShape &sh);

@@ -85,6 +85,7 @@ def _load():
         "nitro_sync_status": (I32, [VP]),
         "nitro_status_str": (ctypes.c_char_p, [I32]),
         "nitro_block_query": (I32, [P(BlockDesc), P(ctypes.c_size_t)]),
+        "nitro_block_saved": (I32, [P(BlockDesc), VP, I32, P(VP), P(VP)]),
         "nitro_block_forward": (I32, [VP, P(BlockDesc), P(BlockParams), VP, VP, VP]),
         "nitro_block_backward": (I32, [VP, P(BlockDesc), P(BlockParams), VP, VP, VP, VP, VP,
                                        P(BlockGrads), P(BlockTaps)]),
@@ -109,7 +110,8 @@ LIB = _load()
 
 # every symbol the header declares (checked by the ABI tests)
 EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_sync_status",
-           "nitro_status_str", "nitro_block_query", "nitro_block_forward", "nitro_block_backward",
+           "nitro_status_str", "nitro_block_query", "nitro_block_saved", "nitro_block_forward",
+           "nitro_block_backward",
            "nitro_head_backward", "nitro_integer_sgd_step", "nitro_net_query",
            "nitro_net_block_output", "nitro_train_step", "nitro_host_div", "nitro_host_relu_mu",
            "nitro_kernel_timing", "nitro_kernel_time")
@@ -153,6 +155,15 @@ def block_query(desc: BlockDesc) -> int:
     out = ctypes.c_size_t(0)
     check(LIB.nitro_block_query(ctypes.byref(desc), ctypes.byref(out)), "nitro_block_query")
     return out.value
+
+
+def block_saved(desc: BlockDesc, state, j: int):
+    """(act, code) device pointers of forward layer j inside a block state tensor (act is None
+    for the last layer)."""
+    act, code = VP(), VP()
+    check(LIB.nitro_block_saved(ctypes.byref(desc), _p(state), j, ctypes.byref(act),
+                                ctypes.byref(code)), "nitro_block_saved")
+    return act.value, code.value
 
 
 def net_desc(blocks: Sequence[BlockDesc], head: bool) -> NetDesc:
