@@ -19,6 +19,10 @@ CFLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Wall",
     # packed fp32 instructions are kept out of every kernel (none of this code needs them)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in VGPRs: with the AGPR form the register allocator does not tie the
+    # accumulator operand to the result across loop iterations and copies every accumulator on
+    # every iteration (v_accvgpr_mov / read / write); the VGPR form keeps them in place
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-I", INCLUDE, "-I", CSRC,
 ]
 

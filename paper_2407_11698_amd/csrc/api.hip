@@ -95,6 +95,7 @@ struct BlockGeom {
     size_t wt[NITRO_MAX_LAYERS];   // conv: 4 int8 limb planes of W, [ci][9 co]
     size_t slots;                  // uint32 [8]: max|W_j| (0..3), max|g_j| (4..7)
     size_t gt;                     // weight-gradient scratch: pixel-contiguous limb planes of g
+    size_t xpl;                    // weight-gradient scratch: zero-padded planes of x
     size_t part;                   // weight-gradient scratch: split-K partial sums (int64)
     bool lr_mfma;                  // learning layer on the MFMA path
     size_t lwf, lwt, lft, lpart, lepad, let;   // its scratch
@@ -169,22 +170,25 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
         g->lepad = off; off = align256(off + (size_t)ls.epad_bytes);
         g->let = off;   off = align256(off + (size_t)ls.et_bytes);
     }
-    int64_t gtb = 0;
-    for (int j = 0; j < g->J; j++)
-        if (conv && (mfma_conv_dw_ok(g->L[j].sh) || mfma_conv_dw_smallc_ok(g->L[j].sh))) {
-            const int64_t b = 4 * (int64_t)g->L[j].sh.co * dw_plane_stride(g->L[j].sh);
-            if (b > gtb) gtb = b;
+    int64_t gtb = 0, xpb = 0, parts = 0;
+    for (int j = 0; j < g->J && conv; j++) {
+        const ConvShape &sh = g->L[j].sh;
+        int64_t b = 0, c = 0;
+        if (dwp_ok(sh)) {
+            b = dwp_gplane_bytes(sh);
+            c = dwp_partial_count(sh);
+            if (dwp_xplane_bytes(sh) > xpb) xpb = dwp_xplane_bytes(sh);
+        } else if (mfma_conv_dw_ok(sh) || mfma_conv_dw_smallc_ok(sh)) {
+            b = 4 * (int64_t)sh.co * dw_plane_stride(sh);
+            c = dw_partial_count(sh);
+        } else if (smallc_dw_ok(sh)) {
+            c = smallc_dw_partial_count(sh);
         }
-    g->gt = off; off = align256(off + (size_t)gtb);
-    int64_t parts = 0;
-    for (int j = 0; j < g->J; j++) {
-        if (!conv) continue;
-        int64_t c = 0;
-        if (mfma_conv_dw_ok(g->L[j].sh) || mfma_conv_dw_smallc_ok(g->L[j].sh))
-            c = dw_partial_count(g->L[j].sh);
-        else if (smallc_dw_ok(g->L[j].sh)) c = smallc_dw_partial_count(g->L[j].sh);
+        if (b > gtb) gtb = b;
         if (c > parts) parts = c;
     }
+    g->gt = off;  off = align256(off + (size_t)gtb);
+    g->xpl = off; off = align256(off + (size_t)xpb);
     g->part = off; off = align256(off + (size_t)parts * 8);
     const int64_t G = d->n_classes;
     g->yhat = off;  off = align256(off + (size_t)(d->n * G) * 4);
@@ -301,7 +305,11 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         const int8_t *xin = j == 0 ? x : (const int8_t *)at(state, g.act[j - 1]);
         const int32_t *gj = gb[cur];
         if (L.conv) {
-            if (mfma_conv_dw_ok(L.sh) || mfma_conv_dw_smallc_ok(L.sh))
+            if (dwp_ok(L.sh))
+                launch_conv_dw_planes(s, L.sh, gj, &slots[4 + j], xin, (int8_t *)at(state, g.gt),
+                                      (int8_t *)at(state, g.xpl), (int64_t *)at(state, g.part),
+                                      gr->dw[j], ctx->flags);
+            else if (mfma_conv_dw_ok(L.sh) || mfma_conv_dw_smallc_ok(L.sh))
                 launch_conv_dw_mfma(s, L.sh, gj, &slots[4 + j], xin, (int8_t *)at(state, g.gt),
                                     (int64_t *)at(state, g.part), gr->dw[j], ctx->flags);
             else if (smallc_dw_ok(L.sh))

@@ -1,0 +1,392 @@
+// Weight gradient of the 3x3 IntConv2D (section 3.2.1, 3x3 / stride 1 / pad 1 per Tab. 1) on
+// gfx950 int8 MFMA, exact:
+//   dW[co][r][s][ci] = sum_p g[p][co] * x[p + (r-1, s-1)][ci]          (int64)
+//
+// Padded pixel planes. Both operands are first rewritten pixel-contiguous on a zero-padded
+// grid: every image row is followed by one zero column and every image by one zero row, so pixel
+// (n, h, w) sits at position k = (n (H+1) + h) (W+1) + w and each neighbour outside the image
+// lands on a zero. A tap (r, s) is then the plain position offset (r-1)(W+1) + (s-1):
+//   dW[co][r][s][ci] = sum_k gp[co][k] * xp[ci][h0 + k + (r-1)(W+1) + (s-1)]
+// with no bounds test. gp holds the balanced int8 limbs of g (one plane per limb, zeros at pad
+// positions); xp holds x with a zero halo of h0 >= W + 2 positions on both sides.
+//
+// GEMM: M = co, N = ci (times 9 taps), K = padded positions. A workgroup owns a 64 co x 16 ci
+// tile, all 9 taps, over a range of K; its four waves split that range and run independently
+// (no barrier in the main loop). A fragments (g limbs) are loaded from the planes straight into
+// registers, one 256-position super-step ahead. The x window of a super-step (plus the halo) is
+// staged in the wave's own double-buffered LDS slice; the fragment of tap (r, s) is read from it
+// at byte offset h0 + (r-1)(W+1) + (s-1), and a funnel shift (v_alignbit) realigns the dwords.
+// The waves' int32 sums are added in int64 through LDS at the end. Each limb of g is one pass;
+// a wave's range is at most 128000 positions, so |sum| <= 128 * 128 * 128000 < 2^31.
+#include <type_traits>
+
+#include "mfma_common.h"
+
+namespace nitro {
+
+constexpr int DWP_KS = 256;        // padded positions per super-step (4 MFMA K-steps of 64)
+constexpr int DWP_HMAX = 64;       // largest halo: W <= 62
+constexpr int DWP_CHUNK_MAX = 2000;   // super-steps per workgroup (a wave: <= 500 * 256)
+constexpr int DWP_WIN = DWP_KS + 2 * DWP_HMAX;   // staged window of a super-step (bytes/row)
+constexpr int DWP_RS = DWP_WIN + 4;             // its LDS row stride: an odd number of dwords
+constexpr int DWP_NCH = 16 * DWP_WIN / 16 / 64;  // 16-byte chunks per lane (16 rows, 64 lanes)
+
+struct DwpGeom {
+    int wp, hp;          // W + 1, H + 1
+    int h0;              // halo (multiple of 16, >= W + 2)
+    int64_t kraw;        // positions of the padded grid: n (H+1) (W+1)
+    int64_t kp;          // positions processed (kraw rounded up to a super-step)
+    int64_t xs;          // row length of an x plane (multiple of 64, >= kp + 2 HMAX)
+};
+
+DwpGeom dwp_geom(const ConvShape &sh)
+{
+    DwpGeom g;
+    g.wp = sh.w + 1;
+    g.hp = sh.h + 1;
+    g.h0 = (g.wp + 1 + 15) / 16 * 16;
+    g.kraw = (int64_t)sh.n * g.hp * g.wp;
+    g.kp = (g.kraw + DWP_KS - 1) / DWP_KS * DWP_KS;
+    g.xs = g.kp + DWP_WIN - DWP_KS;   // the last super-step's window ends there
+    return g;
+}
+
+bool dwp_ok(const ConvShape &sh)
+{
+    if (sh.c % 16 || sh.co % 16 || sh.w + 2 > DWP_HMAX) return false;
+    const DwpGeom g = dwp_geom(sh);
+    // 32-bit offsets inside the planes and in the preparation kernels
+    const int64_t lim = (int64_t)1 << 31;
+    return (int64_t)sh.c * g.xs < lim && 4 * (int64_t)sh.co * g.kp < lim &&
+           (int64_t)sh.n * sh.h * sh.w * sh.co < lim && (int64_t)sh.n * sh.h * sh.w * sh.c < lim;
+}
+
+struct DwpPlan {
+    int tiles_co, tiles_ci, nss, chunk, nsplit;
+};
+
+// About one workgroup per compute unit; at least 8 super-steps (2 per wave) per workgroup.
+static DwpPlan dwp_plan(const ConvShape &sh)
+{
+    const DwpGeom g = dwp_geom(sh);
+    DwpPlan p;
+    p.tiles_co = (sh.co + 63) / 64;
+    p.tiles_ci = sh.c / 16;
+    p.nss = (int)(g.kp / DWP_KS);
+    const int tiles = p.tiles_co * p.tiles_ci;
+    int s = (256 + tiles - 1) / tiles;
+    const int smax = p.nss / 8 > 1 ? p.nss / 8 : 1;
+    if (s > smax) s = smax;
+    p.chunk = (p.nss + s - 1) / s;
+    if (p.chunk > DWP_CHUNK_MAX) p.chunk = DWP_CHUNK_MAX;
+    p.nsplit = (p.nss + p.chunk - 1) / p.chunk;
+    return p;
+}
+
+int64_t dwp_partial_count(const ConvShape &sh)
+{
+    const DwpPlan p = dwp_plan(sh);
+    return p.nsplit > 1 ? (int64_t)p.nsplit * sh.co * 9 * sh.c : 0;
+}
+
+int64_t dwp_gplane_bytes(const ConvShape &sh) { return 4 * (int64_t)sh.co * dwp_geom(sh).kp; }
+int64_t dwp_xplane_bytes(const ConvShape &sh) { return (int64_t)sh.c * dwp_geom(sh).xs; }
+
+// Position k of the padded grid -> NHWC pixel index, or -1 at a pad position.
+__device__ inline int padded_pixel(int k, int n, int h, int w, int hp, int wp)
+{
+    if (k < 0) return -1;
+    const int per = hp * wp;
+    const int img = k / per;
+    const int rem = k - img * per;
+    const int hh = rem / wp, ww = rem - hh * wp;
+    if (img >= n || hh >= h || ww >= w) return -1;
+    return (img * h + hh) * w + ww;
+}
+
+// ---------------------------------------------------------------------------------------------
+// x int8 NHWC [P][C] -> xp [C][xs], xp[c][h0 + k] = x at padded position k (zeros elsewhere).
+// A workgroup: 64 plane positions x 64 channels, transposed through LDS.
+__global__ __launch_bounds__(256) void k_dwp_act_planes(const int8_t *__restrict__ x, int n, int h,
+                                                        int w, int c, int hp, int wp, int h0,
+                                                        int xs, int8_t *__restrict__ xp)
+{
+    __shared__ uint32_t T[64][17];       // [position][channel dword]
+    const int tid = threadIdx.x;
+    const int i0 = blockIdx.x * 64;
+    const int c0 = blockIdx.y * 64;
+    {
+        const int pi = tid >> 2, cq = tid & 3;
+        const int pix = padded_pixel(i0 + pi - h0, n, h, w, hp, wp);
+        v4i v = v4i{0, 0, 0, 0};
+        if (pix >= 0 && c0 + 16 * cq < c) v = *(const v4i *)(x + (int64_t)pix * c + c0 + 16 * cq);
+#pragma unroll
+        for (int u = 0; u < 4; u++) T[pi][4 * cq + u] = (uint32_t)v[u];
+    }
+    __syncthreads();
+    const int cc = tid >> 2, pq = tid & 3;
+    if (c0 + cc >= c) return;
+    v4i o;
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        uint32_t d = 0;
+#pragma unroll
+        for (int b = 0; b < 4; b++)
+            d |= ((T[16 * pq + 4 * q + b][cc >> 2] >> (8 * (cc & 3))) & 0xFFu) << (8 * b);
+        o[q] = (int)d;
+    }
+    *(v4i *)(xp + (int64_t)(c0 + cc) * xs + i0 + 16 * pq) = o;
+}
+
+// g int32 NHWC [P][C] -> gp [l][C][kp] for l < limbs(max|g|): limb l of g at padded position k
+// (zeros at pad positions). A workgroup: 64 positions x 64 channels, transposed through LDS.
+__global__ __launch_bounds__(256) void k_dwp_grad_planes(const int32_t *__restrict__ g, int n,
+                                                         int h, int w, int c, int hp, int wp,
+                                                         int kp, const uint32_t *gmax,
+                                                         int8_t *__restrict__ gp)
+{
+    __shared__ int32_t T[64][65];        // [position][channel]
+    const int LA = limbs_for(*gmax);
+    if (LA > 4) return;                  // the weight-gradient kernel flags it
+    const int tid = threadIdx.x;
+    const int k0 = blockIdx.x * 64;
+    const int c0 = blockIdx.y * 64;
+    {
+        const int pi = tid >> 2, cq = tid & 3;
+        const int pix = padded_pixel(k0 + pi, n, h, w, hp, wp);
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            const int ch = c0 + 16 * cq + 4 * u;
+            v4i v = v4i{0, 0, 0, 0};
+            if (pix >= 0 && ch < c) v = *(const v4i *)(g + (int64_t)pix * c + ch);
+#pragma unroll
+            for (int e = 0; e < 4; e++) T[pi][16 * cq + 4 * u + e] = v[e];
+        }
+    }
+    __syncthreads();
+    const int cc = tid >> 2, pq = tid & 3;
+    if (c0 + cc >= c) return;
+    int32_t v[16];
+#pragma unroll
+    for (int e = 0; e < 16; e++) v[e] = T[16 * pq + e][cc];
+#pragma unroll
+    for (int l = 0; l < 4; l++) {
+        if (l < LA) {
+            v4i o;
+#pragma unroll
+            for (int q = 0; q < 4; q++)
+                o[q] = (int)limb4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3], l);
+            *(v4i *)(gp + ((int64_t)l * c + c0 + cc) * kp + k0 + 16 * pq) = o;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
+struct DwpArgs {
+    const int8_t *gp;      // [LA][co][kp]
+    int64_t kp;
+    const int8_t *xp;      // [ci][xs]
+    int64_t xs;
+    int h0, wp, co, ci;
+    int tiles_ci, tiles_co, nss, chunk;
+    const uint32_t *gmax;
+    int64_t *out;          // [nsplit][co][9][ci]; dW itself when there is one split
+    uint32_t *flags;
+};
+
+// bits [b, b + 32) of the 64-bit value hi:lo (v_alignbit_b32), 0 <= b < 32
+__device__ inline uint32_t funnel_shr(uint32_t hi, uint32_t lo, uint32_t bits)
+{
+    return __builtin_amdgcn_alignbit(hi, lo, bits);
+}
+
+// Wave-local LDS hand-off: this wave's LDS writes are complete before its later reads, and the
+// compiler keeps memory accesses on their side of it.
+__device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+__global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
+{
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int LA = limbs_for(*p.gmax);
+    if (LA > 4) {
+        if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
+        return;
+    }
+    // Work item. Workgroups of one K range (they read the same g rows) get consecutive numbers
+    // and, as the dispatcher deals workgroups round-robin to the 8 XCDs, one XCD (one L2).
+    const int nwg = gridDim.x;
+    int wid = blockIdx.x;
+    if ((nwg & 7) == 0) wid = (wid & 7) * (nwg >> 3) + (wid >> 3);
+    const int tci = wid % p.tiles_ci;
+    const int rest = wid / p.tiles_ci;
+    const int tco = rest % p.tiles_co;
+    const int split = rest / p.tiles_co;
+    const int co0 = tco * 64, ci0 = tci * 16;
+
+    // this wave's super-steps
+    const int sb = split * p.chunk;
+    const int se = sb + p.chunk < p.nss ? sb + p.chunk : p.nss;
+    const int per = (se - sb + 3) >> 2;
+    const int wb = sb + wave * per < se ? sb + wave * per : se;
+    const int nst = (wb + per < se ? wb + per : se) - wb;
+
+    constexpr int RS = DWP_RS, CR = DWP_WIN / 16;
+    uint8_t *wl = lds + wave * (2 * 16 * RS);  // this wave's two stages [16 rows][RS]
+
+    const int j = lane & 15, g4 = lane >> 4;
+    // 32-bit offsets from the plane bases (the host checks that both fit)
+    const uint32_t plane = (uint32_t)p.co * (uint32_t)p.kp;
+    // co rows past the end (a partial last tile) read row co - 1; their sums are not stored
+    uint32_t aoff[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const int row = co0 + 16 * i + j < p.co ? co0 + 16 * i + j : p.co - 1;
+        aoff[i] = (uint32_t)row * (uint32_t)p.kp + 16 * g4;
+    }
+    // staged chunks of this lane: chunk lane + 64 m of the 16 x CR window
+    const int8_t *xbase = p.xp + (int64_t)ci0 * p.xs;
+    uint32_t boff[DWP_NCH];
+    int bdst[DWP_NCH];
+#pragma unroll
+    for (int m = 0; m < DWP_NCH; m++) {
+        const int c = lane + 64 * m;
+        const int row = c / CR, col = c - row * CR;
+        boff[m] = (uint32_t)row * (uint32_t)p.xs + 16 * col;
+        bdst[m] = row * RS + 16 * col;
+    }
+    // tap (r, s): byte offset o = h0 + (r-1) wp + (s-1) >= 0 of its fragment in the window
+    int tq[9];
+    uint32_t tsh[9];
+#pragma unroll
+    for (int t = 0; t < 9; t++) {
+        const int o = p.h0 + (t / 3 - 1) * p.wp + (t % 3 - 1);
+        tq[t] = o >> 2;
+        tsh[t] = (uint32_t)(o & 3) * 8;
+    }
+    const int lane_b = j * RS + 16 * g4;
+
+    v4i acc[9][4];
+    v4i a[4][4];                 // A fragments [K-step][co tile]
+    v4i bst[DWP_NCH];
+
+    auto load_a = [&](int u, int ss, int l) {
+        const uint32_t k = (uint32_t)ss * DWP_KS + (uint32_t)l * plane + 64 * u;
+#pragma unroll
+        for (int i = 0; i < 4; i++) a[u][i] = *(const v4i *)(p.gp + (aoff[i] + k));
+    };
+    auto load_b = [&](int ss) {
+        const uint32_t k = (uint32_t)ss * DWP_KS;
+#pragma unroll
+        for (int m = 0; m < DWP_NCH; m++) bst[m] = *(const v4i *)(xbase + (boff[m] + k));
+    };
+    auto store_b = [&](int stage) {
+        uint8_t *dst = wl + stage * 16 * RS;
+#pragma unroll
+        for (int m = 0; m < DWP_NCH; m++) {
+            uint32_t *d = (uint32_t *)(dst + bdst[m]);
+            d[0] = (uint32_t)bst[m][0];
+            d[1] = (uint32_t)bst[m][1];
+            d[2] = (uint32_t)bst[m][2];
+            d[3] = (uint32_t)bst[m][3];
+        }
+    };
+    // one super-step from LDS stage `stage`; with RELOAD each K-step's A fragments are reloaded
+    // for super-step `next` as soon as they are used
+    auto compute = [&](auto reload, int stage, int next, int l) {
+        const uint8_t *base = wl + stage * 16 * RS + lane_b;
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+#pragma unroll
+            for (int t = 0; t < 9; t++) {
+                const uint32_t *s = (const uint32_t *)(base + 64 * u) + tq[t];
+                const uint32_t d0 = s[0], d1 = s[1], d2 = s[2], d3 = s[3], d4 = s[4];
+                v4i b;
+                b[0] = (int)funnel_shr(d1, d0, tsh[t]);
+                b[1] = (int)funnel_shr(d2, d1, tsh[t]);
+                b[2] = (int)funnel_shr(d3, d2, tsh[t]);
+                b[3] = (int)funnel_shr(d4, d3, tsh[t]);
+#pragma unroll
+                for (int i = 0; i < 4; i++)
+                    acc[t][i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[u][i], b, acc[t][i], 0, 0, 0);
+            }
+            if (decltype(reload)::value) load_a(u, next, l);
+        }
+    };
+
+    for (int l = 0; l < LA; l++) {
+#pragma unroll
+        for (int t = 0; t < 9; t++)
+#pragma unroll
+            for (int i = 0; i < 4; i++) acc[t][i] = v4i{0, 0, 0, 0};
+        if (nst > 0) {
+#pragma unroll
+            for (int u = 0; u < 4; u++) load_a(u, wb, l);
+            load_b(wb);
+            store_b(0);
+            wave_lds_sync();
+            for (int s = 0; s + 1 < nst; s++) {
+                load_b(wb + s + 1);
+                compute(std::true_type(), s & 1, wb + s + 1, l);
+                store_b((s + 1) & 1);
+                wave_lds_sync();
+            }
+            compute(std::false_type(), (nst - 1) & 1, 0, l);
+        }
+        // sum of the four waves (int64) -> this split's tile; limb l carries weight 256^l
+        __syncthreads();
+        int32_t *red = (int32_t *)lds;        // [wave][3 taps][64 co][16 ci]
+        const int64_t wl_ = (int64_t)1 << (8 * l);
+#pragma unroll
+        for (int t0 = 0; t0 < 9; t0 += 3) {
+#pragma unroll
+            for (int tt = 0; tt < 3; tt++)
+#pragma unroll
+                for (int i = 0; i < 4; i++)
+#pragma unroll
+                    for (int r = 0; r < 4; r++)
+                        red[((wave * 3 + tt) * 64 + 16 * i + 4 * g4 + r) * 16 + j] = acc[t0 + tt][i][r];
+            __syncthreads();
+            for (int e = tid; e < 3 * 1024; e += 256) {
+                const int tt = e >> 10, co = co0 + ((e >> 4) & 63), ci = ci0 + (e & 15);
+                int64_t v = 0;
+#pragma unroll
+                for (int w = 0; w < 4; w++) v += red[(w * 3 + tt) * 1024 + (e & 1023)];
+                if (co < p.co && ci < p.ci) {
+                    int64_t *dst = p.out + (((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci + ci;
+                    *dst = l == 0 ? v * wl_ : *dst + v * wl_;
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
+                           const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
+                           int64_t *part, int64_t *dw, uint32_t *flags)
+{
+    const DwpGeom ge = dwp_geom(sh);
+    const DwpPlan pl = dwp_plan(sh);
+    hipLaunchKernelGGL(k_dwp_act_planes, dim3((unsigned)(ge.xs / 64), (unsigned)((sh.c + 63) / 64)),
+                       dim3(256), 0, s, x, sh.n, sh.h, sh.w, sh.c, ge.hp, ge.wp, ge.h0, (int)ge.xs, xp);
+    hipLaunchKernelGGL(k_dwp_grad_planes, dim3((unsigned)(ge.kp / 64), (unsigned)((sh.co + 63) / 64)),
+                       dim3(256), 0, s, g, sh.n, sh.h, sh.w, sh.co, ge.hp, ge.wp, (int)ge.kp, gmax, gp);
+    DwpArgs a{};
+    a.gp = gp; a.kp = ge.kp;
+    a.xp = xp; a.xs = ge.xs;
+    a.h0 = ge.h0; a.wp = ge.wp; a.co = sh.co; a.ci = sh.c;
+    a.tiles_ci = pl.tiles_ci; a.tiles_co = pl.tiles_co; a.nss = pl.nss; a.chunk = pl.chunk;
+    a.gmax = gmax;
+    a.out = pl.nsplit > 1 ? part : dw;
+    a.flags = flags;
+    const size_t lds_stage = (size_t)4 * 2 * 16 * DWP_RS, lds_red = (size_t)4 * 3 * 1024 * 4;
+    const unsigned nwg = (unsigned)(pl.tiles_co * pl.tiles_ci * pl.nsplit);
+    timer_begin(TIMED_DW_MFMA);
+    hipLaunchKernelGGL(k_conv_dw_planes, dim3(nwg), dim3(256), lds_stage > lds_red ? lds_stage : lds_red,
+                       s, a);
+    timer_end(TIMED_DW_MFMA);
+    if (pl.nsplit > 1) launch_sum_partials(s, part, pl.nsplit, (int64_t)sh.co * 9 * sh.c, dw);
+}
+
+}  // namespace nitro

@@ -766,9 +766,7 @@ void launch_conv_dw_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g,
     if (mfma_conv_dw_ok(sh)) {
         dim3 grid((unsigned)((sh.co + DW_BM - 1) / DW_BM), (unsigned)((sh.c + DW_BC - 1) / DW_BC),
                   (unsigned)nz);
-        timer_begin(TIMED_DW_MFMA);
         hipLaunchKernelGGL(k_conv_dw_mfma, grid, dim3(256), 0, s, a);
-        timer_end(TIMED_DW_MFMA);
     } else {
         dim3 grid((unsigned)((sh.co + DW_BM - 1) / DW_BM), 1, (unsigned)nz);
         hipLaunchKernelGGL(k_conv_dw_mfma_smallc, grid, dim3(256), 0, s, a);

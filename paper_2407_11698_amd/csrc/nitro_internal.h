@@ -152,6 +152,7 @@ inline unsigned grid_stride_blocks(int64_t n, int per = 256, unsigned cap = 2048
 // Optional per-kernel timing: launchers bracket the launches of the timed kernel classes with
 // begin/end; the API entry points install the calling context's timer for the duration of a
 // call (thread-local, so concurrent contexts on other threads are not affected).
+// classes: 0 k_igemm_conv forward, 1 k_igemm_conv input gradient, 2 k_conv_dw_planes
 enum { TIMED_IGEMM_FWD = 0, TIMED_IGEMM_DX = 1, TIMED_DW_MFMA = 2, TIMED_CLASSES = 3 };
 struct LaunchTimer {
     virtual void begin(int cls) = 0;
@@ -255,6 +256,16 @@ int64_t dw_partial_count(const ConvShape &sh);
 void launch_conv_dw_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g,
                          const uint32_t *gmax, const int8_t *x, int8_t *gt, int64_t *part,
                          int64_t *dw, uint32_t *flags);
+// ---- weight gradient over zero-padded pixel planes (conv_dw.hip): C_in and C_out multiples of
+// 16, W <= 62. Scratch: gp (dwp_gplane_bytes), xp (dwp_xplane_bytes), part (dwp_partial_count
+// int64 words; none when the pixel range is not split).
+bool dwp_ok(const ConvShape &sh);
+int64_t dwp_gplane_bytes(const ConvShape &sh);
+int64_t dwp_xplane_bytes(const ConvShape &sh);
+int64_t dwp_partial_count(const ConvShape &sh);
+void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
+                           const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
+                           int64_t *part, int64_t *dw, uint32_t *flags);
 void launch_conv_dx_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g, const uint32_t *gmax_in,
                          const int8_t *wt, const uint32_t *wmax, const uint8_t *prev_code,
                          const Relu &rp, int32_t *gout, int64_t *out64, uint32_t *gmax_out,
