@@ -30,7 +30,7 @@ PEAK_INT8_TOPS = 5000.0          # dense int8 MFMA, TOP/s
 PEAK_HBM_GBS = 8000.0
 
 # timed kernel classes of the library (nitro_kernel_time) and the HIP kernels they bracket
-KERNEL_CLASSES = {0: "k_igemm_conv<fwd>", 1: "k_igemm_conv<dx>", 2: "k_conv_dw_planes"}
+KERNEL_CLASSES = {0: "k_conv_tile<fwd>", 1: "k_conv_tile<dx>", 2: "k_conv_dw_planes"}
 
 
 def conv_layer_ops(wl):
@@ -40,10 +40,10 @@ def conv_layer_ops(wl):
     A layer with N*H*W output pixels, C_in inputs and C_out outputs has N*H*W*C_out*9*C_in MACs
     in each of its forward, input-gradient and weight-gradient GEMMs. The input gradient is
     computed for every layer but the first of a block (nothing leaves a block). The library
-    routes a layer to the timed kernels when its shape fits them (forward: C_in a multiple of
-    16; input gradient: C_out a multiple of 16; weight gradient: both multiples of 16 and
-    W <= 62); the first layer of an RGB network (C_in = 3) uses other kernels and is not
-    counted."""
+    routes a layer to the timed kernels when its shape fits them (forward and input gradient:
+    128 % W == 0 and the GEMM's K channels 16, 32 or a multiple of 64, an input with fewer than
+    16 channels being zero-padded to 16; weight gradient: C_out a multiple of 16 and W <= 62).
+    Only the layer's own MACs are counted, not the padding."""
     from paper_2407_11698_amd.workloads import Conv3x3
     ops = {name: 0 for name in KERNEL_CLASSES.values()}
     for (inp, _), blk in zip(wl.block_shapes(), wl.blocks):
@@ -53,11 +53,13 @@ def conv_layer_ops(wl):
         for j, ly in enumerate(blk.layers):
             macs = wl.batch * h * w * ly.c_out * 9 * ly.c_in
             pool = blk.maxpool and j == len(blk.layers) - 1
-            if ly.c_in % 16 == 0 and (not pool or 128 % (2 * w) == 0):
-                ops["k_igemm_conv<fwd>"] += 2 * macs
-            if j > 0 and ly.c_out % 16 == 0:
-                ops["k_igemm_conv<dx>"] += 2 * macs
-            if ly.c_in % 16 == 0 and ly.c_out % 16 == 0 and w <= 62:
+            tiles = 128 % w == 0
+            kok = lambda c: c in (16, 32) or c % 64 == 0
+            if tiles and (kok(ly.c_in) or ly.c_in < 16) and ly.c_out % 16 == 0:
+                ops["k_conv_tile<fwd>"] += 2 * macs
+            if j > 0 and tiles and kok(ly.c_out) and ly.c_in % 16 == 0:
+                ops["k_conv_tile<dx>"] += 2 * macs
+            if ly.c_out % 16 == 0 and w <= 62:
                 ops["k_conv_dw_planes"] += 2 * macs
     return ops
 

@@ -81,6 +81,9 @@ struct LayerGeom {
     int64_t in_elems;         // per batch
     int64_t out_elems;        // full resolution, per batch
     int64_t sf;               // 2^8 * fan_in
+    bool pad16;               // forward on the MFMA GEMM with C_in zero-padded to 16
+    bool fwd_tile;            // forward on k_conv_tile (with the padded input when pad16)
+    bool dx_tile;             // input gradient on k_conv_tile (g's NHWC limb planes from dW)
 };
 
 struct BlockGeom {
@@ -91,11 +94,13 @@ struct BlockGeom {
     // state buffer offsets
     size_t act[NITRO_MAX_LAYERS];
     size_t code[NITRO_MAX_LAYERS];
-    size_t wf[NITRO_MAX_LAYERS];   // conv: 4 int8 limb planes of W, [co][9 ci]
+    size_t wf[NITRO_MAX_LAYERS];   // conv: 4 int8 limb planes of W, [co][9 ci] (ci padded: 16)
     size_t wt[NITRO_MAX_LAYERS];   // conv: 4 int8 limb planes of W, [ci][9 co]
-    size_t slots;                  // uint32 [8]: max|W_j| (0..3), max|g_j| (4..7)
+    size_t slots;                  // max slots: |W_j| (0..3), |g_j| (4..7), |W_lr| (8), |e| (9)
     size_t gt;                     // weight-gradient scratch: pixel-contiguous limb planes of g
     size_t xpl;                    // weight-gradient scratch: zero-padded planes of x
+    size_t xpad;                   // forward scratch: a layer input with channels padded to 16
+    size_t gnl;                    // backward scratch: NHWC limb planes of g [4][P][co]
     size_t part;                   // weight-gradient scratch: split-K partial sums (int64)
     bool lr_mfma;                  // learning layer on the MFMA path
     size_t lwf, lwt, lft, lpart, lepad, let;   // its scratch
@@ -131,6 +136,16 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
         L.in_elems = hw * ly.c_in;
         L.out_elems = hw * ly.c_out;
         L.sf = 256 * (int64_t)(conv ? 9 * ly.c_in : ly.c_in);
+        const bool pool = j == d->n_layers - 1 && d->maxpool;
+        L.pad16 = L.fwd_tile = L.dx_tile = false;
+        if (conv) {
+            ConvShape s16 = L.sh;
+            if (ly.c_in < 16) s16.c = 16;
+            L.fwd_tile = tile_conv_fwd_ok(s16, pool, L.sf, d->alpha_inv);
+            L.pad16 = ly.c_in < 16 && (L.fwd_tile || mfma_conv_fwd_ok(s16, pool));
+            if (ly.c_in < 16 && !L.pad16) L.fwd_tile = false;
+            L.dx_tile = dwp_ok(L.sh) && tile_conv_dx_ok(L.sh);
+        }
         c = ly.c_out;
     }
     // the elementwise kernels index activations and weights with 32-bit arithmetic
@@ -153,12 +168,16 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
         off = align256(off + (size_t)(last ? (d->maxpool ? g->out_elems : full) : full));
         if (full > gmax) gmax = full;
     }
+    int64_t xpadb = 0;
     for (int j = 0; j < g->J; j++) {
         const int64_t nw = conv ? 9 * (int64_t)d->layer[j].c_in * d->layer[j].c_out : 0;
-        g->wf[j] = off; off = align256(off + (size_t)(4 * nw));
+        const int64_t nwf = g->L[j].pad16 ? 9 * 16 * (int64_t)d->layer[j].c_out : nw;
+        g->wf[j] = off; off = align256(off + (size_t)(4 * nwf));
         g->wt[j] = off; off = align256(off + (size_t)(4 * nw));
+        if (g->L[j].pad16 && (int64_t)d->n * hw * 16 > xpadb) xpadb = (int64_t)d->n * hw * 16;
     }
-    g->slots = off; off = align256(off + 16 * 4);
+    g->xpad = off; off = align256(off + (size_t)xpadb);
+    g->slots = off; off = align256(off + 16 * SLOT_WORDS * 4);
     g->lr_mfma = d->n_classes > 0 && mfma_learning_ok(d->n, g->d, d->n_classes);
     {
         LearningScratch ls{};
@@ -170,10 +189,12 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
         g->lepad = off; off = align256(off + (size_t)ls.epad_bytes);
         g->let = off;   off = align256(off + (size_t)ls.et_bytes);
     }
-    int64_t gtb = 0, xpb = 0, parts = 0;
+    int64_t gtb = 0, xpb = 0, parts = 0, gnb = 0;
     for (int j = 0; j < g->J && conv; j++) {
         const ConvShape &sh = g->L[j].sh;
         int64_t b = 0, c = 0;
+        if (g->L[j].dx_tile && 4 * (int64_t)sh.n * sh.h * sh.w * sh.co > gnb)
+            gnb = 4 * (int64_t)sh.n * sh.h * sh.w * sh.co;
         if (dwp_ok(sh)) {
             b = dwp_gplane_bytes(sh);
             c = dwp_partial_count(sh);
@@ -189,6 +210,7 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     }
     g->gt = off;  off = align256(off + (size_t)gtb);
     g->xpl = off; off = align256(off + (size_t)xpb);
+    g->gnl = off; off = align256(off + (size_t)gnb);
     g->part = off; off = align256(off + (size_t)parts * 8);
     const int64_t G = d->n_classes;
     g->yhat = off;  off = align256(off + (size_t)(d->n * G) * 4);
@@ -202,10 +224,7 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
 
 Relu make_relu(int alpha_inv, int round)
 {
-    Relu r;
-    r.alpha = make_div(alpha_inv, round);
-    r.mu = nitro_host_relu_mu(alpha_inv, round);
-    return r;
+    return make_relu_params(alpha_inv, nitro_host_relu_mu(alpha_inv, round), round);
 }
 
 inline uint8_t *at(void *base, size_t off) { return (uint8_t *)base + off; }
@@ -217,7 +236,7 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
     hipStream_t s = ctx->stream;
     const Relu rp = make_relu(desc->alpha_inv, desc->round);
     uint32_t *slots = (uint32_t *)at(state, g.slots);
-    if (hipMemsetAsync(slots, 0, 8 * 4, s) != hipSuccess) return NITRO_EHIP;
+    if (hipMemsetAsync(slots, 0, 8 * SLOT_WORDS * 4, s) != hipSuccess) return NITRO_EHIP;
     const int8_t *cur = x;
     for (int j = 0; j < g.J; j++) {
         const LayerGeom &L = g.L[j];
@@ -228,10 +247,26 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
         const Div sf = make_div(L.sf, desc->round);
         if (L.conv) {
             // limb planes for this call's forward and input-gradient GEMMs, and max|W_j|
-            launch_pack_conv_weights(s, p->w[j], L.sh.co, L.sh.c, (int8_t *)at(state, g.wf[j]),
-                                     (int8_t *)at(state, g.wt[j]), &slots[j]);
-            if (mfma_conv_fwd_ok(L.sh, pool))
-                launch_conv_fwd_mfma(s, L.sh, cur, (const int8_t *)at(state, g.wf[j]), &slots[j],
+            launch_pack_conv_weights(s, p->w[j], L.sh.co, L.sh.c, L.pad16 ? 16 : L.sh.c,
+                                     (int8_t *)at(state, g.wf[j]),
+                                     (int8_t *)at(state, g.wt[j]), slots + (j) * SLOT_WORDS);
+            const int8_t *wf = (const int8_t *)at(state, g.wf[j]);
+            uint32_t *wmax = slots + j * SLOT_WORDS;
+            ConvShape sx = L.sh;
+            const int8_t *xin = cur;
+            if (L.pad16) {
+                int8_t *xpad = (int8_t *)at(state, g.xpad);
+                launch_pad_channels16(s, cur, L.sh.n * L.sh.h * L.sh.w, L.sh.c, xpad);
+                sx.c = 16;
+                xin = xpad;
+            }
+            if (L.fwd_tile)
+                launch_conv_fwd_tile(s, sx, xin, wf, wmax, L.sf, desc->alpha_inv, desc->round, rp,
+                                     pool, out, code, ctx->flags);
+            else if (L.pad16)
+                launch_conv_fwd_mfma(s, sx, xin, wf, wmax, sf, rp, pool, out, code, ctx->flags);
+            else if (mfma_conv_fwd_ok(L.sh, pool))
+                launch_conv_fwd_mfma(s, L.sh, cur, (const int8_t *)at(state, g.wf[j]), slots + (j) * SLOT_WORDS,
                                      sf, rp, pool, out, code, ctx->flags);
             else if (smallc_fwd_ok(L.sh))
                 launch_conv_fwd_smallc(s, L.sh, cur, p->w[j], sf, rp, pool, out, code);
@@ -260,7 +295,8 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
     const LayerGeom &LJ = g.L[J - 1];
     uint32_t *slots = (uint32_t *)at(state, g.slots);
     // max|g_j| (4..7), max|W_lr| (8), max|e| (9) are produced by this call
-    if (hipMemsetAsync(slots + 4, 0, 6 * 4, s) != hipSuccess) return NITRO_EHIP;
+    if (hipMemsetAsync(slots + 4 * SLOT_WORDS, 0, 6 * SLOT_WORDS * 4, s) != hipSuccess)
+        return NITRO_EHIP;
     bool have_g = false;
     if (G > 0) {
         int32_t *yhat = (int32_t *)at(state, g.yhat);
@@ -274,9 +310,9 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
             lb.part = (int64_t *)at(state, g.lpart);
             lb.epad = (int32_t *)at(state, g.lepad);
             lb.et = (int32_t *)at(state, g.let);
-            lb.wmax = &slots[8];
-            lb.emax = &slots[9];
-            lb.gmax = &slots[4 + J - 1];
+            lb.wmax = slots + (8) * SLOT_WORDS;
+            lb.emax = slots + (9) * SLOT_WORDS;
+            lb.gmax = slots + (4 + J - 1) * SLOT_WORDS;
             launch_learning_mfma(s, n, g.d, G, a_out, p->w_lr, sf, labels, lb,
                                  at(state, g.code[J - 1]), rp, LJ.sh.h, LJ.sh.w, LJ.sh.co,
                                  desc->maxpool != 0, gb[0], taps ? taps->delta : nullptr, yhat, e,
@@ -298,19 +334,21 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
     }
     if (!have_g)
         launch_unpool_relu_bwd(s, n, LJ.sh.h, LJ.sh.w, LJ.sh.co, desc->maxpool != 0, delta,
-                               at(state, g.code[J - 1]), rp, gb[0], &slots[4 + J - 1], ctx->flags);
+                               at(state, g.code[J - 1]), rp, gb[0], slots + (4 + J - 1) * SLOT_WORDS, ctx->flags);
     int cur = 0;
     for (int j = J - 1; j >= 0; j--) {
         const LayerGeom &L = g.L[j];
         const int8_t *xin = j == 0 ? x : (const int8_t *)at(state, g.act[j - 1]);
         const int32_t *gj = gb[cur];
         if (L.conv) {
+            const bool need_dx = j > 0 || (taps && taps->dx);
             if (dwp_ok(L.sh))
-                launch_conv_dw_planes(s, L.sh, gj, &slots[4 + j], xin, (int8_t *)at(state, g.gt),
-                                      (int8_t *)at(state, g.xpl), (int64_t *)at(state, g.part),
-                                      gr->dw[j], ctx->flags);
+                launch_conv_dw_planes(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, xin,
+                                      (int8_t *)at(state, g.gt), (int8_t *)at(state, g.xpl),
+                                      L.dx_tile && need_dx ? (int8_t *)at(state, g.gnl) : nullptr,
+                                      (int64_t *)at(state, g.part), gr->dw[j], ctx->flags);
             else if (mfma_conv_dw_ok(L.sh) || mfma_conv_dw_smallc_ok(L.sh))
-                launch_conv_dw_mfma(s, L.sh, gj, &slots[4 + j], xin, (int8_t *)at(state, g.gt),
+                launch_conv_dw_mfma(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, xin, (int8_t *)at(state, g.gt),
                                     (int64_t *)at(state, g.part), gr->dw[j], ctx->flags);
             else if (smallc_dw_ok(L.sh))
                 launch_conv_dw_smallc(s, L.sh, gj, xin, (int64_t *)at(state, g.part), gr->dw[j]);
@@ -331,11 +369,16 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
             dst64 = taps->dx;
         }
         if (dst || dst64) {
-            uint32_t *gmax_out = j > 0 ? &slots[4 + j - 1] : nullptr;
+            uint32_t *gmax_out = j > 0 ? slots + (4 + j - 1) * SLOT_WORDS : nullptr;
             if (L.conv) {
-                if (mfma_conv_dx_ok(L.sh))
-                    launch_conv_dx_mfma(s, L.sh, gj, &slots[4 + j], (const int8_t *)at(state, g.wt[j]),
-                                        &slots[j], code, rp, dst, dst64, gmax_out, ctx->flags);
+                if (L.dx_tile)
+                    launch_conv_dx_tile(s, L.sh, (const int8_t *)at(state, g.gnl),
+                                        slots + (4 + j) * SLOT_WORDS,
+                                        (const int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS,
+                                        code, rp, dst, dst64, gmax_out, ctx->flags);
+                else if (mfma_conv_dx_ok(L.sh))
+                    launch_conv_dx_mfma(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, (const int8_t *)at(state, g.wt[j]),
+                                        slots + (j) * SLOT_WORDS, code, rp, dst, dst64, gmax_out, ctx->flags);
                 else
                     launch_conv_dx(s, L.sh, gj, p->w[j], code, rp, dst, dst64, gmax_out, ctx->flags);
             } else {

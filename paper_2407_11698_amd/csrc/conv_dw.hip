@@ -51,13 +51,17 @@ DwpGeom dwp_geom(const ConvShape &sh)
     return g;
 }
 
+// Input channels are computed in multiples of 16: a layer with C_in % 16 != 0 gets zero x
+// planes up to the next multiple (their weight-gradient columns are computed and dropped).
+static int dwp_c16(const ConvShape &sh) { return (sh.c + 15) / 16 * 16; }
+
 bool dwp_ok(const ConvShape &sh)
 {
-    if (sh.c % 16 || sh.co % 16 || sh.w + 2 > DWP_HMAX) return false;
+    if (sh.c < 1 || sh.co % 16 || sh.w + 2 > DWP_HMAX) return false;
     const DwpGeom g = dwp_geom(sh);
     // 32-bit offsets inside the planes and in the preparation kernels
     const int64_t lim = (int64_t)1 << 31;
-    return (int64_t)sh.c * g.xs < lim && 4 * (int64_t)sh.co * g.kp < lim &&
+    return (int64_t)dwp_c16(sh) * g.xs < lim && 4 * (int64_t)sh.co * g.kp < lim &&
            (int64_t)sh.n * sh.h * sh.w * sh.co < lim && (int64_t)sh.n * sh.h * sh.w * sh.c < lim;
 }
 
@@ -71,7 +75,7 @@ static DwpPlan dwp_plan(const ConvShape &sh)
     const DwpGeom g = dwp_geom(sh);
     DwpPlan p;
     p.tiles_co = (sh.co + 63) / 64;
-    p.tiles_ci = sh.c / 16;
+    p.tiles_ci = dwp_c16(sh) / 16;
     p.nss = (int)(g.kp / DWP_KS);
     const int tiles = p.tiles_co * p.tiles_ci;
     int s = (256 + tiles - 1) / tiles;
@@ -90,7 +94,7 @@ int64_t dwp_partial_count(const ConvShape &sh)
 }
 
 int64_t dwp_gplane_bytes(const ConvShape &sh) { return 4 * (int64_t)sh.co * dwp_geom(sh).kp; }
-int64_t dwp_xplane_bytes(const ConvShape &sh) { return (int64_t)sh.c * dwp_geom(sh).xs; }
+int64_t dwp_xplane_bytes(const ConvShape &sh) { return (int64_t)dwp_c16(sh) * dwp_geom(sh).xs; }
 
 // Position k of the padded grid -> NHWC pixel index, or -1 at a pad position.
 __device__ inline int padded_pixel(int k, int n, int h, int w, int hp, int wp)
@@ -105,11 +109,12 @@ __device__ inline int padded_pixel(int k, int n, int h, int w, int hp, int wp)
 }
 
 // ---------------------------------------------------------------------------------------------
-// x int8 NHWC [P][C] -> xp [C][xs], xp[c][h0 + k] = x at padded position k (zeros elsewhere).
-// A workgroup: 64 plane positions x 64 channels, transposed through LDS.
+// x int8 NHWC [P][C] -> xp [C16][xs], xp[c][h0 + k] = x at padded position k (zeros elsewhere
+// and in channels C..C16-1). A workgroup: 64 plane positions x 64 channels, transposed through
+// LDS.
 __global__ __launch_bounds__(256) void k_dwp_act_planes(const int8_t *__restrict__ x, int n, int h,
-                                                        int w, int c, int hp, int wp, int h0,
-                                                        int xs, int8_t *__restrict__ xp)
+                                                        int w, int c, int c16, int hp, int wp,
+                                                        int h0, int xs, int8_t *__restrict__ xp)
 {
     __shared__ uint32_t T[64][17];       // [position][channel dword]
     const int tid = threadIdx.x;
@@ -118,14 +123,20 @@ __global__ __launch_bounds__(256) void k_dwp_act_planes(const int8_t *__restrict
     {
         const int pi = tid >> 2, cq = tid & 3;
         const int pix = padded_pixel(i0 + pi - h0, n, h, w, hp, wp);
+        const int ch = c0 + 16 * cq;
         v4i v = v4i{0, 0, 0, 0};
-        if (pix >= 0 && c0 + 16 * cq < c) v = *(const v4i *)(x + (int64_t)pix * c + c0 + 16 * cq);
+        if ((c & 15) == 0) {
+            if (pix >= 0 && ch < c) v = *(const v4i *)(x + (int64_t)pix * c + ch);
+        } else if (pix >= 0) {
+            for (int e = 0; e < 16 && ch + e < c; e++)
+                v[e >> 2] |= (int)((uint32_t)(uint8_t)x[(int64_t)pix * c + ch + e] << (8 * (e & 3)));
+        }
 #pragma unroll
         for (int u = 0; u < 4; u++) T[pi][4 * cq + u] = (uint32_t)v[u];
     }
     __syncthreads();
     const int cc = tid >> 2, pq = tid & 3;
-    if (c0 + cc >= c) return;
+    if (c0 + cc >= c16) return;
     v4i o;
 #pragma unroll
     for (int q = 0; q < 4; q++) {
@@ -139,14 +150,17 @@ __global__ __launch_bounds__(256) void k_dwp_act_planes(const int8_t *__restrict
 }
 
 // g int32 NHWC [P][C] -> gp [l][C][kp] for l < limbs(max|g|): limb l of g at padded position k
-// (zeros at pad positions). A workgroup: 64 positions x 64 channels, transposed through LDS.
+// (zeros at pad positions); when gn is not null also the NHWC limb planes gn [l][P][C] (the A
+// operand of the input-gradient GEMM). A workgroup: 64 positions x 64 channels, transposed
+// through LDS.
 __global__ __launch_bounds__(256) void k_dwp_grad_planes(const int32_t *__restrict__ g, int n,
                                                          int h, int w, int c, int hp, int wp,
                                                          int kp, const uint32_t *gmax,
-                                                         int8_t *__restrict__ gp)
+                                                         int8_t *__restrict__ gp,
+                                                         int8_t *__restrict__ gn)
 {
     __shared__ int32_t T[64][65];        // [position][channel]
-    const int LA = limbs_for(*gmax);
+    const int LA = limbs_for(slot_read(gmax));
     if (LA > 4) return;                  // the weight-gradient kernel flags it
     const int tid = threadIdx.x;
     const int k0 = blockIdx.x * 64;
@@ -154,13 +168,30 @@ __global__ __launch_bounds__(256) void k_dwp_grad_planes(const int32_t *__restri
     {
         const int pi = tid >> 2, cq = tid & 3;
         const int pix = padded_pixel(k0 + pi, n, h, w, hp, wp);
+        int32_t v[16];
 #pragma unroll
         for (int u = 0; u < 4; u++) {
             const int ch = c0 + 16 * cq + 4 * u;
-            v4i v = v4i{0, 0, 0, 0};
-            if (pix >= 0 && ch < c) v = *(const v4i *)(g + (int64_t)pix * c + ch);
+            v4i x = v4i{0, 0, 0, 0};
+            if (pix >= 0 && ch < c) x = *(const v4i *)(g + (int64_t)pix * c + ch);
 #pragma unroll
-            for (int e = 0; e < 4; e++) T[pi][16 * cq + 4 * u + e] = v[e];
+            for (int e = 0; e < 4; e++) {
+                v[4 * u + e] = x[e];
+                T[pi][16 * cq + 4 * u + e] = x[e];
+            }
+        }
+        if (gn && pix >= 0 && c0 + 16 * cq < c) {
+            const int64_t P = (int64_t)n * h * w;
+#pragma unroll
+            for (int l = 0; l < 4; l++) {
+                if (l < LA) {
+                    v4i o;
+#pragma unroll
+                    for (int q = 0; q < 4; q++)
+                        o[q] = (int)limb4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3], l);
+                    *(v4i *)(gn + (int64_t)l * P * c + (int64_t)pix * c + c0 + 16 * cq) = o;
+                }
+            }
         }
     }
     __syncthreads();
@@ -187,10 +218,11 @@ struct DwpArgs {
     int64_t kp;
     const int8_t *xp;      // [ci][xs]
     int64_t xs;
-    int h0, wp, co, ci;
+    int h0, wp, co, ci;          // ci: computed input channels (a multiple of 16)
+    int ci_out;                  // input channels of dW (<= ci)
     int tiles_ci, tiles_co, nss, chunk;
     const uint32_t *gmax;
-    int64_t *out;          // [nsplit][co][9][ci]; dW itself when there is one split
+    int64_t *out;          // [nsplit][co][9][ci_out]; dW itself when there is one split
     uint32_t *flags;
 };
 
@@ -208,7 +240,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 {
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int LA = limbs_for(*p.gmax);
+    const int LA = limbs_for(slot_read(p.gmax));
     if (LA > 4) {
         if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
         return;
@@ -352,8 +384,8 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
                 int64_t v = 0;
 #pragma unroll
                 for (int w = 0; w < 4; w++) v += red[(w * 3 + tt) * 1024 + (e & 1023)];
-                if (co < p.co && ci < p.ci) {
-                    int64_t *dst = p.out + (((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci + ci;
+                if (co < p.co && ci < p.ci_out) {
+                    int64_t *dst = p.out + (((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci_out + ci;
                     *dst = l == 0 ? v * wl_ : *dst + v * wl_;
                 }
             }
@@ -364,18 +396,21 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
-                           int64_t *part, int64_t *dw, uint32_t *flags)
+                           int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags)
 {
     const DwpGeom ge = dwp_geom(sh);
     const DwpPlan pl = dwp_plan(sh);
-    hipLaunchKernelGGL(k_dwp_act_planes, dim3((unsigned)(ge.xs / 64), (unsigned)((sh.c + 63) / 64)),
-                       dim3(256), 0, s, x, sh.n, sh.h, sh.w, sh.c, ge.hp, ge.wp, ge.h0, (int)ge.xs, xp);
+    const int c16 = dwp_c16(sh);
+    hipLaunchKernelGGL(k_dwp_act_planes, dim3((unsigned)(ge.xs / 64), (unsigned)((c16 + 63) / 64)),
+                       dim3(256), 0, s, x, sh.n, sh.h, sh.w, sh.c, c16, ge.hp, ge.wp, ge.h0,
+                       (int)ge.xs, xp);
     hipLaunchKernelGGL(k_dwp_grad_planes, dim3((unsigned)(ge.kp / 64), (unsigned)((sh.co + 63) / 64)),
-                       dim3(256), 0, s, g, sh.n, sh.h, sh.w, sh.co, ge.hp, ge.wp, (int)ge.kp, gmax, gp);
+                       dim3(256), 0, s, g, sh.n, sh.h, sh.w, sh.co, ge.hp, ge.wp, (int)ge.kp, gmax, gp,
+                       gn);
     DwpArgs a{};
     a.gp = gp; a.kp = ge.kp;
     a.xp = xp; a.xs = ge.xs;
-    a.h0 = ge.h0; a.wp = ge.wp; a.co = sh.co; a.ci = sh.c;
+    a.h0 = ge.h0; a.wp = ge.wp; a.co = sh.co; a.ci = c16; a.ci_out = sh.c;
     a.tiles_ci = pl.tiles_ci; a.tiles_co = pl.tiles_co; a.nss = pl.nss; a.chunk = pl.chunk;
     a.gmax = gmax;
     a.out = pl.nsplit > 1 ? part : dw;

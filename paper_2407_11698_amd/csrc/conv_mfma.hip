@@ -19,16 +19,23 @@
 namespace nitro {
 
 // ---------------------------------------------------------------------------------------------
-// Weight packing: W int32 KRSC [co][3][3][ci] -> 4 limb planes of [co][9 ci] (forward) and,
-// when wt != null, of [ci][9 co] with the same tap order (input gradient); max|W| -> *wmax.
-// Two passes, each with coalesced stores: the forward planes in W's own order, the swapped
-// planes in their order (gathering W through the cache).
-__global__ void k_pack_conv_weights(const int32_t *__restrict__ w, uint32_t total,
-                                    int8_t *__restrict__ wf, uint32_t *wmax)
+// Weight packing: W int32 KRSC [co][3][3][ci] -> 4 limb planes of [co][9 cpad] (forward; input
+// channels ci..cpad-1 are zeros) and, when wt != null, of [ci][9 co] with the same tap order
+// (input gradient); max|W| -> the max slot wmax. Two passes, each with coalesced stores: the
+// forward planes in W's own order, the swapped planes in their order (gathering W through the
+// cache).
+__global__ void k_pack_conv_weights(const int32_t *__restrict__ w, uint32_t total, int ci,
+                                    int cpad, int8_t *__restrict__ wf, uint32_t *wmax)
 {
     uint32_t m = 0;
     for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
-        const int32_t v = w[i];
+        int32_t v;
+        if (cpad == ci) {
+            v = w[i];
+        } else {
+            const uint32_t c = i % (uint32_t)cpad, row = i / (uint32_t)cpad;
+            v = (int)c < ci ? w[row * ci + c] : 0;
+        }
         const uint32_t a = abs_u32(v);
         m = a > m ? a : m;
 #pragma unroll
@@ -50,16 +57,36 @@ __global__ void k_pack_conv_weights_t(const int32_t *__restrict__ w, uint32_t co
     for (int l = 0; l < 4; l++) wt[(int64_t)l * total + ti] = limb1(v, l);
 }
 
-void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,
-                              int8_t *wt, uint32_t *wmax)
+void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, int cpad,
+                              int8_t *wf, int8_t *wt, uint32_t *wmax)
 {
     const uint32_t total = (uint32_t)co * 9 * (uint32_t)ci;
+    const uint32_t total_pad = (uint32_t)co * 9 * (uint32_t)cpad;
     const dim3 grid((total + 255) / 256);
-    hipLaunchKernelGGL(k_pack_conv_weights, dim3(grid_stride_blocks(total)), dim3(256), 0, s, w,
-                       total, wf, wmax);
+    hipLaunchKernelGGL(k_pack_conv_weights, dim3(grid_stride_blocks(total_pad)), dim3(256), 0, s,
+                       w, total_pad, ci, cpad, wf, wmax);
     if (wt)
         hipLaunchKernelGGL(k_pack_conv_weights_t, grid, dim3(256), 0, s, w, (uint32_t)co,
                            (uint32_t)ci, wt);
+}
+
+// x int8 [P][c] -> [P][16] with zero channels c..15 (c < 16): the forward GEMM's K then takes
+// whole 16-channel chunks per tap.
+__global__ __launch_bounds__(256) void k_pad_channels16(const int8_t *__restrict__ x, int P, int c,
+                                                        int8_t *__restrict__ xpad)
+{
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    if (p >= P) return;
+    v4i v = v4i{0, 0, 0, 0};
+    for (int e = 0; e < c; e++)
+        v[e >> 2] |= (int)((uint32_t)(uint8_t)x[(int64_t)p * c + e] << (8 * (e & 3)));
+    *(v4i *)(xpad + (int64_t)p * 16) = v;
+}
+
+void launch_pad_channels16(hipStream_t s, const int8_t *x, int P, int c, int8_t *xpad)
+{
+    hipLaunchKernelGGL(k_pad_channels16, dim3((unsigned)((P + 255) / 256)), dim3(256), 0, s, x, P,
+                       c, xpad);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -117,8 +144,8 @@ __global__ __launch_bounds__(256) void k_igemm_conv(IgemmArgs p)
     const int K = 9 * p.ck;
     const int ksteps = (K + IG_BK - 1) / IG_BK;
 
-    const int LA = MODE == IG_FWD ? 1 : limbs_for(*p.a_max);
-    const int LB = limbs_for(*p.b_max);
+    const int LA = MODE == IG_FWD ? 1 : limbs_for(slot_read(p.a_max));
+    const int LB = limbs_for(slot_read(p.b_max));
     if (LA > 4 || LB > 4) {
         if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
         return;
@@ -404,7 +431,7 @@ __global__ __launch_bounds__(256) void k_grad_limb_planes(const int32_t *__restr
                                                           const uint32_t *gmax,
                                                           int8_t *__restrict__ gt)
 {
-    const int LA = limbs_for(*gmax);
+    const int LA = limbs_for(slot_read(gmax));
     const int cq4 = (C + 3) / 4;
     const int64_t pq4 = pstride / 4;
     const int64_t task = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -452,7 +479,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_mfma(DwArgs p)
     __shared__ __attribute__((aligned(16))) uint8_t Bs[2][9][DW_BC][DW_LDS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int LA = limbs_for(*p.gmax);
+    const int LA = limbs_for(slot_read(p.gmax));
     if (LA > 4) {
         if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
         return;
@@ -583,7 +610,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_mfma_smallc(DwArgs p)
     __shared__ __attribute__((aligned(16))) uint8_t Bs[2][64][DW_LDS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int LA = limbs_for(*p.gmax);
+    const int LA = limbs_for(slot_read(p.gmax));
     if (LA > 4) {
         if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
         return;

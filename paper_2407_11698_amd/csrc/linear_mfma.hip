@@ -52,8 +52,8 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     const int kb = blockIdx.z * p.kchunk;
     const int ke = kb + p.kchunk < p.K ? kb + p.kchunk : p.K;
     const int ksteps = (ke - kb + LG_BK - 1) / LG_BK;
-    const int LA = A32 ? limbs_for(*p.a_max) : 1;
-    const int LB = p.b_max ? limbs_for(*p.b_max) : 1;
+    const int LA = A32 ? limbs_for(slot_read(p.a_max)) : 1;
+    const int LB = p.b_max ? limbs_for(slot_read(p.b_max)) : 1;
     if (LA > 4 || LB > 4) {
         if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
         return;

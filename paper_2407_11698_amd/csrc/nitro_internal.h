@@ -69,6 +69,8 @@ __host__ __device__ inline int64_t idiv(int64_t n, const Div &v)
 struct Relu {
     Div alpha;        // alpha_inv
     int32_t mu;
+    uint32_t a32_m;   // 32-bit reciprocal of alpha_inv (Div32 fields), for |values| < 2^32
+    int32_t a32_l;
 };
 
 enum : uint8_t { REG_PASS = 0, REG_SLOPE = 1, REG_ZERO = 2 };
@@ -85,11 +87,151 @@ __device__ inline int32_t relu_fwd(int64_t zs, const Relu &rp, uint8_t &region)
     return (int32_t)(c - rp.mu);
 }
 
+
+// The same method for 32-bit numerators (n < 2^32, 1 <= d < 2^32): m fits 32 bits and the sum
+// t + n is formed in 64 bits. Used where a value is known to be small.
+struct Div32 {
+    uint32_t m;
+    int32_t l;
+};
+
+inline Div32 make_div32(uint32_t d)
+{
+    Div32 r;
+    int l = 0;
+    while (l < 32 && ((uint64_t)1 << l) < d) l++;
+    r.m = (uint32_t)((((uint64_t)1 << 32) * (((uint64_t)1 << l) - d)) / d + 1);
+    r.l = l;
+    return r;
+}
+
+__host__ __device__ inline uint32_t udiv32(uint32_t n, const Div32 &v)
+{
+#if defined(__HIP_DEVICE_COMPILE__)
+    const uint32_t t = __umulhi(v.m, n);
+#else
+    const uint32_t t = (uint32_t)(((uint64_t)v.m * n) >> 32);
+#endif
+    return (uint32_t)(((uint64_t)t + n) >> v.l);
+}
+
+// NITRO-Scaling followed by NITRO-ReLU, with 32-bit division. The quotient z / SF only matters
+// exactly while it lies in [-128, 128]; beyond, both rounding modes give a saturated region and
+// the clamped value. So z >= 128 SF and z <= -128 SF are decided by comparison, and every other
+// z has |z| < 128 SF <= 2^32 (required of SF by make_scale_relu's caller).
+struct ScaleRelu {
+    Div32 sf, alpha;
+    int64_t lim;          // 128 * SF
+    int32_t mu;
+    int32_t trunc;
+};
+
+inline ScaleRelu make_scale_relu(int64_t sf, int64_t alpha_inv, int32_t mu, int round)
+{
+    ScaleRelu q;
+    q.sf = make_div32((uint32_t)sf);
+    q.alpha = make_div32((uint32_t)alpha_inv);
+    q.lim = 128 * sf;
+    q.mu = mu;
+    q.trunc = round == NITRO_ROUND_TRUNC;
+    return q;
+}
+
+inline bool scale_relu_ok(int64_t sf, int64_t alpha_inv)
+{
+    return sf >= 1 && 128 * sf <= ((int64_t)1 << 32) && alpha_inv >= 1 && alpha_inv < ((int64_t)1 << 31);
+}
+
+// floor or trunc of -n / d for 0 < n < 2^32
+__host__ __device__ inline int32_t neg_div32(uint32_t n, const Div32 &d, int trunc)
+{
+    return trunc ? -(int32_t)udiv32(n, d) : -1 - (int32_t)udiv32(n - 1, d);
+}
+
+__host__ __device__ inline int32_t scale_relu(int64_t z, const ScaleRelu &q, uint8_t &region)
+{
+    int32_t zs;
+    if (z >= q.lim) zs = 128;
+    else if (z <= -q.lim) zs = -128;
+    else if (z >= 0) zs = (int32_t)udiv32((uint32_t)z, q.sf);
+    else zs = neg_div32((uint32_t)(-z), q.sf, q.trunc);
+    if (zs < 0) {
+        region = zs >= -127 ? REG_SLOPE : REG_ZERO;
+        const int32_t c = zs < -127 ? -127 : zs;
+        return neg_div32((uint32_t)(-c), q.alpha, q.trunc) - q.mu;
+    }
+    region = zs <= 127 ? REG_PASS : REG_ZERO;
+    return (zs > 127 ? 127 : zs) - q.mu;
+}
+
+inline Relu make_relu_params(int64_t alpha_inv, int32_t mu, int round)
+{
+    Relu r;
+    r.alpha = make_div(alpha_inv, round);
+    r.mu = mu;
+    const Div32 a = make_div32((uint32_t)alpha_inv);
+    r.a32_m = a.m;
+    r.a32_l = a.l;
+    return r;
+}
+
 __device__ inline int64_t relu_bwd(int64_t delta, uint8_t region, const Relu &rp)
 {
     if (region == REG_PASS) return delta;
-    if (region == REG_SLOPE) return idiv(delta, rp.alpha);
+    if (region == REG_SLOPE) {
+        const Div32 a{rp.a32_m, rp.a32_l};
+        const int64_t lim = (int64_t)1 << 32;
+        if (delta >= 0 && delta < lim) return udiv32((uint32_t)delta, a);
+        if (delta < 0 && delta > -lim) return neg_div32((uint32_t)(-delta), a, rp.alpha.trunc);
+        return idiv(delta, rp.alpha);
+    }
     return 0;
+}
+
+// Branch-free NITRO-Scaling + NITRO-ReLU of an int32 pre-activation (the workgroup's sums fit
+// int32). Both divisions use the round-up method without the 33-bit sum:
+// q = (t + ((n - t) >> 1)) >> (l - 1), t = mulhi(m, n), valid for divisors >= 2.
+struct ScaleRelu32 {
+    uint32_t sf_m, a_m;
+    int32_t sf_l, a_l;
+    int32_t mu;
+    int32_t trunc;
+};
+
+inline ScaleRelu32 make_scale_relu32(int64_t sf, int64_t alpha_inv, int32_t mu, int round)
+{
+    const Div32 a = make_div32((uint32_t)sf), b = make_div32((uint32_t)alpha_inv);
+    return ScaleRelu32{a.m, b.m, a.l, b.l, mu, round == NITRO_ROUND_TRUNC};
+}
+
+inline bool scale_relu32_ok(int64_t sf, int64_t alpha_inv)
+{
+    return sf >= 2 && sf < ((int64_t)1 << 31) && alpha_inv >= 2 && alpha_inv < ((int64_t)1 << 31);
+}
+
+__host__ __device__ inline uint32_t udiv32_nf(uint32_t n, uint32_t m, int l)
+{
+#if defined(__HIP_DEVICE_COMPILE__)
+    const uint32_t t = __umulhi(m, n);
+#else
+    const uint32_t t = (uint32_t)(((uint64_t)m * n) >> 32);
+#endif
+    return (t + ((n - t) >> 1)) >> (l - 1);
+}
+
+__host__ __device__ inline int32_t scale_relu32(int32_t z, const ScaleRelu32 &q, uint8_t &region)
+{
+    const int32_t sg = z >> 31;                                   // 0 or -1
+    // floor: n = ~z for z < 0 and zs = ~q; trunc: n = -z and zs = -q
+    const uint32_t n = q.trunc ? (uint32_t)((z ^ sg) - sg) : (uint32_t)(z ^ sg);
+    const uint32_t d = udiv32_nf(n, q.sf_m, q.sf_l);
+    const int32_t zs = q.trunc ? (((int32_t)d ^ sg) - sg) : ((int32_t)d ^ sg);
+    const int32_t c = zs < -127 ? -127 : (zs > 127 ? 127 : zs);
+    region = c != zs ? REG_ZERO : (c < 0 ? REG_SLOPE : REG_PASS);
+    const uint32_t n2 = q.trunc ? (uint32_t)(-c) : (uint32_t)(~c);  // used only when c < 0
+    const int32_t d2 = (int32_t)udiv32_nf(n2, q.a_m, q.a_l);
+    const int32_t neg = q.trunc ? -d2 : ~d2;
+    return (c < 0 ? neg : c) - q.mu;
 }
 
 // Sticky status flags written by kernels (bit or).
@@ -116,8 +258,13 @@ __device__ inline uint32_t wave_max_u32(uint32_t v)
     return v;
 }
 
-// Workgroup-wide maximum folded into a device slot with one atomic per workgroup. Every thread
-// of the workgroup must call it (it contains a barrier); at most 1024 threads.
+// A max slot is SLOT_WORDS words: a workgroup folds its maximum into word (workgroup index mod
+// SLOT_WORDS), so that concurrent workgroups seldom meet on one address (same-address device
+// atomics serialise across the XCDs), and a reader takes the maximum over the words.
+constexpr int SLOT_WORDS = 64;
+
+// Workgroup-wide maximum folded into a max slot with one atomic per workgroup. Every thread of
+// the workgroup must call it (it contains a barrier); at most 1024 threads.
 __device__ inline void block_slot_max(uint32_t *slot, uint32_t m)
 {
     __shared__ uint32_t red[16];
@@ -127,8 +274,16 @@ __device__ inline void block_slot_max(uint32_t *slot, uint32_t m)
     if (threadIdx.x == 0) {
         uint32_t r = 0;
         for (unsigned w = 0; w < (blockDim.x + 63) / 64; w++) r = red[w] > r ? red[w] : r;
-        slot_max(slot, r);
+        const unsigned b = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+        slot_max(slot + b % SLOT_WORDS, r);
     }
+}
+
+// The value of a max slot. Every lane of the calling wave must be active.
+__device__ inline uint32_t slot_read(const uint32_t *slot)
+{
+    static_assert(SLOT_WORDS == 64, "one word per lane");
+    return wave_max_u32(slot[threadIdx.x & 63]);
 }
 
 __device__ inline uint32_t abs_u32(int32_t v) { return v < 0 ? (uint32_t)(-(int64_t)v) : (uint32_t)v; }
@@ -238,10 +393,12 @@ void launch_conv_dw_smallc(hipStream_t s, const ConvShape &sh, const int32_t *g,
 // ---- int8 MFMA implicit-GEMM path (conv_mfma.hip)
 bool mfma_conv_fwd_ok(const ConvShape &sh, bool pool);
 bool mfma_conv_dx_ok(const ConvShape &sh);
-// W int32 KRSC -> 4 balanced int8 limb planes [co][9 ci] (wf) and [ci][9 co] (wt, optional);
-// max|W| -> *wmax (atomic max: the slot must be zeroed first).
-void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,
-                              int8_t *wt, uint32_t *wmax);
+// W int32 KRSC -> 4 balanced int8 limb planes [co][9 cpad] (wf; channels ci..cpad-1 zero) and
+// [ci][9 co] (wt, optional); max|W| -> the max slot wmax (zeroed first).
+void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, int cpad,
+                              int8_t *wf, int8_t *wt, uint32_t *wmax);
+// x int8 [P][c] (c < 16) -> [P][16], channels c..15 zero.
+void launch_pad_channels16(hipStream_t s, const int8_t *x, int P, int c, int8_t *xpad);
 void launch_conv_fwd_mfma(hipStream_t s, const ConvShape &sh, const int8_t *x, const int8_t *wf,
                           const uint32_t *wmax, const Div &sf, const Relu &rp, bool pool,
                           int8_t *out, uint8_t *code, uint32_t *flags);
@@ -263,9 +420,22 @@ bool dwp_ok(const ConvShape &sh);
 int64_t dwp_gplane_bytes(const ConvShape &sh);
 int64_t dwp_xplane_bytes(const ConvShape &sh);
 int64_t dwp_partial_count(const ConvShape &sh);
+// gn (optional): also write g's NHWC limb planes [4][P][co] (the input-gradient tile kernel's A).
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
-                           int64_t *part, int64_t *dw, uint32_t *flags);
+                           int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags);
+
+// ---- implicit-GEMM conv with the input tile staged once (conv_tile.hip)
+bool tile_conv_fwd_ok(const ConvShape &sh, bool pool, int64_t sf, int alpha_inv);
+bool tile_conv_dx_ok(const ConvShape &sh);
+void launch_conv_fwd_tile(hipStream_t s, const ConvShape &sh, const int8_t *x, const int8_t *wf,
+                          const uint32_t *wmax, int64_t sf, int alpha_inv, int round,
+                          const Relu &rp, bool pool, int8_t *out, uint8_t *code, uint32_t *flags);
+// gl: g's NHWC limb planes [LA][P][co] (max|g| in gmax_in); otherwise as launch_conv_dx_mfma
+void launch_conv_dx_tile(hipStream_t s, const ConvShape &sh, const int8_t *gl,
+                         const uint32_t *gmax_in, const int8_t *wt, const uint32_t *wmax,
+                         const uint8_t *prev_code, const Relu &rp, int32_t *gout, int64_t *out64,
+                         uint32_t *gmax_out, uint32_t *flags);
 void launch_conv_dx_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g, const uint32_t *gmax_in,
                          const int8_t *wt, const uint32_t *wmax, const uint8_t *prev_code,
                          const Relu &rp, int32_t *gout, int64_t *out64, uint32_t *gmax_out,
