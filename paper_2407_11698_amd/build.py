@@ -19,12 +19,14 @@ CFLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Wall",
     # packed fp32 instructions are kept out of every kernel (none of this code needs them)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # MFMA accumulators in VGPRs: with the AGPR form the register allocator does not tie the
-    # accumulator operand to the result across loop iterations and copies every accumulator on
-    # every iteration (v_accvgpr_mov / read / write); the VGPR form keeps them in place
-    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-I", INCLUDE, "-I", CSRC,
 ]
+# MFMA accumulators in VGPRs: when a loop's accumulators start from a literal zero, the AGPR form
+# is not tied across iterations and every accumulator is copied on every iteration (v_accvgpr_*);
+# the VGPR form keeps them in place. conv_dw.hip peels its first step instead (its 144
+# accumulators need the AGPRs).
+VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
+AGPR_FILES = {"conv_dw.hip"}
 
 
 def sources():
@@ -34,6 +36,8 @@ def sources():
 def _compile(src: str) -> str:
     obj = os.path.join(OBJ, os.path.basename(src)[:-4] + ".o")
     cmd = ["hipcc", "-c", src, "-o", obj] + CFLAGS
+    if os.path.basename(src) not in AGPR_FILES:
+        cmd += VGPR_FORM
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s" % (src, r.stdout))

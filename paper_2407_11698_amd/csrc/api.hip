@@ -178,7 +178,8 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     }
     g->xpad = off; off = align256(off + (size_t)xpadb);
     g->slots = off; off = align256(off + 16 * SLOT_WORDS * 4);
-    g->lr_mfma = d->n_classes > 0 && mfma_learning_ok(d->n, g->d, d->n_classes);
+    g->lr_mfma = d->n_classes > 0 &&
+                 mfma_learning_ok(d->n, g->d, d->n_classes, d->layer[g->J - 1].c_out);
     {
         LearningScratch ls{};
         if (g->lr_mfma) ls = learning_scratch(d->n, g->d, d->n_classes);

@@ -11,13 +11,14 @@
 // positions); xp holds x with a zero halo of h0 >= W + 2 positions on both sides.
 //
 // GEMM: M = co, N = ci (times 9 taps), K = padded positions. A workgroup owns a 64 co x 16 ci
-// tile, all 9 taps, over a range of K; its four waves split that range and run independently
-// (no barrier in the main loop). A fragments (g limbs) are loaded from the planes straight into
+// tile, all 9 taps, over a range of K. Its four waves run independently (no barrier in the main
+// loop), each on one limb of g and one part of the range: with L limbs, Q = 4 / L parts (L = 3:
+// one part, one wave idle). A fragments (g limbs) are loaded from the planes straight into
 // registers, one 256-position super-step ahead. The x window of a super-step (plus the halo) is
 // staged in the wave's own double-buffered LDS slice; the fragment of tap (r, s) is read from it
 // at byte offset h0 + (r-1)(W+1) + (s-1), and a funnel shift (v_alignbit) realigns the dwords.
-// The waves' int32 sums are added in int64 through LDS at the end. Each limb of g is one pass;
-// a wave's range is at most 128000 positions, so |sum| <= 128 * 128 * 128000 < 2^31.
+// The waves' int32 sums, weighted 256^limb, are added in int64 through LDS at the end. A wave's
+// range is at most 511 * 256 positions, so |sum| <= 128 * 128 * 130816 < 2^31.
 #include <type_traits>
 
 #include "mfma_common.h"
@@ -26,9 +27,10 @@ namespace nitro {
 
 constexpr int DWP_KS = 256;        // padded positions per super-step (4 MFMA K-steps of 64)
 constexpr int DWP_HMAX = 64;       // largest halo: W <= 62
-constexpr int DWP_CHUNK_MAX = 2000;   // super-steps per workgroup (a wave: <= 500 * 256)
+constexpr int DWP_CHUNK_MAX = 511;    // super-steps per workgroup (and per wave: <= 511 * 256)
 constexpr int DWP_WIN = DWP_KS + 2 * DWP_HMAX;   // staged window of a super-step (bytes/row)
-constexpr int DWP_RS = DWP_WIN + 4;             // its LDS row stride: an odd number of dwords
+constexpr int DWP_RS = DWP_WIN + 20;            // its LDS row stride: 101 dwords spreads the
+                                                // 16 rows x 4 lane groups evenly over the banks
 constexpr int DWP_NCH = 16 * DWP_WIN / 16 / 64;  // 16-byte chunks per lane (16 rows, 64 lanes)
 
 struct DwpGeom {
@@ -239,7 +241,8 @@ __device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" :::
 __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 {
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
     const int LA = limbs_for(slot_read(p.gmax));
     if (LA > 4) {
         if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
@@ -256,12 +259,14 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
     const int split = rest / p.tiles_co;
     const int co0 = tco * 64, ci0 = tci * 16;
 
-    // this wave's super-steps
+    // this wave's limb and super-steps
+    const int Q = LA == 1 ? 4 : LA == 2 ? 2 : 1;
+    const int limb = wave / Q, part = wave - limb * Q;
     const int sb = split * p.chunk;
     const int se = sb + p.chunk < p.nss ? sb + p.chunk : p.nss;
-    const int per = (se - sb + 3) >> 2;
-    const int wb = sb + wave * per < se ? sb + wave * per : se;
-    const int nst = (wb + per < se ? wb + per : se) - wb;
+    const int per = (se - sb + Q - 1) / Q;
+    const int wb = sb + part * per < se ? sb + part * per : se;
+    const int nst = limb < LA ? (wb + per < se ? wb + per : se) - wb : 0;
 
     constexpr int RS = DWP_RS, CR = DWP_WIN / 16;
     uint8_t *wl = lds + wave * (2 * 16 * RS);  // this wave's two stages [16 rows][RS]
@@ -298,9 +303,15 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
     }
     const int lane_b = j * RS + 16 * g4;
 
+    // Pipeline (per wave, super-step s): at its start the x window of s + 1 is requested; s
+    // computes from LDS stage s & 1, and each K-step's A fragments are requested for s + 1 as
+    // soon as that K-step has used them; at its end the window of s + 1 goes to LDS stage
+    // (s + 1) & 1. The first super-step of a pass starts its accumulators from zero inside the
+    // MFMAs (peeled): a loop whose accumulators enter as literal zeros is compiled with copies
+    // of every accumulator on every iteration.
     v4i acc[9][4];
     v4i a[4][4];                 // A fragments [K-step][co tile]
-    v4i bst[DWP_NCH];
+    v4i bst[DWP_NCH];            // staged x window
 
     auto load_a = [&](int u, int ss, int l) {
         const uint32_t k = (uint32_t)ss * DWP_KS + (uint32_t)l * plane + 64 * u;
@@ -323,9 +334,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
             d[3] = (uint32_t)bst[m][3];
         }
     };
-    // one super-step from LDS stage `stage`; with RELOAD each K-step's A fragments are reloaded
-    // for super-step `next` as soon as they are used
-    auto compute = [&](auto reload, int stage, int next, int l) {
+    auto compute = [&](auto first, auto reload, int stage, int next, int l) {
         const uint8_t *base = wl + stage * 16 * RS + lane_b;
 #pragma unroll
         for (int u = 0; u < 4; u++) {
@@ -340,35 +349,47 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
                 b[3] = (int)funnel_shr(d4, d3, tsh[t]);
 #pragma unroll
                 for (int i = 0; i < 4; i++)
-                    acc[t][i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[u][i], b, acc[t][i], 0, 0, 0);
+                    acc[t][i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
+                        a[u][i], b, (decltype(first)::value && u == 0) ? v4i{0, 0, 0, 0} : acc[t][i],
+                        0, 0, 0);
             }
             if (decltype(reload)::value) load_a(u, next, l);
         }
     };
 
-    for (int l = 0; l < LA; l++) {
-#pragma unroll
-        for (int t = 0; t < 9; t++)
-#pragma unroll
-            for (int i = 0; i < 4; i++) acc[t][i] = v4i{0, 0, 0, 0};
+    {
+        const int l = limb;
         if (nst > 0) {
 #pragma unroll
             for (int u = 0; u < 4; u++) load_a(u, wb, l);
             load_b(wb);
             store_b(0);
             wave_lds_sync();
-            for (int s = 0; s + 1 < nst; s++) {
-                load_b(wb + s + 1);
-                compute(std::true_type(), s & 1, wb + s + 1, l);
-                store_b((s + 1) & 1);
+            // super-step 0 (peeled), then 1 .. nst - 1; the last one requests nothing
+            if (nst > 1) {
+                load_b(wb + 1);
+                compute(std::true_type(), std::true_type(), 0, wb + 1, l);
+                store_b(1);
                 wave_lds_sync();
+                for (int s = 1; s + 1 < nst; s++) {
+                    load_b(wb + s + 1);
+                    compute(std::false_type(), std::true_type(), s & 1, wb + s + 1, l);
+                    store_b((s + 1) & 1);
+                    wave_lds_sync();
+                }
+                compute(std::false_type(), std::false_type(), (nst - 1) & 1, 0, l);
+            } else {
+                compute(std::true_type(), std::false_type(), 0, 0, l);
             }
-            compute(std::false_type(), (nst - 1) & 1, 0, l);
+        } else {
+#pragma unroll
+            for (int t = 0; t < 9; t++)
+#pragma unroll
+                for (int i = 0; i < 4; i++) acc[t][i] = v4i{0, 0, 0, 0};
         }
-        // sum of the four waves (int64) -> this split's tile; limb l carries weight 256^l
+        // sum of the four waves (int64), each weighted 256^limb -> this split's tile
         __syncthreads();
         int32_t *red = (int32_t *)lds;        // [wave][3 taps][64 co][16 ci]
-        const int64_t wl_ = (int64_t)1 << (8 * l);
 #pragma unroll
         for (int t0 = 0; t0 < 9; t0 += 3) {
 #pragma unroll
@@ -383,11 +404,10 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
                 const int tt = e >> 10, co = co0 + ((e >> 4) & 63), ci = ci0 + (e & 15);
                 int64_t v = 0;
 #pragma unroll
-                for (int w = 0; w < 4; w++) v += red[(w * 3 + tt) * 1024 + (e & 1023)];
-                if (co < p.co && ci < p.ci_out) {
-                    int64_t *dst = p.out + (((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci_out + ci;
-                    *dst = l == 0 ? v * wl_ : *dst + v * wl_;
-                }
+                for (int w = 0; w < 4; w++)
+                    v += (int64_t)red[(w * 3 + tt) * 1024 + (e & 1023)] * ((int64_t)1 << (8 * (w / Q)));
+                if (co < p.co && ci < p.ci_out)
+                    p.out[(((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci_out + ci] = v;
             }
             __syncthreads();
         }

@@ -72,7 +72,9 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
     constexpr int BD = 3;                         // B prefetch distance (K-steps)
     constexpr int STAGE = CT_NPMAX * C::PS;
     constexpr int SMEM_A = 2 * STAGE;
-    constexpr int SMEM_EPI = CT_BM * CT_BN * (MODE == IG_FWD ? 2 : 4);
+    constexpr int OS = CT_BN + 16;                // epilogue byte-tile row stride (forward)
+    constexpr int GS = CT_BN + 1;                 // epilogue int32-tile row stride (input gradient)
+    constexpr int SMEM_EPI = MODE == IG_FWD ? 2 * CT_BM * OS : CT_BM * GS * 4;
     constexpr int SMEM = SMEM_A > SMEM_EPI ? SMEM_A : SMEM_EPI;
     __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
 
@@ -231,8 +233,8 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
     if (MODE == IG_FWD) {
         // NITRO-Scaling + NITRO-ReLU per element into LDS, then coalesced (and pooled) stores.
         // Several passes: the int64 sum saturated to int32 still saturates z* (128 SF < 2^31).
-        uint8_t *Os = smem;                   // [BM][BN] int8 activations
-        uint8_t *Rs = smem + CT_BM * CT_BN;   // [BM][BN] region codes
+        uint8_t *Os = smem;                   // [BM][OS] int8 activations
+        uint8_t *Rs = smem + CT_BM * OS;      // [BM][OS] region codes
 #pragma unroll
         for (int i = 0; i < TM; i++)
 #pragma unroll
@@ -243,8 +245,8 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
                     const int col = wn * 32 + j * 16 + (lane & 15);
                     uint8_t reg;
                     const int32_t a = scale_relu32(sat_i32(value(i, j, t)), p.sr, reg);
-                    Os[row * CT_BN + col] = (uint8_t)(int8_t)a;
-                    Rs[row * CT_BN + col] = reg;
+                    Os[row * OS + col] = (uint8_t)(int8_t)a;
+                    Rs[row * OS + col] = reg;
                 }
         __syncthreads();
         if (!p.pool) {
@@ -253,8 +255,8 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
                 const int64_t m = m0 + row;
                 if (m >= M || n0 + cc >= p.no) continue;
                 const int64_t o = m * p.no + n0 + cc;
-                *(v4i *)(p.out + o) = *(const v4i *)(Os + row * CT_BN + cc);
-                *(v4i *)(p.code + o) = *(const v4i *)(Rs + row * CT_BN + cc);
+                *(v4i *)(p.out + o) = *(const v4i *)(Os + row * OS + cc);
+                *(v4i *)(p.code + o) = *(const v4i *)(Rs + row * OS + cc);
             }
         } else {
             // 2x2 windows, 4 channels per thread: the tile holds rt (even) whole image rows
@@ -273,8 +275,8 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
 #pragma unroll
                     for (int t = 0; t < 4; t++) {
                         const int at = q + (t >> 1) * W + (t & 1);
-                        const int v = (int)(int8_t)Os[at * CT_BN + col + e];
-                        if (v > best) { best = v; arg = t; breg = Rs[at * CT_BN + col + e]; }
+                        const int v = (int)(int8_t)Os[at * OS + col + e];
+                        if (v > best) { best = v; arg = t; breg = Rs[at * OS + col + e]; }
                     }
                     ov |= (uint32_t)(uint8_t)(int8_t)best << (8 * e);
                     cv |= (uint32_t)(arg | (breg << 2)) << (8 * e);
@@ -300,7 +302,7 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
                 }
     } else {
         // int32 sums into LDS, then 16 channels per thread: ReLU' with 16 codes, 64-byte rows
-        int32_t *Gs = (int32_t *)smem;        // [BM][BN]
+        int32_t *Gs = (int32_t *)smem;        // [BM][GS]
         bool bad = false;
 #pragma unroll
         for (int i = 0; i < TM; i++)
@@ -312,7 +314,7 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
                     const int col = wn * 32 + j * 16 + (lane & 15);
                     const int64_t v = value(i, j, t);
                     bad |= !fits_i32(v);
-                    Gs[row * CT_BN + col] = (int32_t)v;
+                    Gs[row * GS + col] = (int32_t)v;
                 }
         __syncthreads();
         uint32_t mx = 0;
@@ -326,7 +328,7 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
             v4i outv[4];
 #pragma unroll
             for (int e = 0; e < 16; e++) {
-                const int32_t v = Gs[row * CT_BN + cc + e];
+                const int32_t v = Gs[row * GS + cc + e];
                 int64_t gv = v;
                 if (p.prev_code) gv = relu_bwd(v, (uint8_t)((uint32_t)cd[e >> 2] >> (8 * (e & 3))), p.rp);
                 outv[e >> 2][e & 3] = (int32_t)gv;

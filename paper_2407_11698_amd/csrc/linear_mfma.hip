@@ -44,7 +44,10 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     constexpr int TM = WM / 16, TN = WN / 16;
     constexpr int A_CHUNKS = LG_BM * 4 / 256, B_CHUNKS = LG_BN * 4 / 256;
     constexpr int STAGE = (LG_BM + LG_BN) * LG_LDS;
-    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+    constexpr int DS = LG_BN + 1;                 // epilogue int32-tile row stride
+    constexpr int SMEM_EPI = MODE == LIN_UNPOOL ? LG_BM * DS * 4 : 0;
+    constexpr int SMEM = 2 * STAGE > SMEM_EPI ? 2 * STAGE : SMEM_EPI;
+    __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -157,56 +160,91 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
         }
     }
 
-    uint32_t mx = 0;
+    if (MODE != LIN_UNPOOL) {
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int j = 0; j < TN; j++)
+#pragma unroll
+                for (int t = 0; t < 4; t++) {
+                    const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + t;
+                    const int col = n0 + wn * WN + j * 16 + (lane & 15);
+                    if (m >= p.M || col >= p.N) continue;
+                    const int64_t v = acc64[i][j][t];
+                    if (MODE == LIN_PART) p.out64[((int64_t)blockIdx.z * p.M + m) * p.N + col] = v;
+                    else if (m < p.m_valid) p.out64[(int64_t)m * p.ldc + col] = v;
+                }
+        return;
+    }
+    // LIN_UNPOOL. m = sample, col = index in the block output. delta (int32: it must fit) goes
+    // through LDS; then each thread takes 16 consecutive outputs of one sample (one pooled pixel,
+    // 16 channels: N and c are multiples of 16), applies NITRO-ReLU backward with their 16 region
+    // codes and writes the 2x2 window of each (the gradient at the argmax, 0 elsewhere) as
+    // 64-byte rows.
     bool bad = false;
+    int32_t *Ds = (int32_t *)smem;            // [LG_BM][DS]
 #pragma unroll
     for (int i = 0; i < TM; i++)
 #pragma unroll
         for (int j = 0; j < TN; j++)
 #pragma unroll
             for (int t = 0; t < 4; t++) {
-                const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + t;
-                const int col = n0 + wn * WN + j * 16 + (lane & 15);
-                if (m >= p.M || col >= p.N) continue;
+                const int row = wm * WM + i * 16 + (lane >> 4) * 4 + t;
+                const int col = wn * WN + j * 16 + (lane & 15);
                 const int64_t v = acc64[i][j][t];
-                if (MODE == LIN_PART) {
-                    p.out64[((int64_t)blockIdx.z * p.M + m) * p.N + col] = v;
-                } else if (MODE == LIN_DW) {
-                    if (m < p.m_valid) p.out64[(int64_t)m * p.ldc + col] = v;
-                } else {
-                    // m = sample, col = index in the block output; delta leaves no int32 range
-                    bad |= !fits_i32(v);
-                    const int64_t o = (int64_t)m * p.N + col;
-                    if (p.delta) p.delta[o] = (int32_t)v;
-                    if (p.pool) {
-                        const uint8_t cd = p.code[o];
-                        const int64_t gv = relu_bwd(v, (uint8_t)(cd >> 2), p.rp);
-                        bad |= !fits_i32(gv);
-                        const uint32_t a = abs_i64_sat(gv);
-                        mx = a > mx ? a : mx;
-                        const uint32_t W2 = (uint32_t)p.w / 2;
-                        const uint32_t ch = (uint32_t)col % (uint32_t)p.c, pp = (uint32_t)col / (uint32_t)p.c;
-                        const uint32_t q2 = pp % W2, h2 = pp / W2;
-                        const int arg = cd & 3;
-                        int32_t *gb = p.g + (int64_t)m * p.h * p.w * p.c;
-#pragma unroll
-                        for (int u = 0; u < 4; u++) {
-                            const uint32_t pix = (2 * h2 + (u >> 1)) * (uint32_t)p.w + 2 * q2 + (u & 1);
-                            gb[(int64_t)pix * p.c + ch] = u == arg ? (int32_t)gv : 0;
-                        }
-                    } else {
-                        const int64_t gv = relu_bwd(v, p.code[o], p.rp);
-                        bad |= !fits_i32(gv);
-                        const uint32_t a = abs_i64_sat(gv);
-                        mx = a > mx ? a : mx;
-                        p.g[o] = (int32_t)gv;
-                    }
-                }
+                bad |= !fits_i32(v);
+                Ds[row * DS + col] = (int32_t)v;
             }
-    if (MODE == LIN_UNPOOL) {
-        if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
-        block_slot_max(p.gmax, mx);
+    __syncthreads();
+    uint32_t mx = 0;
+    const uint32_t W2 = (uint32_t)p.w / 2;
+    for (int it = tid; it < LG_BM * (LG_BN / 16); it += 256) {
+        const int row = it / (LG_BN / 16), cc = (it % (LG_BN / 16)) * 16;
+        const int m = m0 + row, col = n0 + cc;
+        if (m >= p.M || col >= p.N) continue;
+        const int64_t o = (int64_t)m * p.N + col;
+        const v4i cd = *(const v4i *)(p.code + o);
+        v4i dv[4], gv[4];
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            const int32_t v = Ds[row * DS + cc + e];
+            const uint32_t c8 = ((uint32_t)cd[e >> 2] >> (8 * (e & 3))) & 0xFFu;
+            const int64_t g = relu_bwd(v, (uint8_t)(p.pool ? c8 >> 2 : c8), p.rp);
+            bad |= !fits_i32(g);
+            const uint32_t a = abs_i64_sat(g);
+            mx = a > mx ? a : mx;
+            dv[e >> 2][e & 3] = v;
+            gv[e >> 2][e & 3] = (int32_t)g;
+        }
+        if (p.delta)
+#pragma unroll
+            for (int q = 0; q < 4; q++) *(v4i *)(p.delta + o + 4 * q) = dv[q];
+        if (!p.pool) {
+#pragma unroll
+            for (int q = 0; q < 4; q++) *(v4i *)(p.g + o + 4 * q) = gv[q];
+            continue;
+        }
+        const uint32_t ch = (uint32_t)col % (uint32_t)p.c, pp = (uint32_t)col / (uint32_t)p.c;
+        const uint32_t q2 = pp % W2, h2 = pp / W2;
+        int32_t *gb = p.g + (int64_t)m * p.h * p.w * p.c + ch;
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            const uint32_t pix = (2 * h2 + (u >> 1)) * (uint32_t)p.w + 2 * q2 + (u & 1);
+#pragma unroll
+            for (int q = 0; q < 4; q++) {
+                v4i o4;
+#pragma unroll
+                for (int r = 0; r < 4; r++) {
+                    const int e = 4 * q + r;
+                    const uint32_t arg = ((uint32_t)cd[e >> 2] >> (8 * (e & 3))) & 3u;
+                    o4[r] = arg == (uint32_t)u ? gv[q][r] : 0;
+                }
+                *(v4i *)(gb + (int64_t)pix * p.c + 4 * q) = o4;
+            }
+        }
     }
+    if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
+    block_slot_max(p.gmax, mx);
 }
 
 template <bool A32, int MODE>
@@ -297,9 +335,10 @@ __global__ void k_loss_from_partials(const int64_t *__restrict__ part, int nz, i
 }
 
 // ---------------------------------------------------------------------------------------------
-bool mfma_learning_ok(int n, int64_t d, int G)
+bool mfma_learning_ok(int n, int64_t d, int G, int c)
 {
-    return d % 16 == 0 && n >= 1 && G >= 1 && (int64_t)n * d < ((int64_t)1 << 31) &&
+    // c: channels of the block output (its 16-column epilogue groups stay inside one pixel)
+    return d % 16 == 0 && c % 16 == 0 && n >= 1 && G >= 1 && (int64_t)n * d < ((int64_t)1 << 31) &&
            (int64_t)G * d < ((int64_t)1 << 31) && G <= 4096;
 }
 

@@ -371,7 +371,7 @@ struct LearningBuffers {
     int32_t *epad, *et;            // e as [np][gp] and [gp][np] (zero padded)
     uint32_t *wmax, *emax, *gmax;  // max|W|, max|e|, max|g| slots (zeroed before the call)
 };
-bool mfma_learning_ok(int n, int64_t d, int G);
+bool mfma_learning_ok(int n, int64_t d, int G, int c);   // c: block output channels
 LearningScratch learning_scratch(int n, int64_t d, int G);
 // yhat, e, dW of the learning layer on f = the block output [n][d], and the gradient g at the
 // last forward layer's pre-activation (un-pool and NITRO-ReLU backward of delta = e W).
