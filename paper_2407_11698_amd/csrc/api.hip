@@ -230,14 +230,16 @@ Relu make_relu(int alpha_inv, int round)
 
 inline uint8_t *at(void *base, size_t off) { return (uint8_t *)base + off; }
 
+// zero_slots: clear the block's max slots first (a training iteration clears every block's
+// slots once, up front, instead)
 nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, const BlockGeom &g,
                                 const nitro_block_params *p, const int8_t *x, int8_t *a_out,
-                                void *state)
+                                void *state, bool zero_slots = true)
 {
     hipStream_t s = ctx->stream;
     const Relu rp = make_relu(desc->alpha_inv, desc->round);
     uint32_t *slots = (uint32_t *)at(state, g.slots);
-    if (hipMemsetAsync(slots, 0, 8 * SLOT_WORDS * 4, s) != hipSuccess) return NITRO_EHIP;
+    if (zero_slots && hipMemsetAsync(slots, 0, 8 * SLOT_WORDS * 4, s) != hipSuccess) return NITRO_EHIP;
     const int8_t *cur = x;
     for (int j = 0; j < g.J; j++) {
         const LayerGeom &L = g.L[j];
@@ -248,9 +250,13 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
         const Div sf = make_div(L.sf, desc->round);
         if (L.conv) {
             // limb planes for this call's forward and input-gradient GEMMs, and max|W_j|
-            launch_pack_conv_weights(s, p->w[j], L.sh.co, L.sh.c, L.pad16 ? 16 : L.sh.c,
-                                     (int8_t *)at(state, g.wf[j]),
-                                     (int8_t *)at(state, g.wt[j]), slots + (j) * SLOT_WORDS);
+            if (!L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c))
+                launch_pack_conv_tiled(s, p->w[j], L.sh.co, L.sh.c, (int8_t *)at(state, g.wf[j]),
+                                       (int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS);
+            else
+                launch_pack_conv_weights(s, p->w[j], L.sh.co, L.sh.c, L.pad16 ? 16 : L.sh.c,
+                                         (int8_t *)at(state, g.wf[j]),
+                                         (int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS);
             const int8_t *wf = (const int8_t *)at(state, g.wf[j]);
             uint32_t *wmax = slots + j * SLOT_WORDS;
             ConvShape sx = L.sh;
@@ -284,7 +290,8 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
 nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, const BlockGeom &g,
                                  const nitro_block_params *p, const int8_t *x, const int8_t *a_out,
                                  const int32_t *labels, const int32_t *delta_out, void *state,
-                                 const nitro_block_grads *gr, const nitro_block_taps *taps)
+                                 const nitro_block_grads *gr, const nitro_block_taps *taps,
+                                 bool zero_slots = true)
 {
     hipStream_t s = ctx->stream;
     const Relu rp = make_relu(desc->alpha_inv, desc->round);
@@ -296,7 +303,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
     const LayerGeom &LJ = g.L[J - 1];
     uint32_t *slots = (uint32_t *)at(state, g.slots);
     // max|g_j| (4..7), max|W_lr| (8), max|e| (9) are produced by this call
-    if (hipMemsetAsync(slots + 4 * SLOT_WORDS, 0, 6 * SLOT_WORDS * 4, s) != hipSuccess)
+    if (zero_slots && hipMemsetAsync(slots + 4 * SLOT_WORDS, 0, 6 * SLOT_WORDS * 4, s) != hipSuccess)
         return NITRO_EHIP;
     bool have_g = false;
     if (G > 0) {
@@ -395,6 +402,28 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
 bool mul_ok(int64_t a, int64_t b, int64_t *out)
 {
     return !__builtin_mul_overflow(a, b, out);
+}
+
+// One IntegerSGD update as an entry of a batched launch (validation as sgd_impl). A full batch
+// is launched first: its entries' gradients are complete when later entries are added.
+nitro_status sgd_entry(nitro_ctx *ctx, SgdBatch &b, int32_t *w, const int64_t *dw, int64_t count,
+                       int64_t gamma_inv, int64_t lambda_inv, int64_t eta_override, int32_t round)
+{
+    if (!w || !dw || count < 0 || gamma_inv < 1 || lambda_inv < 0) return NITRO_EINVAL;
+    if (b.n == SGD_MAX) {
+        launch_sgd_batch(ctx->stream, b);
+        b.n = 0;
+    }
+    int64_t eta = eta_override;
+    if (eta < 0 && !mul_ok(gamma_inv, lambda_inv, &eta)) return NITRO_EINVAL;
+    SgdTensor &t = b.t[b.n++];
+    t.w = w;
+    t.dw = dw;
+    t.count = count;
+    t.gamma = make_div(gamma_inv, round);
+    t.eta = make_div(eta > 0 ? eta : 1, round);
+    t.decay = eta != 0;
+    return NITRO_OK;
 }
 
 nitro_status sgd_impl(nitro_ctx *ctx, int32_t *w, const int64_t *dw, int64_t count,
@@ -684,6 +713,17 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     if (net->head && !params->w_head) return NITRO_EINVAL;
     DeviceGuard guard(ctx->device);
     TimerScope timer(ctx);
+    // every block's max slots cleared in one launch; every update applied in one launch at the
+    // end (blocks and the output layer share no weights, so the order of updates is free)
+    {
+        SlotList sl{};
+        sl.words = 16 * SLOT_WORDS;
+        for (int b = 0; b < net->n_blocks; b++)
+            sl.p[b] = (uint32_t *)at(at(workspace, g.state[b]), g.b[b].slots);
+        launch_zero_slots(ctx->stream, sl, net->n_blocks);
+    }
+    SgdBatch sgd{};
+    sgd.flags = ctx->flags;
 
     // 1. forward through every block (pre-update weights)
     const int8_t *cur = x;
@@ -692,7 +732,8 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         for (int j = 0; j < net->block[b].n_layers; j++) bp.w[j] = params->w[b][j];
         bp.w_lr = params->w_lr[b];
         int8_t *aout = (int8_t *)at(workspace, g.aout[b]);
-        st = block_forward_impl(ctx, &net->block[b], g.b[b], &bp, cur, aout, at(workspace, g.state[b]));
+        st = block_forward_impl(ctx, &net->block[b], g.b[b], &bp, cur, aout, at(workspace, g.state[b]),
+                                false);
         if (st != NITRO_OK) return st;
         cur = aout;
     }
@@ -706,11 +747,11 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                                (int32_t *)at(workspace, g.hyhat), (int32_t *)at(workspace, g.he),
                                ctx->flags);
         launch_linear_dw(ctx->stream, n, (int)d, G, (const int32_t *)at(workspace, g.he), cur, hdw);
-        st = sgd_impl(ctx, params->w_head, hdw, (int64_t)G * d, hp->gamma_inv, hp->lambda_inv_lr,
-                      eta_lr, round);
+        st = sgd_entry(ctx, sgd, params->w_head, hdw, (int64_t)G * d, hp->gamma_inv, hp->lambda_inv_lr,
+                       eta_lr, round);
         if (st != NITRO_OK) return st;
     }
-    // 3. local training of every block, then its updates
+    // 3. local training of every block
     for (int b = 0; b < net->n_blocks; b++) {
         const nitro_block_desc &d = net->block[b];
         const int8_t *xin = b == 0 ? x : (const int8_t *)at(workspace, g.aout[b - 1]);
@@ -723,18 +764,20 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         bp.w_lr = params->w_lr[b];
         gr.dw_lr = (int64_t *)at(workspace, g.dwlr[b]);
         st = block_backward_impl(ctx, &d, g.b[b], &bp, xin, (const int8_t *)at(workspace, g.aout[b]),
-                                 labels, nullptr, at(workspace, g.state[b]), &gr, nullptr);
+                                 labels, nullptr, at(workspace, g.state[b]), &gr, nullptr, false);
         if (st != NITRO_OK) return st;
-        st = sgd_impl(ctx, params->w_lr[b], gr.dw_lr, (int64_t)G * g.b[b].d, hp->gamma_inv,
-                      hp->lambda_inv_lr, eta_lr, round);
+        st = sgd_entry(ctx, sgd, params->w_lr[b], gr.dw_lr, (int64_t)G * g.b[b].d, hp->gamma_inv,
+                       hp->lambda_inv_lr, eta_lr, round);
         if (st != NITRO_OK) return st;
         for (int j = 0; j < d.n_layers; j++) {
-            st = sgd_impl(ctx, params->w[b][j], gr.dw[j], weight_count(d.layer[j]), gamma_fw,
-                          hp->lambda_inv_fw, eta_fw, round);
+            st = sgd_entry(ctx, sgd, params->w[b][j], gr.dw[j], weight_count(d.layer[j]), gamma_fw,
+                           hp->lambda_inv_fw, eta_fw, round);
             if (st != NITRO_OK) return st;
         }
     }
-    return NITRO_OK;
+    // 4. IntegerSGD (Alg. 1) of every weight tensor
+    launch_sgd_batch(ctx->stream, sgd);
+    return hip_status();
 }
 
 nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable)

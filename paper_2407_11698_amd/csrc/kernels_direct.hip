@@ -23,22 +23,32 @@ void launch_fill_i64(hipStream_t s, int64_t *p, int64_t count)
     hipLaunchKernelGGL(k_fill_i64, dim3(g), dim3(256), 0, s, p, count);
 }
 
-__global__ void k_sum_partials(const int64_t *__restrict__ part, int nz, int64_t count,
-                               int64_t *__restrict__ out)
+// Each workgroup: 64 consecutive outputs x 4 groups of partials (group q adds z = q, q + 4, ...),
+// the groups' sums added in LDS in a fixed order (integer addition: the order does not matter).
+__global__ __launch_bounds__(256) void k_sum_partials(const int64_t *__restrict__ part, int nz,
+                                                      int64_t count, int64_t *__restrict__ out)
 {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        int64_t v = 0;
-        for (int z = 0; z < nz; z++) v += part[(int64_t)z * count + i];
-        out[i] = v;
+    __shared__ int64_t red[4][64];
+    const int il = threadIdx.x & 63, q = threadIdx.x >> 6;
+    const int64_t i = (int64_t)blockIdx.x * 64 + il;
+    int64_t v = 0;
+    if (i < count) {
+        int z = q;
+        for (; z + 12 < nz; z += 16)
+            v += part[(int64_t)z * count + i] + part[(int64_t)(z + 4) * count + i] +
+                 part[(int64_t)(z + 8) * count + i] + part[(int64_t)(z + 12) * count + i];
+        for (; z < nz; z += 4) v += part[(int64_t)z * count + i];
     }
+    red[q][il] = v;
+    __syncthreads();
+    if (q == 0 && i < count) out[i] = red[0][il] + red[1][il] + red[2][il] + red[3][il];
 }
 
 void launch_sum_partials(hipStream_t s, const int64_t *part, int nz, int64_t count, int64_t *out)
 {
     if (count <= 0) return;
-    hipLaunchKernelGGL(k_sum_partials, dim3(grid_stride_blocks(count, 256, 8192)), dim3(256), 0, s,
-                       part, nz, count, out);
+    hipLaunchKernelGGL(k_sum_partials, dim3((unsigned)((count + 63) / 64)), dim3(256), 0, s, part,
+                       nz, count, out);
 }
 
 // ---------------------------------------------------------------------------------------------

@@ -372,9 +372,7 @@ void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *
 {
     const LearningScratch sc = learning_scratch(n, d, G);
     // operands: learning-weight limb planes, the transposed block output
-    hipLaunchKernelGGL(k_pack_learning_weights, dim3(grid_stride_blocks((int64_t)G * d, 256, 1024)),
-                       dim3(256), 0, s, w, (uint32_t)G, (uint32_t)d, (uint32_t)sc.gp, b.wf, b.wt,
-                       b.wmax);
+    launch_pack_matrix(s, w, G, (int)d, sc.gp, b.wf, b.wt, b.wmax);
     hipLaunchKernelGGL(k_transpose_i8, dim3((unsigned)((d + 63) / 64), (unsigned)((sc.np + 63) / 64)),
                        dim3(256), 0, s, f, n, (int)d, sc.np, b.ft);
     // forward: split-K partials, then yhat / e

@@ -443,6 +443,36 @@ void launch_conv_dx_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g, c
 // conv weight gradient, int64 KRSC, overwritten.
 void launch_conv_dw(hipStream_t s, const ConvShape &sh, const int32_t *g, const int8_t *x,
                     int64_t *dw);
+// ---- preparation and bookkeeping (prep.hip)
+// Conv weight W [co][9][ci] -> wf [4][co][9 ci] and wt [4][ci][9 co] in one pass (co, ci % 16 == 0).
+bool pack_conv_tiled_ok(int co, int ci);
+void launch_pack_conv_tiled(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,
+                            int8_t *wt, uint32_t *wmax);
+// Matrix X [R][C] (C % 16 == 0, Rpad % 16 == 0) -> limb planes P [4][R][C] and T [4][C][Rpad].
+void launch_pack_matrix(hipStream_t s, const int32_t *w, int R, int C, int Rpad, int8_t *p,
+                        int8_t *t, uint32_t *wmax);
+constexpr int SGD_MAX = 24;
+constexpr int SGD_ITEMS = 8;
+struct SgdTensor {
+    int32_t *w;
+    const int64_t *dw;
+    int64_t count;
+    Div gamma, eta;
+    int32_t decay;
+};
+struct SgdBatch {
+    SgdTensor t[SGD_MAX];
+    int64_t first[SGD_MAX];       // first workgroup of each tensor (set by the launcher)
+    int n;
+    uint32_t *flags;
+};
+void launch_sgd_batch(hipStream_t s, SgdBatch b);
+struct SlotList {
+    uint32_t *p[NITRO_MAX_BLOCKS];
+    int words;
+};
+void launch_zero_slots(hipStream_t s, const SlotList &l, int nblocks);
+
 // IntegerSGD (Alg. 1) in place.
 void launch_sgd(hipStream_t s, int32_t *w, const int64_t *dw, int64_t count, const Div &gamma,
                 const Div &eta, bool decay, uint32_t *flags);

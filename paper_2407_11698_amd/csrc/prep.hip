@@ -1,0 +1,153 @@
+// Operand preparation and bookkeeping kernels shared by the training iteration: limb planes of
+// int32 weight matrices (plain and transposed) in one pass, batched IntegerSGD, max-slot
+// clearing, and the split-K partial sums.
+#include "mfma_common.h"
+
+namespace nitro {
+
+// ---------------------------------------------------------------------------------------------
+// X int32 [R][C] (element (r, c) at x[z zx + r xs + c]) -> balanced int8 limb planes
+//   P[l][r][c] at p[z zp + l pplane + r ps + c]                          (when p != null)
+//   T[l][c][r] at t[z zt + l tplane + c ts + r] for r < Rpad, zero rows r >= R  (when t != null)
+// and max|X| into a max slot. One workgroup: a 64 x 64 tile, z = blockIdx.z (the taps of a
+// conv weight). C, ps, ts, Rpad and the z offsets keep every 16-byte row chunk aligned.
+struct PackArgs {
+    const int32_t *x;
+    int64_t xs, zx;
+    int R, C, Rpad;
+    int8_t *p;
+    int64_t ps, pplane, zp;
+    int8_t *t;
+    int64_t ts, tplane, zt;
+    uint32_t *wmax;
+};
+
+__global__ __launch_bounds__(256) void k_pack_limbs(PackArgs a)
+{
+    constexpr int LS = 68;                   // LDS row stride (bytes) of the transposed tile
+    __shared__ __attribute__((aligned(16))) uint8_t L[4][64][LS];
+    const int tid = threadIdx.x;
+    const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64, z = blockIdx.z;
+    const int r = tid >> 2, cq = (tid & 3) * 16;
+    const int gr = r0 + r, gc = c0 + cq;
+    const bool ok = gr < a.R && gc < a.C;
+    int32_t v[16];
+    uint32_t m = 0;
+    const int32_t *src = a.x + z * a.zx + (int64_t)(ok ? gr : 0) * a.xs + (ok ? gc : 0);
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        const v4i x4 = ok ? *(const v4i *)(src + 4 * q) : v4i{0, 0, 0, 0};
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            v[4 * q + e] = x4[e];
+            const uint32_t av = abs_u32(x4[e]);
+            m = av > m ? av : m;
+        }
+    }
+#pragma unroll
+    for (int l = 0; l < 4; l++) {
+        v4i d;
+#pragma unroll
+        for (int q = 0; q < 4; q++) d[q] = (int)limb4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3], l);
+        if (a.p && ok) *(v4i *)(a.p + z * a.zp + l * a.pplane + (int64_t)gr * a.ps + gc) = d;
+        if (a.t)
+#pragma unroll
+            for (int e = 0; e < 16; e++) L[l][cq + e][r] = (uint8_t)((uint32_t)d[e >> 2] >> (8 * (e & 3)));
+    }
+    if (a.t) {
+        __syncthreads();
+        const int c = tid >> 2, rq = (tid & 3) * 16;
+        if (c0 + c < a.C && r0 + rq < a.Rpad) {
+#pragma unroll
+            for (int l = 0; l < 4; l++) {
+                const uint32_t *s = (const uint32_t *)&L[l][c][rq];
+                const v4i o = v4i{(int)s[0], (int)s[1], (int)s[2], (int)s[3]};
+                *(v4i *)(a.t + z * a.zt + l * a.tplane + (int64_t)(c0 + c) * a.ts + r0 + rq) = o;
+            }
+        }
+    }
+    block_slot_max(a.wmax, m);
+}
+
+static void launch_pack(hipStream_t s, const PackArgs &a, int batches)
+{
+    const dim3 grid((unsigned)((a.C + 63) / 64), (unsigned)((a.Rpad + 63) / 64), (unsigned)batches);
+    hipLaunchKernelGGL(k_pack_limbs, grid, dim3(256), 0, s, a);
+}
+
+bool pack_conv_tiled_ok(int co, int ci) { return co % 16 == 0 && ci % 16 == 0; }
+
+void launch_pack_conv_tiled(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,
+                            int8_t *wt, uint32_t *wmax)
+{
+    // per tap t: X_t[o][c] = W[o][t][c]; wf = [l][o][9 ci] (tap-major K), wt = [l][c][9 co]
+    PackArgs a{};
+    a.x = w; a.xs = 9 * (int64_t)ci; a.zx = ci;
+    a.R = co; a.C = ci; a.Rpad = co;
+    a.p = wf; a.ps = 9 * (int64_t)ci; a.pplane = (int64_t)co * 9 * ci; a.zp = ci;
+    a.t = wt; a.ts = 9 * (int64_t)co; a.tplane = (int64_t)ci * 9 * co; a.zt = co;
+    a.wmax = wmax;
+    launch_pack(s, a, 9);
+}
+
+void launch_pack_matrix(hipStream_t s, const int32_t *w, int R, int C, int Rpad, int8_t *p,
+                        int8_t *t, uint32_t *wmax)
+{
+    PackArgs a{};
+    a.x = w; a.xs = C; a.zx = 0;
+    a.R = R; a.C = C; a.Rpad = Rpad;
+    a.p = p; a.ps = C; a.pplane = (int64_t)R * C; a.zp = 0;
+    a.t = t; a.ts = Rpad; a.tplane = (int64_t)C * Rpad; a.zt = 0;
+    a.wmax = wmax;
+    launch_pack(s, a, 1);
+}
+
+// ---------------------------------------------------------------------------------------------
+// IntegerSGD (Alg. 1) over several tensors in one launch: d = dw / gamma (+ w / eta when
+// eta != 0); w <- w - d. Workgroups are dealt to tensors in order (first[k] .. first[k+1]).
+__global__ __launch_bounds__(256) void k_sgd_batch(SgdBatch b)
+{
+    int k = 0;
+    while (k + 1 < b.n && (int64_t)blockIdx.x >= b.first[k + 1]) k++;
+    const SgdTensor &t = b.t[k];
+    const int64_t base = ((int64_t)blockIdx.x - b.first[k]) * 256 * SGD_ITEMS;
+    for (int q = 0; q < SGD_ITEMS; q++) {
+        const int64_t i = base + q * 256 + threadIdx.x;
+        if (i >= t.count) break;
+        const int64_t wv = t.w[i];
+        int64_t d = idiv(t.dw[i], t.gamma);
+        if (t.decay) d += idiv(wv, t.eta);
+        const int64_t nw = wv - d;
+        if (!fits_i32(nw)) {
+            raise_flag(b.flags, FLAG_OVERFLOW);
+            continue;
+        }
+        t.w[i] = (int32_t)nw;
+    }
+}
+
+void launch_sgd_batch(hipStream_t s, SgdBatch b)
+{
+    int64_t blocks = 0;
+    for (int k = 0; k < b.n; k++) {
+        b.first[k] = blocks;
+        blocks += (b.t[k].count + 256 * SGD_ITEMS - 1) / (256 * SGD_ITEMS);
+    }
+    if (blocks == 0) return;
+    hipLaunchKernelGGL(k_sgd_batch, dim3((unsigned)blocks), dim3(256), 0, s, b);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Zero the max slots of several blocks (one workgroup per block).
+__global__ __launch_bounds__(256) void k_zero_slots(SlotList l)
+{
+    uint32_t *p = l.p[blockIdx.x];
+    for (int i = threadIdx.x; i < l.words; i += 256) p[i] = 0;
+}
+
+void launch_zero_slots(hipStream_t s, const SlotList &l, int nblocks)
+{
+    if (nblocks > 0) hipLaunchKernelGGL(k_zero_slots, dim3((unsigned)nblocks), dim3(256), 0, s, l);
+}
+
+}  // namespace nitro
