@@ -17,14 +17,19 @@ thread_local LaunchTimer *g_timer = nullptr;
 struct nitro_ctx : public LaunchTimer {
     int device = 0;
     hipStream_t stream = nullptr;
+    // streams of their own for the blocks' local training in a training iteration (the blocks'
+    // backward passes depend only on their own forward state), created on first use
+    hipStream_t aux[NITRO_MAX_BLOCKS] = {};
+    hipEvent_t fork = nullptr, join[NITRO_MAX_BLOCKS] = {};
+    bool aux_ready = false;
     uint32_t *flags = nullptr;                  // device: sticky status bits
     bool timing = false;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[TIMED_CLASSES];
     size_t used[TIMED_CLASSES] = {0, 0, 0};
     hipEvent_t pending_stop = nullptr;
 
-    // HIP events around one launch of a timed kernel class, on the context's stream
-    void begin(int cls) override
+    // HIP events around one launch of a timed kernel class, on the launch's stream
+    void begin(int cls, hipStream_t s) override
     {
         if (used[cls] == ev[cls].size()) {
             hipEvent_t a, b;
@@ -33,13 +38,24 @@ struct nitro_ctx : public LaunchTimer {
             ev[cls].push_back({a, b});
         }
         auto &p = ev[cls][used[cls]++];
-        (void)hipEventRecord(p.first, stream);
+        (void)hipEventRecord(p.first, s);
         pending_stop = p.second;
     }
-    void end(int) override
+    void end(int, hipStream_t s) override
     {
-        if (pending_stop) (void)hipEventRecord(pending_stop, stream);
+        if (pending_stop) (void)hipEventRecord(pending_stop, s);
         pending_stop = nullptr;
+    }
+    nitro_status ensure_aux()
+    {
+        if (aux_ready) return NITRO_OK;
+        if (hipEventCreateWithFlags(&fork, hipEventDisableTiming) != hipSuccess) return NITRO_EHIP;
+        for (int b = 0; b < NITRO_MAX_BLOCKS; b++) {
+            if (hipStreamCreateWithFlags(&aux[b], hipStreamNonBlocking) != hipSuccess) return NITRO_EHIP;
+            if (hipEventCreateWithFlags(&join[b], hipEventDisableTiming) != hipSuccess) return NITRO_EHIP;
+        }
+        aux_ready = true;
+        return NITRO_OK;
     }
 };
 
@@ -291,9 +307,9 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                                  const nitro_block_params *p, const int8_t *x, const int8_t *a_out,
                                  const int32_t *labels, const int32_t *delta_out, void *state,
                                  const nitro_block_grads *gr, const nitro_block_taps *taps,
-                                 bool zero_slots = true)
+                                 bool zero_slots = true, hipStream_t stream = nullptr)
 {
-    hipStream_t s = ctx->stream;
+    hipStream_t s = stream ? stream : ctx->stream;
     const Relu rp = make_relu(desc->alpha_inv, desc->round);
     const int n = desc->n;
     const int G = desc->n_classes;
@@ -556,6 +572,14 @@ void nitro_destroy(nitro_ctx *ctx)
     if (!ctx) return;
     DeviceGuard guard(ctx->device);
     (void)hipStreamSynchronize(ctx->stream);
+    if (ctx->aux_ready) {
+        for (int b = 0; b < NITRO_MAX_BLOCKS; b++) {
+            (void)hipStreamSynchronize(ctx->aux[b]);
+            (void)hipStreamDestroy(ctx->aux[b]);
+            (void)hipEventDestroy(ctx->join[b]);
+        }
+        (void)hipEventDestroy(ctx->fork);
+    }
     for (auto &v : ctx->ev)
         for (auto &p : v) { (void)hipEventDestroy(p.first); (void)hipEventDestroy(p.second); }
     (void)hipFree(ctx->flags);
@@ -751,7 +775,13 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                        eta_lr, round);
         if (st != NITRO_OK) return st;
     }
-    // 3. local training of every block
+    // 3. local training of every block, each on a stream of its own (forked after the forward
+    // pass and the output layer, joined before the updates)
+    st = ctx->ensure_aux();
+    if (st != NITRO_OK) return st;
+    if (hipEventRecord(ctx->fork, ctx->stream) != hipSuccess) return NITRO_EHIP;
+    for (int b = 0; b < net->n_blocks; b++)
+        if (hipStreamWaitEvent(ctx->aux[b], ctx->fork, 0) != hipSuccess) return NITRO_EHIP;
     for (int b = 0; b < net->n_blocks; b++) {
         const nitro_block_desc &d = net->block[b];
         const int8_t *xin = b == 0 ? x : (const int8_t *)at(workspace, g.aout[b - 1]);
@@ -764,8 +794,11 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         bp.w_lr = params->w_lr[b];
         gr.dw_lr = (int64_t *)at(workspace, g.dwlr[b]);
         st = block_backward_impl(ctx, &d, g.b[b], &bp, xin, (const int8_t *)at(workspace, g.aout[b]),
-                                 labels, nullptr, at(workspace, g.state[b]), &gr, nullptr, false);
+                                 labels, nullptr, at(workspace, g.state[b]), &gr, nullptr, false,
+                                 ctx->aux[b]);
         if (st != NITRO_OK) return st;
+        if (hipEventRecord(ctx->join[b], ctx->aux[b]) != hipSuccess) return NITRO_EHIP;
+        if (hipStreamWaitEvent(ctx->stream, ctx->join[b], 0) != hipSuccess) return NITRO_EHIP;
         st = sgd_entry(ctx, sgd, params->w_lr[b], gr.dw_lr, (int64_t)G * g.b[b].d, hp->gamma_inv,
                        hp->lambda_inv_lr, eta_lr, round);
         if (st != NITRO_OK) return st;

@@ -437,10 +437,10 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
     a.flags = flags;
     const size_t lds_stage = (size_t)4 * 2 * 16 * DWP_RS, lds_red = (size_t)4 * 3 * 1024 * 4;
     const unsigned nwg = (unsigned)(pl.tiles_co * pl.tiles_ci * pl.nsplit);
-    timer_begin(TIMED_DW_MFMA);
+    timer_begin(TIMED_DW_MFMA, s);
     hipLaunchKernelGGL(k_conv_dw_planes, dim3(nwg), dim3(256), lds_stage > lds_red ? lds_stage : lds_red,
                        s, a);
-    timer_end(TIMED_DW_MFMA);
+    timer_end(TIMED_DW_MFMA, s);
     if (pl.nsplit > 1) launch_sum_partials(s, part, pl.nsplit, (int64_t)sh.co * 9 * sh.c, dw);
 }
 

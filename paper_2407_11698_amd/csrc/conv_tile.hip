@@ -390,13 +390,13 @@ static void launch_tile(hipStream_t s, TileArgs a)
     a.d_rw = make_div32((uint32_t)(a.rs * a.w));
     const dim3 grid((unsigned)((a.n * a.h + a.rt - 1) / a.rt), (unsigned)((a.no + CT_BN - 1) / CT_BN));
     const int cls = MODE == IG_FWD ? TIMED_IGEMM_FWD : TIMED_IGEMM_DX;
-    timer_begin(cls);
+    timer_begin(cls, s);
     switch (a.ck == 16 ? 16 : a.ck == 32 ? 32 : 64) {
     case 16: hipLaunchKernelGGL((k_conv_tile<MODE, 16>), grid, dim3(256), 0, s, a); break;
     case 32: hipLaunchKernelGGL((k_conv_tile<MODE, 32>), grid, dim3(256), 0, s, a); break;
     default: hipLaunchKernelGGL((k_conv_tile<MODE, 64>), grid, dim3(256), 0, s, a); break;
     }
-    timer_end(cls);
+    timer_end(cls, s);
 }
 
 void launch_conv_fwd_tile(hipStream_t s, const ConvShape &sh, const int8_t *x, const int8_t *wf,

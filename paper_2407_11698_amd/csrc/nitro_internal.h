@@ -310,13 +310,13 @@ inline unsigned grid_stride_blocks(int64_t n, int per = 256, unsigned cap = 2048
 // classes: 0 k_igemm_conv forward, 1 k_igemm_conv input gradient, 2 k_conv_dw_planes
 enum { TIMED_IGEMM_FWD = 0, TIMED_IGEMM_DX = 1, TIMED_DW_MFMA = 2, TIMED_CLASSES = 3 };
 struct LaunchTimer {
-    virtual void begin(int cls) = 0;
-    virtual void end(int cls) = 0;
+    virtual void begin(int cls, hipStream_t s) = 0;
+    virtual void end(int cls, hipStream_t s) = 0;
     virtual ~LaunchTimer() {}
 };
 extern thread_local LaunchTimer *g_timer;
-inline void timer_begin(int cls) { if (g_timer) g_timer->begin(cls); }
-inline void timer_end(int cls) { if (g_timer) g_timer->end(cls); }
+inline void timer_begin(int cls, hipStream_t s) { if (g_timer) g_timer->begin(cls, s); }
+inline void timer_end(int cls, hipStream_t s) { if (g_timer) g_timer->end(cls, s); }
 
 // ------------------------------------------------------------------------------------------
 // Kernel launchers (each enqueues on `s`; shapes are validated by the caller).
