@@ -97,6 +97,12 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true",
+                    help="launch every kernel from the host each step instead of replaying the "
+                         "captured iteration (nitro_train_step_graph)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="run one device-to-device copy of this many MiB before the warm-up: "
+                         "the known-size reference for hardware byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only; --gpus %d is not supported" % args.gpus,
@@ -111,9 +117,15 @@ def main():
     wl = WL.VGG_CNN
     dev = torch.device("cuda", 0)
     dr = WL.draw_workload(wl, runner.kaiming_bound)
+    graph = not args.eager
+    # the library runs on a stream of its own (a captured graph needs a non-default stream);
+    # torch's copies below are issued on the same stream, so they are ordered with it
+    stream = torch.cuda.Stream(dev)
+    torch.cuda.set_stream(stream)
     w0 = [torch.from_numpy(w).to(dev) for w in dr.weights]
     xs = [torch.from_numpy(x).to(dev) for x, _ in dr.batches]
     ys = [torch.from_numpy(y).to(dev) for _, y in dr.batches]
+    xb, yb = torch.empty_like(xs[0]), torch.empty_like(ys[0])    # the graph's input buffers
     net = runner.GpuNet(wl, dr.weights)
     period = len(xs)
 
@@ -122,25 +134,44 @@ def main():
             if i % period == 0:
                 for a, b in zip(net.w, w0):
                     a.copy_(b)
-            net.step(xs[i % period], ys[i % period])
+            if graph:
+                xb.copy_(xs[i % period])
+                yb.copy_(ys[i % period])
+                net.step_graph(xb, yb)
+            else:
+                net.step(xs[i % period], ys[i % period])
 
-    run(0, args.warmup)
+    if args.copy_mib > 0:
+        src = torch.zeros(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    # per-kernel timing is switched on before the warm-up: the graph is captured once, with its
+    # timing events, outside the timed region (the events then hold the last replay's times)
+    warmup = max(args.warmup, 1) if graph else args.warmup
+    if graph:
+        net.ctx.kernel_timing(True)
+    run(0, warmup)
     net.ctx.sync()
-    net.ctx.kernel_timing(True)
+    if not graph:
+        net.ctx.kernel_timing(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run(args.warmup, args.steps)
+    run(warmup, args.steps)
     torch.cuda.synchronize()
     el = time.perf_counter() - t0
     net.ctx.sync()                        # raises if any kernel flagged overflow or a bad label
     ktime = {KERNEL_CLASSES[c]: net.ctx.kernel_time(c) for c in KERNEL_CLASSES}
     net.ctx.kernel_timing(False)
+    timed_steps = 1 if graph else args.steps    # graph: the events of the last replay
 
     ops = conv_layer_ops(wl)
     per_class = {}
     for name, (ms, launches) in ktime.items():
-        tops = ops[name] * args.steps / (ms * 1e-3) / 1e12 if ms > 0 else 0.0
-        per_class[name] = {"ms_per_step": round(ms / args.steps, 4), "launches": launches,
+        tops = ops[name] * timed_steps / (ms * 1e-3) / 1e12 if ms > 0 else 0.0
+        per_class[name] = {"ms_per_step": round(ms / timed_steps, 4), "launches": launches,
                            "avg_launch_us": round(ms * 1e3 / launches, 2) if launches else None,
                            "algorithmic_TOPs": round(tops, 3)}
     dom = max(per_class, key=lambda k: per_class[k]["ms_per_step"])
@@ -154,7 +185,7 @@ def main():
         "unit": "images/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": warmup,
         "ms_per_step": round(el * 1e3 / args.steps, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -165,7 +196,8 @@ def main():
                    "blocks": "conv 3-64-64, 64-128-128, 128-256-256, 256-512-512, pool, "
                              "learning layer to 100 classes", "gamma_inv": wl.gamma_inv,
                    "lambda_inv_fw": wl.lambda_inv_fw, "lambda_inv_lr": wl.lambda_inv_lr,
-                   "alpha_inv": wl.alpha_inv, "rounding": "floor"},
+                   "alpha_inv": wl.alpha_inv, "rounding": "floor",
+                   "launch": "graph replay" if graph else "eager"},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved,
                      "peak": PEAK_INT8_TOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_INT8_TOPS, 5), "traffic": None},

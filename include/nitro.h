@@ -219,6 +219,18 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                               const nitro_net_params *params, void *workspace,
                               const int8_t *x, const int32_t *labels, const nitro_hparams *hp);
 
+/* nitro_train_step replayed from a HIP graph. The first call, and any call whose arguments
+ * differ from the captured call's (compared by value: descriptors, parameter pointers,
+ * workspace, x, labels, hyper-parameters, the context's stream and timing switch), captures one
+ * iteration on the context's stream and instantiates it; every call then launches the graph.
+ * The graph reads x and labels from the captured buffers, so a caller that changes the batch
+ * writes it into the same buffers. The context's stream must not be the legacy default stream
+ * (EINVAL). Capture errors return the error of the failing call or NITRO_EHIP. The context
+ * keeps one graph; nitro_destroy releases it. */
+nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
+                                    const nitro_net_params *params, void *workspace,
+                                    const int8_t *x, const int32_t *labels, const nitro_hparams *hp);
+
 /* Device pointer, inside a workspace laid out by nitro_net_query, of block b's output a_b
  * (int8), so that callers can inspect the forward activations after nitro_train_step. */
 nitro_status nitro_net_block_output(const nitro_net_desc *net, void *workspace, int32_t b,
@@ -234,11 +246,15 @@ int64_t nitro_host_div(int64_t n, int64_t d, int32_t round);
 /* NITRO-ReLU mean for alpha_inv (section 3.2.2) under `round`. */
 int32_t nitro_host_relu_mu(int32_t alpha_inv, int32_t round);
 
-/* Per-kernel timing for profiling: when enabled, the library records HIP events on the context
- * stream around every launch of one kernel of class `cls`: 0 the int8 MFMA conv forward kernel,
- * 1 the int8 MFMA conv input-gradient kernel, 2 the int8 MFMA conv weight-gradient kernel
- * (layers that take other kernels are not timed). nitro_kernel_time synchronises the stream and
- * returns the accumulated milliseconds and launch count since the last read or enable. */
+/* Per-kernel timing for profiling. While enabled, every launch of a timed kernel class records,
+ * on the device, the wall-clock time from its first workgroup's start to its last workgroup's
+ * end (this also works inside a graph replayed by nitro_train_step_graph). Classes: 0 the tiled
+ * int8 MFMA conv forward kernel, 1 the tiled conv input-gradient kernel, 2 the conv
+ * weight-gradient kernel over padded pixel planes (layers that take other kernels are not
+ * timed). Enabling allocates the context's timing buffer once (ENOMEM) and restarts the count.
+ * nitro_kernel_time synchronises the context's stream and returns the summed milliseconds and
+ * the number of launches: of the launches enqueued since the last read or enable, or, when a
+ * graph was captured with timing on, of the last replay. */
 nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable);
 nitro_status nitro_kernel_time(nitro_ctx *ctx, int32_t cls, double *ms, int64_t *launches);
 

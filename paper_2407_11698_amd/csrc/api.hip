@@ -17,34 +17,27 @@ thread_local LaunchTimer *g_timer = nullptr;
 struct nitro_ctx : public LaunchTimer {
     int device = 0;
     hipStream_t stream = nullptr;
+    uint32_t *flags = nullptr;                  // device: sticky status bits
     // streams of their own for the blocks' local training in a training iteration (the blocks'
     // backward passes depend only on their own forward state), created on first use
     hipStream_t aux[NITRO_MAX_BLOCKS] = {};
     hipEvent_t fork = nullptr, join[NITRO_MAX_BLOCKS] = {};
     bool aux_ready = false;
-    uint32_t *flags = nullptr;                  // device: sticky status bits
-    bool timing = false;
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev[TIMED_CLASSES];
+    // the captured training iteration of nitro_train_step_graph and the arguments it holds
+    hipGraphExec_t gexec = nullptr;
+    std::vector<uint8_t> gkey;
+    // per-kernel timing: TS_CAP slots per class in tsbuf (allocated when timing is first
+    // enabled); used[c] slots of class c assigned since the last reset. A graph captured with
+    // timing keeps writing its slots on every replay (ts_graph).
+    static constexpr int TS_CAP = 1024;
+    bool timing = false, ts_graph = false;
+    uint64_t *tsbuf = nullptr;
     size_t used[TIMED_CLASSES] = {0, 0, 0};
-    hipEvent_t pending_stop = nullptr;
 
-    // HIP events around one launch of a timed kernel class, on the launch's stream
-    void begin(int cls, hipStream_t s) override
+    uint64_t *slot(int cls) override
     {
-        if (used[cls] == ev[cls].size()) {
-            hipEvent_t a, b;
-            if (hipEventCreate(&a) != hipSuccess) return;
-            if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
-            ev[cls].push_back({a, b});
-        }
-        auto &p = ev[cls][used[cls]++];
-        (void)hipEventRecord(p.first, s);
-        pending_stop = p.second;
-    }
-    void end(int, hipStream_t s) override
-    {
-        if (pending_stop) (void)hipEventRecord(pending_stop, s);
-        pending_stop = nullptr;
+        if (!tsbuf || used[cls] >= (size_t)TS_CAP) return nullptr;
+        return tsbuf + ((size_t)cls * TS_CAP + used[cls]++) * TS_WORDS;
     }
     nitro_status ensure_aux()
     {
@@ -572,6 +565,8 @@ void nitro_destroy(nitro_ctx *ctx)
     if (!ctx) return;
     DeviceGuard guard(ctx->device);
     (void)hipStreamSynchronize(ctx->stream);
+    if (ctx->gexec) (void)hipGraphExecDestroy(ctx->gexec);
+    if (ctx->tsbuf) (void)hipFree(ctx->tsbuf);
     if (ctx->aux_ready) {
         for (int b = 0; b < NITRO_MAX_BLOCKS; b++) {
             (void)hipStreamSynchronize(ctx->aux[b]);
@@ -580,8 +575,6 @@ void nitro_destroy(nitro_ctx *ctx)
         }
         (void)hipEventDestroy(ctx->fork);
     }
-    for (auto &v : ctx->ev)
-        for (auto &p : v) { (void)hipEventDestroy(p.first); (void)hipEventDestroy(p.second); }
     (void)hipFree(ctx->flags);
     delete ctx;
 }
@@ -737,8 +730,14 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     if (net->head && !params->w_head) return NITRO_EINVAL;
     DeviceGuard guard(ctx->device);
     TimerScope timer(ctx);
-    // every block's max slots cleared in one launch; every update applied in one launch at the
-    // end (blocks and the output layer share no weights, so the order of updates is free)
+    // a captured iteration with timing clears its timing slots first (every replay measures
+    // afresh); every block's max slots cleared in one launch; every update applied in one
+    // launch at the end (blocks and the output layer share no weights)
+    if (ctx->timing && ctx->tsbuf) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(ctx->stream, &cs) == hipSuccess && cs == hipStreamCaptureStatusActive)
+            launch_ts_reset(ctx->stream, ctx->tsbuf, (int64_t)TIMED_CLASSES * nitro_ctx::TS_CAP);
+    }
     {
         SlotList sl{};
         sl.words = 16 * SLOT_WORDS;
@@ -761,28 +760,28 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         if (st != NITRO_OK) return st;
         cur = aout;
     }
-    // 2. output layer: global gradient, then its IntegerSGD update
+    // 2. output layer: global gradient (its update comes with the others, step 4)
     const int n = net->block[0].n;
+    int64_t *hdw = (int64_t *)at(workspace, g.hdw);
     if (net->head) {
         const int64_t d = g.hd;
         const Div sf = make_div(256 * d, round);
-        int64_t *hdw = (int64_t *)at(workspace, g.hdw);
         launch_linear_fwd_loss(ctx->stream, n, (int)d, G, cur, params->w_head, sf, labels,
                                (int32_t *)at(workspace, g.hyhat), (int32_t *)at(workspace, g.he),
                                ctx->flags);
         launch_linear_dw(ctx->stream, n, (int)d, G, (const int32_t *)at(workspace, g.he), cur, hdw);
-        st = sgd_entry(ctx, sgd, params->w_head, hdw, (int64_t)G * d, hp->gamma_inv, hp->lambda_inv_lr,
-                       eta_lr, round);
-        if (st != NITRO_OK) return st;
     }
-    // 3. local training of every block, each on a stream of its own (forked after the forward
-    // pass and the output layer, joined before the updates)
+    // 3. local training of every block, each on a stream of its own: forked after the forward
+    // pass and the output layer; the last block runs on the context's stream, which is
+    // otherwise idle meanwhile; joined before the updates
     st = ctx->ensure_aux();
     if (st != NITRO_OK) return st;
+    const int last = net->n_blocks - 1;
     if (hipEventRecord(ctx->fork, ctx->stream) != hipSuccess) return NITRO_EHIP;
-    for (int b = 0; b < net->n_blocks; b++)
+    for (int b = 0; b < last; b++)
         if (hipStreamWaitEvent(ctx->aux[b], ctx->fork, 0) != hipSuccess) return NITRO_EHIP;
     for (int b = 0; b < net->n_blocks; b++) {
+        hipStream_t bs = b == last ? ctx->stream : ctx->aux[b];
         const nitro_block_desc &d = net->block[b];
         const int8_t *xin = b == 0 ? x : (const int8_t *)at(workspace, g.aout[b - 1]);
         nitro_block_params bp{};
@@ -795,16 +794,26 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         gr.dw_lr = (int64_t *)at(workspace, g.dwlr[b]);
         st = block_backward_impl(ctx, &d, g.b[b], &bp, xin, (const int8_t *)at(workspace, g.aout[b]),
                                  labels, nullptr, at(workspace, g.state[b]), &gr, nullptr, false,
-                                 ctx->aux[b]);
+                                 bs);
         if (st != NITRO_OK) return st;
-        if (hipEventRecord(ctx->join[b], ctx->aux[b]) != hipSuccess) return NITRO_EHIP;
+        if (b != last && hipEventRecord(ctx->join[b], bs) != hipSuccess) return NITRO_EHIP;
+    }
+    for (int b = 0; b < last; b++)
         if (hipStreamWaitEvent(ctx->stream, ctx->join[b], 0) != hipSuccess) return NITRO_EHIP;
-        st = sgd_entry(ctx, sgd, params->w_lr[b], gr.dw_lr, (int64_t)G * g.b[b].d, hp->gamma_inv,
+    // 4. IntegerSGD (Alg. 1) of every weight tensor, after every gradient is complete
+    if (net->head) {
+        st = sgd_entry(ctx, sgd, params->w_head, hdw, (int64_t)G * g.hd, hp->gamma_inv,
                        hp->lambda_inv_lr, eta_lr, round);
         if (st != NITRO_OK) return st;
+    }
+    for (int b = 0; b < net->n_blocks; b++) {
+        const nitro_block_desc &d = net->block[b];
+        st = sgd_entry(ctx, sgd, params->w_lr[b], (const int64_t *)at(workspace, g.dwlr[b]),
+                       (int64_t)G * g.b[b].d, hp->gamma_inv, hp->lambda_inv_lr, eta_lr, round);
+        if (st != NITRO_OK) return st;
         for (int j = 0; j < d.n_layers; j++) {
-            st = sgd_entry(ctx, sgd, params->w[b][j], gr.dw[j], weight_count(d.layer[j]), gamma_fw,
-                           hp->lambda_inv_fw, eta_fw, round);
+            st = sgd_entry(ctx, sgd, params->w[b][j], (const int64_t *)at(workspace, g.dw[b][j]),
+                           weight_count(d.layer[j]), gamma_fw, hp->lambda_inv_fw, eta_fw, round);
             if (st != NITRO_OK) return st;
         }
     }
@@ -813,11 +822,71 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     return hip_status();
 }
 
+nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
+                                    const nitro_net_params *params, void *workspace,
+                                    const int8_t *x, const int32_t *labels, const nitro_hparams *hp)
+{
+    if (!ctx || !net || !params || !workspace || !x || !labels || !hp) return NITRO_EINVAL;
+    if (!ctx->stream) return NITRO_EINVAL;           // the legacy default stream cannot capture
+    DeviceGuard guard(ctx->device);
+    std::vector<uint8_t> key;
+    auto put = [&](const void *p, size_t n) {
+        const uint8_t *b = (const uint8_t *)p;
+        key.insert(key.end(), b, b + n);
+    };
+    put(net, sizeof(*net));
+    put(params, sizeof(*params));
+    put(&workspace, sizeof(workspace));
+    put(&x, sizeof(x));
+    put(&labels, sizeof(labels));
+    put(hp, sizeof(*hp));
+    put(&ctx->stream, sizeof(ctx->stream));
+    put(&ctx->timing, sizeof(ctx->timing));
+    if (!ctx->gexec || key != ctx->gkey) {
+        if (ctx->gexec) {
+            (void)hipGraphExecDestroy(ctx->gexec);
+            ctx->gexec = nullptr;
+        }
+        nitro_status st = ctx->ensure_aux();
+        if (st != NITRO_OK) return st;
+        for (auto &u : ctx->used) u = 0;
+        if (hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeRelaxed) != hipSuccess)
+            return NITRO_EHIP;
+        st = nitro_train_step(ctx, net, params, workspace, x, labels, hp);
+        hipGraph_t graph = nullptr;
+        const hipError_t e = hipStreamEndCapture(ctx->stream, &graph);
+        if (st == NITRO_OK && e != hipSuccess) st = NITRO_EHIP;
+        if (st == NITRO_OK && hipGraphInstantiate(&ctx->gexec, graph, nullptr, nullptr, 0) != hipSuccess) {
+            ctx->gexec = nullptr;
+            st = NITRO_EHIP;
+        }
+        if (graph) (void)hipGraphDestroy(graph);
+        (void)hipGetLastError();
+        if (st != NITRO_OK) return st;
+        ctx->gkey = key;
+        ctx->ts_graph = ctx->timing && ctx->tsbuf;
+    }
+    if (hipGraphLaunch(ctx->gexec, ctx->stream) != hipSuccess) return NITRO_EHIP;
+    return NITRO_OK;
+}
+
 nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable)
 {
     if (!ctx) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
     ctx->timing = enable != 0;
+    if (ctx->timing) {
+        const int64_t nslots = (int64_t)TIMED_CLASSES * nitro_ctx::TS_CAP;
+        if (!ctx->tsbuf && hipMalloc((void **)&ctx->tsbuf, (size_t)nslots * TS_WORDS * 8) != hipSuccess) {
+            ctx->tsbuf = nullptr;
+            ctx->timing = false;
+            return NITRO_ENOMEM;
+        }
+        launch_ts_reset(ctx->stream, ctx->tsbuf, nslots);
+        if (hipGetLastError() != hipSuccess) return NITRO_EHIP;
+    }
     for (auto &u : ctx->used) u = 0;
+    ctx->ts_graph = false;
     return NITRO_OK;
 }
 
@@ -825,17 +894,38 @@ nitro_status nitro_kernel_time(nitro_ctx *ctx, int32_t cls, double *ms, int64_t 
 {
     if (!ctx || cls < 0 || cls >= TIMED_CLASSES || !ms || !launches) return NITRO_EINVAL;
     DeviceGuard guard(ctx->device);
+    *ms = 0.0;
+    *launches = 0;
+    if (!ctx->tsbuf || ctx->used[cls] == 0) return NITRO_OK;
     if (hipStreamSynchronize(ctx->stream) != hipSuccess) return NITRO_EHIP;
+    int khz = 0;
+    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, ctx->device) != hipSuccess ||
+        khz <= 0)
+        return NITRO_EHIP;
+    const size_t n = ctx->used[cls];
+    std::vector<uint64_t> h(n * TS_WORDS);
+    uint64_t *src = ctx->tsbuf + (size_t)cls * nitro_ctx::TS_CAP * TS_WORDS;
+    if (hipMemcpy(h.data(), src, h.size() * 8, hipMemcpyDeviceToHost) != hipSuccess) return NITRO_EHIP;
     double tot = 0.0;
-    for (size_t i = 0; i < ctx->used[cls]; i++) {
-        float t = 0.f;
-        if (hipEventElapsedTime(&t, ctx->ev[cls][i].first, ctx->ev[cls][i].second) != hipSuccess)
-            return NITRO_EHIP;
-        tot += t;
+    int64_t cnt = 0;
+    for (size_t i = 0; i < n; i++) {
+        uint64_t t0 = ~(uint64_t)0, t1 = 0;
+        for (int w = 0; w < TS_SPREAD; w++) {
+            t0 = h[i * TS_WORDS + w] < t0 ? h[i * TS_WORDS + w] : t0;
+            t1 = h[i * TS_WORDS + TS_SPREAD + w] > t1 ? h[i * TS_WORDS + TS_SPREAD + w] : t1;
+        }
+        if (t1 > t0) {
+            tot += (double)(t1 - t0) / khz;    // ticks / (ticks per ms)
+            cnt++;
+        }
     }
     *ms = tot;
-    *launches = (int64_t)ctx->used[cls];
-    ctx->used[cls] = 0;
+    *launches = cnt;
+    if (!ctx->ts_graph) {
+        // eager launches: the next read covers the launches after this one
+        ctx->used[cls] = 0;
+        launch_ts_reset(ctx->stream, src, nitro_ctx::TS_CAP);
+    }
     return NITRO_OK;
 }
 

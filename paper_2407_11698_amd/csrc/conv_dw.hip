@@ -226,6 +226,7 @@ struct DwpArgs {
     const uint32_t *gmax;
     int64_t *out;          // [nsplit][co][9][ci_out]; dW itself when there is one split
     uint32_t *flags;
+    uint64_t *ts;          // timing slot (null: untimed)
 };
 
 // bits [b, b + 32) of the 64-bit value hi:lo (v_alignbit_b32), 0 <= b < 32
@@ -241,6 +242,7 @@ __device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" :::
 __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 {
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+    ts_start(p.ts);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
     const int LA = limbs_for(slot_read(p.gmax));
@@ -412,6 +414,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
             __syncthreads();
         }
     }
+    ts_end(p.ts);
 }
 
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
@@ -437,10 +440,9 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
     a.flags = flags;
     const size_t lds_stage = (size_t)4 * 2 * 16 * DWP_RS, lds_red = (size_t)4 * 3 * 1024 * 4;
     const unsigned nwg = (unsigned)(pl.tiles_co * pl.tiles_ci * pl.nsplit);
-    timer_begin(TIMED_DW_MFMA, s);
+    a.ts = timer_slot(TIMED_DW);
     hipLaunchKernelGGL(k_conv_dw_planes, dim3(nwg), dim3(256), lds_stage > lds_red ? lds_stage : lds_red,
                        s, a);
-    timer_end(TIMED_DW_MFMA, s);
     if (pl.nsplit > 1) launch_sum_partials(s, part, pl.nsplit, (int64_t)sh.co * 9 * sh.c, dw);
 }
 

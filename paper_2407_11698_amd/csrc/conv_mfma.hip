@@ -353,10 +353,7 @@ static void launch_igemm(hipStream_t s, const IgemmArgs &a)
     const int64_t M = (int64_t)a.n * a.h * a.w;
     constexpr int BM = 128, BN = 64;
     dim3 grid((unsigned)((M + BM - 1) / BM), (unsigned)((a.no + BN - 1) / BN));
-    const int cls = MODE == IG_FWD ? TIMED_IGEMM_FWD : TIMED_IGEMM_DX;
-    timer_begin(cls, s);
     hipLaunchKernelGGL((k_igemm_conv<MODE, BM, BN>), grid, dim3(256), 0, s, a);
-    timer_end(cls, s);
 }
 
 // K = 9 * ck <= 9 * 8192 keeps 128 * 128 * K below 2^31 (one limb pass in int32).

@@ -54,6 +54,7 @@ struct TileArgs {
     int64_t *out64;
     uint32_t *gmax;
     uint32_t *flags;
+    uint64_t *ts;                  // timing slot (null: untimed)
 };
 
 __device__ inline int32_t sat_i32(int64_t v)
@@ -78,6 +79,7 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
     constexpr int SMEM = SMEM_A > SMEM_EPI ? SMEM_A : SMEM_EPI;
     __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
 
+    ts_start(p.ts);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int g4 = lane >> 4;
@@ -341,6 +343,7 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
         if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
         if (p.gmax) block_slot_max(p.gmax, mx);
     }
+    ts_end(p.ts);
 }
 
 // Tile geometry: rt = 128 / W image rows; either rt divides H (one image segment) or H divides
@@ -389,14 +392,12 @@ static void launch_tile(hipStream_t s, TileArgs a)
     a.d_w = make_div32((uint32_t)a.w);
     a.d_rw = make_div32((uint32_t)(a.rs * a.w));
     const dim3 grid((unsigned)((a.n * a.h + a.rt - 1) / a.rt), (unsigned)((a.no + CT_BN - 1) / CT_BN));
-    const int cls = MODE == IG_FWD ? TIMED_IGEMM_FWD : TIMED_IGEMM_DX;
-    timer_begin(cls, s);
+    a.ts = timer_slot(MODE == IG_FWD ? TIMED_CONV_FWD : TIMED_CONV_DX);
     switch (a.ck == 16 ? 16 : a.ck == 32 ? 32 : 64) {
     case 16: hipLaunchKernelGGL((k_conv_tile<MODE, 16>), grid, dim3(256), 0, s, a); break;
     case 32: hipLaunchKernelGGL((k_conv_tile<MODE, 32>), grid, dim3(256), 0, s, a); break;
     default: hipLaunchKernelGGL((k_conv_tile<MODE, 64>), grid, dim3(256), 0, s, a); break;
     }
-    timer_end(cls, s);
 }
 
 void launch_conv_fwd_tile(hipStream_t s, const ConvShape &sh, const int8_t *x, const int8_t *wf,

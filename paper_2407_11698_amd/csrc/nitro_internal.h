@@ -304,19 +304,45 @@ inline unsigned grid_stride_blocks(int64_t n, int per = 256, unsigned cap = 2048
 }
 
 // ------------------------------------------------------------------------------------------
-// Optional per-kernel timing: launchers bracket the launches of the timed kernel classes with
-// begin/end; the API entry points install the calling context's timer for the duration of a
-// call (thread-local, so concurrent contexts on other threads are not affected).
-// classes: 0 k_igemm_conv forward, 1 k_igemm_conv input gradient, 2 k_conv_dw_planes
-enum { TIMED_IGEMM_FWD = 0, TIMED_IGEMM_DX = 1, TIMED_DW_MFMA = 2, TIMED_CLASSES = 3 };
+// Optional per-kernel timing, measured on the device so that it also works inside a replayed
+// graph. A timed launch gets a slot of TS_WORDS uint64 words in a context-owned buffer: words
+// [0, TS_SPREAD) take the minimum start time of its workgroups and [TS_SPREAD, 2 TS_SPREAD) the
+// maximum end time (the constant-rate wall clock), each workgroup folding into word
+// (workgroup id mod TS_SPREAD). Slots are assigned when launches are enqueued (also while a graph
+// is being captured); the API entry points install the calling context's timer for the duration
+// of a call (thread-local, so concurrent contexts on other threads are not affected).
+// classes: 0 k_conv_tile forward, 1 k_conv_tile input gradient, 2 k_conv_dw_planes
+enum { TIMED_CONV_FWD = 0, TIMED_CONV_DX = 1, TIMED_DW = 2, TIMED_CLASSES = 3 };
+constexpr int TS_SPREAD = 16, TS_WORDS = 2 * TS_SPREAD;
 struct LaunchTimer {
-    virtual void begin(int cls, hipStream_t s) = 0;
-    virtual void end(int cls, hipStream_t s) = 0;
+    virtual uint64_t *slot(int cls) = 0;
     virtual ~LaunchTimer() {}
 };
 extern thread_local LaunchTimer *g_timer;
-inline void timer_begin(int cls, hipStream_t s) { if (g_timer) g_timer->begin(cls, s); }
-inline void timer_end(int cls, hipStream_t s) { if (g_timer) g_timer->end(cls, s); }
+inline uint64_t *timer_slot(int cls) { return g_timer ? g_timer->slot(cls) : nullptr; }
+
+__device__ inline unsigned ts_block_id()
+{
+    return blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+}
+// first statement of a timed kernel
+__device__ inline void ts_start(uint64_t *ts)
+{
+    if (ts && threadIdx.x == 0)
+        atomicMin((unsigned long long *)&ts[ts_block_id() % TS_SPREAD], (unsigned long long)wall_clock64());
+}
+// last statement of a timed kernel; every thread of the workgroup must reach it
+__device__ inline void ts_end(uint64_t *ts)
+{
+    if (ts) {
+        __syncthreads();
+        if (threadIdx.x == 0)
+            atomicMax((unsigned long long *)&ts[TS_SPREAD + ts_block_id() % TS_SPREAD],
+                      (unsigned long long)wall_clock64());
+    }
+}
+// reset n slots: starts to the largest value, ends to 0
+void launch_ts_reset(hipStream_t s, uint64_t *buf, int64_t nslots);
 
 // ------------------------------------------------------------------------------------------
 // Kernel launchers (each enqueues on `s`; shapes are validated by the caller).

@@ -150,4 +150,18 @@ void launch_zero_slots(hipStream_t s, const SlotList &l, int nblocks)
     if (nblocks > 0) hipLaunchKernelGGL(k_zero_slots, dim3((unsigned)nblocks), dim3(256), 0, s, l);
 }
 
+// ---------------------------------------------------------------------------------------------
+__global__ void k_ts_reset(uint64_t *buf, int64_t nwords)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nwords;
+         i += (int64_t)gridDim.x * blockDim.x)
+        buf[i] = (i % TS_WORDS) < TS_SPREAD ? ~(uint64_t)0 : 0;
+}
+
+void launch_ts_reset(hipStream_t s, uint64_t *buf, int64_t nslots)
+{
+    const int64_t n = nslots * TS_WORDS;
+    if (n > 0) hipLaunchKernelGGL(k_ts_reset, dim3(grid_stride_blocks(n, 256, 256)), dim3(256), 0, s, buf, n);
+}
+
 }  // namespace nitro

@@ -94,6 +94,7 @@ def _load():
         "nitro_net_query": (I32, [P(NetDesc), P(ctypes.c_size_t)]),
         "nitro_net_block_output": (I32, [P(NetDesc), VP, I32, P(VP)]),
         "nitro_train_step": (I32, [VP, P(NetDesc), P(NetParams), VP, VP, VP, P(HParams)]),
+        "nitro_train_step_graph": (I32, [VP, P(NetDesc), P(NetParams), VP, VP, VP, P(HParams)]),
         "nitro_host_div": (I64, [I64, I64, I32]),
         "nitro_host_relu_mu": (I32, [I32, I32]),
         "nitro_kernel_timing": (I32, [VP, I32]),
@@ -113,7 +114,8 @@ EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_sync_stat
            "nitro_status_str", "nitro_block_query", "nitro_block_saved", "nitro_block_forward",
            "nitro_block_backward",
            "nitro_head_backward", "nitro_integer_sgd_step", "nitro_net_query",
-           "nitro_net_block_output", "nitro_train_step", "nitro_host_div", "nitro_host_relu_mu",
+           "nitro_net_block_output", "nitro_train_step", "nitro_train_step_graph",
+           "nitro_host_div", "nitro_host_relu_mu",
            "nitro_kernel_timing", "nitro_kernel_time")
 
 
@@ -271,6 +273,12 @@ class Context:
     def train_step(self, nd: NetDesc, params: NetParams, workspace, x, labels, hp: HParams) -> None:
         check(LIB.nitro_train_step(self.h, ctypes.byref(nd), ctypes.byref(params), _p(workspace),
                                    _p(x), _p(labels), ctypes.byref(hp)), "nitro_train_step")
+
+    def train_step_graph(self, nd: NetDesc, params: NetParams, workspace, x, labels,
+                         hp: HParams) -> None:
+        check(LIB.nitro_train_step_graph(self.h, ctypes.byref(nd), ctypes.byref(params),
+                                         _p(workspace), _p(x), _p(labels), ctypes.byref(hp)),
+              "nitro_train_step_graph")
 
     def net_block_output_ptr(self, nd: NetDesc, workspace, b: int) -> int:
         out = VP()

@@ -66,6 +66,11 @@ class GpuNet:
     def step(self, x: torch.Tensor, y: torch.Tensor) -> None:
         self.ctx.train_step(self.nd, self.params, self.workspace, x, y, self.hp)
 
+    def step_graph(self, x: torch.Tensor, y: torch.Tensor) -> None:
+        """One iteration replayed from the context's captured graph (captured on the first call
+        with these buffers; x and y must keep their storage, only their contents change)."""
+        self.ctx.train_step_graph(self.nd, self.params, self.workspace, x, y, self.hp)
+
     def block_output(self, b: int) -> torch.Tensor:
         """Block b's output from the last step (int8, NHWC or [n][d])."""
         ptr = self.ctx.net_block_output_ptr(self.nd, self.workspace, b)

@@ -284,3 +284,39 @@ def test_deterministic(ctx):
         outs.append(net.weights_np())
     for a, b in zip(*outs):
         assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("wl", [WL.scaled(WL.SMALL_CNN, 16), WL.scaled(WL.VGG_CNN, 8)],
+                         ids=["small_cnn_b16", "vgg_b8"])
+def test_train_step_graph_matches_eager(wl):
+    """nitro_train_step_graph replays a captured iteration: after every replay (with eager torch
+    work and host syncs in between) its weights and block outputs equal the eager path's, which
+    the oracle-parity tests pin. The batch changes by writing into the captured buffers."""
+    import torch
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        gctx = N.Context(0, stream=stream)
+        ectx = N.Context(0, stream=stream)
+        dr = WL.draw_workload(wl, O.kaiming_bound, steps=4)
+        eager = runner.GpuNet(wl, dr.weights, ctx=ectx)
+        graph = runner.GpuNet(wl, dr.weights, ctx=gctx)
+        xb = torch.empty_like(dev(dr.batches[0][0]))
+        yb = torch.empty_like(dev(dr.batches[0][1]))
+        for s, (x, y) in enumerate(dr.batches * 2):
+            print("graph replay", wl.name, "step", s, flush=True)
+            xd, yd = dev(x), dev(y)
+            eager.step(xd, yd)
+            xb.copy_(xd)
+            yb.copy_(yd)
+            graph.step_graph(xb, yb)
+            junk = torch.ones(1 << 16, device="cuda", dtype=torch.int32).cumsum(0)   # eager work
+            torch.cuda.synchronize()
+            gctx.sync()
+            ectx.sync()
+            for a, b in zip(eager.weights_np(), graph.weights_np()):
+                assert np.array_equal(a, b), "step %d weights" % s
+            for b in range(len(wl.blocks)):
+                assert torch.equal(eager.block_output(b), graph.block_output(b)), "step %d block %d" % (s, b)
+            del junk
+        gctx.close()
+        ectx.close()
