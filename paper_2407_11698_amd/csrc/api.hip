@@ -19,9 +19,12 @@ struct nitro_ctx : public LaunchTimer {
     hipStream_t stream = nullptr;
     uint32_t *flags = nullptr;                  // device: sticky status bits
     // streams of their own for the blocks' local training in a training iteration (the blocks'
-    // backward passes depend only on their own forward state), created on first use
-    hipStream_t aux[NITRO_MAX_BLOCKS] = {};
-    hipEvent_t fork = nullptr, join[NITRO_MAX_BLOCKS] = {};
+    // backward passes depend only on their own forward state), created on first use. Only
+    // NAUX of them: streams share the process's few hardware queues round-robin (4 by
+    // default), and two streams on one queue run one after the other.
+    static constexpr int NAUX = 3;
+    hipStream_t aux[NAUX] = {};
+    hipEvent_t fork = nullptr, join[NAUX] = {};
     bool aux_ready = false;
     // the captured training iteration of nitro_train_step_graph and the arguments it holds
     hipGraphExec_t gexec = nullptr;
@@ -43,7 +46,7 @@ struct nitro_ctx : public LaunchTimer {
     {
         if (aux_ready) return NITRO_OK;
         if (hipEventCreateWithFlags(&fork, hipEventDisableTiming) != hipSuccess) return NITRO_EHIP;
-        for (int b = 0; b < NITRO_MAX_BLOCKS; b++) {
+        for (int b = 0; b < NAUX; b++) {
             if (hipStreamCreateWithFlags(&aux[b], hipStreamNonBlocking) != hipSuccess) return NITRO_EHIP;
             if (hipEventCreateWithFlags(&join[b], hipEventDisableTiming) != hipSuccess) return NITRO_EHIP;
         }
@@ -568,7 +571,7 @@ void nitro_destroy(nitro_ctx *ctx)
     if (ctx->gexec) (void)hipGraphExecDestroy(ctx->gexec);
     if (ctx->tsbuf) (void)hipFree(ctx->tsbuf);
     if (ctx->aux_ready) {
-        for (int b = 0; b < NITRO_MAX_BLOCKS; b++) {
+        for (int b = 0; b < nitro_ctx::NAUX; b++) {
             (void)hipStreamSynchronize(ctx->aux[b]);
             (void)hipStreamDestroy(ctx->aux[b]);
             (void)hipEventDestroy(ctx->join[b]);
@@ -771,17 +774,17 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                                ctx->flags);
         launch_linear_dw(ctx->stream, n, (int)d, G, (const int32_t *)at(workspace, g.he), cur, hdw);
     }
-    // 3. local training of every block, each on a stream of its own: forked after the forward
-    // pass and the output layer; the last block runs on the context's stream, which is
-    // otherwise idle meanwhile; joined before the updates
+    // 3. local training of every block on its own stream: forked after the forward pass and the
+    // output layer, joined before the updates. Block 0 (the largest feature maps, the longest
+    // chain) runs on the context's stream; block b > 0 on auxiliary stream (b - 1) mod NAUX.
     st = ctx->ensure_aux();
     if (st != NITRO_OK) return st;
-    const int last = net->n_blocks - 1;
+    const int naux = net->n_blocks - 1 < nitro_ctx::NAUX ? net->n_blocks - 1 : nitro_ctx::NAUX;
     if (hipEventRecord(ctx->fork, ctx->stream) != hipSuccess) return NITRO_EHIP;
-    for (int b = 0; b < last; b++)
-        if (hipStreamWaitEvent(ctx->aux[b], ctx->fork, 0) != hipSuccess) return NITRO_EHIP;
+    for (int a = 0; a < naux; a++)
+        if (hipStreamWaitEvent(ctx->aux[a], ctx->fork, 0) != hipSuccess) return NITRO_EHIP;
     for (int b = 0; b < net->n_blocks; b++) {
-        hipStream_t bs = b == last ? ctx->stream : ctx->aux[b];
+        hipStream_t bs = b == 0 ? ctx->stream : ctx->aux[(b - 1) % nitro_ctx::NAUX];
         const nitro_block_desc &d = net->block[b];
         const int8_t *xin = b == 0 ? x : (const int8_t *)at(workspace, g.aout[b - 1]);
         nitro_block_params bp{};
@@ -796,10 +799,11 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                                  labels, nullptr, at(workspace, g.state[b]), &gr, nullptr, false,
                                  bs);
         if (st != NITRO_OK) return st;
-        if (b != last && hipEventRecord(ctx->join[b], bs) != hipSuccess) return NITRO_EHIP;
     }
-    for (int b = 0; b < last; b++)
-        if (hipStreamWaitEvent(ctx->stream, ctx->join[b], 0) != hipSuccess) return NITRO_EHIP;
+    for (int a = 0; a < naux; a++) {
+        if (hipEventRecord(ctx->join[a], ctx->aux[a]) != hipSuccess) return NITRO_EHIP;
+        if (hipStreamWaitEvent(ctx->stream, ctx->join[a], 0) != hipSuccess) return NITRO_EHIP;
+    }
     // 4. IntegerSGD (Alg. 1) of every weight tensor, after every gradient is complete
     if (net->head) {
         st = sgd_entry(ctx, sgd, params->w_head, hdw, (int64_t)G * g.hd, hp->gamma_inv,
