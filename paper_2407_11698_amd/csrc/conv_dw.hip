@@ -2,23 +2,25 @@
 // gfx950 int8 MFMA, exact:
 //   dW[co][r][s][ci] = sum_p g[p][co] * x[p + (r-1, s-1)][ci]          (int64)
 //
-// Padded pixel planes. Both operands are first rewritten pixel-contiguous on a zero-padded
-// grid: every image row is followed by one zero column and every image by one zero row, so pixel
-// (n, h, w) sits at position k = (n (H+1) + h) (W+1) + w and each neighbour outside the image
-// lands on a zero. A tap (r, s) is then the plain position offset (r-1)(W+1) + (s-1):
-//   dW[co][r][s][ci] = sum_k gp[co][k] * xp[ci][h0 + k + (r-1)(W+1) + (s-1)]
-// with no bounds test. gp holds the balanced int8 limbs of g (one plane per limb, zeros at pad
-// positions); xp holds x with a zero halo of h0 >= W + 2 positions on both sides.
+// Padded pixel grid. Both operands are first rewritten on a zero-padded grid: every image row
+// is followed by one zero column and every image by one zero row, so pixel (n, h, w) sits at
+// position k = (n (H+1) + h) (W+1) + w and each neighbour outside the image lands on a zero. A
+// tap (r, s) is then the plain position offset (r-1)(W+1) + (s-1):
+//   dW[co][r][s][ci] = sum_k gp[co][k] * xr[ci][HMAX + k + (r-1)(W+1) + (s-1)]
+// with no bounds test. gp holds the balanced int8 limbs of g, one plane per limb, positions
+// contiguous (zeros at pad positions). xr holds x in rows of 16 channels: [C_in / 16][position]
+// [16 channels], with a zero halo of HMAX >= W + 2 positions on both sides.
 //
 // GEMM: M = co, N = ci (times 9 taps), K = padded positions. A workgroup owns a 64 co x 16 ci
 // tile, all 9 taps, over a range of K. Its four waves run independently (no barrier in the main
 // loop), each on one limb of g and one part of the range: with L limbs, Q = 4 / L parts (L = 3:
 // one part, one wave idle). A fragments (g limbs) are loaded from the planes straight into
-// registers, one 256-position super-step ahead. The x window of a super-step (plus the halo) is
-// staged in the wave's own double-buffered LDS slice; the fragment of tap (r, s) is read from it
-// at byte offset h0 + (r-1)(W+1) + (s-1), and a funnel shift (v_alignbit) realigns the dwords.
-// The waves' int32 sums, weighted 256^limb, are added in int64 through LDS at the end. A wave's
-// range is at most 511 * 256 positions, so |sum| <= 128 * 128 * 130816 < 2^31.
+// registers, one 256-position super-step ahead. The x rows of a super-step (plus the halo) are
+// staged in the wave's own double-buffered LDS slice, and the B fragment of tap (r, s) -- 16
+// positions of one channel per lane -- is read from them with two transposing LDS reads
+// (ds_read_b64_tr_b8) at a row offset of (r-1)(W+1) + (s-1). The waves' int32 sums, weighted
+// 256^limb, are added in int64 through LDS at the end. A wave's range is at most 511 * 256
+// positions, so |sum| <= 128 * 128 * 130816 < 2^31.
 #include <type_traits>
 
 #include "mfma_common.h"
@@ -28,17 +30,14 @@ namespace nitro {
 constexpr int DWP_KS = 256;        // padded positions per super-step (4 MFMA K-steps of 64)
 constexpr int DWP_HMAX = 64;       // largest halo: W <= 62
 constexpr int DWP_CHUNK_MAX = 511;    // super-steps per workgroup (and per wave: <= 511 * 256)
-constexpr int DWP_WIN = DWP_KS + 2 * DWP_HMAX;   // staged window of a super-step (bytes/row)
-constexpr int DWP_RS = DWP_WIN + 20;            // its LDS row stride: 101 dwords spreads the
-                                                // 16 rows x 4 lane groups evenly over the banks
-constexpr int DWP_NCH = 16 * DWP_WIN / 16 / 64;  // 16-byte chunks per lane (16 rows, 64 lanes)
+constexpr int DWP_WIN = DWP_KS + 2 * DWP_HMAX;   // staged rows (positions) of a super-step
+constexpr int DWP_NCH = DWP_WIN / 64;            // 16-byte rows per lane
 
 struct DwpGeom {
     int wp, hp;          // W + 1, H + 1
-    int h0;              // halo (multiple of 16, >= W + 2)
     int64_t kraw;        // positions of the padded grid: n (H+1) (W+1)
     int64_t kp;          // positions processed (kraw rounded up to a super-step)
-    int64_t xs;          // row length of an x plane (multiple of 64, >= kp + 2 HMAX)
+    int64_t xs;          // positions of an x row block: HMAX + kp + HMAX
 };
 
 DwpGeom dwp_geom(const ConvShape &sh)
@@ -46,7 +45,6 @@ DwpGeom dwp_geom(const ConvShape &sh)
     DwpGeom g;
     g.wp = sh.w + 1;
     g.hp = sh.h + 1;
-    g.h0 = (g.wp + 1 + 15) / 16 * 16;
     g.kraw = (int64_t)sh.n * g.hp * g.wp;
     g.kp = (g.kraw + DWP_KS - 1) / DWP_KS * DWP_KS;
     g.xs = g.kp + DWP_WIN - DWP_KS;   // the last super-step's window ends there
@@ -111,44 +109,28 @@ __device__ inline int padded_pixel(int k, int n, int h, int w, int hp, int wp)
 }
 
 // ---------------------------------------------------------------------------------------------
-// x int8 NHWC [P][C] -> xp [C16][xs], xp[c][h0 + k] = x at padded position k (zeros elsewhere
-// and in channels C..C16-1). A workgroup: 64 plane positions x 64 channels, transposed through
-// LDS.
-__global__ __launch_bounds__(256) void k_dwp_act_planes(const int8_t *__restrict__ x, int n, int h,
-                                                        int w, int c, int c16, int hp, int wp,
-                                                        int h0, int xs, int8_t *__restrict__ xp)
+// x int8 NHWC [P][C] -> xr [C16 / 16][xs][16]: row HMAX + k holds the 16 channels of tile t at
+// padded position k (zeros at pad positions, in the halo and in channels C..C16-1). One thread:
+// one 16-byte row.
+__global__ __launch_bounds__(256) void k_dwp_act_rows(const int8_t *__restrict__ x, int n, int h,
+                                                      int w, int c, int hp, int wp, int xs,
+                                                      int8_t *__restrict__ xr)
 {
-    __shared__ uint32_t T[64][17];       // [position][channel dword]
-    const int tid = threadIdx.x;
-    const int i0 = blockIdx.x * 64;
-    const int c0 = blockIdx.y * 64;
-    {
-        const int pi = tid >> 2, cq = tid & 3;
-        const int pix = padded_pixel(i0 + pi - h0, n, h, w, hp, wp);
-        const int ch = c0 + 16 * cq;
-        v4i v = v4i{0, 0, 0, 0};
+    const int i = blockIdx.x * 256 + threadIdx.x;     // row within the tile's block
+    const int t = blockIdx.y;                         // 16-channel tile
+    if (i >= xs) return;
+    const int pix = padded_pixel(i - DWP_HMAX, n, h, w, hp, wp);
+    const int ch = 16 * t;
+    v4i v = v4i{0, 0, 0, 0};
+    if (pix >= 0) {
         if ((c & 15) == 0) {
-            if (pix >= 0 && ch < c) v = *(const v4i *)(x + (int64_t)pix * c + ch);
-        } else if (pix >= 0) {
+            v = *(const v4i *)(x + (int64_t)pix * c + ch);
+        } else {
             for (int e = 0; e < 16 && ch + e < c; e++)
                 v[e >> 2] |= (int)((uint32_t)(uint8_t)x[(int64_t)pix * c + ch + e] << (8 * (e & 3)));
         }
-#pragma unroll
-        for (int u = 0; u < 4; u++) T[pi][4 * cq + u] = (uint32_t)v[u];
     }
-    __syncthreads();
-    const int cc = tid >> 2, pq = tid & 3;
-    if (c0 + cc >= c16) return;
-    v4i o;
-#pragma unroll
-    for (int q = 0; q < 4; q++) {
-        uint32_t d = 0;
-#pragma unroll
-        for (int b = 0; b < 4; b++)
-            d |= ((T[16 * pq + 4 * q + b][cc >> 2] >> (8 * (cc & 3))) & 0xFFu) << (8 * b);
-        o[q] = (int)d;
-    }
-    *(v4i *)(xp + (int64_t)(c0 + cc) * xs + i0 + 16 * pq) = o;
+    *(v4i *)(xr + ((int64_t)t * xs + i) * 16) = v;
 }
 
 // g int32 NHWC [P][C] -> gp [l][C][kp] for l < limbs(max|g|): limb l of g at padded position k
@@ -218,9 +200,9 @@ __global__ __launch_bounds__(256) void k_dwp_grad_planes(const int32_t *__restri
 struct DwpArgs {
     const int8_t *gp;      // [LA][co][kp]
     int64_t kp;
-    const int8_t *xp;      // [ci][xs]
+    const int8_t *xr;      // [ci / 16][xs][16]
     int64_t xs;
-    int h0, wp, co, ci;          // ci: computed input channels (a multiple of 16)
+    int wp, co, ci;              // ci: computed input channels (a multiple of 16)
     int ci_out;                  // input channels of dW (<= ci)
     int tiles_ci, tiles_co, nss, chunk;
     const uint32_t *gmax;
@@ -229,10 +211,13 @@ struct DwpArgs {
     uint64_t *ts;          // timing slot (null: untimed)
 };
 
-// bits [b, b + 32) of the 64-bit value hi:lo (v_alignbit_b32), 0 <= b < 32
-__device__ inline uint32_t funnel_shr(uint32_t hi, uint32_t lo, uint32_t bits)
+typedef int v2i __attribute__((ext_vector_type(2)));
+
+// Transposing LDS read (gfx950 ds_read_b64_tr_b8). Within each group of 16 lanes, output lane
+// 8 h + j receives, as its byte b (b = 0..7), byte j of the 8 bytes addressed by lane 2 b + h.
+__device__ inline v2i lds_read_tr8(const uint8_t *p)
 {
-    return __builtin_amdgcn_alignbit(hi, lo, bits);
+    return __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) v2i *)p);
 }
 
 // Wave-local LDS hand-off: this wave's LDS writes are complete before its later reads, and the
@@ -270,8 +255,8 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
     const int wb = sb + part * per < se ? sb + part * per : se;
     const int nst = limb < LA ? (wb + per < se ? wb + per : se) - wb : 0;
 
-    constexpr int RS = DWP_RS, CR = DWP_WIN / 16;
-    uint8_t *wl = lds + wave * (2 * 16 * RS);  // this wave's two stages [16 rows][RS]
+    constexpr int STAGE = DWP_WIN * 16;        // bytes of one staged window (rows of 16 B)
+    uint8_t *wl = lds + wave * (2 * STAGE);    // this wave's two stages
 
     const int j = lane & 15, g4 = lane >> 4;
     // 32-bit offsets from the plane bases (the host checks that both fit)
@@ -283,28 +268,17 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
         const int row = co0 + 16 * i + j < p.co ? co0 + 16 * i + j : p.co - 1;
         aoff[i] = (uint32_t)row * (uint32_t)p.kp + 16 * g4;
     }
-    // staged chunks of this lane: chunk lane + 64 m of the 16 x CR window
-    const int8_t *xbase = p.xp + (int64_t)ci0 * p.xs;
-    uint32_t boff[DWP_NCH];
-    int bdst[DWP_NCH];
+    // this wave's x rows: the window of super-step ss is rows ss KS .. ss KS + WIN of the tile's
+    // row block, contiguous; lane stages rows lane + 64 m
+    const int8_t *xbase = p.xr + (int64_t)tci * p.xs * 16;
+    // B fragment of tap t at K-step u: the transposing reads of lane s = 16 q + 2 b + h take row
+    // HMAX + off_t + 64 u + 16 q + b (+ 8), bytes 8 h .. 8 h + 7 (the channels 8 h + j of lane
+    // 8 h + j)
+    const int lane_row = 16 * g4 + ((lane & 15) >> 1);
+    const int lane_b = (DWP_HMAX + lane_row) * 16 + 8 * (lane & 1);
+    int toff[9];
 #pragma unroll
-    for (int m = 0; m < DWP_NCH; m++) {
-        const int c = lane + 64 * m;
-        const int row = c / CR, col = c - row * CR;
-        boff[m] = (uint32_t)row * (uint32_t)p.xs + 16 * col;
-        bdst[m] = row * RS + 16 * col;
-    }
-    // tap (r, s): byte offset o = h0 + (r-1) wp + (s-1) >= 0 of its fragment in the window
-    int tq[9];
-    uint32_t tsh[9];
-#pragma unroll
-    for (int t = 0; t < 9; t++) {
-        const int o = p.h0 + (t / 3 - 1) * p.wp + (t % 3 - 1);
-        tq[t] = o >> 2;
-        tsh[t] = (uint32_t)(o & 3) * 8;
-    }
-    const int lane_b = j * RS + 16 * g4;
-
+    for (int t = 0; t < 9; t++) toff[t] = ((t / 3 - 1) * p.wp + (t % 3 - 1)) * 16;
     // Pipeline (per wave, super-step s): at its start the x window of s + 1 is requested; s
     // computes from LDS stage s & 1, and each K-step's A fragments are requested for s + 1 as
     // soon as that K-step has used them; at its end the window of s + 1 goes to LDS stage
@@ -313,7 +287,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
     // of every accumulator on every iteration.
     v4i acc[9][4];
     v4i a[4][4];                 // A fragments [K-step][co tile]
-    v4i bst[DWP_NCH];            // staged x window
+    v4i bst[DWP_NCH];            // staged x rows
 
     auto load_a = [&](int u, int ss, int l) {
         const uint32_t k = (uint32_t)ss * DWP_KS + (uint32_t)l * plane + 64 * u;
@@ -321,34 +295,24 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
         for (int i = 0; i < 4; i++) a[u][i] = *(const v4i *)(p.gp + (aoff[i] + k));
     };
     auto load_b = [&](int ss) {
-        const uint32_t k = (uint32_t)ss * DWP_KS;
+        const int8_t *src = xbase + ((int64_t)ss * DWP_KS + lane) * 16;
 #pragma unroll
-        for (int m = 0; m < DWP_NCH; m++) bst[m] = *(const v4i *)(xbase + (boff[m] + k));
+        for (int m = 0; m < DWP_NCH; m++) bst[m] = *(const v4i *)(src + 64 * 16 * m);
     };
     auto store_b = [&](int stage) {
-        uint8_t *dst = wl + stage * 16 * RS;
+        uint8_t *dst = wl + stage * STAGE + lane * 16;
 #pragma unroll
-        for (int m = 0; m < DWP_NCH; m++) {
-            uint32_t *d = (uint32_t *)(dst + bdst[m]);
-            d[0] = (uint32_t)bst[m][0];
-            d[1] = (uint32_t)bst[m][1];
-            d[2] = (uint32_t)bst[m][2];
-            d[3] = (uint32_t)bst[m][3];
-        }
+        for (int m = 0; m < DWP_NCH; m++) *(v4i *)(dst + 64 * 16 * m) = bst[m];
     };
     auto compute = [&](auto first, auto reload, int stage, int next, int l) {
-        const uint8_t *base = wl + stage * 16 * RS + lane_b;
+        const uint8_t *base = wl + stage * STAGE + lane_b;
 #pragma unroll
         for (int u = 0; u < 4; u++) {
 #pragma unroll
             for (int t = 0; t < 9; t++) {
-                const uint32_t *s = (const uint32_t *)(base + 64 * u) + tq[t];
-                const uint32_t d0 = s[0], d1 = s[1], d2 = s[2], d3 = s[3], d4 = s[4];
-                v4i b;
-                b[0] = (int)funnel_shr(d1, d0, tsh[t]);
-                b[1] = (int)funnel_shr(d2, d1, tsh[t]);
-                b[2] = (int)funnel_shr(d3, d2, tsh[t]);
-                b[3] = (int)funnel_shr(d4, d3, tsh[t]);
+                const uint8_t *r = base + toff[t] + 64 * 16 * u;
+                const v2i lo = lds_read_tr8(r), hi = lds_read_tr8(r + 8 * 16);
+                const v4i b = v4i{lo[0], lo[1], hi[0], hi[1]};
 #pragma unroll
                 for (int i = 0; i < 4; i++)
                     acc[t][i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(
@@ -424,21 +388,20 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
     const DwpGeom ge = dwp_geom(sh);
     const DwpPlan pl = dwp_plan(sh);
     const int c16 = dwp_c16(sh);
-    hipLaunchKernelGGL(k_dwp_act_planes, dim3((unsigned)(ge.xs / 64), (unsigned)((c16 + 63) / 64)),
-                       dim3(256), 0, s, x, sh.n, sh.h, sh.w, sh.c, c16, ge.hp, ge.wp, ge.h0,
-                       (int)ge.xs, xp);
+    hipLaunchKernelGGL(k_dwp_act_rows, dim3((unsigned)((ge.xs + 255) / 256), (unsigned)(c16 / 16)),
+                       dim3(256), 0, s, x, sh.n, sh.h, sh.w, sh.c, ge.hp, ge.wp, (int)ge.xs, xp);
     hipLaunchKernelGGL(k_dwp_grad_planes, dim3((unsigned)(ge.kp / 64), (unsigned)((sh.co + 63) / 64)),
                        dim3(256), 0, s, g, sh.n, sh.h, sh.w, sh.co, ge.hp, ge.wp, (int)ge.kp, gmax, gp,
                        gn);
     DwpArgs a{};
     a.gp = gp; a.kp = ge.kp;
-    a.xp = xp; a.xs = ge.xs;
-    a.h0 = ge.h0; a.wp = ge.wp; a.co = sh.co; a.ci = c16; a.ci_out = sh.c;
+    a.xr = xp; a.xs = ge.xs;
+    a.wp = ge.wp; a.co = sh.co; a.ci = c16; a.ci_out = sh.c;
     a.tiles_ci = pl.tiles_ci; a.tiles_co = pl.tiles_co; a.nss = pl.nss; a.chunk = pl.chunk;
     a.gmax = gmax;
     a.out = pl.nsplit > 1 ? part : dw;
     a.flags = flags;
-    const size_t lds_stage = (size_t)4 * 2 * 16 * DWP_RS, lds_red = (size_t)4 * 3 * 1024 * 4;
+    const size_t lds_stage = (size_t)4 * 2 * DWP_WIN * 16, lds_red = (size_t)4 * 3 * 1024 * 4;
     const unsigned nwg = (unsigned)(pl.tiles_co * pl.tiles_ci * pl.nsplit);
     a.ts = timer_slot(TIMED_DW);
     hipLaunchKernelGGL(k_conv_dw_planes, dim3(nwg), dim3(256), lds_stage > lds_red ? lds_stage : lds_red,
