@@ -8,7 +8,9 @@ steps the weights are reset to their initial values, so each timed step is one o
 verified iterations.
 
 Prints one JSON line with the throughput, the roofline position of the dominant kernel (its own
-HIP-event time inside the timed region) and the CPU oracle's throughput on a bounded sample.
+device time inside the timed region, from timestamps its workgroups record), the single
+conv-layer stress case's kernels measured alone after the timed region, and the CPU oracle's
+throughput on a bounded sample.
 """
 from __future__ import annotations
 
@@ -64,6 +66,64 @@ def conv_layer_ops(wl):
     return ops
 
 
+def limbs_for(m: int) -> int:
+    """Balanced signed base-256 int8 limbs needed for magnitudes up to m (|v| <= m)."""
+    return 1 if m <= 127 else 2 if m <= 32639 else 3 if m <= 8355711 else 4
+
+
+def stress_layer(reps: int):
+    """The single conv-layer stress case (256x256x32x32 int8 activations, conv 256 -> 256, int32
+    error signal in [-2^15, 2^15] at the NITRO-ReLU output), its forward and back-propagation
+    run alone on the GPU, `reps` times, with each kernel's own device time. Outside the timed
+    region of the training iterations.
+
+    Algorithmic ops count each GEMM once (2 x N*H*W*C_out*9*C_in); MFMA ops count every limb
+    pass the kernel executes (the error signal needs 3 int8 limbs at this bound)."""
+    import torch
+    from paper_2407_11698_amd import runner
+    from paper_2407_11698_amd import workloads as WL
+    wl = WL.CONV_STRESS
+    dr = WL.draw_workload(wl, runner.kaiming_bound)
+    dev = torch.device("cuda", 0)
+    st = runner.GpuConvStress(wl, dr.weights[0])
+    xd = torch.from_numpy(dr.batches[0][0]).to(dev)
+    dd = torch.from_numpy(dr.delta).to(dev)
+    g = torch.empty(dd.shape, dtype=torch.int32, device=dev)
+
+    def once():
+        st.ctx.block_forward(st.desc, [st.w], xd, st.a, st.state)
+        st.ctx.block_backward(st.desc, [st.w], None, xd, st.a, None, dd, st.state, [st.dw], None,
+                              {"dx": st.dx, "g": [g]})
+
+    once()
+    st.ctx.sync()
+    st.ctx.kernel_timing(True)
+    for _ in range(reps):
+        once()
+    st.ctx.sync()
+    kt = {name: st.ctx.kernel_time(c) for c, name in KERNEL_CLASSES.items()}
+    st.ctx.kernel_timing(False)
+    ly = wl.blocks[0].layers[0]
+    c, h, w = wl.in_shape
+    macs = wl.batch * h * w * ly.c_out * 9 * ly.c_in
+    lw = limbs_for(int(st.w.abs().max().item()))
+    lg = limbs_for(int(g.abs().max().item()))
+    passes = {"k_conv_tile<fwd>": lw, "k_conv_tile<dx>": lg * lw, "k_conv_dw_planes": lg}
+    out = {}
+    for name, (ms, launches) in kt.items():
+        if launches == 0:
+            continue
+        per = ms * 1e-3 / reps
+        tops = 2 * macs / per / 1e12
+        out[name] = {"avg_launch_us": round(ms * 1e3 / launches, 2), "launches": launches,
+                     "ms_per_pass": round(ms / reps, 4), "algorithmic_TOPs": round(tops, 2),
+                     "frac": round(tops / PEAK_INT8_TOPS, 4), "limb_passes": passes[name],
+                     "mfma_TOPs": round(tops * passes[name], 2),
+                     "mfma_frac": round(tops * passes[name] / PEAK_INT8_TOPS, 4)}
+    del st, xd, dd, g
+    return {"workload": wl.name, "repeats": reps, "kernels": out}
+
+
 def cpu_baseline(wl, min_s: float = 12.0, budget_s: float = 25.0):
     """The CPU oracle, untuned, on a bounded sample of the same workload: full training
     iterations at a reduced batch (cycling through the ten seeded batches) until at least
@@ -100,6 +160,9 @@ def main():
     ap.add_argument("--eager", action="store_true",
                     help="launch every kernel from the host each step instead of replaying the "
                          "captured iteration (nitro_train_step_graph)")
+    ap.add_argument("--stress-reps", type=int, default=10,
+                    help="repeats of the single conv-layer stress case measured after the "
+                         "training iterations (0 skips it)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB before the warm-up: "
                          "the known-size reference for hardware byte counters")
@@ -205,6 +268,8 @@ def main():
                       "frac_of_int8_peak": round(conv_tops / PEAK_INT8_TOPS, 5),
                       "per_kernel": per_class},
     }
+    if args.stress_reps > 0:
+        out["stress_conv"] = stress_layer(args.stress_reps)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(out), flush=True)

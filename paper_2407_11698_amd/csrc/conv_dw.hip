@@ -179,11 +179,13 @@ __global__ __launch_bounds__(256) void k_dwp_grad_planes(const int32_t *__restri
         }
     }
     __syncthreads();
+    // the weight-gradient kernel reads every odd block of 16 positions with its two halves of 8
+    // exchanged (its transposing LDS reads take them in that order); the planes store them so
     const int cc = tid >> 2, pq = tid & 3;
     if (c0 + cc >= c) return;
     int32_t v[16];
 #pragma unroll
-    for (int e = 0; e < 16; e++) v[e] = T[16 * pq + e][cc];
+    for (int e = 0; e < 16; e++) v[e] = T[16 * pq + (e ^ ((pq & 1) << 3))][cc];
 #pragma unroll
     for (int l = 0; l < 4; l++) {
         if (l < LA) {
@@ -273,9 +275,12 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
     const int8_t *xbase = p.xr + (int64_t)tci * p.xs * 16;
     // B fragment of tap t at K-step u: the transposing reads of lane s = 16 q + 2 b + h take row
     // HMAX + off_t + 64 u + 16 q + b (+ 8), bytes 8 h .. 8 h + 7 (the channels 8 h + j of lane
-    // 8 h + j)
-    const int lane_row = 16 * g4 + ((lane & 15) >> 1);
+    // 8 h + j). Lane groups q odd read the rows + 8 first: in each read the two groups of 16
+    // lanes that share an LDS cycle then use different halves of the banks. Their A fragments
+    // hold the same order (odd 16-position blocks of the g planes have their halves exchanged).
+    const int lane_row = 16 * g4 + ((lane & 15) >> 1) + 8 * (g4 & 1);
     const int lane_b = (DWP_HMAX + lane_row) * 16 + 8 * (lane & 1);
+    const int second = (g4 & 1) ? -8 * 16 : 8 * 16;
     int toff[9];
 #pragma unroll
     for (int t = 0; t < 9; t++) toff[t] = ((t / 3 - 1) * p.wp + (t % 3 - 1)) * 16;
@@ -311,7 +316,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 #pragma unroll
             for (int t = 0; t < 9; t++) {
                 const uint8_t *r = base + toff[t] + 64 * 16 * u;
-                const v2i lo = lds_read_tr8(r), hi = lds_read_tr8(r + 8 * 16);
+                const v2i lo = lds_read_tr8(r), hi = lds_read_tr8(r + second);
                 const v4i b = v4i{lo[0], lo[1], hi[0], hi[1]};
 #pragma unroll
                 for (int i = 0; i < 4; i++)

@@ -9,26 +9,45 @@
 // on each side, zeros outside the image. The A fragment of tap (r, s) is then the LDS pixel at
 // offset (r-1)(W+2) + (s-1) from the output pixel (the opposite offset for the input gradient):
 // the nine taps share one staging and need no bounds tests. The B operand (4 packed limb planes
-// of W, [N][9 ck], tap-major) is read from global memory one K-step ahead. Operands wider than
-// int8 are split into balanced int8 limbs; each limb pair is one pass over K accumulated in int32
-// (|sum| <= 128 * 128 * 9 * 8192 < 2^31) and folded into int64 with its shift.
+// of W, [N][9 ck], tap-major) is staged beside it, the nine taps of the chunk for the tile's 64
+// columns. Operands wider than int8 are split into balanced int8 limbs; each limb pair is one
+// pass over K accumulated in int32 (|sum| <= 128 * 128 * 9 * 8192 < 2^31) and folded into int64
+// with its shift.
+#include <type_traits>
+
 #include "mfma_common.h"
 
 namespace nitro {
 
 enum { IG_FWD = 0, IG_DX = 1 };
 
-constexpr int CT_BM = 128;         // output pixels per workgroup
 constexpr int CT_BN = 64;          // GEMM columns per workgroup
-constexpr int CT_NPMAX = 320;      // largest staged pixel count (W >= 4)
 
-template <int CC>
+// Tile shapes. WM = 2: 128 output pixels, 4 waves, one LDS stage (two workgroups per CU).
+// WM = 4: 256 output pixels, 8 waves, two LDS stages (one workgroup per CU), the next phase's
+// operands written to the idle stage while the current one computes.
+template <int WM>
+struct CtShape {
+    static constexpr int BM = 64 * WM;                  // output pixels per workgroup
+    static constexpr int NT = 128 * WM;                 // threads
+    static constexpr int NPMAX = WM == 2 ? 320 : 448;   // largest staged pixel count
+    static constexpr int NBUF = WM == 2 ? 1 : 2;        // LDS stages
+};
+
+// LDS stages. A: [pixel][PS bytes], PS = 96 for chunks of 32 or 64 channels (a fragment read,
+// 16 consecutive pixels by 4 lane groups, then touches every bank once per cycle). B:
+// [tap][column][CC bytes]; with 64 channels the 16-byte unit u of column c sits in slot
+// u ^ ((c >> 1) & 3), which keeps both its fragment reads and the staging writes (4 lanes per
+// column) free of bank conflicts.
+template <int CC, int WM>
 struct CtCfg {
-    static constexpr int PS = CC == 16 ? 16 : CC == 32 ? 48 : 80;   // LDS bytes per pixel
+    static constexpr int PS = CC == 16 ? 16 : 96;      // LDS bytes per staged pixel
     static constexpr int GPT = CC / 16;                 // 16-channel groups per tap and chunk
     static constexpr int KSC = (9 * GPT + 3) / 4;        // K-steps (of 4 groups) per chunk
-    static constexpr int NIT = (CT_NPMAX * GPT + 255) / 256;   // staged 16-byte items per thread
+    static constexpr int NIT = (CtShape<WM>::NPMAX * GPT + CtShape<WM>::NT - 1) / CtShape<WM>::NT;
 };
+
+__host__ __device__ constexpr int ct_bswz(int cc, int c) { return cc == 64 ? (c >> 1) & 3 : 0; }
 
 struct TileArgs {
     int n, h, w;
@@ -43,7 +62,7 @@ struct TileArgs {
     int rt, ns, rs;                // image rows per tile; images per tile; rows per image segment
     Div32 d_w2, d_seg, d_w, d_rw;  // reciprocals of W + 2, (rs + 2)(W + 2), W and rs W
     // forward epilogue
-    ScaleRelu32 sr;
+    ScaleFast sf;
     int pool;
     int8_t *out;
     uint8_t *code;
@@ -62,35 +81,50 @@ __device__ inline int32_t sat_i32(int64_t v)
     return v > INT32_MAX ? INT32_MAX : (v < INT32_MIN ? INT32_MIN : (int32_t)v);
 }
 
-// One tile per workgroup. B fragments are prefetched BD K-steps ahead (a ring of BD + 1 register
-// sets, the K-step loop unrolled per chunk); the next chunk's A staging is loaded while the
-// current chunk computes.
-template <int MODE, int CC>
-__global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
+// One tile per workgroup. Both operands go through LDS: each phase (a limb pair and a chunk of CC
+// channels) stages the A pixels and the B block of 9 taps x 64 columns x CC. The next phase's
+// global loads are issued before the current phase computes; the fragments of the next K-step
+// are read from LDS while the MFMAs of the current one run.
+template <int MODE, int CC, int WM>
+__global__ __launch_bounds__(128 * WM) void k_conv_tile(TileArgs p)
 {
-    using C = CtCfg<CC>;
+    using S = CtShape<WM>;
+    using C = CtCfg<CC, WM>;
+    constexpr int BM = S::BM, NT = S::NT;
     constexpr int TM = 4, TN = 2;                 // 16x16 tiles per wave: 64 pixels x 32 columns
-    constexpr int BD = 3;                         // B prefetch distance (K-steps)
-    constexpr int STAGE = CT_NPMAX * C::PS;
-    constexpr int SMEM_A = 2 * STAGE;
-    constexpr int OS = CT_BN + 16;                // epilogue byte-tile row stride (forward)
-    constexpr int GS = CT_BN + 1;                 // epilogue int32-tile row stride (input gradient)
-    constexpr int SMEM_EPI = MODE == IG_FWD ? 2 * CT_BM * OS : CT_BM * GS * 4;
-    constexpr int SMEM = SMEM_A > SMEM_EPI ? SMEM_A : SMEM_EPI;
+    constexpr int NU = CC / 16;                   // 16-byte units per (tap, column) row of B
+    constexpr int SA = S::NPMAX * C::PS;          // A stage bytes
+    constexpr int BITEMS = 9 * CT_BN * NU;        // 16-byte units of a B stage
+    constexpr int BIT = (BITEMS + NT - 1) / NT;   // B units per thread
+    constexpr int SAB = SA + BITEMS * 16;         // one stage
+    constexpr int OS = CT_BN + 16;                // forward epilogue: LDS row stride in bytes
+    constexpr int SMEM_EPI = MODE == IG_FWD ? 2 * BM * OS : 0;
+    constexpr int SMEM_MAIN = S::NBUF * SAB > SMEM_EPI ? S::NBUF * SAB : SMEM_EPI;
+    constexpr int SMEM = SMEM_MAIN + (MODE == IG_FWD ? 528 : 0);   // + the NITRO-ReLU table
     __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
 
     ts_start(p.ts);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int g4 = lane >> 4;
+    uint16_t *const tab = (uint16_t *)(smem + SMEM_MAIN);   // forward: entry for zs = -128 .. 128
+    if (MODE == IG_FWD)
+        for (int k = tid; k < 257; k += NT) tab[k] = relu_table_entry(k - 128, p.sf);
+    // tile of this workgroup: the eight XCDs each take a contiguous range of tiles, so the column
+    // tiles of one pixel tile run together and share their A rows in that XCD's L2
+    const int ntile_n = (p.no + CT_BN - 1) / CT_BN;
+    const int ntiles = (int)gridDim.x;
+    int tile = blockIdx.x;
+    if ((ntiles & 7) == 0) tile = (tile & 7) * (ntiles >> 3) + (tile >> 3);
+    const int mt = tile / ntile_n, nt = tile - mt * ntile_n;
     const int W2 = p.w + 2;
     const int segpx = (p.rs + 2) * W2;
     const int np = p.ns * segpx;
-    const int R0 = blockIdx.x * p.rt;              // first image row of the tile (over all images)
+    const int R0 = mt * p.rt;                      // first image row of the tile (over all images)
     const int img0 = R0 / p.h, row0 = R0 - img0 * p.h;
     const int64_t M = (int64_t)p.n * p.h * p.w;
     const int64_t m0 = (int64_t)R0 * p.w;
-    const int n0 = blockIdx.y * CT_BN;
+    const int n0 = nt * CT_BN;
     const int K = 9 * p.ck;
     const int nchunk = p.ck / CC;
 
@@ -101,14 +135,20 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
         return;
     }
     const int npass = LA * LB;
+    const int nph = npass * nchunk;
 
-    // staged items of this thread: item tid + 256 v = (LDS pixel q, 16-channel group e); the
-    // global byte offset within a chunk, or -1 for a zero (outside the image)
+    // staged A items of this thread: item tid + NT v = (LDS pixel q, 16-channel group e), the
+    // groups of one pixel on consecutive lanes; the global byte offset within a chunk, or -1 for
+    // a zero (outside the image)
+    auto a_item = [&](int item, int &q, int &e) {
+        q = item / C::GPT;
+        e = item - q * C::GPT;
+    };
     int it_g[C::NIT];
 #pragma unroll
     for (int v = 0; v < C::NIT; v++) {
-        const int item = tid + 256 * v;
-        const int q = item / C::GPT, e = item - q * C::GPT;
+        int q, e;
+        a_item(tid + NT * v, q, e);
         it_g[v] = -1;
         if (q < np) {
             const int seg = (int)udiv32(q, p.d_seg), r = q - seg * segpx;
@@ -118,50 +158,71 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
                 it_g[v] = ((img * p.h + hh) * p.w + ww) * p.ck + 16 * e;
         }
     }
+    // staged B units of this thread: unit tid + NT v is (tap t, column c, unit u), the units of a
+    // column on consecutive lanes; c and u are fixed by tid and t = v TPV + t0
+    constexpr int TPV = NT / (CT_BN * NU);        // taps per NT units
+    const int b_c = (tid % (CT_BN * NU)) / NU, b_u = tid % NU, b_t0 = tid / (CT_BN * NU);
+    const int b_g0 = (n0 + b_c < p.no ? n0 + b_c : p.no - 1) * K + b_t0 * p.ck + 16 * b_u;
+    const int b_l0 = (b_t0 * CT_BN + b_c) * CC + 16 * (b_u ^ ct_bswz(CC, b_c));
     int cpix[TM];
 #pragma unroll
     for (int i = 0; i < TM; i++) {
         const int mloc = wm * 64 + 16 * i + (lane & 15);
         const int seg = (int)udiv32(mloc, p.d_rw), rem = mloc - seg * p.rs * p.w;
         const int row = (int)udiv32(rem, p.d_w), col = rem - row * p.w;
-        cpix[i] = seg * segpx + (row + 1) * W2 + col + 1;
+        cpix[i] = (seg * segpx + (row + 1) * W2 + col + 1) * C::PS;
     }
-    int brow[TN];
+    // LDS byte offset of this lane's B unit in each column tile (tap 0): column c, unit c16 of
+    // the lane's group (fixed per lane: 4 ks + g4 = g4 modulo GPT)
+    const int c16l = g4 % C::GPT;
+    int bcol[TN];
 #pragma unroll
     for (int j = 0; j < TN; j++) {
-        const int col = n0 + wn * 32 + 16 * j + (lane & 15);
-        brow[j] = (col < p.no ? col : p.no - 1) * K;
+        const int c = wn * 32 + 16 * j + (lane & 15);
+        bcol[j] = c * CC + 16 * (c16l ^ ct_bswz(CC, c));
     }
     const int sgn = MODE == IG_FWD ? 1 : -1;
 
-    v4i stg[C::NIT];
-    auto stage_load = [&](int la, int chunk) {
-        const int8_t *src = p.a + (int64_t)la * p.aplane + chunk * CC;
+    v4i stga[C::NIT], stgb[BIT];
+    auto stage_load = [&](int ph) {
+        const int chunk = ph % nchunk, pass = ph / nchunk;
+        const int la = pass / LB, lb = pass - la * LB;
+        const int8_t *srca = p.a + (int64_t)la * p.aplane + chunk * CC;
 #pragma unroll
-        for (int v = 0; v < C::NIT; v++) stg[v] = *(const v4i *)(src + (it_g[v] >= 0 ? it_g[v] : 0));
+        for (int v = 0; v < C::NIT; v++) stga[v] = *(const v4i *)(srca + (it_g[v] >= 0 ? it_g[v] : 0));
+        const int8_t *srcb = p.b + (int64_t)lb * p.bplane + chunk * CC + b_g0;
+#pragma unroll
+        for (int v = 0; v < BIT; v++)
+            if (b_t0 + v * TPV < 9) stgb[v] = *(const v4i *)(srcb + v * TPV * p.ck);
     };
     auto stage_store = [&](int buf) {
-        uint8_t *dst = smem + buf * STAGE;
+        uint8_t *As = smem + buf * SAB, *Bs = As + SA;
 #pragma unroll
         for (int v = 0; v < C::NIT; v++) {
-            const int item = tid + 256 * v;
-            const int q = item / C::GPT, e = item - q * C::GPT;
-            if (q < np) *(v4i *)(dst + q * C::PS + 16 * e) = it_g[v] >= 0 ? stg[v] : v4i{0, 0, 0, 0};
+            int q, e;
+            a_item(tid + NT * v, q, e);
+            if (q < np) *(v4i *)(As + q * C::PS + 16 * e) = it_g[v] >= 0 ? stga[v] : v4i{0, 0, 0, 0};
         }
-    };
-    auto kslice = [&](int ks, int &t, int &c16) {
-        const int G = 4 * ks + g4;
-        t = G / C::GPT;
-        c16 = G - t * C::GPT;
-    };
-    // B fragments of K-step ks of a chunk
-    auto load_b = [&](v4i(&dst)[TN], int lb, int chunk, int ks) {
-        int t, c16;
-        kslice(ks, t, c16);
-        const int tc = t < 9 ? t : 8;
-        const int8_t *src = p.b + (int64_t)lb * p.bplane + tc * p.ck + chunk * CC + 16 * c16;
 #pragma unroll
-        for (int j = 0; j < TN; j++) dst[j] = *(const v4i *)(src + brow[j]);
+        for (int v = 0; v < BIT; v++)
+            if (b_t0 + v * TPV < 9) *(v4i *)(Bs + b_l0 + v * NT * 16) = stgb[v];
+    };
+    // fragments of K-step ks: group G = 4 ks + g4 is (tap t, 16-channel group c16); a K-step past
+    // the ninth tap (chunks of 16 or 32 channels) has zero A fragments
+    auto load_frags = [&](const uint8_t *As, v4i(&af)[TM], v4i(&bf)[TN], int ks) {
+        const uint8_t *Bs = As + SA;
+        const int G = 4 * ks + g4;
+        const int t = G / C::GPT, c16 = G - t * C::GPT;
+        const bool valid = t < 9;
+        const int tc = valid ? t : 8;
+        const int toff = sgn * ((tc / 3 - 1) * W2 + (tc % 3 - 1)) * C::PS + 16 * c16;
+#pragma unroll
+        for (int i = 0; i < TM; i++) {
+            const v4i v = *(const v4i *)(As + cpix[i] + toff);
+            af[i] = valid ? v : v4i{0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int j = 0; j < TN; j++) bf[j] = *(const v4i *)(Bs + tc * CT_BN * CC + bcol[j]);
     };
 
     int64_t acc64[TM][TN][4];
@@ -177,181 +238,219 @@ __global__ __launch_bounds__(256) void k_conv_tile(TileArgs p)
 #pragma unroll
         for (int j = 0; j < TN; j++) acc[i][j] = v4i{0, 0, 0, 0};
 
-    for (int la = 0; la < LA; la++) {
-        for (int lb = 0; lb < LB; lb++) {
-            stage_load(la, 0);
-            stage_store(0);
-            __syncthreads();
-            for (int chunk = 0; chunk < nchunk; chunk++) {
-                const bool more = chunk + 1 < nchunk;
-                if (more) stage_load(la, chunk + 1);
-                v4i bq[BD + 1][TN];               // ring of prefetched B fragments
+    auto compute = [&](const uint8_t *As) {
+        v4i af[2][TM], bf[2][TN];
+        load_frags(As, af[0], bf[0], 0);
 #pragma unroll
-                for (int d = 0; d < BD && d < C::KSC; d++) load_b(bq[d], lb, chunk, d);
-                const uint8_t *As = smem + (chunk & 1) * STAGE;
+        for (int ks = 0; ks < C::KSC; ks++) {
+            if (ks + 1 < C::KSC) load_frags(As, af[(ks + 1) & 1], bf[(ks + 1) & 1], ks + 1);
 #pragma unroll
-                for (int ks = 0; ks < C::KSC; ks++) {
-                    if (ks + BD < C::KSC) load_b(bq[(ks + BD) % (BD + 1)], lb, chunk, ks + BD);
-                    int t, c16;
-                    kslice(ks, t, c16);
-                    const bool valid = t < 9;
-                    const int tc = valid ? t : 8;
-                    const int toff = sgn * ((tc / 3 - 1) * W2 + (tc % 3 - 1));
-                    v4i af[TM];
+            for (int i = 0; i < TM; i++)
 #pragma unroll
-                    for (int i = 0; i < TM; i++) {
-                        const v4i v = *(const v4i *)(As + (cpix[i] + toff) * C::PS + 16 * c16);
-                        af[i] = valid ? v : v4i{0, 0, 0, 0};
-                    }
-#pragma unroll
-                    for (int i = 0; i < TM; i++)
-#pragma unroll
-                        for (int j = 0; j < TN; j++)
-                            acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bq[ks % (BD + 1)][j],
-                                                                              acc[i][j], 0, 0, 0);
-                }
-                if (more) stage_store((chunk + 1) & 1);
-                __syncthreads();
-            }
-            if (npass > 1) {
-                // fold this limb pass into int64 with its weight 256^(la + lb)
-                const int64_t sh = (int64_t)1 << (8 * (la + lb));
-#pragma unroll
-                for (int i = 0; i < TM; i++)
-#pragma unroll
-                    for (int j = 0; j < TN; j++) {
-#pragma unroll
-                        for (int t = 0; t < 4; t++) acc64[i][j][t] += (int64_t)acc[i][j][t] * sh;
-                        acc[i][j] = v4i{0, 0, 0, 0};
-                    }
-            }
+                for (int j = 0; j < TN; j++)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bf[ks & 1][j], af[ks & 1][i],
+                                                                      acc[i][j], 0, 0, 0);
         }
-    }
-    auto value = [&](int i, int j, int t) -> int64_t {
-        return npass > 1 ? acc64[i][j][t] : (int64_t)acc[i][j][t];
+    };
+    auto fold = [&](int ph) {
+        if (npass > 1 && (ph + 1) % nchunk == 0) {
+            // fold this limb pass into int64 with its weight 256^(la + lb)
+            const int pass = ph / nchunk, la = pass / LB, lb = pass - la * LB;
+            const int64_t sh = (int64_t)1 << (8 * (la + lb));
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++) {
+#pragma unroll
+                    for (int t = 0; t < 4; t++) acc64[i][j][t] += (int64_t)acc[i][j][t] * sh;
+                    acc[i][j] = v4i{0, 0, 0, 0};
+                }
+        }
     };
 
+    stage_load(0);
+    if (S::NBUF == 1) {
+        for (int ph = 0; ph < nph; ph++) {
+            __syncthreads();                      // every wave is done with the previous stage
+            stage_store(0);
+            __syncthreads();
+            if (ph + 1 < nph) stage_load(ph + 1);
+            compute(smem);
+            fold(ph);
+        }
+    } else {
+        // stage ph & 1 is complete after the barrier of iteration ph; the other stage was last
+        // read in iteration ph - 1, before that barrier, so it can take phase ph + 1's operands
+        stage_store(0);
+        for (int ph = 0; ph < nph; ph++) {
+            __syncthreads();
+            if (ph + 1 < nph) stage_load(ph + 1);
+            compute(smem + (ph & 1) * SAB);
+            fold(ph);
+            if (ph + 1 < nph) stage_store((ph + 1) & 1);
+        }
+    }
+    __syncthreads();                              // the epilogue reuses the stages' LDS
     // ---------------------------------------------------------------- epilogues
+    // The MFMAs took B as the first operand: lane l of tile (i, j) holds output channels
+    // cb = wn 32 + 16 j + 4 g4 .. cb + 3 of pixel wm 64 + 16 i + l % 16.
+    const int pxl = wm * 64 + (lane & 15);
+    const int cbl = wn * 32 + 4 * g4;
     if (MODE == IG_FWD) {
-        // NITRO-Scaling + NITRO-ReLU per element into LDS, then coalesced (and pooled) stores.
-        // Several passes: the int64 sum saturated to int32 still saturates z* (128 SF < 2^31).
-        uint8_t *Os = smem;                   // [BM][OS] int8 activations
-        uint8_t *Rs = smem + CT_BM * OS;      // [BM][OS] region codes
+        // NITRO-Scaling (shift, clamp, one multiply-high) and the table's NITRO-ReLU per element;
+        // four channels packed per dword into LDS, then 16-byte (or pooled) stores. Several limb
+        // passes: the int64 sum saturated to int32 still saturates z* (128 SF < 2^31).
+        if (npass > 1) {
 #pragma unroll
-        for (int i = 0; i < TM; i++)
+            for (int i = 0; i < TM; i++)
 #pragma unroll
-            for (int j = 0; j < TN; j++)
+                for (int j = 0; j < TN; j++)
 #pragma unroll
-                for (int t = 0; t < 4; t++) {
-                    const int row = wm * 64 + i * 16 + g4 * 4 + t;
-                    const int col = wn * 32 + j * 16 + (lane & 15);
-                    uint8_t reg;
-                    const int32_t a = scale_relu32(sat_i32(value(i, j, t)), p.sr, reg);
-                    Os[row * OS + col] = (uint8_t)(int8_t)a;
-                    Rs[row * OS + col] = reg;
+                    for (int t = 0; t < 4; t++) acc[i][j][t] = sat_i32(acc64[i][j][t]);
+        }
+        constexpr int OW = OS / 4;                // row stride in dwords
+        uint32_t *Ov = (uint32_t *)smem;          // [BM][OW] packed activations
+        uint32_t *Rv = Ov + BM * OW;              // [BM][OW] packed region codes
+        auto pack = [&](auto trunc_tag) {
+            constexpr bool TR = decltype(trunc_tag)::value;
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++) {
+                    uint32_t av = 0, rv = 0;
+#pragma unroll
+                    for (int t = 0; t < 4; t++) {
+                        const uint32_t e = tab[scale_fast<TR>(acc[i][j][t], p.sf) + 128];
+                        av |= (e & 0xffu) << (8 * t);
+                        rv |= (e >> 8) << (8 * t);
+                    }
+                    const int o = (pxl + 16 * i) * OW + (cbl + 16 * j) / 4;
+                    Ov[o] = av;
+                    Rv[o] = rv;
                 }
+        };
+        if (p.sf.trunc) pack(std::true_type{});
+        else pack(std::false_type{});
         __syncthreads();
         if (!p.pool) {
-            for (int c = tid; c < CT_BM * CT_BN / 16; c += 256) {
-                const int row = c / (CT_BN / 16), cc = (c % (CT_BN / 16)) * 16;
+            for (int c = tid; c < BM * CT_BN / 16; c += NT) {
+                const int row = c / (CT_BN / 16), q = c % (CT_BN / 16);
                 const int64_t m = m0 + row;
-                if (m >= M || n0 + cc >= p.no) continue;
-                const int64_t o = m * p.no + n0 + cc;
-                *(v4i *)(p.out + o) = *(const v4i *)(Os + row * OS + cc);
-                *(v4i *)(p.code + o) = *(const v4i *)(Rs + row * OS + cc);
+                if (m >= M || n0 + 16 * q >= p.no) continue;
+                const int64_t o = m * p.no + n0 + 16 * q;
+                *(v4i *)(p.out + o) = *(const v4i *)(Ov + row * OW + 4 * q);
+                *(v4i *)(p.code + o) = *(const v4i *)(Rv + row * OW + 4 * q);
             }
         } else {
-            // 2x2 windows, 4 channels per thread: the tile holds rt (even) whole image rows
+            // 2x2 windows, 4 channels per thread: the tile holds rt (even) whole image rows; the
+            // first maximum in (0,0), (0,1), (1,0), (1,1) order wins
             const int W = p.w, Wh = p.w / 2;
-            for (int c = tid; c < (CT_BM / 4) * (CT_BN / 4); c += 256) {
-                const int win = c / (CT_BN / 4), col = (c % (CT_BN / 4)) * 4;
+            for (int c = tid; c < (BM / 4) * (CT_BN / 4); c += NT) {
+                const int win = c / (CT_BN / 4), cw = c % (CT_BN / 4);
                 const int wr = win / Wh, wc = win - wr * Wh;
                 const int q = 2 * wr * W + 2 * wc;
                 const int64_t m = m0 + q;
-                if (m >= M || n0 + col >= p.no) continue;
+                if (m >= M || n0 + 4 * cw >= p.no) continue;
+                uint32_t va[4], ra[4];
+#pragma unroll
+                for (int t = 0; t < 4; t++) {
+                    const int at = q + (t >> 1) * W + (t & 1);
+                    va[t] = Ov[at * OW + cw];
+                    ra[t] = Rv[at * OW + cw];
+                }
                 uint32_t ov = 0, cv = 0;
 #pragma unroll
                 for (int e = 0; e < 4; e++) {
-                    int best = -1000, arg = 0;
-                    uint8_t breg = 0;
+                    int best = (int)(int8_t)(va[0] >> (8 * e));
+                    uint32_t code = (ra[0] >> (8 * e)) & 0xffu;
+                    code <<= 2;
 #pragma unroll
-                    for (int t = 0; t < 4; t++) {
-                        const int at = q + (t >> 1) * W + (t & 1);
-                        const int v = (int)(int8_t)Os[at * OS + col + e];
-                        if (v > best) { best = v; arg = t; breg = Rs[at * OS + col + e]; }
+                    for (int t = 1; t < 4; t++) {
+                        const int v = (int)(int8_t)(va[t] >> (8 * e));
+                        if (v > best) {
+                            best = v;
+                            code = (((ra[t] >> (8 * e)) & 0xffu) << 2) | (uint32_t)t;
+                        }
                     }
                     ov |= (uint32_t)(uint8_t)(int8_t)best << (8 * e);
-                    cv |= (uint32_t)(arg | (breg << 2)) << (8 * e);
+                    cv |= code << (8 * e);
                 }
                 const int64_t grow = m / W;
                 const int64_t pp = (grow / 2) * Wh + (m % W) / 2;
-                const int64_t o = pp * p.no + n0 + col;
+                const int64_t o = pp * p.no + n0 + 4 * cw;
                 *(uint32_t *)(p.out + o) = ov;
                 *(uint32_t *)(p.code + o) = cv;
             }
         }
     } else if (p.out64) {
-        // raw int64 input gradient (the first layer of a network)
+        // raw int64 input gradient (the first layer of a network): 4 channels per lane and tile
 #pragma unroll
         for (int i = 0; i < TM; i++)
 #pragma unroll
-            for (int j = 0; j < TN; j++)
+            for (int j = 0; j < TN; j++) {
+                const int64_t m = m0 + pxl + 16 * i;
+                const int col = n0 + cbl + 16 * j;
+                if (m >= M || col >= p.no) continue;
+                int64_t *dst = p.out64 + m * p.no + col;
 #pragma unroll
-                for (int t = 0; t < 4; t++) {
-                    const int64_t m = m0 + wm * 64 + i * 16 + g4 * 4 + t;
-                    const int col = n0 + wn * 32 + j * 16 + (lane & 15);
-                    if (m < M && col < p.no) p.out64[m * p.no + col] = value(i, j, t);
-                }
-    } else {
-        // int32 sums into LDS, then 16 channels per thread: ReLU' with 16 codes, 64-byte rows
-        int32_t *Gs = (int32_t *)smem;        // [BM][GS]
-        bool bad = false;
-#pragma unroll
-        for (int i = 0; i < TM; i++)
-#pragma unroll
-            for (int j = 0; j < TN; j++)
-#pragma unroll
-                for (int t = 0; t < 4; t++) {
-                    const int row = wm * 64 + i * 16 + g4 * 4 + t;
-                    const int col = wn * 32 + j * 16 + (lane & 15);
-                    const int64_t v = value(i, j, t);
-                    bad |= !fits_i32(v);
-                    Gs[row * GS + col] = (int32_t)v;
-                }
-        __syncthreads();
-        uint32_t mx = 0;
-        for (int c = tid; c < CT_BM * CT_BN / 16; c += 256) {
-            const int row = c / (CT_BN / 16), cc = (c % (CT_BN / 16)) * 16;
-            const int64_t m = m0 + row;
-            if (m >= M || n0 + cc >= p.no) continue;
-            const int64_t o = m * p.no + n0 + cc;
-            v4i cd = v4i{0, 0, 0, 0};
-            if (p.prev_code) cd = *(const v4i *)(p.prev_code + o);
-            v4i outv[4];
-#pragma unroll
-            for (int e = 0; e < 16; e++) {
-                const int32_t v = Gs[row * GS + cc + e];
-                int64_t gv = v;
-                if (p.prev_code) gv = relu_bwd(v, (uint8_t)((uint32_t)cd[e >> 2] >> (8 * (e & 3))), p.rp);
-                outv[e >> 2][e & 3] = (int32_t)gv;
-                const uint32_t ag = abs_u32((int32_t)gv);
-                mx = ag > mx ? ag : mx;
+                for (int t = 0; t < 4; t++) dst[t] = npass > 1 ? acc64[i][j][t] : (int64_t)acc[i][j][t];
             }
+    } else {
+        // int32 sums, ReLU' of the previous layer with its 4 region codes, one 16-byte store per
+        // lane and tile
+        bool bad = false;
+        if (npass > 1) {
 #pragma unroll
-            for (int q = 0; q < 4; q++) *(v4i *)(p.gout + o + 4 * q) = outv[q];
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++)
+#pragma unroll
+                    for (int t = 0; t < 4; t++) {
+                        bad |= !fits_i32(acc64[i][j][t]);
+                        acc[i][j][t] = (int32_t)acc64[i][j][t];
+                    }
         }
+        uint32_t mx = 0;
+        auto emit = [&](auto trunc_tag) {
+            constexpr bool TR = decltype(trunc_tag)::value;
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++) {
+                    const int64_t m = m0 + pxl + 16 * i;
+                    const int col = n0 + cbl + 16 * j;
+                    if (m >= M || col >= p.no) continue;
+                    const int64_t o = m * p.no + col;
+                    v4i g = acc[i][j];
+                    if (p.prev_code) {
+                        const uint32_t cd = *(const uint32_t *)(p.prev_code + o);
+#pragma unroll
+                        for (int t = 0; t < 4; t++) g[t] = relu_bwd32<TR>(g[t], (cd >> (8 * t)) & 0xffu, p.rp);
+                    }
+#pragma unroll
+                    for (int t = 0; t < 4; t++) {
+                        const uint32_t ag = abs_u32(g[t]);
+                        mx = ag > mx ? ag : mx;
+                    }
+                    *(v4i *)(p.gout + o) = g;
+                }
+        };
+        if (p.rp.alpha.trunc) emit(std::true_type{});
+        else emit(std::false_type{});
         if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
         if (p.gmax) block_slot_max(p.gmax, mx);
     }
     ts_end(p.ts);
 }
 
-// Tile geometry: rt = 128 / W image rows; either rt divides H (one image segment) or H divides
-// rt (rt / H whole images); at most CT_NPMAX staged pixels.
+// Tile geometry: rt = BM / W image rows; either rt divides H (one image segment) or H divides
+// rt (rt / H whole images); at most NPMAX staged pixels.
+template <int WM>
 static bool tile_geom(int h, int w, int *rt, int *ns, int *rs)
 {
-    if (w < 1 || w > CT_BM || CT_BM % w) return false;
-    *rt = CT_BM / w;
+    constexpr int BM = CtShape<WM>::BM;
+    if (w < 1 || w > BM || BM % w) return false;
+    *rt = BM / w;
     if (*rt <= h) {
         if (h % *rt) return false;
         *ns = 1;
@@ -361,7 +460,7 @@ static bool tile_geom(int h, int w, int *rt, int *ns, int *rs)
         *ns = *rt / h;
         *rs = h;
     }
-    return *ns * (*rs + 2) * (w + 2) <= CT_NPMAX;
+    return *ns * (*rs + 2) * (w + 2) <= CtShape<WM>::NPMAX;
 }
 
 static bool tile_chunk_ok(int ck) { return ck == 16 || ck == 32 || (ck % 64 == 0 && ck <= 8192); }
@@ -369,34 +468,46 @@ static bool tile_chunk_ok(int ck) { return ck == 16 || ck == 32 || (ck % 64 == 0
 bool tile_conv_fwd_ok(const ConvShape &sh, bool pool, int64_t sf, int alpha_inv)
 {
     int rt, ns, rs;
-    if (!tile_geom(sh.h, sh.w, &rt, &ns, &rs) || !tile_chunk_ok(sh.c) || sh.co % 16) return false;
+    if (!tile_geom<2>(sh.h, sh.w, &rt, &ns, &rs) || !tile_chunk_ok(sh.c) || sh.co % 16) return false;
     if (pool && (rt % 2 || sh.h % 2 || sh.w % 2)) return false;
     return (int64_t)sh.n * sh.h * sh.w * sh.c < ((int64_t)1 << 31) &&
-           (int64_t)sh.co * 9 * sh.c < ((int64_t)1 << 31) && scale_relu32_ok(sf, alpha_inv) &&
+           (int64_t)sh.co * 9 * sh.c < ((int64_t)1 << 31) && scale_fast_ok(sf) && alpha_inv >= 2 &&
            128 * sf < ((int64_t)1 << 31);   // a saturated int32 sum still saturates z*
 }
 
 bool tile_conv_dx_ok(const ConvShape &sh)
 {
     int rt, ns, rs;
-    if (!tile_geom(sh.h, sh.w, &rt, &ns, &rs) || !tile_chunk_ok(sh.co) || sh.c % 16) return false;
+    if (!tile_geom<2>(sh.h, sh.w, &rt, &ns, &rs) || !tile_chunk_ok(sh.co) || sh.c % 16) return false;
     return (int64_t)sh.n * sh.h * sh.w * sh.co < ((int64_t)1 << 31) &&
            (int64_t)sh.co * 9 * sh.c < ((int64_t)1 << 31);
 }
 
-template <int MODE>
+// The 256-pixel tile where it fits and still gives at least two tiles per CU; pooling needs an
+// even number of rows per tile.
+static bool use_wide_tile(int n, int h, int w, int no, bool pool)
+{
+    int rt, ns, rs;
+    if (!tile_geom<4>(h, w, &rt, &ns, &rs) || (pool && rt % 2)) return false;
+    const int64_t tiles = ((int64_t)n * h / rt) * ((no + CT_BN - 1) / CT_BN);
+    return tiles >= 512;
+}
+
+template <int MODE, int WM>
 static void launch_tile(hipStream_t s, TileArgs a)
 {
+    tile_geom<WM>(a.h, a.w, &a.rt, &a.ns, &a.rs);
     a.d_w2 = make_div32((uint32_t)(a.w + 2));
     a.d_seg = make_div32((uint32_t)((a.rs + 2) * (a.w + 2)));
     a.d_w = make_div32((uint32_t)a.w);
     a.d_rw = make_div32((uint32_t)(a.rs * a.w));
-    const dim3 grid((unsigned)((a.n * a.h + a.rt - 1) / a.rt), (unsigned)((a.no + CT_BN - 1) / CT_BN));
+    const dim3 grid((unsigned)(((a.n * a.h + a.rt - 1) / a.rt) * ((a.no + CT_BN - 1) / CT_BN)));
+    const dim3 block(CtShape<WM>::NT);
     a.ts = timer_slot(MODE == IG_FWD ? TIMED_CONV_FWD : TIMED_CONV_DX);
     switch (a.ck == 16 ? 16 : a.ck == 32 ? 32 : 64) {
-    case 16: hipLaunchKernelGGL((k_conv_tile<MODE, 16>), grid, dim3(256), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((k_conv_tile<MODE, 32>), grid, dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((k_conv_tile<MODE, 64>), grid, dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((k_conv_tile<MODE, 16, WM>), grid, block, 0, s, a); break;
+    case 32: hipLaunchKernelGGL((k_conv_tile<MODE, 32, WM>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((k_conv_tile<MODE, 64, WM>), grid, block, 0, s, a); break;
     }
 }
 
@@ -409,12 +520,12 @@ void launch_conv_fwd_tile(hipStream_t s, const ConvShape &sh, const int8_t *x, c
     a.ck = sh.c; a.no = sh.co;
     a.a = x; a.aplane = 0; a.a_max = nullptr;
     a.b = wf; a.bplane = (int64_t)sh.co * 9 * sh.c; a.b_max = wmax;
-    tile_geom(sh.h, sh.w, &a.rt, &a.ns, &a.rs);
-    a.sr = make_scale_relu32(sf, alpha_inv, rp.mu, round);
+    a.sf = make_scale_fast(sf, alpha_inv, rp.mu, round);
     a.pool = pool ? 1 : 0;
     a.out = out; a.code = code;
     a.flags = flags;
-    launch_tile<IG_FWD>(s, a);
+    if (use_wide_tile(sh.n, sh.h, sh.w, sh.co, pool)) launch_tile<IG_FWD, 4>(s, a);
+    else launch_tile<IG_FWD, 2>(s, a);
 }
 
 void launch_conv_dx_tile(hipStream_t s, const ConvShape &sh, const int8_t *gl,
@@ -427,11 +538,11 @@ void launch_conv_dx_tile(hipStream_t s, const ConvShape &sh, const int8_t *gl,
     a.ck = sh.co; a.no = sh.c;
     a.a = gl; a.aplane = (int64_t)sh.n * sh.h * sh.w * sh.co; a.a_max = gmax_in;
     a.b = wt; a.bplane = (int64_t)sh.c * 9 * sh.co; a.b_max = wmax;
-    tile_geom(sh.h, sh.w, &a.rt, &a.ns, &a.rs);
     a.rp = rp;
     a.prev_code = prev_code; a.gout = gout; a.out64 = out64; a.gmax = gmax_out;
     a.flags = flags;
-    launch_tile<IG_DX>(s, a);
+    if (use_wide_tile(sh.n, sh.h, sh.w, sh.c, false)) launch_tile<IG_DX, 4>(s, a);
+    else launch_tile<IG_DX, 2>(s, a);
 }
 
 }  // namespace nitro

@@ -234,6 +234,89 @@ __host__ __device__ inline int32_t scale_relu32(int32_t z, const ScaleRelu32 &q,
     return (c < 0 ? neg : c) - q.mu;
 }
 
+// NITRO-Scaling of an int32 sum for the tile epilogue, clamped to [-128, 128]. SF = 2^e D with D
+// odd: floor(z / 2^e) is an arithmetic shift (truncation: the shift after adding 2^e - 1 to a
+// negative z), and clamping that to [-128 D, 128 D] keeps its quotient by D inside [-128, 128]
+// and saturates it to -128 or 128 outside. The clamped quotient is exact with one multiply-high
+// by m = ceil(2^32 / D): for n <= 128 D, n (m D - 2^32) < 128 D^2 < 2^32. The NITRO-ReLU of the
+// result (and its region) is a lookup in a 257-entry table.
+struct ScaleFast {
+    int32_t e;
+    uint32_t m;        // ceil(2^32 / D)
+    int32_t lo, hi;    // -128 D, 128 D
+    int32_t alpha, mu, trunc;
+};
+
+// SF a power of two is taken as 2^(e-1) * 2, so that D >= 2 and m is a 32-bit number.
+inline bool scale_fast_ok(int64_t sf)
+{
+    if (sf < 2 || sf >= ((int64_t)1 << 31)) return false;
+    int64_t d = sf;
+    while (!(d & 1)) d >>= 1;
+    return 128 * d * d < ((int64_t)1 << 32);
+}
+
+inline ScaleFast make_scale_fast(int64_t sf, int32_t alpha_inv, int32_t mu, int round)
+{
+    ScaleFast q{};
+    int64_t d = sf;
+    while (!(d & 1)) {
+        d >>= 1;
+        q.e++;
+    }
+    if (d == 1) {
+        d = 2;
+        q.e--;
+    }
+    q.m = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)d - 1) / (uint64_t)d);
+    q.lo = (int32_t)(-128 * d);
+    q.hi = (int32_t)(128 * d);
+    q.alpha = alpha_inv;
+    q.mu = mu;
+    q.trunc = round == NITRO_ROUND_TRUNC;
+    return q;
+}
+
+template <bool TRUNC>
+__host__ __device__ inline int32_t scale_fast(int32_t z, const ScaleFast &q)
+{
+    int32_t s = TRUNC ? (z + ((z >> 31) & ((1 << q.e) - 1))) >> q.e : z >> q.e;
+    s = max(min(s, q.hi), q.lo);
+    const int32_t sg = s >> 31;
+    const uint32_t n = TRUNC ? (uint32_t)((s ^ sg) - sg) : (uint32_t)(s ^ sg);
+#if defined(__HIP_DEVICE_COMPILE__)
+    const uint32_t dq = __umulhi(n, q.m);
+#else
+    const uint32_t dq = (uint32_t)(((uint64_t)n * q.m) >> 32);
+#endif
+    return TRUNC ? (((int32_t)dq ^ sg) - sg) : ((int32_t)dq ^ sg);
+}
+
+// Table entry for a scaled value zs in [-128, 128]: the NITRO-ReLU output byte | region << 8.
+__host__ __device__ inline uint16_t relu_table_entry(int32_t zs, const ScaleFast &q)
+{
+    const int32_t c = zs < -127 ? -127 : (zs > 127 ? 127 : zs);
+    const uint32_t reg = c != zs ? REG_ZERO : (c < 0 ? REG_SLOPE : REG_PASS);
+    int32_t a = c;
+    if (c < 0) {
+        a = c / q.alpha;
+        if (!q.trunc && a * q.alpha != c) a -= 1;
+    }
+    a -= q.mu;
+    return (uint16_t)((uint32_t)(uint8_t)(int8_t)a | (reg << 8));
+}
+
+// NITRO-ReLU backward of an int32 gradient, branch-free (same result as relu_bwd).
+template <bool TRUNC>
+__device__ inline int32_t relu_bwd32(int32_t d, uint32_t region, const Relu &rp)
+{
+    const int32_t sg = d >> 31;
+    const uint32_t n = TRUNC ? (uint32_t)((d ^ sg) - sg) : (uint32_t)(d ^ sg);
+    const uint32_t qd = udiv32_nf(n, rp.a32_m, rp.a32_l);
+    const int32_t s = TRUNC ? (((int32_t)qd ^ sg) - sg) : ((int32_t)qd ^ sg);
+    return region == REG_PASS ? d : (region == REG_SLOPE ? s : 0);
+}
+
 // Sticky status flags written by kernels (bit or).
 enum : uint32_t { FLAG_OVERFLOW = 1u, FLAG_LABEL = 2u };
 
