@@ -80,6 +80,11 @@ nitro_status nitro_create(nitro_ctx **out, int device, void *hip_stream);
 void nitro_destroy(nitro_ctx *ctx);
 /* Change the stream later calls enqueue on. */
 nitro_status nitro_set_stream(nitro_ctx *ctx, void *hip_stream);
+/* Tile of the tiled int8 MFMA convolution kernels (forward and input gradient): 0 chooses by
+ * shape (the default), 128 or 256 output pixels per workgroup force that tile wherever its
+ * geometry fits the layer (other layers keep the automatic choice). Results do not depend on it.
+ * EINVAL for any other value. */
+nitro_status nitro_set_conv_tile(nitro_ctx *ctx, int32_t pixels);
 /* Synchronise the stream, then return and clear the sticky device flags: NITRO_OK, or the first
  * of NITRO_EOVERFLOW, NITRO_ELABEL that was raised. */
 nitro_status nitro_sync_status(nitro_ctx *ctx);

@@ -17,6 +17,7 @@ thread_local LaunchTimer *g_timer = nullptr;
 struct nitro_ctx : public LaunchTimer {
     int device = 0;
     hipStream_t stream = nullptr;
+    int conv_tile = 0;                          // nitro_set_conv_tile
     uint32_t *flags = nullptr;                  // device: sticky status bits
     // streams of their own for the blocks' local training in a training iteration (the blocks'
     // backward passes depend only on their own forward state), created on first use. Only
@@ -280,7 +281,7 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
                 xin = xpad;
             }
             if (L.fwd_tile)
-                launch_conv_fwd_tile(s, sx, xin, wf, wmax, L.sf, desc->alpha_inv, desc->round, rp,
+                launch_conv_fwd_tile(s, ctx->conv_tile, sx, xin, wf, wmax, L.sf, desc->alpha_inv, desc->round, rp,
                                      pool, out, code, ctx->flags);
             else if (L.pad16)
                 launch_conv_fwd_mfma(s, sx, xin, wf, wmax, sf, rp, pool, out, code, ctx->flags);
@@ -392,7 +393,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
             uint32_t *gmax_out = j > 0 ? slots + (4 + j - 1) * SLOT_WORDS : nullptr;
             if (L.conv) {
                 if (L.dx_tile)
-                    launch_conv_dx_tile(s, L.sh, (const int8_t *)at(state, g.gnl),
+                    launch_conv_dx_tile(s, ctx->conv_tile, L.sh, (const int8_t *)at(state, g.gnl),
                                         slots + (4 + j) * SLOT_WORDS,
                                         (const int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS,
                                         code, rp, dst, dst64, gmax_out, ctx->flags);
@@ -586,6 +587,13 @@ nitro_status nitro_set_stream(nitro_ctx *ctx, void *hip_stream)
 {
     if (!ctx) return NITRO_EINVAL;
     ctx->stream = (hipStream_t)hip_stream;
+    return NITRO_OK;
+}
+
+nitro_status nitro_set_conv_tile(nitro_ctx *ctx, int32_t pixels)
+{
+    if (!ctx || (pixels != 0 && pixels != 128 && pixels != 256)) return NITRO_EINVAL;
+    ctx->conv_tile = pixels;
     return NITRO_OK;
 }
 

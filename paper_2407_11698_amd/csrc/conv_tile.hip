@@ -483,12 +483,13 @@ bool tile_conv_dx_ok(const ConvShape &sh)
            (int64_t)sh.co * 9 * sh.c < ((int64_t)1 << 31);
 }
 
-// The 256-pixel tile where it fits and still gives at least two tiles per CU; pooling needs an
-// even number of rows per tile.
-static bool use_wide_tile(int n, int h, int w, int no, bool pool)
+// The 256-pixel tile where it fits (pooling needs an even number of rows per tile) and, chosen by
+// shape, where it still gives at least two tiles per CU.
+static bool use_wide_tile(int pref, int n, int h, int w, int no, bool pool)
 {
     int rt, ns, rs;
-    if (!tile_geom<4>(h, w, &rt, &ns, &rs) || (pool && rt % 2)) return false;
+    if (pref == 128 || !tile_geom<4>(h, w, &rt, &ns, &rs) || (pool && rt % 2)) return false;
+    if (pref == 256) return true;
     const int64_t tiles = ((int64_t)n * h / rt) * ((no + CT_BN - 1) / CT_BN);
     return tiles >= 512;
 }
@@ -511,7 +512,7 @@ static void launch_tile(hipStream_t s, TileArgs a)
     }
 }
 
-void launch_conv_fwd_tile(hipStream_t s, const ConvShape &sh, const int8_t *x, const int8_t *wf,
+void launch_conv_fwd_tile(hipStream_t s, int tile, const ConvShape &sh, const int8_t *x, const int8_t *wf,
                           const uint32_t *wmax, int64_t sf, int alpha_inv, int round,
                           const Relu &rp, bool pool, int8_t *out, uint8_t *code, uint32_t *flags)
 {
@@ -524,11 +525,11 @@ void launch_conv_fwd_tile(hipStream_t s, const ConvShape &sh, const int8_t *x, c
     a.pool = pool ? 1 : 0;
     a.out = out; a.code = code;
     a.flags = flags;
-    if (use_wide_tile(sh.n, sh.h, sh.w, sh.co, pool)) launch_tile<IG_FWD, 4>(s, a);
+    if (use_wide_tile(tile, sh.n, sh.h, sh.w, sh.co, pool)) launch_tile<IG_FWD, 4>(s, a);
     else launch_tile<IG_FWD, 2>(s, a);
 }
 
-void launch_conv_dx_tile(hipStream_t s, const ConvShape &sh, const int8_t *gl,
+void launch_conv_dx_tile(hipStream_t s, int tile, const ConvShape &sh, const int8_t *gl,
                          const uint32_t *gmax_in, const int8_t *wt, const uint32_t *wmax,
                          const uint8_t *prev_code, const Relu &rp, int32_t *gout, int64_t *out64,
                          uint32_t *gmax_out, uint32_t *flags)
@@ -541,7 +542,7 @@ void launch_conv_dx_tile(hipStream_t s, const ConvShape &sh, const int8_t *gl,
     a.rp = rp;
     a.prev_code = prev_code; a.gout = gout; a.out64 = out64; a.gmax = gmax_out;
     a.flags = flags;
-    if (use_wide_tile(sh.n, sh.h, sh.w, sh.c, false)) launch_tile<IG_DX, 4>(s, a);
+    if (use_wide_tile(tile, sh.n, sh.h, sh.w, sh.c, false)) launch_tile<IG_DX, 4>(s, a);
     else launch_tile<IG_DX, 2>(s, a);
 }
 

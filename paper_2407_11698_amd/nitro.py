@@ -82,6 +82,7 @@ def _load():
         "nitro_create": (I32, [P(VP), ctypes.c_int, VP]),
         "nitro_destroy": (None, [VP]),
         "nitro_set_stream": (I32, [VP, VP]),
+        "nitro_set_conv_tile": (I32, [VP, I32]),
         "nitro_sync_status": (I32, [VP]),
         "nitro_status_str": (ctypes.c_char_p, [I32]),
         "nitro_block_query": (I32, [P(BlockDesc), P(ctypes.c_size_t)]),
@@ -110,7 +111,8 @@ def _load():
 LIB = _load()
 
 # every symbol the header declares (checked by the ABI tests)
-EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_sync_status",
+EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_set_conv_tile",
+           "nitro_sync_status",
            "nitro_status_str", "nitro_block_query", "nitro_block_saved", "nitro_block_forward",
            "nitro_block_backward",
            "nitro_head_backward", "nitro_integer_sgd_step", "nitro_net_query",
@@ -221,6 +223,9 @@ class Context:
     def set_stream(self, stream):
         self.stream = stream
         check(LIB.nitro_set_stream(self.h, VP(stream.cuda_stream)), "nitro_set_stream")
+
+    def set_conv_tile(self, pixels: int) -> None:
+        check(LIB.nitro_set_conv_tile(self.h, pixels), "nitro_set_conv_tile")
 
     def sync_status(self) -> int:
         return int(LIB.nitro_sync_status(self.h))

@@ -133,6 +133,30 @@ def test_conv_block(ctx, case, modes):
     run_block(ctx, rng, n, h, w, chans, pool, G, alpha, modes[0], modes[1], wmax=wmax)
 
 
+# shapes the tiled conv kernels take with either tile (128 or 256 output pixels per workgroup):
+# whole small images per tile, image rows per tile, multi-limb weights, with and without pooling
+TILE_CASES = [
+    (2, 8, 8, [64, 128, 128], True, 100, 16, 6000),
+    (1, 32, 32, [3, 64, 64], True, 100, 10, 44),
+    (3, 16, 16, [32, 64, 64], True, 10, 10, 300),
+    (2, 16, 16, [64, 64, 64], False, 0, 10, 127),
+]
+
+
+@pytest.mark.parametrize("tile", [128, 256])
+@pytest.mark.parametrize("case", TILE_CASES)
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_conv_block_tile(ctx, tile, case, modes):
+    """The same block results whichever conv tile is forced (nitro_set_conv_tile)."""
+    n, h, w, chans, pool, G, alpha, wmax = case
+    rng = np.random.default_rng(hash((n, h, w, tuple(chans), G, tile)) % (1 << 31))
+    ctx.set_conv_tile(tile)
+    try:
+        run_block(ctx, rng, n, h, w, chans, pool, G, alpha, modes[0], modes[1], wmax=wmax)
+    finally:
+        ctx.set_conv_tile(0)
+
+
 @pytest.mark.parametrize("chans,G,wmax", [([784, 100], 10, 7), ([100, 50, 30], 10, 300),
                                           ([37, 5], 3, 20000), ([64, 65], 0, 127)])
 @pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
