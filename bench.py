@@ -8,9 +8,11 @@ steps the weights are reset to their initial values, so each timed step is one o
 verified iterations.
 
 Prints one JSON line with the throughput, the roofline position of the dominant kernel (its own
-device time inside the timed region, from timestamps its workgroups record), the single
-conv-layer stress case's kernels measured alone after the timed region, and the CPU oracle's
-throughput on a bounded sample.
+device time inside the timed region, from timestamps its workgroups record; beside it, the same
+kernel's time per launch in a few iterations run afterwards with every block on one stream, and
+its HBM bytes per launch from the hardware-counter summary under profiles/ while that kernel's
+source is unchanged), the single conv-layer stress case's kernels measured alone after the timed
+region, and the CPU oracle's throughput on a bounded sample.
 """
 from __future__ import annotations
 
@@ -64,6 +66,22 @@ def conv_layer_ops(wl):
             if ly.c_out % 16 == 0 and w <= 62:
                 ops["k_conv_dw_planes"] += 2 * macs
     return ops
+
+
+def recorded_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` in the training iteration, from the hardware-counter
+    summary under profiles/ (FETCH_SIZE and WRITE_SIZE passes, each calibrated by a copy of
+    known size); None when there is no summary or the kernel's source has changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "%s_vgg_cnn_b256_traffic.txt" % kernel.split("<")[0])
+    try:
+        kv = dict(line.split(": ", 1) for line in open(path).read().splitlines() if ": " in line)
+        src = open(os.path.join(ROOT, kv["source"]), "rb").read()
+    except (OSError, KeyError, ValueError):
+        return None
+    if kv.get("kernel") != kernel or hashlib.sha256(src).hexdigest() != kv.get("source_sha256"):
+        return None
+    return int(float(kv["traffic_bytes_per_launch"]))
 
 
 def limbs_for(m: int) -> int:
@@ -160,6 +178,9 @@ def main():
     ap.add_argument("--eager", action="store_true",
                     help="launch every kernel from the host each step instead of replaying the "
                          "captured iteration (nitro_train_step_graph)")
+    ap.add_argument("--serial-steps", type=int, default=3,
+                    help="training iterations run after the timed region with every block on "
+                         "one stream, for per-launch kernel times without overlap (0 skips)")
     ap.add_argument("--stress-reps", type=int, default=10,
                     help="repeats of the single conv-layer stress case measured after the "
                          "training iterations (0 skips it)")
@@ -239,6 +260,25 @@ def main():
                            "algorithmic_TOPs": round(tops, 3)}
     dom = max(per_class, key=lambda k: per_class[k]["ms_per_step"])
     achieved = per_class[dom]["algorithmic_TOPs"]
+
+    # the same kernels with the blocks' local training on one stream, after the timed region:
+    # each launch then has the GPU to itself, as under a kernel-trace profiler
+    serial = {}
+    if args.serial_steps > 0:
+        net.ctx.set_aux_streams(0)
+        run(0, 1)
+        net.ctx.sync()
+        net.ctx.kernel_timing(True)
+        run(1, args.serial_steps)
+        net.ctx.sync()
+        steps_timed = 1 if graph else args.serial_steps     # graph: the last replay's times
+        for c, name in KERNEL_CLASSES.items():
+            ms, launches = net.ctx.kernel_time(c)
+            if launches:
+                serial[name] = {"avg_launch_us": round(ms * 1e3 / launches, 2),
+                                "algorithmic_TOPs": round(ops[name] * steps_timed / (ms * 1e-3) / 1e12, 3)}
+        net.ctx.kernel_timing(False)
+        net.ctx.set_aux_streams(3)
     conv_ms = sum(v["ms_per_step"] for v in per_class.values())
     conv_tops = sum(ops.values()) / (conv_ms * 1e-3) / 1e12 if conv_ms > 0 else 0.0
 
@@ -263,11 +303,19 @@ def main():
                    "launch": "graph replay" if graph else "eager"},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved,
                      "peak": PEAK_INT8_TOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_INT8_TOPS, 5), "traffic": None},
+                     "frac": round(achieved / PEAK_INT8_TOPS, 5),
+                     "traffic": recorded_traffic(dom)},
         "conv_mfma": {"algorithmic_TOPs": round(conv_tops, 3),
                       "frac_of_int8_peak": round(conv_tops / PEAK_INT8_TOPS, 5),
                       "per_kernel": per_class},
     }
+    if serial:
+        sd = serial.get(dom)
+        out["roofline"]["serial"] = {
+            "steps": args.serial_steps, "avg_launch_us": sd["avg_launch_us"] if sd else None,
+            "achieved": sd["algorithmic_TOPs"] if sd else None,
+            "frac": round(sd["algorithmic_TOPs"] / PEAK_INT8_TOPS, 5) if sd else None}
+        out["conv_mfma"]["serial_per_kernel"] = serial
     if args.stress_reps > 0:
         out["stress_conv"] = stress_layer(args.stress_reps)
     if not args.no_cpu_baseline:

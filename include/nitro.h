@@ -85,6 +85,13 @@ nitro_status nitro_set_stream(nitro_ctx *ctx, void *hip_stream);
  * geometry fits the layer (other layers keep the automatic choice). Results do not depend on it.
  * EINVAL for any other value. */
 nitro_status nitro_set_conv_tile(nitro_ctx *ctx, int32_t pixels);
+/* Number of auxiliary streams nitro_train_step runs the blocks' local training on (0 to 3,
+ * default 3): the forward pass runs on the context's stream; block b's local training starts
+ * when block b's forward is done, on auxiliary stream b mod n, except the last block's, which
+ * follows on the context's stream; with 0 everything runs on the context's stream, in that
+ * order. The streams are the context's own, created on first use. Results do not depend on it.
+ * EINVAL outside 0..3. */
+nitro_status nitro_set_aux_streams(nitro_ctx *ctx, int32_t n);
 /* Synchronise the stream, then return and clear the sticky device flags: NITRO_OK, or the first
  * of NITRO_EOVERFLOW, NITRO_ELABEL that was raised. */
 nitro_status nitro_sync_status(nitro_ctx *ctx);

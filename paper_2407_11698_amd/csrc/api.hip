@@ -18,6 +18,7 @@ struct nitro_ctx : public LaunchTimer {
     int device = 0;
     hipStream_t stream = nullptr;
     int conv_tile = 0;                          // nitro_set_conv_tile
+    int aux_use = 3;                            // nitro_set_aux_streams (<= NAUX)
     uint32_t *flags = nullptr;                  // device: sticky status bits
     // streams of their own for the blocks' local training in a training iteration (the blocks'
     // backward passes depend only on their own forward state), created on first use. Only
@@ -25,7 +26,7 @@ struct nitro_ctx : public LaunchTimer {
     // default), and two streams on one queue run one after the other.
     static constexpr int NAUX = 3;
     hipStream_t aux[NAUX] = {};
-    hipEvent_t fork = nullptr, join[NAUX] = {};
+    hipEvent_t fev[NITRO_MAX_BLOCKS] = {}, join[NAUX] = {};   // block b's forward done; aux done
     bool aux_ready = false;
     // the captured training iteration of nitro_train_step_graph and the arguments it holds
     hipGraphExec_t gexec = nullptr;
@@ -46,7 +47,8 @@ struct nitro_ctx : public LaunchTimer {
     nitro_status ensure_aux()
     {
         if (aux_ready) return NITRO_OK;
-        if (hipEventCreateWithFlags(&fork, hipEventDisableTiming) != hipSuccess) return NITRO_EHIP;
+        for (int b = 0; b < NITRO_MAX_BLOCKS; b++)
+            if (hipEventCreateWithFlags(&fev[b], hipEventDisableTiming) != hipSuccess) return NITRO_EHIP;
         for (int b = 0; b < NAUX; b++) {
             if (hipStreamCreateWithFlags(&aux[b], hipStreamNonBlocking) != hipSuccess) return NITRO_EHIP;
             if (hipEventCreateWithFlags(&join[b], hipEventDisableTiming) != hipSuccess) return NITRO_EHIP;
@@ -577,7 +579,7 @@ void nitro_destroy(nitro_ctx *ctx)
             (void)hipStreamDestroy(ctx->aux[b]);
             (void)hipEventDestroy(ctx->join[b]);
         }
-        (void)hipEventDestroy(ctx->fork);
+        for (int b = 0; b < NITRO_MAX_BLOCKS; b++) (void)hipEventDestroy(ctx->fev[b]);
     }
     (void)hipFree(ctx->flags);
     delete ctx;
@@ -594,6 +596,13 @@ nitro_status nitro_set_conv_tile(nitro_ctx *ctx, int32_t pixels)
 {
     if (!ctx || (pixels != 0 && pixels != 128 && pixels != 256)) return NITRO_EINVAL;
     ctx->conv_tile = pixels;
+    return NITRO_OK;
+}
+
+nitro_status nitro_set_aux_streams(nitro_ctx *ctx, int32_t n)
+{
+    if (!ctx || n < 0 || n > nitro_ctx::NAUX) return NITRO_EINVAL;
+    ctx->aux_use = n;
     return NITRO_OK;
 }
 
@@ -759,7 +768,31 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     SgdBatch sgd{};
     sgd.flags = ctx->flags;
 
-    // 1. forward through every block (pre-update weights)
+    // 1. forward through the blocks on the context's stream (pre-update weights). A block's
+    // local training (3.) needs only its own forward state and the labels, so it is enqueued as
+    // soon as its forward is: on auxiliary stream b mod the number in use, which first waits for
+    // an event recorded behind the block's forward, while the context's stream goes on with the
+    // next block. The last block trains on the context's stream after the output layer (2.).
+    // With no auxiliary stream (nitro_set_aux_streams) everything runs on the context's stream.
+    st = ctx->ensure_aux();
+    if (st != NITRO_OK) return st;
+    const int nuse = ctx->aux_use;
+    unsigned used_aux = 0;
+    auto backward = [&](int b, hipStream_t bs) -> nitro_status {
+        const nitro_block_desc &d = net->block[b];
+        const int8_t *xin = b == 0 ? x : (const int8_t *)at(workspace, g.aout[b - 1]);
+        nitro_block_params bp{};
+        nitro_block_grads gr{};
+        for (int j = 0; j < d.n_layers; j++) {
+            bp.w[j] = params->w[b][j];
+            gr.dw[j] = (int64_t *)at(workspace, g.dw[b][j]);
+        }
+        bp.w_lr = params->w_lr[b];
+        gr.dw_lr = (int64_t *)at(workspace, g.dwlr[b]);
+        return block_backward_impl(ctx, &d, g.b[b], &bp, xin, (const int8_t *)at(workspace, g.aout[b]),
+                                   labels, nullptr, at(workspace, g.state[b]), &gr, nullptr, false,
+                                   bs);
+    };
     const int8_t *cur = x;
     for (int b = 0; b < net->n_blocks; b++) {
         nitro_block_params bp{};
@@ -770,6 +803,17 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                                 false);
         if (st != NITRO_OK) return st;
         cur = aout;
+        if (b + 1 == net->n_blocks) break;
+        hipStream_t bs = ctx->stream;
+        if (nuse > 0) {
+            const int a = b % nuse;
+            bs = ctx->aux[a];
+            if (hipEventRecord(ctx->fev[b], ctx->stream) != hipSuccess) return NITRO_EHIP;
+            if (hipStreamWaitEvent(bs, ctx->fev[b], 0) != hipSuccess) return NITRO_EHIP;
+            used_aux |= 1u << a;
+        }
+        st = backward(b, bs);
+        if (st != NITRO_OK) return st;
     }
     // 2. output layer: global gradient (its update comes with the others, step 4)
     const int n = net->block[0].n;
@@ -782,33 +826,11 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                                ctx->flags);
         launch_linear_dw(ctx->stream, n, (int)d, G, (const int32_t *)at(workspace, g.he), cur, hdw);
     }
-    // 3. local training of every block on its own stream: forked after the forward pass and the
-    // output layer, joined before the updates. Block 0 (the largest feature maps, the longest
-    // chain) runs on the context's stream; block b > 0 on auxiliary stream (b - 1) mod NAUX.
-    st = ctx->ensure_aux();
+    // 3. the last block's local training; the context's stream then waits for the others
+    st = backward(net->n_blocks - 1, ctx->stream);
     if (st != NITRO_OK) return st;
-    const int naux = net->n_blocks - 1 < nitro_ctx::NAUX ? net->n_blocks - 1 : nitro_ctx::NAUX;
-    if (hipEventRecord(ctx->fork, ctx->stream) != hipSuccess) return NITRO_EHIP;
-    for (int a = 0; a < naux; a++)
-        if (hipStreamWaitEvent(ctx->aux[a], ctx->fork, 0) != hipSuccess) return NITRO_EHIP;
-    for (int b = 0; b < net->n_blocks; b++) {
-        hipStream_t bs = b == 0 ? ctx->stream : ctx->aux[(b - 1) % nitro_ctx::NAUX];
-        const nitro_block_desc &d = net->block[b];
-        const int8_t *xin = b == 0 ? x : (const int8_t *)at(workspace, g.aout[b - 1]);
-        nitro_block_params bp{};
-        nitro_block_grads gr{};
-        for (int j = 0; j < d.n_layers; j++) {
-            bp.w[j] = params->w[b][j];
-            gr.dw[j] = (int64_t *)at(workspace, g.dw[b][j]);
-        }
-        bp.w_lr = params->w_lr[b];
-        gr.dw_lr = (int64_t *)at(workspace, g.dwlr[b]);
-        st = block_backward_impl(ctx, &d, g.b[b], &bp, xin, (const int8_t *)at(workspace, g.aout[b]),
-                                 labels, nullptr, at(workspace, g.state[b]), &gr, nullptr, false,
-                                 bs);
-        if (st != NITRO_OK) return st;
-    }
-    for (int a = 0; a < naux; a++) {
+    for (int a = 0; a < nuse; a++) {
+        if (!(used_aux & (1u << a))) continue;
         if (hipEventRecord(ctx->join[a], ctx->aux[a]) != hipSuccess) return NITRO_EHIP;
         if (hipStreamWaitEvent(ctx->stream, ctx->join[a], 0) != hipSuccess) return NITRO_EHIP;
     }
@@ -854,6 +876,8 @@ nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
     put(hp, sizeof(*hp));
     put(&ctx->stream, sizeof(ctx->stream));
     put(&ctx->timing, sizeof(ctx->timing));
+    put(&ctx->aux_use, sizeof(ctx->aux_use));
+    put(&ctx->conv_tile, sizeof(ctx->conv_tile));
     if (!ctx->gexec || key != ctx->gkey) {
         if (ctx->gexec) {
             (void)hipGraphExecDestroy(ctx->gexec);

@@ -310,6 +310,27 @@ def test_deterministic(ctx):
         assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("naux", [0, 1, 2])
+def test_train_step_aux_streams(ctx, naux):
+    """The blocks' local training on 0, 1 or 2 auxiliary streams gives the weights of the
+    default 3 (nitro_set_aux_streams), step after step."""
+    wl = WL.scaled(WL.VGG_CNN, 4)
+    dr = WL.draw_workload(wl, O.kaiming_bound, steps=3)
+    outs = []
+    for n in (3, naux):
+        ctx.set_aux_streams(n)
+        try:
+            net = runner.GpuNet(wl, dr.weights, ctx=ctx)
+            for x, y in dr.batches:
+                net.step(dev(x), dev(y))
+            ctx.sync()
+            outs.append(net.weights_np())
+        finally:
+            ctx.set_aux_streams(3)
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
+
+
 @pytest.mark.parametrize("wl", [WL.scaled(WL.SMALL_CNN, 16), WL.scaled(WL.VGG_CNN, 8)],
                          ids=["small_cnn_b16", "vgg_b8"])
 def test_train_step_graph_matches_eager(wl):
