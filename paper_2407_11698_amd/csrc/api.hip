@@ -249,7 +249,7 @@ inline uint8_t *at(void *base, size_t off) { return (uint8_t *)base + off; }
 // slots once, up front, instead)
 nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, const BlockGeom &g,
                                 const nitro_block_params *p, const int8_t *x, int8_t *a_out,
-                                void *state, bool zero_slots = true)
+                                void *state, bool zero_slots = true, bool prepacked = false)
 {
     hipStream_t s = ctx->stream;
     const Relu rp = make_relu(desc->alpha_inv, desc->round);
@@ -264,11 +264,13 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
         uint8_t *code = at(state, g.code[j]);
         const Div sf = make_div(L.sf, desc->round);
         if (L.conv) {
-            // limb planes for this call's forward and input-gradient GEMMs, and max|W_j|
-            if (!L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c))
-                launch_pack_conv_tiled(s, p->w[j], L.sh.co, L.sh.c, (int8_t *)at(state, g.wf[j]),
-                                       (int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS);
-            else
+            // limb planes for this call's forward and input-gradient GEMMs, and max|W_j| (the
+            // training iteration packs the tiled ones of every block in one launch first)
+            if (!L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c)) {
+                if (!prepacked)
+                    launch_pack_conv_tiled(s, p->w[j], L.sh.co, L.sh.c, (int8_t *)at(state, g.wf[j]),
+                                           (int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS);
+            } else
                 launch_pack_conv_weights(s, p->w[j], L.sh.co, L.sh.c, L.pad16 ? 16 : L.sh.c,
                                          (int8_t *)at(state, g.wf[j]),
                                          (int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS);
@@ -306,7 +308,8 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                                  const nitro_block_params *p, const int8_t *x, const int8_t *a_out,
                                  const int32_t *labels, const int32_t *delta_out, void *state,
                                  const nitro_block_grads *gr, const nitro_block_taps *taps,
-                                 bool zero_slots = true, hipStream_t stream = nullptr)
+                                 bool zero_slots = true, hipStream_t stream = nullptr,
+                                 bool prepacked = false)
 {
     hipStream_t s = stream ? stream : ctx->stream;
     const Relu rp = make_relu(desc->alpha_inv, desc->round);
@@ -339,7 +342,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
             launch_learning_mfma(s, n, g.d, G, a_out, p->w_lr, sf, labels, lb,
                                  at(state, g.code[J - 1]), rp, LJ.sh.h, LJ.sh.w, LJ.sh.co,
                                  desc->maxpool != 0, gb[0], taps ? taps->delta : nullptr, yhat, e,
-                                 gr->dw_lr, ctx->flags);
+                                 gr->dw_lr, ctx->flags, prepacked);
             have_g = true;
         } else {
             int32_t *dl = (int32_t *)at(state, g.delta);
@@ -765,6 +768,31 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
             sl.p[b] = (uint32_t *)at(at(workspace, g.state[b]), g.b[b].slots);
         launch_zero_slots(ctx->stream, sl, net->n_blocks);
     }
+    // limb planes (and max |W|) of the tiled conv layers' and the MFMA learning layers' weights
+    // of every block, in one launch ahead of the forward pass
+    {
+        PackList pl;
+        for (int b = 0; b < net->n_blocks; b++) {
+            const BlockGeom &bg = g.b[b];
+            void *state = at(workspace, g.state[b]);
+            uint32_t *slots = (uint32_t *)at(state, bg.slots);
+            for (int j = 0; j < bg.J; j++) {
+                const LayerGeom &L = bg.L[j];
+                if (L.conv && !L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c))
+                    pl.add(ctx->stream,
+                           pack_conv_args(params->w[b][j], L.sh.co, L.sh.c, (int8_t *)at(state, bg.wf[j]),
+                                          (int8_t *)at(state, bg.wt[j]), slots + j * SLOT_WORDS), 9);
+            }
+            if (net->block[b].n_classes > 0 && bg.lr_mfma) {
+                const LearningScratch sc = learning_scratch(net->block[b].n, bg.d, net->block[b].n_classes);
+                pl.add(ctx->stream,
+                       pack_matrix_args(params->w_lr[b], net->block[b].n_classes, (int)bg.d, sc.gp,
+                                        (int8_t *)at(state, bg.lwf), (int8_t *)at(state, bg.lwt),
+                                        slots + 8 * SLOT_WORDS), 1);
+            }
+        }
+        pl.flush(ctx->stream);
+    }
     SgdBatch sgd{};
     sgd.flags = ctx->flags;
 
@@ -791,7 +819,7 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         gr.dw_lr = (int64_t *)at(workspace, g.dwlr[b]);
         return block_backward_impl(ctx, &d, g.b[b], &bp, xin, (const int8_t *)at(workspace, g.aout[b]),
                                    labels, nullptr, at(workspace, g.state[b]), &gr, nullptr, false,
-                                   bs);
+                                   bs, true);
     };
     const int8_t *cur = x;
     for (int b = 0; b < net->n_blocks; b++) {
@@ -800,7 +828,7 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         bp.w_lr = params->w_lr[b];
         int8_t *aout = (int8_t *)at(workspace, g.aout[b]);
         st = block_forward_impl(ctx, &net->block[b], g.b[b], &bp, cur, aout, at(workspace, g.state[b]),
-                                false);
+                                false, true);
         if (st != NITRO_OK) return st;
         cur = aout;
         if (b + 1 == net->n_blocks) break;

@@ -368,11 +368,13 @@ void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *
                           const int32_t *w, const Div &sf, const int32_t *labels,
                           const LearningBuffers &b, const uint8_t *code, const Relu &rp, int h,
                           int wdt, int c, bool pool, int32_t *g, int32_t *delta_copy,
-                          int32_t *yhat, int32_t *e, int64_t *dw, uint32_t *flags)
+                          int32_t *yhat, int32_t *e, int64_t *dw, uint32_t *flags,
+                          bool prepacked)
 {
     const LearningScratch sc = learning_scratch(n, d, G);
-    // operands: learning-weight limb planes, the transposed block output
-    launch_pack_matrix(s, w, G, (int)d, sc.gp, b.wf, b.wt, b.wmax);
+    // operands: learning-weight limb planes (unless the caller packed them), the transposed
+    // block output
+    if (!prepacked) launch_pack_matrix(s, w, G, (int)d, sc.gp, b.wf, b.wt, b.wmax);
     hipLaunchKernelGGL(k_transpose_i8, dim3((unsigned)((d + 63) / 64), (unsigned)((sc.np + 63) / 64)),
                        dim3(256), 0, s, f, n, (int)d, sc.np, b.ft);
     // forward: split-K partials, then yhat / e

@@ -488,7 +488,7 @@ void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *
                           const int32_t *w, const Div &sf, const int32_t *labels,
                           const LearningBuffers &b, const uint8_t *code, const Relu &rp, int h,
                           int wdt, int c, bool pool, int32_t *g, int32_t *delta_copy,
-                          int32_t *yhat, int32_t *e, int64_t *dw, uint32_t *flags);
+                          int32_t *yhat, int32_t *e, int64_t *dw, uint32_t *flags, bool prepacked = false);
 
 // ---- few input channels (conv_smallc.hip)
 bool smallc_fwd_ok(const ConvShape &sh);
@@ -556,6 +556,34 @@ void launch_conv_dw(hipStream_t s, const ConvShape &sh, const int32_t *g, const 
 // ---- preparation and bookkeeping (prep.hip)
 // Conv weight W [co][9][ci] -> wf [4][co][9 ci] and wt [4][ci][9 co] in one pass (co, ci % 16 == 0).
 bool pack_conv_tiled_ok(int co, int ci);
+// int32 values -> 4 balanced int8 limb planes, plain p and transposed t (rows padded to Rpad),
+// in 64 x 64 tiles, batched over z; max |value| into wmax
+struct PackArgs {
+    const int32_t *x;
+    int64_t xs, zx;
+    int R, C, Rpad;
+    int8_t *p;
+    int64_t ps, pplane, zp;
+    int8_t *t;
+    int64_t ts, tplane, zt;
+    uint32_t *wmax;
+};
+PackArgs pack_conv_args(const int32_t *w, int co, int ci, int8_t *wf, int8_t *wt, uint32_t *wmax);
+PackArgs pack_matrix_args(const int32_t *w, int R, int C, int Rpad, int8_t *p, int8_t *t,
+                          uint32_t *wmax);
+constexpr int PACK_BATCH = 16;
+struct PackBatch {
+    PackArgs t[PACK_BATCH];
+    int gx[PACK_BATCH], gy[PACK_BATCH];
+    int first[PACK_BATCH + 1];
+    int n;
+};
+// packs gathered on the host and enqueued as one launch (flushed when full)
+struct PackList {
+    PackBatch b{};
+    void add(hipStream_t s, const PackArgs &a, int batches);   // batches: 9 for a conv weight
+    void flush(hipStream_t s);
+};
 void launch_pack_conv_tiled(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,
                             int8_t *wt, uint32_t *wmax);
 // Matrix X [R][C] (C % 16 == 0, Rpad % 16 == 0) -> limb planes P [4][R][C] and T [4][C][Rpad].

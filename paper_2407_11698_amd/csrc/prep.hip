@@ -11,23 +11,15 @@ namespace nitro {
 //   T[l][c][r] at t[z zt + l tplane + c ts + r] for r < Rpad, zero rows r >= R  (when t != null)
 // and max|X| into a max slot. One workgroup: a 64 x 64 tile, z = blockIdx.z (the taps of a
 // conv weight). C, ps, ts, Rpad and the z offsets keep every 16-byte row chunk aligned.
-struct PackArgs {
-    const int32_t *x;
-    int64_t xs, zx;
-    int R, C, Rpad;
-    int8_t *p;
-    int64_t ps, pplane, zp;
-    int8_t *t;
-    int64_t ts, tplane, zt;
-    uint32_t *wmax;
-};
 
-__global__ __launch_bounds__(256) void k_pack_limbs(PackArgs a)
+constexpr int PACK_LS = 68;                  // LDS row stride (bytes) of the transposed tile
+
+// One 64 x 64 tile (column tile bx, row tile by, batch z) of a pack: the four limb planes of
+// every value, plain and (through LDS) transposed, and the tile's max |value| into the slot.
+__device__ void pack_tile(const PackArgs &a, int bx, int by, int z, uint8_t (*L)[64][PACK_LS])
 {
-    constexpr int LS = 68;                   // LDS row stride (bytes) of the transposed tile
-    __shared__ __attribute__((aligned(16))) uint8_t L[4][64][LS];
     const int tid = threadIdx.x;
-    const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64, z = blockIdx.z;
+    const int c0 = bx * 64, r0 = by * 64;
     const int r = tid >> 2, cq = (tid & 3) * 16;
     const int gr = r0 + r, gc = c0 + cq;
     const bool ok = gr < a.R && gc < a.C;
@@ -69,6 +61,47 @@ __global__ __launch_bounds__(256) void k_pack_limbs(PackArgs a)
     block_slot_max(a.wmax, m);
 }
 
+__global__ __launch_bounds__(256) void k_pack_limbs(PackArgs a)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t L[4][64][PACK_LS];
+    pack_tile(a, blockIdx.x, blockIdx.y, blockIdx.z, L);
+}
+
+// Several packs in one launch: workgroups are dealt to the packs in order (first[k] ..
+// first[k+1]), each pack's tiles numbered column tile fastest, then row tile, then batch.
+__global__ __launch_bounds__(256) void k_pack_batch(PackBatch b)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t L[4][64][PACK_LS];
+    const int wid = blockIdx.x;
+    int k = 0;
+    while (k + 1 < b.n && wid >= b.first[k + 1]) k++;
+    const int loc = wid - b.first[k];
+    const int bx = loc % b.gx[k], rest = loc / b.gx[k];
+    pack_tile(b.t[k], bx, rest % b.gy[k], rest / b.gy[k], L);
+}
+
+static void pack_grid(const PackArgs &a, int *gx, int *gy) { *gx = (a.C + 63) / 64; *gy = (a.Rpad + 63) / 64; }
+
+void PackList::add(hipStream_t s, const PackArgs &a, int batches)
+{
+    if (b.n == PACK_BATCH) flush(s);
+    int gx, gy;
+    pack_grid(a, &gx, &gy);
+    b.t[b.n] = a;
+    b.gx[b.n] = gx;
+    b.gy[b.n] = gy;
+    b.first[b.n + 1] = b.first[b.n] + gx * gy * batches;
+    b.n++;
+}
+
+void PackList::flush(hipStream_t s)
+{
+    if (b.n == 0) return;
+    hipLaunchKernelGGL(k_pack_batch, dim3((unsigned)b.first[b.n]), dim3(256), 0, s, b);
+    b.n = 0;
+    b.first[0] = 0;
+}
+
 static void launch_pack(hipStream_t s, const PackArgs &a, int batches)
 {
     const dim3 grid((unsigned)((a.C + 63) / 64), (unsigned)((a.Rpad + 63) / 64), (unsigned)batches);
@@ -76,6 +109,30 @@ static void launch_pack(hipStream_t s, const PackArgs &a, int batches)
 }
 
 bool pack_conv_tiled_ok(int co, int ci) { return co % 16 == 0 && ci % 16 == 0; }
+
+PackArgs pack_conv_args(const int32_t *w, int co, int ci, int8_t *wf, int8_t *wt, uint32_t *wmax)
+{
+    // per tap t: X_t[o][c] = W[o][t][c]; wf = [l][o][9 ci] (tap-major K), wt = [l][c][9 co]
+    PackArgs a{};
+    a.x = w; a.xs = 9 * (int64_t)ci; a.zx = ci;
+    a.R = co; a.C = ci; a.Rpad = co;
+    a.p = wf; a.ps = 9 * (int64_t)ci; a.pplane = (int64_t)co * 9 * ci; a.zp = ci;
+    a.t = wt; a.ts = 9 * (int64_t)co; a.tplane = (int64_t)ci * 9 * co; a.zt = co;
+    a.wmax = wmax;
+    return a;
+}
+
+PackArgs pack_matrix_args(const int32_t *w, int R, int C, int Rpad, int8_t *p, int8_t *t,
+                          uint32_t *wmax)
+{
+    PackArgs a{};
+    a.x = w; a.xs = C; a.zx = 0;
+    a.R = R; a.C = C; a.Rpad = Rpad;
+    a.p = p; a.ps = C; a.pplane = (int64_t)R * C; a.zp = 0;
+    a.t = t; a.ts = Rpad; a.tplane = (int64_t)C * Rpad; a.zt = 0;
+    a.wmax = wmax;
+    return a;
+}
 
 void launch_pack_conv_tiled(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,
                             int8_t *wt, uint32_t *wmax)
