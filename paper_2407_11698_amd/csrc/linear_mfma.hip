@@ -6,6 +6,8 @@
 //   gradient   dW[g][k] = sum_n e[n][g] f[n][k]
 // All three are C[m][j] = sum_k A[m][k] B[j][k] with K-contiguous rows: one kernel, three
 // epilogues. Wide operands use balanced int8 limbs as in the convolution kernels.
+#include <type_traits>
+
 #include "mfma_common.h"
 
 namespace nitro {
@@ -198,51 +200,56 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     __syncthreads();
     uint32_t mx = 0;
     const uint32_t W2 = (uint32_t)p.w / 2;
-    for (int it = tid; it < LG_BM * (LG_BN / 16); it += 256) {
-        const int row = it / (LG_BN / 16), cc = (it % (LG_BN / 16)) * 16;
-        const int m = m0 + row, col = n0 + cc;
-        if (m >= p.M || col >= p.N) continue;
-        const int64_t o = (int64_t)m * p.N + col;
-        const v4i cd = *(const v4i *)(p.code + o);
-        v4i dv[4], gv[4];
+    auto emit = [&](auto trunc_tag) {
+        constexpr bool TR = decltype(trunc_tag)::value;
+        for (int it = tid; it < LG_BM * (LG_BN / 16); it += 256) {
+            const int row = it / (LG_BN / 16), cc = (it % (LG_BN / 16)) * 16;
+            const int m = m0 + row, col = n0 + cc;
+            if (m >= p.M || col >= p.N) continue;
+            const int64_t o = (int64_t)m * p.N + col;
+            const v4i cd = *(const v4i *)(p.code + o);
+            v4i dv[4], gv[4];
 #pragma unroll
-        for (int e = 0; e < 16; e++) {
-            const int32_t v = Ds[row * DS + cc + e];
-            const uint32_t c8 = ((uint32_t)cd[e >> 2] >> (8 * (e & 3))) & 0xFFu;
-            const int64_t g = relu_bwd(v, (uint8_t)(p.pool ? c8 >> 2 : c8), p.rp);
-            bad |= !fits_i32(g);
-            const uint32_t a = abs_i64_sat(g);
-            mx = a > mx ? a : mx;
-            dv[e >> 2][e & 3] = v;
-            gv[e >> 2][e & 3] = (int32_t)g;
-        }
-        if (p.delta)
+            for (int e = 0; e < 16; e++) {
+                // |g| <= |delta|, and delta was checked to fit int32
+                const int32_t v = Ds[row * DS + cc + e];
+                const uint32_t c8 = ((uint32_t)cd[e >> 2] >> (8 * (e & 3))) & 0xFFu;
+                const int32_t g = relu_bwd32<TR>(v, p.pool ? c8 >> 2 : c8, p.rp);
+                const uint32_t a = abs_u32(g);
+                mx = a > mx ? a : mx;
+                dv[e >> 2][e & 3] = v;
+                gv[e >> 2][e & 3] = g;
+            }
+            if (p.delta)
 #pragma unroll
-            for (int q = 0; q < 4; q++) *(v4i *)(p.delta + o + 4 * q) = dv[q];
-        if (!p.pool) {
+                for (int q = 0; q < 4; q++) *(v4i *)(p.delta + o + 4 * q) = dv[q];
+            if (!p.pool) {
 #pragma unroll
-            for (int q = 0; q < 4; q++) *(v4i *)(p.g + o + 4 * q) = gv[q];
-            continue;
-        }
-        const uint32_t ch = (uint32_t)col % (uint32_t)p.c, pp = (uint32_t)col / (uint32_t)p.c;
-        const uint32_t q2 = pp % W2, h2 = pp / W2;
-        int32_t *gb = p.g + (int64_t)m * p.h * p.w * p.c + ch;
+                for (int q = 0; q < 4; q++) *(v4i *)(p.g + o + 4 * q) = gv[q];
+                continue;
+            }
+            const uint32_t ch = (uint32_t)col % (uint32_t)p.c, pp = (uint32_t)col / (uint32_t)p.c;
+            const uint32_t q2 = pp % W2, h2 = pp / W2;
+            int32_t *gb = p.g + (int64_t)m * p.h * p.w * p.c + ch;
 #pragma unroll
-        for (int u = 0; u < 4; u++) {
-            const uint32_t pix = (2 * h2 + (u >> 1)) * (uint32_t)p.w + 2 * q2 + (u & 1);
+            for (int u = 0; u < 4; u++) {
+                const uint32_t pix = (2 * h2 + (u >> 1)) * (uint32_t)p.w + 2 * q2 + (u & 1);
 #pragma unroll
-            for (int q = 0; q < 4; q++) {
-                v4i o4;
+                for (int q = 0; q < 4; q++) {
+                    v4i o4;
 #pragma unroll
-                for (int r = 0; r < 4; r++) {
-                    const int e = 4 * q + r;
-                    const uint32_t arg = ((uint32_t)cd[e >> 2] >> (8 * (e & 3))) & 3u;
-                    o4[r] = arg == (uint32_t)u ? gv[q][r] : 0;
+                    for (int r = 0; r < 4; r++) {
+                        const int e = 4 * q + r;
+                        const uint32_t arg = ((uint32_t)cd[e >> 2] >> (8 * (e & 3))) & 3u;
+                        o4[r] = arg == (uint32_t)u ? gv[q][r] : 0;
+                    }
+                    *(v4i *)(gb + (int64_t)pix * p.c + 4 * q) = o4;
                 }
-                *(v4i *)(gb + (int64_t)pix * p.c + 4 * q) = o4;
             }
         }
-    }
+    };
+    if (p.rp.alpha.trunc) emit(std::true_type{});
+    else emit(std::false_type{});
     if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
     block_slot_max(p.gmax, mx);
 }

@@ -15,7 +15,9 @@ from typing import Optional, Sequence
 import torch  # noqa: F401
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libnitro.so")
+# NITRO_LIBRARY names another build of the library to load (for comparing builds); the default
+# is the in-tree one
+LIB_PATH = os.environ.get("NITRO_LIBRARY") or os.path.join(HERE, "libnitro.so")
 
 MAX_LAYERS = 4
 MAX_BLOCKS = 8
@@ -74,8 +76,8 @@ class HParams(ctypes.Structure):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError("libnitro.so is not built (run `python -m paper_2407_11698_amd.build`); "
-                          "there is no fallback path")
+        raise ImportError("%s is not built (run `python -m paper_2407_11698_amd.build`); "
+                          "there is no fallback path" % LIB_PATH)
     lib = ctypes.CDLL(LIB_PATH)
     P = ctypes.POINTER
     sig = {
