@@ -73,13 +73,16 @@ def recorded_traffic(kernel: str):
     summary under profiles/ (FETCH_SIZE and WRITE_SIZE passes, each calibrated by a copy of
     known size); None when there is no summary or the kernel's source has changed since."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "%s_vgg_cnn_b256_traffic.txt" % kernel.split("<")[0])
+    tag = kernel.replace("<", "_").replace(">", "")
+    path = os.path.join(ROOT, "profiles", "%s_vgg_cnn_b256_traffic.txt" % tag)
     try:
         kv = dict(line.split(": ", 1) for line in open(path).read().splitlines() if ": " in line)
-        src = open(os.path.join(ROOT, kv["source"]), "rb").read()
+        h = hashlib.sha256()
+        for f in kv["sources"].split():
+            h.update(open(os.path.join(ROOT, f), "rb").read())
     except (OSError, KeyError, ValueError):
         return None
-    if kv.get("kernel") != kernel or hashlib.sha256(src).hexdigest() != kv.get("source_sha256"):
+    if kv.get("kernel") != kernel or h.hexdigest() != kv.get("sources_sha256"):
         return None
     return int(float(kv["traffic_bytes_per_launch"]))
 
