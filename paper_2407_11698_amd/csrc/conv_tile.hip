@@ -86,7 +86,8 @@ __device__ inline int32_t sat_i32(int64_t v)
 // global loads are issued before the current phase computes; the fragments of the next K-step
 // are read from LDS while the MFMAs of the current one run.
 template <int MODE, int CC, int WM>
-__global__ __launch_bounds__(128 * WM) void k_conv_tile(TileArgs p)
+__global__ __launch_bounds__(128 * WM) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_conv_tile(TileArgs p)
 {
     using S = CtShape<WM>;
     using C = CtCfg<CC, WM>;
@@ -241,15 +242,22 @@ __global__ __launch_bounds__(128 * WM) void k_conv_tile(TileArgs p)
     auto compute = [&](const uint8_t *As) {
         v4i af[2][TM], bf[2][TN];
         load_frags(As, af[0], bf[0], 0);
+        // the next K-step's fragment reads are issued before this K-step's MFMAs, and the
+        // scheduling barriers keep them there: left to itself the scheduler issues each read just
+        // before its first use and then waits for it. (The 128-pixel input-gradient kernel has
+        // no registers left for the second set of fragments.)
+        constexpr bool PIPE = !(WM == 2 && MODE == IG_DX);
 #pragma unroll
         for (int ks = 0; ks < C::KSC; ks++) {
             if (ks + 1 < C::KSC) load_frags(As, af[(ks + 1) & 1], bf[(ks + 1) & 1], ks + 1);
+            if (PIPE) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int i = 0; i < TM; i++)
 #pragma unroll
                 for (int j = 0; j < TN; j++)
                     acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(bf[ks & 1][j], af[ks & 1][i],
                                                                       acc[i][j], 0, 0, 0);
+            if (PIPE) __builtin_amdgcn_sched_barrier(0);
         }
     };
     auto fold = [&](int ph) {
