@@ -247,6 +247,16 @@ inline uint8_t *at(void *base, size_t off) { return (uint8_t *)base + off; }
 
 // zero_slots: clear the block's max slots first (a training iteration clears every block's
 // slots once, up front, instead)
+// The block's last layer takes the weight-gradient kernel over padded planes and the layer
+// before it the tiled forward (not pooled, being an inner layer): that forward also writes its
+// output as the last layer's x rows, and the backward only zeroes their pad rows.
+static bool rows_from_forward(const BlockGeom &g)
+{
+    if (g.J < 2) return false;
+    const LayerGeom &P = g.L[g.J - 2], &L = g.L[g.J - 1];
+    return P.conv && L.conv && P.fwd_tile && dwp_ok(L.sh) && L.sh.c % 16 == 0;
+}
+
 nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, const BlockGeom &g,
                                 const nitro_block_params *p, const int8_t *x, int8_t *a_out,
                                 void *state, bool zero_slots = true, bool prepacked = false)
@@ -284,9 +294,12 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
                 sx.c = 16;
                 xin = xpad;
             }
+            const bool rows = j == g.J - 2 && rows_from_forward(g);
             if (L.fwd_tile)
                 launch_conv_fwd_tile(s, ctx->conv_tile, sx, xin, wf, wmax, L.sf, desc->alpha_inv, desc->round, rp,
-                                     pool, out, code, ctx->flags);
+                                     pool, out, code, ctx->flags,
+                                     rows ? (int8_t *)at(state, g.xpl) : nullptr,
+                                     rows ? dwp_rows_stride(g.L[j + 1].sh) : 0);
             else if (L.pad16)
                 launch_conv_fwd_mfma(s, sx, xin, wf, wmax, sf, rp, pool, out, code, ctx->flags);
             else if (mfma_conv_fwd_ok(L.sh, pool))
@@ -372,7 +385,8 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                 launch_conv_dw_planes(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, xin,
                                       (int8_t *)at(state, g.gt), (int8_t *)at(state, g.xpl),
                                       L.dx_tile && need_dx ? (int8_t *)at(state, g.gnl) : nullptr,
-                                      (int64_t *)at(state, g.part), gr->dw[j], ctx->flags);
+                                      (int64_t *)at(state, g.part), gr->dw[j], ctx->flags,
+                                      j == J - 1 && rows_from_forward(g));
             else if (mfma_conv_dw_ok(L.sh) || mfma_conv_dw_smallc_ok(L.sh))
                 launch_conv_dw_mfma(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, xin, (int8_t *)at(state, g.gt),
                                     (int64_t *)at(state, g.part), gr->dw[j], ctx->flags);

@@ -28,7 +28,6 @@
 namespace nitro {
 
 constexpr int DWP_KS = 256;        // padded positions per super-step (4 MFMA K-steps of 64)
-constexpr int DWP_HMAX = 64;       // largest halo: W <= 62
 constexpr int DWP_CHUNK_MAX = 511;    // super-steps per workgroup (and per wave: <= 511 * 256)
 constexpr int DWP_WIN = DWP_KS + 2 * DWP_HMAX;   // staged rows (positions) of a super-step
 constexpr int DWP_NCH = DWP_WIN / 64;            // 16-byte rows per lane
@@ -93,6 +92,8 @@ int64_t dwp_partial_count(const ConvShape &sh)
     return p.nsplit > 1 ? (int64_t)p.nsplit * sh.co * 9 * sh.c : 0;
 }
 
+int64_t dwp_rows_stride(const ConvShape &sh) { return dwp_geom(sh).xs; }
+
 int64_t dwp_gplane_bytes(const ConvShape &sh) { return 4 * (int64_t)sh.co * dwp_geom(sh).kp; }
 int64_t dwp_xplane_bytes(const ConvShape &sh) { return (int64_t)dwp_c16(sh) * dwp_geom(sh).xs; }
 
@@ -131,6 +132,30 @@ __global__ __launch_bounds__(256) void k_dwp_act_rows(const int8_t *__restrict__
         }
     }
     *(v4i *)(xr + ((int64_t)t * xs + i) * 16) = v;
+}
+
+// Zeros in the pad rows of xr (the halos, the column after every image row, the row after every
+// image, the tail): the rows of the real pixels were written by the previous layer's forward.
+// One thread: one pad position of one 16-channel tile.
+__global__ __launch_bounds__(256) void k_dwp_pad_rows(int n, int h, int w, int hp, int wp,
+                                                      int64_t kraw, int64_t xs,
+                                                      int8_t *__restrict__ xr)
+{
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int t = blockIdx.y;
+    const int64_t inner = (int64_t)n * (h + w + 1);
+    int64_t row;
+    if (i < inner) {
+        const int img = (int)(i / (h + w + 1)), j = (int)(i - (int64_t)img * (h + w + 1));
+        const int hh = j < h ? j : h, ww = j < h ? w : j - h;
+        row = DWP_HMAX + ((int64_t)img * hp + hh) * wp + ww;
+    } else if (i < inner + DWP_HMAX) {
+        row = i - inner;
+    } else {
+        row = DWP_HMAX + kraw + (i - inner - DWP_HMAX);
+        if (row >= xs) return;
+    }
+    *(v4i *)(xr + ((int64_t)t * xs + row) * 16) = v4i{0, 0, 0, 0};
 }
 
 // g int32 NHWC [P][C] -> gp [l][C][kp] for l < limbs(max|g|): limb l of g at padded position k
@@ -388,13 +413,20 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
-                           int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags)
+                           int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags,
+                           bool x_rows_ready)
 {
     const DwpGeom ge = dwp_geom(sh);
     const DwpPlan pl = dwp_plan(sh);
     const int c16 = dwp_c16(sh);
-    hipLaunchKernelGGL(k_dwp_act_rows, dim3((unsigned)((ge.xs + 255) / 256), (unsigned)(c16 / 16)),
-                       dim3(256), 0, s, x, sh.n, sh.h, sh.w, sh.c, ge.hp, ge.wp, (int)ge.xs, xp);
+    if (x_rows_ready) {
+        const int64_t pads = (int64_t)sh.n * (sh.h + sh.w + 1) + DWP_HMAX + (ge.xs - DWP_HMAX - ge.kraw);
+        hipLaunchKernelGGL(k_dwp_pad_rows, dim3((unsigned)((pads + 255) / 256), (unsigned)(c16 / 16)),
+                           dim3(256), 0, s, sh.n, sh.h, sh.w, ge.hp, ge.wp, ge.kraw, ge.xs, xp);
+    } else {
+        hipLaunchKernelGGL(k_dwp_act_rows, dim3((unsigned)((ge.xs + 255) / 256), (unsigned)(c16 / 16)),
+                           dim3(256), 0, s, x, sh.n, sh.h, sh.w, sh.c, ge.hp, ge.wp, (int)ge.xs, xp);
+    }
     hipLaunchKernelGGL(k_dwp_grad_planes, dim3((unsigned)(ge.kp / 64), (unsigned)((sh.co + 63) / 64)),
                        dim3(256), 0, s, g, sh.n, sh.h, sh.w, sh.co, ge.hp, ge.wp, (int)ge.kp, gmax, gp,
                        gn);

@@ -66,6 +66,9 @@ struct TileArgs {
     int pool;
     int8_t *out;
     uint8_t *code;
+    int8_t *xr;                    // optional (not pooled): the next layer's weight-gradient x rows
+    int64_t xs;                    // their stride (positions per 16-channel tile)
+    Div32 d_h;                     // reciprocal of H
     // input-gradient epilogue
     const uint8_t *prev_code;
     Relu rp;
@@ -346,8 +349,16 @@ void k_conv_tile(TileArgs p)
                 const int64_t m = m0 + row;
                 if (m >= M || n0 + 16 * q >= p.no) continue;
                 const int64_t o = m * p.no + n0 + 16 * q;
-                *(v4i *)(p.out + o) = *(const v4i *)(Ov + row * OW + 4 * q);
+                const v4i av = *(const v4i *)(Ov + row * OW + 4 * q);
+                *(v4i *)(p.out + o) = av;
                 *(v4i *)(p.code + o) = *(const v4i *)(Rv + row * OW + 4 * q);
+                if (p.xr) {
+                    // padded position of pixel m: (n (H+1) + h)(W+1) + w = (R + R / H)(W+1) + w,
+                    // R = m / W its row over all images
+                    const uint32_t R = udiv32((uint32_t)m, p.d_w), ww = (uint32_t)m - R * (uint32_t)p.w;
+                    const int64_t k = (int64_t)(R + udiv32(R, p.d_h)) * (p.w + 1) + ww;
+                    *(v4i *)(p.xr + ((int64_t)((n0 >> 4) + q) * p.xs + DWP_HMAX + k) * 16) = av;
+                }
             }
         } else {
             // 2x2 windows, 4 channels per thread: the tile holds rt (even) whole image rows; the
@@ -510,6 +521,7 @@ static void launch_tile(hipStream_t s, TileArgs a)
     a.d_seg = make_div32((uint32_t)((a.rs + 2) * (a.w + 2)));
     a.d_w = make_div32((uint32_t)a.w);
     a.d_rw = make_div32((uint32_t)(a.rs * a.w));
+    a.d_h = make_div32((uint32_t)a.h);
     const dim3 grid((unsigned)(((a.n * a.h + a.rt - 1) / a.rt) * ((a.no + CT_BN - 1) / CT_BN)));
     const dim3 block(CtShape<WM>::NT);
     a.ts = timer_slot(MODE == IG_FWD ? TIMED_CONV_FWD : TIMED_CONV_DX);
@@ -522,7 +534,8 @@ static void launch_tile(hipStream_t s, TileArgs a)
 
 void launch_conv_fwd_tile(hipStream_t s, int tile, const ConvShape &sh, const int8_t *x, const int8_t *wf,
                           const uint32_t *wmax, int64_t sf, int alpha_inv, int round,
-                          const Relu &rp, bool pool, int8_t *out, uint8_t *code, uint32_t *flags)
+                          const Relu &rp, bool pool, int8_t *out, uint8_t *code, uint32_t *flags,
+                          int8_t *xr, int64_t xs)
 {
     TileArgs a{};
     a.n = sh.n; a.h = sh.h; a.w = sh.w;
@@ -532,6 +545,7 @@ void launch_conv_fwd_tile(hipStream_t s, int tile, const ConvShape &sh, const in
     a.sf = make_scale_fast(sf, alpha_inv, rp.mu, round);
     a.pool = pool ? 1 : 0;
     a.out = out; a.code = code;
+    a.xr = pool ? nullptr : xr; a.xs = xs;
     a.flags = flags;
     if (use_wide_tile(tile, sh.n, sh.h, sh.w, sh.co, pool)) launch_tile<IG_FWD, 4>(s, a);
     else launch_tile<IG_FWD, 2>(s, a);

@@ -530,17 +530,26 @@ int64_t dwp_gplane_bytes(const ConvShape &sh);
 int64_t dwp_xplane_bytes(const ConvShape &sh);
 int64_t dwp_partial_count(const ConvShape &sh);
 // gn (optional): also write g's NHWC limb planes [4][P][co] (the input-gradient tile kernel's A).
+// x rows [C16 / 16][xs][16] of the weight-gradient kernel: a zero halo of DWP_HMAX positions,
+// then padded position k = (n (H+1) + h)(W+1) + w at row DWP_HMAX + k. With x_rows_ready the
+// caller has written every real pixel's row (the forward epilogue of the previous layer) and
+// only the pad rows are zeroed here.
+constexpr int DWP_HMAX = 64;
+int64_t dwp_rows_stride(const ConvShape &sh);   // xs
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
-                           int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags);
+                           int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags,
+                           bool x_rows_ready = false);
 
 // ---- implicit-GEMM conv with the input tile staged once (conv_tile.hip)
 bool tile_conv_fwd_ok(const ConvShape &sh, bool pool, int64_t sf, int alpha_inv);
 bool tile_conv_dx_ok(const ConvShape &sh);
-// tile: 0 by shape, 128 or 256 pixels forced where that tile fits (nitro_set_conv_tile)
+// tile: 0 by shape, 128 or 256 pixels forced where that tile fits (nitro_set_conv_tile); xr
+// (not pooled): also write the output into the next layer's weight-gradient x rows
 void launch_conv_fwd_tile(hipStream_t s, int tile, const ConvShape &sh, const int8_t *x, const int8_t *wf,
                           const uint32_t *wmax, int64_t sf, int alpha_inv, int round,
-                          const Relu &rp, bool pool, int8_t *out, uint8_t *code, uint32_t *flags);
+                          const Relu &rp, bool pool, int8_t *out, uint8_t *code, uint32_t *flags,
+                          int8_t *xr = nullptr, int64_t xs = 0);
 // gl: g's NHWC limb planes [LA][P][co] (max|g| in gmax_in); otherwise as launch_conv_dx_mfma
 void launch_conv_dx_tile(hipStream_t s, int tile, const ConvShape &sh, const int8_t *gl,
                          const uint32_t *gmax_in, const int8_t *wt, const uint32_t *wmax,
