@@ -503,14 +503,15 @@ bool tile_conv_dx_ok(const ConvShape &sh)
 }
 
 // The 256-pixel tile where it fits (pooling needs an even number of rows per tile) and, chosen by
-// shape, where it still gives at least two tiles per CU.
+// shape, where it still gives at least one tile per two CUs (measured on the VGG-style layers:
+// even at 8x8 images with 128 to 256 tiles it beats two 128-pixel workgroups per CU).
 static bool use_wide_tile(int pref, int n, int h, int w, int no, bool pool)
 {
     int rt, ns, rs;
     if (pref == 128 || !tile_geom<4>(h, w, &rt, &ns, &rs) || (pool && rt % 2)) return false;
     if (pref == 256) return true;
     const int64_t tiles = ((int64_t)n * h / rt) * ((no + CT_BN - 1) / CT_BN);
-    return tiles >= 512;
+    return tiles >= 128;
 }
 
 template <int MODE, int WM>
