@@ -85,6 +85,12 @@ nitro_status nitro_set_stream(nitro_ctx *ctx, void *hip_stream);
  * geometry fits the layer (other layers keep the automatic choice). Results do not depend on it.
  * EINVAL for any other value. */
 nitro_status nitro_set_conv_tile(nitro_ctx *ctx, int32_t pixels);
+/* Workgroups of the tiled convolution kernels with the 256-pixel tile: 0 chooses by size (the
+ * default: for a launch of at least 4 tiles per compute unit, one persistent workgroup per compute
+ * unit, each taking tiles b, b + G, b + 2G, ...; otherwise one workgroup per tile), 1 makes every
+ * such launch persistent (with about 4 tiles per workgroup), -1 none. Results do not depend on
+ * it. EINVAL for any other value. */
+nitro_status nitro_set_conv_persistent(nitro_ctx *ctx, int32_t mode);
 /* Number of auxiliary streams nitro_train_step runs the blocks' local training on (0 to 3,
  * default 3): the forward pass runs on the context's stream; block b's local training starts
  * when block b's forward is done, on auxiliary stream b mod n, except the last block's, which

@@ -18,6 +18,7 @@ struct nitro_ctx : public LaunchTimer {
     int device = 0;
     hipStream_t stream = nullptr;
     int conv_tile = 0;                          // nitro_set_conv_tile
+    int conv_persist = 0;                       // nitro_set_conv_persistent
     int aux_use = 3;                            // nitro_set_aux_streams (<= NAUX)
     uint32_t *flags = nullptr;                  // device: sticky status bits
     // streams of their own for the blocks' local training in a training iteration (the blocks'
@@ -296,7 +297,7 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
             }
             const bool rows = j == g.J - 2 && rows_from_forward(g);
             if (L.fwd_tile)
-                launch_conv_fwd_tile(s, ctx->conv_tile, sx, xin, wf, wmax, L.sf, desc->alpha_inv, desc->round, rp,
+                launch_conv_fwd_tile(s, ctx->conv_tile, ctx->conv_persist, sx, xin, wf, wmax, L.sf, desc->alpha_inv, desc->round, rp,
                                      pool, out, code, ctx->flags,
                                      rows ? (int8_t *)at(state, g.xpl) : nullptr,
                                      rows ? dwp_rows_stride(g.L[j + 1].sh) : 0);
@@ -412,7 +413,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
             uint32_t *gmax_out = j > 0 ? slots + (4 + j - 1) * SLOT_WORDS : nullptr;
             if (L.conv) {
                 if (L.dx_tile)
-                    launch_conv_dx_tile(s, ctx->conv_tile, L.sh, (const int8_t *)at(state, g.gnl),
+                    launch_conv_dx_tile(s, ctx->conv_tile, ctx->conv_persist, L.sh, (const int8_t *)at(state, g.gnl),
                                         slots + (4 + j) * SLOT_WORDS,
                                         (const int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS,
                                         code, rp, dst, dst64, gmax_out, ctx->flags);
@@ -613,6 +614,13 @@ nitro_status nitro_set_conv_tile(nitro_ctx *ctx, int32_t pixels)
 {
     if (!ctx || (pixels != 0 && pixels != 128 && pixels != 256)) return NITRO_EINVAL;
     ctx->conv_tile = pixels;
+    return NITRO_OK;
+}
+
+nitro_status nitro_set_conv_persistent(nitro_ctx *ctx, int32_t mode)
+{
+    if (!ctx || mode < -1 || mode > 1) return NITRO_EINVAL;
+    ctx->conv_persist = mode;
     return NITRO_OK;
 }
 
@@ -920,6 +928,7 @@ nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
     put(&ctx->timing, sizeof(ctx->timing));
     put(&ctx->aux_use, sizeof(ctx->aux_use));
     put(&ctx->conv_tile, sizeof(ctx->conv_tile));
+    put(&ctx->conv_persist, sizeof(ctx->conv_persist));
     if (!ctx->gexec || key != ctx->gkey) {
         if (ctx->gexec) {
             (void)hipGraphExecDestroy(ctx->gexec);

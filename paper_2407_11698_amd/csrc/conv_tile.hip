@@ -53,6 +53,7 @@ struct TileArgs {
     int n, h, w;
     int ck;                        // channels of A; K = 9 ck (a multiple of the chunk size CC)
     int no;                        // GEMM N (a multiple of 16)
+    int ntiles;                    // output tiles (the grid may be smaller: persistent workgroups)
     const int8_t *a;               // forward: x NHWC; input gradient: limb planes [LA][P][ck]
     int64_t aplane;                // P * ck
     const uint32_t *a_max;         // input gradient: max|g| slot
@@ -88,7 +89,7 @@ __device__ inline int32_t sat_i32(int64_t v)
 // channels) stages the A pixels and the B block of 9 taps x 64 columns x CC. The next phase's
 // global loads are issued before the current phase computes; the fragments of the next K-step
 // are read from LDS while the MFMAs of the current one run.
-template <int MODE, int CC, int WM>
+template <int MODE, int CC, int WM, bool PERSIST>
 __global__ __launch_bounds__(128 * WM) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_conv_tile(TileArgs p)
 {
@@ -114,21 +115,12 @@ void k_conv_tile(TileArgs p)
     uint16_t *const tab = (uint16_t *)(smem + SMEM_MAIN);   // forward: entry for zs = -128 .. 128
     if (MODE == IG_FWD)
         for (int k = tid; k < 257; k += NT) tab[k] = relu_table_entry(k - 128, p.sf);
-    // tile of this workgroup: the eight XCDs each take a contiguous range of tiles, so the column
-    // tiles of one pixel tile run together and share their A rows in that XCD's L2
     const int ntile_n = (p.no + CT_BN - 1) / CT_BN;
-    const int ntiles = (int)gridDim.x;
-    int tile = blockIdx.x;
-    if ((ntiles & 7) == 0) tile = (tile & 7) * (ntiles >> 3) + (tile >> 3);
-    const int mt = tile / ntile_n, nt = tile - mt * ntile_n;
+    const int ntiles = p.ntiles;
     const int W2 = p.w + 2;
     const int segpx = (p.rs + 2) * W2;
     const int np = p.ns * segpx;
-    const int R0 = mt * p.rt;                      // first image row of the tile (over all images)
-    const int img0 = R0 / p.h, row0 = R0 - img0 * p.h;
     const int64_t M = (int64_t)p.n * p.h * p.w;
-    const int64_t m0 = (int64_t)R0 * p.w;
-    const int n0 = nt * CT_BN;
     const int K = 9 * p.ck;
     const int nchunk = p.ck / CC;
 
@@ -142,32 +134,46 @@ void k_conv_tile(TileArgs p)
     const int nph = npass * nchunk;
 
     // staged A items of this thread: item tid + NT v = (LDS pixel q, 16-channel group e), the
-    // groups of one pixel on consecutive lanes; the global byte offset within a chunk, or -1 for
-    // a zero (outside the image)
+    // groups of one pixel on consecutive lanes
     auto a_item = [&](int item, int &q, int &e) {
         q = item / C::GPT;
         e = item - q * C::GPT;
     };
-    int it_g[C::NIT];
-#pragma unroll
-    for (int v = 0; v < C::NIT; v++) {
-        int q, e;
-        a_item(tid + NT * v, q, e);
-        it_g[v] = -1;
-        if (q < np) {
-            const int seg = (int)udiv32(q, p.d_seg), r = q - seg * segpx;
-            const int lr = (int)udiv32(r, p.d_w2), lc = r - lr * W2;
-            const int img = img0 + seg, hh = row0 + lr - 1, ww = lc - 1;
-            if (img < p.n && hh >= 0 && hh < p.h && ww >= 0 && ww < p.w)
-                it_g[v] = ((img * p.h + hh) * p.w + ww) * p.ck + 16 * e;
-        }
-    }
     // staged B units of this thread: unit tid + NT v is (tap t, column c, unit u), the units of a
     // column on consecutive lanes; c and u are fixed by tid and t = v TPV + t0
     constexpr int TPV = NT / (CT_BN * NU);        // taps per NT units
     const int b_c = (tid % (CT_BN * NU)) / NU, b_u = tid % NU, b_t0 = tid / (CT_BN * NU);
-    const int b_g0 = (n0 + b_c < p.no ? n0 + b_c : p.no - 1) * K + b_t0 * p.ck + 16 * b_u;
     const int b_l0 = (b_t0 * CT_BN + b_c) * CC + 16 * (b_u ^ ct_bswz(CC, b_c));
+
+    // The current tile: its first output pixel m0 and column n0; the global byte offset within a
+    // chunk of each staged A item (-1: a zero, outside the image) and of this thread's B units.
+    // Tile order: each of the eight XCDs takes a contiguous range of tiles, so the column tiles of
+    // one pixel tile run together and share their A rows in that XCD's L2.
+    int64_t m0;
+    int n0, b_g0;
+    int it_g[C::NIT];
+    auto set_tile = [&](int v) {
+        const int tile = (ntiles & 7) == 0 ? (v & 7) * (ntiles >> 3) + (v >> 3) : v;
+        const int mt = tile / ntile_n, nt = tile - mt * ntile_n;
+        const int R0 = mt * p.rt;                  // first image row of the tile (over all images)
+        const int img0 = (int)udiv32((uint32_t)R0, p.d_h), row0 = R0 - img0 * p.h;
+        m0 = (int64_t)R0 * p.w;
+        n0 = nt * CT_BN;
+#pragma unroll
+        for (int u = 0; u < C::NIT; u++) {
+            int q, e;
+            a_item(tid + NT * u, q, e);
+            it_g[u] = -1;
+            if (q < np) {
+                const int seg = (int)udiv32(q, p.d_seg), r = q - seg * segpx;
+                const int lr = (int)udiv32(r, p.d_w2), lc = r - lr * W2;
+                const int img = img0 + seg, hh = row0 + lr - 1, ww = lc - 1;
+                if (img < p.n && hh >= 0 && hh < p.h && ww >= 0 && ww < p.w)
+                    it_g[u] = ((img * p.h + hh) * p.w + ww) * p.ck + 16 * e;
+            }
+        }
+        b_g0 = (n0 + b_c < p.no ? n0 + b_c : p.no - 1) * K + b_t0 * p.ck + 16 * b_u;
+    };
     int cpix[TM];
 #pragma unroll
     for (int i = 0; i < TM; i++) {
@@ -230,17 +236,7 @@ void k_conv_tile(TileArgs p)
     };
 
     int64_t acc64[TM][TN][4];
-#pragma unroll
-    for (int i = 0; i < TM; i++)
-#pragma unroll
-        for (int j = 0; j < TN; j++)
-#pragma unroll
-            for (int t = 0; t < 4; t++) acc64[i][j][t] = 0;
     v4i acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; i++)
-#pragma unroll
-        for (int j = 0; j < TN; j++) acc[i][j] = v4i{0, 0, 0, 0};
 
     auto compute = [&](const uint8_t *As) {
         v4i af[2][TM], bf[2][TN];
@@ -279,183 +275,221 @@ void k_conv_tile(TileArgs p)
         }
     };
 
+    // Persistent (two stages, one workgroup per CU): workgroup b takes tiles b, b + G, b + 2G, ...
+    // (G = the grid size), its set-up done once, and the global loads of the next tile's first
+    // phase are issued before the epilogue and overlap it. Otherwise one tile per workgroup.
+    uint32_t mx = 0;                              // input gradient: max |g| over this workgroup
+    bool bad = false;                             // input gradient: a sum outside int32
+    int v = blockIdx.x;
+    set_tile(v);
     stage_load(0);
-    if (S::NBUF == 1) {
-        for (int ph = 0; ph < nph; ph++) {
-            __syncthreads();                      // every wave is done with the previous stage
-            stage_store(0);
-            __syncthreads();
-            if (ph + 1 < nph) stage_load(ph + 1);
-            compute(smem);
-            fold(ph);
-        }
-    } else {
-        // stage ph & 1 is complete after the barrier of iteration ph; the other stage was last
-        // read in iteration ph - 1, before that barrier, so it can take phase ph + 1's operands
-        stage_store(0);
-        for (int ph = 0; ph < nph; ph++) {
-            __syncthreads();
-            if (ph + 1 < nph) stage_load(ph + 1);
-            compute(smem + (ph & 1) * SAB);
-            fold(ph);
-            if (ph + 1 < nph) stage_store((ph + 1) & 1);
-        }
-    }
-    __syncthreads();                              // the epilogue reuses the stages' LDS
-    // ---------------------------------------------------------------- epilogues
-    // The MFMAs took B as the first operand: lane l of tile (i, j) holds output channels
-    // cb = wn 32 + 16 j + 4 g4 .. cb + 3 of pixel wm 64 + 16 i + l % 16.
-    const int pxl = wm * 64 + (lane & 15);
-    const int cbl = wn * 32 + 4 * g4;
-    if (MODE == IG_FWD) {
-        // NITRO-Scaling (shift, clamp, one multiply-high) and the table's NITRO-ReLU per element;
-        // four channels packed per dword into LDS, then 16-byte (or pooled) stores. Several limb
-        // passes: the int64 sum saturated to int32 still saturates z* (128 SF < 2^31).
-        if (npass > 1) {
-#pragma unroll
-            for (int i = 0; i < TM; i++)
-#pragma unroll
-                for (int j = 0; j < TN; j++)
-#pragma unroll
-                    for (int t = 0; t < 4; t++) acc[i][j][t] = sat_i32(acc64[i][j][t]);
-        }
-        constexpr int OW = OS / 4;                // row stride in dwords
-        uint32_t *Ov = (uint32_t *)smem;          // [BM][OW] packed activations
-        uint32_t *Rv = Ov + BM * OW;              // [BM][OW] packed region codes
-        auto pack = [&](auto trunc_tag) {
-            constexpr bool TR = decltype(trunc_tag)::value;
-#pragma unroll
-            for (int i = 0; i < TM; i++)
-#pragma unroll
-                for (int j = 0; j < TN; j++) {
-                    uint32_t av = 0, rv = 0;
-#pragma unroll
-                    for (int t = 0; t < 4; t++) {
-                        const uint32_t e = tab[scale_fast<TR>(acc[i][j][t], p.sf) + 128];
-                        av |= (e & 0xffu) << (8 * t);
-                        rv |= (e >> 8) << (8 * t);
-                    }
-                    const int o = (pxl + 16 * i) * OW + (cbl + 16 * j) / 4;
-                    Ov[o] = av;
-                    Rv[o] = rv;
-                }
-        };
-        if (p.sf.trunc) pack(std::true_type{});
-        else pack(std::false_type{});
-        __syncthreads();
-        if (!p.pool) {
-            for (int c = tid; c < BM * CT_BN / 16; c += NT) {
-                const int row = c / (CT_BN / 16), q = c % (CT_BN / 16);
-                const int64_t m = m0 + row;
-                if (m >= M || n0 + 16 * q >= p.no) continue;
-                const int64_t o = m * p.no + n0 + 16 * q;
-                const v4i av = *(const v4i *)(Ov + row * OW + 4 * q);
-                *(v4i *)(p.out + o) = av;
-                *(v4i *)(p.code + o) = *(const v4i *)(Rv + row * OW + 4 * q);
-                if (p.xr) {
-                    // padded position of pixel m: (n (H+1) + h)(W+1) + w = (R + R / H)(W+1) + w,
-                    // R = m / W its row over all images
-                    const uint32_t R = udiv32((uint32_t)m, p.d_w), ww = (uint32_t)m - R * (uint32_t)p.w;
-                    const int64_t k = (int64_t)(R + udiv32(R, p.d_h)) * (p.w + 1) + ww;
-                    *(v4i *)(p.xr + ((int64_t)((n0 >> 4) + q) * p.xs + DWP_HMAX + k) * 16) = av;
-                }
-            }
-        } else {
-            // 2x2 windows, 4 channels per thread: the tile holds rt (even) whole image rows; the
-            // first maximum in (0,0), (0,1), (1,0), (1,1) order wins
-            const int W = p.w, Wh = p.w / 2;
-            for (int c = tid; c < (BM / 4) * (CT_BN / 4); c += NT) {
-                const int win = c / (CT_BN / 4), cw = c % (CT_BN / 4);
-                const int wr = win / Wh, wc = win - wr * Wh;
-                const int q = 2 * wr * W + 2 * wc;
-                const int64_t m = m0 + q;
-                if (m >= M || n0 + 4 * cw >= p.no) continue;
-                uint32_t va[4], ra[4];
-#pragma unroll
-                for (int t = 0; t < 4; t++) {
-                    const int at = q + (t >> 1) * W + (t & 1);
-                    va[t] = Ov[at * OW + cw];
-                    ra[t] = Rv[at * OW + cw];
-                }
-                uint32_t ov = 0, cv = 0;
-#pragma unroll
-                for (int e = 0; e < 4; e++) {
-                    int best = (int)(int8_t)(va[0] >> (8 * e));
-                    uint32_t code = (ra[0] >> (8 * e)) & 0xffu;
-                    code <<= 2;
-#pragma unroll
-                    for (int t = 1; t < 4; t++) {
-                        const int v = (int)(int8_t)(va[t] >> (8 * e));
-                        if (v > best) {
-                            best = v;
-                            code = (((ra[t] >> (8 * e)) & 0xffu) << 2) | (uint32_t)t;
-                        }
-                    }
-                    ov |= (uint32_t)(uint8_t)(int8_t)best << (8 * e);
-                    cv |= code << (8 * e);
-                }
-                const int64_t grow = m / W;
-                const int64_t pp = (grow / 2) * Wh + (m % W) / 2;
-                const int64_t o = pp * p.no + n0 + 4 * cw;
-                *(uint32_t *)(p.out + o) = ov;
-                *(uint32_t *)(p.code + o) = cv;
-            }
-        }
-    } else if (p.out64) {
-        // raw int64 input gradient (the first layer of a network): 4 channels per lane and tile
+    if (S::NBUF == 2) stage_store(0);
+    for (;;) {
+        const int vn = v + (int)gridDim.x;
+        const bool more = PERSIST && vn < ntiles;
+        const int64_t em0 = m0;                   // this tile's, for the epilogue
+        const int en0 = n0;
 #pragma unroll
         for (int i = 0; i < TM; i++)
 #pragma unroll
             for (int j = 0; j < TN; j++) {
-                const int64_t m = m0 + pxl + 16 * i;
-                const int col = n0 + cbl + 16 * j;
-                if (m >= M || col >= p.no) continue;
-                int64_t *dst = p.out64 + m * p.no + col;
+                acc[i][j] = v4i{0, 0, 0, 0};
 #pragma unroll
-                for (int t = 0; t < 4; t++) dst[t] = npass > 1 ? acc64[i][j][t] : (int64_t)acc[i][j][t];
+                for (int t = 0; t < 4; t++) acc64[i][j][t] = 0;
             }
-    } else {
-        // int32 sums, ReLU' of the previous layer with its 4 region codes, one 16-byte store per
-        // lane and tile
-        bool bad = false;
-        if (npass > 1) {
+        if (S::NBUF == 1) {
+            for (int ph = 0; ph < nph; ph++) {
+                __syncthreads();                  // every wave is done with the previous stage
+                stage_store(0);
+                __syncthreads();
+                if (ph + 1 < nph) stage_load(ph + 1);
+                compute(smem);
+                fold(ph);
+            }
+        } else {
+            // stage ph & 1 is complete after the barrier of iteration ph; the other stage was last
+            // read in iteration ph - 1, before that barrier, so it can take phase ph + 1's operands
+            for (int ph = 0; ph < nph; ph++) {
+                __syncthreads();
+                if (ph + 1 < nph) stage_load(ph + 1);
+                compute(smem + (ph & 1) * SAB);
+                fold(ph);
+                if (ph + 1 < nph) stage_store((ph + 1) & 1);
+            }
+        }
+        if (more) {
+            set_tile(vn);
+            stage_load(0);
+        }
+        __syncthreads();                          // the epilogue reuses the stages' LDS
+        // ------------------------------------------------------------ epilogues
+        // The MFMAs took B as the first operand: lane l of tile (i, j) holds output channels
+        // cb = wn 32 + 16 j + 4 g4 .. cb + 3 of pixel wm 64 + 16 i + l % 16. The thread index is
+        // taken through an opaque copy so that the epilogue's address terms are recomputed per
+        // tile rather than held in registers across the tile loop.
+        int etid = tid;
+        asm volatile("" : "+v"(etid));
+        const int pxl = (etid >> 7) * 64 + (etid & 15);
+        const int cbl = ((etid >> 6) & 1) * 32 + 4 * ((etid >> 4) & 3);
+        if (MODE == IG_FWD) {
+            // NITRO-Scaling (shift, clamp, one multiply-high) and the table's NITRO-ReLU per
+            // element; four channels packed per dword into LDS, then 16-byte (or pooled) stores.
+            // Several limb passes: the int64 sum saturated to int32 still saturates z*
+            // (128 SF < 2^31).
+            if (npass > 1) {
 #pragma unroll
-            for (int i = 0; i < TM; i++)
+                for (int i = 0; i < TM; i++)
 #pragma unroll
-                for (int j = 0; j < TN; j++)
+                    for (int j = 0; j < TN; j++)
+#pragma unroll
+                        for (int t = 0; t < 4; t++) acc[i][j][t] = sat_i32(acc64[i][j][t]);
+            }
+            constexpr int OW = OS / 4;                // row stride in dwords
+            uint32_t *Ov = (uint32_t *)smem;          // [BM][OW] packed activations
+            uint32_t *Rv = Ov + BM * OW;              // [BM][OW] packed region codes
+            auto pack = [&](auto trunc_tag) {
+                constexpr bool TR = decltype(trunc_tag)::value;
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int j = 0; j < TN; j++) {
+                        uint32_t av = 0, rv = 0;
+#pragma unroll
+                        for (int t = 0; t < 4; t++) {
+                            const uint32_t e = tab[scale_fast<TR>(acc[i][j][t], p.sf) + 128];
+                            av |= (e & 0xffu) << (8 * t);
+                            rv |= (e >> 8) << (8 * t);
+                        }
+                        const int o = (pxl + 16 * i) * OW + (cbl + 16 * j) / 4;
+                        Ov[o] = av;
+                        Rv[o] = rv;
+                    }
+            };
+            if (p.sf.trunc) pack(std::true_type{});
+            else pack(std::false_type{});
+            __syncthreads();
+            if (!p.pool) {
+                for (int c = etid; c < BM * CT_BN / 16; c += NT) {
+                    const int row = c / (CT_BN / 16), q = c % (CT_BN / 16);
+                    const int64_t m = em0 + row;
+                    if (m >= M || en0 + 16 * q >= p.no) continue;
+                    const int64_t o = m * p.no + en0 + 16 * q;
+                    const v4i av = *(const v4i *)(Ov + row * OW + 4 * q);
+                    *(v4i *)(p.out + o) = av;
+                    *(v4i *)(p.code + o) = *(const v4i *)(Rv + row * OW + 4 * q);
+                    if (p.xr) {
+                        // padded position of pixel m: (n (H+1) + h)(W+1) + w
+                        // = (R + R / H)(W+1) + w, R = m / W its row over all images
+                        const uint32_t R = udiv32((uint32_t)m, p.d_w);
+                        const uint32_t ww = (uint32_t)m - R * (uint32_t)p.w;
+                        const int64_t k = (int64_t)(R + udiv32(R, p.d_h)) * (p.w + 1) + ww;
+                        const int64_t row16 = (int64_t)((en0 >> 4) + q) * p.xs + DWP_HMAX + k;
+                        *(v4i *)(p.xr + row16 * 16) = av;
+                    }
+                }
+            } else {
+                // 2x2 windows, 4 channels per thread: the tile holds rt (even) whole image rows;
+                // the first maximum in (0,0), (0,1), (1,0), (1,1) order wins
+                const int W = p.w, Wh = p.w / 2;
+                for (int c = etid; c < (BM / 4) * (CT_BN / 4); c += NT) {
+                    const int win = c / (CT_BN / 4), cw = c % (CT_BN / 4);
+                    const int wr = win / Wh, wc = win - wr * Wh;
+                    const int q = 2 * wr * W + 2 * wc;
+                    const int64_t m = em0 + q;
+                    if (m >= M || en0 + 4 * cw >= p.no) continue;
+                    uint32_t va[4], ra[4];
 #pragma unroll
                     for (int t = 0; t < 4; t++) {
-                        bad |= !fits_i32(acc64[i][j][t]);
-                        acc[i][j][t] = (int32_t)acc64[i][j][t];
+                        const int at = q + (t >> 1) * W + (t & 1);
+                        va[t] = Ov[at * OW + cw];
+                        ra[t] = Rv[at * OW + cw];
                     }
-        }
-        uint32_t mx = 0;
-        auto emit = [&](auto trunc_tag) {
-            constexpr bool TR = decltype(trunc_tag)::value;
+                    uint32_t ov = 0, cv = 0;
+#pragma unroll
+                    for (int e = 0; e < 4; e++) {
+                        int best = (int)(int8_t)(va[0] >> (8 * e));
+                        uint32_t code = (ra[0] >> (8 * e)) & 0xffu;
+                        code <<= 2;
+#pragma unroll
+                        for (int t = 1; t < 4; t++) {
+                            const int v = (int)(int8_t)(va[t] >> (8 * e));
+                            if (v > best) {
+                                best = v;
+                                code = (((ra[t] >> (8 * e)) & 0xffu) << 2) | (uint32_t)t;
+                            }
+                        }
+                        ov |= (uint32_t)(uint8_t)(int8_t)best << (8 * e);
+                        cv |= code << (8 * e);
+                    }
+                    const int64_t grow = m / W;
+                    const int64_t pp = (grow / 2) * Wh + (m % W) / 2;
+                    const int64_t o = pp * p.no + en0 + 4 * cw;
+                    *(uint32_t *)(p.out + o) = ov;
+                    *(uint32_t *)(p.code + o) = cv;
+                }
+            }
+        } else if (p.out64) {
+            // raw int64 input gradient (the first layer of a network): 4 channels per lane and tile
 #pragma unroll
             for (int i = 0; i < TM; i++)
 #pragma unroll
                 for (int j = 0; j < TN; j++) {
-                    const int64_t m = m0 + pxl + 16 * i;
-                    const int col = n0 + cbl + 16 * j;
+                    const int64_t m = em0 + pxl + 16 * i;
+                    const int col = en0 + cbl + 16 * j;
                     if (m >= M || col >= p.no) continue;
-                    const int64_t o = m * p.no + col;
-                    v4i g = acc[i][j];
-                    if (p.prev_code) {
-                        const uint32_t cd = *(const uint32_t *)(p.prev_code + o);
+                    int64_t *dst = p.out64 + m * p.no + col;
 #pragma unroll
-                        for (int t = 0; t < 4; t++) g[t] = relu_bwd32<TR>(g[t], (cd >> (8 * t)) & 0xffu, p.rp);
-                    }
-#pragma unroll
-                    for (int t = 0; t < 4; t++) {
-                        const uint32_t ag = abs_u32(g[t]);
-                        mx = ag > mx ? ag : mx;
-                    }
-                    *(v4i *)(p.gout + o) = g;
+                    for (int t = 0; t < 4; t++)
+                        dst[t] = npass > 1 ? acc64[i][j][t] : (int64_t)acc[i][j][t];
                 }
-        };
-        if (p.rp.alpha.trunc) emit(std::true_type{});
-        else emit(std::false_type{});
+        } else {
+            // int32 sums, ReLU' of the previous layer with its 4 region codes, one 16-byte store
+            // per lane and tile
+            if (npass > 1) {
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int j = 0; j < TN; j++)
+#pragma unroll
+                        for (int t = 0; t < 4; t++) {
+                            bad |= !fits_i32(acc64[i][j][t]);
+                            acc[i][j][t] = (int32_t)acc64[i][j][t];
+                        }
+            }
+            auto emit = [&](auto trunc_tag) {
+                constexpr bool TR = decltype(trunc_tag)::value;
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int j = 0; j < TN; j++) {
+                        const int64_t m = em0 + pxl + 16 * i;
+                        const int col = en0 + cbl + 16 * j;
+                        if (m >= M || col >= p.no) continue;
+                        const int64_t o = m * p.no + col;
+                        v4i g = acc[i][j];
+                        if (p.prev_code) {
+                            const uint32_t cd = *(const uint32_t *)(p.prev_code + o);
+#pragma unroll
+                            for (int t = 0; t < 4; t++)
+                                g[t] = relu_bwd32<TR>(g[t], (cd >> (8 * t)) & 0xffu, p.rp);
+                        }
+#pragma unroll
+                        for (int t = 0; t < 4; t++) {
+                            const uint32_t ag = abs_u32(g[t]);
+                            mx = ag > mx ? ag : mx;
+                        }
+                        *(v4i *)(p.gout + o) = g;
+                    }
+            };
+            if (p.rp.alpha.trunc) emit(std::true_type{});
+            else emit(std::false_type{});
+        }
+        if (!more) break;
+        v = vn;
+        __syncthreads();                          // the epilogue is done with the LDS
+        stage_store(0);
+    }
+    if (MODE == IG_DX && !p.out64) {
         if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
         if (p.gmax) block_slot_max(p.gmax, mx);
     }
@@ -514,8 +548,40 @@ static bool use_wide_tile(int pref, int n, int h, int w, int no, bool pool)
     return tiles >= 128;
 }
 
+// Compute units of the current device (cached per device).
+static int device_cu_count()
+{
+    static int cached[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (!cached[dev]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+            n = 256;
+        cached[dev] = n;
+    }
+    return cached[dev];
+}
+
+// Launches of at least this many tiles per CU take the persistent 256-pixel kernel (forced
+// persistent launches: about this many tiles per workgroup).
+constexpr int CT_PERSIST_TILES_PER_CU = 4;
+
+template <int MODE, int WM, bool PERSIST>
+static void launch_tile_cc(hipStream_t s, const TileArgs &a, dim3 grid)
+{
+    const dim3 block(CtShape<WM>::NT);
+    switch (a.ck == 16 ? 16 : a.ck == 32 ? 32 : 64) {
+    case 16: hipLaunchKernelGGL((k_conv_tile<MODE, 16, WM, PERSIST>), grid, block, 0, s, a); break;
+    case 32: hipLaunchKernelGGL((k_conv_tile<MODE, 32, WM, PERSIST>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((k_conv_tile<MODE, 64, WM, PERSIST>), grid, block, 0, s, a); break;
+    }
+}
+
+// One workgroup per tile, or (256-pixel tiles, many of them) one persistent workgroup per CU:
+// its two LDS stages take the whole LDS.
 template <int MODE, int WM>
-static void launch_tile(hipStream_t s, TileArgs a)
+static void launch_tile(hipStream_t s, int persist, TileArgs a)
 {
     tile_geom<WM>(a.h, a.w, &a.rt, &a.ns, &a.rs);
     a.d_w2 = make_div32((uint32_t)(a.w + 2));
@@ -523,17 +589,20 @@ static void launch_tile(hipStream_t s, TileArgs a)
     a.d_w = make_div32((uint32_t)a.w);
     a.d_rw = make_div32((uint32_t)(a.rs * a.w));
     a.d_h = make_div32((uint32_t)a.h);
-    const dim3 grid((unsigned)(((a.n * a.h + a.rt - 1) / a.rt) * ((a.no + CT_BN - 1) / CT_BN)));
-    const dim3 block(CtShape<WM>::NT);
+    a.ntiles = ((a.n * a.h + a.rt - 1) / a.rt) * ((a.no + CT_BN - 1) / CT_BN);
     a.ts = timer_slot(MODE == IG_FWD ? TIMED_CONV_FWD : TIMED_CONV_DX);
-    switch (a.ck == 16 ? 16 : a.ck == 32 ? 32 : 64) {
-    case 16: hipLaunchKernelGGL((k_conv_tile<MODE, 16, WM>), grid, block, 0, s, a); break;
-    case 32: hipLaunchKernelGGL((k_conv_tile<MODE, 32, WM>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((k_conv_tile<MODE, 64, WM>), grid, block, 0, s, a); break;
+    const int cus = device_cu_count();
+    const bool big = a.ntiles >= CT_PERSIST_TILES_PER_CU * cus;
+    if (WM == 4 && (persist > 0 || (persist == 0 && big))) {
+        int g = (a.ntiles + CT_PERSIST_TILES_PER_CU - 1) / CT_PERSIST_TILES_PER_CU;
+        if (g > cus) g = cus;
+        launch_tile_cc<MODE, WM, WM == 4>(s, a, dim3((unsigned)g));
+    } else {
+        launch_tile_cc<MODE, WM, false>(s, a, dim3((unsigned)a.ntiles));
     }
 }
 
-void launch_conv_fwd_tile(hipStream_t s, int tile, const ConvShape &sh, const int8_t *x, const int8_t *wf,
+void launch_conv_fwd_tile(hipStream_t s, int tile, int persist, const ConvShape &sh, const int8_t *x, const int8_t *wf,
                           const uint32_t *wmax, int64_t sf, int alpha_inv, int round,
                           const Relu &rp, bool pool, int8_t *out, uint8_t *code, uint32_t *flags,
                           int8_t *xr, int64_t xs)
@@ -548,11 +617,11 @@ void launch_conv_fwd_tile(hipStream_t s, int tile, const ConvShape &sh, const in
     a.out = out; a.code = code;
     a.xr = pool ? nullptr : xr; a.xs = xs;
     a.flags = flags;
-    if (use_wide_tile(tile, sh.n, sh.h, sh.w, sh.co, pool)) launch_tile<IG_FWD, 4>(s, a);
-    else launch_tile<IG_FWD, 2>(s, a);
+    if (use_wide_tile(tile, sh.n, sh.h, sh.w, sh.co, pool)) launch_tile<IG_FWD, 4>(s, persist, a);
+    else launch_tile<IG_FWD, 2>(s, persist, a);
 }
 
-void launch_conv_dx_tile(hipStream_t s, int tile, const ConvShape &sh, const int8_t *gl,
+void launch_conv_dx_tile(hipStream_t s, int tile, int persist, const ConvShape &sh, const int8_t *gl,
                          const uint32_t *gmax_in, const int8_t *wt, const uint32_t *wmax,
                          const uint8_t *prev_code, const Relu &rp, int32_t *gout, int64_t *out64,
                          uint32_t *gmax_out, uint32_t *flags)
@@ -565,8 +634,8 @@ void launch_conv_dx_tile(hipStream_t s, int tile, const ConvShape &sh, const int
     a.rp = rp;
     a.prev_code = prev_code; a.gout = gout; a.out64 = out64; a.gmax = gmax_out;
     a.flags = flags;
-    if (use_wide_tile(tile, sh.n, sh.h, sh.w, sh.c, false)) launch_tile<IG_DX, 4>(s, a);
-    else launch_tile<IG_DX, 2>(s, a);
+    if (use_wide_tile(tile, sh.n, sh.h, sh.w, sh.c, false)) launch_tile<IG_DX, 4>(s, persist, a);
+    else launch_tile<IG_DX, 2>(s, persist, a);
 }
 
 }  // namespace nitro

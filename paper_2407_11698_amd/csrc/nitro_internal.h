@@ -544,14 +544,16 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
 // ---- implicit-GEMM conv with the input tile staged once (conv_tile.hip)
 bool tile_conv_fwd_ok(const ConvShape &sh, bool pool, int64_t sf, int alpha_inv);
 bool tile_conv_dx_ok(const ConvShape &sh);
-// tile: 0 by shape, 128 or 256 pixels forced where that tile fits (nitro_set_conv_tile); xr
-// (not pooled): also write the output into the next layer's weight-gradient x rows
-void launch_conv_fwd_tile(hipStream_t s, int tile, const ConvShape &sh, const int8_t *x, const int8_t *wf,
+// tile: 0 by shape, 128 or 256 pixels forced where that tile fits (nitro_set_conv_tile);
+// persist: persistent 256-pixel workgroups by size (0), always (1), never (-1)
+// (nitro_set_conv_persistent); xr (not pooled): also write the output into the next layer's
+// weight-gradient x rows
+void launch_conv_fwd_tile(hipStream_t s, int tile, int persist, const ConvShape &sh, const int8_t *x, const int8_t *wf,
                           const uint32_t *wmax, int64_t sf, int alpha_inv, int round,
                           const Relu &rp, bool pool, int8_t *out, uint8_t *code, uint32_t *flags,
                           int8_t *xr = nullptr, int64_t xs = 0);
 // gl: g's NHWC limb planes [LA][P][co] (max|g| in gmax_in); otherwise as launch_conv_dx_mfma
-void launch_conv_dx_tile(hipStream_t s, int tile, const ConvShape &sh, const int8_t *gl,
+void launch_conv_dx_tile(hipStream_t s, int tile, int persist, const ConvShape &sh, const int8_t *gl,
                          const uint32_t *gmax_in, const int8_t *wt, const uint32_t *wmax,
                          const uint8_t *prev_code, const Relu &rp, int32_t *gout, int64_t *out64,
                          uint32_t *gmax_out, uint32_t *flags);

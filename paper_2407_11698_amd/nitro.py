@@ -85,6 +85,7 @@ def _load():
         "nitro_destroy": (None, [VP]),
         "nitro_set_stream": (I32, [VP, VP]),
         "nitro_set_conv_tile": (I32, [VP, I32]),
+        "nitro_set_conv_persistent": (I32, [VP, I32]),
         "nitro_set_aux_streams": (I32, [VP, I32]),
         "nitro_sync_status": (I32, [VP]),
         "nitro_status_str": (ctypes.c_char_p, [I32]),
@@ -115,7 +116,7 @@ LIB = _load()
 
 # every symbol the header declares (checked by the ABI tests)
 EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_set_conv_tile",
-           "nitro_set_aux_streams",
+           "nitro_set_conv_persistent", "nitro_set_aux_streams",
            "nitro_sync_status",
            "nitro_status_str", "nitro_block_query", "nitro_block_saved", "nitro_block_forward",
            "nitro_block_backward",
@@ -230,6 +231,9 @@ class Context:
 
     def set_conv_tile(self, pixels: int) -> None:
         check(LIB.nitro_set_conv_tile(self.h, pixels), "nitro_set_conv_tile")
+
+    def set_conv_persistent(self, mode: int) -> None:
+        check(LIB.nitro_set_conv_persistent(self.h, mode), "nitro_set_conv_persistent")
 
     def set_aux_streams(self, n: int) -> None:
         check(LIB.nitro_set_aux_streams(self.h, n), "nitro_set_aux_streams")

@@ -157,6 +157,31 @@ def test_conv_block_tile(ctx, tile, case, modes):
         ctx.set_conv_tile(0)
 
 
+# persistent 256-pixel workgroups (about 4 tiles each): 1 workgroup on 2 to 4 tiles, 3 on 10
+# (ragged), 2 on 8 (the XCD-ordered tile map), with and without pooling and weight limbs
+PERSIST_CASES = [
+    (3, 16, 16, [32, 64, 64], True, 10, 10, 300),
+    (5, 16, 16, [64, 128, 128], True, 100, 16, 6000),
+    (8, 16, 16, [32, 64, 64], False, 0, 10, 127),
+    (1, 32, 32, [3, 64, 64], True, 100, 10, 44),
+]
+
+
+@pytest.mark.parametrize("case", PERSIST_CASES)
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_conv_block_persistent(ctx, case, modes):
+    """The same block results with persistent conv workgroups (nitro_set_conv_persistent)."""
+    n, h, w, chans, pool, G, alpha, wmax = case
+    rng = np.random.default_rng(hash((n, h, w, tuple(chans), G, 9001)) % (1 << 31))
+    ctx.set_conv_tile(256)
+    ctx.set_conv_persistent(1)
+    try:
+        run_block(ctx, rng, n, h, w, chans, pool, G, alpha, modes[0], modes[1], wmax=wmax)
+    finally:
+        ctx.set_conv_tile(0)
+        ctx.set_conv_persistent(0)
+
+
 @pytest.mark.parametrize("chans,G,wmax", [([784, 100], 10, 7), ([100, 50, 30], 10, 300),
                                           ([37, 5], 3, 20000), ([64, 65], 0, 127)])
 @pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
