@@ -49,6 +49,13 @@ struct CtCfg {
 
 __host__ __device__ constexpr int ct_bswz(int cc, int c) { return cc == 64 ? (c >> 1) & 3 : 0; }
 
+// A straight into LDS (64-channel chunks, W a multiple of 16, two stages): staged rows of apitch
+// pixels (W + 2 used); LDS unit 64 b + 16 e + r holds 16-channel group e of staged pixel 16 b + r,
+// so that the load is lane-linear and a fragment read (16 consecutive pixels, one group) touches
+// 16 different unit positions modulo 16, whatever its first pixel.
+constexpr int CT_NPMAX_DIRECT = 576;           // staged pixels
+__device__ __attribute__((aligned(16))) const int8_t ct_zero16[16] = {};   // source of zero units
+
 struct TileArgs {
     int n, h, w;
     int ck;                        // channels of A; K = 9 ck (a multiple of the chunk size CC)
@@ -61,6 +68,8 @@ struct TileArgs {
     int64_t bplane;                // no * 9 ck
     const uint32_t *b_max;
     int rt, ns, rs;                // image rows per tile; images per tile; rows per image segment
+    int apitch;                    // A loaded straight into LDS: staged row pitch (a multiple of 16)
+    Div32 d_apitch, d_aseg;        // its reciprocals of apitch and (rs + 2) apitch
     Div32 d_w2, d_seg, d_w, d_rw;  // reciprocals of W + 2, (rs + 2)(W + 2), W and rs W
     // forward epilogue
     ScaleFast sf;
@@ -89,23 +98,30 @@ __device__ inline int32_t sat_i32(int64_t v)
 // channels) stages the A pixels and the B block of 9 taps x 64 columns x CC. The next phase's
 // global loads are issued before the current phase computes; the fragments of the next K-step
 // are read from LDS while the MFMAs of the current one run.
-template <int MODE, int CC, int WM, bool PERSIST>
+template <int MODE, int CC, int WM, bool PERSIST, bool ADMA>
 __global__ __launch_bounds__(128 * WM) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_conv_tile(TileArgs p)
 {
     using S = CtShape<WM>;
     using C = CtCfg<CC, WM>;
+    static_assert(!ADMA || (CC == 64 && S::NBUF == 2), "A straight into LDS: 64 channels, two stages");
     constexpr int BM = S::BM, NT = S::NT;
     constexpr int TM = 4, TN = 2;                 // 16x16 tiles per wave: 64 pixels x 32 columns
     constexpr int NU = CC / 16;                   // 16-byte units per (tap, column) row of B
-    constexpr int SA = S::NPMAX * C::PS;          // A stage bytes
+    constexpr int SA = ADMA ? CT_NPMAX_DIRECT * 64 : S::NPMAX * C::PS;   // A stage bytes
+    constexpr int NIA = ADMA ? (CT_NPMAX_DIRECT * 4 + NT - 1) / NT : C::NIT;   // A items per thread
     constexpr int BITEMS = 9 * CT_BN * NU;        // 16-byte units of a B stage
     constexpr int BIT = (BITEMS + NT - 1) / NT;   // B units per thread
     constexpr int SAB = SA + BITEMS * 16;         // one stage
     constexpr int OS = CT_BN + 16;                // forward epilogue: LDS row stride in bytes
     constexpr int SMEM_EPI = MODE == IG_FWD ? 2 * BM * OS : 0;
-    constexpr int SMEM_MAIN = S::NBUF * SAB > SMEM_EPI ? S::NBUF * SAB : SMEM_EPI;
-    constexpr int SMEM = SMEM_MAIN + (MODE == IG_FWD ? 528 : 0);   // + the NITRO-ReLU table
+    // the forward epilogue's LDS: one stage; two stages: the one the last phase computed from
+    // (the other holds the next tile's first phase), or after both where it does not fit one
+    constexpr bool EPI_IN_STAGE = S::NBUF == 1 || SMEM_EPI <= SAB;
+    constexpr int SMEM_MAIN = S::NBUF == 1 ? (SAB > SMEM_EPI ? SAB : SMEM_EPI)
+                                           : 2 * SAB + (EPI_IN_STAGE ? 0 : SMEM_EPI);
+    constexpr int SMEM_SINK = SMEM_MAIN + (MODE == IG_FWD ? 528 : 0);   // after the NITRO-ReLU table
+    constexpr int SMEM = SMEM_SINK + 1024;        // + a sink for staging lanes with nothing to store
     __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
 
     ts_start(p.ts);
@@ -119,7 +135,8 @@ void k_conv_tile(TileArgs p)
     const int ntiles = p.ntiles;
     const int W2 = p.w + 2;
     const int segpx = (p.rs + 2) * W2;
-    const int np = p.ns * segpx;
+    const int aseg = (p.rs + 2) * p.apitch;       // A straight into LDS: staged pixels per segment
+    const int np = ADMA ? p.ns * aseg : p.ns * segpx;
     const int64_t M = (int64_t)p.n * p.h * p.w;
     const int K = 9 * p.ck;
     const int nchunk = p.ck / CC;
@@ -151,7 +168,7 @@ void k_conv_tile(TileArgs p)
     // one pixel tile run together and share their A rows in that XCD's L2.
     int64_t m0;
     int n0, b_g0;
-    int it_g[C::NIT];
+    int it_g[NIA];
     auto set_tile = [&](int v) {
         const int tile = (ntiles & 7) == 0 ? (v & 7) * (ntiles >> 3) + (v >> 3) : v;
         const int mt = tile / ntile_n, nt = tile - mt * ntile_n;
@@ -160,27 +177,58 @@ void k_conv_tile(TileArgs p)
         m0 = (int64_t)R0 * p.w;
         n0 = nt * CT_BN;
 #pragma unroll
-        for (int u = 0; u < C::NIT; u++) {
+        for (int u = 0; u < NIA; u++) {
             int q, e;
-            a_item(tid + NT * u, q, e);
+            if (ADMA) {
+                const int unit = tid + NT * u;
+                q = 16 * (unit >> 6) + (unit & 15);
+                e = (unit >> 4) & 3;
+            } else {
+                a_item(tid + NT * u, q, e);
+            }
             it_g[u] = -1;
             if (q < np) {
-                const int seg = (int)udiv32(q, p.d_seg), r = q - seg * segpx;
-                const int lr = (int)udiv32(r, p.d_w2), lc = r - lr * W2;
+                int seg, lr, lc;
+                if (ADMA) {
+                    seg = (int)udiv32(q, p.d_aseg);
+                    const int r = q - seg * aseg;
+                    lr = (int)udiv32(r, p.d_apitch);
+                    lc = r - lr * p.apitch;
+                } else {
+                    seg = (int)udiv32(q, p.d_seg);
+                    const int r = q - seg * segpx;
+                    lr = (int)udiv32(r, p.d_w2);
+                    lc = r - lr * W2;
+                }
                 const int img = img0 + seg, hh = row0 + lr - 1, ww = lc - 1;
                 if (img < p.n && hh >= 0 && hh < p.h && ww >= 0 && ww < p.w)
                     it_g[u] = ((img * p.h + hh) * p.w + ww) * p.ck + 16 * e;
             }
         }
-        b_g0 = (n0 + b_c < p.no ? n0 + b_c : p.no - 1) * K + b_t0 * p.ck + 16 * b_u;
+        // A and B straight into LDS: lane-linear, so B's unit swizzle is applied to the source;
+        // otherwise through registers, swizzled on the store
+        const int bu = ADMA ? b_u ^ ct_bswz(CC, b_c) : b_u;
+        b_g0 = (n0 + b_c < p.no ? n0 + b_c : p.no - 1) * K + b_t0 * p.ck + 16 * bu;
     };
-    int cpix[TM];
+    // LDS byte offset of this lane's A pixel in fragment i (tap (1, 1)). A straight into LDS:
+    // the fragment's 16 pixels lie in one image row, from a column that is a multiple of 16, so
+    // the offset is that 16-pixel block's plus the lane's channel group; the lane's position in
+    // the block for column offset s - 1 (s = 0, 1, 2) is in alast[s].
+    int cpix[TM], alast[3];
 #pragma unroll
     for (int i = 0; i < TM; i++) {
-        const int mloc = wm * 64 + 16 * i + (lane & 15);
+        const int mloc = wm * 64 + 16 * i + (ADMA ? 0 : (lane & 15));
         const int seg = (int)udiv32(mloc, p.d_rw), rem = mloc - seg * p.rs * p.w;
         const int row = (int)udiv32(rem, p.d_w), col = rem - row * p.w;
-        cpix[i] = (seg * segpx + (row + 1) * W2 + col + 1) * C::PS;
+        if (ADMA)
+            cpix[i] = (seg * aseg + (row + 1) * p.apitch + col) * 64 + 256 * g4;
+        else
+            cpix[i] = (seg * segpx + (row + 1) * W2 + col + 1) * C::PS;
+    }
+#pragma unroll
+    for (int t = 0; t < 3; t++) {
+        const int l = (lane & 15) + t;
+        alast[t] = (l >> 4) * 1024 + (l & 15) * 16;
     }
     // LDS byte offset of this lane's B unit in each column tile (tap 0): column c, unit c16 of
     // the lane's group (fixed per lane: 4 ks + g4 = g4 modulo GPT)
@@ -193,29 +241,64 @@ void k_conv_tile(TileArgs p)
     }
     const int sgn = MODE == IG_FWD ? 1 : -1;
 
-    v4i stga[C::NIT], stgb[BIT];
-    auto stage_load = [&](int ph) {
+    // operands of phase ph: limb pair (la, lb) and the chunk of CC channels
+    auto src_a = [&](int ph) {
         const int chunk = ph % nchunk, pass = ph / nchunk;
-        const int la = pass / LB, lb = pass - la * LB;
-        const int8_t *srca = p.a + (int64_t)la * p.aplane + chunk * CC;
+        return p.a + (int64_t)(pass / LB) * p.aplane + chunk * CC;
+    };
+    auto src_b = [&](int ph) {
+        const int chunk = ph % nchunk, pass = ph / nchunk;
+        return p.b + (int64_t)(pass % LB) * p.bplane + chunk * CC + b_g0;
+    };
+    v4i stga[NIA], stgb[BIT];
+    auto a_load = [&](const int8_t *srca, int v) {
+        stga[v] = *(const v4i *)(srca + (it_g[v] >= 0 ? it_g[v] : 0));
+    };
+    // (branch-free: a lane whose item lies past the staged pixels stores into the sink)
+    auto a_store = [&](int buf, int v) {
+        int q, e;
+        a_item(tid + NT * v, q, e);
+        const int off = q < np ? buf * SAB + q * C::PS + 16 * e : SMEM_SINK + 16 * lane;
+        *(v4i *)(smem + off) = it_g[v] >= 0 ? stga[v] : v4i{0, 0, 0, 0};
+    };
+    // B unit tid + NT v straight into LDS byte 16 (tid + NT v) (A straight into LDS): a wave's
+    // 64 units are contiguous (its tap, b_t0 + v TPV, is the same on every lane); a wave past the
+    // ninth tap has nothing to load
+    typedef __attribute__((address_space(3))) void *LdsPtr;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int b_t0u = __builtin_amdgcn_readfirstlane(b_t0);
+    auto b_direct = [&](int buf, const int8_t *srcb, int v) {
+        if (b_t0u + v * TPV < 9)
+            __builtin_amdgcn_global_load_lds((const void *)(srcb + v * TPV * p.ck),
+                                             (LdsPtr)(smem + buf * SAB + SA + 16 * (NT * v + 64 * wave_u)),
+                                             16, 0, 0);
+    };
+    // A unit tid + NT v straight into LDS (A straight into LDS): a wave's 64 units are
+    // contiguous and all staged, or (past the staged pixels) none; a zero unit is read from
+    // ct_zero16
+    const int npa4u = __builtin_amdgcn_readfirstlane(4 * np);
+    auto a_direct = [&](int buf, const int8_t *srca, int v) {
+        if (NT * v + 64 * wave_u < npa4u) {
+            const int8_t *src = it_g[v] >= 0 ? srca + it_g[v] : ct_zero16;
+            __builtin_amdgcn_global_load_lds((const void *)src,
+                                             (LdsPtr)(smem + buf * SAB + 16 * (NT * v + 64 * wave_u)), 16, 0, 0);
+        }
+    };
+    // one stage: the whole phase through registers, loaded before the compute, stored after it
+    auto stage_load = [&](int ph) {
+        const int8_t *srca = src_a(ph), *srcb = src_b(ph);
 #pragma unroll
-        for (int v = 0; v < C::NIT; v++) stga[v] = *(const v4i *)(srca + (it_g[v] >= 0 ? it_g[v] : 0));
-        const int8_t *srcb = p.b + (int64_t)lb * p.bplane + chunk * CC + b_g0;
+        for (int v = 0; v < NIA; v++) a_load(srca, v);
 #pragma unroll
         for (int v = 0; v < BIT; v++)
             if (b_t0 + v * TPV < 9) stgb[v] = *(const v4i *)(srcb + v * TPV * p.ck);
     };
     auto stage_store = [&](int buf) {
-        uint8_t *As = smem + buf * SAB, *Bs = As + SA;
 #pragma unroll
-        for (int v = 0; v < C::NIT; v++) {
-            int q, e;
-            a_item(tid + NT * v, q, e);
-            if (q < np) *(v4i *)(As + q * C::PS + 16 * e) = it_g[v] >= 0 ? stga[v] : v4i{0, 0, 0, 0};
-        }
+        for (int v = 0; v < NIA; v++) a_store(buf, v);
 #pragma unroll
         for (int v = 0; v < BIT; v++)
-            if (b_t0 + v * TPV < 9) *(v4i *)(Bs + b_l0 + v * NT * 16) = stgb[v];
+            if (b_t0 + v * TPV < 9) *(v4i *)(smem + buf * SAB + SA + b_l0 + v * NT * 16) = stgb[v];
     };
     // fragments of K-step ks: group G = 4 ks + g4 is (tap t, 16-channel group c16); a K-step past
     // the ninth tap (chunks of 16 or 32 channels) has zero A fragments
@@ -225,11 +308,19 @@ void k_conv_tile(TileArgs p)
         const int t = G / C::GPT, c16 = G - t * C::GPT;
         const bool valid = t < 9;
         const int tc = valid ? t : 8;
-        const int toff = sgn * ((tc / 3 - 1) * W2 + (tc % 3 - 1)) * C::PS + 16 * c16;
+        if (ADMA) {
+            // (64 channels: tap ks, group g4 on every lane)
+            const int dr = sgn * (ks / 3 - 1), dc = sgn * (ks % 3 - 1);
+            const int roff = dr * p.apitch * 64;
 #pragma unroll
-        for (int i = 0; i < TM; i++) {
-            const v4i v = *(const v4i *)(As + cpix[i] + toff);
-            af[i] = valid ? v : v4i{0, 0, 0, 0};
+            for (int i = 0; i < TM; i++) af[i] = *(const v4i *)(As + cpix[i] + alast[1 + dc] + roff);
+        } else {
+            const int toff = sgn * ((tc / 3 - 1) * W2 + (tc % 3 - 1)) * C::PS + 16 * c16;
+#pragma unroll
+            for (int i = 0; i < TM; i++) {
+                const v4i v = *(const v4i *)(As + cpix[i] + toff);
+                af[i] = valid ? v : v4i{0, 0, 0, 0};
+            }
         }
 #pragma unroll
         for (int j = 0; j < TN; j++) bf[j] = *(const v4i *)(Bs + tc * CT_BN * CC + bcol[j]);
@@ -238,7 +329,13 @@ void k_conv_tile(TileArgs p)
     int64_t acc64[TM][TN][4];
     v4i acc[TM][TN];
 
-    auto compute = [&](const uint8_t *As) {
+    // A straight into LDS: while a phase computes, the other stage receives the next phase's
+    // operands, their LDS-direct loads spread over all but the last two K-steps so that the
+    // address unit takes them alongside the MFMAs.
+    constexpr int NLD = NIA + BIT;                // loads per thread and phase
+    constexpr int LDK = C::KSC - 2;               // K-steps issuing them
+    auto compute = [&](auto stage_tag, const uint8_t *As, int sbuf, const int8_t *sa, const int8_t *sb) {
+        constexpr bool STG = decltype(stage_tag)::value;
         v4i af[2][TM], bf[2][TN];
         load_frags(As, af[0], bf[0], 0);
         // the next K-step's fragment reads are issued before this K-step's MFMAs, and the
@@ -248,6 +345,14 @@ void k_conv_tile(TileArgs p)
         constexpr bool PIPE = !(WM == 2 && MODE == IG_DX);
 #pragma unroll
         for (int ks = 0; ks < C::KSC; ks++) {
+            if (ADMA && STG) {
+#pragma unroll
+                for (int i = 0; i < NLD; i++)
+                    if (i * LDK / NLD == ks) {
+                        if (i < NIA) a_direct(sbuf, sa, i);
+                        else b_direct(sbuf, sb, i - NIA);
+                    }
+            }
             if (ks + 1 < C::KSC) load_frags(As, af[(ks + 1) & 1], bf[(ks + 1) & 1], ks + 1);
             if (PIPE) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -281,9 +386,18 @@ void k_conv_tile(TileArgs p)
     uint32_t mx = 0;                              // input gradient: max |g| over this workgroup
     bool bad = false;                             // input gradient: a sum outside int32
     int v = blockIdx.x;
+    int gph = 0;                                  // phases computed: stage gph & 1 is current
     set_tile(v);
-    stage_load(0);
-    if (S::NBUF == 2) stage_store(0);
+    if (ADMA) {
+        const int8_t *sa = src_a(0), *sb = src_b(0);
+#pragma unroll
+        for (int u = 0; u < NIA; u++) a_direct(0, sa, u);
+#pragma unroll
+        for (int u = 0; u < BIT; u++) b_direct(0, sb, u);
+    } else {
+        stage_load(0);
+        if (S::NBUF == 2) stage_store(0);
+    }
     for (;;) {
         const int vn = v + (int)gridDim.x;
         const bool more = PERSIST && vn < ntiles;
@@ -303,23 +417,44 @@ void k_conv_tile(TileArgs p)
                 stage_store(0);
                 __syncthreads();
                 if (ph + 1 < nph) stage_load(ph + 1);
-                compute(smem);
+                compute(std::false_type{}, smem, 0, nullptr, nullptr);
                 fold(ph);
+                gph++;
             }
         } else {
-            // stage ph & 1 is complete after the barrier of iteration ph; the other stage was last
-            // read in iteration ph - 1, before that barrier, so it can take phase ph + 1's operands
+            // the barrier publishes stage gph & 1 (staged during the previous phase, of this tile
+            // or the one before) and ends every read of the other stage, which then receives
+            // this tile's next phase or, in its last phase, the next tile's first. A straight
+            // into LDS: during the compute. Otherwise loaded into registers before the compute
+            // and stored after it; the next tile's first phase loaded after the last compute and
+            // stored after the epilogue.
             for (int ph = 0; ph < nph; ph++) {
                 __syncthreads();
-                if (ph + 1 < nph) stage_load(ph + 1);
-                compute(smem + (ph & 1) * SAB);
+                const int cb = gph & 1;
+                if (ADMA) {
+                    const int8_t *sa = nullptr, *sb = nullptr;
+                    if (ph + 1 < nph) {
+                        sa = src_a(ph + 1);
+                        sb = src_b(ph + 1);
+                    } else if (more) {
+                        set_tile(vn);
+                        sa = src_a(0);
+                        sb = src_b(0);
+                    }
+                    if (sa) compute(std::true_type{}, smem + cb * SAB, cb ^ 1, sa, sb);
+                    else compute(std::false_type{}, smem + cb * SAB, 0, nullptr, nullptr);
+                } else {
+                    if (ph + 1 < nph) stage_load(ph + 1);
+                    compute(std::false_type{}, smem + cb * SAB, 0, nullptr, nullptr);
+                }
                 fold(ph);
-                if (ph + 1 < nph) stage_store((ph + 1) & 1);
+                if (!ADMA && ph + 1 < nph) stage_store(cb ^ 1);
+                gph++;
             }
-        }
-        if (more) {
-            set_tile(vn);
-            stage_load(0);
+            if (!ADMA && more) {
+                set_tile(vn);
+                stage_load(0);
+            }
         }
         __syncthreads();                          // the epilogue reuses the stages' LDS
         // ------------------------------------------------------------ epilogues
@@ -345,7 +480,8 @@ void k_conv_tile(TileArgs p)
                         for (int t = 0; t < 4; t++) acc[i][j][t] = sat_i32(acc64[i][j][t]);
             }
             constexpr int OW = OS / 4;                // row stride in dwords
-            uint32_t *Ov = (uint32_t *)smem;          // [BM][OW] packed activations
+            const int epi = !EPI_IN_STAGE ? 2 * SAB : S::NBUF == 2 ? ((gph - 1) & 1) * SAB : 0;
+            uint32_t *Ov = (uint32_t *)(smem + epi);  // [BM][OW] packed activations
             uint32_t *Rv = Ov + BM * OW;              // [BM][OW] packed region codes
             auto pack = [&](auto trunc_tag) {
                 constexpr bool TR = decltype(trunc_tag)::value;
@@ -486,8 +622,8 @@ void k_conv_tile(TileArgs p)
         }
         if (!more) break;
         v = vn;
-        __syncthreads();                          // the epilogue is done with the LDS
-        stage_store(0);
+        // (the epilogue uses the other stage)
+        if (!ADMA && S::NBUF == 2) stage_store(gph & 1);
     }
     if (MODE == IG_DX && !p.out64) {
         if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
@@ -568,13 +704,18 @@ static int device_cu_count()
 constexpr int CT_PERSIST_TILES_PER_CU = 4;
 
 template <int MODE, int WM, bool PERSIST>
-static void launch_tile_cc(hipStream_t s, const TileArgs &a, dim3 grid)
+static void launch_tile_cc(hipStream_t s, const TileArgs &a, dim3 grid, bool adma)
 {
     const dim3 block(CtShape<WM>::NT);
     switch (a.ck == 16 ? 16 : a.ck == 32 ? 32 : 64) {
-    case 16: hipLaunchKernelGGL((k_conv_tile<MODE, 16, WM, PERSIST>), grid, block, 0, s, a); break;
-    case 32: hipLaunchKernelGGL((k_conv_tile<MODE, 32, WM, PERSIST>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((k_conv_tile<MODE, 64, WM, PERSIST>), grid, block, 0, s, a); break;
+    case 16: hipLaunchKernelGGL((k_conv_tile<MODE, 16, WM, PERSIST, false>), grid, block, 0, s, a); break;
+    case 32: hipLaunchKernelGGL((k_conv_tile<MODE, 32, WM, PERSIST, false>), grid, block, 0, s, a); break;
+    default:
+        if (WM == 4 && adma)
+            hipLaunchKernelGGL((k_conv_tile<MODE, 64, WM, PERSIST, WM == 4>), grid, block, 0, s, a);
+        else
+            hipLaunchKernelGGL((k_conv_tile<MODE, 64, WM, PERSIST, false>), grid, block, 0, s, a);
+        break;
     }
 }
 
@@ -591,14 +732,20 @@ static void launch_tile(hipStream_t s, int persist, TileArgs a)
     a.d_h = make_div32((uint32_t)a.h);
     a.ntiles = ((a.n * a.h + a.rt - 1) / a.rt) * ((a.no + CT_BN - 1) / CT_BN);
     a.ts = timer_slot(MODE == IG_FWD ? TIMED_CONV_FWD : TIMED_CONV_DX);
+    // A straight into LDS: 256-pixel tiles, 64-channel chunks, rows of whole 16-pixel blocks
+    a.apitch = (a.w + 2 + 15) / 16 * 16;
+    const bool adma = WM == 4 && a.ck % 64 == 0 && a.w % 16 == 0 &&
+                      a.ns * (a.rs + 2) * a.apitch <= CT_NPMAX_DIRECT;
+    a.d_apitch = make_div32((uint32_t)a.apitch);
+    a.d_aseg = make_div32((uint32_t)((a.rs + 2) * a.apitch));
     const int cus = device_cu_count();
     const bool big = a.ntiles >= CT_PERSIST_TILES_PER_CU * cus;
     if (WM == 4 && (persist > 0 || (persist == 0 && big))) {
         int g = (a.ntiles + CT_PERSIST_TILES_PER_CU - 1) / CT_PERSIST_TILES_PER_CU;
         if (g > cus) g = cus;
-        launch_tile_cc<MODE, WM, WM == 4>(s, a, dim3((unsigned)g));
+        launch_tile_cc<MODE, WM, WM == 4>(s, a, dim3((unsigned)g), adma);
     } else {
-        launch_tile_cc<MODE, WM, false>(s, a, dim3((unsigned)a.ntiles));
+        launch_tile_cc<MODE, WM, false>(s, a, dim3((unsigned)a.ntiles), adma);
     }
 }
 
