@@ -203,6 +203,8 @@ void k_conv_tile(TileArgs p)
                 const int img = img0 + seg, hh = row0 + lr - 1, ww = lc - 1;
                 if (img < p.n && hh >= 0 && hh < p.h && ww >= 0 && ww < p.w)
                     it_g[u] = ((img * p.h + hh) * p.w + ww) * p.ck + 16 * e;
+                else if (ADMA && ww > p.w)
+                    it_g[u] = -2;                  // row padding: never read, not loaded
             }
         }
         // A and B straight into LDS: lane-linear, so B's unit swizzle is applied to the source;
@@ -275,10 +277,10 @@ void k_conv_tile(TileArgs p)
     };
     // A unit tid + NT v straight into LDS (A straight into LDS): a wave's 64 units are
     // contiguous and all staged, or (past the staged pixels) none; a zero unit is read from
-    // ct_zero16
+    // ct_zero16; a lane on row padding loads nothing
     const int npa4u = __builtin_amdgcn_readfirstlane(4 * np);
     auto a_direct = [&](int buf, const int8_t *srca, int v) {
-        if (NT * v + 64 * wave_u < npa4u) {
+        if (NT * v + 64 * wave_u < npa4u && it_g[v] != -2) {
             const int8_t *src = it_g[v] >= 0 ? srca + it_g[v] : ct_zero16;
             __builtin_amdgcn_global_load_lds((const void *)src,
                                              (LdsPtr)(smem + buf * SAB + 16 * (NT * v + 64 * wave_u)), 16, 0, 0);
@@ -330,10 +332,10 @@ void k_conv_tile(TileArgs p)
     v4i acc[TM][TN];
 
     // A straight into LDS: while a phase computes, the other stage receives the next phase's
-    // operands, their LDS-direct loads spread over all but the last two K-steps so that the
-    // address unit takes them alongside the MFMAs.
+    // operands, their LDS-direct loads spread over all but the last K-step so that the address
+    // unit takes them alongside the MFMAs.
     constexpr int NLD = NIA + BIT;                // loads per thread and phase
-    constexpr int LDK = C::KSC - 2;               // K-steps issuing them
+    constexpr int LDK = C::KSC - 1;               // K-steps issuing them
     auto compute = [&](auto stage_tag, const uint8_t *As, int sbuf, const int8_t *sa, const int8_t *sb) {
         constexpr bool STG = decltype(stage_tag)::value;
         v4i af[2][TM], bf[2][TN];
