@@ -338,6 +338,13 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
     if (zero_slots && hipMemsetAsync(slots + 4 * SLOT_WORDS, 0, 6 * SLOT_WORDS * 4, s) != hipSuccess)
         return NITRO_EHIP;
     bool have_g = false;
+    // The last layer's g left pooled by the learning layer and un-pooled by the weight-gradient
+    // planes, which then give every other reader its values: a pooled conv block on the MFMA
+    // learning layer and planes weight gradient, its input gradient (if any) on the tile, and
+    // no tap asking for that g.
+    const bool need_dx_last = J > 1 || (taps && taps->dx);
+    const bool g_pooled = G > 0 && g.lr_mfma && desc->maxpool != 0 && LJ.conv && dwp_ok(LJ.sh) &&
+                          (!need_dx_last || LJ.dx_tile) && !(taps && taps->g[J - 1]);
     if (G > 0) {
         int32_t *yhat = (int32_t *)at(state, g.yhat);
         int32_t *e = (int32_t *)at(state, g.e);
@@ -348,15 +355,15 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
             lb.wt = (int8_t *)at(state, g.lwt);
             lb.ft = (int8_t *)at(state, g.lft);
             lb.part = (int64_t *)at(state, g.lpart);
-            lb.epad = (int32_t *)at(state, g.lepad);
-            lb.et = (int32_t *)at(state, g.let);
+            lb.epad = (int8_t *)at(state, g.lepad);
+            lb.et = (int8_t *)at(state, g.let);
             lb.wmax = slots + (8) * SLOT_WORDS;
             lb.emax = slots + (9) * SLOT_WORDS;
             lb.gmax = slots + (4 + J - 1) * SLOT_WORDS;
             launch_learning_mfma(s, n, g.d, G, a_out, p->w_lr, sf, labels, lb,
                                  at(state, g.code[J - 1]), rp, LJ.sh.h, LJ.sh.w, LJ.sh.co,
                                  desc->maxpool != 0, gb[0], taps ? taps->delta : nullptr, yhat, e,
-                                 gr->dw_lr, ctx->flags, prepacked);
+                                 gr->dw_lr, ctx->flags, prepacked, g_pooled);
             have_g = true;
         } else {
             int32_t *dl = (int32_t *)at(state, g.delta);
@@ -387,7 +394,8 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                                       (int8_t *)at(state, g.gt), (int8_t *)at(state, g.xpl),
                                       L.dx_tile && need_dx ? (int8_t *)at(state, g.gnl) : nullptr,
                                       (int64_t *)at(state, g.part), gr->dw[j], ctx->flags,
-                                      j == J - 1 && rows_from_forward(g));
+                                      j == J - 1 && rows_from_forward(g),
+                                      j == J - 1 && g_pooled ? at(state, g.code[J - 1]) : nullptr);
             else if (mfma_conv_dw_ok(L.sh) || mfma_conv_dw_smallc_ok(L.sh))
                 launch_conv_dw_mfma(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, xin, (int8_t *)at(state, g.gt),
                                     (int64_t *)at(state, g.part), gr->dw[j], ctx->flags);

@@ -161,10 +161,13 @@ __global__ __launch_bounds__(256) void k_dwp_pad_rows(int n, int h, int w, int h
 // g int32 NHWC [P][C] -> gp [l][C][kp] for l < limbs(max|g|): limb l of g at padded position k
 // (zeros at pad positions); when gn is not null also the NHWC limb planes gn [l][P][C] (the A
 // operand of the input-gradient GEMM). A workgroup: 64 positions x 64 channels, transposed
-// through LDS.
+// through LDS. With pcode, g holds a 2x2-pooled layer's gradient at the pooled positions only,
+// [n][h/2][w/2][C]: pixel (y, x) takes it where the pool's argmax (the code's low 2 bits) is
+// window position 2 (y & 1) + (x & 1), and zero elsewhere.
 __global__ __launch_bounds__(256) void k_dwp_grad_planes(const int32_t *__restrict__ g, int n,
                                                          int h, int w, int c, int hp, int wp,
                                                          int kp, const uint32_t *gmax,
+                                                         const uint8_t *__restrict__ pcode,
                                                          int8_t *__restrict__ gp,
                                                          int8_t *__restrict__ gn)
 {
@@ -177,12 +180,27 @@ __global__ __launch_bounds__(256) void k_dwp_grad_planes(const int32_t *__restri
     {
         const int pi = tid >> 2, cq = tid & 3;
         const int pix = padded_pixel(k0 + pi, n, h, w, hp, wp);
+        int src = pix;                   // pixel of g holding this position's value
+        uint32_t win = 0;                // pooled g: this pixel's position in its window
+        if (pcode && pix >= 0) {
+            const int row = pix / w, ww = pix - row * w;   // row over all images
+            const int img = row / h, hh = row - img * h;
+            src = (img * (h >> 1) + (hh >> 1)) * (w >> 1) + (ww >> 1);
+            win = 2u * (hh & 1) + (ww & 1);
+        }
         int32_t v[16];
 #pragma unroll
         for (int u = 0; u < 4; u++) {
             const int ch = c0 + 16 * cq + 4 * u;
             v4i x = v4i{0, 0, 0, 0};
-            if (pix >= 0 && ch < c) x = *(const v4i *)(g + (int64_t)pix * c + ch);
+            if (pix >= 0 && ch < c) {
+                x = *(const v4i *)(g + (int64_t)src * c + ch);
+                if (pcode) {
+                    const uint32_t cd = *(const uint32_t *)(pcode + (int64_t)src * c + ch);
+#pragma unroll
+                    for (int e = 0; e < 4; e++) x[e] = ((cd >> (8 * e)) & 3u) == win ? x[e] : 0;
+                }
+            }
 #pragma unroll
             for (int e = 0; e < 4; e++) {
                 v[4 * u + e] = x[e];
@@ -414,7 +432,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
                            int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags,
-                           bool x_rows_ready)
+                           bool x_rows_ready, const uint8_t *pool_code)
 {
     const DwpGeom ge = dwp_geom(sh);
     const DwpPlan pl = dwp_plan(sh);
@@ -428,8 +446,8 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            dim3(256), 0, s, x, sh.n, sh.h, sh.w, sh.c, ge.hp, ge.wp, (int)ge.xs, xp);
     }
     hipLaunchKernelGGL(k_dwp_grad_planes, dim3((unsigned)(ge.kp / 64), (unsigned)((sh.co + 63) / 64)),
-                       dim3(256), 0, s, g, sh.n, sh.h, sh.w, sh.co, ge.hp, ge.wp, (int)ge.kp, gmax, gp,
-                       gn);
+                       dim3(256), 0, s, g, sh.n, sh.h, sh.w, sh.co, ge.hp, ge.wp, (int)ge.kp, gmax,
+                       pool_code, gp, gn);
     DwpArgs a{};
     a.gp = gp; a.kp = ge.kp;
     a.xr = xp; a.xs = ge.xs;

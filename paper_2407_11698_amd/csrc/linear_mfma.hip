@@ -5,7 +5,8 @@
 //              routing and NITRO-ReLU backward of the block's last layer
 //   gradient   dW[g][k] = sum_n e[n][g] f[n][k]
 // All three are C[m][j] = sum_k A[m][k] B[j][k] with K-contiguous rows: one kernel, three
-// epilogues. Wide operands use balanced int8 limbs as in the convolution kernels.
+// epilogues. Wide operands use balanced int8 limbs as in the convolution kernels: the weights'
+// limb planes are packed before the step, e's written by the kernel that computes e.
 #include <type_traits>
 
 #include "mfma_common.h"
@@ -16,9 +17,9 @@ enum { LIN_PART = 0, LIN_UNPOOL = 1, LIN_DW = 2 };
 
 struct LgemmArgs {
     int M, N, K;                  // K: a multiple of 16 (zero padded rows)
-    const void *a;                // A rows [M][lda]: int8 or int32
-    int64_t lda;
-    const uint32_t *a_max;        // int32 A: max|A|
+    const int8_t *a;              // A rows [M][lda]; limb planes aplane apart when a_max is set
+    int64_t lda, aplane;
+    const uint32_t *a_max;        // limb planes of A: max|A| (null: one int8 plane)
     const int8_t *b;              // B limb planes [4][N][ldb] (one plane when b_max is null)
     int64_t ldb, bplane;
     const uint32_t *b_max;
@@ -31,6 +32,7 @@ struct LgemmArgs {
     const uint8_t *code;
     Relu rp;
     int h, w, c, pool;
+    int gpooled;                  // pooled: g at the pooled positions only (the argmax's value)
     int32_t *g;                   // gradient at the last layer's pre-activation, NHWC
     int32_t *delta;               // optional copy of delta (int32, pooled NHWC)
     uint32_t *gmax;
@@ -39,7 +41,7 @@ struct LgemmArgs {
 
 constexpr int LG_BM = 128, LG_BN = 64, LG_BK = 64, LG_LDS = 80;
 
-template <bool A32, int MODE>
+template <int MODE>
 __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
 {
     constexpr int WM = LG_BM / 2, WN = LG_BN / 2;
@@ -57,7 +59,7 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     const int kb = blockIdx.z * p.kchunk;
     const int ke = kb + p.kchunk < p.K ? kb + p.kchunk : p.K;
     const int ksteps = (ke - kb + LG_BK - 1) / LG_BK;
-    const int LA = A32 ? limbs_for(slot_read(p.a_max)) : 1;
+    const int LA = p.a_max ? limbs_for(slot_read(p.a_max)) : 1;
     const int LB = p.b_max ? limbs_for(slot_read(p.b_max)) : 1;
     if (LA > 4 || LB > 4) {
         if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
@@ -65,8 +67,7 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     }
     const int kc = tid & 3;
 
-    typedef typename std::conditional<A32, v4i[4], v4i[1]>::type ARaw;
-    ARaw ar[A_CHUNKS];
+    v4i ar[A_CHUNKS];
     v4i br[B_CHUNKS];
     int64_t acc64[TM][TN][4];
 #pragma unroll
@@ -78,6 +79,7 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
 
     for (int la = 0; la < LA; la++) {
         for (int lb = 0; lb < LB; lb++) {
+            const int8_t *apl = p.a + la * p.aplane;
             const int8_t *bpl = p.b + lb * p.bplane;
             auto load = [&](int ks) {
                 const int k = kb + ks * LG_BK + kc * 16;
@@ -86,14 +88,7 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
                 for (int i = 0; i < A_CHUNKS; i++) {
                     const int m = m0 + (tid >> 2) + 64 * i;
                     const bool ok = kin && m < p.M;
-                    if (A32) {
-                        const v4i *src = (const v4i *)((const int32_t *)p.a + (int64_t)m * p.lda + k);
-#pragma unroll
-                        for (int u = 0; u < 4; u++) ar[i][u] = ok ? src[u] : v4i{0, 0, 0, 0};
-                    } else {
-                        ar[i][0] = ok ? *(const v4i *)((const int8_t *)p.a + (int64_t)m * p.lda + k)
-                                      : v4i{0, 0, 0, 0};
-                    }
+                    ar[i] = ok ? *(const v4i *)(apl + (int64_t)m * p.lda + k) : v4i{0, 0, 0, 0};
                 }
 #pragma unroll
                 for (int i = 0; i < B_CHUNKS; i++) {
@@ -106,17 +101,8 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
                 uint8_t *As = smem + buf * STAGE;
                 uint8_t *Bs = As + LG_BM * LG_LDS;
 #pragma unroll
-                for (int i = 0; i < A_CHUNKS; i++) {
-                    v4i v;
-                    if (A32) {
-#pragma unroll
-                        for (int u = 0; u < 4; u++)
-                            v[u] = (int)limb4(ar[i][u][0], ar[i][u][1], ar[i][u][2], ar[i][u][3], la);
-                    } else {
-                        v = ar[i][0];
-                    }
-                    *(v4i *)(As + ((tid >> 2) + 64 * i) * LG_LDS + kc * 16) = v;
-                }
+                for (int i = 0; i < A_CHUNKS; i++)
+                    *(v4i *)(As + ((tid >> 2) + 64 * i) * LG_LDS + kc * 16) = ar[i];
 #pragma unroll
                 for (int i = 0; i < B_CHUNKS; i++)
                     *(v4i *)(Bs + ((tid >> 2) + 64 * i) * LG_LDS + kc * 16) = br[i];
@@ -223,7 +209,7 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
             if (p.delta)
 #pragma unroll
                 for (int q = 0; q < 4; q++) *(v4i *)(p.delta + o + 4 * q) = dv[q];
-            if (!p.pool) {
+            if (!p.pool || p.gpooled) {
 #pragma unroll
                 for (int q = 0; q < 4; q++) *(v4i *)(p.g + o + 4 * q) = gv[q];
                 continue;
@@ -254,12 +240,12 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     block_slot_max(p.gmax, mx);
 }
 
-template <bool A32, int MODE>
+template <int MODE>
 static void launch_lgemm(hipStream_t s, const LgemmArgs &a, int splits)
 {
     dim3 grid((unsigned)((a.M + LG_BM - 1) / LG_BM), (unsigned)((a.N + LG_BN - 1) / LG_BN),
               (unsigned)splits);
-    hipLaunchKernelGGL((k_lgemm<A32, MODE>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_lgemm<MODE>), grid, dim3(256), 0, s, a);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -311,7 +297,7 @@ __global__ __launch_bounds__(256) void k_transpose_i8(const int8_t *__restrict__
 __global__ void k_loss_from_partials(const int64_t *__restrict__ part, int nz, int N, int G, int gp,
                                      int np, Div sf, const int32_t *__restrict__ labels,
                                      int32_t *__restrict__ yhat, int32_t *__restrict__ e,
-                                     int32_t *__restrict__ epad, int32_t *__restrict__ et,
+                                     int8_t *__restrict__ epad, int8_t *__restrict__ et,
                                      uint32_t *emax, uint32_t *flags)
 {
     uint32_t m = 0;
@@ -333,8 +319,15 @@ __global__ void k_loss_from_partials(const int64_t *__restrict__ part, int nz, i
             const uint32_t a = abs_i64_sat(ev);
             m = a > m ? a : m;
         }
-        if (n < N) epad[n * gp + g] = (int32_t)ev;
-        et[(int64_t)g * np + n] = (int32_t)ev;
+        // e's four balanced limb planes in both layouts (a value outside int32 is flagged above)
+        const int32_t e32 = (int32_t)ev;
+        const int64_t plane = (int64_t)np * gp;
+#pragma unroll
+        for (int l = 0; l < 4; l++) {
+            const int8_t d = limb1(e32, l);
+            if (n < N) epad[l * plane + n * gp + g] = d;
+            et[l * plane + (int64_t)g * np + n] = d;
+        }
     }
     if (bad) raise_flag(flags, FLAG_OVERFLOW);
     if (badlab) raise_flag(flags, FLAG_LABEL);
@@ -376,7 +369,7 @@ void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *
                           const LearningBuffers &b, const uint8_t *code, const Relu &rp, int h,
                           int wdt, int c, bool pool, int32_t *g, int32_t *delta_copy,
                           int32_t *yhat, int32_t *e, int64_t *dw, uint32_t *flags,
-                          bool prepacked)
+                          bool prepacked, bool g_pooled)
 {
     const LearningScratch sc = learning_scratch(n, d, G);
     // operands: learning-weight limb planes (unless the caller packed them), the transposed
@@ -393,7 +386,7 @@ void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *
         a.kchunk = (int)sc.kchunk;
         a.out64 = b.part;
         a.flags = flags;
-        launch_lgemm<false, LIN_PART>(s, a, sc.splits);
+        launch_lgemm<LIN_PART>(s, a, sc.splits);
         hipLaunchKernelGGL(k_loss_from_partials, dim3(grid_stride_blocks((int64_t)sc.np * sc.gp, 256, 256)),
                            dim3(256), 0, s, b.part, sc.splits, n, G, sc.gp, sc.np, sf, labels, yhat,
                            e, b.epad, b.et, b.emax, flags);
@@ -402,24 +395,25 @@ void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *
     {
         LgemmArgs a{};
         a.M = sc.gp; a.N = (int)d; a.K = sc.np;
-        a.a = b.et; a.lda = sc.np; a.a_max = b.emax;
+        a.a = b.et; a.lda = sc.np; a.aplane = (int64_t)sc.gp * sc.np; a.a_max = b.emax;
         a.b = b.ft; a.ldb = sc.np; a.bplane = 0; a.b_max = nullptr;
         a.kchunk = sc.np;
         a.out64 = dw; a.ldc = d; a.m_valid = G;
         a.flags = flags;
-        launch_lgemm<true, LIN_DW>(s, a, 1);
+        launch_lgemm<LIN_DW>(s, a, 1);
     }
     // delta = e W (pre-update), routed through the pool and NITRO-ReLU backward into g
     {
         LgemmArgs a{};
         a.M = n; a.N = (int)d; a.K = sc.gp;
-        a.a = b.epad; a.lda = sc.gp; a.a_max = b.emax;
+        a.a = b.epad; a.lda = sc.gp; a.aplane = (int64_t)sc.np * sc.gp; a.a_max = b.emax;
         a.b = b.wt; a.ldb = sc.gp; a.bplane = d * sc.gp; a.b_max = b.wmax;
         a.kchunk = sc.gp;
         a.code = code; a.rp = rp; a.h = h; a.w = wdt; a.c = c; a.pool = pool ? 1 : 0;
+        a.gpooled = pool && g_pooled ? 1 : 0;
         a.g = g; a.delta = delta_copy; a.gmax = b.gmax;
         a.flags = flags;
-        launch_lgemm<true, LIN_UNPOOL>(s, a, 1);
+        launch_lgemm<LIN_UNPOOL>(s, a, 1);
     }
 }
 

@@ -477,18 +477,21 @@ struct LearningScratch {
 struct LearningBuffers {
     int8_t *wf, *wt, *ft;          // weight limb planes [4][G][d], [4][d][gp]; f^T [d][np]
     int64_t *part;                 // forward split-K partial sums
-    int32_t *epad, *et;            // e as [np][gp] and [gp][np] (zero padded)
+    int8_t *epad, *et;             // e's 4 limb planes as [np][gp] and [gp][np] (zero padded)
     uint32_t *wmax, *emax, *gmax;  // max|W|, max|e|, max|g| slots (zeroed before the call)
 };
 bool mfma_learning_ok(int n, int64_t d, int G, int c);   // c: block output channels
 LearningScratch learning_scratch(int n, int64_t d, int G);
 // yhat, e, dW of the learning layer on f = the block output [n][d], and the gradient g at the
 // last forward layer's pre-activation (un-pool and NITRO-ReLU backward of delta = e W).
+// g_pooled (pooled block): g is left at the pooled positions, [n][h/2][w/2][c], the value of each
+// window's argmax (the others are zero); launch_conv_dw_planes un-pools it with the codes.
 void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *f,
                           const int32_t *w, const Div &sf, const int32_t *labels,
                           const LearningBuffers &b, const uint8_t *code, const Relu &rp, int h,
                           int wdt, int c, bool pool, int32_t *g, int32_t *delta_copy,
-                          int32_t *yhat, int32_t *e, int64_t *dw, uint32_t *flags, bool prepacked = false);
+                          int32_t *yhat, int32_t *e, int64_t *dw, uint32_t *flags, bool prepacked = false,
+                          bool g_pooled = false);
 
 // ---- few input channels (conv_smallc.hip)
 bool smallc_fwd_ok(const ConvShape &sh);
@@ -536,10 +539,12 @@ int64_t dwp_partial_count(const ConvShape &sh);
 // only the pad rows are zeroed here.
 constexpr int DWP_HMAX = 64;
 int64_t dwp_rows_stride(const ConvShape &sh);   // xs
+// pool_code (a pooled layer's codes, [n][h/2][w/2][co]): g is given at the pooled positions only
+// (launch_learning_mfma with g_pooled) and each window's argmax takes the value
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
                            int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags,
-                           bool x_rows_ready = false);
+                           bool x_rows_ready = false, const uint8_t *pool_code = nullptr);
 
 // ---- implicit-GEMM conv with the input tile staged once (conv_tile.hip)
 bool tile_conv_fwd_ok(const ConvShape &sh, bool pool, int64_t sf, int alpha_inv);

@@ -37,8 +37,9 @@ def rand(rng, shape, lo, hi, dtype):
 
 
 def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dmax=1 << 15,
-              conv=True):
-    """One nitro_block_forward + nitro_block_backward against the oracle's block functions."""
+              conv=True, tap_last_g=True):
+    """One nitro_block_forward + nitro_block_backward against the oracle's block functions.
+    tap_last_g=False leaves the last layer's g untapped (the library may then keep it pooled)."""
     print("block case", dict(n=n, h=h, w=w, chans=chans, pool=maxpool, G=G, alpha=alpha,
                              mode=nm, wmax=wmax, conv=conv), flush=True)
     J = len(chans) - 1
@@ -84,7 +85,8 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
     ctx.block_forward(desc, wd, xd, a_out, state)
     dws = [torch.empty(a.shape, dtype=torch.int64, device=DEV) for a in ws]
     dw_lr = torch.empty((G, d), dtype=torch.int64, device=DEV) if G else None
-    taps = {"g": [torch.empty(l.zs.shape, dtype=torch.int32, device=DEV) for l in rec.layers],
+    taps = {"g": [torch.empty(l.zs.shape, dtype=torch.int32, device=DEV)
+                  if tap_last_g or j < J - 1 else None for j, l in enumerate(rec.layers)],
             "dx": torch.empty(x.shape, dtype=torch.int64, device=DEV) if want_dx else None}
     if G:
         taps["yhat"] = torch.empty((n, G), dtype=torch.int32, device=DEV)
@@ -104,7 +106,8 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
         assert np.array_equal(host(dw_lr), rec.dw_lr), "dW learning"
         assert np.array_equal(host(taps["delta"]), rec.delta_fw.reshape(out_shape)), "delta_fw"
     for j in range(J):
-        assert np.array_equal(host(taps["g"][j]), rec.g[j]), "g layer %d" % j
+        if taps["g"][j] is not None:
+            assert np.array_equal(host(taps["g"][j]), rec.g[j]), "g layer %d" % j
         assert np.array_equal(host(dws[j]), rec.dw[j]), "dW layer %d" % j
     if want_dx:
         assert np.array_equal(host(taps["dx"]), rec.dx), "dx"
@@ -180,6 +183,31 @@ def test_conv_block_persistent(ctx, case, modes):
     finally:
         ctx.set_conv_tile(0)
         ctx.set_conv_persistent(0)
+
+
+# pooled blocks on the MFMA learning layer whose last layer's g is not tapped: the learning layer
+# leaves that g pooled and the weight-gradient planes un-pool it (one and two conv layers, both
+# conv tiles)
+POOLED_G_CASES = [
+    (2, 8, 8, [64, 128, 128], True, 100, 16, 6000),
+    (1, 32, 32, [3, 64, 64], True, 100, 10, 44),
+    (3, 16, 16, [32, 64, 64], True, 10, 10, 300),
+    (2, 6, 10, [64, 64], True, 10, 10, 127),
+]
+
+
+@pytest.mark.parametrize("tile", [128, 256])
+@pytest.mark.parametrize("case", POOLED_G_CASES)
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_conv_block_pooled_g(ctx, tile, case, modes):
+    n, h, w, chans, pool, G, alpha, wmax = case
+    rng = np.random.default_rng(hash((n, h, w, tuple(chans), G, tile, 77)) % (1 << 31))
+    ctx.set_conv_tile(tile)
+    try:
+        run_block(ctx, rng, n, h, w, chans, pool, G, alpha, modes[0], modes[1], wmax=wmax,
+                  tap_last_g=False)
+    finally:
+        ctx.set_conv_tile(0)
 
 
 @pytest.mark.parametrize("chans,G,wmax", [([784, 100], 10, 7), ([100, 50, 30], 10, 300),
