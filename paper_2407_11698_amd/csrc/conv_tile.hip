@@ -468,6 +468,9 @@ void k_conv_tile(TileArgs p)
         asm volatile("" : "+v"(etid));
         const int pxl = (etid >> 7) * 64 + (etid & 15);
         const int cbl = ((etid >> 6) & 1) * 32 + 4 * ((etid >> 4) & 3);
+        // (input gradient, register staging: the next tile's first phase to its stage before
+        // the epilogue's global stores, as in the forward epilogue)
+        if (MODE == IG_DX && !ADMA && S::NBUF == 2 && more) stage_store(gph & 1);
         if (MODE == IG_FWD) {
             // NITRO-Scaling (shift, clamp, one multiply-high) and the table's NITRO-ReLU per
             // element; four channels packed per dword into LDS, then 16-byte (or pooled) stores.
@@ -485,26 +488,33 @@ void k_conv_tile(TileArgs p)
             const int epi = !EPI_IN_STAGE ? 2 * SAB : S::NBUF == 2 ? ((gph - 1) & 1) * SAB : 0;
             uint32_t *Ov = (uint32_t *)(smem + epi);  // [BM][OW] packed activations
             uint32_t *Rv = Ov + BM * OW;              // [BM][OW] packed region codes
+            // (every table read is issued before the first is used; each entry is the output
+            // byte | region << 8, and two byte permutes gather four entries' outputs and regions)
             auto pack = [&](auto trunc_tag) {
                 constexpr bool TR = decltype(trunc_tag)::value;
+                uint32_t ent[TM][TN][4];
+#pragma unroll
+                for (int i = 0; i < TM; i++)
+#pragma unroll
+                    for (int j = 0; j < TN; j++)
+#pragma unroll
+                        for (int t = 0; t < 4; t++) ent[i][j][t] = tab[scale_fast<TR>(acc[i][j][t], p.sf) + 128];
 #pragma unroll
                 for (int i = 0; i < TM; i++)
 #pragma unroll
                     for (int j = 0; j < TN; j++) {
-                        uint32_t av = 0, rv = 0;
-#pragma unroll
-                        for (int t = 0; t < 4; t++) {
-                            const uint32_t e = tab[scale_fast<TR>(acc[i][j][t], p.sf) + 128];
-                            av |= (e & 0xffu) << (8 * t);
-                            rv |= (e >> 8) << (8 * t);
-                        }
+                        const uint32_t x01 = ent[i][j][0] | (ent[i][j][1] << 16);
+                        const uint32_t x23 = ent[i][j][2] | (ent[i][j][3] << 16);
                         const int o = (pxl + 16 * i) * OW + (cbl + 16 * j) / 4;
-                        Ov[o] = av;
-                        Rv[o] = rv;
+                        Ov[o] = __builtin_amdgcn_perm(x23, x01, 0x06040200u);
+                        Rv[o] = __builtin_amdgcn_perm(x23, x01, 0x07050301u);
                     }
             };
             if (p.sf.trunc) pack(std::true_type{});
             else pack(std::false_type{});
+            // register staging: the next tile's first phase goes to its stage now (its loads
+            // were issued before this epilogue), ahead of the epilogue's global stores
+            if (!ADMA && S::NBUF == 2 && more) stage_store(gph & 1);
             __syncthreads();
             if (!p.pool) {
                 for (int c = etid; c < BM * CT_BN / 16; c += NT) {
@@ -624,8 +634,6 @@ void k_conv_tile(TileArgs p)
         }
         if (!more) break;
         v = vn;
-        // (the epilogue uses the other stage)
-        if (!ADMA && S::NBUF == 2) stage_store(gph & 1);
     }
     if (MODE == IG_DX && !p.out64) {
         if (bad) raise_flag(p.flags, FLAG_OVERFLOW);
