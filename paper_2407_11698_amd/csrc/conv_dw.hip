@@ -7,9 +7,14 @@
 // position k = (n (H+1) + h) (W+1) + w and each neighbour outside the image lands on a zero. A
 // tap (r, s) is then the plain position offset (r-1)(W+1) + (s-1):
 //   dW[co][r][s][ci] = sum_k gp[co][k] * xr[ci][HMAX + k + (r-1)(W+1) + (s-1)]
-// with no bounds test. gp holds the balanced int8 limbs of g, one plane per limb, positions
-// contiguous (zeros at pad positions). xr holds x in rows of 16 channels: [C_in / 16][position]
-// [16 channels], with a zero halo of HMAX >= W + 2 positions on both sides.
+// with no bounds test. gp holds the balanced int8 limbs of g, one plane per limb (zeros at pad
+// positions), stored as the MFMA A fragments themselves: for each super-step of 256 positions,
+// 16-channel block of co and K-step of 64 positions, one 1 KB fragment whose lane L = 16 q + j
+// (16 bytes at 16 L) holds co row j, positions 16 q .. 16 q + 15 of the K-step. A fragment load
+// is then one contiguous 1 KB read (with rows [co][kp] the four lanes sharing a 64-byte row
+// segment are 16 lanes apart, and every lane is a cache access of its own). xr holds x in rows
+// of 16 channels: [C_in / 16][position][16 channels], with a zero halo of HMAX >= W + 2
+// positions on both sides.
 //
 // GEMM: M = co, N = ci (times 9 taps), K = padded positions. A workgroup owns a 64 co x 16 ci
 // tile, all 9 taps, over a range of K. Its four waves run independently (no barrier in the main
@@ -158,8 +163,10 @@ __global__ __launch_bounds__(256) void k_dwp_pad_rows(int n, int h, int w, int h
     *(v4i *)(xr + ((int64_t)t * xs + row) * 16) = v4i{0, 0, 0, 0};
 }
 
-// g int32 NHWC [P][C] -> gp [l][C][kp] for l < limbs(max|g|): limb l of g at padded position k
-// (zeros at pad positions); when gn is not null also the NHWC limb planes gn [l][P][C] (the A
+// g int32 NHWC [P][C] -> gp, limb planes l < limbs(max|g|) in fragment order: limb l of g at
+// padded position k (zeros at pad positions), 16-byte chunk (channel c, positions k .. k + 15)
+// at l C kp + ((k / 256 * C / 16 + c / 16) * 4 + k % 256 / 64) * 1024 + 256 (k % 64 / 16)
+// + 16 (c % 16); when gn is not null also the NHWC limb planes gn [l][P][C] (the A
 // operand of the input-gradient GEMM). A workgroup: 64 positions x 64 channels, transposed
 // through LDS. With pcode, g holds a 2x2-pooled layer's gradient at the pooled positions only,
 // [n][h/2][w/2][C]: pixel (y, x) takes it where the pool's argmax (the code's low 2 bits) is
@@ -236,14 +243,17 @@ __global__ __launch_bounds__(256) void k_dwp_grad_planes(const int32_t *__restri
 #pragma unroll
             for (int q = 0; q < 4; q++)
                 o[q] = (int)limb4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3], l);
-            *(v4i *)(gp + ((int64_t)l * c + c0 + cc) * kp + k0 + 16 * pq) = o;
+            const int co = c0 + cc;
+            *(v4i *)(gp + (int64_t)l * c * kp +
+                     (((int64_t)(k0 >> 8) * (c >> 4) + (co >> 4)) * 4 + ((k0 & 255) >> 6)) * 1024 +
+                     256 * pq + 16 * (co & 15)) = o;
         }
     }
 }
 
 // ---------------------------------------------------------------------------------------------
 struct DwpArgs {
-    const int8_t *gp;      // [LA][co][kp]
+    const int8_t *gp;      // LA planes of co kp, fragment order
     int64_t kp;
     const int8_t *xr;      // [ci / 16][xs][16]
     int64_t xs;
@@ -306,12 +316,14 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
     const int j = lane & 15, g4 = lane >> 4;
     // 32-bit offsets from the plane bases (the host checks that both fit)
     const uint32_t plane = (uint32_t)p.co * (uint32_t)p.kp;
-    // co rows past the end (a partial last tile) read row co - 1; their sums are not stored
+    // fragment (super-step ss, co block b, K-step u) of a plane at ((ss CT + b) 4 + u) 1 KB;
+    // co blocks past the end (a partial last tile) read block CT - 1, their sums not stored
+    const uint32_t CT = (uint32_t)p.co / 16;
     uint32_t aoff[4];
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        const int row = co0 + 16 * i + j < p.co ? co0 + 16 * i + j : p.co - 1;
-        aoff[i] = (uint32_t)row * (uint32_t)p.kp + 16 * g4;
+        const uint32_t blk = (uint32_t)co0 / 16 + i < CT ? (uint32_t)co0 / 16 + i : CT - 1;
+        aoff[i] = blk * 4096u + 16u * (uint32_t)lane;
     }
     // this wave's x rows: the window of super-step ss is rows ss KS .. ss KS + WIN of the tile's
     // row block, contiguous; lane stages rows lane + 64 m
@@ -338,7 +350,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
     v4i bst[DWP_NCH];            // staged x rows
 
     auto load_a = [&](int u, int ss, int l) {
-        const uint32_t k = (uint32_t)ss * DWP_KS + (uint32_t)l * plane + 64 * u;
+        const uint32_t k = (uint32_t)l * plane + (uint32_t)ss * CT * 4096u + 1024u * u;
 #pragma unroll
         for (int i = 0; i < 4; i++) a[u][i] = *(const v4i *)(p.gp + (aoff[i] + k));
     };
@@ -367,7 +379,12 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
                         a[u][i], b, (decltype(first)::value && u == 0) ? v4i{0, 0, 0, 0} : acc[t][i],
                         0, 0, 0);
             }
-            if (decltype(reload)::value) load_a(u, next, l);
+            if (decltype(reload)::value) {
+                load_a(u, next, l);
+                // (kept here: left to itself the scheduler sinks every load of the next
+                // super-step to the end of this one, and each is then waited for)
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
     };
 
@@ -382,11 +399,13 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
             // super-step 0 (peeled), then 1 .. nst - 1; the last one requests nothing
             if (nst > 1) {
                 load_b(wb + 1);
+                __builtin_amdgcn_sched_barrier(0);
                 compute(std::true_type(), std::true_type(), 0, wb + 1, l);
                 store_b(1);
                 wave_lds_sync();
                 for (int s = 1; s + 1 < nst; s++) {
                     load_b(wb + s + 1);
+                    __builtin_amdgcn_sched_barrier(0);
                     compute(std::false_type(), std::true_type(), s & 1, wb + s + 1, l);
                     store_b((s + 1) & 1);
                     wave_lds_sync();

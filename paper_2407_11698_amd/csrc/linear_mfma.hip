@@ -23,7 +23,7 @@ struct LgemmArgs {
     const int8_t *b;              // B limb planes [4][N][ldb] (one plane when b_max is null)
     int64_t ldb, bplane;
     const uint32_t *b_max;
-    int kchunk;                   // K per split (multiple of 64); grid.z = number of splits
+    int kchunk;                   // K per split (a multiple of 16); grid.z = number of splits
     // LIN_PART: part[z][M][N]; LIN_DW: out64[m * ldc + j] for m < m_valid
     int64_t *out64;
     int64_t ldc;
@@ -39,18 +39,27 @@ struct LgemmArgs {
     uint32_t *flags;
 };
 
-constexpr int LG_BM = 128, LG_BN = 64, LG_BK = 64, LG_LDS = 80;
+constexpr int LG_BM = 128, LG_BN = 64, LG_BK = 64;
+constexpr int LG_KC = 128;                // K per staged chunk (two MFMA K-steps)
+constexpr int LG_LS = LG_KC + 16;         // LDS row stride: 16 rows of a fragment read hit
+                                          // 16 different bank quads
+constexpr int LG_SA = LG_BM * LG_LS;      // one A limb plane of a chunk
+constexpr int LG_SB = LG_BN * LG_LS;      // one B limb plane
 
+// A workgroup: a 128 x 64 tile of C over its K range, in chunks of 128. Every limb plane of both
+// operands for a chunk is staged in LDS at once (one load round per chunk, the next chunk's loads
+// issued before this one's MFMAs), then each limb pair (la, lb) runs its two K-steps from LDS
+// and is folded into int64 with its weight 256^(la + lb).
 template <int MODE>
 __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
 {
     constexpr int WM = LG_BM / 2, WN = LG_BN / 2;
     constexpr int TM = WM / 16, TN = WN / 16;
-    constexpr int A_CHUNKS = LG_BM * 4 / 256, B_CHUNKS = LG_BN * 4 / 256;
-    constexpr int STAGE = (LG_BM + LG_BN) * LG_LDS;
+    constexpr int AU = LG_BM * (LG_KC / 16) / 256, BU = LG_BN * (LG_KC / 16) / 256;  // units/thread
     constexpr int DS = LG_BN + 1;                 // epilogue int32-tile row stride
     constexpr int SMEM_EPI = MODE == LIN_UNPOOL ? LG_BM * DS * 4 : 0;
-    constexpr int SMEM = 2 * STAGE > SMEM_EPI ? 2 * STAGE : SMEM_EPI;
+    constexpr int SMEM_OP = 4 * LG_SA + 4 * LG_SB;
+    constexpr int SMEM = SMEM_OP > SMEM_EPI ? SMEM_OP : SMEM_EPI;
     __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -58,17 +67,51 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     const int m0 = blockIdx.x * LG_BM, n0 = blockIdx.y * LG_BN;
     const int kb = blockIdx.z * p.kchunk;
     const int ke = kb + p.kchunk < p.K ? kb + p.kchunk : p.K;
-    const int ksteps = (ke - kb + LG_BK - 1) / LG_BK;
-    const int LA = p.a_max ? limbs_for(slot_read(p.a_max)) : 1;
-    const int LB = p.b_max ? limbs_for(slot_read(p.b_max)) : 1;
-    if (LA > 4 || LB > 4) {
-        if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
-        return;
-    }
-    const int kc = tid & 3;
+    const int nck = (ke - kb + LG_KC - 1) / LG_KC;
+    uint8_t *As = smem, *Bs = smem + 4 * LG_SA;
 
-    v4i ar[A_CHUNKS];
-    v4i br[B_CHUNKS];
+    // unit u of a thread: row (tid >> 3) + 32 u, 16-byte column tid & 7. Limb plane 0 (always
+    // used) of the first chunk is requested before the limb counts are known; planes 1-3 of a
+    // chunk only when used.
+    const int ur = tid >> 3, uc = (tid & 7) * 16;
+    v4i ar[4][AU], br[4][BU];
+    int LA = 1, LB = 1;
+    auto load = [&](int ck, int l0, int l1) {
+        const int k = kb + ck * LG_KC + uc;
+        const bool kin = k < ke;
+#pragma unroll
+        for (int l = 0; l < 4; l++) {
+            if (l < l0 || l >= l1) continue;
+            if (l < LA) {
+                const int8_t *apl = p.a + l * p.aplane;
+#pragma unroll
+                for (int u = 0; u < AU; u++) {
+                    const int m = m0 + ur + 32 * u;
+                    ar[l][u] = kin && m < p.M ? *(const v4i *)(apl + (int64_t)m * p.lda + k) : v4i{0, 0, 0, 0};
+                }
+            }
+            if (l < LB) {
+                const int8_t *bpl = p.b + l * p.bplane;
+#pragma unroll
+                for (int u = 0; u < BU; u++) {
+                    const int nn = n0 + ur + 32 * u;
+                    br[l][u] = kin && nn < p.N ? *(const v4i *)(bpl + (int64_t)nn * p.ldb + k) : v4i{0, 0, 0, 0};
+                }
+            }
+        }
+    };
+    auto store = [&]() {
+#pragma unroll
+        for (int l = 0; l < 4; l++) {
+            if (l < LA)
+#pragma unroll
+                for (int u = 0; u < AU; u++) *(v4i *)(As + l * LG_SA + (ur + 32 * u) * LG_LS + uc) = ar[l][u];
+            if (l < LB)
+#pragma unroll
+                for (int u = 0; u < BU; u++) *(v4i *)(Bs + l * LG_SB + (ur + 32 * u) * LG_LS + uc) = br[l][u];
+        }
+    };
+
     int64_t acc64[TM][TN][4];
 #pragma unroll
     for (int i = 0; i < TM; i++)
@@ -77,76 +120,64 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
 #pragma unroll
             for (int t = 0; t < 4; t++) acc64[i][j][t] = 0;
 
-    for (int la = 0; la < LA; la++) {
-        for (int lb = 0; lb < LB; lb++) {
-            const int8_t *apl = p.a + la * p.aplane;
-            const int8_t *bpl = p.b + lb * p.bplane;
-            auto load = [&](int ks) {
-                const int k = kb + ks * LG_BK + kc * 16;
-                const bool kin = k < ke;
+    if (nck > 0) load(0, 0, 1);
+    LA = p.a_max ? limbs_for(slot_read(p.a_max)) : 1;
+    LB = p.b_max ? limbs_for(slot_read(p.b_max)) : 1;
+    if (LA > 4 || LB > 4) {
+        if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
+        return;
+    }
+    if (nck > 0) load(0, 1, 4);
+    // (LIN_UNPOOL: the epilogue's region codes, requested now)
+    constexpr int EIT = MODE == LIN_UNPOOL ? LG_BM * (LG_BN / 16) / 256 : 1;
+    v4i cdp[EIT];
+    if (MODE == LIN_UNPOOL) {
 #pragma unroll
-                for (int i = 0; i < A_CHUNKS; i++) {
-                    const int m = m0 + (tid >> 2) + 64 * i;
-                    const bool ok = kin && m < p.M;
-                    ar[i] = ok ? *(const v4i *)(apl + (int64_t)m * p.lda + k) : v4i{0, 0, 0, 0};
-                }
-#pragma unroll
-                for (int i = 0; i < B_CHUNKS; i++) {
-                    const int nn = n0 + (tid >> 2) + 64 * i;
-                    br[i] = (kin && nn < p.N) ? *(const v4i *)(bpl + (int64_t)nn * p.ldb + k)
-                                              : v4i{0, 0, 0, 0};
-                }
-            };
-            auto store = [&](int buf) {
-                uint8_t *As = smem + buf * STAGE;
-                uint8_t *Bs = As + LG_BM * LG_LDS;
-#pragma unroll
-                for (int i = 0; i < A_CHUNKS; i++)
-                    *(v4i *)(As + ((tid >> 2) + 64 * i) * LG_LDS + kc * 16) = ar[i];
-#pragma unroll
-                for (int i = 0; i < B_CHUNKS; i++)
-                    *(v4i *)(Bs + ((tid >> 2) + 64 * i) * LG_LDS + kc * 16) = br[i];
-            };
-            v4i acc[TM][TN];
-#pragma unroll
-            for (int i = 0; i < TM; i++)
-#pragma unroll
-                for (int j = 0; j < TN; j++) acc[i][j] = v4i{0, 0, 0, 0};
-            if (ksteps > 0) {
-                load(0);
-                store(0);
-            }
-            __syncthreads();
-            for (int ks = 0; ks < ksteps; ks++) {
-                const int cur = ks & 1;
-                const bool more = ks + 1 < ksteps;
-                if (more) load(ks + 1);
-                const uint8_t *As = smem + cur * STAGE;
-                const uint8_t *Bs = As + LG_BM * LG_LDS;
-                v4i af[TM], bf[TN];
+        for (int q = 0; q < EIT; q++) {
+            const int it = tid + 256 * q;
+            const int m = m0 + it / (LG_BN / 16), col = n0 + (it % (LG_BN / 16)) * 16;
+            cdp[q] = m < p.M && col < p.N ? *(const v4i *)(p.code + (int64_t)m * p.N + col) : v4i{0, 0, 0, 0};
+        }
+    }
+    for (int ck = 0; ck < nck; ck++) {
+        __syncthreads();                          // every wave is done with the previous chunk
+        store();
+        __syncthreads();
+        if (ck + 1 < nck) load(ck + 1, 0, 4);
+        for (int la = 0; la < LA; la++) {
+            for (int lb = 0; lb < LB; lb++) {
+                const uint8_t *Ap = As + la * LG_SA, *Bp = Bs + lb * LG_SB;
+                v4i acc[TM][TN];
 #pragma unroll
                 for (int i = 0; i < TM; i++)
-                    af[i] = *(const v4i *)(As + (wm * WM + i * 16 + (lane & 15)) * LG_LDS + (lane >> 4) * 16);
 #pragma unroll
-                for (int j = 0; j < TN; j++)
-                    bf[j] = *(const v4i *)(Bs + (wn * WN + j * 16 + (lane & 15)) * LG_LDS + (lane >> 4) * 16);
+                    for (int j = 0; j < TN; j++) acc[i][j] = v4i{0, 0, 0, 0};
+#pragma unroll
+                for (int ks = 0; ks < LG_KC / LG_BK; ks++) {
+                    v4i af[TM], bf[TN];
+#pragma unroll
+                    for (int i = 0; i < TM; i++)
+                        af[i] = *(const v4i *)(Ap + (wm * WM + i * 16 + (lane & 15)) * LG_LS + ks * LG_BK + (lane >> 4) * 16);
+#pragma unroll
+                    for (int j = 0; j < TN; j++)
+                        bf[j] = *(const v4i *)(Bp + (wn * WN + j * 16 + (lane & 15)) * LG_LS + ks * LG_BK + (lane >> 4) * 16);
+#pragma unroll
+                    for (int i = 0; i < TM; i++)
+#pragma unroll
+                        for (int j = 0; j < TN; j++)
+                            acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
+                }
+                const int sh = 8 * (la + lb);
 #pragma unroll
                 for (int i = 0; i < TM; i++)
 #pragma unroll
                     for (int j = 0; j < TN; j++)
-                        acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
-                if (more) store(cur ^ 1);
-                __syncthreads();
+#pragma unroll
+                        for (int t = 0; t < 4; t++) acc64[i][j][t] += (int64_t)acc[i][j][t] << sh;
             }
-            const int sh = 8 * (la + lb);
-#pragma unroll
-            for (int i = 0; i < TM; i++)
-#pragma unroll
-                for (int j = 0; j < TN; j++)
-#pragma unroll
-                    for (int t = 0; t < 4; t++) acc64[i][j][t] += (int64_t)acc[i][j][t] << sh;
         }
     }
+    __syncthreads();                              // (the epilogue reuses the LDS)
 
     if (MODE != LIN_UNPOOL) {
 #pragma unroll
@@ -188,12 +219,14 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     const uint32_t W2 = (uint32_t)p.w / 2;
     auto emit = [&](auto trunc_tag) {
         constexpr bool TR = decltype(trunc_tag)::value;
-        for (int it = tid; it < LG_BM * (LG_BN / 16); it += 256) {
+#pragma unroll
+        for (int q = 0; q < EIT; q++) {
+            const int it = tid + 256 * q;
             const int row = it / (LG_BN / 16), cc = (it % (LG_BN / 16)) * 16;
             const int m = m0 + row, col = n0 + cc;
             if (m >= p.M || col >= p.N) continue;
             const int64_t o = (int64_t)m * p.N + col;
-            const v4i cd = *(const v4i *)(p.code + o);
+            const v4i cd = cdp[q];
             v4i dv[4], gv[4];
 #pragma unroll
             for (int e = 0; e < 16; e++) {
@@ -307,8 +340,19 @@ __global__ void k_loss_from_partials(const int64_t *__restrict__ part, int nz, i
         const int n = i / gp, g = i % gp;
         int64_t ev = 0;
         if (n < N && g < G) {
-            int64_t z = 0;
-            for (int s = 0; s < nz; s++) z += part[((int64_t)s * N + n) * G + g];
+            // (four independent sums: the split partials are read four loads at a time)
+            const int64_t st = (int64_t)N * G;
+            const int64_t *pp = part + (int64_t)n * G + g;
+            int64_t z0 = 0, z1 = 0, z2 = 0, z3 = 0;
+            int s = 0;
+            for (; s + 3 < nz; s += 4) {
+                z0 += pp[s * st];
+                z1 += pp[(s + 1) * st];
+                z2 += pp[(s + 2) * st];
+                z3 += pp[(s + 3) * st];
+            }
+            for (; s < nz; s++) z0 += pp[s * st];
+            const int64_t z = (z0 + z1) + (z2 + z3);
             const int64_t y = idiv(z, sf);
             const int lab = labels[n];
             badlab |= lab < 0 || lab >= G;
@@ -347,12 +391,13 @@ LearningScratch learning_scratch(int n, int64_t d, int G)
     LearningScratch s{};
     s.gp = (G + 15) / 16 * 16;
     s.np = (n + 15) / 16 * 16;
-    int splits = (int)((d + 1023) / 1024);
+    // forward split-K: about two staged chunks (256 of K) per workgroup, at most 1024 workgroups
+    int splits = (int)((d + 255) / 256);
     if (splits < 1) splits = 1;
     const int tiles = ((n + LG_BM - 1) / LG_BM) * ((G + LG_BN - 1) / LG_BN);
     if (splits * tiles > 1024) splits = (1024 + tiles - 1) / tiles;
     int64_t kchunk = (d + splits - 1) / splits;
-    kchunk = (kchunk + LG_BK - 1) / LG_BK * LG_BK;
+    kchunk = (kchunk + LG_KC - 1) / LG_KC * LG_KC;
     s.kchunk = kchunk;
     s.splits = (int)((d + kchunk - 1) / kchunk);
     s.wf_bytes = 4 * (int64_t)G * d;

@@ -210,6 +210,27 @@ def test_conv_block_pooled_g(ctx, tile, case, modes):
         ctx.set_conv_tile(0)
 
 
+# weight gradients on channel-tile waves (four 16-channel input tiles per workgroup, 64 output
+# channels x 4 tile groups >= 16 tiles): g in 1 to 4 limbs, one K split (dW written directly) and
+# two (int64 partials), a partial output-channel tile with C_in % 16 != 0, pooled and not
+CHANNEL_WAVE_CASES = [
+    # n, h, w, chans, pool, dmax
+    (2, 6, 6, [256, 256], False, 100),
+    (2, 6, 6, [256, 256], True, 5000),
+    (2, 6, 6, [32, 256, 256], False, 1 << 15),
+    (1, 4, 4, [256, 256], False, 1 << 24),
+    (1, 4, 4, [250, 272], False, 1 << 15),
+    (8, 16, 16, [256, 256], True, 5000),
+]
+
+
+@pytest.mark.parametrize("case", CHANNEL_WAVE_CASES)
+def test_conv_block_channel_waves(ctx, case):
+    n, h, w, chans, pool, dmax = case
+    rng = np.random.default_rng(hash((n, h, w, tuple(chans), dmax, 4242)) % (1 << 31))
+    run_block(ctx, rng, n, h, w, chans, pool, 0, 10, N.ROUND_FLOOR, O.FLOOR, dmax=dmax)
+
+
 @pytest.mark.parametrize("chans,G,wmax", [([784, 100], 10, 7), ([100, 50, 30], 10, 300),
                                           ([37, 5], 3, 20000), ([64, 65], 0, 127)])
 @pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
