@@ -50,9 +50,11 @@ struct CtCfg {
 __host__ __device__ constexpr int ct_bswz(int cc, int c) { return cc == 64 ? (c >> 1) & 3 : 0; }
 
 // A straight into LDS (64-channel chunks, W a multiple of 16, two stages): staged rows of apitch
-// pixels (W + 2 used); LDS unit 64 b + 16 e + r holds 16-channel group e of staged pixel 16 b + r,
-// so that the load is lane-linear and a fragment read (16 consecutive pixels, one group) touches
-// 16 different unit positions modulo 16, whatever its first pixel.
+// pixels (W + 2 used); LDS unit 4 q + (e ^ ((q >> 1) & 3)) holds 16-channel group e of staged
+// pixel q. The load is lane-linear, four consecutive lanes taking one pixel's 64 contiguous bytes
+// (one cache access), and a fragment read (16 consecutive pixels, one group, from any first
+// pixel) runs without bank conflicts (measured; the swizzle (q >> 2) & 3 costs about 4 conflict
+// cycles per read).
 constexpr int CT_NPMAX_DIRECT = 576;           // staged pixels
 __device__ __attribute__((aligned(16))) const int8_t ct_zero16[16] = {};   // source of zero units
 
@@ -181,8 +183,8 @@ void k_conv_tile(TileArgs p)
             int q, e;
             if (ADMA) {
                 const int unit = tid + NT * u;
-                q = 16 * (unit >> 6) + (unit & 15);
-                e = (unit >> 4) & 3;
+                q = unit >> 2;
+                e = (unit & 3) ^ ((q >> 1) & 3);
             } else {
                 a_item(tid + NT * u, q, e);
             }
@@ -214,8 +216,9 @@ void k_conv_tile(TileArgs p)
     };
     // LDS byte offset of this lane's A pixel in fragment i (tap (1, 1)). A straight into LDS:
     // the fragment's 16 pixels lie in one image row, from a column that is a multiple of 16, so
-    // the offset is that 16-pixel block's plus the lane's channel group; the lane's position in
-    // the block for column offset s - 1 (s = 0, 1, 2) is in alast[s].
+    // the offset is that 16-pixel block's; the lane's pixel l = lane % 16 + s in the block for
+    // column offset s - 1 (s = 0, 1, 2) and its channel group give alast[s] (row offsets are
+    // whole blocks, so the swizzle depends on l only).
     int cpix[TM], alast[3];
 #pragma unroll
     for (int i = 0; i < TM; i++) {
@@ -223,14 +226,14 @@ void k_conv_tile(TileArgs p)
         const int seg = (int)udiv32(mloc, p.d_rw), rem = mloc - seg * p.rs * p.w;
         const int row = (int)udiv32(rem, p.d_w), col = rem - row * p.w;
         if (ADMA)
-            cpix[i] = (seg * aseg + (row + 1) * p.apitch + col) * 64 + 256 * g4;
+            cpix[i] = (seg * aseg + (row + 1) * p.apitch + col) * 64;
         else
             cpix[i] = (seg * segpx + (row + 1) * W2 + col + 1) * C::PS;
     }
 #pragma unroll
     for (int t = 0; t < 3; t++) {
         const int l = (lane & 15) + t;
-        alast[t] = (l >> 4) * 1024 + (l & 15) * 16;
+        alast[t] = 64 * l + 16 * (g4 ^ ((l >> 1) & 3));
     }
     // LDS byte offset of this lane's B unit in each column tile (tap 0): column c, unit c16 of
     // the lane's group (fixed per lane: 4 ks + g4 = g4 modulo GPT)
