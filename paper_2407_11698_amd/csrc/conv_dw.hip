@@ -279,6 +279,11 @@ __device__ inline v2i lds_read_tr8(const uint8_t *p)
 // compiler keeps memory accesses on their side of it.
 __device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+// L3: launched for long ranges (at least DWP_L3_MIN super-steps per workgroup), where g in 3 limbs
+// takes all four waves (see below); a separate instance, as it needs more registers.
+constexpr int DWP_L3_MIN = 32;
+
+template <bool L3>
 __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 {
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -301,14 +306,20 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
     const int split = rest / p.tiles_co;
     const int co0 = tco * 64, ci0 = tci * 16;
 
-    // this wave's limb and super-steps
-    const int Q = LA == 1 ? 4 : LA == 2 ? 2 : 1;
-    const int limb = wave / Q, part = wave - limb * Q;
+    // this wave's limb and super-steps: wave w takes limb w / Q, part w % Q of the range (Q =
+    // 4 / L parts for L limbs; L = 3: one part, one wave idle). With L = 3 and a long range (the
+    // L3 instance) instead wave w takes part w of every limb in turn (l3), the limbs' sums folded
+    // into int64 between them: a pass's set-up and fold then cost less than the idle wave.
+    const bool l3 = L3 && LA == 3;
+    const int Q = LA == 1 || l3 ? 4 : LA == 2 ? 2 : 1;
+    const int npass = l3 ? 3 : 1;
+    const int limb = l3 ? 0 : wave / Q, part = wave - limb * Q;
     const int sb = split * p.chunk;
     const int se = sb + p.chunk < p.nss ? sb + p.chunk : p.nss;
     const int per = (se - sb + Q - 1) / Q;
     const int wb = sb + part * per < se ? sb + part * per : se;
     const int nst = limb < LA ? (wb + per < se ? wb + per : se) - wb : 0;
+    int64_t tot[L3 ? 3 : 1][12];   // (L3) the tile's sums, 12 per thread and 3-tap group
 
     constexpr int STAGE = DWP_WIN * 16;        // bytes of one staged window (rows of 16 B)
     uint8_t *wl = lds + wave * (2 * STAGE);    // this wave's two stages
@@ -388,8 +399,8 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
         }
     };
 
-    {
-        const int l = limb;
+    for (int pass = 0; pass < npass; pass++) {
+        const int l = l3 ? pass : limb;
         if (nst > 0) {
 #pragma unroll
             for (int u = 0; u < 4; u++) load_a(u, wb, l);
@@ -420,7 +431,9 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 #pragma unroll
                 for (int i = 0; i < 4; i++) acc[t][i] = v4i{0, 0, 0, 0};
         }
-        // sum of the four waves (int64), each weighted 256^limb -> this split's tile
+        // sum of the four waves (int64), each weighted 256^limb: straight into this split's
+        // tile, or (L3) into this thread's 36 values (3-tap group t0 / 3, element e = tid + 256 k
+        // of the group's 3 x 64 x 16), stored after the last pass
         __syncthreads();
         int32_t *red = (int32_t *)lds;        // [wave][3 taps][64 co][16 ci]
 #pragma unroll
@@ -433,17 +446,41 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
                     for (int r = 0; r < 4; r++)
                         red[((wave * 3 + tt) * 64 + 16 * i + 4 * g4 + r) * 16 + j] = acc[t0 + tt][i][r];
             __syncthreads();
-            for (int e = tid; e < 3 * 1024; e += 256) {
-                const int tt = e >> 10, co = co0 + ((e >> 4) & 63), ci = ci0 + (e & 15);
-                int64_t v = 0;
+            if (L3) {
 #pragma unroll
-                for (int w = 0; w < 4; w++)
-                    v += (int64_t)red[(w * 3 + tt) * 1024 + (e & 1023)] * ((int64_t)1 << (8 * (w / Q)));
-                if (co < p.co && ci < p.ci_out)
-                    p.out[(((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci_out + ci] = v;
+                for (int k = 0; k < 12; k++) {
+                    const int e = tid + 256 * k;
+                    int64_t v = 0;
+#pragma unroll
+                    for (int w = 0; w < 4; w++)
+                        v += (int64_t)red[(w * 3 + e / 1024) * 1024 + (e & 1023)] *
+                             ((int64_t)1 << (8 * (l3 ? l : w / Q)));
+                    tot[L3 ? t0 / 3 : 0][k] = pass == 0 ? v : tot[L3 ? t0 / 3 : 0][k] + v;
+                }
+            } else {
+                for (int e = tid; e < 3 * 1024; e += 256) {
+                    const int tt = e >> 10, co = co0 + ((e >> 4) & 63), ci = ci0 + (e & 15);
+                    int64_t v = 0;
+#pragma unroll
+                    for (int w = 0; w < 4; w++)
+                        v += (int64_t)red[(w * 3 + tt) * 1024 + (e & 1023)] * ((int64_t)1 << (8 * (w / Q)));
+                    if (co < p.co && ci < p.ci_out)
+                        p.out[(((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci_out + ci] = v;
+                }
             }
             __syncthreads();
         }
+    }
+    if (L3) {
+#pragma unroll
+        for (int t0 = 0; t0 < 9; t0 += 3)
+#pragma unroll
+            for (int k = 0; k < 12; k++) {
+                const int e = tid + 256 * k;
+                const int tt = e >> 10, co = co0 + ((e >> 4) & 63), ci = ci0 + (e & 15);
+                if (co < p.co && ci < p.ci_out)
+                    p.out[(((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci_out + ci] = tot[L3 ? t0 / 3 : 0][k];
+            }
     }
     ts_end(p.ts);
 }
@@ -478,8 +515,11 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
     const size_t lds_stage = (size_t)4 * 2 * DWP_WIN * 16, lds_red = (size_t)4 * 3 * 1024 * 4;
     const unsigned nwg = (unsigned)(pl.tiles_co * pl.tiles_ci * pl.nsplit);
     a.ts = timer_slot(TIMED_DW);
-    hipLaunchKernelGGL(k_conv_dw_planes, dim3(nwg), dim3(256), lds_stage > lds_red ? lds_stage : lds_red,
-                       s, a);
+    const size_t lds = lds_stage > lds_red ? lds_stage : lds_red;
+    if (pl.chunk >= DWP_L3_MIN)
+        hipLaunchKernelGGL(k_conv_dw_planes<true>, dim3(nwg), dim3(256), lds, s, a);
+    else
+        hipLaunchKernelGGL(k_conv_dw_planes<false>, dim3(nwg), dim3(256), lds, s, a);
     if (pl.nsplit > 1) launch_sum_partials(s, part, pl.nsplit, (int64_t)sh.co * 9 * sh.c, dw);
 }
 

@@ -210,10 +210,11 @@ def test_conv_block_pooled_g(ctx, tile, case, modes):
         ctx.set_conv_tile(0)
 
 
-# weight gradients on channel-tile waves (four 16-channel input tiles per workgroup, 64 output
-# channels x 4 tile groups >= 16 tiles): g in 1 to 4 limbs, one K split (dW written directly) and
-# two (int64 partials), a partial output-channel tile with C_in % 16 != 0, pooled and not
-CHANNEL_WAVE_CASES = [
+# weight gradients of wide layers (256 to 512 output channels, 64-channel tiles x 16-channel input
+# tiles): g in 1 to 4 limbs, one K split (dW written directly) and several (int64 partials), a
+# partial output-channel tile with C_in % 16 != 0, pooled and not; the last two cases have at
+# least 32 super-steps per workgroup, where g in 3 limbs takes all four waves of a workgroup
+WIDE_DW_CASES = [
     # n, h, w, chans, pool, dmax
     (2, 6, 6, [256, 256], False, 100),
     (2, 6, 6, [256, 256], True, 5000),
@@ -221,11 +222,13 @@ CHANNEL_WAVE_CASES = [
     (1, 4, 4, [256, 256], False, 1 << 24),
     (1, 4, 4, [250, 272], False, 1 << 15),
     (8, 16, 16, [256, 256], True, 5000),
+    (16, 32, 32, [256, 512], False, 1 << 15),
+    (16, 32, 32, [256, 512], False, 5000),
 ]
 
 
-@pytest.mark.parametrize("case", CHANNEL_WAVE_CASES)
-def test_conv_block_channel_waves(ctx, case):
+@pytest.mark.parametrize("case", WIDE_DW_CASES)
+def test_conv_block_wide_weight_gradient(ctx, case):
     n, h, w, chans, pool, dmax = case
     rng = np.random.default_rng(hash((n, h, w, tuple(chans), dmax, 4242)) % (1 << 31))
     run_block(ctx, rng, n, h, w, chans, pool, 0, 10, N.ROUND_FLOOR, O.FLOOR, dmax=dmax)
