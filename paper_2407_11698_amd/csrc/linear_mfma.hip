@@ -46,10 +46,11 @@ constexpr int LG_LS = LG_KC + 16;         // LDS row stride: 16 rows of a fragme
 constexpr int LG_SA = LG_BM * LG_LS;      // one A limb plane of a chunk
 constexpr int LG_SB = LG_BN * LG_LS;      // one B limb plane
 
-// A workgroup: a 128 x 64 tile of C over its K range, in chunks of 128. Every limb plane of both
-// operands for a chunk is staged in LDS at once (one load round per chunk, the next chunk's loads
-// issued before this one's MFMAs), then each limb pair (la, lb) runs its two K-steps from LDS
-// and is folded into int64 with its weight 256^(la + lb).
+// A workgroup: a 128 x 64 tile of C over its K range, in chunks of 128. The limb planes of both
+// operands for a chunk are staged in LDS two per operand at a time (one load round for the
+// usual one or two limbs; 55 KiB of LDS, two workgroups per CU), the next round's loads issued
+// before this one's MFMAs; each limb pair (la, lb) runs its two K-steps from LDS and is folded
+// into int64 with its weight 256^(la + lb).
 template <int MODE>
 __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
 {
@@ -58,7 +59,7 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     constexpr int AU = LG_BM * (LG_KC / 16) / 256, BU = LG_BN * (LG_KC / 16) / 256;  // units/thread
     constexpr int DS = LG_BN + 1;                 // epilogue int32-tile row stride
     constexpr int SMEM_EPI = MODE == LIN_UNPOOL ? LG_BM * DS * 4 : 0;
-    constexpr int SMEM_OP = 4 * LG_SA + 4 * LG_SB;
+    constexpr int SMEM_OP = 2 * LG_SA + 2 * LG_SB;
     constexpr int SMEM = SMEM_OP > SMEM_EPI ? SMEM_OP : SMEM_EPI;
     __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
 
@@ -68,47 +69,49 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     const int kb = blockIdx.z * p.kchunk;
     const int ke = kb + p.kchunk < p.K ? kb + p.kchunk : p.K;
     const int nck = (ke - kb + LG_KC - 1) / LG_KC;
-    uint8_t *As = smem, *Bs = smem + 4 * LG_SA;
+    uint8_t *As = smem, *Bs = smem + 2 * LG_SA;
 
-    // unit u of a thread: row (tid >> 3) + 32 u, 16-byte column tid & 7. Limb plane 0 (always
-    // used) of the first chunk is requested before the limb counts are known; planes 1-3 of a
-    // chunk only when used.
+    // unit u of a thread: row (tid >> 3) + 32 u, 16-byte column tid & 7. Round r = (chunk, A
+    // plane pair, B plane pair); limb plane 0 of the first round is requested before the limb
+    // counts are known.
     const int ur = tid >> 3, uc = (tid & 7) * 16;
-    v4i ar[4][AU], br[4][BU];
-    int LA = 1, LB = 1;
-    auto load = [&](int ck, int l0, int l1) {
+    v4i ar[2][AU], br[2][BU];
+    int LA = 1, LB = 1, NA = 1, NB = 1;
+    auto load = [&](int r, int lmin) {
+        const int ck = r / (NA * NB), pa = (r / NB) % NA, pb = r % NB;
         const int k = kb + ck * LG_KC + uc;
         const bool kin = k < ke;
 #pragma unroll
-        for (int l = 0; l < 4; l++) {
-            if (l < l0 || l >= l1) continue;
-            if (l < LA) {
-                const int8_t *apl = p.a + l * p.aplane;
+        for (int h = 0; h < 2; h++) {
+            const int la = 2 * pa + h, lb = 2 * pb + h;
+            if (la >= lmin && la < LA) {
+                const int8_t *apl = p.a + la * p.aplane;
 #pragma unroll
                 for (int u = 0; u < AU; u++) {
                     const int m = m0 + ur + 32 * u;
-                    ar[l][u] = kin && m < p.M ? *(const v4i *)(apl + (int64_t)m * p.lda + k) : v4i{0, 0, 0, 0};
+                    ar[h][u] = kin && m < p.M ? *(const v4i *)(apl + (int64_t)m * p.lda + k) : v4i{0, 0, 0, 0};
                 }
             }
-            if (l < LB) {
-                const int8_t *bpl = p.b + l * p.bplane;
+            if (lb >= lmin && lb < LB) {
+                const int8_t *bpl = p.b + lb * p.bplane;
 #pragma unroll
                 for (int u = 0; u < BU; u++) {
                     const int nn = n0 + ur + 32 * u;
-                    br[l][u] = kin && nn < p.N ? *(const v4i *)(bpl + (int64_t)nn * p.ldb + k) : v4i{0, 0, 0, 0};
+                    br[h][u] = kin && nn < p.N ? *(const v4i *)(bpl + (int64_t)nn * p.ldb + k) : v4i{0, 0, 0, 0};
                 }
             }
         }
     };
-    auto store = [&]() {
+    auto store = [&](int r) {
+        const int pa = (r / NB) % NA, pb = r % NB;
 #pragma unroll
-        for (int l = 0; l < 4; l++) {
-            if (l < LA)
+        for (int h = 0; h < 2; h++) {
+            if (2 * pa + h < LA)
 #pragma unroll
-                for (int u = 0; u < AU; u++) *(v4i *)(As + l * LG_SA + (ur + 32 * u) * LG_LS + uc) = ar[l][u];
-            if (l < LB)
+                for (int u = 0; u < AU; u++) *(v4i *)(As + h * LG_SA + (ur + 32 * u) * LG_LS + uc) = ar[h][u];
+            if (2 * pb + h < LB)
 #pragma unroll
-                for (int u = 0; u < BU; u++) *(v4i *)(Bs + l * LG_SB + (ur + 32 * u) * LG_LS + uc) = br[l][u];
+                for (int u = 0; u < BU; u++) *(v4i *)(Bs + h * LG_SB + (ur + 32 * u) * LG_LS + uc) = br[h][u];
         }
     };
 
@@ -120,14 +123,17 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
 #pragma unroll
             for (int t = 0; t < 4; t++) acc64[i][j][t] = 0;
 
-    if (nck > 0) load(0, 0, 1);
+    if (nck > 0) load(0, 0);                     // (LA = LB = 1: plane 0 only)
     LA = p.a_max ? limbs_for(slot_read(p.a_max)) : 1;
     LB = p.b_max ? limbs_for(slot_read(p.b_max)) : 1;
     if (LA > 4 || LB > 4) {
         if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
         return;
     }
-    if (nck > 0) load(0, 1, 4);
+    NA = (LA + 1) / 2;
+    NB = (LB + 1) / 2;
+    const int nr = nck * NA * NB;
+    if (nck > 0) load(0, 1);
     // (LIN_UNPOOL: the epilogue's region codes, requested now)
     constexpr int EIT = MODE == LIN_UNPOOL ? LG_BM * (LG_BN / 16) / 256 : 1;
     v4i cdp[EIT];
@@ -139,14 +145,15 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
             cdp[q] = m < p.M && col < p.N ? *(const v4i *)(p.code + (int64_t)m * p.N + col) : v4i{0, 0, 0, 0};
         }
     }
-    for (int ck = 0; ck < nck; ck++) {
-        __syncthreads();                          // every wave is done with the previous chunk
-        store();
+    for (int r = 0; r < nr; r++) {
+        __syncthreads();                          // every wave is done with the previous round
+        store(r);
         __syncthreads();
-        if (ck + 1 < nck) load(ck + 1, 0, 4);
-        for (int la = 0; la < LA; la++) {
-            for (int lb = 0; lb < LB; lb++) {
-                const uint8_t *Ap = As + la * LG_SA, *Bp = Bs + lb * LG_SB;
+        if (r + 1 < nr) load(r + 1, 0);
+        const int pa = (r / NB) % NA, pb = r % NB;
+        for (int ha = 0; ha < 2 && 2 * pa + ha < LA; ha++) {
+            for (int hb = 0; hb < 2 && 2 * pb + hb < LB; hb++) {
+                const uint8_t *Ap = As + ha * LG_SA, *Bp = Bs + hb * LG_SB;
                 v4i acc[TM][TN];
 #pragma unroll
                 for (int i = 0; i < TM; i++)
@@ -167,7 +174,7 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
                         for (int j = 0; j < TN; j++)
                             acc[i][j] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[i], bf[j], acc[i][j], 0, 0, 0);
                 }
-                const int sh = 8 * (la + lb);
+                const int sh = 8 * (2 * pa + ha + 2 * pb + hb);
 #pragma unroll
                 for (int i = 0; i < TM; i++)
 #pragma unroll
