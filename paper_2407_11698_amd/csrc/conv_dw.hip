@@ -117,13 +117,12 @@ __device__ inline int padded_pixel(int k, int n, int h, int w, int hp, int wp)
 // ---------------------------------------------------------------------------------------------
 // x int8 NHWC [P][C] -> xr [C16 / 16][xs][16]: row HMAX + k holds the 16 channels of tile t at
 // padded position k (zeros at pad positions, in the halo and in channels C..C16-1). One thread:
-// one 16-byte row.
-__global__ __launch_bounds__(256) void k_dwp_act_rows(const int8_t *__restrict__ x, int n, int h,
-                                                      int w, int c, int hp, int wp, int xs,
-                                                      int8_t *__restrict__ xr)
+// one 16-byte row (workgroup (bx, by): rows 256 bx .., tile by).
+__device__ void dwp_act_rows(const int8_t *__restrict__ x, int n, int h, int w, int c, int hp,
+                             int wp, int xs, int8_t *__restrict__ xr, int bx, int by)
 {
-    const int i = blockIdx.x * 256 + threadIdx.x;     // row within the tile's block
-    const int t = blockIdx.y;                         // 16-channel tile
+    const int i = bx * 256 + threadIdx.x;             // row within the tile's block
+    const int t = by;                                 // 16-channel tile
     if (i >= xs) return;
     const int pix = padded_pixel(i - DWP_HMAX, n, h, w, hp, wp);
     const int ch = 16 * t;
@@ -141,13 +140,13 @@ __global__ __launch_bounds__(256) void k_dwp_act_rows(const int8_t *__restrict__
 
 // Zeros in the pad rows of xr (the halos, the column after every image row, the row after every
 // image, the tail): the rows of the real pixels were written by the previous layer's forward.
-// One thread: one pad position of one 16-channel tile.
-__global__ __launch_bounds__(256) void k_dwp_pad_rows(int n, int h, int w, int hp, int wp,
-                                                      int64_t kraw, int64_t xs,
-                                                      int8_t *__restrict__ xr)
+// One thread: one pad position of one 16-channel tile (workgroup (bx, by): positions 256 bx ..,
+// tile by).
+__device__ void dwp_pad_rows(int n, int h, int w, int hp, int wp, int64_t kraw, int64_t xs,
+                             int8_t *__restrict__ xr, int bx, int by)
 {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int t = blockIdx.y;
+    const int64_t i = (int64_t)bx * 256 + threadIdx.x;
+    const int t = by;
     const int64_t inner = (int64_t)n * (h + w + 1);
     int64_t row;
     if (i < inner) {
@@ -170,20 +169,19 @@ __global__ __launch_bounds__(256) void k_dwp_pad_rows(int n, int h, int w, int h
 // operand of the input-gradient GEMM). A workgroup: 64 positions x 64 channels, transposed
 // through LDS. With pcode, g holds a 2x2-pooled layer's gradient at the pooled positions only,
 // [n][h/2][w/2][C]: pixel (y, x) takes it where the pool's argmax (the code's low 2 bits) is
-// window position 2 (y & 1) + (x & 1), and zero elsewhere.
-__global__ __launch_bounds__(256) void k_dwp_grad_planes(const int32_t *__restrict__ g, int n,
-                                                         int h, int w, int c, int hp, int wp,
-                                                         int kp, const uint32_t *gmax,
-                                                         const uint8_t *__restrict__ pcode,
-                                                         int8_t *__restrict__ gp,
-                                                         int8_t *__restrict__ gn)
+// window position 2 (y & 1) + (x & 1), and zero elsewhere. Workgroup (bx, by): positions
+// 64 bx .., channels 64 by ...
+__device__ void dwp_grad_planes(const int32_t *__restrict__ g, int n, int h, int w, int c, int hp,
+                                int wp, int kp, const uint32_t *gmax,
+                                const uint8_t *__restrict__ pcode, int8_t *__restrict__ gp,
+                                int8_t *__restrict__ gn, int bx, int by)
 {
     __shared__ int32_t T[64][65];        // [position][channel]
     const int LA = limbs_for(slot_read(gmax));
     if (LA > 4) return;                  // the weight-gradient kernel flags it
     const int tid = threadIdx.x;
-    const int k0 = blockIdx.x * 64;
-    const int c0 = blockIdx.y * 64;
+    const int k0 = bx * 64;
+    const int c0 = by * 64;
     {
         const int pi = tid >> 2, cq = tid & 3;
         const int pix = padded_pixel(k0 + pi, n, h, w, hp, wp);
@@ -249,6 +247,37 @@ __global__ __launch_bounds__(256) void k_dwp_grad_planes(const int32_t *__restri
                      256 * pq + 16 * (co & 15)) = o;
         }
     }
+}
+
+// The two independent preparations of a weight-gradient launch in one launch: workgroups
+// 0 .. rows_gx rows_gy - 1 write x's rows (or zero their pad positions), the rest g's planes.
+struct DwpPrep {
+    int rows;                    // 1: x rows from x; 2: zeros at the pad positions of rows
+                                 //    written by the previous layer's forward
+    int rows_gx, rows_gy, gp_gx;
+    const int8_t *x;
+    int n, h, w, c, co, hp, wp, kp;
+    int64_t kraw, xs;
+    int8_t *xr;
+    const int32_t *g;
+    const uint32_t *gmax;
+    const uint8_t *pcode;
+    int8_t *gp, *gn;
+};
+
+__global__ __launch_bounds__(256) void k_dwp_prep(DwpPrep a)
+{
+    const int nrows = a.rows_gx * a.rows_gy;
+    const int b = blockIdx.x;
+    if (b < nrows) {
+        const int bx = b % a.rows_gx, by = b / a.rows_gx;
+        if (a.rows == 1) dwp_act_rows(a.x, a.n, a.h, a.w, a.c, a.hp, a.wp, (int)a.xs, a.xr, bx, by);
+        else dwp_pad_rows(a.n, a.h, a.w, a.hp, a.wp, a.kraw, a.xs, a.xr, bx, by);
+        return;
+    }
+    const int q = b - nrows;
+    dwp_grad_planes(a.g, a.n, a.h, a.w, a.co, a.hp, a.wp, a.kp, a.gmax, a.pcode, a.gp, a.gn,
+                    q % a.gp_gx, q / a.gp_gx);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -493,17 +522,19 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
     const DwpGeom ge = dwp_geom(sh);
     const DwpPlan pl = dwp_plan(sh);
     const int c16 = dwp_c16(sh);
-    if (x_rows_ready) {
+    {
+        DwpPrep pa{};
+        pa.rows = x_rows_ready ? 2 : 1;
         const int64_t pads = (int64_t)sh.n * (sh.h + sh.w + 1) + DWP_HMAX + (ge.xs - DWP_HMAX - ge.kraw);
-        hipLaunchKernelGGL(k_dwp_pad_rows, dim3((unsigned)((pads + 255) / 256), (unsigned)(c16 / 16)),
-                           dim3(256), 0, s, sh.n, sh.h, sh.w, ge.hp, ge.wp, ge.kraw, ge.xs, xp);
-    } else {
-        hipLaunchKernelGGL(k_dwp_act_rows, dim3((unsigned)((ge.xs + 255) / 256), (unsigned)(c16 / 16)),
-                           dim3(256), 0, s, x, sh.n, sh.h, sh.w, sh.c, ge.hp, ge.wp, (int)ge.xs, xp);
+        pa.rows_gx = (int)(((x_rows_ready ? pads : ge.xs) + 255) / 256);
+        pa.rows_gy = c16 / 16;
+        pa.gp_gx = (int)(ge.kp / 64);
+        pa.x = x; pa.n = sh.n; pa.h = sh.h; pa.w = sh.w; pa.c = sh.c; pa.co = sh.co;
+        pa.hp = ge.hp; pa.wp = ge.wp; pa.kp = (int)ge.kp; pa.kraw = ge.kraw; pa.xs = ge.xs; pa.xr = xp;
+        pa.g = g; pa.gmax = gmax; pa.pcode = pool_code; pa.gp = gp; pa.gn = gn;
+        const int64_t nwg = (int64_t)pa.rows_gx * pa.rows_gy + (int64_t)pa.gp_gx * ((sh.co + 63) / 64);
+        hipLaunchKernelGGL(k_dwp_prep, dim3((unsigned)nwg), dim3(256), 0, s, pa);
     }
-    hipLaunchKernelGGL(k_dwp_grad_planes, dim3((unsigned)(ge.kp / 64), (unsigned)((sh.co + 63) / 64)),
-                       dim3(256), 0, s, g, sh.n, sh.h, sh.w, sh.co, ge.hp, ge.wp, (int)ge.kp, gmax,
-                       pool_code, gp, gn);
     DwpArgs a{};
     a.gp = gp; a.kp = ge.kp;
     a.xr = xp; a.xs = ge.xs;

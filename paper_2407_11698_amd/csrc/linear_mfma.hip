@@ -51,22 +51,22 @@ constexpr int LG_SB = LG_BN * LG_LS;      // one B limb plane
 // usual one or two limbs; 55 KiB of LDS, two workgroups per CU), the next round's loads issued
 // before this one's MFMAs; each limb pair (la, lb) runs its two K-steps from LDS and is folded
 // into int64 with its weight 256^(la + lb).
+constexpr int LG_DS = LG_BN + 1;               // LIN_UNPOOL epilogue: int32-tile row stride
+constexpr int LG_SMEM = 2 * LG_SA + 2 * LG_SB > LG_BM * LG_DS * 4 ? 2 * LG_SA + 2 * LG_SB : LG_BM * LG_DS * 4;
+
+// One workgroup's tile (bx, by) of split bz; smem: LG_SMEM bytes.
 template <int MODE>
-__global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
+__device__ void lgemm_tile(const LgemmArgs &p, uint8_t *smem, int bx, int by, int bz)
 {
     constexpr int WM = LG_BM / 2, WN = LG_BN / 2;
     constexpr int TM = WM / 16, TN = WN / 16;
     constexpr int AU = LG_BM * (LG_KC / 16) / 256, BU = LG_BN * (LG_KC / 16) / 256;  // units/thread
-    constexpr int DS = LG_BN + 1;                 // epilogue int32-tile row stride
-    constexpr int SMEM_EPI = MODE == LIN_UNPOOL ? LG_BM * DS * 4 : 0;
-    constexpr int SMEM_OP = 2 * LG_SA + 2 * LG_SB;
-    constexpr int SMEM = SMEM_OP > SMEM_EPI ? SMEM_OP : SMEM_EPI;
-    __shared__ __attribute__((aligned(16))) uint8_t smem[SMEM];
+    constexpr int DS = LG_DS;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int m0 = blockIdx.x * LG_BM, n0 = blockIdx.y * LG_BN;
-    const int kb = blockIdx.z * p.kchunk;
+    const int m0 = bx * LG_BM, n0 = by * LG_BN;
+    const int kb = bz * p.kchunk;
     const int ke = kb + p.kchunk < p.K ? kb + p.kchunk : p.K;
     const int nck = (ke - kb + LG_KC - 1) / LG_KC;
     uint8_t *As = smem, *Bs = smem + 2 * LG_SA;
@@ -197,7 +197,7 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
                     const int col = n0 + wn * WN + j * 16 + (lane & 15);
                     if (m >= p.M || col >= p.N) continue;
                     const int64_t v = acc64[i][j][t];
-                    if (MODE == LIN_PART) p.out64[((int64_t)blockIdx.z * p.M + m) * p.N + col] = v;
+                    if (MODE == LIN_PART) p.out64[((int64_t)bz * p.M + m) * p.N + col] = v;
                     else if (m < p.m_valid) p.out64[(int64_t)m * p.ldc + col] = v;
                 }
         return;
@@ -280,13 +280,6 @@ __global__ __launch_bounds__(256) void k_lgemm(LgemmArgs p)
     block_slot_max(p.gmax, mx);
 }
 
-template <int MODE>
-static void launch_lgemm(hipStream_t s, const LgemmArgs &a, int splits)
-{
-    dim3 grid((unsigned)((a.M + LG_BM - 1) / LG_BM), (unsigned)((a.N + LG_BN - 1) / LG_BN),
-              (unsigned)splits);
-    hipLaunchKernelGGL((k_lgemm<MODE>), grid, dim3(256), 0, s, a);
-}
 
 // ---------------------------------------------------------------------------------------------
 // Learning weights W [G][d] int32 -> limb planes [4][G][d] and [4][d][gp] (zero rows g >= G);
@@ -315,12 +308,13 @@ __global__ void k_pack_learning_weights(const int32_t *__restrict__ w, uint32_t 
     block_slot_max(wmax, m);
 }
 
-// f [n][d] int8 -> fT [d][np] (zero columns n >= N): 64 x 64 tiles through LDS.
-__global__ __launch_bounds__(256) void k_transpose_i8(const int8_t *__restrict__ f, int N, int d,
-                                                      int np, int8_t *__restrict__ ft)
+// f [n][d] int8 -> fT [d][np] (zero columns n >= N): 64 x 64 tiles through LDS, tile (bx, by)
+// = features 64 bx .., samples 64 by ...
+__device__ void transpose_i8_tile(const int8_t *__restrict__ f, int N, int d, int np,
+                                  int8_t *__restrict__ ft, int bx, int by)
 {
     __shared__ int8_t t[64][65];
-    const int n0 = blockIdx.y * 64, k0 = blockIdx.x * 64;
+    const int n0 = by * 64, k0 = bx * 64;
     for (int e = threadIdx.x; e < 64 * 64; e += 256) {
         const int r = e / 64, c = e % 64;                 // r: sample, c: feature
         t[r][c] = (n0 + r < N && k0 + c < d) ? f[(int64_t)(n0 + r) * d + k0 + c] : 0;
@@ -330,6 +324,38 @@ __global__ __launch_bounds__(256) void k_transpose_i8(const int8_t *__restrict__
         const int r = e / 64, c = e % 64;                 // r: feature, c: sample
         if (k0 + r < d && n0 + c < np) ft[(int64_t)(k0 + r) * np + n0 + c] = t[c][r];
     }
+}
+
+// Forward of the learning layer in one launch: workgroups 0 .. tgx tgy - 1 transpose f (for the
+// weight gradient), the rest compute the split-K partial tiles (x fastest, then y, then split).
+__global__ __launch_bounds__(256) void k_lgemm_fwd(LgemmArgs p, const int8_t *f, int N, int d, int np,
+                                                   int8_t *ft, int tgx, int tgy)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t smem[LG_SMEM];
+    const int b = blockIdx.x;
+    if (b < tgx * tgy) {
+        transpose_i8_tile(f, N, d, np, ft, b % tgx, b / tgx);
+        return;
+    }
+    const int q = b - tgx * tgy;
+    const int gx = (p.M + LG_BM - 1) / LG_BM, gy = (p.N + LG_BN - 1) / LG_BN;
+    lgemm_tile<LIN_PART>(p, smem, q % gx, (q / gx) % gy, q / (gx * gy));
+}
+
+// Backward of the learning layer in one launch (both read e only): workgroups 0 .. ndw - 1 the
+// weight-gradient tiles, the rest delta's (with the un-pool and ReLU' epilogue).
+__global__ __launch_bounds__(256) void k_lgemm_bwd(LgemmArgs dw, LgemmArgs up)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t smem[LG_SMEM];
+    const int dgx = (dw.M + LG_BM - 1) / LG_BM, dgy = (dw.N + LG_BN - 1) / LG_BN;
+    const int b = blockIdx.x;
+    if (b < dgx * dgy) {
+        lgemm_tile<LIN_DW>(dw, smem, b % dgx, b / dgx, 0);
+        return;
+    }
+    const int q = b - dgx * dgy;
+    const int ugx = (up.M + LG_BM - 1) / LG_BM;
+    lgemm_tile<LIN_UNPOOL>(up, smem, q % ugx, q / ugx, 0);
 }
 
 // yhat and e from the split-K partial sums; also e padded to [n][gp] and transposed to [gp][np]
@@ -427,9 +453,7 @@ void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *
     // operands: learning-weight limb planes (unless the caller packed them), the transposed
     // block output
     if (!prepacked) launch_pack_matrix(s, w, G, (int)d, sc.gp, b.wf, b.wt, b.wmax);
-    hipLaunchKernelGGL(k_transpose_i8, dim3((unsigned)((d + 63) / 64), (unsigned)((sc.np + 63) / 64)),
-                       dim3(256), 0, s, f, n, (int)d, sc.np, b.ft);
-    // forward: split-K partials, then yhat / e
+    // forward: the transposed block output and the split-K partials (one launch), then yhat / e
     {
         LgemmArgs a{};
         a.M = n; a.N = G; a.K = (int)d;
@@ -438,25 +462,27 @@ void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *
         a.kchunk = (int)sc.kchunk;
         a.out64 = b.part;
         a.flags = flags;
-        launch_lgemm<LIN_PART>(s, a, sc.splits);
+        const int tgx = (int)((d + 63) / 64), tgy = (sc.np + 63) / 64;
+        const int64_t nwg = (int64_t)tgx * tgy + (int64_t)((n + LG_BM - 1) / LG_BM) * ((G + LG_BN - 1) / LG_BN) * sc.splits;
+        hipLaunchKernelGGL(k_lgemm_fwd, dim3((unsigned)nwg), dim3(256), 0, s, a, f, n, (int)d, sc.np, b.ft, tgx, tgy);
         hipLaunchKernelGGL(k_loss_from_partials, dim3(grid_stride_blocks((int64_t)sc.np * sc.gp, 256, 256)),
                            dim3(256), 0, s, b.part, sc.splits, n, G, sc.gp, sc.np, sf, labels, yhat,
                            e, b.epad, b.et, b.emax, flags);
     }
-    // weight gradient: dW[g][k] = sum_n e[n][g] f[n][k]   (M = gp, N = d, K = np)
+    // weight gradient dW[g][k] = sum_n e[n][g] f[n][k] (M = gp, N = d, K = np) and delta = e W
+    // (pre-update), routed through the pool and NITRO-ReLU backward into g: one launch
+    LgemmArgs da{}, ua{};
     {
-        LgemmArgs a{};
+        LgemmArgs &a = da;
         a.M = sc.gp; a.N = (int)d; a.K = sc.np;
         a.a = b.et; a.lda = sc.np; a.aplane = (int64_t)sc.gp * sc.np; a.a_max = b.emax;
         a.b = b.ft; a.ldb = sc.np; a.bplane = 0; a.b_max = nullptr;
         a.kchunk = sc.np;
         a.out64 = dw; a.ldc = d; a.m_valid = G;
         a.flags = flags;
-        launch_lgemm<LIN_DW>(s, a, 1);
     }
-    // delta = e W (pre-update), routed through the pool and NITRO-ReLU backward into g
     {
-        LgemmArgs a{};
+        LgemmArgs &a = ua;
         a.M = n; a.N = (int)d; a.K = sc.gp;
         a.a = b.epad; a.lda = sc.gp; a.aplane = (int64_t)sc.np * sc.gp; a.a_max = b.emax;
         a.b = b.wt; a.ldb = sc.gp; a.bplane = d * sc.gp; a.b_max = b.wmax;
@@ -465,8 +491,10 @@ void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *
         a.gpooled = pool && g_pooled ? 1 : 0;
         a.g = g; a.delta = delta_copy; a.gmax = b.gmax;
         a.flags = flags;
-        launch_lgemm<LIN_UNPOOL>(s, a, 1);
     }
+    const int64_t nwg = (int64_t)((da.M + LG_BM - 1) / LG_BM) * ((da.N + LG_BN - 1) / LG_BN) +
+                        (int64_t)((ua.M + LG_BM - 1) / LG_BM) * ((ua.N + LG_BN - 1) / LG_BN);
+    hipLaunchKernelGGL(k_lgemm_bwd, dim3((unsigned)nwg), dim3(256), 0, s, da, ua);
 }
 
 }  // namespace nitro
