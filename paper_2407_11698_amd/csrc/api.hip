@@ -260,7 +260,8 @@ static bool rows_from_forward(const BlockGeom &g)
 
 nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, const BlockGeom &g,
                                 const nitro_block_params *p, const int8_t *x, int8_t *a_out,
-                                void *state, bool zero_slots = true, bool prepacked = false)
+                                void *state, bool zero_slots = true, bool prepacked = false,
+                                bool x_prepadded = false)
 {
     hipStream_t s = ctx->stream;
     const Relu rp = make_relu(desc->alpha_inv, desc->round);
@@ -276,22 +277,25 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
         const Div sf = make_div(L.sf, desc->round);
         if (L.conv) {
             // limb planes for this call's forward and input-gradient GEMMs, and max|W_j| (the
-            // training iteration packs the tiled ones of every block in one launch first)
-            if (!L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c)) {
-                if (!prepacked)
+            // training iteration packs every block's in one launch first, prepacked)
+            if (!prepacked) {
+                if (!L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c))
                     launch_pack_conv_tiled(s, p->w[j], L.sh.co, L.sh.c, (int8_t *)at(state, g.wf[j]),
                                            (int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS);
-            } else
-                launch_pack_conv_weights(s, p->w[j], L.sh.co, L.sh.c, L.pad16 ? 16 : L.sh.c,
-                                         (int8_t *)at(state, g.wf[j]),
-                                         (int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS);
+                else
+                    launch_pack_conv_weights(s, p->w[j], L.sh.co, L.sh.c, L.pad16 ? 16 : L.sh.c,
+                                             (int8_t *)at(state, g.wf[j]),
+                                             (int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS);
+            }
             const int8_t *wf = (const int8_t *)at(state, g.wf[j]);
             uint32_t *wmax = slots + j * SLOT_WORDS;
             ConvShape sx = L.sh;
             const int8_t *xin = cur;
             if (L.pad16) {
+                // (x_prepadded: the block's input was padded by the iteration's first launch)
                 int8_t *xpad = (int8_t *)at(state, g.xpad);
-                launch_pad_channels16(s, cur, L.sh.n * L.sh.h * L.sh.w, L.sh.c, xpad);
+                if (!(j == 0 && x_prepadded))
+                    launch_pad_channels16(s, cur, L.sh.n * L.sh.h * L.sh.w, L.sh.c, xpad);
                 sx.c = 16;
                 xin = xpad;
             }
@@ -796,7 +800,16 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         sl.words = 16 * SLOT_WORDS;
         for (int b = 0; b < net->n_blocks; b++)
             sl.p[b] = (uint32_t *)at(at(workspace, g.state[b]), g.b[b].slots);
-        launch_zero_slots(ctx->stream, sl, net->n_blocks);
+        // (with them, block 0's input zero-padded to 16 channels where its first layer takes it so)
+        Pad16Args pad{};
+        const BlockGeom &b0 = g.b[0];
+        if (b0.L[0].conv && b0.L[0].pad16) {
+            pad.x = x;
+            pad.P = b0.L[0].sh.n * b0.L[0].sh.h * b0.L[0].sh.w;
+            pad.c = b0.L[0].sh.c;
+            pad.xpad = (int8_t *)at(at(workspace, g.state[0]), b0.xpad);
+        }
+        launch_zero_slots(ctx->stream, sl, net->n_blocks, &pad);
     }
     // limb planes (and max |W|) of the tiled conv layers' and the MFMA learning layers' weights
     // of every block, in one launch ahead of the forward pass
@@ -808,10 +821,15 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
             uint32_t *slots = (uint32_t *)at(state, bg.slots);
             for (int j = 0; j < bg.J; j++) {
                 const LayerGeom &L = bg.L[j];
-                if (L.conv && !L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c))
+                if (!L.conv) continue;
+                if (!L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c))
                     pl.add(ctx->stream,
                            pack_conv_args(params->w[b][j], L.sh.co, L.sh.c, (int8_t *)at(state, bg.wf[j]),
                                           (int8_t *)at(state, bg.wt[j]), slots + j * SLOT_WORDS), 9);
+                else
+                    pl.add_conv(ctx->stream, params->w[b][j], L.sh.co, L.sh.c, L.pad16 ? 16 : L.sh.c,
+                                (int8_t *)at(state, bg.wf[j]), (int8_t *)at(state, bg.wt[j]),
+                                slots + j * SLOT_WORDS);
             }
             if (net->block[b].n_classes > 0 && bg.lr_mfma) {
                 const LearningScratch sc = learning_scratch(net->block[b].n, bg.d, net->block[b].n_classes);
@@ -858,7 +876,7 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         bp.w_lr = params->w_lr[b];
         int8_t *aout = (int8_t *)at(workspace, g.aout[b]);
         st = block_forward_impl(ctx, &net->block[b], g.b[b], &bp, cur, aout, at(workspace, g.state[b]),
-                                false, true);
+                                false, true, b == 0);
         if (st != NITRO_OK) return st;
         cur = aout;
         if (b + 1 == net->n_blocks) break;

@@ -27,34 +27,13 @@ namespace nitro {
 __global__ void k_pack_conv_weights(const int32_t *__restrict__ w, uint32_t total, int ci,
                                     int cpad, int8_t *__restrict__ wf, uint32_t *wmax)
 {
-    uint32_t m = 0;
-    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
-        int32_t v;
-        if (cpad == ci) {
-            v = w[i];
-        } else {
-            const uint32_t c = i % (uint32_t)cpad, row = i / (uint32_t)cpad;
-            v = (int)c < ci ? w[row * ci + c] : 0;
-        }
-        const uint32_t a = abs_u32(v);
-        m = a > m ? a : m;
-#pragma unroll
-        for (int l = 0; l < 4; l++) wf[(int64_t)l * total + i] = limb1(v, l);
-    }
-    block_slot_max(wmax, m);
+    pack_conv_weights_part(w, total, ci, cpad, wf, wmax, blockIdx.x, gridDim.x);
 }
 
 __global__ void k_pack_conv_weights_t(const int32_t *__restrict__ w, uint32_t co, uint32_t ci,
                                       int8_t *__restrict__ wt)
 {
-    const uint32_t total = co * 9 * ci;
-    const uint32_t ti = blockIdx.x * blockDim.x + threadIdx.x;   // = (c * 9 + rs) * co + o
-    if (ti >= total) return;
-    const uint32_t o = ti % co, crs = ti / co;
-    const uint32_t rs = crs % 9, c = crs / 9;
-    const int32_t v = w[(o * 9 + rs) * ci + c];
-#pragma unroll
-    for (int l = 0; l < 4; l++) wt[(int64_t)l * total + ti] = limb1(v, l);
+    pack_conv_weights_t_part(w, co, ci, wt, blockIdx.x);
 }
 
 void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, int cpad,
@@ -75,12 +54,7 @@ void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, i
 __global__ __launch_bounds__(256) void k_pad_channels16(const int8_t *__restrict__ x, int P, int c,
                                                         int8_t *__restrict__ xpad)
 {
-    const int p = blockIdx.x * 256 + threadIdx.x;
-    if (p >= P) return;
-    v4i v = v4i{0, 0, 0, 0};
-    for (int e = 0; e < c; e++)
-        v[e >> 2] |= (int)((uint32_t)(uint8_t)x[(int64_t)p * c + e] << (8 * (e & 3)));
-    *(v4i *)(xpad + (int64_t)p * 16) = v;
+    pad_channels16_part(x, P, c, xpad, blockIdx.x);
 }
 
 void launch_pad_channels16(hipStream_t s, const int8_t *x, int P, int c, int8_t *xpad)

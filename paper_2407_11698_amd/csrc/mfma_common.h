@@ -46,4 +46,57 @@ __device__ inline void transpose4x4(uint32_t a0, uint32_t a1, uint32_t a2, uint3
     o3 = __builtin_amdgcn_perm(t3, t1, 0x07060302u);
 }
 
+// ---------------------------------------------------------------------------------------------
+// Bodies shared by the per-call kernels and the training iteration's batched launches.
+
+// Conv weight W int32 KRSC [co][3][3][ci] -> 4 limb planes of [co][9 cpad] (channels ci..cpad-1
+// zero), elements i = bid 256 + tid, stepping nb 256; max|W| into the slot wmax.
+__device__ inline void pack_conv_weights_part(const int32_t *__restrict__ w, uint32_t total, int ci,
+                                              int cpad, int8_t *__restrict__ wf, uint32_t *wmax,
+                                              uint32_t bid, uint32_t nb)
+{
+    uint32_t m = 0;
+    for (uint32_t i = bid * 256 + threadIdx.x; i < total; i += nb * 256) {
+        int32_t v;
+        if (cpad == ci) {
+            v = w[i];
+        } else {
+            const uint32_t c = i % (uint32_t)cpad, row = i / (uint32_t)cpad;
+            v = (int)c < ci ? w[row * ci + c] : 0;
+        }
+        const uint32_t a = abs_u32(v);
+        m = a > m ? a : m;
+#pragma unroll
+        for (int l = 0; l < 4; l++) wf[(int64_t)l * total + i] = limb1(v, l);
+    }
+    block_slot_max(wmax, m);
+}
+
+// The same weight's channel-swapped planes [ci][9 co] (input gradient), element
+// (c 9 + rs) co + o = bid 256 + tid.
+__device__ inline void pack_conv_weights_t_part(const int32_t *__restrict__ w, uint32_t co,
+                                                uint32_t ci, int8_t *__restrict__ wt, uint32_t bid)
+{
+    const uint32_t total = co * 9 * ci;
+    const uint32_t ti = bid * 256 + threadIdx.x;
+    if (ti >= total) return;
+    const uint32_t o = ti % co, crs = ti / co;
+    const uint32_t rs = crs % 9, c = crs / 9;
+    const int32_t v = w[(o * 9 + rs) * ci + c];
+#pragma unroll
+    for (int l = 0; l < 4; l++) wt[(int64_t)l * total + ti] = limb1(v, l);
+}
+
+// x int8 [P][c] -> [P][16] with zero channels c..15 (c < 16): pixel p = bid 256 + tid.
+__device__ inline void pad_channels16_part(const int8_t *__restrict__ x, int P, int c,
+                                           int8_t *__restrict__ xpad, int bid)
+{
+    const int p = bid * 256 + threadIdx.x;
+    if (p >= P) return;
+    v4i v = v4i{0, 0, 0, 0};
+    for (int e = 0; e < c; e++)
+        v[e >> 2] |= (int)((uint32_t)(uint8_t)x[(int64_t)p * c + e] << (8 * (e & 3)));
+    *(v4i *)(xpad + (int64_t)p * 16) = v;
+}
+
 }  // namespace nitro

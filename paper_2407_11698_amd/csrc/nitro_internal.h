@@ -588,16 +588,31 @@ PackArgs pack_conv_args(const int32_t *w, int co, int ci, int8_t *wf, int8_t *wt
 PackArgs pack_matrix_args(const int32_t *w, int R, int C, int Rpad, int8_t *p, int8_t *t,
                           uint32_t *wmax);
 constexpr int PACK_BATCH = 16;
+// Conv weights packed element-wise (C_in not a multiple of 16, or zero-padded to 16): the planes
+// of k_pack_conv_weights and k_pack_conv_weights_t as entries of a batched launch.
+constexpr int PACK_CONV = 4;
+struct ConvPackArgs {
+    const int32_t *w;
+    uint32_t co, ci, cpad;
+    int8_t *wf, *wt;
+    uint32_t *wmax;
+    int nf, nt;                    // workgroups of the plain and of the swapped planes
+};
 struct PackBatch {
     PackArgs t[PACK_BATCH];
     int gx[PACK_BATCH], gy[PACK_BATCH];
     int first[PACK_BATCH + 1];
     int n;
+    ConvPackArgs c[PACK_CONV];     // dealt the workgroups after first[n], in order
+    int nc;
 };
 // packs gathered on the host and enqueued as one launch (flushed when full)
 struct PackList {
     PackBatch b{};
     void add(hipStream_t s, const PackArgs &a, int batches);   // batches: 9 for a conv weight
+    // a conv weight packed element-wise (launch_pack_conv_weights' planes and max)
+    void add_conv(hipStream_t s, const int32_t *w, int co, int ci, int cpad, int8_t *wf, int8_t *wt,
+                  uint32_t *wmax);
     void flush(hipStream_t s);
 };
 void launch_pack_conv_tiled(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,
@@ -625,7 +640,14 @@ struct SlotList {
     uint32_t *p[NITRO_MAX_BLOCKS];
     int words;
 };
-void launch_zero_slots(hipStream_t s, const SlotList &l, int nblocks);
+// pad (optional): in the same launch, a network input zero-padded to 16 channels
+// (launch_pad_channels16).
+struct Pad16Args {
+    const int8_t *x;
+    int P, c;
+    int8_t *xpad;
+};
+void launch_zero_slots(hipStream_t s, const SlotList &l, int nblocks, const Pad16Args *pad = nullptr);
 
 // IntegerSGD (Alg. 1) in place.
 void launch_sgd(hipStream_t s, int32_t *w, const int64_t *dw, int64_t count, const Div &gamma,

@@ -68,11 +68,30 @@ __global__ __launch_bounds__(256) void k_pack_limbs(PackArgs a)
 }
 
 // Several packs in one launch: workgroups are dealt to the packs in order (first[k] ..
-// first[k+1]), each pack's tiles numbered column tile fastest, then row tile, then batch.
+// first[k+1]), each pack's tiles numbered column tile fastest, then row tile, then batch; then to
+// the element-wise conv packs (each: its plain planes' workgroups, then its swapped planes').
 __global__ __launch_bounds__(256) void k_pack_batch(PackBatch b)
 {
     __shared__ __attribute__((aligned(16))) uint8_t L[4][64][PACK_LS];
-    const int wid = blockIdx.x;
+    int wid = blockIdx.x;
+    if (wid >= b.first[b.n]) {
+        wid -= b.first[b.n];
+        for (int k = 0; k < b.nc; k++) {
+            const ConvPackArgs &c = b.c[k];
+            if (wid < c.nf) {
+                pack_conv_weights_part(c.w, c.co * 9 * c.cpad, (int)c.ci, (int)c.cpad, c.wf, c.wmax,
+                                       (uint32_t)wid, (uint32_t)c.nf);
+                return;
+            }
+            wid -= c.nf;
+            if (wid < c.nt) {
+                pack_conv_weights_t_part(c.w, c.co, c.ci, c.wt, (uint32_t)wid);
+                return;
+            }
+            wid -= c.nt;
+        }
+        return;
+    }
     int k = 0;
     while (k + 1 < b.n && wid >= b.first[k + 1]) k++;
     const int loc = wid - b.first[k];
@@ -94,11 +113,29 @@ void PackList::add(hipStream_t s, const PackArgs &a, int batches)
     b.n++;
 }
 
+void PackList::add_conv(hipStream_t s, const int32_t *w, int co, int ci, int cpad, int8_t *wf,
+                        int8_t *wt, uint32_t *wmax)
+{
+    if (b.nc == PACK_CONV) flush(s);
+    ConvPackArgs &c = b.c[b.nc++];
+    c.w = w;
+    c.co = (uint32_t)co;
+    c.ci = (uint32_t)ci;
+    c.cpad = (uint32_t)cpad;
+    c.wf = wf;
+    c.wt = wt;
+    c.wmax = wmax;
+    c.nf = grid_stride_blocks((int64_t)co * 9 * cpad);
+    c.nt = wt ? (int)(((int64_t)co * 9 * ci + 255) / 256) : 0;
+}
+
 void PackList::flush(hipStream_t s)
 {
-    if (b.n == 0) return;
-    hipLaunchKernelGGL(k_pack_batch, dim3((unsigned)b.first[b.n]), dim3(256), 0, s, b);
+    int64_t nwg = b.first[b.n];
+    for (int k = 0; k < b.nc; k++) nwg += b.c[k].nf + b.c[k].nt;
+    if (nwg > 0) hipLaunchKernelGGL(k_pack_batch, dim3((unsigned)nwg), dim3(256), 0, s, b);
     b.n = 0;
+    b.nc = 0;
     b.first[0] = 0;
 }
 
@@ -195,16 +232,25 @@ void launch_sgd_batch(hipStream_t s, SgdBatch b)
 }
 
 // ---------------------------------------------------------------------------------------------
-// Zero the max slots of several blocks (one workgroup per block).
-__global__ __launch_bounds__(256) void k_zero_slots(SlotList l)
+// Zero the max slots of several blocks (one workgroup per block); the workgroups after them pad
+// a network input to 16 channels (pad.P > 0).
+__global__ __launch_bounds__(256) void k_zero_slots(SlotList l, int nblocks, Pad16Args pad)
 {
+    if ((int)blockIdx.x >= nblocks) {
+        pad_channels16_part(pad.x, pad.P, pad.c, pad.xpad, (int)blockIdx.x - nblocks);
+        return;
+    }
     uint32_t *p = l.p[blockIdx.x];
     for (int i = threadIdx.x; i < l.words; i += 256) p[i] = 0;
 }
 
-void launch_zero_slots(hipStream_t s, const SlotList &l, int nblocks)
+void launch_zero_slots(hipStream_t s, const SlotList &l, int nblocks, const Pad16Args *pad)
 {
-    if (nblocks > 0) hipLaunchKernelGGL(k_zero_slots, dim3((unsigned)nblocks), dim3(256), 0, s, l);
+    Pad16Args pa{};
+    if (pad) pa = *pad;
+    const int npad = pa.P > 0 ? (pa.P + 255) / 256 : 0;
+    if (nblocks + npad > 0)
+        hipLaunchKernelGGL(k_zero_slots, dim3((unsigned)(nblocks + npad)), dim3(256), 0, s, l, nblocks, pa);
 }
 
 // ---------------------------------------------------------------------------------------------
