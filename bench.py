@@ -169,7 +169,18 @@ def cpu_baseline(wl, min_s: float = 12.0, budget_s: float = 25.0):
     return {"value": round(batch * steps / el, 3), "unit": "images/s", "cores": O.num_threads(),
             "kind": "oracle",
             "sample": "%d training iterations of the same workload at batch %d (%.1f s); "
-                      "host %s" % (steps, batch, el, platform.processor() or platform.machine())}
+                      "host %s" % (steps, batch, el, cpu_model())}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 def main():
@@ -187,6 +198,8 @@ def main():
     ap.add_argument("--stress-reps", type=int, default=10,
                     help="repeats of the single conv-layer stress case measured after the "
                          "training iterations (0 skips it)")
+    ap.add_argument("--mfma-probe-iters", type=int, default=20000,
+                    help="MFMAs per chain of the int8 matrix-core rate probe (0: skip it)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB before the warm-up: "
                          "the known-size reference for hardware byte counters")
@@ -254,6 +267,19 @@ def main():
     net.ctx.kernel_timing(False)
     timed_steps = 1 if graph else args.steps    # graph: the events of the last replay
 
+    # per-iteration times (median and min), after the timed region: events on the library's
+    # stream around each iteration of the same sequence
+    per_step = []
+    for i in range(args.steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        run(warmup + i, 1)
+        e1.record(stream)
+        per_step.append((e0, e1))
+    torch.cuda.synchronize()
+    step_ms = sorted(a.elapsed_time(b) for a, b in per_step)
+    net.ctx.sync()
+
     ops = conv_layer_ops(wl)
     per_class = {}
     for name, (ms, launches) in ktime.items():
@@ -293,6 +319,9 @@ def main():
         "steps": args.steps,
         "warmup": warmup,
         "ms_per_step": round(el * 1e3 / args.steps, 4),
+        "step_ms": {"median": round(step_ms[len(step_ms) // 2], 4), "min": round(step_ms[0], 4),
+                    "iterations": len(step_ms), "timing": "HIP events around each iteration, "
+                                                          "after the timed region"},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -319,6 +348,11 @@ def main():
             "achieved": sd["algorithmic_TOPs"] if sd else None,
             "frac": round(sd["algorithmic_TOPs"] / PEAK_INT8_TOPS, 5) if sd else None}
         out["conv_mfma"]["serial_per_kernel"] = serial
+    if args.mfma_probe_iters > 0:
+        # the dense int8 matrix-core rate on this GPU (register-only MFMA chains, two waves per
+        # SIMD); `peak` above stays the published figure
+        out["mfma_rate_probe"] = {"TOPs": round(net.ctx.mfma_rate(2, args.mfma_probe_iters), 1),
+                                  "waves_per_simd": 2, "published_TOPs": PEAK_INT8_TOPS}
     if args.stress_reps > 0:
         out["stress_conv"] = stress_layer(args.stress_reps)
     if not args.no_cpu_baseline:

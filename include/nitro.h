@@ -276,6 +276,16 @@ int32_t nitro_host_relu_mu(int32_t alpha_inv, int32_t round);
 nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable);
 nitro_status nitro_kernel_time(nitro_ctx *ctx, int32_t cls, double *ms, int64_t *launches);
 
+/* Rate probe of the int8 matrix cores, which states the dense peak that the conv kernels'
+ * throughput is priced against. One launch runs 8 independent v_mfma_i32_16x16x64_i8 chains per
+ * wave on operands held in registers (no memory traffic but one 4-byte store per thread at the
+ * end), with waves_per_simd (1..4) waves on every SIMD of every compute unit and iters (>= 1)
+ * MFMAs per chain, timed with HIP events on the context's stream after a short warm-up launch.
+ * *tops receives the rate achieved in 10^12 int8 ops per second (2 * 16 * 16 * 64 ops per MFMA).
+ * Synchronous. Allocates and frees a result buffer of 1 KiB per workgroup (ENOMEM); EINVAL for a
+ * null argument or a count out of range, EHIP for a failed launch or event. */
+nitro_status nitro_mfma_rate(nitro_ctx *ctx, int32_t waves_per_simd, int32_t iters, double *tops);
+
 #ifdef __cplusplus
 }
 #endif

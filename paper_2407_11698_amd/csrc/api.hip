@@ -1003,6 +1003,38 @@ nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable)
     return NITRO_OK;
 }
 
+nitro_status nitro_mfma_rate(nitro_ctx *ctx, int32_t waves_per_simd, int32_t iters, double *tops)
+{
+    if (!ctx || !tops || waves_per_simd < 1 || waves_per_simd > 4 || iters < 1) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, ctx->device) != hipSuccess ||
+        cus < 1)
+        return NITRO_EHIP;
+    // 4-wave workgroups, one wave per SIMD: waves_per_simd workgroups per compute unit
+    const int grid = cus * waves_per_simd;
+    int32_t *out = nullptr;
+    if (hipMalloc((void **)&out, (size_t)grid * 256 * sizeof(int32_t)) != hipSuccess) return NITRO_ENOMEM;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    nitro_status st = NITRO_OK;
+    float ms = 0.f;
+    if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) st = NITRO_EHIP;
+    if (st == NITRO_OK) {
+        launch_mfma_rate(ctx->stream, grid, iters < 64 ? iters : 64, out);     // warm-up (clocks)
+        if (hipEventRecord(e0, ctx->stream) != hipSuccess) st = NITRO_EHIP;
+        launch_mfma_rate(ctx->stream, grid, iters, out);
+        if (hipGetLastError() != hipSuccess || hipEventRecord(e1, ctx->stream) != hipSuccess ||
+            hipEventSynchronize(e1) != hipSuccess || hipEventElapsedTime(&ms, e0, e1) != hipSuccess ||
+            !(ms > 0.f))
+            st = NITRO_EHIP;
+    }
+    if (st == NITRO_OK) *tops = (double)mfma_rate_ops(grid, iters) / (ms * 1e-3) / 1e12;
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    (void)hipFree(out);
+    return st;
+}
+
 nitro_status nitro_kernel_time(nitro_ctx *ctx, int32_t cls, double *ms, int64_t *launches)
 {
     if (!ctx || cls < 0 || cls >= TIMED_CLASSES || !ms || !launches) return NITRO_EINVAL;

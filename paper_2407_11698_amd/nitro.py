@@ -104,6 +104,7 @@ def _load():
         "nitro_host_relu_mu": (I32, [I32, I32]),
         "nitro_kernel_timing": (I32, [VP, I32]),
         "nitro_kernel_time": (I32, [VP, I32, P(ctypes.c_double), P(I64)]),
+        "nitro_mfma_rate": (I32, [VP, I32, I32, P(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -123,7 +124,7 @@ EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_set_conv_
            "nitro_head_backward", "nitro_integer_sgd_step", "nitro_net_query",
            "nitro_net_block_output", "nitro_train_step", "nitro_train_step_graph",
            "nitro_host_div", "nitro_host_relu_mu",
-           "nitro_kernel_timing", "nitro_kernel_time")
+           "nitro_kernel_timing", "nitro_kernel_time", "nitro_mfma_rate")
 
 
 def status_str(code: int) -> str:
@@ -312,3 +313,9 @@ class Context:
         check(LIB.nitro_kernel_time(self.h, cls, ctypes.byref(ms), ctypes.byref(n)),
               "nitro_kernel_time")
         return ms.value, n.value
+
+    def mfma_rate(self, waves_per_simd: int = 2, iters: int = 20000) -> float:
+        """Dense int8 matrix-core rate in 10^12 ops/s, measured by a register-only probe."""
+        tops = ctypes.c_double(0)
+        check(LIB.nitro_mfma_rate(self.h, waves_per_simd, iters, ctypes.byref(tops)), "nitro_mfma_rate")
+        return tops.value
