@@ -7,6 +7,7 @@
 #include <vector>
 
 #include "nitro_internal.h"
+#include "probe.h"
 
 using namespace nitro;
 

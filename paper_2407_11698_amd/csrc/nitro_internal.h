@@ -636,11 +636,6 @@ struct SgdBatch {
     uint32_t *flags;
 };
 void launch_sgd_batch(hipStream_t s, SgdBatch b);
-
-// int8 matrix-core rate probe: `grid` workgroups of 4 waves, `iters` MFMAs per chain; the ops one
-// launch executes; out holds grid * 256 int32
-void launch_mfma_rate(hipStream_t s, int grid, int iters, int32_t *out);
-int64_t mfma_rate_ops(int grid, int iters);
 struct SlotList {
     uint32_t *p[NITRO_MAX_BLOCKS];
     int words;

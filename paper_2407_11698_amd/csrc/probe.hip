@@ -3,6 +3,7 @@
 // accumulator chains of v_mfma_i32_16x16x64_i8 on operands held in registers; the only memory
 // access is one 4-byte store per thread at the end, which keeps the chains live.
 #include "mfma_common.h"
+#include "probe.h"
 
 namespace nitro {
 
