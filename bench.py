@@ -269,6 +269,8 @@ def main():
 
     # per-iteration times (median and min), after the timed region: events on the library's
     # stream around each iteration of the same sequence
+    if graph:
+        run(warmup, 1)                    # the graph again, now captured without timing
     per_step = []
     for i in range(args.steps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

@@ -237,14 +237,17 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                               const nitro_net_params *params, void *workspace,
                               const int8_t *x, const int32_t *labels, const nitro_hparams *hp);
 
-/* nitro_train_step replayed from a HIP graph. The first call, and any call whose arguments
- * differ from the captured call's (compared by value: descriptors, parameter pointers,
- * workspace, x, labels, hyper-parameters, the context's stream and timing switch), captures one
- * iteration on the context's stream and instantiates it; every call then launches the graph.
- * The graph reads x and labels from the captured buffers, so a caller that changes the batch
- * writes it into the same buffers. The context's stream must not be the legacy default stream
- * (EINVAL). Capture errors return the error of the failing call or NITRO_EHIP. The context
- * keeps one graph; nitro_destroy releases it. */
+/* nitro_train_step replayed from a HIP graph. The context keeps up to 16 captured iterations,
+ * one per distinct key (compared by value: descriptors, parameter pointers, workspace, x,
+ * labels, hyper-parameters, the context's stream and settings, the timing switch). A call whose
+ * key has no graph captures one iteration on the context's stream and instantiates it (beyond
+ * 16, in place of the least recently replayed, after synchronising the stream); every call then
+ * launches its key's graph. A graph reads x and labels from the buffers it was captured with:
+ * a caller changes the batch by writing into those buffers, or by passing other resident
+ * buffers, which get graphs of their own (all of them share the one workspace, so replays run
+ * in stream order). The context's stream must not be the legacy default stream (EINVAL).
+ * Capture errors return the error of the failing call or NITRO_EHIP. nitro_kernel_timing and
+ * nitro_destroy release every graph (synchronising the stream first). */
 nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
                                     const nitro_net_params *params, void *workspace,
                                     const int8_t *x, const int32_t *labels, const nitro_hparams *hp);

@@ -30,9 +30,29 @@ struct nitro_ctx : public LaunchTimer {
     hipStream_t aux[NAUX] = {};
     hipEvent_t fev[NITRO_MAX_BLOCKS] = {}, join[NAUX] = {};   // block b's forward done; aux done
     bool aux_ready = false;
-    // the captured training iteration of nitro_train_step_graph and the arguments it holds
-    hipGraphExec_t gexec = nullptr;
-    std::vector<uint8_t> gkey;
+    // the captured training iterations of nitro_train_step_graph, one per distinct set of
+    // arguments and settings (its key), at most GCACHE; a new set replaces the least recently
+    // replayed
+    static constexpr int GCACHE = 16;
+    struct GraphEntry {
+        hipGraphExec_t exec = nullptr;
+        std::vector<uint8_t> key;
+        uint64_t last = 0;
+    };
+    GraphEntry graphs[GCACHE];
+    uint64_t gclock = 0;
+    // (a replay still in flight on the stream finishes before its graph is released)
+    void drop_graphs()
+    {
+        bool any = false;
+        for (auto &g : graphs) any |= g.exec != nullptr;
+        if (any) (void)hipStreamSynchronize(stream);
+        for (auto &g : graphs) {
+            if (g.exec) (void)hipGraphExecDestroy(g.exec);
+            g.exec = nullptr;
+            g.key.clear();
+        }
+    }
     // per-kernel timing: TS_CAP slots per class in tsbuf (allocated when timing is first
     // enabled); used[c] slots of class c assigned since the last reset. A graph captured with
     // timing keeps writing its slots on every replay (ts_graph).
@@ -602,7 +622,7 @@ void nitro_destroy(nitro_ctx *ctx)
     if (!ctx) return;
     DeviceGuard guard(ctx->device);
     (void)hipStreamSynchronize(ctx->stream);
-    if (ctx->gexec) (void)hipGraphExecDestroy(ctx->gexec);
+    ctx->drop_graphs();
     if (ctx->tsbuf) (void)hipFree(ctx->tsbuf);
     if (ctx->aux_ready) {
         for (int b = 0; b < nitro_ctx::NAUX; b++) {
@@ -956,11 +976,19 @@ nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
     put(&ctx->aux_use, sizeof(ctx->aux_use));
     put(&ctx->conv_tile, sizeof(ctx->conv_tile));
     put(&ctx->conv_persist, sizeof(ctx->conv_persist));
-    if (!ctx->gexec || key != ctx->gkey) {
-        if (ctx->gexec) {
-            (void)hipGraphExecDestroy(ctx->gexec);
-            ctx->gexec = nullptr;
+    nitro_ctx::GraphEntry *ge = nullptr;
+    for (auto &g : ctx->graphs)
+        if (g.exec && g.key == key) ge = &g;
+    if (!ge) {
+        ge = &ctx->graphs[0];
+        for (auto &g : ctx->graphs)
+            if (!g.exec || (ge->exec && g.last < ge->last)) ge = &g;
+        if (ge->exec) {
+            if (hipStreamSynchronize(ctx->stream) != hipSuccess) return NITRO_EHIP;
+            (void)hipGraphExecDestroy(ge->exec);
         }
+        ge->exec = nullptr;
+        ge->key.clear();
         nitro_status st = ctx->ensure_aux();
         if (st != NITRO_OK) return st;
         for (auto &u : ctx->used) u = 0;
@@ -970,17 +998,18 @@ nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
         hipGraph_t graph = nullptr;
         const hipError_t e = hipStreamEndCapture(ctx->stream, &graph);
         if (st == NITRO_OK && e != hipSuccess) st = NITRO_EHIP;
-        if (st == NITRO_OK && hipGraphInstantiate(&ctx->gexec, graph, nullptr, nullptr, 0) != hipSuccess) {
-            ctx->gexec = nullptr;
+        if (st == NITRO_OK && hipGraphInstantiate(&ge->exec, graph, nullptr, nullptr, 0) != hipSuccess) {
+            ge->exec = nullptr;
             st = NITRO_EHIP;
         }
         if (graph) (void)hipGraphDestroy(graph);
         (void)hipGetLastError();
         if (st != NITRO_OK) return st;
-        ctx->gkey = key;
+        ge->key = std::move(key);
         ctx->ts_graph = ctx->timing && ctx->tsbuf;
     }
-    if (hipGraphLaunch(ctx->gexec, ctx->stream) != hipSuccess) return NITRO_EHIP;
+    ge->last = ++ctx->gclock;
+    if (hipGraphLaunch(ge->exec, ctx->stream) != hipSuccess) return NITRO_EHIP;
     return NITRO_OK;
 }
 
@@ -988,6 +1017,8 @@ nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable)
 {
     if (!ctx) return NITRO_EINVAL;
     DeviceGuard guard(ctx->device);
+    // graphs captured before hold the timing state and slot assignment of their capture
+    ctx->drop_graphs();
     ctx->timing = enable != 0;
     if (ctx->timing) {
         const int64_t nslots = (int64_t)TIMED_CLASSES * nitro_ctx::TS_CAP;

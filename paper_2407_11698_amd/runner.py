@@ -67,8 +67,8 @@ class GpuNet:
         self.ctx.train_step(self.nd, self.params, self.workspace, x, y, self.hp)
 
     def step_graph(self, x: torch.Tensor, y: torch.Tensor) -> None:
-        """One iteration replayed from the context's captured graph (captured on the first call
-        with these buffers; x and y must keep their storage, only their contents change)."""
+        """One iteration replayed from the context's captured graph for these buffers (captured
+        on the first call with them; up to 16 buffer sets keep graphs of their own)."""
         self.ctx.train_step_graph(self.nd, self.params, self.workspace, x, y, self.hp)
 
     def block_output(self, b: int) -> torch.Tensor:

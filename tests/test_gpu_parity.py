@@ -408,12 +408,16 @@ def test_train_step_aux_streams(ctx, naux):
         assert np.array_equal(a, b)
 
 
-@pytest.mark.parametrize("wl", [WL.scaled(WL.SMALL_CNN, 16), WL.scaled(WL.VGG_CNN, 8)],
+@pytest.mark.parametrize("feed", ["copy", "resident"])
+@pytest.mark.parametrize("wl,nbuf", [(WL.scaled(WL.SMALL_CNN, 16), 18), (WL.scaled(WL.VGG_CNN, 8), 4)],
                          ids=["small_cnn_b16", "vgg_b8"])
-def test_train_step_graph_matches_eager(wl):
-    """nitro_train_step_graph replays a captured iteration: after every replay (with eager torch
+def test_train_step_graph_matches_eager(wl, nbuf, feed):
+    """nitro_train_step_graph replays captured iterations: after every replay (with eager torch
     work and host syncs in between) its weights and block outputs equal the eager path's, which
-    the oracle-parity tests pin. The batch changes by writing into the captured buffers."""
+    the oracle-parity tests pin. The batch changes by writing into the captured buffers (copy),
+    or by passing one of nbuf resident buffer sets, each replayed from a graph of its own
+    (resident; on the small network more sets than the context keeps graphs for, so that graphs
+    are replaced and captured again)."""
     import torch
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
@@ -424,13 +428,19 @@ def test_train_step_graph_matches_eager(wl):
         graph = runner.GpuNet(wl, dr.weights, ctx=gctx)
         xb = torch.empty_like(dev(dr.batches[0][0]))
         yb = torch.empty_like(dev(dr.batches[0][1]))
-        for s, (x, y) in enumerate(dr.batches * 2):
-            print("graph replay", wl.name, "step", s, flush=True)
-            xd, yd = dev(x), dev(y)
+        bufs = [(dev(dr.batches[k % 4][0]), dev(dr.batches[k % 4][1])) for k in range(nbuf)]
+        steps = 8 if feed == "copy" else 2 * nbuf
+        for s in range(steps):
+            k = s % nbuf if feed == "resident" else s % 4
+            print("graph replay", wl.name, feed, "step", s, "batch", k % 4, flush=True)
+            xd, yd = bufs[k] if feed == "resident" else (dev(dr.batches[k][0]), dev(dr.batches[k][1]))
             eager.step(xd, yd)
-            xb.copy_(xd)
-            yb.copy_(yd)
-            graph.step_graph(xb, yb)
+            if feed == "resident":
+                graph.step_graph(xd, yd)
+            else:
+                xb.copy_(xd)
+                yb.copy_(yd)
+                graph.step_graph(xb, yb)
             junk = torch.ones(1 << 16, device="cuda", dtype=torch.int32).cumsum(0)   # eager work
             torch.cuda.synchronize()
             gctx.sync()
