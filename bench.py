@@ -172,6 +172,44 @@ def cpu_baseline(wl, min_s: float = 12.0, budget_s: float = 25.0):
                       "host %s" % (steps, batch, el, cpu_model())}
 
 
+ONE_CORE_SRC = """
+import sys, time, json
+sys.path.insert(0, %r)
+from oracle import oracle as O
+from paper_2407_11698_amd import workloads as WL
+sample = WL.scaled(WL.SMALL_CNN, 16)
+dr = WL.draw_workload(sample, O.kaiming_bound, steps=sample.steps)
+hp = O.Hyper(sample.gamma_inv, sample.lambda_inv_fw, sample.lambda_inv_lr, sample.alpha_inv,
+             sample.n_classes)
+net = O.OracleNet([(len(b.layers), b.maxpool, b.learning) for b in sample.blocks], sample.head,
+                  dr.weights, hp)
+t0 = time.perf_counter(); steps = 0
+while True:
+    net.train_step(*dr.batches[steps %% len(dr.batches)]); steps += 1
+    el = time.perf_counter() - t0
+    if el >= %f:
+        break
+print(json.dumps({"steps": steps, "seconds": el, "threads": O.num_threads()}))
+"""
+
+
+def cpu_baseline_one_core(min_s: float = 5.0):
+    """The CPU oracle on one core (a child process with OMP_NUM_THREADS=1, started before this
+    process touches the GPU): training iterations of the three-block CIFAR-shaped CNN at batch
+    16, for at least `min_s` seconds."""
+    import subprocess
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    r = subprocess.run([sys.executable, "-c", ONE_CORE_SRC % (ROOT, min_s)], env=env,
+                       stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=120)
+    if r.returncode != 0:
+        return {"error": r.stderr.strip().splitlines()[-1:] or ["exit %d" % r.returncode]}
+    d = json.loads(r.stdout.strip().splitlines()[-1])
+    return {"value": round(16 * d["steps"] / d["seconds"], 3), "unit": "images/s",
+            "cores": d["threads"], "kind": "oracle",
+            "sample": "%d training iterations of the three-block CNN (3x32x32 input, conv 3-32, "
+                      "32-64, 64-128, 10 classes) at batch 16 (%.1f s)" % (d["steps"], d["seconds"])}
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -208,6 +246,9 @@ def main():
         print("bench.py: this build runs on one GPU only; --gpus %d is not supported" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
+
+    # the one-core oracle figure first, in a child process, before this process uses the GPU
+    one_core = None if args.no_cpu_baseline else cpu_baseline_one_core()
 
     import torch
     from paper_2407_11698_amd import nitro as N
@@ -359,6 +400,7 @@ def main():
         out["stress_conv"] = stress_layer(args.stress_reps)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)
+        out["cpu_baseline"]["one_core"] = one_core
     print(json.dumps(out), flush=True)
 
 
