@@ -17,10 +17,12 @@ Readings of passages that the paper leaves open (each is a switch or a documente
     gradient);
   * the backward of NITRO-ReLU is the derivative of its piecewise map evaluated at the stored
     rescaled pre-activation z*: identity for 0 <= z* <= 127, division by alpha_inv (same rounding
-    mode) for -127 <= z* < 0, zero where the map saturates (z* > 127 or z* < -127);
+    mode) for -127 <= z* < 0, zero where the map saturates (z* > 127 or z* < -127) (switch:
+    ``Hyper.relu_grad_ste`` passes the gradient unchanged on the leaky segment instead);
   * max-pool keeps the first maximum of the 2x2 window in row-major order and routes the whole
     gradient to it;
-  * delta^fw is computed with the learning-layer weights from before their update;
+  * delta^fw is computed with the learning-layer weights from before their update (switch:
+    ``Hyper.delta_fw_post_update`` takes them after it, the literal order of section 3.3);
   * every layer's scaling factor uses its own fan-in; learning and output layers are rescaled too
     but have no NITRO-ReLU;
   * eta = gamma * lambda is formed in int64 (an explicit eta may override it).
@@ -220,11 +222,13 @@ def nitro_relu(zs, alpha_inv: int, mode: int = FLOOR):
     return np.where(zs < 0, neg, pos)
 
 
-def nitro_relu_grad(delta, zs, alpha_inv: int, mode: int = FLOOR):
-    """Backward of NITRO-ReLU at the stored z* (the reading stated in the module docstring)."""
+def nitro_relu_grad(delta, zs, alpha_inv: int, mode: int = FLOOR, ste: bool = False):
+    """Backward of NITRO-ReLU at the stored z* (the reading stated in the module docstring).
+    ``ste=True`` is the alternative reading: a plain straight-through pass (gradient unchanged)
+    on the leaky segment as well; the saturated segments still pass nothing."""
     delta = np.asarray(delta, dtype=np.int64)
     zs = np.asarray(zs, dtype=np.int64)
-    slope = idiv(delta, alpha_inv, mode)
+    slope = delta if ste else idiv(delta, alpha_inv, mode)
     out = np.where((zs >= 0) & (zs <= 127), delta, 0)
     out = np.where((zs < 0) & (zs >= -127), slope, out)
     return out
@@ -271,16 +275,15 @@ def amplification_factor(G: int) -> int:
 
 
 def integer_sgd(w, dw, gamma_inv: int, lambda_inv: int, mode: int = FLOOR, eta_inv: int = -1):
-    """IntegerSGD with weight decay (Alg. 1): eta = gamma*lambda; delta = dW / gamma;
-    if eta != 0: delta += W / eta; W <- W - delta."""
+    """IntegerSGD with weight decay (Alg. 1) in closed form:
+    W' = W - (dW / gamma_inv + [eta_inv != 0] * W / eta_inv), with eta_inv = gamma_inv * lambda_inv
+    unless an explicit eta_inv is given, every division by the rounding rule."""
     if gamma_inv < 1 or lambda_inv < 0:
         raise ValueError("gamma_inv >= 1 and lambda_inv >= 0 required")
     eta = gamma_inv * lambda_inv if eta_inv < 0 else eta_inv
     w = np.asarray(w, dtype=np.int64)
-    d = idiv(dw, gamma_inv, mode)
-    if eta != 0:
-        d = d + idiv(w, eta, mode)
-    return check_int32(w - d, "updated weights")
+    decay = idiv(w, eta, mode) if eta != 0 else np.zeros_like(w)
+    return check_int32(w - (idiv(dw, gamma_inv, mode) + decay), "updated weights")
 
 
 def kaiming_bound(fan_in: int) -> int:
@@ -352,9 +355,10 @@ def learning_forward(f, w_lr, mode: int):
 
 
 def block_backward(rec: BlockRecord, ws: list, delta_out, maxpool: bool, alpha_inv: int,
-                   mode: int, want_dx: bool = False) -> None:
+                   mode: int, want_dx: bool = False, ste: bool = False) -> None:
     """Back-propagate the gradient at the block output through the forward layers of the block,
-    using the weights from before the update. Fills rec.g, rec.dw (and rec.dx)."""
+    using the weights from before the update. Fills rec.g, rec.dw (and rec.dx). ``ste`` selects
+    the straight-through reading of the NITRO-ReLU backward (nitro_relu_grad)."""
     J = len(ws)
     last = rec.layers[-1]
     d = np.asarray(delta_out, dtype=np.int64)
@@ -363,7 +367,7 @@ def block_backward(rec: BlockRecord, ws: list, delta_out, maxpool: bool, alpha_i
     d = d.reshape(last.zs.shape)
     gs = [None] * J
     dws = [None] * J
-    g = check_int32(nitro_relu_grad(d, last.zs, alpha_inv, mode), "ReLU gradient")
+    g = check_int32(nitro_relu_grad(d, last.zs, alpha_inv, mode, ste), "ReLU gradient")
     for j in range(J - 1, -1, -1):
         gs[j] = g
         ly = rec.layers[j]
@@ -378,7 +382,7 @@ def block_backward(rec: BlockRecord, ws: list, delta_out, maxpool: bool, alpha_i
                 dx = linear_dx(g, ws[j])
             if j > 0:
                 dx = check_int32(dx, "input gradient")
-                g = check_int32(nitro_relu_grad(dx, rec.layers[j - 1].zs, alpha_inv, mode),
+                g = check_int32(nitro_relu_grad(dx, rec.layers[j - 1].zs, alpha_inv, mode, ste),
                                 "ReLU gradient")
             else:
                 rec.dx = dx       # leaves the block: never used by the method, kept in int64
@@ -397,6 +401,11 @@ class Hyper:
     af_classes: int = 0          # G for the amplification factor when n_classes == 0
     eta_fw: int = -1             # explicit eta overrides (< 0: gamma * lambda)
     eta_lr: int = -1
+    # alternative readings (both off by default):
+    relu_grad_ste: bool = False  # NITRO-ReLU backward passes the gradient unchanged on its leaky
+    #                              segment (straight through) instead of dividing by alpha_inv
+    delta_fw_post_update: bool = False   # delta^fw from the learning weights after their update
+    #                              (the literal order of the training procedure in section 3.3)
 
     @property
     def gamma_fw(self) -> int:
@@ -475,11 +484,12 @@ class OracleNet:
             rec.yhat = learning_forward(f, w_lr, mode)
             rec.e = check_int32(loss_grad(rec.yhat, labels, G), "loss gradient")
             rec.dw_lr = linear_dw(rec.e, f)
-            rec.delta_fw = check_int32(linear_dx(rec.e, w_lr), "delta_fw")   # pre-update W^il
             new_w[lr] = integer_sgd(w_lr, rec.dw_lr, hp.gamma_inv, hp.lambda_inv_lr, mode,
                                     hp.eta_lr).astype(np.int32)
+            w_delta = new_w[lr] if hp.delta_fw_post_update else w_lr       # default: pre-update
+            rec.delta_fw = check_int32(linear_dx(rec.e, w_delta), "delta_fw")
             block_backward(rec, [self.w[k] for k in fw], rec.delta_fw.reshape(rec.out.shape),
-                           pool, hp.alpha_inv, mode)
+                           pool, hp.alpha_inv, mode, ste=hp.relu_grad_ste)
             for j, k in enumerate(fw):
                 new_w[k] = integer_sgd(self.w[k], rec.dw[j], hp.gamma_fw, hp.lambda_inv_fw, mode,
                                        hp.eta_fw).astype(np.int32)
@@ -493,7 +503,8 @@ class OracleNet:
         fw, _ = self.index[0]
         ws = [self.w[k] for k in fw]
         rec = block_forward(x, ws, self.specs[0][1], hp.alpha_inv, hp.mode)
-        block_backward(rec, ws, delta, self.specs[0][1], hp.alpha_inv, hp.mode, want_dx=True)
+        block_backward(rec, ws, delta, self.specs[0][1], hp.alpha_inv, hp.mode, want_dx=True,
+                       ste=hp.relu_grad_ste)
         for j, k in enumerate(fw):
             self.w[k] = integer_sgd(self.w[k], rec.dw[j], hp.gamma_fw, hp.lambda_inv_fw, hp.mode,
                                     hp.eta_fw).astype(np.int32)

@@ -115,6 +115,139 @@ def test_mini_step(mode):
     assert net.w[0].tolist() == exp["W1_new"]
 
 
+def _hyper(g, mode, **kw):
+    return O.Hyper(gamma_inv=g["gamma_inv"], lambda_inv_fw=g["lambda_inv_fw"],
+                   lambda_inv_lr=g.get("lambda_inv_lr", 0), alpha_inv=g["alpha_inv"],
+                   n_classes=g.get("G", 0), mode=mode, **kw)
+
+
+@pytest.mark.parametrize("mode", ["floor", "trunc"])
+def test_two_layer_block_step(mode):
+    """A block with two forward layers: the input gradient of the second layer goes through the
+    NITRO-ReLU of the first (its z*), then to the first layer's weight gradient."""
+    g = gold("two_layer_block.json")
+    exp = g[mode]
+    net = O.OracleNet([(2, False, True)], False,
+                      [np.array(g[k], np.int32) for k in ("W1", "W2", "Wlr")], _hyper(g, MODES[mode]))
+    st = net.train_step(np.array(g["x"], np.int8), np.array(g["label"], np.int32))
+    b = st.blocks[0]
+    assert b.layers[0].zs.tolist() == exp["zs1"]
+    assert b.layers[0].a.tolist() == exp["a1"]
+    assert b.layers[1].zs.tolist() == exp["zs2"]
+    assert b.out.tolist() == exp["a2"]
+    assert b.yhat.tolist() == exp["yhat"]
+    assert b.e.tolist() == exp["e"]
+    assert b.dw_lr.tolist() == exp["dWlr"]
+    assert b.delta_fw.tolist() == exp["delta_fw"]
+    assert b.g[1].tolist() == exp["g2"]
+    assert b.dw[1].tolist() == exp["dW2"]
+    assert b.g[0].tolist() == exp["g1"]
+    assert b.dw[0].tolist() == exp["dW1"]
+    assert net.w[2].tolist() == exp["Wlr_new"]
+    assert net.w[1].tolist() == exp["W2_new"]
+    assert net.w[0].tolist() == exp["W1_new"]
+
+
+@pytest.mark.parametrize("mode", ["floor", "trunc"])
+def test_pooled_conv_block_step(mode):
+    """Two conv layers and a 2x2 max-pool: the learning layer's gradient is routed to the
+    window's first maximum, then through both NITRO-ReLUs and the second conv's input gradient."""
+    g = gold("pooled_conv_block.json")
+    exp = g[mode]
+    net = O.OracleNet([(2, True, True)], False,
+                      [np.array(g[k], np.int32) for k in ("W1", "W2", "Wlr")], _hyper(g, MODES[mode]))
+    st = net.train_step(np.array(g["x"], np.int8), np.array(g["label"], np.int32))
+    b = st.blocks[0]
+    hw = lambda a: np.asarray(a)[0, :, :, 0].tolist()          # one image, one channel
+    assert hw(b.layers[0].zs) == exp["zs1"]
+    assert hw(b.layers[0].a) == exp["a1"]
+    assert hw(b.layers[1].zs) == exp["zs2"]
+    assert int(b.pool_idx[0, 0, 0, 0]) == exp["pool_idx"]
+    assert int(b.out[0, 0, 0, 0]) == exp["out"]
+    assert b.yhat.tolist() == exp["yhat"]
+    assert b.e.tolist() == exp["e"]
+    assert b.dw_lr.tolist() == exp["dWlr"]
+    assert int(b.delta_fw[0, 0]) == exp["delta_fw"]
+    assert hw(b.g[1]) == exp["g2"]
+    assert b.dw[1][0, :, :, 0].tolist() == exp["dW2"]
+    assert hw(b.g[0]) == exp["g1"]
+    assert b.dw[0][0, :, :, 0].tolist() == exp["dW1"]
+    assert net.w[2].tolist() == exp["Wlr_new"]
+    assert net.w[1][0, :, :, 0].tolist() == exp["W2_new"]
+    assert net.w[0][0, :, :, 0].tolist() == exp["W1_new"]
+
+
+@pytest.mark.parametrize("mode", ["floor", "trunc"])
+def test_output_head_step(mode):
+    """The output layer takes the global loss gradient and IntegerSGD with gamma (not gamma^fw)."""
+    g = gold("head_step.json")
+    exp = g[mode]
+    net = O.OracleNet([(1, False, True)], True,
+                      [np.array(g[k], np.int32) for k in ("W1", "Wlr", "Wh")], _hyper(g, MODES[mode]))
+    st = net.train_step(np.array(g["x"], np.int8), np.array(g["label"], np.int32))
+    assert st.head_yhat.tolist() == exp["yhat"]
+    assert st.head_e.tolist() == exp["e"]
+    assert st.head_dw.tolist() == exp["dWh"]
+    assert net.w[2].tolist() == exp["Wh_new"]
+    assert net.w[1].tolist() == exp["Wlr_new"]
+    assert net.w[0].tolist() == exp["W1_new"]
+
+
+@pytest.mark.parametrize("mode", ["floor", "trunc"])
+def test_stress_repeat(mode):
+    """One repeat of the single conv layer with a given gradient at the NITRO-ReLU output:
+    every segment of the backward, the int64 input gradient, gamma^fw = 2^6 * 10 * gamma."""
+    g = gold("stress_repeat.json")
+    exp = g[mode]
+    hp = O.Hyper(gamma_inv=g["gamma_inv"], lambda_inv_fw=g["lambda_inv_fw"], lambda_inv_lr=0,
+                 alpha_inv=g["alpha_inv"], n_classes=0, mode=MODES[mode], af_classes=g["af_classes"])
+    net = O.OracleNet([(1, False, False)], False, [np.array(g["W"], np.int32)], hp)
+    rec = net.stress_repeat(np.array(g["x"], np.int8), np.array(g["delta"], np.int64))
+    hw = lambda a: np.asarray(a)[0, :, :, 0].tolist()
+    assert hw(rec.layers[0].zs) == exp["zs"]
+    assert hw(rec.out) == exp["a"]
+    assert hw(rec.g[0]) == exp["g"]
+    assert rec.dw[0][0, :, :, 0].tolist() == exp["dW"]
+    assert hw(rec.dx) == exp["dX"]
+    assert net.w[0][0, :, :, 0].tolist() == exp["W_new"]
+
+
+def test_alternative_readings():
+    """The oracle's switches for the straight-through NITRO-ReLU backward and for delta^fw from
+    the updated learning weights (floor mode, the mini_step block)."""
+    g = gold("mini_step.json")
+    alt = g["alternatives"]
+    for key, kw in (("ste", {"relu_grad_ste": True}), ("post_update", {"delta_fw_post_update": True})):
+        exp = alt[key]
+        net = O.OracleNet([(1, False, True)], False,
+                          [np.array(g["W1"], np.int32), np.array(g["Wlr"], np.int32)],
+                          _hyper(g, O.FLOOR, **kw))
+        st = net.train_step(np.array(g["x"], np.int8), np.array(g["label"], np.int32))
+        b = st.blocks[0]
+        if "delta_fw" in exp:
+            assert b.delta_fw.tolist() == exp["delta_fw"]
+        assert b.g[0].tolist() == exp["g"]
+        assert b.dw[0].tolist() == exp["dW1"]
+        assert net.w[0].tolist() == exp["W1_new"]
+
+
+def test_inner_input_gradient_must_fit_int32():
+    """The gradient that crosses a forward layer inside a block is stored as int32: an input
+    gradient beyond int32 raises, even where the leaky segment's division would bring it back
+    into range."""
+    x = np.array([[127, 127]], np.int8)
+    big = 1 << 20
+    # layer 1: z = -254, z* = -1 (leaky segment); layer 2's two inputs are equal, so its
+    # opposite-signed weights give z = 0 (identity segment) and the gradient passes unchanged:
+    # dX = +-2 * 4096 * 2^20 = +-2^33, while dX / alpha_inv would fit int32
+    ws = [np.array([[-1, -1], [-1, -1]], np.int32), np.array([[big, -big], [big, -big]], np.int32)]
+    rec = O.block_forward(x, ws, False, 10, O.FLOOR)
+    assert rec.layers[0].zs.tolist() == [[-1, -1]] and rec.layers[1].zs.tolist() == [[0, 0]]
+    O.block_backward(rec, ws, np.array([[1, 1]]), False, 10, O.FLOOR)      # fits: no error
+    with pytest.raises(OverflowError):
+        O.block_backward(rec, ws, np.array([[1 << 12, 1 << 12]]), False, 10, O.FLOOR)
+
+
 # ---------------------------------------------------------------- brute force, tiny shapes
 
 def _rand(rng, shape, lo, hi, dtype=np.int64):
