@@ -94,12 +94,16 @@ def limbs_for(m: int) -> int:
 
 def stress_layer(reps: int):
     """The single conv-layer stress case (256x256x32x32 int8 activations, conv 256 -> 256, int32
-    error signal in [-2^15, 2^15] at the NITRO-ReLU output), its forward and back-propagation
-    run alone on the GPU, `reps` times, with each kernel's own device time. Outside the timed
-    region of the training iterations.
+    error signal in [-2^15, 2^15] at the NITRO-ReLU output), `reps` cumulative repeats, each a
+    forward, the back-propagation of the error signal (weight and int64 input gradients) and the
+    IntegerSGD step with the amplified rate, run alone on the GPU after the training iterations.
 
-    Algorithmic ops count each GEMM once (2 x N*H*W*C_out*9*C_in); MFMA ops count every limb
-    pass the kernel executes (the error signal needs 3 int8 limbs at this bound)."""
+    Each repeat is timed whole with HIP events on the library's stream (every kernel of the
+    repeat, IntegerSGD included), and its three conv GEMM kernels by their own device time.
+    Algorithmic ops count each GEMM once (2 x N*H*W*C_out*9*C_in, three GEMMs per repeat); MFMA
+    ops count every limb pass the kernel executes, from the repeat's own max|W| and max|g|. The
+    weights leave int8 after the first repeat, so repeat 1 and the steady state (median over the
+    later repeats) are reported separately."""
     import torch
     from paper_2407_11698_amd import runner
     from paper_2407_11698_amd import workloads as WL
@@ -110,39 +114,50 @@ def stress_layer(reps: int):
     xd = torch.from_numpy(dr.batches[0][0]).to(dev)
     dd = torch.from_numpy(dr.delta).to(dev)
     g = torch.empty(dd.shape, dtype=torch.int32, device=dev)
-
-    def once():
-        st.ctx.block_forward(st.desc, [st.w], xd, st.a, st.state)
-        st.ctx.block_backward(st.desc, [st.w], None, xd, st.a, None, dd, st.state, [st.dw], None,
-                              {"dx": st.dx, "g": [g]})
-
-    once()
-    st.ctx.sync()
-    st.ctx.kernel_timing(True)
-    for _ in range(reps):
-        once()
-    st.ctx.sync()
-    kt = {name: st.ctx.kernel_time(c) for c, name in KERNEL_CLASSES.items()}
-    st.ctx.kernel_timing(False)
+    stream = torch.cuda.current_stream(dev)
     ly = wl.blocks[0].layers[0]
     c, h, w = wl.in_shape
     macs = wl.batch * h * w * ly.c_out * 9 * ly.c_in
-    lw = limbs_for(int(st.w.abs().max().item()))
-    lg = limbs_for(int(g.abs().max().item()))
-    passes = {"k_conv_tile<fwd>": lw, "k_conv_tile<dx>": lg * lw, "k_conv_dw_planes": lg}
-    out = {}
-    for name, (ms, launches) in kt.items():
-        if launches == 0:
-            continue
-        per = ms * 1e-3 / reps
-        tops = 2 * macs / per / 1e12
-        out[name] = {"avg_launch_us": round(ms * 1e3 / launches, 2), "launches": launches,
-                     "ms_per_pass": round(ms / reps, 4), "algorithmic_TOPs": round(tops, 2),
-                     "frac": round(tops / PEAK_INT8_TOPS, 4), "limb_passes": passes[name],
-                     "mfma_TOPs": round(tops * passes[name], 2),
-                     "mfma_frac": round(tops * passes[name] / PEAK_INT8_TOPS, 4)}
+    per = []
+    st.ctx.kernel_timing(True)
+    for r in range(reps):
+        lw = limbs_for(int(st.w.abs().max().item()))          # the weights this repeat reads
+        st.ctx.sync()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        st.repeat(xd, dd, taps={"g": [g]})
+        e1.record(stream)
+        st.ctx.sync()
+        kt = {name: st.ctx.kernel_time(c)[0] for c, name in KERNEL_CLASSES.items()}
+        lg = limbs_for(int(g.abs().max().item()))
+        per.append({"ms": e0.elapsed_time(e1), "kernels_ms": kt,
+                    "passes": {"k_conv_tile<fwd>": lw, "k_conv_tile<dx>": lg * lw,
+                               "k_conv_dw_planes": lg}})
+    st.ctx.kernel_timing(False)
+
+    def summary(rs):
+        ms = float(np.median([r["ms"] for r in rs]))
+        out = {"repeats": len(rs), "ms_per_repeat": round(ms, 4),
+               "algorithmic_TOPs": round(3 * 2 * macs / (ms * 1e-3) / 1e12, 2),
+               "frac": round(3 * 2 * macs / (ms * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4), "kernels": {}}
+        for name in KERNEL_CLASSES.values():
+            kms = float(np.median([r["kernels_ms"][name] for r in rs]))
+            passes = int(np.median([r["passes"][name] for r in rs]))
+            tops = 2 * macs / (kms * 1e-3) / 1e12 if kms > 0 else 0.0
+            out["kernels"][name] = {"ms": round(kms, 4), "algorithmic_TOPs": round(tops, 2),
+                                    "frac": round(tops / PEAK_INT8_TOPS, 4), "limb_passes": passes,
+                                    "mfma_TOPs": round(tops * passes, 2),
+                                    "mfma_frac": round(tops * passes / PEAK_INT8_TOPS, 4)}
+        return out
+
+    res = {"workload": wl.name, "repeats": reps, "gop_per_repeat": round(3 * 2 * macs / 1e9, 1),
+           "timing": "HIP events around each whole repeat (forward, back-propagation, IntegerSGD); "
+                     "kernel times from the kernels' own device timestamps",
+           "repeat_1": summary(per[:1])}
+    if reps > 1:
+        res["steady_state"] = summary(per[1:])
     del st, xd, dd, g
-    return {"workload": wl.name, "repeats": reps, "kernels": out}
+    return res
 
 
 def cpu_baseline(wl, min_s: float = 12.0, budget_s: float = 25.0):
@@ -177,7 +192,7 @@ import sys, time, json
 sys.path.insert(0, %r)
 from oracle import oracle as O
 from paper_2407_11698_amd import workloads as WL
-sample = WL.scaled(WL.SMALL_CNN, 16)
+sample = WL.scaled(WL.VGG_CNN, %d)
 dr = WL.draw_workload(sample, O.kaiming_bound, steps=sample.steps)
 hp = O.Hyper(sample.gamma_inv, sample.lambda_inv_fw, sample.lambda_inv_lr, sample.alpha_inv,
              sample.n_classes)
@@ -193,21 +208,21 @@ print(json.dumps({"steps": steps, "seconds": el, "threads": O.num_threads()}))
 """
 
 
-def cpu_baseline_one_core(min_s: float = 5.0):
+def cpu_baseline_one_core(min_s: float = 8.0, batch: int = 4):
     """The CPU oracle on one core (a child process with OMP_NUM_THREADS=1, started before this
-    process touches the GPU): training iterations of the three-block CIFAR-shaped CNN at batch
-    16, for at least `min_s` seconds."""
+    process touches the GPU): training iterations of the benchmark workload at batch `batch`,
+    for at least `min_s` seconds."""
     import subprocess
     env = dict(os.environ, OMP_NUM_THREADS="1")
-    r = subprocess.run([sys.executable, "-c", ONE_CORE_SRC % (ROOT, min_s)], env=env,
-                       stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=120)
+    r = subprocess.run([sys.executable, "-c", ONE_CORE_SRC % (ROOT, batch, min_s)], env=env,
+                       stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=180)
     if r.returncode != 0:
         return {"error": r.stderr.strip().splitlines()[-1:] or ["exit %d" % r.returncode]}
     d = json.loads(r.stdout.strip().splitlines()[-1])
-    return {"value": round(16 * d["steps"] / d["seconds"], 3), "unit": "images/s",
+    return {"value": round(batch * d["steps"] / d["seconds"], 3), "unit": "images/s",
             "cores": d["threads"], "kind": "oracle",
-            "sample": "%d training iterations of the three-block CNN (3x32x32 input, conv 3-32, "
-                      "32-64, 64-128, 10 classes) at batch 16 (%.1f s)" % (d["steps"], d["seconds"])}
+            "sample": "%d training iterations of the same workload at batch %d (%.1f s)"
+                      % (d["steps"], batch, d["seconds"])}
 
 
 def cpu_model() -> str:
@@ -233,9 +248,9 @@ def main():
     ap.add_argument("--serial-steps", type=int, default=3,
                     help="training iterations run after the timed region with every block on "
                          "one stream, for per-launch kernel times without overlap (0 skips)")
-    ap.add_argument("--stress-reps", type=int, default=10,
-                    help="repeats of the single conv-layer stress case measured after the "
-                         "training iterations (0 skips it)")
+    ap.add_argument("--stress-reps", type=int, default=20,
+                    help="cumulative repeats of the single conv-layer stress case measured after "
+                         "the training iterations (0 skips it)")
     ap.add_argument("--mfma-probe-iters", type=int, default=20000,
                     help="MFMAs per chain of the int8 matrix-core rate probe (0: skip it)")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -377,7 +392,7 @@ def main():
                    "alpha_inv": wl.alpha_inv, "rounding": "floor",
                    "launch": "graph replay" if graph else "eager"},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved,
-                     "peak": PEAK_INT8_TOPS, "unit": "TFLOP/s",
+                     "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                      "frac": round(achieved / PEAK_INT8_TOPS, 5),
                      "traffic": recorded_traffic(dom)},
         "conv_mfma": {"algorithmic_TOPs": round(conv_tops, 3),

@@ -189,13 +189,45 @@ nitro_status nitro_head_backward(nitro_ctx *ctx, int32_t n, int32_t d, int32_t n
                                  int32_t round, int64_t *dw, int32_t *yhat, int32_t *e);
 
 /* IntegerSGD with weight decay (Alg. 1) on `count` int32 weights, in place:
- *   eta = gamma_inv * lambda_inv (or eta_override when >= 0);
- *   d = dw / gamma_inv; if eta != 0: d += w / eta; w -= d.
+ *   w' = w - (dw / gamma_inv + [eta != 0] * w / eta),
+ * with eta = gamma_inv * lambda_inv (or eta_override when >= 0) and every division rounded per
+ * `round`.
  * gamma_inv >= 1, lambda_inv >= 0 (EINVAL otherwise). A result outside int32 raises
  * NITRO_EOVERFLOW (the weight is then left unchanged). */
 nitro_status nitro_integer_sgd_step(nitro_ctx *ctx, int32_t *w, const int64_t *dw, int64_t count,
                                     int64_t gamma_inv, int64_t lambda_inv, int64_t eta_override,
                                     int32_t round);
+
+/* Writable weights of one block, for its IntegerSGD step. */
+typedef struct {
+    int32_t *w[NITRO_MAX_LAYERS];          /* forward-layer weights                            */
+    int32_t *w_lr;                         /* learning layer [G][d]; NULL iff n_classes == 0    */
+} nitro_block_weights;
+
+/* Hyper-parameters of IntegerSGD (Alg. 1) and of the amplification factor (Eq. 6) for a block or
+ * a whole network. */
+typedef struct {
+    int64_t gamma_inv;        /* gamma_inv of learning and output layers (>= 1)                 */
+    int64_t lambda_inv_fw;    /* lambda_inv of forward layers (>= 0, 0: no decay)               */
+    int64_t lambda_inv_lr;    /* lambda_inv of learning and output layers                       */
+    int64_t af;               /* amplification factor; 0 means 2^6 * G (Eq. 6)                 */
+    int64_t eta_fw;           /* < 0: eta = (AF * gamma_inv) * lambda_inv_fw; else this eta     */
+    int64_t eta_lr;           /* < 0: eta = gamma_inv * lambda_inv_lr; else this eta           */
+    int32_t af_classes;       /* G entering AF = 2^6 G when af == 0 and the block has no
+                                 learning layer (n_classes == 0); ignored otherwise             */
+    int32_t reserved;         /* must be 0                                                      */
+} nitro_hparams;
+
+/* IntegerSGD (Alg. 1) of one block after nitro_block_backward: every forward layer with
+ * gamma^fw = AF * gamma_inv (Eq. 6), lambda_inv_fw, and the learning layer (when
+ * n_classes > 0) with gamma_inv, lambda_inv_lr; one launch. AF = hp->af, or 2^6 G with G the
+ * block's n_classes (hp->af_classes for a block without learning layer; EINVAL if both are 0).
+ * Weights are updated in place; a result outside int32 raises NITRO_EOVERFLOW and leaves that
+ * weight unchanged. EINVAL for a null pointer or a divisor out of range (as
+ * nitro_integer_sgd_step) or an eta = gamma * lambda beyond int64. */
+nitro_status nitro_block_sgd_step(nitro_ctx *ctx, const nitro_block_desc *desc,
+                                  const nitro_block_weights *weights,
+                                  const nitro_block_grads *grads, const nitro_hparams *hp);
 
 /* ------------------------------------------------------------------------------------------ */
 /* A whole network: one training iteration                                                    */
@@ -213,15 +245,6 @@ typedef struct {
     int32_t *w_lr[NITRO_MAX_BLOCKS];                  /* learning-layer weights (updated)       */
     int32_t *w_head;                                  /* output layer [G][d_L] (if head)        */
 } nitro_net_params;
-
-typedef struct {
-    int64_t gamma_inv;        /* gamma_inv of learning and output layers (>= 1)                 */
-    int64_t lambda_inv_fw;    /* lambda_inv of forward layers (>= 0, 0: no decay)               */
-    int64_t lambda_inv_lr;    /* lambda_inv of learning and output layers                       */
-    int64_t af;               /* amplification factor; 0 means 2^6 * G (Eq. 6)                 */
-    int64_t eta_fw;           /* < 0: eta = (AF * gamma_inv) * lambda_inv_fw; else this eta     */
-    int64_t eta_lr;           /* < 0: eta = gamma_inv * lambda_inv_lr; else this eta           */
-} nitro_hparams;
 
 /* Size in bytes of the network workspace: every block's state and output, and every weight
  * gradient. */
@@ -257,6 +280,30 @@ nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
 nitro_status nitro_net_block_output(const nitro_net_desc *net, void *workspace, int32_t b,
                                     int8_t **a_out);
 
+/* Device pointers, inside a workspace laid out by nitro_net_query, of what a training iteration
+ * leaves there for block b (for inspection; valid after the iteration's work has run):
+ *   a_out    int8 block output (pooled if the block pools), NHWC or [n][d];
+ *   act[j]   int8 output of forward layer j < n_layers - 1 (NULL for the last layer);
+ *   code[j]  NITRO-ReLU region codes of layer j, as described at nitro_block_saved;
+ *   yhat, e  int32 [n][G] learning-layer prediction and loss gradient;
+ *   dw[j]    int64 weight gradient of forward layer j (KRSC / [out][in]);
+ *   dw_lr    int64 [G][d] learning-layer weight gradient.
+ * Unused entries are NULL. */
+typedef struct {
+    int8_t *a_out;
+    int8_t *act[NITRO_MAX_LAYERS];
+    uint8_t *code[NITRO_MAX_LAYERS];
+    int32_t *yhat, *e;
+    int64_t *dw[NITRO_MAX_LAYERS];
+    int64_t *dw_lr;
+} nitro_block_view;
+nitro_status nitro_net_block_view(const nitro_net_desc *net, void *workspace, int32_t b,
+                                  nitro_block_view *out);
+/* The output layer's int32 [n][G] prediction and loss gradient and its int64 [G][d] weight
+ * gradient inside the workspace (EINVAL when the network has no output layer). */
+nitro_status nitro_net_head_view(const nitro_net_desc *net, void *workspace, int32_t **yhat,
+                                 int32_t **e, int64_t **dw);
+
 /* ------------------------------------------------------------------------------------------ */
 /* Host-side helpers (no device work)                                                         */
 /* ------------------------------------------------------------------------------------------ */
@@ -266,6 +313,10 @@ nitro_status nitro_net_block_output(const nitro_net_desc *net, void *workspace, 
 int64_t nitro_host_div(int64_t n, int64_t d, int32_t round);
 /* NITRO-ReLU mean for alpha_inv (section 3.2.2) under `round`. */
 int32_t nitro_host_relu_mu(int32_t alpha_inv, int32_t round);
+/* Bound b of the integer Kaiming initialisation (section 3.3.1): weights are drawn uniformly from
+ * [-b, b] with b = floor(128 * 1732 / (isqrt(fan_in) * 1000)), isqrt the integer square root.
+ * Returns 0 for fan_in < 1. */
+int32_t nitro_host_kaiming_bound(int64_t fan_in);
 
 /* Per-kernel timing for profiling. While enabled, every launch of a timed kernel class records,
  * on the device, the wall-clock time from its first workgroup's start to its last workgroup's

@@ -15,6 +15,7 @@ namespace nitro {
 thread_local LaunchTimer *g_timer = nullptr;
 }
 
+
 struct nitro_ctx : public LaunchTimer {
     int device = 0;
     hipStream_t stream = nullptr;
@@ -282,7 +283,7 @@ static bool rows_from_forward(const BlockGeom &g)
 nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, const BlockGeom &g,
                                 const nitro_block_params *p, const int8_t *x, int8_t *a_out,
                                 void *state, bool zero_slots = true, bool prepacked = false,
-                                bool x_prepadded = false)
+                                bool x_prepadded = false, bool rows_ok = true)
 {
     hipStream_t s = ctx->stream;
     const Relu rp = make_relu(desc->alpha_inv, desc->round);
@@ -320,7 +321,7 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
                 sx.c = 16;
                 xin = xpad;
             }
-            const bool rows = j == g.J - 2 && rows_from_forward(g);
+            const bool rows = rows_ok && j == g.J - 2 && rows_from_forward(g);
             if (L.fwd_tile)
                 launch_conv_fwd_tile(s, ctx->conv_tile, ctx->conv_persist, sx, xin, wf, wmax, L.sf, desc->alpha_inv, desc->round, rp,
                                      pool, out, code, ctx->flags,
@@ -505,6 +506,29 @@ nitro_status sgd_impl(nitro_ctx *ctx, int32_t *w, const int64_t *dw, int64_t cou
     return hip_status();
 }
 
+// The IntegerSGD rates of an iteration: gamma^fw = AF * gamma (Eq. 6) with AF = hp->af or 2^6 G,
+// eta = gamma * lambda unless given (Alg. 1). G is the learning layers' class count (or
+// hp->af_classes for a block without learning layer).
+struct Rates {
+    int64_t gamma_fw, eta_fw, eta_lr;
+};
+
+nitro_status resolve_rates(const nitro_hparams *hp, int G, Rates *r)
+{
+    if (!hp || hp->gamma_inv < 1 || hp->lambda_inv_fw < 0 || hp->lambda_inv_lr < 0 || hp->af < 0 ||
+        hp->af_classes < 0 || hp->reserved != 0)
+        return NITRO_EINVAL;
+    const int64_t g = G > 0 ? G : hp->af_classes;
+    const int64_t af = hp->af ? hp->af : 64 * g;
+    if (af < 1) return NITRO_EINVAL;
+    if (!mul_ok(af, hp->gamma_inv, &r->gamma_fw)) return NITRO_EINVAL;
+    r->eta_fw = hp->eta_fw;
+    r->eta_lr = hp->eta_lr;
+    if (r->eta_fw < 0 && !mul_ok(r->gamma_fw, hp->lambda_inv_fw, &r->eta_fw)) return NITRO_EINVAL;
+    if (r->eta_lr < 0 && !mul_ok(hp->gamma_inv, hp->lambda_inv_lr, &r->eta_lr)) return NITRO_EINVAL;
+    return NITRO_OK;
+}
+
 // ------------------------------------------------------------------------------------------
 // Network workspace layout.
 struct NetGeom {
@@ -599,6 +623,18 @@ int32_t nitro_host_relu_mu(int32_t alpha_inv, int32_t round)
     const int64_t s1 = idiv(-127, make_div(alpha_inv, round));
     const int64_t s2 = idiv(-127, make_div(2 * (int64_t)alpha_inv, round));
     return (int32_t)idiv(s1 + s2 + 63 + 127, make_div(4, round));
+}
+
+int32_t nitro_host_kaiming_bound(int64_t fan_in)
+{
+    if (fan_in < 1) return 0;
+    // integer square root by bisection: the largest r with r * r <= fan_in
+    int64_t lo = 1, hi = 3037000499;               // floor(sqrt(2^63 - 1))
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo + 1) / 2;
+        if (mid <= fan_in / mid) lo = mid; else hi = mid - 1;
+    }
+    return (int32_t)((128 * 1732) / (lo * 1000));
 }
 
 nitro_status nitro_create(nitro_ctx **out, int device, void *hip_stream)
@@ -782,6 +818,74 @@ nitro_status nitro_net_block_output(const nitro_net_desc *net, void *workspace, 
     return NITRO_OK;
 }
 
+nitro_status nitro_block_sgd_step(nitro_ctx *ctx, const nitro_block_desc *desc,
+                                  const nitro_block_weights *weights,
+                                  const nitro_block_grads *grads, const nitro_hparams *hp)
+{
+    if (!ctx || !weights || !grads) return NITRO_EINVAL;
+    BlockGeom g;
+    nitro_status st = block_geom(desc, &g);
+    if (st != NITRO_OK) return st;
+    Rates r;
+    st = resolve_rates(hp, desc->n_classes, &r);
+    if (st != NITRO_OK) return st;
+    for (int j = 0; j < g.J; j++)
+        if (!weights->w[j] || !grads->dw[j]) return NITRO_EINVAL;
+    if (desc->n_classes > 0 && (!weights->w_lr || !grads->dw_lr)) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+    SgdBatch b{};
+    b.flags = ctx->flags;
+    if (desc->n_classes > 0) {
+        st = sgd_entry(ctx, b, weights->w_lr, grads->dw_lr, (int64_t)desc->n_classes * g.d,
+                       hp->gamma_inv, hp->lambda_inv_lr, r.eta_lr, desc->round);
+        if (st != NITRO_OK) return st;
+    }
+    for (int j = 0; j < g.J; j++) {
+        st = sgd_entry(ctx, b, weights->w[j], grads->dw[j], weight_count(desc->layer[j]), r.gamma_fw,
+                       hp->lambda_inv_fw, r.eta_fw, desc->round);
+        if (st != NITRO_OK) return st;
+    }
+    launch_sgd_batch(ctx->stream, b);
+    return hip_status();
+}
+
+nitro_status nitro_net_block_view(const nitro_net_desc *net, void *workspace, int32_t b,
+                                  nitro_block_view *out)
+{
+    if (!workspace || !out) return NITRO_EINVAL;
+    NetGeom g;
+    nitro_status st = net_geom(net, &g);
+    if (st != NITRO_OK) return st;
+    if (b < 0 || b >= net->n_blocks) return NITRO_EINVAL;
+    *out = nitro_block_view{};
+    const BlockGeom &bg = g.b[b];
+    uint8_t *state = at(workspace, g.state[b]);
+    out->a_out = (int8_t *)at(workspace, g.aout[b]);
+    for (int j = 0; j < bg.J; j++) {
+        out->act[j] = j == bg.J - 1 ? nullptr : (int8_t *)(state + bg.act[j]);
+        out->code[j] = state + bg.code[j];
+        out->dw[j] = (int64_t *)at(workspace, g.dw[b][j]);
+    }
+    out->yhat = (int32_t *)(state + bg.yhat);
+    out->e = (int32_t *)(state + bg.e);
+    out->dw_lr = (int64_t *)at(workspace, g.dwlr[b]);
+    return NITRO_OK;
+}
+
+nitro_status nitro_net_head_view(const nitro_net_desc *net, void *workspace, int32_t **yhat,
+                                 int32_t **e, int64_t **dw)
+{
+    if (!workspace || !yhat || !e || !dw) return NITRO_EINVAL;
+    NetGeom g;
+    nitro_status st = net_geom(net, &g);
+    if (st != NITRO_OK) return st;
+    if (!net->head) return NITRO_EINVAL;
+    *yhat = (int32_t *)at(workspace, g.hyhat);
+    *e = (int32_t *)at(workspace, g.he);
+    *dw = (int64_t *)at(workspace, g.hdw);
+    return NITRO_OK;
+}
+
 nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                               const nitro_net_params *params, void *workspace,
                               const int8_t *x, const int32_t *labels, const nitro_hparams *hp)
@@ -792,14 +896,10 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     if (st != NITRO_OK) return st;
     const int G = net->block[0].n_classes;
     const int round = net->block[0].round;
-    if (hp->gamma_inv < 1 || hp->lambda_inv_fw < 0 || hp->lambda_inv_lr < 0 || hp->af < 0)
-        return NITRO_EINVAL;
-    int64_t af = hp->af ? hp->af : 64 * (int64_t)G;
-    int64_t gamma_fw;
-    if (!mul_ok(af, hp->gamma_inv, &gamma_fw)) return NITRO_EINVAL;
-    int64_t eta_fw = hp->eta_fw, eta_lr = hp->eta_lr;
-    if (eta_fw < 0 && !mul_ok(gamma_fw, hp->lambda_inv_fw, &eta_fw)) return NITRO_EINVAL;
-    if (eta_lr < 0 && !mul_ok(hp->gamma_inv, hp->lambda_inv_lr, &eta_lr)) return NITRO_EINVAL;
+    Rates rates;
+    st = resolve_rates(hp, G, &rates);
+    if (st != NITRO_OK) return st;
+    const int64_t gamma_fw = rates.gamma_fw, eta_fw = rates.eta_fw, eta_lr = rates.eta_lr;
     for (int b = 0; b < net->n_blocks; b++) {
         for (int j = 0; j < net->block[b].n_layers; j++)
             if (!params->w[b][j]) return NITRO_EINVAL;

@@ -422,17 +422,15 @@ void launch_conv_dw(hipStream_t s, const ConvShape &sh, const int32_t *g, const 
 }
 
 // ---------------------------------------------------------------------------------------------
-// IntegerSGD (Alg. 1): d = dw / gamma (+ w / eta when eta != 0); w <- w - d.
+// IntegerSGD (Alg. 1) in closed form: w' = w - (dw / gamma + [eta != 0] w / eta).
 __global__ void k_sgd(int32_t *__restrict__ w, const int64_t *__restrict__ dw, int64_t count,
                       Div gamma, Div eta, int decay, uint32_t *flags)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (; i < count; i += stride) {
-        int64_t wv = w[i];
-        int64_t d = idiv(dw[i], gamma);
-        if (decay) d += idiv(wv, eta);
-        int64_t nw = wv - d;
+        const int64_t wv = w[i];
+        const int64_t nw = wv - (idiv(dw[i], gamma) + (decay ? idiv(wv, eta) : 0));
         if (!fits_i32(nw)) {
             raise_flag(flags, FLAG_OVERFLOW);
             continue;

@@ -197,8 +197,9 @@ void launch_pack_matrix(hipStream_t s, const int32_t *w, int R, int C, int Rpad,
 }
 
 // ---------------------------------------------------------------------------------------------
-// IntegerSGD (Alg. 1) over several tensors in one launch: d = dw / gamma (+ w / eta when
-// eta != 0); w <- w - d. Workgroups are dealt to tensors in order (first[k] .. first[k+1]).
+// IntegerSGD (Alg. 1) over several tensors in one launch, in closed form:
+// w' = w - (dw / gamma + [eta != 0] w / eta). Workgroups are dealt to tensors in order
+// (first[k] .. first[k+1]).
 __global__ __launch_bounds__(256) void k_sgd_batch(SgdBatch b)
 {
     int k = 0;
@@ -209,9 +210,7 @@ __global__ __launch_bounds__(256) void k_sgd_batch(SgdBatch b)
         const int64_t i = base + q * 256 + threadIdx.x;
         if (i >= t.count) break;
         const int64_t wv = t.w[i];
-        int64_t d = idiv(t.dw[i], t.gamma);
-        if (t.decay) d += idiv(wv, t.eta);
-        const int64_t nw = wv - d;
+        const int64_t nw = wv - (idiv(t.dw[i], t.gamma) + (t.decay ? idiv(wv, t.eta) : 0));
         if (!fits_i32(nw)) {
             raise_flag(b.flags, FLAG_OVERFLOW);
             continue;

@@ -71,7 +71,16 @@ class NetParams(ctypes.Structure):
 
 class HParams(ctypes.Structure):
     _fields_ = [("gamma_inv", I64), ("lambda_inv_fw", I64), ("lambda_inv_lr", I64), ("af", I64),
-                ("eta_fw", I64), ("eta_lr", I64)]
+                ("eta_fw", I64), ("eta_lr", I64), ("af_classes", I32), ("reserved", I32)]
+
+
+class BlockWeights(ctypes.Structure):
+    _fields_ = [("w", VP * MAX_LAYERS), ("w_lr", VP)]
+
+
+class BlockView(ctypes.Structure):
+    _fields_ = [("a_out", VP), ("act", VP * MAX_LAYERS), ("code", VP * MAX_LAYERS), ("yhat", VP),
+                ("e", VP), ("dw", VP * MAX_LAYERS), ("dw_lr", VP)]
 
 
 def _load():
@@ -96,12 +105,16 @@ def _load():
                                        P(BlockGrads), P(BlockTaps)]),
         "nitro_head_backward": (I32, [VP, I32, I32, I32, VP, VP, VP, I32, VP, VP, VP]),
         "nitro_integer_sgd_step": (I32, [VP, VP, VP, I64, I64, I64, I64, I32]),
+        "nitro_block_sgd_step": (I32, [VP, P(BlockDesc), P(BlockWeights), P(BlockGrads), P(HParams)]),
+        "nitro_net_block_view": (I32, [P(NetDesc), VP, I32, P(BlockView)]),
+        "nitro_net_head_view": (I32, [P(NetDesc), VP, P(VP), P(VP), P(VP)]),
         "nitro_net_query": (I32, [P(NetDesc), P(ctypes.c_size_t)]),
         "nitro_net_block_output": (I32, [P(NetDesc), VP, I32, P(VP)]),
         "nitro_train_step": (I32, [VP, P(NetDesc), P(NetParams), VP, VP, VP, P(HParams)]),
         "nitro_train_step_graph": (I32, [VP, P(NetDesc), P(NetParams), VP, VP, VP, P(HParams)]),
         "nitro_host_div": (I64, [I64, I64, I32]),
         "nitro_host_relu_mu": (I32, [I32, I32]),
+        "nitro_host_kaiming_bound": (I32, [I64]),
         "nitro_kernel_timing": (I32, [VP, I32]),
         "nitro_kernel_time": (I32, [VP, I32, P(ctypes.c_double), P(I64)]),
         "nitro_mfma_rate": (I32, [VP, I32, I32, P(ctypes.c_double)]),
@@ -121,9 +134,10 @@ EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_set_conv_
            "nitro_sync_status",
            "nitro_status_str", "nitro_block_query", "nitro_block_saved", "nitro_block_forward",
            "nitro_block_backward",
-           "nitro_head_backward", "nitro_integer_sgd_step", "nitro_net_query",
+           "nitro_head_backward", "nitro_integer_sgd_step", "nitro_block_sgd_step",
+           "nitro_net_block_view", "nitro_net_head_view", "nitro_net_query",
            "nitro_net_block_output", "nitro_train_step", "nitro_train_step_graph",
-           "nitro_host_div", "nitro_host_relu_mu",
+           "nitro_host_div", "nitro_host_relu_mu", "nitro_host_kaiming_bound",
            "nitro_kernel_timing", "nitro_kernel_time", "nitro_mfma_rate")
 
 
@@ -191,12 +205,38 @@ def net_query(nd: NetDesc) -> int:
     return out.value
 
 
+def hparams(gamma_inv: int, lambda_inv_fw: int, lambda_inv_lr: int, af_classes: int = 0,
+            af: int = 0, eta_fw: int = -1, eta_lr: int = -1) -> HParams:
+    return HParams(gamma_inv, lambda_inv_fw, lambda_inv_lr, af, eta_fw, eta_lr, af_classes, 0)
+
+
+def net_block_view(nd: NetDesc, workspace, b: int) -> dict:
+    """Device pointers of block b's tensors inside a network workspace (None where unused)."""
+    v = BlockView()
+    check(LIB.nitro_net_block_view(ctypes.byref(nd), _p(workspace), b, ctypes.byref(v)),
+          "nitro_net_block_view")
+    return {"a_out": v.a_out, "act": list(v.act), "code": list(v.code), "yhat": v.yhat, "e": v.e,
+            "dw": list(v.dw), "dw_lr": v.dw_lr}
+
+
+def net_head_view(nd: NetDesc, workspace) -> dict:
+    y, e, d = VP(), VP(), VP()
+    check(LIB.nitro_net_head_view(ctypes.byref(nd), _p(workspace), ctypes.byref(y), ctypes.byref(e),
+                                  ctypes.byref(d)), "nitro_net_head_view")
+    return {"yhat": y.value, "e": e.value, "dw": d.value}
+
+
 def host_div(n: int, d: int, round_mode: int = ROUND_FLOOR) -> int:
     return int(LIB.nitro_host_div(n, d, round_mode))
 
 
 def host_relu_mu(alpha_inv: int, round_mode: int = ROUND_FLOOR) -> int:
     return int(LIB.nitro_host_relu_mu(alpha_inv, round_mode))
+
+
+def kaiming_bound(fan_in: int) -> int:
+    """Integer Kaiming bound (section 3.3.1), computed by the library."""
+    return int(LIB.nitro_host_kaiming_bound(fan_in))
 
 
 # ----------------------------------------------------------------------------- context
@@ -285,6 +325,18 @@ class Context:
                          round_mode: int = ROUND_FLOOR) -> None:
         check(LIB.nitro_integer_sgd_step(self.h, _p(w), _p(dw), w.numel(), gamma_inv, lambda_inv,
                                          eta, round_mode), "nitro_integer_sgd_step")
+
+    def block_sgd_step(self, desc: BlockDesc, ws, w_lr, dws, dw_lr, hp: HParams) -> None:
+        bw = BlockWeights()
+        for j, w in enumerate(ws):
+            bw.w[j] = _p(w)
+        bw.w_lr = _p(w_lr)
+        gr = BlockGrads()
+        for j, d in enumerate(dws):
+            gr.dw[j] = _p(d)
+        gr.dw_lr = _p(dw_lr)
+        check(LIB.nitro_block_sgd_step(self.h, ctypes.byref(desc), ctypes.byref(bw), ctypes.byref(gr),
+                                       ctypes.byref(hp)), "nitro_block_sgd_step")
 
     # -- network level ------------------------------------------------------------------
     def train_step(self, nd: NetDesc, params: NetParams, workspace, x, labels, hp: HParams) -> None:

@@ -3,7 +3,6 @@ description, hold weights and the workspace in torch device memory, and call nit
 (or the block-level calls for the single-layer stress case). Marshalling only."""
 from __future__ import annotations
 
-import math
 from typing import List
 
 import numpy as np
@@ -13,9 +12,8 @@ from . import nitro as N
 from .workloads import Conv3x3, Workload
 
 
-def kaiming_bound(fan_in: int) -> int:
-    """Integer Kaiming bound of section 3.3.1: floor(128 * 1732 / (isqrt(fan_in) * 1000))."""
-    return (128 * 1732) // (math.isqrt(fan_in) * 1000)
+# weight initialisation bound (section 3.3.1), computed by the library
+kaiming_bound = N.kaiming_bound
 
 
 def block_descs(wl: Workload, round_mode: int = N.ROUND_FLOOR) -> List[N.BlockDesc]:
@@ -61,7 +59,7 @@ class GpuNet:
             k += 1
         assert k == len(self.w)
         self.workspace = torch.empty(N.net_query(self.nd), dtype=torch.uint8, device=self.dev)
-        self.hp = N.HParams(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr, 0, -1, -1)
+        self.hp = N.hparams(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr)
 
     def step(self, x: torch.Tensor, y: torch.Tensor) -> None:
         self.ctx.train_step(self.nd, self.params, self.workspace, x, y, self.hp)
@@ -70,6 +68,49 @@ class GpuNet:
         """One iteration replayed from the context's captured graph for these buffers (captured
         on the first call with them; up to 16 buffer sets keep graphs of their own)."""
         self.ctx.train_step_graph(self.nd, self.params, self.workspace, x, y, self.hp)
+
+    def view(self, b: int) -> dict:
+        """Block b's tensors from the last step, as torch views of the workspace: "a_out",
+        "act" (list, None for the last layer), "code" (list), "yhat", "e", "dw" (list), "dw_lr"."""
+        ptrs = N.net_block_view(self.nd, self.workspace, b)
+        blk = self.wl.blocks[b]
+        (inp, out) = self.wl.block_shapes()[b]
+        n, G = self.wl.batch, self.wl.n_classes
+        conv = isinstance(blk.layers[0], Conv3x3)
+        full = []                    # per layer: output shape at full resolution
+        for ly in blk.layers:
+            full.append((n, inp[1], inp[2], ly.c_out) if conv else (n, ly.d_out))
+        a_shape = (n, out[1], out[2], out[0]) if conv else (n,) + tuple(out)
+        last = len(blk.layers) - 1
+        res = {"a_out": self._at(ptrs["a_out"], a_shape, torch.int8),
+               "act": [self._at(ptrs["act"][j], full[j], torch.int8) if j < last else None
+                       for j in range(len(blk.layers))],
+               "code": [self._at(ptrs["code"][j], a_shape if (j == last and blk.maxpool) else full[j],
+                                 torch.uint8) for j in range(len(blk.layers))],
+               "yhat": self._at(ptrs["yhat"], (n, G), torch.int32),
+               "e": self._at(ptrs["e"], (n, G), torch.int32),
+               "dw": [self._at(ptrs["dw"][j], tuple(w.shape), torch.int64)
+                      for j, w in enumerate(self.w[self._first_weight(b):self._first_weight(b) + len(blk.layers)])],
+               "dw_lr": self._at(ptrs["dw_lr"], (G, int(np.prod(out))), torch.int64)}
+        return res
+
+    def head_view(self) -> dict:
+        ptrs = N.net_head_view(self.nd, self.workspace)
+        n, G, d = self.wl.batch, self.wl.n_classes, self.wl.head_dim()
+        return {"yhat": self._at(ptrs["yhat"], (n, G), torch.int32),
+                "e": self._at(ptrs["e"], (n, G), torch.int32),
+                "dw": self._at(ptrs["dw"], (G, d), torch.int64)}
+
+    def _first_weight(self, b: int) -> int:
+        k = 0
+        for blk in self.wl.blocks[:b]:
+            k += len(blk.layers) + (1 if blk.learning else 0)
+        return k
+
+    def _at(self, ptr: int, shape, dtype) -> torch.Tensor:
+        off = ptr - self.workspace.data_ptr()
+        nb = int(np.prod(shape)) * torch.tensor([], dtype=dtype).element_size()
+        return self.workspace[off:off + nb].view(dtype).view(shape)
 
     def block_output(self, b: int) -> torch.Tensor:
         """Block b's output from the last step (int8, NHWC or [n][d])."""
@@ -102,11 +143,18 @@ class GpuConvStress:
         self.a = torch.empty((wl.batch, h, w, ly.c_out), dtype=torch.int8, device=self.dev)
         self.dw = torch.empty((ly.c_out, 3, 3, ly.c_in), dtype=torch.int64, device=self.dev)
         self.dx = torch.empty((wl.batch, h, w, ly.c_in), dtype=torch.int64, device=self.dev)
-        self.gamma_fw = (1 << 6) * wl.af_classes * wl.gamma_inv
+        self.hp = N.hparams(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr,
+                            af_classes=wl.af_classes)
 
-    def repeat(self, x: torch.Tensor, delta: torch.Tensor, want_dx: bool = True) -> None:
+    def repeat(self, x: torch.Tensor, delta: torch.Tensor, want_dx: bool = True,
+               taps: dict = None) -> None:
+        """Forward, back-propagation of `delta` (the int64 input gradient when want_dx), then
+        IntegerSGD with the forward layers' amplified rate. `taps` adds extra outputs (the
+        gradient at the pre-activation: {"g": [tensor]})."""
+        t = dict(taps or {})
+        if want_dx:
+            t["dx"] = self.dx
         self.ctx.block_forward(self.desc, [self.w], x, self.a, self.state)
         self.ctx.block_backward(self.desc, [self.w], None, x, self.a, None, delta, self.state,
-                                [self.dw], None, {"dx": self.dx} if want_dx else None)
-        self.ctx.integer_sgd_step(self.w, self.dw, self.gamma_fw, self.wl.lambda_inv_fw,
-                                  round_mode=self.round)
+                                [self.dw], None, t or None)
+        self.ctx.block_sgd_step(self.desc, [self.w], None, [self.dw], None, self.hp)

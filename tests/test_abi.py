@@ -118,3 +118,4 @@ def test_null_context_rejected():
     assert N.LIB.nitro_block_forward(None, d, N.BlockParams(), None, None, None) == N.EINVAL
     assert N.LIB.nitro_integer_sgd_step(None, None, None, 0, 1, 0, -1, 0) == N.EINVAL
     assert N.LIB.nitro_sync_status(None) == N.EINVAL
+

@@ -1,22 +1,24 @@
-"""Parity at full size, in the configuration bench.py times.
+"""Parity at full size, in the configuration bench.py times: every tensor after every step.
 
-The full oracle of a VGG-style step at batch 256 costs about 1.5e11 int64 multiply-adds, so each
-step is checked inductively: every quantity is recomputed by the oracle from inputs that were
-themselves verified, either completely or at seeded sample positions:
-  * block outputs and inner activations: at sampled 2x2 pooling windows, by running the oracle's
-    forward layers on a cropped input patch whose receptive field is exact (zeros only where the
-    image itself is padded);
-  * learning layer: yhat, e, delta and its weight gradient completely;
-  * gradients at each layer's pre-activation: at the sampled windows and positions;
-  * weight gradients: sampled entries, each a full sum over every pixel of the batch;
-  * IntegerSGD: every weight of every tensor.
-nitro_train_step (what the benchmark calls) is run in lockstep and must produce the same weights
-as the block-level calls checked here."""
+The oracle's results for the two benchmark-sized workloads are stored as per-step SHA-256 digests
+of every tensor (``tests/golden/make_digests.py``, which runs only the oracle): the VGG-style CNN
+at batch 256 over its ten training iterations, and the single 256 -> 256 conv layer on
+256x256x32x32 over its twenty repeats with IntegerSGD between them. Each GPU tensor is hashed in
+its storage dtype and must match; on a mismatch the stored sample values name the positions that
+differ.
+
+The VGG iteration is run twice in lockstep: through nitro_train_step (what the benchmark calls;
+its workspace views give the activations, region codes, yhat, e and every weight gradient) and
+through the block-level calls with every tap (which add delta^fw and the gradient at each layer's
+pre-activation). Both must produce the oracle's weights after every step."""
+import hashlib
+import json
+import os
+
 import numpy as np
 import pytest
 import torch
 
-from oracle import oracle as O
 from paper_2407_11698_amd import nitro as N
 from paper_2407_11698_amd import runner
 from paper_2407_11698_amd import workloads as WL
@@ -24,6 +26,8 @@ from paper_2407_11698_amd import workloads as WL
 pytestmark = pytest.mark.gpu
 
 DEV = torch.device("cuda", 0)
+GOLD = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+DTYPES = {"int8": torch.int8, "uint8": torch.uint8, "int32": torch.int32, "int64": torch.int64}
 
 
 @pytest.fixture(scope="module")
@@ -33,29 +37,31 @@ def ctx():
     c.close()
 
 
+def load_digests(name):
+    path = os.path.join(GOLD, name)
+    if not os.path.exists(path):
+        pytest.fail("%s is missing: run tests/golden/make_digests.py" % path)
+    with open(path) as f:
+        return json.load(f)
+
+
 def dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
 
 
-def host(t):
-    torch.cuda.synchronize()
-    return t.cpu().numpy()
-
-
-def view(state, ptr, shape, dtype):
-    off = ptr - state.data_ptr()
-    n = int(np.prod(shape)) * torch.tensor([], dtype=dtype).element_size()
-    return state[off:off + n].view(dtype).view(shape)
-
-
-def crop(x, n, r0, c0, size):
-    """x[n, r0:r0+size, c0:c0+size, :] with zeros outside the image."""
-    _, H, W, C = x.shape
-    out = np.zeros((1, size, size, C), x.dtype)
-    rs, re = max(r0, 0), min(r0 + size, H)
-    cs, ce = max(c0, 0), min(c0 + size, W)
-    out[0, rs - r0:re - r0, cs - c0:ce - c0, :] = x[n, rs:re, cs:ce, :]
-    return out
+def check(exp: dict, name: str, t: torch.Tensor, where: str):
+    """The tensor's digest (in the stored dtype) against the oracle's; on a mismatch, report the
+    sample positions that differ."""
+    e = exp[name]
+    assert t.dtype == DTYPES[e["dtype"]], (where, name, t.dtype)
+    assert list(t.shape) == e["shape"], (where, name, list(t.shape), e["shape"])
+    a = t.contiguous().cpu().numpy()
+    if hashlib.sha256(a.tobytes()).hexdigest() == e["sha256"]:
+        return
+    flat = a.reshape(-1)
+    bad = [(p, v, int(flat[p])) for p, v in e["sample"] if int(flat[p]) != v]
+    pytest.fail("%s %s differs from the oracle; sampled (position, oracle, gpu) mismatches: %s"
+                % (where, name, bad[:8] or "none among the samples"))
 
 
 class BlockLevelNet:
@@ -64,6 +70,7 @@ class BlockLevelNet:
     def __init__(self, ctx, wl, weights):
         self.ctx, self.wl = ctx, wl
         self.descs = runner.block_descs(wl)
+        self.hp = N.hparams(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr)
         self.w = [dev(w) for w in weights]
         self.blocks = []
         k = 0
@@ -73,7 +80,6 @@ class BlockLevelNet:
             wlr = self.w[k + J]
             k += J + 1
             c, h, w = out
-            d = c * h * w
             _, h0, w0 = inp
             taps = {"yhat": torch.empty((wl.batch, wl.n_classes), dtype=torch.int32, device=DEV),
                     "e": torch.empty((wl.batch, wl.n_classes), dtype=torch.int32, device=DEV),
@@ -81,13 +87,12 @@ class BlockLevelNet:
                     "g": [torch.empty((wl.batch, h0, w0, ly.c_out), dtype=torch.int32, device=DEV)
                           for ly in blk.layers]}
             self.blocks.append(dict(
-                desc=desc, ws=ws, wlr=wlr, J=J,
+                desc=desc, ws=ws, wlr=wlr, J=J, hw=(h0, w0), chans=[ly.c_out for ly in blk.layers],
                 state=torch.empty(N.block_query(desc), dtype=torch.uint8, device=DEV),
                 a_out=torch.empty((wl.batch, h, w, c), dtype=torch.int8, device=DEV),
                 dws=[torch.empty(t.shape, dtype=torch.int64, device=DEV) for t in ws],
-                dw_lr=torch.empty((wl.n_classes, d), dtype=torch.int64, device=DEV),
+                dw_lr=torch.empty((wl.n_classes, c * h * w), dtype=torch.int64, device=DEV),
                 taps=taps))
-        self.gamma_fw = (1 << 6) * wl.n_classes * wl.gamma_inv
 
     def step(self, x, y):
         cur = x
@@ -95,149 +100,88 @@ class BlockLevelNet:
             self.ctx.block_forward(B["desc"], B["ws"], cur, B["a_out"], B["state"])
             B["x"] = cur
             cur = B["a_out"]
-        self.w_before = [host(t) for t in self.w]
         for B in self.blocks:
             self.ctx.block_backward(B["desc"], B["ws"], B["wlr"], B["x"], B["a_out"], y, None,
                                     B["state"], B["dws"], B["dw_lr"], B["taps"])
         for B in self.blocks:
-            self.ctx.integer_sgd_step(B["wlr"], B["dw_lr"], self.wl.gamma_inv, self.wl.lambda_inv_lr)
-            for w, dw in zip(B["ws"], B["dws"]):
-                self.ctx.integer_sgd_step(w, dw, self.gamma_fw, self.wl.lambda_inv_fw)
+            self.ctx.block_sgd_step(B["desc"], B["ws"], B["wlr"], B["dws"], B["dw_lr"], self.hp)
         self.ctx.sync()
 
-
-def check_block(B, x_in, labels, W, Wlr, wl, rng, samples=16, dw_samples=12):
-    """One block of one step against the oracle (x_in, W, Wlr: verified host arrays)."""
-    alpha, mode = wl.alpha_inv, O.FLOOR
-    J = B["J"]
-    assert J == 2
-    a_out = host(B["a_out"])
-    act_ptr, code_ptr = N.block_saved(B["desc"], B["state"], 0)
-    _, h, w, c1 = x_in.shape[0], x_in.shape[1], x_in.shape[2], W[0].shape[0]
-    act1 = host(view(B["state"], act_ptr, (wl.batch, h, w, c1), torch.int8))
-    g1 = host(B["taps"]["g"][0])
-    g2 = host(B["taps"]["g"][1])
-    delta_all = host(B["taps"]["delta"])
-    # ---- forward and gradients at sampled 2x2 windows
-    for _ in range(samples):
-        n = int(rng.integers(wl.batch))
-        h2, w2 = int(rng.integers(h // 2)), int(rng.integers(w // 2))
-        patch = crop(x_in, n, 2 * h2 - 2, 2 * w2 - 2, 6)
-        l1 = O.layer_forward(patch, W[0], alpha, mode)
-        # layer 2 sees zero padding outside the image, not NITRO-ReLU(0)
-        a1 = l1.a.copy()
-        for i in range(6):
-            for jj in range(6):
-                if not (0 <= 2 * h2 - 2 + i < h and 0 <= 2 * w2 - 2 + jj < w):
-                    a1[0, i, jj, :] = 0
-        l2 = O.layer_forward(a1, W[1], alpha, mode)
-        # layer-1 activations are exact on the 4x4 centre (rows/cols 1..4 of the patch)
-        for dr in range(4):
-            for dc in range(4):
-                hh, ww = 2 * h2 - 1 + dr, 2 * w2 - 1 + dc
-                if 0 <= hh < h and 0 <= ww < w:
-                    assert np.array_equal(act1[n, hh, ww], l1.a[0, 1 + dr, 1 + dc]), "act1"
-        win_a = l2.a[0, 2:4, 2:4]                        # 2x2 x C2, exact
-        win_zs = l2.zs[0, 2:4, 2:4]
-        pooled, idx = O.maxpool2(win_a[None])
-        assert np.array_equal(a_out[n, h2, w2], pooled[0, 0, 0]), "block output"
-        # gradient at layer 2's pre-activation: delta routed to the argmax through ReLU'
-        delta = delta_all[n, h2, w2].astype(np.int64)
-        exp = np.zeros((2, 2, win_a.shape[-1]), np.int64)
-        for ch in range(win_a.shape[-1]):
-            t = int(idx[0, 0, 0, ch])
-            exp[t // 2, t % 2, ch] = int(O.nitro_relu_grad(delta[ch], win_zs[t // 2, t % 2, ch], alpha, mode))
-        assert np.array_equal(g2[n, 2 * h2:2 * h2 + 2, 2 * w2:2 * w2 + 2], exp), "g layer 2"
-        # gradient at layer 1's pre-activation at the window's top-left pixel
-        hh, ww = 2 * h2, 2 * w2
-        dx = np.array([O.conv3x3_dx_at(g2, W[1], n, hh, ww, ci) for ci in range(c1)])
-        exp1 = O.nitro_relu_grad(dx, l1.zs[0, 2, 2], alpha, mode)
-        assert np.array_equal(g1[n, hh, ww], exp1), "g layer 1"
-    # ---- learning layer, completely
-    f = a_out.reshape(wl.batch, -1)
-    yhat = O.learning_forward(f, Wlr, mode)
-    e = O.loss_grad(yhat, labels, wl.n_classes)
-    assert np.array_equal(host(B["taps"]["yhat"]), yhat), "yhat"
-    assert np.array_equal(host(B["taps"]["e"]), e), "e"
-    assert np.array_equal(host(B["dw_lr"]), O.linear_dw(e, f)), "dW learning"
-    assert np.array_equal(delta_all.reshape(wl.batch, -1), O.linear_dx(e, Wlr)), "delta"
-    # ---- weight gradients at sampled entries (each a sum over every pixel)
-    for j, (g, xin) in enumerate(((g1, x_in), (g2, act1))):
-        dW = host(B["dws"][j])
-        co_n, ci_n = dW.shape[0], dW.shape[3]
-        for _ in range(dw_samples):
-            co, r, s, ci = (int(rng.integers(co_n)), int(rng.integers(3)), int(rng.integers(3)),
-                            int(rng.integers(ci_n)))
-            assert dW[co, r, s, ci] == O.conv3x3_dw_at(g, xin, co, r, s, ci), "dW layer %d" % j
-    return a_out
+    def saved(self, B, j, what):
+        """Layer j's saved int8 activations ("act") or region codes ("code") in the state."""
+        act, code = N.block_saved(B["desc"], B["state"], j)
+        n = self.wl.batch
+        h, w = B["hw"]
+        pooled = j == B["J"] - 1 and B["desc"].maxpool
+        shape = (n, h // 2, w // 2, B["chans"][j]) if pooled else (n, h, w, B["chans"][j])
+        ptr, dt = (act, torch.int8) if what == "act" else (code, torch.uint8)
+        off = ptr - B["state"].data_ptr()
+        return B["state"][off:off + int(np.prod(shape))].view(dt).view(shape)
 
 
-def test_vgg_full_batch_ten_steps(ctx):
-    """The benchmark workload (batch 256, 100 classes), all ten steps of its trajectory."""
+def test_vgg_full_batch_every_tensor(ctx):
+    """The benchmark workload (batch 256, 100 classes), all ten steps of its trajectory, every
+    tensor of both the whole-iteration call and the block-level calls."""
     wl = WL.VGG_CNN
+    dg = load_digests("digests_vgg_cnn_b256.json")
+    assert dg["workload"] == wl.name and dg["batch"] == wl.batch
     print("full-size case", wl.name, flush=True)
-    dr = WL.draw_workload(wl, O.kaiming_bound)
-    net = BlockLevelNet(ctx, wl, dr.weights)
-    bench_net = runner.GpuNet(wl, dr.weights, ctx=ctx)
-    for step, (x, y) in enumerate(dr.batches):
-        print("step", step, flush=True)
+    dr = WL.draw_workload(wl, runner.kaiming_bound, steps=len(dg["steps"]))
+    blk_net = BlockLevelNet(ctx, wl, dr.weights)
+    net = runner.GpuNet(wl, dr.weights, ctx=ctx)
+    for s, ((x, y), exp) in enumerate(zip(dr.batches, dg["steps"])):
+        print("step", s, flush=True)
         xd, yd = dev(x), dev(y)
+        blk_net.step(xd, yd)
         net.step(xd, yd)
-        bench_net.step(xd, yd)
         ctx.sync()
-        rng = np.random.default_rng(1000 + step)
-        k = 0
-        cur = x
-        for B in net.blocks:
-            W = net.w_before[k:k + 2]
-            Wlr = net.w_before[k + 2]
-            cur = check_block(B, cur, y, W, Wlr, wl, rng)
-            # IntegerSGD, every weight
-            dws = [host(t) for t in B["dws"]] + [host(B["dw_lr"])]
-            gammas = [net.gamma_fw, net.gamma_fw, wl.gamma_inv]
-            lams = [wl.lambda_inv_fw, wl.lambda_inv_fw, wl.lambda_inv_lr]
-            for i in range(3):
-                ref = O.integer_sgd(net.w_before[k + i], dws[i], gammas[i], lams[i])
-                assert np.array_equal(host(net.w[k + i]), ref), "SGD tensor %d" % (k + i)
-            k += 3
-        for a, b in zip(bench_net.weights_np(), [host(t) for t in net.w]):
-            assert np.array_equal(a, b), "nitro_train_step differs from the block-level calls"
+        for b, B in enumerate(blk_net.blocks):
+            v = net.view(b)
+            for path, src in (("train_step", v), ("block calls", None)):
+                where = "step %d (%s)" % (s, path)
+                for j in range(B["J"]):
+                    if j < B["J"] - 1:
+                        act = v["act"][j] if src else blk_net.saved(B, j, "act")
+                        check(exp, "b%d.act%d" % (b, j), act, where)
+                    code = v["code"][j] if src else blk_net.saved(B, j, "code")
+                    check(exp, "b%d.code%d" % (b, j), code, where)
+                    check(exp, "b%d.dw%d" % (b, j), v["dw"][j] if src else B["dws"][j], where)
+                    if not src:
+                        check(exp, "b%d.g%d" % (b, j), B["taps"]["g"][j], where)
+                check(exp, "b%d.out" % b, v["a_out"] if src else B["a_out"], where)
+                check(exp, "b%d.yhat" % b, v["yhat"] if src else B["taps"]["yhat"], where)
+                check(exp, "b%d.e" % b, v["e"] if src else B["taps"]["e"], where)
+                check(exp, "b%d.dw_lr" % b, v["dw_lr"] if src else B["dw_lr"], where)
+                if not src:
+                    check(exp, "b%d.delta" % b, B["taps"]["delta"], where)
+        for k in range(len(net.w)):
+            check(exp, "w%d" % k, net.w[k], "step %d (train_step)" % s)
+            check(exp, "w%d" % k, blk_net.w[k], "step %d (block calls)" % s)
 
 
 def test_conv_stress_full_size_twenty_repeats(ctx):
-    """256x256x32x32, conv 256->256, fixed activations and error signal, 20 cumulative repeats."""
+    """256x256x32x32, conv 256 -> 256, fixed activations and error signal, twenty cumulative
+    repeats with IntegerSGD between them (the weights leave int8 after the first)."""
     wl = WL.CONV_STRESS
+    dg = load_digests("digests_conv_stress.json")
+    assert dg["workload"] == wl.name and dg["batch"] == wl.batch
     print("full-size case", wl.name, flush=True)
-    dr = WL.draw_workload(wl, O.kaiming_bound)
+    dr = WL.draw_workload(wl, runner.kaiming_bound)
     x, _ = dr.batches[0]
-    delta = dr.delta
     st = runner.GpuConvStress(wl, dr.weights[0], ctx=ctx)
-    g = torch.empty(delta.shape, dtype=torch.int32, device=DEV)
-    xd, dd = dev(x), dev(delta)
-    W = dr.weights[0].copy()
-    alpha, mode = wl.alpha_inv, O.FLOOR
-    for rep in range(wl.steps):
-        print("repeat", rep, flush=True)
-        st.ctx.block_forward(st.desc, [st.w], xd, st.a, st.state)
-        st.ctx.block_backward(st.desc, [st.w], None, xd, st.a, None, dd, st.state, [st.dw], None,
-                              {"dx": st.dx, "g": [g]})
+    g = torch.empty(dr.delta.shape, dtype=torch.int32, device=DEV)
+    xd, dd = dev(x), dev(dr.delta)
+    _, code_ptr = N.block_saved(st.desc, st.state, 0)
+    off = code_ptr - st.state.data_ptr()
+    code = st.state[off:off + st.a.numel()].view(st.a.shape)
+    for r, exp in enumerate(dg["steps"]):
+        print("repeat", r, flush=True)
+        st.repeat(xd, dd, taps={"g": [g]})
         ctx.sync()
-        a, gg, dW = host(st.a), host(g), host(st.dw)
-        rng = np.random.default_rng(2000 + rep)
-        for _ in range(16):
-            n, hh, ww = int(rng.integers(wl.batch)), int(rng.integers(32)), int(rng.integers(32))
-            patch = crop(x, n, hh - 1, ww - 1, 3)
-            lr = O.layer_forward(patch, W, alpha, mode)
-            assert np.array_equal(a[n, hh, ww], lr.a[0, 1, 1]), "activation"
-            exp_g = O.nitro_relu_grad(delta[n, hh, ww].astype(np.int64), lr.zs[0, 1, 1], alpha, mode)
-            assert np.array_equal(gg[n, hh, ww], exp_g), "gradient at z"
-            dx = host(st.dx[n, hh, ww])
-            for ci in rng.integers(0, 256, 8):
-                assert dx[ci] == O.conv3x3_dx_at(gg, W, n, hh, ww, int(ci)), "input gradient"
-        for _ in range(12):
-            co, r, s, ci = int(rng.integers(256)), int(rng.integers(3)), int(rng.integers(3)), int(rng.integers(256))
-            assert dW[co, r, s, ci] == O.conv3x3_dw_at(gg, x, co, r, s, ci), "dW"
-        st.ctx.integer_sgd_step(st.w, st.dw, st.gamma_fw, wl.lambda_inv_fw)
-        ctx.sync()
-        W = O.integer_sgd(W, dW, st.gamma_fw, wl.lambda_inv_fw).astype(np.int32)
-        assert np.array_equal(host(st.w), W), "SGD"
+        where = "repeat %d" % r
+        check(exp, "a", st.a, where)
+        check(exp, "code", code, where)
+        check(exp, "g", g, where)
+        check(exp, "dw", st.dw, where)
+        check(exp, "dx", st.dx, where)
+        check(exp, "w", st.w, where)

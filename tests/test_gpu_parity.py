@@ -322,17 +322,57 @@ def oracle_net(wl, weights, om):
     return O.OracleNet(specs, wl.head, weights, hp)
 
 
+def region_codes(zs):
+    """NITRO-ReLU segment per element as the library stores it: 0 identity, 1 leaky, 2 saturated."""
+    zs = np.asarray(zs)
+    return np.where((zs >= 0) & (zs <= 127), 0, np.where((zs < 0) & (zs >= -127), 1, 2))
+
+
+def pooled_codes(zs, idx):
+    """Per pooled element: winning window index | the winner's segment << 2."""
+    N_, H, W, C = zs.shape
+    v = np.asarray(zs).reshape(N_, H // 2, 2, W // 2, 2, C).transpose(0, 1, 3, 2, 4, 5)
+    win = np.take_along_axis(v.reshape(N_, H // 2, W // 2, 4, C), idx[:, :, :, None, :], axis=3)[..., 0, :]
+    return idx + 4 * region_codes(win)
+
+
 def check_training(ctx, wl, steps, nm, om):
+    """nitro_train_step against OracleNet.train_step: after every step, every tensor the
+    iteration leaves in its workspace (block outputs, inner activations, region codes, yhat, e,
+    every weight gradient, the output layer's yhat, e and weight gradient) and every weight."""
     print("training case", wl.name, "batch", wl.batch, "steps", steps, "mode", nm, flush=True)
     dr = WL.draw_workload(wl, O.kaiming_bound, steps=steps)
     ref = oracle_net(wl, dr.weights, om)
     net = runner.GpuNet(wl, dr.weights, nm, ctx=ctx)
+
+    def same(t, a, what):
+        assert np.array_equal(host(t), np.asarray(a)), what
+
     for s, (x, y) in enumerate(dr.batches):
         st = ref.train_step(x, y)
         net.step(dev(x), dev(y))
         ctx.sync()
         for b, rec in enumerate(st.blocks):
-            assert np.array_equal(host(net.block_output(b)), rec.out), "step %d block %d output" % (s, b)
+            v = net.view(b)
+            tag = "step %d block %d " % (s, b)
+            same(v["a_out"], rec.out, tag + "output")
+            J = len(rec.layers)
+            for j, ly in enumerate(rec.layers):
+                if j < J - 1:
+                    same(v["act"][j], ly.a, tag + "activation %d" % j)
+                    same(v["code"][j], region_codes(ly.zs), tag + "codes %d" % j)
+                same(v["dw"][j], rec.dw[j], tag + "dW %d" % j)
+            last = rec.layers[-1]
+            same(v["code"][J - 1], pooled_codes(last.zs, rec.pool_idx) if rec.pool_idx is not None
+                 else region_codes(last.zs), tag + "codes %d" % (J - 1))
+            same(v["yhat"], rec.yhat, tag + "yhat")
+            same(v["e"], rec.e, tag + "e")
+            same(v["dw_lr"], rec.dw_lr, tag + "dW learning")
+        if wl.head:
+            hv = net.head_view()
+            same(hv["yhat"], st.head_yhat, "step %d head yhat" % s)
+            same(hv["e"], st.head_e, "step %d head e" % s)
+            same(hv["dw"], st.head_dw, "step %d head dW" % s)
         for k, (wg, wo) in enumerate(zip(net.weights_np(), ref.w)):
             assert np.array_equal(wg, wo), "step %d weight tensor %d" % (s, k)
 
@@ -347,30 +387,62 @@ def test_train_mlp(ctx, modes):
     check_training(ctx, WL.MLP, 10, *modes)
 
 
-def test_train_small_cnn(ctx):
-    check_training(ctx, WL.SMALL_CNN, 10, N.ROUND_FLOOR, O.FLOOR)
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_train_small_cnn(ctx, modes):
+    check_training(ctx, WL.SMALL_CNN, 10, *modes)
 
 
-def test_train_vgg_reduced_batch(ctx):
-    check_training(ctx, WL.scaled(WL.VGG_CNN, 4), 10, N.ROUND_FLOOR, O.FLOOR)
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_train_vgg_reduced_batch(ctx, modes):
+    check_training(ctx, WL.scaled(WL.VGG_CNN, 4), 10, *modes)
 
 
-def test_conv_stress_reduced_batch(ctx):
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_conv_stress_reduced_batch(ctx, modes):
+    """The single conv layer at batch 2, ten repeats with IntegerSGD (through
+    nitro_block_sgd_step) between them: every tensor of every repeat."""
     wl = WL.scaled(WL.CONV_STRESS, 2)
-    print("stress case batch", wl.batch, flush=True)
+    print("stress case batch", wl.batch, "mode", modes[0], flush=True)
     dr = WL.draw_workload(wl, O.kaiming_bound)
-    ref = oracle_net(wl, dr.weights, O.FLOOR)
-    st = runner.GpuConvStress(wl, dr.weights[0], ctx=ctx)
+    ref = oracle_net(wl, dr.weights, modes[1])
+    st = runner.GpuConvStress(wl, dr.weights[0], modes[0], ctx=ctx)
     x, _ = dr.batches[0]
     xd, dd = dev(x), dev(dr.delta)
-    for r in range(3):
+    g = torch.empty(dr.delta.shape, dtype=torch.int32, device=DEV)
+    for r in range(10):
         rec = ref.stress_repeat(x, dr.delta)
-        st.repeat(xd, dd)
+        st.repeat(xd, dd, taps={"g": [g]})
         ctx.sync()
         assert np.array_equal(host(st.a), rec.out), "repeat %d output" % r
+        assert np.array_equal(host(g), rec.g[0]), "repeat %d g" % r
         assert np.array_equal(host(st.dw), rec.dw[0]), "repeat %d dW" % r
         assert np.array_equal(host(st.dx), rec.dx), "repeat %d dx" % r
         assert np.array_equal(host(st.w), ref.w[0]), "repeat %d W" % r
+
+
+@pytest.mark.parametrize("af", [0, 640])
+def test_block_sgd_step(ctx, af):
+    """nitro_block_sgd_step: forward layers with AF * gamma (AF = 2^6 G, or given), learning
+    layer with gamma, against the oracle's IntegerSGD on every tensor."""
+    rng = np.random.default_rng(21)
+    G, d = 10, 48
+    desc = N.block_desc(2, 4, 4, [N.layer(N.CONV3X3, 8, 12), N.layer(N.CONV3X3, 12, 12)], True,
+                        G, 10)
+    ws = [rand(rng, (12, 3, 3, 8), -(1 << 20), 1 << 20, np.int32),
+          rand(rng, (12, 3, 3, 12), -(1 << 20), 1 << 20, np.int32)]
+    wlr = rand(rng, (G, d), -(1 << 20), 1 << 20, np.int32)
+    dws = [rand(rng, w.shape, -(1 << 40), 1 << 40, np.int64) for w in ws]
+    dwlr = rand(rng, (G, d), -(1 << 30), 1 << 30, np.int64)
+    gamma, lam_fw, lam_lr = 512, 25, 3
+    wd = [dev(w) for w in ws]
+    wlrd = dev(wlr)
+    ctx.block_sgd_step(desc, wd, wlrd, [dev(a) for a in dws], dev(dwlr),
+                       N.hparams(gamma, lam_fw, lam_lr, af=af))
+    ctx.sync()
+    gfw = (af or (1 << 6) * G) * gamma
+    for w, dw, wg in zip(ws, dws, wd):
+        assert np.array_equal(host(wg), O.integer_sgd(w, dw, gfw, lam_fw))
+    assert np.array_equal(host(wlrd), O.integer_sgd(wlr, dwlr, gamma, lam_lr))
 
 
 def test_deterministic(ctx):
