@@ -3,6 +3,7 @@
 // layer, IntegerSGD and a whole training iteration (section 3.3).
 #include <string.h>
 
+#include <mutex>
 #include <utility>
 #include <vector>
 
@@ -15,6 +16,35 @@ namespace nitro {
 thread_local LaunchTimer *g_timer = nullptr;
 }
 
+// Scratch of nitro_block_forward_noalloc: a library-owned device array, one copy per device for
+// the life of the process. Host code never passes the array's name to a kernel or a copy (on the
+// host it is only a stand-in for the symbol): it uses the device address that
+// hipGetSymbolAddress returns, looked up once per device (with that device current) by
+// nitro_create.
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)64 << 20;
+static __device__ __align__(256) uint8_t scratch[NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[MAX_DEVICES] = {};
+
+// The device address of `scratch` on `device` (which must be current); nullptr if the lookup
+// fails.
+void *scratch_address(int device)
+{
+    if (device < 0 || device >= MAX_DEVICES) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[device]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess && p)
+            g_scratch_ptr[device] = p;
+        else
+            (void)hipGetLastError();
+    }
+    return g_scratch_ptr[device];
+}
+}  // namespace
 
 struct nitro_ctx : public LaunchTimer {
     int device = 0;
@@ -649,6 +679,9 @@ nitro_status nitro_create(nitro_ctx **out, int device, void *hip_stream)
     c->stream = (hipStream_t)hip_stream;
     if (hipMalloc((void **)&c->flags, 256) != hipSuccess) { delete c; return NITRO_ENOMEM; }
     if (hipMemset(c->flags, 0, 256) != hipSuccess) { (void)hipFree(c->flags); delete c; return NITRO_EHIP; }
+    // the device address of the no-allocation scratch, looked up once per device (a failed
+    // lookup only disables nitro_block_forward_noalloc, which then returns NITRO_EHIP)
+    (void)scratch_address(device);
     *out = c;
     return NITRO_OK;
 }
@@ -749,6 +782,34 @@ nitro_status nitro_block_forward(nitro_ctx *ctx, const nitro_block_desc *desc,
     DeviceGuard guard(ctx->device);
     TimerScope timer(ctx);
     return block_forward_impl(ctx, desc, g, params, x, a_out, state);
+}
+
+nitro_status nitro_block_forward_noalloc(nitro_ctx *ctx, const nitro_block_desc *desc,
+                                         const nitro_block_params *params, const int8_t *x,
+                                         int8_t *a_out)
+{
+    if (!params || !x || !a_out) return NITRO_EINVAL;
+    BlockGeom g;
+    nitro_status st = block_geom(desc, &g);
+    if (st != NITRO_OK) return st;
+    for (int j = 0; j < g.J; j++)
+        if (!params->w[j]) return NITRO_EINVAL;
+    // the forward pass uses the front of the block state: saved activations and codes, weight
+    // limb planes, the channel-padded input and the max slots (the backward's scratch follows);
+    // the size is checked before the context, so that the limit holds whatever else is wrong
+    const size_t need = align256(g.slots + 16 * SLOT_WORDS * 4);
+    if (need > NOALLOC_SCRATCH_BYTES) return NITRO_EUNSUPPORTED;
+    if (!ctx) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+    void *state = scratch_address(ctx->device);
+    if (!state) return NITRO_EHIP;
+    TimerScope timer(ctx);
+    // the max slots start at zero: cleared by a kernel (no memset node if the caller captures)
+    SlotList sl{};
+    sl.p[0] = (uint32_t *)at(state, g.slots);
+    sl.words = 8 * SLOT_WORDS;
+    launch_zero_slots(ctx->stream, sl, 1);
+    return block_forward_impl(ctx, desc, g, params, x, a_out, state, false, false, false, false);
 }
 
 nitro_status nitro_block_backward(nitro_ctx *ctx, const nitro_block_desc *desc,

@@ -101,6 +101,7 @@ def _load():
         "nitro_block_query": (I32, [P(BlockDesc), P(ctypes.c_size_t)]),
         "nitro_block_saved": (I32, [P(BlockDesc), VP, I32, P(VP), P(VP)]),
         "nitro_block_forward": (I32, [VP, P(BlockDesc), P(BlockParams), VP, VP, VP]),
+        "nitro_block_forward_noalloc": (I32, [VP, P(BlockDesc), P(BlockParams), VP, VP]),
         "nitro_block_backward": (I32, [VP, P(BlockDesc), P(BlockParams), VP, VP, VP, VP, VP,
                                        P(BlockGrads), P(BlockTaps)]),
         "nitro_head_backward": (I32, [VP, I32, I32, I32, VP, VP, VP, I32, VP, VP, VP]),
@@ -133,6 +134,7 @@ EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_set_conv_
            "nitro_set_conv_persistent", "nitro_set_aux_streams",
            "nitro_sync_status",
            "nitro_status_str", "nitro_block_query", "nitro_block_saved", "nitro_block_forward",
+           "nitro_block_forward_noalloc",
            "nitro_block_backward",
            "nitro_head_backward", "nitro_integer_sgd_step", "nitro_block_sgd_step",
            "nitro_net_block_view", "nitro_net_head_view", "nitro_net_query",
@@ -292,6 +294,13 @@ class Context:
             bp.w[j] = _p(w)
         check(LIB.nitro_block_forward(self.h, ctypes.byref(desc), ctypes.byref(bp), _p(x),
                                       _p(a_out), _p(state)), "nitro_block_forward")
+
+    def block_forward_noalloc(self, desc: BlockDesc, ws, x, a_out) -> None:
+        bp = BlockParams()
+        for j, w in enumerate(ws):
+            bp.w[j] = _p(w)
+        check(LIB.nitro_block_forward_noalloc(self.h, ctypes.byref(desc), ctypes.byref(bp), _p(x),
+                                              _p(a_out)), "nitro_block_forward_noalloc")
 
     def block_backward(self, desc: BlockDesc, ws, w_lr, x, a_out, labels, delta_out, state,
                        dws, dw_lr, taps: Optional[dict] = None) -> None:

@@ -119,3 +119,26 @@ def test_null_context_rejected():
     assert N.LIB.nitro_integer_sgd_step(None, None, None, 0, 1, 0, -1, 0) == N.EINVAL
     assert N.LIB.nitro_sync_status(None) == N.EINVAL
 
+
+def test_noalloc_forward_size_limit():
+    """nitro_block_forward_noalloc checks the block against its 64 MiB scratch before anything
+    else (no device work, no context needed): a VGG-style block at batch 1024 is rejected with
+    NITRO_EUNSUPPORTED, a small block gets as far as the missing context (EINVAL), and so does
+    one just under the limit."""
+    import ctypes
+    bp = N.BlockParams()
+    bp.w[0] = bp.w[1] = 1                       # never dereferenced: rejected on the host
+    one = ctypes.c_void_p(1)
+    big = N.block_desc(1024, 32, 32, [N.layer(N.CONV3X3, 64, 128), N.layer(N.CONV3X3, 128, 128)],
+                       False, 0, 10)
+    assert N.LIB.nitro_block_forward_noalloc(None, big, bp, one, one) == N.EUNSUPPORTED
+    small = N.block_desc(2, 8, 8, [N.layer(N.CONV3X3, 64, 128), N.layer(N.CONV3X3, 128, 128)],
+                         True, 0, 10)
+    assert N.LIB.nitro_block_forward_noalloc(None, small, bp, one, one) == N.EINVAL
+    # 256 x 32 x 32 x 64 twice (inner activations and codes) plus the last layer's pooled codes:
+    # about 38 MB, inside the limit
+    vgg1 = N.block_desc(256, 32, 32, [N.layer(N.CONV3X3, 3, 64), N.layer(N.CONV3X3, 64, 64)],
+                        True, 0, 10)
+    assert N.LIB.nitro_block_forward_noalloc(None, vgg1, bp, one, one) == N.EINVAL
+    bp.w[1] = None
+    assert N.LIB.nitro_block_forward_noalloc(None, small, bp, one, one) == N.EINVAL
