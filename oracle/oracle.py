@@ -25,7 +25,11 @@ Readings of passages that the paper leaves open (each is a switch or a documente
     ``Hyper.delta_fw_post_update`` takes them after it, the literal order of section 3.3);
   * every layer's scaling factor uses its own fan-in; learning and output layers are rescaled too
     but have no NITRO-ReLU;
-  * eta = gamma * lambda is formed in int64 (an explicit eta may override it).
+  * eta = gamma * lambda is formed in int64 (an explicit eta may override it);
+  * the learning layers of a conv block read its output max-pooled to at most d^lr features
+    (``learning_pool_window``: height and width halved in turn, first maximum of the window);
+    without d^lr they read the block output itself;
+  * a linear block after a conv block reads the conv output flattened in (h, w, c) order.
 """
 from __future__ import annotations
 
@@ -254,6 +258,48 @@ def maxpool2_bwd(dp, idx, full_shape):
     return v.reshape(N, H // 2, W // 2, 2, 2, C).transpose(0, 1, 3, 2, 4, 5).reshape(N, H, W, C)
 
 
+def learning_pool_window(c: int, h: int, w: int, d_lr: int):
+    """Window (kh, kw) of the learning layers' max-pool (the pooling of section 3.3 that turns a
+    block's activations a_l into z^mp, d^lr of Tab. 6). Reading: starting from the whole
+    resolution, the height and the width are halved in turn, the height first, until
+    c * (h / kh) * (w / kw) <= d_lr or neither can be halved; d_lr = 0 means no pooling."""
+    kh = kw = 1
+    turn_h = True
+    while d_lr > 0 and c * (h // kh) * (w // kw) > d_lr:
+        can_h = (h // kh) % 2 == 0
+        can_w = (w // kw) % 2 == 0
+        if not (can_h or can_w):
+            break
+        if (turn_h and can_h) or not can_w:
+            kh *= 2
+        else:
+            kw *= 2
+        turn_h = not turn_h
+    return kh, kw
+
+
+def maxpool_window(a, kh: int, kw: int):
+    """Non-overlapping kh x kw max-pool on NHWC. Returns (pooled, index 0 .. kh*kw-1 of the first
+    maximum in row-major window order)."""
+    a = np.asarray(a)
+    N, H, W, C = a.shape
+    v = a.reshape(N, H // kh, kh, W // kw, kw, C).transpose(0, 1, 3, 2, 4, 5)
+    v = v.reshape(N, H // kh, W // kw, kh * kw, C)
+    idx = np.argmax(v, axis=3)                # first occurrence of the maximum
+    pooled = np.take_along_axis(v, idx[:, :, :, None, :], axis=3)[:, :, :, 0, :]
+    return pooled, idx
+
+
+def maxpool_window_bwd(dp, idx, full_shape, kh: int, kw: int):
+    """Route each pooled gradient to the window position that won the forward max."""
+    N, H, W, C = full_shape
+    dp = np.asarray(dp, dtype=np.int64)
+    v = np.zeros((N, H // kh, W // kw, kh * kw, C), np.int64)
+    np.put_along_axis(v, idx[:, :, :, None, :], dp[:, :, :, None, :], axis=3)
+    v = v.reshape(N, H // kh, W // kw, kh, kw, C).transpose(0, 1, 3, 2, 4, 5)
+    return v.reshape(N, H, W, C)
+
+
 def one_hot32(labels, G: int):
     """The custom one-hot target: 32 at the label, 0 elsewhere (section 3.3.4, Appendix A)."""
     labels = np.asarray(labels, dtype=np.int64)
@@ -311,7 +357,11 @@ class BlockRecord:
     yhat: Optional[np.ndarray] = None       # learning-layer prediction, int32 values
     e: Optional[np.ndarray] = None          # local loss gradient
     dw_lr: Optional[np.ndarray] = None
-    delta_fw: Optional[np.ndarray] = None   # gradient at the block output
+    f: Optional[np.ndarray] = None          # learning-layer input: the block output, max-pooled
+    #                                         to at most d_lr features when d_lr is set
+    f_idx: Optional[np.ndarray] = None      # its window argmax (None: f is the block output)
+    f_window: tuple = (1, 1)
+    delta_fw: Optional[np.ndarray] = None   # gradient at the learning layer's input f
     g: List[np.ndarray] = field(default_factory=list)     # gradient at each layer's z (after ReLU')
     dw: List[np.ndarray] = field(default_factory=list)    # per forward layer, int64
     dx: Optional[np.ndarray] = None         # input gradient of the first layer (when asked for)
@@ -401,6 +451,7 @@ class Hyper:
     af_classes: int = 0          # G for the amplification factor when n_classes == 0
     eta_fw: int = -1             # explicit eta overrides (< 0: gamma * lambda)
     eta_lr: int = -1
+    d_lr: int = 0                # learning-layer input size of conv blocks (0: the block output)
     # alternative readings (both off by default):
     relu_grad_ste: bool = False  # NITRO-ReLU backward passes the gradient unchanged on its leaky
     #                              segment (straight through) instead of dividing by alpha_inv
@@ -451,7 +502,10 @@ class OracleNet:
         cur = x
         for b, (nl, pool, _) in enumerate(self.specs):
             fw, _ = self.index[b]
-            rec = block_forward(cur, [self.w[k] for k in fw], pool, self.hp.alpha_inv, self.hp.mode)
+            ws = [self.w[k] for k in fw]
+            if not _is_conv(ws[0]) and cur.ndim == 4:
+                cur = cur.reshape(cur.shape[0], -1)       # flatten in (h, w, c) order
+            rec = block_forward(cur, ws, pool, self.hp.alpha_inv, self.hp.mode)
             recs.append(rec)
             cur = rec.out
         return recs
@@ -479,7 +533,13 @@ class OracleNet:
             fw, lr = self.index[b]
             if not has_lr:
                 continue
-            f = rec.out.reshape(rec.out.shape[0], -1)
+            rec.f = rec.out
+            if rec.out.ndim == 4 and hp.d_lr > 0:
+                N_, H_, W_, C_ = rec.out.shape
+                rec.f_window = learning_pool_window(C_, H_, W_, hp.d_lr)
+                if rec.f_window != (1, 1):
+                    rec.f, rec.f_idx = maxpool_window(rec.out, *rec.f_window)
+            f = rec.f.reshape(rec.f.shape[0], -1)
             w_lr = self.w[lr]
             rec.yhat = learning_forward(f, w_lr, mode)
             rec.e = check_int32(loss_grad(rec.yhat, labels, G), "loss gradient")
@@ -488,7 +548,10 @@ class OracleNet:
                                     hp.eta_lr).astype(np.int32)
             w_delta = new_w[lr] if hp.delta_fw_post_update else w_lr       # default: pre-update
             rec.delta_fw = check_int32(linear_dx(rec.e, w_delta), "delta_fw")
-            block_backward(rec, [self.w[k] for k in fw], rec.delta_fw.reshape(rec.out.shape),
+            d_out = rec.delta_fw.reshape(rec.f.shape)
+            if rec.f_idx is not None:              # back through the learning layers' pooling
+                d_out = maxpool_window_bwd(d_out, rec.f_idx, rec.out.shape, *rec.f_window)
+            block_backward(rec, [self.w[k] for k in fw], d_out,
                            pool, hp.alpha_inv, mode, ste=hp.relu_grad_ste)
             for j, k in enumerate(fw):
                 new_w[k] = integer_sgd(self.w[k], rec.dw[j], hp.gamma_fw, hp.lambda_inv_fw, mode,

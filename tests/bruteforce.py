@@ -93,3 +93,23 @@ def maxpool(a):
                     P[n][i][j][c] = win[best]
                     I[n][i][j][c] = best
     return P, I
+
+
+def maxpool_window(a, kh, kw):
+    """kh x kw max-pool, stride (kh, kw): scan each window row by row and keep the first strict
+    maximum; returns (pooled, index of the winner within its window)."""
+    N, H, W, C = len(a), len(a[0]), len(a[0][0]), len(a[0][0][0])
+    P = [[[[0] * C for _ in range(W // kw)] for _ in range(H // kh)] for _ in range(N)]
+    I = [[[[0] * C for _ in range(W // kw)] for _ in range(H // kh)] for _ in range(N)]
+    for n in range(N):
+        for i in range(H // kh):
+            for j in range(W // kw):
+                for c in range(C):
+                    best, arg = None, 0
+                    for t in range(kh * kw):
+                        v = int(a[n][i * kh + t // kw][j * kw + t % kw][c])
+                        if best is None or v > best:
+                            best, arg = v, t
+                    P[n][i][j][c] = best
+                    I[n][i][j][c] = arg
+    return P, I

@@ -248,6 +248,60 @@ def test_inner_input_gradient_must_fit_int32():
         O.block_backward(rec, ws, np.array([[1 << 12, 1 << 12]]), False, 10, O.FLOOR)
 
 
+def test_learning_pool_windows():
+    g = gold("learning_pool.json")
+    for c, h, w, d, kh, kw in g["windows"]:
+        assert O.learning_pool_window(c, h, w, d) == (kh, kw), (c, h, w, d)
+
+
+@pytest.mark.parametrize("mode", ["floor", "trunc"])
+def test_learning_pool_step(mode):
+    """A conv block whose learning layer reads its output max-pooled to d_lr features: the
+    pooled input, the loss gradient routed back through that pooling, both updates."""
+    g = gold("learning_pool.json")
+    exp = g[mode]
+    hp = O.Hyper(gamma_inv=g["gamma_inv"], lambda_inv_fw=g["lambda_inv_fw"],
+                 lambda_inv_lr=g["lambda_inv_lr"], alpha_inv=g["alpha_inv"], n_classes=g["G"],
+                 mode=MODES[mode], d_lr=g["d_lr"])
+    net = O.OracleNet([(1, False, True)], False, [np.array(g["W"], np.int32),
+                                                 np.array(g["Wlr"], np.int32)], hp)
+    st = net.train_step(np.array(g["x"], np.int8), np.array(g["label"], np.int32))
+    b = st.blocks[0]
+    assert b.f_window == (2, 1)
+    assert b.f.reshape(-1).tolist() == exp["f"]
+    assert b.f_idx.reshape(-1).tolist() == exp["f_idx"]
+    assert b.yhat.tolist() == exp["yhat"]
+    assert b.e.tolist() == exp["e"]
+    assert b.dw_lr.tolist() == exp["dWlr"]
+    assert b.delta_fw.tolist() == exp["delta_fw"]
+    assert b.g[0][0, :, :, 0].tolist() == exp["g"]
+    assert b.dw[0][0, :, :, 0].tolist() == exp["dW"]
+    assert net.w[1].tolist() == exp["Wlr_new"]
+    assert net.w[0][0, :, :, 0].tolist() == exp["W_new"]
+
+
+@pytest.mark.parametrize("kh,kw", [(1, 1), (2, 1), (1, 2), (2, 2), (4, 2), (2, 4), (8, 4)])
+def test_maxpool_window_against_bruteforce(kh, kw):
+    rng = np.random.default_rng(kh * 10 + kw)
+    a = _rand(rng, (2, 8, 8, 3), -2, 2, np.int8)            # a narrow range: many ties
+    p, i = O.maxpool_window(a, kh, kw)
+    bp, bi = BF.maxpool_window(a.tolist(), kh, kw)
+    assert p.tolist() == bp and i.tolist() == bi
+    dp = _rand(rng, p.shape, -1000, 1000)
+    full = O.maxpool_window_bwd(dp, i, a.shape, kh, kw)
+    assert full.sum() == dp.sum()
+    # every pooled gradient lands on its window's winner
+    for n, y, x, c in [(0, 0, 0, 0), (1, 8 // kh - 1, 8 // kw - 1, 2)]:
+        t = int(i[n, y, x, c])
+        assert full[n, y * kh + t // kw, x * kw + t % kw, c] == dp[n, y, x, c]
+
+
+def test_maxpool_window_two_by_two_is_the_forward_pool():
+    rng = np.random.default_rng(13)
+    a = _rand(rng, (2, 6, 4, 5), -3, 3, np.int8)
+    assert all(np.array_equal(u, v) for u, v in zip(O.maxpool_window(a, 2, 2), O.maxpool2(a)))
+
+
 # ---------------------------------------------------------------- brute force, tiny shapes
 
 def _rand(rng, shape, lo, hi, dtype=np.int64):
