@@ -69,7 +69,7 @@ typedef enum { NITRO_ROUND_FLOOR = 0, NITRO_ROUND_TRUNC = 1 } nitro_round;
 typedef enum { NITRO_CONV3X3 = 0, NITRO_LINEAR = 1 } nitro_layer_kind;
 
 #define NITRO_MAX_LAYERS 4
-#define NITRO_MAX_BLOCKS 8
+#define NITRO_MAX_BLOCKS 16
 
 typedef struct nitro_ctx nitro_ctx;
 
@@ -123,6 +123,14 @@ typedef struct {
                                               the caller supplies the output gradient          */
     int32_t alpha_inv;                     /* NITRO-ReLU inverse slope, >= 2                    */
     int32_t round;                         /* nitro_round                                       */
+    int32_t d_lr;                          /* learning-layer input of a conv block: 0 reads the
+                                              block output; > 0 reads it max-pooled to at most
+                                              d_lr features (d^lr of Tab. 6): non-overlapping
+                                              kh x kw windows, kh and kw doubled in turn (kh
+                                              first) while c (h/kh) (w/kw) > d_lr and a side
+                                              can still be halved; the first maximum of a
+                                              window (row-major) wins and takes the gradient.
+                                              Ignored for linear blocks                          */
 } nitro_block_desc;
 
 typedef struct {
@@ -139,7 +147,9 @@ typedef struct {
 typedef struct {
     int32_t *yhat;                         /* [n][G] learning-layer prediction                 */
     int32_t *e;                            /* [n][G] loss gradient yhat - y                     */
-    int32_t *delta;                        /* gradient at the block output (pooled), NHWC      */
+    int32_t *delta;                        /* delta^fw at the learning layer's input: the block
+                                              output (pooled), NHWC, or with d_lr its learning
+                                              pooling [n][h/kh][w/kw][c]                         */
     int32_t *g[NITRO_MAX_LAYERS];          /* gradient at layer j's pre-activation z_j, NHWC   */
     int64_t *dx;                           /* input gradient of the first layer, NHWC; int64
                                               since no gradient leaves a block in the method,
@@ -252,7 +262,9 @@ nitro_status nitro_block_sgd_step(nitro_ctx *ctx, const nitro_block_desc *desc,
 typedef struct {
     int32_t n_blocks;                          /* 1..NITRO_MAX_BLOCKS                           */
     nitro_block_desc block[NITRO_MAX_BLOCKS];  /* shapes must chain: block b+1 reads block b's
-                                                  output; every block has n_classes = G > 0    */
+                                                  output (a linear block after a conv block
+                                                  reads it flattened in (h, w, c) order, c_in =
+                                                  h w c); every block has n_classes = G > 0    */
     int32_t head;                              /* 1: output layer IntLinear(d_L -> G)           */
 } nitro_net_desc;
 

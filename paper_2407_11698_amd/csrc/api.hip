@@ -158,7 +158,9 @@ struct BlockGeom {
     int J;
     LayerGeom L[NITRO_MAX_LAYERS];
     int64_t out_elems;        // block output (pooled if maxpool), whole batch
-    int64_t d;                // per-sample block output size (learning layer input)
+    int64_t d;                // per-sample learning layer input size
+    int64_t out_d;            // per-sample block output size
+    int lr_kh, lr_kw;         // learning layers' pooling window (1, 1: none)
     // state buffer offsets
     size_t act[NITRO_MAX_LAYERS];
     size_t code[NITRO_MAX_LAYERS];
@@ -172,6 +174,7 @@ struct BlockGeom {
     size_t part;                   // weight-gradient scratch: split-K partial sums (int64)
     bool lr_mfma;                  // learning layer on the MFMA path
     size_t lwf, lwt, lft, lpart, lepad, let;   // its scratch
+    size_t lf, lfc;                // learning-pooled block output and its window indices
     size_t yhat, e, delta, g0, g1;
     size_t total;
 };
@@ -182,7 +185,7 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     if (d->n < 1 || d->n_layers < 1 || d->n_layers > NITRO_MAX_LAYERS) return NITRO_EINVAL;
     if (d->alpha_inv < 2) return NITRO_EINVAL;
     if (d->round != NITRO_ROUND_FLOOR && d->round != NITRO_ROUND_TRUNC) return NITRO_EINVAL;
-    if (d->n_classes < 0 || (d->maxpool != 0 && d->maxpool != 1)) return NITRO_EINVAL;
+    if (d->n_classes < 0 || (d->maxpool != 0 && d->maxpool != 1) || d->d_lr < 0) return NITRO_EINVAL;
     const int kind = d->layer[0].kind;
     if (kind != NITRO_CONV3X3 && kind != NITRO_LINEAR) return NITRO_EINVAL;
     const bool conv = kind == NITRO_CONV3X3;
@@ -224,6 +227,14 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     }
     g->d = d->maxpool ? (int64_t)(d->h / 2) * (d->w / 2) * c : hw * c;
     g->out_elems = (int64_t)d->n * g->d;
+    g->out_d = g->d;
+    g->lr_kh = g->lr_kw = 1;
+    if (conv && d->n_classes > 0 && d->d_lr > 0) {
+        const int hb = d->maxpool ? d->h / 2 : d->h, wb = d->maxpool ? d->w / 2 : d->w;
+        lr_pool_window(c, hb, wb, d->d_lr, &g->lr_kh, &g->lr_kw);
+        g->d = (int64_t)(hb / g->lr_kh) * (wb / g->lr_kw) * c;
+    }
+    const bool lrpool = g->lr_kh * g->lr_kw > 1;
     // state buffer layout
     size_t off = 0;
     int64_t gmax = 0;
@@ -246,7 +257,7 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     }
     g->xpad = off; off = align256(off + (size_t)xpadb);
     g->slots = off; off = align256(off + 16 * SLOT_WORDS * 4);
-    g->lr_mfma = d->n_classes > 0 &&
+    g->lr_mfma = d->n_classes > 0 && !lrpool &&
                  mfma_learning_ok(d->n, g->d, d->n_classes, d->layer[g->J - 1].c_out);
     {
         LearningScratch ls{};
@@ -258,6 +269,8 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
         g->lepad = off; off = align256(off + (size_t)ls.epad_bytes);
         g->let = off;   off = align256(off + (size_t)ls.et_bytes);
     }
+    g->lf = off;  off = align256(off + (size_t)(lrpool ? d->n * g->d : 0));
+    g->lfc = off; off = align256(off + (size_t)(lrpool ? d->n * g->d : 0));
     int64_t gtb = 0, xpb = 0, parts = 0, gnb = 0;
     for (int j = 0; j < g->J && conv; j++) {
         const ConvShape &sh = g->L[j].sh;
@@ -420,6 +433,23 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                                  at(state, g.code[J - 1]), rp, LJ.sh.h, LJ.sh.w, LJ.sh.co,
                                  desc->maxpool != 0, gb[0], taps ? taps->delta : nullptr, yhat, e,
                                  gr->dw_lr, ctx->flags, prepacked, g_pooled);
+            have_g = true;
+        } else if (g.lr_kh * g.lr_kw > 1) {
+            // the learning layer reads the block output max-pooled to d features; its delta^fw
+            // goes back through that pooling, the block's pool and NITRO-ReLU in one pass
+            int32_t *dl = (int32_t *)at(state, g.delta);
+            int8_t *f = (int8_t *)at(state, g.lf);
+            uint8_t *fc = at(state, g.lfc);
+            LrPool lp{n, desc->maxpool ? LJ.sh.h / 2 : LJ.sh.h, desc->maxpool ? LJ.sh.w / 2 : LJ.sh.w,
+                      LJ.sh.co, g.lr_kh, g.lr_kw};
+            launch_lr_pool(s, lp, a_out, f, fc);
+            launch_linear_fwd_loss(s, n, (int)g.d, G, f, p->w_lr, sf, labels, yhat, e, ctx->flags);
+            launch_linear_dw(s, n, (int)g.d, G, e, f, gr->dw_lr);
+            launch_linear_dx(s, n, (int)g.d, G, e, p->w_lr, nullptr, rp, dl, nullptr, ctx->flags);
+            if (taps && taps->delta)
+                (void)hipMemcpyAsync(taps->delta, dl, (size_t)n * g.d * 4, hipMemcpyDeviceToDevice, s);
+            launch_lr_unpool_relu_bwd(s, lp, desc->maxpool != 0, dl, fc, at(state, g.code[J - 1]), rp,
+                                      gb[0], slots + (4 + J - 1) * SLOT_WORDS, ctx->flags);
             have_g = true;
         } else {
             int32_t *dl = (int32_t *)at(state, g.delta);
@@ -596,10 +626,14 @@ nitro_status net_geom(const nitro_net_desc *net, NetGeom *g)
             const nitro_layer &pl = pd.layer[pd.n_layers - 1];
             const bool pconv = pl.kind == NITRO_CONV3X3;
             const bool conv = d.layer[0].kind == NITRO_CONV3X3;
-            if (pconv != conv) return NITRO_EINVAL;
+            if (!pconv && conv) return NITRO_EINVAL;
             if (conv) {
                 const int ph = pd.maxpool ? pd.h / 2 : pd.h, pw = pd.maxpool ? pd.w / 2 : pd.w;
                 if (d.h != ph || d.w != pw || d.layer[0].c_in != pl.c_out) return NITRO_EINVAL;
+            } else if (pconv) {
+                // a linear block reads the conv block output flattened in (h, w, c) order
+                const int64_t ph = pd.maxpool ? pd.h / 2 : pd.h, pw = pd.maxpool ? pd.w / 2 : pd.w;
+                if ((int64_t)d.layer[0].c_in != ph * pw * pl.c_out) return NITRO_EINVAL;
             } else if (d.layer[0].c_in != pl.c_out) {
                 return NITRO_EINVAL;
             }
@@ -614,7 +648,7 @@ nitro_status net_geom(const nitro_net_desc *net, NetGeom *g)
     }
     const int L = net->n_blocks - 1;
     const int n = net->block[0].n;
-    g->hd = g->b[L].d;
+    g->hd = g->b[L].out_d;
     g->hyhat = off; off = align256(off + (size_t)(net->head ? n * G : 0) * 4);
     g->he = off;    off = align256(off + (size_t)(net->head ? n * G : 0) * 4);
     g->hdw = off;   off = align256(off + (size_t)(net->head ? G * g->hd : 0) * 8);

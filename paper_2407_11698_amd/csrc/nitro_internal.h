@@ -493,6 +493,21 @@ void launch_learning_mfma(hipStream_t s, int n, int64_t d, int G, const int8_t *
                           int32_t *yhat, int32_t *e, int64_t *dw, uint32_t *flags, bool prepacked = false,
                           bool g_pooled = false);
 
+// ---- learning layers' max-pooling (lrpool.hip)
+struct LrPool {
+    int n, h, w, c;       // the block output [n][h][w][c] (after the block's own pool)
+    int kh, kw;           // window; the pooled input of the learning layer is [n][h/kh][w/kw][c]
+};
+// Window of the learning layers' pooling for a block output c x h x w and d_lr (0: none):
+// kh, kw doubled in turn (kh first) while c (h/kh)(w/kw) > d_lr and a side can be halved.
+void lr_pool_window(int c, int h, int w, int d_lr, int *kh, int *kw);
+void launch_lr_pool(hipStream_t s, const LrPool &p, const int8_t *a, int8_t *f, uint8_t *fcode);
+// g (the last layer's pre-activation gradient, full resolution) from delta_f (the gradient at the
+// pooled learning-layer input), fcode, and the last layer's codes (pooled: argmax | region << 2)
+void launch_lr_unpool_relu_bwd(hipStream_t s, const LrPool &p, bool pool, const int32_t *delta_f,
+                               const uint8_t *fcode, const uint8_t *code, const Relu &rp,
+                               int32_t *g, uint32_t *gmax, uint32_t *flags);
+
 // ---- few input channels (conv_smallc.hip)
 bool smallc_fwd_ok(const ConvShape &sh);
 bool smallc_dw_ok(const ConvShape &sh);

@@ -20,7 +20,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("NITRO_LIBRARY") or os.path.join(HERE, "libnitro.so")
 
 MAX_LAYERS = 4
-MAX_BLOCKS = 8
+MAX_BLOCKS = 16
 CONV3X3 = 0
 LINEAR = 1
 ROUND_FLOOR = 0
@@ -46,7 +46,7 @@ class Layer(ctypes.Structure):
 class BlockDesc(ctypes.Structure):
     _fields_ = [("n", I32), ("h", I32), ("w", I32), ("n_layers", I32),
                 ("layer", Layer * MAX_LAYERS), ("maxpool", I32), ("n_classes", I32),
-                ("alpha_inv", I32), ("round", I32)]
+                ("alpha_inv", I32), ("round", I32), ("d_lr", I32)]
 
 
 class BlockParams(ctypes.Structure):
@@ -164,7 +164,7 @@ def layer(kind: int, c_in: int, c_out: int) -> Layer:
 
 
 def block_desc(n: int, h: int, w: int, layers: Sequence[Layer], maxpool: bool, n_classes: int,
-               alpha_inv: int, round_mode: int = ROUND_FLOOR) -> BlockDesc:
+               alpha_inv: int, round_mode: int = ROUND_FLOOR, d_lr: int = 0) -> BlockDesc:
     d = BlockDesc()
     d.n, d.h, d.w = n, h, w
     d.n_layers = len(layers)
@@ -174,6 +174,7 @@ def block_desc(n: int, h: int, w: int, layers: Sequence[Layer], maxpool: bool, n
     d.n_classes = n_classes
     d.alpha_inv = alpha_inv
     d.round = round_mode
+    d.d_lr = d_lr
     return d
 
 

@@ -26,7 +26,8 @@ def block_descs(wl: Workload, round_mode: int = N.ROUND_FLOOR) -> List[N.BlockDe
             h = w = 1
             layers = [N.layer(N.LINEAR, ly.d_in, ly.d_out) for ly in blk.layers]
         descs.append(N.block_desc(wl.batch, h, w, layers, blk.maxpool,
-                                  wl.n_classes if blk.learning else 0, wl.alpha_inv, round_mode))
+                                  wl.n_classes if blk.learning else 0, wl.alpha_inv, round_mode,
+                                  wl.d_lr))
     return descs
 
 
@@ -91,7 +92,7 @@ class GpuNet:
                "e": self._at(ptrs["e"], (n, G), torch.int32),
                "dw": [self._at(ptrs["dw"][j], tuple(w.shape), torch.int64)
                       for j, w in enumerate(self.w[self._first_weight(b):self._first_weight(b) + len(blk.layers)])],
-               "dw_lr": self._at(ptrs["dw_lr"], (G, int(np.prod(out))), torch.int64)}
+               "dw_lr": self._at(ptrs["dw_lr"], (G, self.wl.learning_dim(b)), torch.int64)}
         return res
 
     def head_view(self) -> dict:

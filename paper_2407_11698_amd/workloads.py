@@ -91,6 +91,8 @@ class Workload:
     head_init: Init = Init("kaiming")
     af_classes: int = 0                # G used for the amplification factor when n_classes == 0
     delta_bound: int = 0               # stress case: |delta| <= delta_bound at the ReLU output
+    d_lr: int = 0                      # learning-layer input size of conv blocks (d^lr, Tab. 6);
+    #                                    0: the learning layer reads the block output
 
     # ---- derived shapes (bookkeeping only) ----
     @property
@@ -111,21 +113,47 @@ class Workload:
                     h, w = h // 2, w // 2
                 out = (c, h, w)
             else:
-                (d,) = cur
+                d = int(np.prod(cur))          # a conv output is read flattened, (h, w, c) order
                 for ly in blk.layers:
-                    assert ly.d_in == d
+                    assert ly.d_in == d, (ly, cur)
                     d = ly.d_out
                 out = (d,)
             shapes.append((cur, out))
             cur = out
         return shapes
 
+    def learning_window(self, b: int):
+        """Window (kh, kw) of block b's learning-layer max-pooling (1, 1: none). Shape
+        bookkeeping of the library's d_lr rule: kh and kw are doubled in turn, kh first, while
+        c (h / kh)(w / kw) > d_lr and a side can still be halved."""
+        _, out = self.block_shapes()[b]
+        if len(out) != 3 or not self.d_lr or not self.blocks[b].learning:
+            return 1, 1
+        c, h, w = out
+        kh = kw = 1
+        turn_h = True
+        while c * (h // kh) * (w // kw) > self.d_lr:
+            can_h, can_w = (h // kh) % 2 == 0, (w // kw) % 2 == 0
+            if not (can_h or can_w):
+                break
+            if (turn_h and can_h) or not can_w:
+                kh *= 2
+            else:
+                kw *= 2
+            turn_h = not turn_h
+        return kh, kw
+
     def learning_dim(self, b: int) -> int:
         _, out = self.block_shapes()[b]
+        kh, kw = self.learning_window(b)
+        if len(out) == 3:
+            return out[0] * (out[1] // kh) * (out[2] // kw)
         return int(np.prod(out))
 
     def head_dim(self) -> int:
-        return self.learning_dim(len(self.blocks) - 1)
+        """Input size of the output layer: the last block's output, flattened."""
+        _, out = self.block_shapes()[-1]
+        return int(np.prod(out))
 
 
 U127 = Init("uniform", 127)
@@ -176,8 +204,48 @@ CONV_STRESS = Workload(
     n_classes=0, head=False, gamma_inv=512, lambda_inv_fw=25000, lambda_inv_lr=3000,
     alpha_inv=10, steps=20, af_classes=10, delta_bound=1 << 15)
 
-WORKLOADS = {w.name: w for w in (TINY_CNN, MLP, SMALL_CNN, VGG_CNN, CONV_STRESS)}
+# The paper's own architectures (Tab. 1) with the hyper-parameters of Tab. 6 (batch 64, gamma_inv
+# 512, the CIFAR-10 or MNIST row). Every IntConv2D with its NITRO-ReLU (and the MaxPool2D that
+# follows it, if any) is one local-loss block; every hidden IntLinear is an integer linear block;
+# the last IntLinear is the output layer. Conv blocks' learning layers read the block output
+# max-pooled to at most d^lr = 4096 features.
+def _vgg(name, convs, lam_fw, lam_lr):
+    blocks = []
+    c = 3
+    for co, pool in convs:
+        blocks.append(Block((Conv3x3(c, co),), maxpool=pool, learning=True))
+        c = co
+    blocks.append(Block((Linear(512 * 2 * 2, 1024),), maxpool=False, learning=True))
+    return Workload(name=name, batch=64, in_shape=(3, 32, 32), blocks=tuple(blocks), n_classes=10,
+                    head=True, gamma_inv=512, lambda_inv_fw=lam_fw, lambda_inv_lr=lam_lr,
+                    alpha_inv=10, steps=10, d_lr=4096)
+
+
+VGG8B = _vgg("vgg8b_cifar10_b64",
+             [(128, False), (256, True), (256, False), (512, True), (512, True), (512, True)],
+             25000, 3000)
+VGG11B = _vgg("vgg11b_cifar10_b64",
+              [(128, False), (128, False), (128, False), (256, True), (256, False), (512, True),
+               (512, False), (512, True), (512, True)], 28000, 4500)
+MLP3 = Workload(
+    name="mlp3_784_1024x3_10_b64", batch=64, in_shape=(784,),
+    blocks=(Block((Linear(784, 1024),), maxpool=False, learning=True),
+            Block((Linear(1024, 1024),), maxpool=False, learning=True),
+            Block((Linear(1024, 1024),), maxpool=False, learning=True)),
+    n_classes=10, head=True, gamma_inv=512, lambda_inv_fw=28000, lambda_inv_lr=5000,
+    alpha_inv=10, steps=10)
+MLP4 = Workload(
+    name="mlp4_1024_3000x3_10_b64", batch=64, in_shape=(1024,),
+    blocks=(Block((Linear(1024, 3000),), maxpool=False, learning=True),
+            Block((Linear(3000, 3000),), maxpool=False, learning=True),
+            Block((Linear(3000, 3000),), maxpool=False, learning=True)),
+    n_classes=10, head=True, gamma_inv=512, lambda_inv_fw=19000, lambda_inv_lr=7500,
+    alpha_inv=10, steps=10)
+
+WORKLOADS = {w.name: w for w in (TINY_CNN, MLP, SMALL_CNN, VGG_CNN, CONV_STRESS, VGG8B, VGG11B,
+                                 MLP3, MLP4)}
 BY_INDEX = (TINY_CNN, MLP, SMALL_CNN, VGG_CNN, CONV_STRESS)
+PAPER_NETS = (VGG8B, VGG11B, MLP3, MLP4)
 
 
 def scaled(wl: Workload, batch: int) -> Workload:

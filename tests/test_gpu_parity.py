@@ -37,7 +37,7 @@ def rand(rng, shape, lo, hi, dtype):
 
 
 def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dmax=1 << 15,
-              conv=True, tap_last_g=True):
+              conv=True, tap_last_g=True, d_lr=0):
     """One nitro_block_forward + nitro_block_backward against the oracle's block functions.
     tap_last_g=False leaves the last layer's g untapped (the library may then keep it pooled)."""
     print("block case", dict(n=n, h=h, w=w, chans=chans, pool=maxpool, G=G, alpha=alpha,
@@ -53,23 +53,32 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
         ws = [rand(rng, (chans[j + 1], chans[j]), -wmax, wmax, np.int32) for j in range(J)]
         layers = [N.layer(N.LINEAR, chans[j], chans[j + 1]) for j in range(J)]
         hh = ww = 1
-    desc = N.block_desc(n, hh, ww, layers, maxpool, G, alpha, nm)
+    desc = N.block_desc(n, hh, ww, layers, maxpool, G, alpha, nm, d_lr)
     # oracle
     rec = O.block_forward(x, ws, maxpool, alpha, om)
     out_shape = rec.out.shape
-    d = int(np.prod(out_shape[1:]))
+    f = rec.out
+    win = (1, 1)
+    if conv and G and d_lr:
+        win = O.learning_pool_window(out_shape[3], out_shape[1], out_shape[2], d_lr)
+        if win != (1, 1):
+            f, f_idx = O.maxpool_window(rec.out, *win)
+    f_shape = f.shape
+    d = int(np.prod(f_shape[1:]))
     labels = rng.integers(0, max(G, 1), n).astype(np.int32)
     want_dx, expect_overflow = True, False
     w_lr = rand(rng, (G, d), -wmax, wmax, np.int32) if G else None
     delta = None if G else rand(rng, out_shape, -dmax, dmax, np.int32)
     try:
         if G > 0:
-            f = rec.out.reshape(n, d)
-            rec.yhat = O.learning_forward(f, w_lr, om)
+            ff = f.reshape(n, d)
+            rec.yhat = O.learning_forward(ff, w_lr, om)
             rec.e = O.check_int32(O.loss_grad(rec.yhat, labels, G), "e")
-            rec.dw_lr = O.linear_dw(rec.e, f)
+            rec.dw_lr = O.linear_dw(rec.e, ff)
             rec.delta_fw = O.check_int32(O.linear_dx(rec.e, w_lr), "delta")
-            delta = rec.delta_fw.reshape(out_shape)
+            delta = rec.delta_fw.reshape(f_shape)
+            if win != (1, 1):
+                delta = O.maxpool_window_bwd(delta, f_idx, out_shape, *win)
         try:
             O.block_backward(rec, ws, delta, maxpool, alpha, om, want_dx=True)
         except OverflowError:
@@ -91,7 +100,7 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
     if G:
         taps["yhat"] = torch.empty((n, G), dtype=torch.int32, device=DEV)
         taps["e"] = torch.empty((n, G), dtype=torch.int32, device=DEV)
-        taps["delta"] = torch.empty(out_shape, dtype=torch.int32, device=DEV)
+        taps["delta"] = torch.empty(f_shape, dtype=torch.int32, device=DEV)
     ctx.block_backward(desc, wd, dev(w_lr) if G else None, xd, a_out,
                        dev(labels) if G else None, None if G else dev(delta), state, dws, dw_lr,
                        taps)
@@ -104,7 +113,7 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
         assert np.array_equal(host(taps["yhat"]), rec.yhat), "yhat"
         assert np.array_equal(host(taps["e"]), rec.e), "e"
         assert np.array_equal(host(dw_lr), rec.dw_lr), "dW learning"
-        assert np.array_equal(host(taps["delta"]), rec.delta_fw.reshape(out_shape)), "delta_fw"
+        assert np.array_equal(host(taps["delta"]), rec.delta_fw.reshape(f_shape)), "delta_fw"
     for j in range(J):
         if taps["g"][j] is not None:
             assert np.array_equal(host(taps["g"][j]), rec.g[j]), "g layer %d" % j
@@ -243,6 +252,28 @@ def test_linear_block(ctx, chans, G, wmax, modes):
               modes[1], wmax=wmax, conv=False)
 
 
+# conv blocks whose learning layer reads the block output max-pooled to at most d_lr features
+# (windows (4, 2), (2, 2), (8, 4), (1, 2) with an odd height, none), pooled and unpooled blocks,
+# one and two conv layers
+LR_POOL_CASES = [
+    # n, h, w, chans, pool, G, d_lr
+    (2, 8, 8, [16, 32], True, 10, 64),
+    (3, 8, 8, [16, 32], False, 10, 512),
+    (2, 32, 32, [3, 128], False, 10, 4096),
+    (1, 5, 6, [8, 16], False, 4, 250),
+    (2, 16, 16, [32, 64, 64], True, 10, 1024),
+    (2, 8, 8, [16, 32], True, 10, 100000),
+]
+
+
+@pytest.mark.parametrize("case", LR_POOL_CASES)
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_conv_block_learning_pool(ctx, case, modes):
+    n, h, w, chans, pool, G, d_lr = case
+    rng = np.random.default_rng(hash((n, h, w, tuple(chans), G, d_lr)) % (1 << 31))
+    run_block(ctx, rng, n, h, w, chans, pool, G, 10, modes[0], modes[1], wmax=300, d_lr=d_lr)
+
+
 def test_gradient_overflow_is_flagged(ctx):
     """A block whose error signal cannot fit int32: the oracle raises, the GPU flags it."""
     rng = np.random.default_rng(77)
@@ -317,7 +348,7 @@ def test_head(ctx, modes):
 
 def oracle_net(wl, weights, om):
     hp = O.Hyper(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr, wl.alpha_inv, wl.n_classes,
-                 mode=om, af_classes=wl.af_classes)
+                 mode=om, af_classes=wl.af_classes, d_lr=wl.d_lr)
     specs = [(len(b.layers), b.maxpool, b.learning) for b in wl.blocks]
     return O.OracleNet(specs, wl.head, weights, hp)
 
@@ -395,6 +426,17 @@ def test_train_small_cnn(ctx, modes):
 @pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
 def test_train_vgg_reduced_batch(ctx, modes):
     check_training(ctx, WL.scaled(WL.VGG_CNN, 4), 10, *modes)
+
+
+@pytest.mark.parametrize("wl,steps", [(WL.scaled(WL.VGG8B, 2), 3), (WL.scaled(WL.VGG11B, 2), 2),
+                                      (WL.MLP3, 10), (WL.scaled(WL.MLP4, 8), 3)],
+                         ids=["vgg8b_b2", "vgg11b_b2", "mlp3_b64", "mlp4_b8"])
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_train_paper_nets(ctx, wl, steps, modes):
+    """The paper's architectures (Tab. 1, Tab. 6 hyper-parameters): learning layers on the
+    block outputs max-pooled to 4096 features, a linear block after the conv blocks, the
+    output layer; every workspace tensor and weight after every step."""
+    check_training(ctx, wl, steps, *modes)
 
 
 @pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
