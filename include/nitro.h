@@ -256,6 +256,27 @@ nitro_status nitro_block_sgd_step(nitro_ctx *ctx, const nitro_block_desc *desc,
                                   const nitro_block_grads *grads, const nitro_hparams *hp);
 
 /* ------------------------------------------------------------------------------------------ */
+/* Integer pre-processing of the input data (Appendix A)                                      */
+/* ------------------------------------------------------------------------------------------ */
+
+/* Size in bytes of the device workspace nitro_preprocess needs for `count` elements (at most
+ * about 1 MiB). EINVAL for count < 1 or count > 2^40. */
+nitro_status nitro_preprocess_query(int64_t count, size_t *workspace_bytes);
+
+/* Integer-only normalisation of a whole dataset of unsigned bytes (Appendix A):
+ *   mu = sum_i x_i / N,  omega = sum_i |x_i - mu| / N,  out_i = (x_i - mu) * 51 / omega,
+ * over all N = count elements, every division rounded per `round`. Readings: mu and omega are
+ * single numbers for the dataset; an omega that rounds to 0 is replaced by 1; out is int8, so a
+ * value outside [-127, 127] is clamped to it.
+ *   x          device, count bytes (any alignment);
+ *   out        device, count int8 (may be x itself: normalisation in place);
+ *   stats      device, 3 int64 written: mu, the omega divided by, the number of clamped values;
+ *   workspace  device, nitro_preprocess_query bytes, any contents (overwritten).
+ * Asynchronous on the context's stream; EINVAL for a null pointer, a bad count or rounding. */
+nitro_status nitro_preprocess(nitro_ctx *ctx, const uint8_t *x, int64_t count, int32_t round,
+                              int8_t *out, int64_t *stats, void *workspace);
+
+/* ------------------------------------------------------------------------------------------ */
 /* A whole network: one training iteration                                                    */
 /* ------------------------------------------------------------------------------------------ */
 

@@ -338,6 +338,36 @@ def kaiming_bound(fan_in: int) -> int:
 
 
 # ---------------------------------------------------------------------------------------------
+# integer pre-processing of the input data (Appendix A)
+# ---------------------------------------------------------------------------------------------
+
+@dataclass
+class Preprocessed:
+    mu: int                   # integer mean of the dataset
+    omega: int                # integer mean absolute deviation (the divisor used: at least 1)
+    xhat: np.ndarray          # normalised data, int8
+    saturated: int            # elements whose normalised value left [-127, 127]
+
+
+def preprocess(x, mode: int = FLOOR) -> Preprocessed:
+    """Appendix A: mu = sum_i x_i / N, omega = sum_i |x_i - mu| / N, xhat_i = (x_i - mu) 51 / omega,
+    every division by the rounding rule, over all N elements of the dataset.
+    Readings: mu and omega are single numbers for the whole dataset; a dataset whose omega
+    rounds to 0 is divided by 1; xhat is stored as int8, so values outside [-127, 127] are
+    clamped to it (and counted)."""
+    x = np.asarray(x, dtype=np.int64).reshape(-1)
+    n = x.size
+    if n == 0:
+        raise ValueError("empty dataset")
+    mu = int(idiv(x.sum(), n, mode))
+    omega = int(idiv(np.abs(x - mu).sum(), n, mode))
+    div = max(omega, 1)
+    v = idiv((x - mu) * 51, div, mode)
+    sat = int(np.count_nonzero((v < -127) | (v > 127)))
+    return Preprocessed(mu=mu, omega=div, xhat=np.clip(v, -127, 127).astype(np.int8), saturated=sat)
+
+
+# ---------------------------------------------------------------------------------------------
 # whole-step composition (section 3.3, training procedure)
 # ---------------------------------------------------------------------------------------------
 

@@ -944,6 +944,24 @@ nitro_status nitro_block_sgd_step(nitro_ctx *ctx, const nitro_block_desc *desc,
     return hip_status();
 }
 
+nitro_status nitro_preprocess_query(int64_t count, size_t *workspace_bytes)
+{
+    if (!workspace_bytes || count < 1 || count > ((int64_t)1 << 40)) return NITRO_EINVAL;
+    *workspace_bytes = preprocess_workspace(count);
+    return NITRO_OK;
+}
+
+nitro_status nitro_preprocess(nitro_ctx *ctx, const uint8_t *x, int64_t count, int32_t round,
+                              int8_t *out, int64_t *stats, void *workspace)
+{
+    if (!ctx || !x || !out || !stats || !workspace) return NITRO_EINVAL;
+    if (count < 1 || count > ((int64_t)1 << 40)) return NITRO_EINVAL;
+    if (round != NITRO_ROUND_FLOOR && round != NITRO_ROUND_TRUNC) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+    launch_preprocess(ctx->stream, x, count, round, out, stats, workspace);
+    return hip_status();
+}
+
 nitro_status nitro_net_block_view(const nitro_net_desc *net, void *workspace, int32_t b,
                                   nitro_block_view *out)
 {

@@ -508,6 +508,15 @@ void launch_lr_unpool_relu_bwd(hipStream_t s, const LrPool &p, bool pool, const 
                                const uint8_t *fcode, const uint8_t *code, const Relu &rp,
                                int32_t *g, uint32_t *gmax, uint32_t *flags);
 
+// ---- integer pre-processing of a uint8 dataset (preprocess.hip)
+constexpr int PRE_MAX_GROUPS = 1024;
+int preprocess_groups(int64_t count);
+size_t preprocess_workspace(int64_t count);          // bytes: partial histograms and the table
+// out = clamp((x - mu) 51 / omega) with mu, omega of the whole dataset; stats = {mu, omega,
+// saturated count} (device, int64); out may be x itself
+void launch_preprocess(hipStream_t s, const uint8_t *x, int64_t count, int round, int8_t *out,
+                       int64_t *stats, void *workspace);
+
 // ---- few input channels (conv_smallc.hip)
 bool smallc_fwd_ok(const ConvShape &sh);
 bool smallc_dw_ok(const ConvShape &sh);

@@ -1,0 +1,160 @@
+// Integer-only pre-processing of an unsigned 8-bit dataset (Appendix A):
+//   mu = sum x / N,  omega = sum |x - mu| / N,  xhat = (x - mu) 51 / omega.
+// A byte has only 256 values, so both sums follow from the dataset's histogram and xhat is a
+// 256-entry table: three passes, of which two stream the data.
+//   1. k_pre_hist: per-workgroup histograms (each wave counts into its own LDS copy), 16 bytes per
+//      thread and load, written as partial histograms (no global atomics);
+//   2. k_pre_stats (one workgroup): the histogram, mu, omega and the table; the divisions by N
+//      and omega are done once, here;
+//   3. k_pre_map: out = table[x], 16 bytes per thread and load/store, the table in LDS.
+// HBM traffic: N bytes read twice, N written.
+#include "nitro_internal.h"
+
+namespace nitro {
+
+namespace {
+
+// [0, head) and [head + 16 nvec, count) are handled byte by byte; the middle as 16-byte vectors
+struct Span {
+    int64_t head, nvec;
+};
+
+__host__ __device__ inline Span span_of(const void *p, int64_t count)
+{
+    const int64_t mis = (int64_t)((uintptr_t)p & 15);
+    int64_t head = mis ? 16 - mis : 0;
+    if (head > count) head = count;
+    return Span{head, (count - head) / 16};
+}
+
+}  // namespace
+
+__global__ __launch_bounds__(256) void k_pre_hist(const uint8_t *__restrict__ x, int64_t count,
+                                                  uint32_t *__restrict__ part)
+{
+    __shared__ uint32_t h[4][256];
+    for (int i = threadIdx.x; i < 4 * 256; i += 256) (&h[0][0])[i] = 0;
+    __syncthreads();
+    uint32_t *mine = h[threadIdx.x >> 6];
+    const Span sp = span_of(x, count);
+    const uint4 *xv = (const uint4 *)(x + sp.head);
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x; v < sp.nvec; v += stride) {
+        const uint4 q = xv[v];
+        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+#pragma unroll
+            for (int b = 0; b < 4; b++) atomicAdd(&mine[(w[k] >> (8 * b)) & 0xffu], 1u);
+        }
+    }
+    const int64_t tail0 = sp.head + 16 * sp.nvec;
+    const int64_t rest = sp.head + (count - tail0);
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < rest; i += stride) {
+        const int64_t e = i < sp.head ? i : tail0 + (i - sp.head);
+        atomicAdd(&mine[x[e]], 1u);
+    }
+    __syncthreads();
+    const int v = threadIdx.x;
+    part[(int64_t)blockIdx.x * 256 + v] = h[0][v] + h[1][v] + h[2][v] + h[3][v];
+}
+
+// Sum of a uint64 over the workgroup's 256 threads (every thread gets it).
+__device__ inline uint64_t block_sum_u64(uint64_t v, uint64_t *red)
+{
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    return red[0] + red[1] + red[2] + red[3];
+}
+
+__device__ inline int64_t div_round(int64_t n, int64_t d, int trunc)
+{
+    const int64_t q = n / d;                      // rounds toward zero
+    return (!trunc && (n % d) != 0 && (n < 0)) ? q - 1 : q;
+}
+
+__global__ __launch_bounds__(256) void k_pre_stats(const uint32_t *__restrict__ part, int groups,
+                                                   int64_t count, int trunc,
+                                                   int64_t *__restrict__ stats,
+                                                   int8_t *__restrict__ table)
+{
+    __shared__ uint64_t red[4];
+    const int v = threadIdx.x;
+    uint64_t hv = 0;
+    for (int g = 0; g < groups; g++) hv += part[(int64_t)g * 256 + v];
+    const uint64_t s1 = block_sum_u64(hv * (uint64_t)v, red);
+    const int64_t mu = div_round((int64_t)s1, count, trunc);
+    const int64_t dev = v > mu ? v - mu : mu - v;
+    const uint64_t s2 = block_sum_u64(hv * (uint64_t)dev, red);
+    int64_t omega = div_round((int64_t)s2, count, trunc);
+    if (omega < 1) omega = 1;
+    const int64_t q = div_round(((int64_t)v - mu) * 51, omega, trunc);
+    const bool sat = q < -127 || q > 127;
+    table[v] = (int8_t)(q < -127 ? -127 : (q > 127 ? 127 : q));
+    const uint64_t ns = block_sum_u64(sat ? hv : 0, red);
+    if (v == 0) {
+        stats[0] = mu;
+        stats[1] = omega;
+        stats[2] = (int64_t)ns;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_pre_map(const uint8_t *x, int64_t count,
+                                                 const int8_t *__restrict__ table, int8_t *out)
+{
+    __shared__ uint8_t t[256];
+    t[threadIdx.x] = (uint8_t)table[threadIdx.x];
+    __syncthreads();
+    // x and out may be the same buffer: every element is read before it is written, by the same
+    // thread; the 16-byte vectors are aligned for both only when the two alignments agree
+    const bool vec = (((uintptr_t)x ^ (uintptr_t)out) & 15) == 0;
+    const Span sp = vec ? span_of(x, count) : Span{count, 0};
+    const uint4 *xv = (const uint4 *)(x + sp.head);
+    uint4 *ov = (uint4 *)(out + sp.head);
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x; v < sp.nvec; v += stride) {
+        const uint4 q = xv[v];
+        uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            uint32_t r = 0;
+#pragma unroll
+            for (int b = 0; b < 4; b++) r |= (uint32_t)t[(w[k] >> (8 * b)) & 0xffu] << (8 * b);
+            w[k] = r;
+        }
+        ov[v] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+    const int64_t tail0 = sp.head + 16 * sp.nvec;
+    const int64_t rest = sp.head + (count - tail0);
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < rest; i += stride) {
+        const int64_t e = i < sp.head ? i : tail0 + (i - sp.head);
+        out[e] = (int8_t)t[x[e]];
+    }
+}
+
+int preprocess_groups(int64_t count)
+{
+    const int64_t g = (count + 16 * 256 * 4 - 1) / (16 * 256 * 4);   // about 4 vectors per thread
+    return (int)(g < 1 ? 1 : (g > PRE_MAX_GROUPS ? PRE_MAX_GROUPS : g));
+}
+
+size_t preprocess_workspace(int64_t count)
+{
+    return (size_t)preprocess_groups(count) * 256 * 4 + 256;
+}
+
+void launch_preprocess(hipStream_t s, const uint8_t *x, int64_t count, int round, int8_t *out,
+                       int64_t *stats, void *workspace)
+{
+    const int groups = preprocess_groups(count);
+    uint32_t *part = (uint32_t *)workspace;
+    int8_t *table = (int8_t *)((uint8_t *)workspace + (size_t)groups * 256 * 4);
+    hipLaunchKernelGGL(k_pre_hist, dim3(groups), dim3(256), 0, s, x, count, part);
+    hipLaunchKernelGGL(k_pre_stats, dim3(1), dim3(256), 0, s, part, groups, count,
+                       round == NITRO_ROUND_TRUNC ? 1 : 0, stats, table);
+    hipLaunchKernelGGL(k_pre_map, dim3(groups), dim3(256), 0, s, x, count, table, out);
+}
+
+}  // namespace nitro

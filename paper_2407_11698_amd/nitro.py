@@ -108,6 +108,8 @@ def _load():
         "nitro_integer_sgd_step": (I32, [VP, VP, VP, I64, I64, I64, I64, I32]),
         "nitro_block_sgd_step": (I32, [VP, P(BlockDesc), P(BlockWeights), P(BlockGrads), P(HParams)]),
         "nitro_net_block_view": (I32, [P(NetDesc), VP, I32, P(BlockView)]),
+        "nitro_preprocess_query": (I32, [I64, P(ctypes.c_size_t)]),
+        "nitro_preprocess": (I32, [VP, VP, I64, I32, VP, VP, VP]),
         "nitro_net_head_view": (I32, [P(NetDesc), VP, P(VP), P(VP), P(VP)]),
         "nitro_net_query": (I32, [P(NetDesc), P(ctypes.c_size_t)]),
         "nitro_net_block_output": (I32, [P(NetDesc), VP, I32, P(VP)]),
@@ -138,6 +140,7 @@ EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_set_conv_
            "nitro_block_backward",
            "nitro_head_backward", "nitro_integer_sgd_step", "nitro_block_sgd_step",
            "nitro_net_block_view", "nitro_net_head_view", "nitro_net_query",
+           "nitro_preprocess_query", "nitro_preprocess",
            "nitro_net_block_output", "nitro_train_step", "nitro_train_step_graph",
            "nitro_host_div", "nitro_host_relu_mu", "nitro_host_kaiming_bound",
            "nitro_kernel_timing", "nitro_kernel_time", "nitro_mfma_rate")
@@ -211,6 +214,12 @@ def net_query(nd: NetDesc) -> int:
 def hparams(gamma_inv: int, lambda_inv_fw: int, lambda_inv_lr: int, af_classes: int = 0,
             af: int = 0, eta_fw: int = -1, eta_lr: int = -1) -> HParams:
     return HParams(gamma_inv, lambda_inv_fw, lambda_inv_lr, af, eta_fw, eta_lr, af_classes, 0)
+
+
+def preprocess_query(count: int) -> int:
+    out = ctypes.c_size_t(0)
+    check(LIB.nitro_preprocess_query(count, ctypes.byref(out)), "nitro_preprocess_query")
+    return out.value
 
 
 def net_block_view(nd: NetDesc, workspace, b: int) -> dict:
@@ -347,6 +356,12 @@ class Context:
         gr.dw_lr = _p(dw_lr)
         check(LIB.nitro_block_sgd_step(self.h, ctypes.byref(desc), ctypes.byref(bw), ctypes.byref(gr),
                                        ctypes.byref(hp)), "nitro_block_sgd_step")
+
+    def preprocess(self, x, out, stats, workspace, round_mode: int = ROUND_FLOOR) -> None:
+        """Appendix A normalisation of the uint8 tensor x into the int8 tensor out; stats (int64,
+        3) receives mu, omega and the clamped count; workspace: preprocess_query(x.numel())."""
+        check(LIB.nitro_preprocess(self.h, _p(x), x.numel(), round_mode, _p(out), _p(stats),
+                                   _p(workspace)), "nitro_preprocess")
 
     # -- network level ------------------------------------------------------------------
     def train_step(self, nd: NetDesc, params: NetParams, workspace, x, labels, hp: HParams) -> None:

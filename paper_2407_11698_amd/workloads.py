@@ -323,3 +323,28 @@ def draw_workload(wl: Workload, kaiming_bound, steps: Optional[int] = None) -> D
         return Draws(ws, [(x, np.zeros(wl.batch, np.int32))], d)
     n = wl.steps if steps is None else steps
     return Draws(ws, [draw_batch(wl, rng) for _ in range(n)])
+
+
+# --------------------------------------------------------------------------------------------
+# raw image bytes for the integer pre-processing (Appendix A)
+# --------------------------------------------------------------------------------------------
+
+# stands in for the CIFAR-10 training images: 50000 x 32 x 32 x 3 unsigned bytes
+CIFAR10_BYTES = (50000, 32, 32, 3)
+
+
+def draw_image_bytes(shape, seed: int = 0) -> np.ndarray:
+    """Seeded uint8 'pixels' of the given shape (images first): each value is N(120, 55) plus a
+    per-image brightness offset N(0, 30), rounded and clipped to [0, 255] (a skewed, clipped
+    distribution like natural images' pixel values)."""
+    rng = np.random.default_rng(seed)
+    n = shape[0]
+    per = int(np.prod(shape[1:]))
+    out = np.empty((n, per), np.uint8)
+    off = rng.normal(0.0, 30.0, n)
+    chunk = max(1, (1 << 24) // per)
+    for i in range(0, n, chunk):
+        j = min(n, i + chunk)
+        v = rng.normal(120.0, 55.0, (j - i, per)) + off[i:j, None]
+        out[i:j] = np.clip(np.rint(v), 0, 255).astype(np.uint8)
+    return out.reshape(shape)

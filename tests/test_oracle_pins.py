@@ -302,6 +302,31 @@ def test_maxpool_window_two_by_two_is_the_forward_pool():
     assert all(np.array_equal(u, v) for u, v in zip(O.maxpool_window(a, 2, 2), O.maxpool2(a)))
 
 
+@pytest.mark.parametrize("mode", ["floor", "trunc"])
+def test_preprocess_table(mode):
+    for c in gold("preprocess.json")["cases"]:
+        r = O.preprocess(np.array(c["x"], np.uint8), MODES[mode])
+        assert (r.mu, r.omega, r.saturated) == (c["mu"], c["omega"], c["saturated"])
+        assert r.xhat.tolist() == c[mode]
+
+
+def test_preprocess_invariants():
+    """Against the statistics numpy computes in floating point (exact here: integers below
+    2^53): mu and omega are the floors of the mean and of the mean absolute deviation around mu;
+    xhat is monotone in x; a dataset symmetric about an integer centre has mu = centre and maps
+    symmetrically under truncation."""
+    rng = np.random.default_rng(17)
+    x = np.clip(np.rint(rng.normal(120, 60, 20011)), 0, 255).astype(np.uint8)
+    r = O.preprocess(x)
+    assert r.mu == int(np.floor(x.astype(np.float64).mean()))
+    assert r.omega == int(np.floor(np.abs(x.astype(np.float64) - r.mu).mean()))
+    order = np.argsort(x, kind="stable")
+    assert np.all(np.diff(r.xhat[order].astype(np.int64)) >= 0)
+    sym = np.array([100 - 37, 100 - 5, 100, 100 + 5, 100 + 37], np.uint8)
+    t = O.preprocess(sym, O.TRUNC)
+    assert t.mu == 100 and t.xhat.tolist() == (-t.xhat[::-1]).tolist()
+
+
 # ---------------------------------------------------------------- brute force, tiny shapes
 
 def _rand(rng, shape, lo, hi, dtype=np.int64):
