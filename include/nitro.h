@@ -309,6 +309,18 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                               const nitro_net_params *params, void *workspace,
                               const int8_t *x, const int32_t *labels, const nitro_hparams *hp);
 
+/* Inference with the current weights (the accuracy protocol of section 4): the forward pass
+ * through every block (section 3.2), then the network's prediction yhat = floor(f W^T / 2^8 d)
+ * of the output layer on the last block's output f, or, without an output layer, of the last
+ * block's learning layer on its input, and the predicted class: the first maximum of each row.
+ *   workspace  laid out by nitro_net_query (a training workspace serves);
+ *   x          int8 input batch;  yhat  int32 [n][G];  pred  int32 [n].
+ * Labels are not needed; every block's n_classes must still be G > 0 (the shapes of the
+ * training network). Weights are not changed. */
+nitro_status nitro_net_infer(nitro_ctx *ctx, const nitro_net_desc *net,
+                             const nitro_net_params *params, void *workspace, const int8_t *x,
+                             int32_t *yhat, int32_t *pred);
+
 /* nitro_train_step replayed from a HIP graph. The context keeps up to 16 captured iterations,
  * one per distinct key (compared by value: descriptors, parameter pointers, workspace, x,
  * labels, hyper-parameters, the context's stream and settings, the timing switch). A call whose

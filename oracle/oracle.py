@@ -315,6 +315,11 @@ def loss_grad(yhat, labels, G: int):
     return np.asarray(yhat, dtype=np.int64) - one_hot32(labels, G)
 
 
+def predict(yhat) -> np.ndarray:
+    """Predicted class per sample: the index of the largest prediction, the first one on ties."""
+    return np.argmax(np.asarray(yhat), axis=1).astype(np.int32)
+
+
 def amplification_factor(G: int) -> int:
     """NITRO Amplification Factor, Eq. 6: AF = 2^6 * G."""
     return (1 << 6) * G
@@ -588,6 +593,27 @@ class OracleNet:
                                        hp.eta_fw).astype(np.int32)
         self.w = new_w
         return step
+
+    def infer(self, x):
+        """Inference: the forward pass, then the network's prediction yhat (the output layer's,
+        or without one the last block's learning layer's) and the predicted class, the first
+        maximum of each row (argmax). Returns (yhat, pred)."""
+        recs = self.forward(x)
+        last = recs[-1]
+        if self.head:
+            f = last.out.reshape(last.out.shape[0], -1)
+            w = self.w[self.head_index]
+        else:
+            f = last.out
+            if f.ndim == 4 and self.hp.d_lr > 0:
+                N_, H_, W_, C_ = f.shape
+                win = learning_pool_window(C_, H_, W_, self.hp.d_lr)
+                if win != (1, 1):
+                    f, _ = maxpool_window(f, *win)
+            f = f.reshape(f.shape[0], -1)
+            w = self.w[self.index[-1][1]]
+        yhat = learning_forward(f, w, self.hp.mode)
+        return yhat, predict(yhat)
 
     def stress_repeat(self, x, delta) -> BlockRecord:
         """The single-layer stress case: forward, then back-propagate a given gradient at the

@@ -913,6 +913,61 @@ nitro_status nitro_net_block_output(const nitro_net_desc *net, void *workspace, 
     return NITRO_OK;
 }
 
+// The start of an iteration (training or inference): every block's max slots cleared in one
+// launch (with block 0's input zero-padded to 16 channels where its first layer takes it so),
+// then the limb planes (and max |W|) of the tiled conv layers' and the MFMA learning layers'
+// weights of every block, in one launch ahead of the forward pass.
+void net_setup(nitro_ctx *ctx, const nitro_net_desc *net, const NetGeom &g,
+               const nitro_net_params *params, void *workspace, const int8_t *x)
+{
+    {
+        SlotList sl{};
+        sl.words = 16 * SLOT_WORDS;
+        for (int b = 0; b < net->n_blocks; b++)
+            sl.p[b] = (uint32_t *)at(at(workspace, g.state[b]), g.b[b].slots);
+        // (with them, block 0's input zero-padded to 16 channels where its first layer takes it so)
+        Pad16Args pad{};
+        const BlockGeom &b0 = g.b[0];
+        if (b0.L[0].conv && b0.L[0].pad16) {
+            pad.x = x;
+            pad.P = b0.L[0].sh.n * b0.L[0].sh.h * b0.L[0].sh.w;
+            pad.c = b0.L[0].sh.c;
+            pad.xpad = (int8_t *)at(at(workspace, g.state[0]), b0.xpad);
+        }
+        launch_zero_slots(ctx->stream, sl, net->n_blocks, &pad);
+    }
+    // limb planes (and max |W|) of the tiled conv layers' and the MFMA learning layers' weights
+    // of every block, in one launch ahead of the forward pass
+    {
+        PackList pl;
+        for (int b = 0; b < net->n_blocks; b++) {
+            const BlockGeom &bg = g.b[b];
+            void *state = at(workspace, g.state[b]);
+            uint32_t *slots = (uint32_t *)at(state, bg.slots);
+            for (int j = 0; j < bg.J; j++) {
+                const LayerGeom &L = bg.L[j];
+                if (!L.conv) continue;
+                if (!L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c))
+                    pl.add(ctx->stream,
+                           pack_conv_args(params->w[b][j], L.sh.co, L.sh.c, (int8_t *)at(state, bg.wf[j]),
+                                          (int8_t *)at(state, bg.wt[j]), slots + j * SLOT_WORDS), 9);
+                else
+                    pl.add_conv(ctx->stream, params->w[b][j], L.sh.co, L.sh.c, L.pad16 ? 16 : L.sh.c,
+                                (int8_t *)at(state, bg.wf[j]), (int8_t *)at(state, bg.wt[j]),
+                                slots + j * SLOT_WORDS);
+            }
+            if (net->block[b].n_classes > 0 && bg.lr_mfma) {
+                const LearningScratch sc = learning_scratch(net->block[b].n, bg.d, net->block[b].n_classes);
+                pl.add(ctx->stream,
+                       pack_matrix_args(params->w_lr[b], net->block[b].n_classes, (int)bg.d, sc.gp,
+                                        (int8_t *)at(state, bg.lwf), (int8_t *)at(state, bg.lwt),
+                                        slots + 8 * SLOT_WORDS), 1);
+            }
+        }
+        pl.flush(ctx->stream);
+    }
+}
+
 nitro_status nitro_block_sgd_step(nitro_ctx *ctx, const nitro_block_desc *desc,
                                   const nitro_block_weights *weights,
                                   const nitro_block_grads *grads, const nitro_hparams *hp)
@@ -1029,52 +1084,7 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         if (hipStreamIsCapturing(ctx->stream, &cs) == hipSuccess && cs == hipStreamCaptureStatusActive)
             launch_ts_reset(ctx->stream, ctx->tsbuf, (int64_t)TIMED_CLASSES * nitro_ctx::TS_CAP);
     }
-    {
-        SlotList sl{};
-        sl.words = 16 * SLOT_WORDS;
-        for (int b = 0; b < net->n_blocks; b++)
-            sl.p[b] = (uint32_t *)at(at(workspace, g.state[b]), g.b[b].slots);
-        // (with them, block 0's input zero-padded to 16 channels where its first layer takes it so)
-        Pad16Args pad{};
-        const BlockGeom &b0 = g.b[0];
-        if (b0.L[0].conv && b0.L[0].pad16) {
-            pad.x = x;
-            pad.P = b0.L[0].sh.n * b0.L[0].sh.h * b0.L[0].sh.w;
-            pad.c = b0.L[0].sh.c;
-            pad.xpad = (int8_t *)at(at(workspace, g.state[0]), b0.xpad);
-        }
-        launch_zero_slots(ctx->stream, sl, net->n_blocks, &pad);
-    }
-    // limb planes (and max |W|) of the tiled conv layers' and the MFMA learning layers' weights
-    // of every block, in one launch ahead of the forward pass
-    {
-        PackList pl;
-        for (int b = 0; b < net->n_blocks; b++) {
-            const BlockGeom &bg = g.b[b];
-            void *state = at(workspace, g.state[b]);
-            uint32_t *slots = (uint32_t *)at(state, bg.slots);
-            for (int j = 0; j < bg.J; j++) {
-                const LayerGeom &L = bg.L[j];
-                if (!L.conv) continue;
-                if (!L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c))
-                    pl.add(ctx->stream,
-                           pack_conv_args(params->w[b][j], L.sh.co, L.sh.c, (int8_t *)at(state, bg.wf[j]),
-                                          (int8_t *)at(state, bg.wt[j]), slots + j * SLOT_WORDS), 9);
-                else
-                    pl.add_conv(ctx->stream, params->w[b][j], L.sh.co, L.sh.c, L.pad16 ? 16 : L.sh.c,
-                                (int8_t *)at(state, bg.wf[j]), (int8_t *)at(state, bg.wt[j]),
-                                slots + j * SLOT_WORDS);
-            }
-            if (net->block[b].n_classes > 0 && bg.lr_mfma) {
-                const LearningScratch sc = learning_scratch(net->block[b].n, bg.d, net->block[b].n_classes);
-                pl.add(ctx->stream,
-                       pack_matrix_args(params->w_lr[b], net->block[b].n_classes, (int)bg.d, sc.gp,
-                                        (int8_t *)at(state, bg.lwf), (int8_t *)at(state, bg.lwt),
-                                        slots + 8 * SLOT_WORDS), 1);
-            }
-        }
-        pl.flush(ctx->stream);
-    }
+    net_setup(ctx, net, g, params, workspace, x);
     SgdBatch sgd{};
     sgd.flags = ctx->flags;
 
@@ -1163,6 +1173,56 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     }
     // 4. IntegerSGD (Alg. 1) of every weight tensor
     launch_sgd_batch(ctx->stream, sgd);
+    return hip_status();
+}
+
+nitro_status nitro_net_infer(nitro_ctx *ctx, const nitro_net_desc *net,
+                             const nitro_net_params *params, void *workspace, const int8_t *x,
+                             int32_t *yhat, int32_t *pred)
+{
+    if (!ctx || !params || !workspace || !x || !yhat || !pred) return NITRO_EINVAL;
+    NetGeom g;
+    nitro_status st = net_geom(net, &g);
+    if (st != NITRO_OK) return st;
+    for (int b = 0; b < net->n_blocks; b++)
+        for (int j = 0; j < net->block[b].n_layers; j++)
+            if (!params->w[b][j]) return NITRO_EINVAL;
+    const int L = net->n_blocks - 1;
+    if (net->head ? !params->w_head : !params->w_lr[L]) return NITRO_EINVAL;
+    DeviceGuard guard(ctx->device);
+    TimerScope timer(ctx);
+    hipStream_t s = ctx->stream;
+    const int n = net->block[0].n, G = net->block[0].n_classes;
+    const int round = net->block[0].round;
+    net_setup(ctx, net, g, params, workspace, x);
+    const int8_t *cur = x;
+    for (int b = 0; b < net->n_blocks; b++) {
+        nitro_block_params bp{};
+        for (int j = 0; j < net->block[b].n_layers; j++) bp.w[j] = params->w[b][j];
+        int8_t *aout = (int8_t *)at(workspace, g.aout[b]);
+        st = block_forward_impl(ctx, &net->block[b], g.b[b], &bp, cur, aout, at(workspace, g.state[b]),
+                                false, true, b == 0);
+        if (st != NITRO_OK) return st;
+        cur = aout;
+    }
+    // the prediction: the output layer on the last block's output, or the last block's learning
+    // layer (on its learning pooling, if any)
+    const BlockGeom &lb = g.b[L];
+    const int8_t *f = cur;
+    int64_t d = net->head ? g.hd : lb.d;
+    const int32_t *w = net->head ? params->w_head : params->w_lr[L];
+    if (!net->head && lb.lr_kh * lb.lr_kw > 1) {
+        const nitro_block_desc &ld = net->block[L];
+        const LayerGeom &LJ = lb.L[lb.J - 1];
+        LrPool lp{n, ld.maxpool ? LJ.sh.h / 2 : LJ.sh.h, ld.maxpool ? LJ.sh.w / 2 : LJ.sh.w, LJ.sh.co,
+                  lb.lr_kh, lb.lr_kw};
+        uint8_t *state = at(workspace, g.state[L]);
+        launch_lr_pool(s, lp, cur, (int8_t *)(state + lb.lf), state + lb.lfc);
+        f = (const int8_t *)(state + lb.lf);
+    }
+    launch_linear_fwd_loss(s, n, (int)d, G, f, w, make_div(256 * d, round), nullptr, yhat, nullptr,
+                           ctx->flags);
+    launch_argmax_rows(s, n, G, yhat, pred);
     return hip_status();
 }
 

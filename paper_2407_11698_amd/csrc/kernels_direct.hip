@@ -185,13 +185,47 @@ __global__ void k_linear_fwd_loss(int n, int k, int g, const int8_t *__restrict_
     int64_t z = linear_point(x + (int64_t)row * k, w + (int64_t)col * k, k, lane);
     if (lane == 0) {
         int64_t y = idiv(z, sf);
-        int lab = labels[row];
-        if (lab < 0 || lab >= g) raise_flag(flags, FLAG_LABEL);
-        int64_t ev = y - (lab == col ? 32 : 0);
-        if (!fits_i32(y) || !fits_i32(ev)) raise_flag(flags, FLAG_OVERFLOW);
+        if (!fits_i32(y)) raise_flag(flags, FLAG_OVERFLOW);
         yhat[o] = (int32_t)y;
-        e[o] = (int32_t)ev;
+        if (labels) {            // training: the loss gradient too (inference passes no labels)
+            int lab = labels[row];
+            if (lab < 0 || lab >= g) raise_flag(flags, FLAG_LABEL);
+            int64_t ev = y - (lab == col ? 32 : 0);
+            if (!fits_i32(ev)) raise_flag(flags, FLAG_OVERFLOW);
+            e[o] = (int32_t)ev;
+        }
     }
+}
+
+// pred[r] = the first column of row r holding the row's maximum (one wave per row).
+__global__ void k_argmax_rows(int n, int g, const int32_t *__restrict__ yhat, int32_t *__restrict__ pred)
+{
+    const int row = blockIdx.x * (blockDim.x / 64) + threadIdx.x / 64;
+    const int lane = threadIdx.x & 63;
+    if (row >= n) return;
+    int32_t best = INT32_MIN;
+    int arg = g;
+    for (int c = lane; c < g; c += 64) {
+        const int32_t v = yhat[(int64_t)row * g + c];
+        if (v > best) {                // strictly greater: a lane keeps its first maximum
+            best = v;
+            arg = c;
+        }
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        const int32_t ob = __shfl_xor(best, off, 64);
+        const int oa = __shfl_xor(arg, off, 64);
+        if (ob > best || (ob == best && oa < arg)) {
+            best = ob;
+            arg = oa;
+        }
+    }
+    if (lane == 0) pred[row] = arg;
+}
+
+void launch_argmax_rows(hipStream_t s, int n, int g, const int32_t *yhat, int32_t *pred)
+{
+    hipLaunchKernelGGL(k_argmax_rows, dim3(blocks_for(n, 4)), dim3(256), 0, s, n, g, yhat, pred);
 }
 
 void launch_linear_fwd_loss(hipStream_t s, int n, int k, int g, const int8_t *x, const int32_t *w,

@@ -445,10 +445,13 @@ void launch_conv_fwd(hipStream_t s, const ConvShape &sh, const int8_t *x, const 
 // forward linear + Scaling + ReLU: x [n][k], w [m][k] -> a [n][m], region codes [n][m].
 void launch_linear_fwd_relu(hipStream_t s, int n, int k, int m, const int8_t *x, const int32_t *w,
                             const Div &sf, const Relu &rp, int8_t *out, uint8_t *code);
-// learning / output layer: yhat = x w^T / sf, e = yhat - 32 onehot(labels).
+// learning / output layer: yhat = x w^T / sf, e = yhat - 32 onehot(labels) (labels NULL: yhat
+// only).
 void launch_linear_fwd_loss(hipStream_t s, int n, int k, int g, const int8_t *x, const int32_t *w,
                             const Div &sf, const int32_t *labels, int32_t *yhat, int32_t *e,
                             uint32_t *flags);
+// pred[r] = first argmax of yhat's row r ([n][g])
+void launch_argmax_rows(hipStream_t s, int n, int g, const int32_t *yhat, int32_t *pred);
 // dx[n][k] = sum_m e[n][m] w[m][k]; optional ReLU' with `code` -> int32 out (overflow flagged),
 // or the raw sum into out64 (int64) when out64 is not null.
 void launch_linear_dx(hipStream_t s, int n, int k, int m, const int32_t *e, const int32_t *w,

@@ -70,6 +70,13 @@ class GpuNet:
         on the first call with them; up to 16 buffer sets keep graphs of their own)."""
         self.ctx.train_step_graph(self.nd, self.params, self.workspace, x, y, self.hp)
 
+    def infer(self, x: torch.Tensor):
+        """Inference with the current weights: (yhat [n][G] int32, predicted class [n] int32)."""
+        yhat = torch.empty((self.wl.batch, self.wl.n_classes), dtype=torch.int32, device=self.dev)
+        pred = torch.empty((self.wl.batch,), dtype=torch.int32, device=self.dev)
+        self.ctx.net_infer(self.nd, self.params, self.workspace, x, yhat, pred)
+        return yhat, pred
+
     def view(self, b: int) -> dict:
         """Block b's tensors from the last step, as torch views of the workspace: "a_out",
         "act" (list, None for the last layer), "code" (list), "yhat", "e", "dw" (list), "dw_lr"."""

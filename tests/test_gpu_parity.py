@@ -566,3 +566,32 @@ def test_train_step_graph_matches_eager(wl, nbuf, feed):
             del junk
         gctx.close()
         ectx.close()
+
+
+@pytest.mark.parametrize("wl,steps", [(WL.TINY_CNN, 2), (WL.MLP, 3), (WL.SMALL_CNN, 2),
+                                      (WL.scaled(WL.VGG_CNN, 8), 2), (WL.scaled(WL.VGG8B, 4), 1),
+                                      (WL.scaled(WL.MLP4, 16), 1)],
+                         ids=["tiny_cnn", "mlp", "small_cnn", "vgg_b8", "vgg8b_b4", "mlp4_b16"])
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_infer(ctx, wl, steps, modes):
+    """nitro_net_infer against the oracle's inference (forward, prediction, first-maximum
+    argmax) on an unseen batch, before and after some training steps (the predictions are
+    small integers, so ties between classes occur and the first-maximum rule is exercised)."""
+    print("inference case", wl.name, "batch", wl.batch, "mode", modes[0], flush=True)
+    dr = WL.draw_workload(wl, O.kaiming_bound, steps=steps + 1)
+    ref = oracle_net(wl, dr.weights, modes[1])
+    net = runner.GpuNet(wl, dr.weights, modes[0], ctx=ctx)
+    xt, _ = dr.batches[-1]
+    ties = 0
+    for s in range(steps + 1):
+        yh, pr = net.infer(dev(xt))
+        ryh, rpr = ref.infer(xt)
+        ctx.sync()
+        assert np.array_equal(host(yh), ryh), "step %d yhat" % s
+        assert np.array_equal(host(pr), rpr), "step %d prediction" % s
+        ties += int(np.sum(np.sum(ryh == ryh.max(axis=1, keepdims=True), axis=1) > 1))
+        if s < steps:
+            x, y = dr.batches[s]
+            ref.train_step(x, y)
+            net.step(dev(x), dev(y))
+    print("rows with tied maxima:", ties, flush=True)

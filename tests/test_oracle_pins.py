@@ -327,6 +327,27 @@ def test_preprocess_invariants():
     assert t.mu == 100 and t.xhat.tolist() == (-t.xhat[::-1]).tolist()
 
 
+def test_predict_first_maximum():
+    assert O.predict([[-3, -4], [5, 5], [1, 9], [2, 7]]).tolist() == [0, 0, 1, 1]
+    assert O.predict([[0, 3, 3, 1]]).tolist() == [1]
+
+
+@pytest.mark.parametrize("mode", ["floor", "trunc"])
+def test_infer_matches_training_forward(mode):
+    """Inference on the hand-worked blocks gives the training iteration's prediction: the
+    mini_step block's yhat without an output layer, head_step.json's with one."""
+    g = gold("mini_step.json")
+    net = O.OracleNet([(1, False, True)], False,
+                      [np.array(g["W1"], np.int32), np.array(g["Wlr"], np.int32)], _hyper(g, MODES[mode]))
+    yhat, pred = net.infer(np.array(g["x"], np.int8))
+    assert yhat.tolist() == g[mode]["yhat"] and pred.tolist() == [int(np.argmax(g[mode]["yhat"][0]))]
+    h = gold("head_step.json")
+    net = O.OracleNet([(1, False, True)], True,
+                      [np.array(h[k], np.int32) for k in ("W1", "Wlr", "Wh")], _hyper(h, MODES[mode]))
+    yhat, pred = net.infer(np.array(h["x"], np.int8))
+    assert yhat.tolist() == h[mode]["yhat"] and pred.tolist() == [0]
+
+
 # ---------------------------------------------------------------- brute force, tiny shapes
 
 def _rand(rng, shape, lo, hi, dtype=np.int64):
