@@ -239,8 +239,12 @@ typedef struct {
     int64_t af;               /* amplification factor; 0 means 2^6 * G (Eq. 6)                 */
     int64_t eta_fw;           /* < 0: eta = (AF * gamma_inv) * lambda_inv_fw; else this eta     */
     int64_t eta_lr;           /* < 0: eta = gamma_inv * lambda_inv_lr; else this eta           */
+    uint64_t dropout_seed;    /* key of the dropout generator (nitro_train_step)               */
+    int64_t dropout_step;     /* its step counter: a different value for every iteration        */
     int32_t af_classes;       /* G entering AF = 2^6 G when af == 0 and the block has no
                                  learning layer (n_classes == 0); ignored otherwise             */
+    int32_t dropout_conv_ppm; /* dropout rate p_c of conv blocks' outputs, parts per million    */
+    int32_t dropout_lin_ppm;  /* dropout rate p_l of linear blocks' outputs (Tab. 6)            */
     int32_t reserved;         /* must be 0                                                      */
 } nitro_hparams;
 
@@ -303,6 +307,13 @@ nitro_status nitro_net_query(const nitro_net_desc *net, size_t *workspace_bytes)
  * IntegerSGD update, then each block's local training and the IntegerSGD update of its learning
  * layer (gamma_inv) and forward layers (AF * gamma_inv). All gradients are taken at the weights
  * from before the iteration. Weights in `params` are updated in place.
+ * Dropout (hp->dropout_conv_ppm, hp->dropout_lin_ppm > 0): each block's output is thinned after
+ * its forward layers; a dropped element becomes 0, for the next block and the learning layer
+ * alike, and passes no gradient back. The mask of block b: element i (flat NHWC / [n][d] order)
+ * takes 64-bit word i mod 4 of Philox4x64-10 (Salmon et al., SC'11) at counter (i div 4 + 1, b,
+ * dropout_step, 0) and key (dropout_seed, 0), and is dropped when the word's upper 32 bits are
+ * below floor(p 2^32), p = ppm / 10^6. No rescaling of the kept elements (the next layer's
+ * NITRO-Scaling sets the scale). The caller advances dropout_step between iterations.
  *   x       int8 input batch (NHWC, or [n][d] for an MLP);
  *   labels  int32 [n] in [0, G). */
 nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,

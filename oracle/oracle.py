@@ -337,6 +337,28 @@ def integer_sgd(w, dw, gamma_inv: int, lambda_inv: int, mode: int = FLOOR, eta_i
     return check_int32(w - (idiv(dw, gamma_inv, mode) + decay), "updated weights")
 
 
+def dropout_threshold(p_ppm: int) -> int:
+    """The dropout probability p, given in parts per million, as a threshold on a 32-bit random
+    number: floor(p_ppm 2^32 / 10^6)."""
+    if not 0 <= p_ppm <= 1000000:
+        raise ValueError("dropout rate outside [0, 10^6] ppm")
+    return (p_ppm << 32) // 1000000
+
+
+def dropout_keep(count: int, seed: int, step: int, block: int, p_ppm: int) -> np.ndarray:
+    """Dropout mask of a block output with `count` elements (flat NHWC / [n][d] order), drawn
+    with the counter-based generator Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): element i
+    takes 64-bit word i mod 4 of the generator's output for counter (i div 4 + 1, block, step, 0)
+    and key (seed, 0), and is kept when the word's upper 32 bits are at least the threshold.
+    numpy's Philox bit generator (which steps its counter before each output) supplies the words."""
+    if p_ppm == 0:
+        return np.ones(count, bool)
+    g = np.random.Philox(key=np.array([seed, 0], np.uint64),
+                         counter=np.array([0, block, step, 0], np.uint64))
+    words = g.random_raw((count + 3) // 4 * 4)[:count]
+    return (words >> np.uint64(32)) >= np.uint64(dropout_threshold(p_ppm))
+
+
 def kaiming_bound(fan_in: int) -> int:
     """Integer Kaiming bound (section 3.3.1): floor(128 * 1732 / (isqrt(fan_in) * 1000))."""
     return (128 * 1732) // (math.isqrt(fan_in) * 1000)
@@ -389,6 +411,7 @@ class BlockRecord:
     layers: List[LayerRecord] = field(default_factory=list)
     out: Optional[np.ndarray] = None        # block output (pooled if the block pools), int8
     pool_idx: Optional[np.ndarray] = None
+    keep: Optional[np.ndarray] = None       # dropout mask of the block output (None: no dropout)
     yhat: Optional[np.ndarray] = None       # learning-layer prediction, int32 values
     e: Optional[np.ndarray] = None          # local loss gradient
     dw_lr: Optional[np.ndarray] = None
@@ -487,6 +510,10 @@ class Hyper:
     eta_fw: int = -1             # explicit eta overrides (< 0: gamma * lambda)
     eta_lr: int = -1
     d_lr: int = 0                # learning-layer input size of conv blocks (0: the block output)
+    dropout_conv_ppm: int = 0    # dropout rate p_c of conv blocks' outputs (parts per million)
+    dropout_lin_ppm: int = 0     # dropout rate p_l of linear blocks' outputs
+    dropout_seed: int = 0        # key of the dropout generator
+    dropout_step: int = 0        # counter of the first training iteration
     # alternative readings (both off by default):
     relu_grad_ste: bool = False  # NITRO-ReLU backward passes the gradient unchanged on its leaky
     #                              segment (straight through) instead of dividing by alpha_inv
@@ -531,16 +558,27 @@ class OracleNet:
             self.index.append((fw, lr))
         self.head_index = i if head else None
         assert len(self.w) == i + (1 if head else 0)
+        self.steps = 0                # training iterations done (the dropout counter)
 
-    def forward(self, x) -> List[BlockRecord]:
+    def forward(self, x, train: bool = False) -> List[BlockRecord]:
+        """The forward layers of every block; in training, a block's output then takes dropout
+        (rate p_c for conv blocks, p_l for linear blocks; dropped elements become 0 for the next
+        block and the learning layer alike, and pass no gradient back)."""
         recs = []
         cur = x
+        hp = self.hp
         for b, (nl, pool, _) in enumerate(self.specs):
             fw, _ = self.index[b]
             ws = [self.w[k] for k in fw]
             if not _is_conv(ws[0]) and cur.ndim == 4:
                 cur = cur.reshape(cur.shape[0], -1)       # flatten in (h, w, c) order
-            rec = block_forward(cur, ws, pool, self.hp.alpha_inv, self.hp.mode)
+            rec = block_forward(cur, ws, pool, hp.alpha_inv, hp.mode)
+            p = hp.dropout_conv_ppm if _is_conv(ws[0]) else hp.dropout_lin_ppm
+            if train and p > 0:
+                keep = dropout_keep(rec.out.size, hp.dropout_seed, hp.dropout_step + self.steps,
+                                    b, p).reshape(rec.out.shape)
+                rec.keep = keep
+                rec.out = np.where(keep, rec.out, 0).astype(np.int8)
             recs.append(rec)
             cur = rec.out
         return recs
@@ -550,7 +588,7 @@ class OracleNet:
         mode = hp.mode
         G = hp.n_classes
         # forward pass through every block's forward layers (section 3.3, first paragraph)
-        recs = self.forward(x)
+        recs = self.forward(x, train=True)
         step = StepRecord(blocks=recs)
         new_w = [w.copy() for w in self.w]
         # output layers: global gradient, weight gradient, IntegerSGD with gamma^lr
@@ -586,12 +624,15 @@ class OracleNet:
             d_out = rec.delta_fw.reshape(rec.f.shape)
             if rec.f_idx is not None:              # back through the learning layers' pooling
                 d_out = maxpool_window_bwd(d_out, rec.f_idx, rec.out.shape, *rec.f_window)
+            if rec.keep is not None:               # dropped outputs pass no gradient
+                d_out = np.where(rec.keep, d_out, 0)
             block_backward(rec, [self.w[k] for k in fw], d_out,
                            pool, hp.alpha_inv, mode, ste=hp.relu_grad_ste)
             for j, k in enumerate(fw):
                 new_w[k] = integer_sgd(self.w[k], rec.dw[j], hp.gamma_fw, hp.lambda_inv_fw, mode,
                                        hp.eta_fw).astype(np.int32)
         self.w = new_w
+        self.steps += 1
         return step
 
     def infer(self, x):

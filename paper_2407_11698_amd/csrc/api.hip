@@ -326,7 +326,8 @@ static bool rows_from_forward(const BlockGeom &g)
 nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, const BlockGeom &g,
                                 const nitro_block_params *p, const int8_t *x, int8_t *a_out,
                                 void *state, bool zero_slots = true, bool prepacked = false,
-                                bool x_prepadded = false, bool rows_ok = true)
+                                bool x_prepadded = false, bool rows_ok = true,
+                                const Dropout *drop = nullptr)
 {
     hipStream_t s = ctx->stream;
     const Relu rp = make_relu(desc->alpha_inv, desc->round);
@@ -384,6 +385,9 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
         }
         cur = out;
     }
+    // dropout of the block output (training iterations): zeroes and "saturated" region codes
+    if (drop && drop->threshold > 0)
+        launch_dropout(s, a_out, at(state, g.code[g.J - 1]), g.out_elems, *drop);
     return hip_status();
 }
 
@@ -576,7 +580,8 @@ struct Rates {
 nitro_status resolve_rates(const nitro_hparams *hp, int G, Rates *r)
 {
     if (!hp || hp->gamma_inv < 1 || hp->lambda_inv_fw < 0 || hp->lambda_inv_lr < 0 || hp->af < 0 ||
-        hp->af_classes < 0 || hp->reserved != 0)
+        hp->af_classes < 0 || hp->reserved != 0 || hp->dropout_conv_ppm < 0 ||
+        hp->dropout_conv_ppm > 1000000 || hp->dropout_lin_ppm < 0 || hp->dropout_lin_ppm > 1000000)
         return NITRO_EINVAL;
     const int64_t g = G > 0 ? G : hp->af_classes;
     const int64_t af = hp->af ? hp->af : 64 * g;
@@ -1119,8 +1124,12 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         for (int j = 0; j < net->block[b].n_layers; j++) bp.w[j] = params->w[b][j];
         bp.w_lr = params->w_lr[b];
         int8_t *aout = (int8_t *)at(workspace, g.aout[b]);
+        const bool bconv = net->block[b].layer[0].kind == NITRO_CONV3X3;
+        const int64_t ppm = bconv ? hp->dropout_conv_ppm : hp->dropout_lin_ppm;
+        Dropout drop{(uint64_t)((ppm << 32) / 1000000), hp->dropout_seed, (uint64_t)hp->dropout_step,
+                     b, net->block[b].maxpool};
         st = block_forward_impl(ctx, &net->block[b], g.b[b], &bp, cur, aout, at(workspace, g.state[b]),
-                                false, true, b == 0);
+                                false, true, b == 0, true, &drop);
         if (st != NITRO_OK) return st;
         cur = aout;
         if (b + 1 == net->n_blocks) break;

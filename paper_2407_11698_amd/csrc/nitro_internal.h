@@ -520,6 +520,15 @@ size_t preprocess_workspace(int64_t count);          // bytes: partial histogram
 void launch_preprocess(hipStream_t s, const uint8_t *x, int64_t count, int round, int8_t *out,
                        int64_t *stats, void *workspace);
 
+// ---- dropout of a block output (dropout.hip)
+struct Dropout {
+    uint64_t threshold;   // floor(p 2^32); 0: no dropout
+    uint64_t seed, step;
+    int32_t block;
+    int32_t pooled;       // codes are argmax | region << 2
+};
+void launch_dropout(hipStream_t s, int8_t *a, uint8_t *code, int64_t count, const Dropout &d);
+
 // ---- few input channels (conv_smallc.hip)
 bool smallc_fwd_ok(const ConvShape &sh);
 bool smallc_dw_ok(const ConvShape &sh);

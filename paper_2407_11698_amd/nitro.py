@@ -71,7 +71,9 @@ class NetParams(ctypes.Structure):
 
 class HParams(ctypes.Structure):
     _fields_ = [("gamma_inv", I64), ("lambda_inv_fw", I64), ("lambda_inv_lr", I64), ("af", I64),
-                ("eta_fw", I64), ("eta_lr", I64), ("af_classes", I32), ("reserved", I32)]
+                ("eta_fw", I64), ("eta_lr", I64), ("dropout_seed", ctypes.c_uint64),
+                ("dropout_step", I64), ("af_classes", I32), ("dropout_conv_ppm", I32),
+                ("dropout_lin_ppm", I32), ("reserved", I32)]
 
 
 class BlockWeights(ctypes.Structure):
@@ -213,8 +215,10 @@ def net_query(nd: NetDesc) -> int:
 
 
 def hparams(gamma_inv: int, lambda_inv_fw: int, lambda_inv_lr: int, af_classes: int = 0,
-            af: int = 0, eta_fw: int = -1, eta_lr: int = -1) -> HParams:
-    return HParams(gamma_inv, lambda_inv_fw, lambda_inv_lr, af, eta_fw, eta_lr, af_classes, 0)
+            af: int = 0, eta_fw: int = -1, eta_lr: int = -1, dropout_conv_ppm: int = 0,
+            dropout_lin_ppm: int = 0, dropout_seed: int = 0, dropout_step: int = 0) -> HParams:
+    return HParams(gamma_inv, lambda_inv_fw, lambda_inv_lr, af, eta_fw, eta_lr, dropout_seed,
+                   dropout_step, af_classes, dropout_conv_ppm, dropout_lin_ppm, 0)
 
 
 def preprocess_query(count: int) -> int:

@@ -60,15 +60,25 @@ class GpuNet:
             k += 1
         assert k == len(self.w)
         self.workspace = torch.empty(N.net_query(self.nd), dtype=torch.uint8, device=self.dev)
-        self.hp = N.hparams(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr)
+        self.hp = N.hparams(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr,
+                            dropout_conv_ppm=wl.dropout_conv_ppm, dropout_lin_ppm=wl.dropout_lin_ppm,
+                            dropout_seed=wl.dropout_seed)
+        self.steps = 0                 # iterations taken: the dropout generator's step counter
 
     def step(self, x: torch.Tensor, y: torch.Tensor) -> None:
+        self.hp.dropout_step = self.steps
         self.ctx.train_step(self.nd, self.params, self.workspace, x, y, self.hp)
+        self.steps += 1
 
     def step_graph(self, x: torch.Tensor, y: torch.Tensor) -> None:
         """One iteration replayed from the context's captured graph for these buffers (captured
-        on the first call with them; up to 16 buffer sets keep graphs of their own)."""
+        on the first call with them; up to 16 buffer sets keep graphs of their own). The dropout
+        step counter is part of a graph's arguments, so workloads with dropout take the eager
+        path instead."""
+        if self.wl.dropout_conv_ppm or self.wl.dropout_lin_ppm:
+            return self.step(x, y)
         self.ctx.train_step_graph(self.nd, self.params, self.workspace, x, y, self.hp)
+        self.steps += 1
 
     def infer(self, x: torch.Tensor):
         """Inference with the current weights: (yhat [n][G] int32, predicted class [n] int32)."""

@@ -93,6 +93,9 @@ class Workload:
     delta_bound: int = 0               # stress case: |delta| <= delta_bound at the ReLU output
     d_lr: int = 0                      # learning-layer input size of conv blocks (d^lr, Tab. 6);
     #                                    0: the learning layer reads the block output
+    dropout_conv_ppm: int = 0          # dropout rates p_c, p_l of Tab. 6, parts per million
+    dropout_lin_ppm: int = 0
+    dropout_seed: int = 0              # key of the dropout generator
 
     # ---- derived shapes (bookkeeping only) ----
     @property
@@ -209,7 +212,7 @@ CONV_STRESS = Workload(
 # follows it, if any) is one local-loss block; every hidden IntLinear is an integer linear block;
 # the last IntLinear is the output layer. Conv blocks' learning layers read the block output
 # max-pooled to at most d^lr = 4096 features.
-def _vgg(name, convs, lam_fw, lam_lr):
+def _vgg(name, convs, lam_fw, lam_lr, p_lin_ppm=0):
     blocks = []
     c = 3
     for co, pool in convs:
@@ -218,12 +221,12 @@ def _vgg(name, convs, lam_fw, lam_lr):
     blocks.append(Block((Linear(512 * 2 * 2, 1024),), maxpool=False, learning=True))
     return Workload(name=name, batch=64, in_shape=(3, 32, 32), blocks=tuple(blocks), n_classes=10,
                     head=True, gamma_inv=512, lambda_inv_fw=lam_fw, lambda_inv_lr=lam_lr,
-                    alpha_inv=10, steps=10, d_lr=4096)
+                    alpha_inv=10, steps=10, d_lr=4096, dropout_lin_ppm=p_lin_ppm, dropout_seed=1)
 
 
 VGG8B = _vgg("vgg8b_cifar10_b64",
              [(128, False), (256, True), (256, False), (512, True), (512, True), (512, True)],
-             25000, 3000)
+             25000, 3000, p_lin_ppm=150000)
 VGG11B = _vgg("vgg11b_cifar10_b64",
               [(128, False), (128, False), (128, False), (256, True), (256, False), (512, True),
                (512, False), (512, True), (512, True)], 28000, 4500)
@@ -240,7 +243,7 @@ MLP4 = Workload(
             Block((Linear(3000, 3000),), maxpool=False, learning=True),
             Block((Linear(3000, 3000),), maxpool=False, learning=True)),
     n_classes=10, head=True, gamma_inv=512, lambda_inv_fw=19000, lambda_inv_lr=7500,
-    alpha_inv=10, steps=10)
+    alpha_inv=10, steps=10, dropout_lin_ppm=100000, dropout_seed=1)
 
 WORKLOADS = {w.name: w for w in (TINY_CNN, MLP, SMALL_CNN, VGG_CNN, CONV_STRESS, VGG8B, VGG11B,
                                  MLP3, MLP4)}

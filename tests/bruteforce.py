@@ -113,3 +113,19 @@ def maxpool_window(a, kh, kw):
                     P[n][i][j][c] = best
                     I[n][i][j][c] = arg
     return P, I
+
+
+def philox4x64_10(ctr, key):
+    """Philox4x64 with 10 rounds, written from its published definition (Salmon et al., SC'11):
+    each round multiplies counter words 0 and 2 by two fixed 64-bit constants, and recombines the
+    128-bit products' halves with words 1 and 3 and the key; the key is bumped by two Weyl
+    constants between rounds. Python integers, so nothing wraps that should not."""
+    mask = (1 << 64) - 1
+    m0, m1 = 0xD2E7470EE14C6C93, 0xCA5A826395121157
+    w0, w1 = 0x9E3779B97F4A7C15, 0xBB67AE8584CAA73B
+    c, k = list(ctr), list(key)
+    for _ in range(10):
+        p0, p1 = m0 * c[0], m1 * c[2]
+        c = [(p1 >> 64) ^ c[1] ^ k[0], p1 & mask, (p0 >> 64) ^ c[3] ^ k[1], p0 & mask]
+        k = [(k[0] + w0) & mask, (k[1] + w1) & mask]
+    return c

@@ -1,6 +1,8 @@
 """GPU parity: the HIP library (through the C ABI) against the CPU oracle, element by element and
 bit-exact, on seeded inputs. Block-level calls at shapes that span several tiles and ragged
 tails, the edge cases of the method, IntegerSGD, the output layer and whole training steps."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -348,7 +350,9 @@ def test_head(ctx, modes):
 
 def oracle_net(wl, weights, om):
     hp = O.Hyper(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr, wl.alpha_inv, wl.n_classes,
-                 mode=om, af_classes=wl.af_classes, d_lr=wl.d_lr)
+                 mode=om, af_classes=wl.af_classes, d_lr=wl.d_lr,
+                 dropout_conv_ppm=wl.dropout_conv_ppm, dropout_lin_ppm=wl.dropout_lin_ppm,
+                 dropout_seed=wl.dropout_seed)
     specs = [(len(b.layers), b.maxpool, b.learning) for b in wl.blocks]
     return O.OracleNet(specs, wl.head, weights, hp)
 
@@ -394,8 +398,11 @@ def check_training(ctx, wl, steps, nm, om):
                     same(v["code"][j], region_codes(ly.zs), tag + "codes %d" % j)
                 same(v["dw"][j], rec.dw[j], tag + "dW %d" % j)
             last = rec.layers[-1]
-            same(v["code"][J - 1], pooled_codes(last.zs, rec.pool_idx) if rec.pool_idx is not None
-                 else region_codes(last.zs), tag + "codes %d" % (J - 1))
+            code = (pooled_codes(last.zs, rec.pool_idx) if rec.pool_idx is not None
+                    else region_codes(last.zs))
+            if rec.keep is not None:       # a dropped output's region reads "saturated"
+                code = np.where(rec.keep, code, (code & 3) + 8 if rec.pool_idx is not None else 2)
+            same(v["code"][J - 1], code, tag + "codes %d" % (J - 1))
             same(v["yhat"], rec.yhat, tag + "yhat")
             same(v["e"], rec.e, tag + "e")
             same(v["dw_lr"], rec.dw_lr, tag + "dW learning")
@@ -437,6 +444,20 @@ def test_train_paper_nets(ctx, wl, steps, modes):
     block outputs max-pooled to 4096 features, a linear block after the conv blocks, the
     output layer; every workspace tensor and weight after every step."""
     check_training(ctx, wl, steps, *modes)
+
+
+@pytest.mark.parametrize("wl", [
+    dataclasses.replace(WL.scaled(WL.SMALL_CNN, 8), dropout_conv_ppm=300000, dropout_seed=12345),
+    dataclasses.replace(WL.MLP, dropout_lin_ppm=500000, dropout_seed=7),
+    dataclasses.replace(WL.scaled(WL.VGG8B, 2), dropout_conv_ppm=100000, dropout_lin_ppm=150000,
+                        dropout_seed=99),
+    dataclasses.replace(WL.scaled(WL.TINY_CNN, 4), dropout_conv_ppm=1000000)],
+    ids=["small_cnn_pc30", "mlp_pl50", "vgg8b_pc10_pl15", "tiny_cnn_pc100"])
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_train_dropout(ctx, wl, modes):
+    """Dropout of block outputs with the Philox4x64-10 masks (conv and linear blocks, pooled and
+    unpooled, rates up to 1): every workspace tensor and weight after every step."""
+    check_training(ctx, wl, 4, *modes)
 
 
 @pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])

@@ -348,6 +348,69 @@ def test_infer_matches_training_forward(mode):
     assert yhat.tolist() == h[mode]["yhat"] and pred.tolist() == [0]
 
 
+def test_philox_known_answers():
+    """The from-definition Philox4x64-10 reproduces the published known-answer vectors, and
+    numpy's Philox bit generator (which the oracle draws from) gives the same words for counter
+    c + 1 when started at c."""
+    for v in gold("philox.json")["vectors"]:
+        ctr = [int(h, 16) for h in v["ctr"]]
+        key = [int(h, 16) for h in v["key"]]
+        assert BF.philox4x64_10(ctr, key) == [int(h, 16) for h in v["out"]]
+    for ctr, key in (([0, 3, 7, 0], [11, 0]), ([41, 0, 2, 0], [2 ** 63 + 5, 0])):
+        g = np.random.Philox(key=np.array(key, np.uint64), counter=np.array(ctr, np.uint64))
+        raw = [int(w) for w in g.random_raw(8)]
+        for j in range(2):
+            c = list(ctr)
+            c[0] += j + 1
+            assert raw[4 * j:4 * j + 4] == BF.philox4x64_10(c, key)
+
+
+def test_dropout_mask_definition():
+    """The oracle's mask against the generator written from its definition, element by element,
+    and its keep rate against 1 - p within six standard deviations."""
+    count, seed, step, block, ppm = 103, 77, 5, 3, 150000
+    keep = O.dropout_keep(count, seed, step, block, ppm)
+    t = (ppm << 32) // 1000000
+    exp = []
+    for i in range(count):
+        w = BF.philox4x64_10([i // 4 + 1, block, step, 0], [seed, 0])[i % 4]
+        exp.append((w >> 32) >= t)
+    assert keep.tolist() == exp
+    big = O.dropout_keep(400000, 1, 0, 0, ppm)
+    sd = (400000 * 0.15 * 0.85) ** 0.5
+    assert abs(int((~big).sum()) - 400000 * 0.15) < 6 * sd
+    assert O.dropout_keep(50, 1, 2, 3, 0).all() and not O.dropout_keep(50, 1, 2, 3, 1000000).any()
+
+
+@pytest.mark.parametrize("mode", ["floor", "trunc"])
+def test_dropout_special_cases(mode):
+    """Rate 0 is the step without dropout; rate 1 zeroes every block output, so no gradient
+    reaches the forward layers (their weights only decay) and the learning layer sees zeros."""
+    from paper_2407_11698_amd import workloads as WL
+    wl = WL.scaled(WL.SMALL_CNN, 4)
+    dr = WL.draw_workload(wl, O.kaiming_bound, steps=1)
+    x, y = dr.batches[0]
+    specs = [(len(b.layers), b.maxpool, b.learning) for b in wl.blocks]
+    base = dict(gamma_inv=wl.gamma_inv, lambda_inv_fw=wl.lambda_inv_fw, lambda_inv_lr=wl.lambda_inv_lr,
+                alpha_inv=wl.alpha_inv, n_classes=wl.n_classes, mode=MODES[mode])
+    ref = O.OracleNet(specs, wl.head, dr.weights, O.Hyper(**base))
+    r0 = O.OracleNet(specs, wl.head, dr.weights, O.Hyper(**base, dropout_conv_ppm=0, dropout_seed=9))
+    ref.train_step(x, y)
+    r0.train_step(x, y)
+    assert all(np.array_equal(a, b) for a, b in zip(ref.w, r0.w))
+    r1 = O.OracleNet(specs, wl.head, dr.weights, O.Hyper(**base, dropout_conv_ppm=1000000))
+    st = r1.train_step(x, y)
+    for b, rec in enumerate(st.blocks):
+        assert not rec.out.any()
+        assert all(not dw.any() for dw in rec.dw) and not rec.dw_lr.any()
+    hp = r1.hp
+    for k, w in enumerate(dr.weights[:-1]):
+        fw = any(k in idx[0] for idx in r1.index)
+        gamma = hp.gamma_fw if fw else hp.gamma_inv
+        lam = hp.lambda_inv_fw if fw else hp.lambda_inv_lr
+        assert np.array_equal(r1.w[k], O.integer_sgd(w, np.zeros_like(w, np.int64), gamma, lam, MODES[mode]))
+
+
 # ---------------------------------------------------------------- brute force, tiny shapes
 
 def _rand(rng, shape, lo, hi, dtype=np.int64):
