@@ -160,6 +160,110 @@ def stress_layer(reps: int):
     return res
 
 
+def paper_nets(steps: int = 10, warmup: int = 2):
+    """The paper's own architectures (Tab. 1) at their batch of 64 (Tab. 6) on synthetic CIFAR-10-
+    and MNIST-shaped inputs: images/s of the training iteration (HIP events around `steps`
+    iterations after `warmup`; graph replay, or eager launches for workloads with dropout, whose
+    generator step changes every iteration) and of inference (nitro_net_infer)."""
+    import torch
+    from paper_2407_11698_amd import runner
+    from paper_2407_11698_amd import workloads as WL
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+    res = {}
+    for wl in WL.PAPER_NETS:
+        dr = WL.draw_workload(wl, runner.kaiming_bound, steps=wl.steps)
+        xs = [torch.from_numpy(x).to(dev) for x, _ in dr.batches]
+        ys = [torch.from_numpy(y).to(dev) for _, y in dr.batches]
+        net = runner.GpuNet(wl, dr.weights)
+        graph = not (wl.dropout_conv_ppm or wl.dropout_lin_ppm)
+        step = net.step_graph if graph else net.step
+        for i in range(warmup):
+            step(xs[i % len(xs)], ys[i % len(ys)])
+        net.ctx.sync()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(steps):
+            step(xs[i % len(xs)], ys[i % len(ys)])
+        e1.record(stream)
+        net.ctx.sync()
+        ms = e0.elapsed_time(e1) / steps
+        net.infer(xs[0])
+        net.ctx.sync()
+        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        f0.record(stream)
+        for i in range(steps):
+            net.infer(xs[i % len(xs)])
+        f1.record(stream)
+        net.ctx.sync()
+        ims = f0.elapsed_time(f1) / steps
+        res[wl.name] = {"batch": wl.batch, "train_images_per_s": round(wl.batch / (ms * 1e-3), 1),
+                        "train_ms_per_step": round(ms, 4), "launch": "graph replay" if graph else "eager",
+                        "dropout_ppm": {"conv": wl.dropout_conv_ppm, "linear": wl.dropout_lin_ppm},
+                        "infer_images_per_s": round(wl.batch / (ims * 1e-3), 1),
+                        "infer_ms_per_batch": round(ims, 4)}
+        del net, xs, ys
+    return res
+
+
+def infer_bench(reps: int = 20):
+    """Inference (forward and prediction, nitro_net_infer) of the benchmark workload with the
+    initial weights, images/s over `reps` batches (HIP events)."""
+    import torch
+    from paper_2407_11698_amd import runner
+    from paper_2407_11698_amd import workloads as WL
+    wl = WL.VGG_CNN
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+    dr = WL.draw_workload(wl, runner.kaiming_bound, steps=2)
+    net = runner.GpuNet(wl, dr.weights)
+    x = torch.from_numpy(dr.batches[0][0]).to(dev)
+    net.infer(x)
+    net.ctx.sync()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        net.infer(x)
+    e1.record(stream)
+    net.ctx.sync()
+    ms = e0.elapsed_time(e1) / reps
+    return {"workload": wl.name, "batch": wl.batch, "images_per_s": round(wl.batch / (ms * 1e-3), 1),
+            "ms_per_batch": round(ms, 4)}
+
+
+def preprocess_bench(reps: int = 10):
+    """The integer pre-processing of Appendix A on the CIFAR-10-sized synthetic byte dataset
+    (50000 x 32 x 32 x 3): device time per pass (HIP events), and HBM rate of its algorithmic
+    traffic, 3 bytes per element (the statistics need the data read once, the normalisation
+    reads it again and writes it), against the 8 TB/s peak."""
+    import torch
+    from paper_2407_11698_amd import nitro as N
+    from paper_2407_11698_amd import workloads as WL
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+    x = torch.from_numpy(WL.draw_image_bytes(WL.CIFAR10_BYTES).reshape(-1)).to(dev)
+    out = torch.empty(x.numel(), dtype=torch.int8, device=dev)
+    stats = torch.zeros(3, dtype=torch.int64, device=dev)
+    ws = torch.empty(N.preprocess_query(x.numel()), dtype=torch.uint8, device=dev)
+    ctx = N.Context(0)
+    ctx.preprocess(x, out, stats, ws)
+    ctx.sync()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        ctx.preprocess(x, out, stats, ws)
+    e1.record(stream)
+    ctx.sync()
+    ms = e0.elapsed_time(e1) / reps
+    gbs = 3 * x.numel() / (ms * 1e-3) / 1e9
+    st = stats.cpu().tolist()
+    ctx.close()
+    return {"dataset": "50000x32x32x3 uint8 (synthetic)", "ms": round(ms, 4),
+            "algorithmic_bytes": 3 * x.numel(), "GB_per_s": round(gbs, 1),
+            "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "mu": st[0], "omega": st[1],
+            "clamped": st[2]}
+
+
 def cpu_baseline(wl, min_s: float = 12.0, budget_s: float = 25.0):
     """The CPU oracle, untuned, on a bounded sample of the same workload: full training
     iterations at a reduced batch (cycling through the ten seeded batches) until at least
@@ -245,7 +349,7 @@ def main():
     ap.add_argument("--eager", action="store_true",
                     help="launch every kernel from the host each step instead of replaying the "
                          "captured iteration (nitro_train_step_graph)")
-    ap.add_argument("--serial-steps", type=int, default=3,
+    ap.add_argument("--serial-steps", type=int, default=9,
                     help="training iterations run after the timed region with every block on "
                          "one stream, for per-launch kernel times without overlap (0 skips)")
     ap.add_argument("--stress-reps", type=int, default=20,
@@ -253,6 +357,9 @@ def main():
                          "the training iterations (0 skips it)")
     ap.add_argument("--mfma-probe-iters", type=int, default=20000,
                     help="MFMAs per chain of the int8 matrix-core rate probe (0: skip it)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the paper architectures, the inference and the pre-processing "
+                         "measurements after the training iterations")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB before the warm-up: "
                          "the known-size reference for hardware byte counters")
@@ -348,23 +455,32 @@ def main():
     dom = max(per_class, key=lambda k: per_class[k]["ms_per_step"])
     achieved = per_class[dom]["algorithmic_TOPs"]
 
-    # the same kernels with the blocks' local training on one stream, after the timed region:
-    # each launch then has the GPU to itself, as under a kernel-trace profiler
-    serial = {}
+    # the roofline kernel's launch durations: the same trajectory after the timed region, launched
+    # eagerly with every block on the library's one stream (a launch then has the GPU to itself,
+    # as under a kernel-trace profiler), each launch of a timed kernel class measured by the
+    # device timestamps its workgroups record (first start to last end); then the same with HIP
+    # events around each launch on its stream, as a cross-check (the event markers add a few
+    # microseconds per launch)
+    serial, serial_ev = {}, {}
     if args.serial_steps > 0:
         net.ctx.set_aux_streams(0)
-        run(0, 1)
-        net.ctx.sync()
-        net.ctx.kernel_timing(True)
-        run(1, args.serial_steps)
-        net.ctx.sync()
-        steps_timed = 1 if graph else args.serial_steps     # graph: the last replay's times
-        for c, name in KERNEL_CLASSES.items():
-            ms, launches = net.ctx.kernel_time(c)
-            if launches:
-                serial[name] = {"avg_launch_us": round(ms * 1e3 / launches, 2),
-                                "algorithmic_TOPs": round(ops[name] * steps_timed / (ms * 1e-3) / 1e12, 3)}
-        net.ctx.kernel_timing(False)
+        for res, events in ((serial, False), (serial_ev, True)):
+            for a, b in zip(net.w, w0):
+                a.copy_(b)
+            net.step(xs[0], ys[0])
+            net.ctx.sync()
+            net.ctx.kernel_timing(True, events=events)
+            for i in range(1, 1 + args.serial_steps):
+                net.step(xs[i % period], ys[i % period])
+            net.ctx.sync()
+            for c, name in KERNEL_CLASSES.items():
+                ms, launches = net.ctx.kernel_time(c)
+                if launches:
+                    res[name] = {"ms_per_step": round(ms / args.serial_steps, 4),
+                                 "launches_per_step": launches // args.serial_steps,
+                                 "avg_launch_us": round(ms * 1e3 / launches, 2),
+                                 "algorithmic_TOPs": round(ops[name] * args.serial_steps / (ms * 1e-3) / 1e12, 3)}
+            net.ctx.kernel_timing(False)
         net.ctx.set_aux_streams(3)
     conv_ms = sum(v["ms_per_step"] for v in per_class.values())
     conv_tops = sum(ops.values()) / (conv_ms * 1e-3) / 1e12 if conv_ms > 0 else 0.0
@@ -391,21 +507,39 @@ def main():
                    "lambda_inv_fw": wl.lambda_inv_fw, "lambda_inv_lr": wl.lambda_inv_lr,
                    "alpha_inv": wl.alpha_inv, "rounding": "floor",
                    "launch": "graph replay" if graph else "eager"},
-        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved,
-                     "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
-                     "frac": round(achieved / PEAK_INT8_TOPS, 5),
-                     "traffic": recorded_traffic(dom)},
         "conv_mfma": {"algorithmic_TOPs": round(conv_tops, 3),
                       "frac_of_int8_peak": round(conv_tops / PEAK_INT8_TOPS, 5),
-                      "per_kernel": per_class},
+                      "timed_region_per_kernel": per_class,
+                      "timed_region_timing": "device timestamps of each launch's first and last "
+                                             "workgroups, inside the replayed graph (blocks on "
+                                             "four streams)"},
     }
     if serial:
-        sd = serial.get(dom)
-        out["roofline"]["serial"] = {
-            "steps": args.serial_steps, "avg_launch_us": sd["avg_launch_us"] if sd else None,
-            "achieved": sd["algorithmic_TOPs"] if sd else None,
-            "frac": round(sd["algorithmic_TOPs"] / PEAK_INT8_TOPS, 5) if sd else None}
+        # the dominant kernel class of the serial pass; achieved = its algorithmic ops per step /
+        # its summed launch time per step (= ops per launch / average launch duration)
+        sdom = max(serial, key=lambda k: serial[k]["ms_per_step"])
+        sd = serial[sdom]
+        out["roofline"] = {"bound": "mfma", "kernel": sdom, "achieved": sd["algorithmic_TOPs"],
+                           "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                           "frac": round(sd["algorithmic_TOPs"] / PEAK_INT8_TOPS, 5),
+                           "avg_launch_us": sd["avg_launch_us"],
+                           "launches_per_step": sd["launches_per_step"],
+                           "ops_per_step": ops[sdom],
+                           "traffic": recorded_traffic(sdom),
+                           "avg_launch_us_events": serial_ev.get(sdom, {}).get("avg_launch_us"),
+                           "timing": "device timestamps of each launch (first workgroup start to "
+                                     "last workgroup end), %d eager iterations of the same "
+                                     "trajectory after the timed region, every block on one "
+                                     "stream; avg_launch_us_events: HIP events around each launch "
+                                     "on its stream in the same setting" % args.serial_steps}
         out["conv_mfma"]["serial_per_kernel"] = serial
+        out["conv_mfma"]["serial_per_kernel_events"] = serial_ev
+    else:
+        out["roofline"] = {"bound": "mfma", "kernel": dom, "achieved": achieved,
+                           "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
+                           "frac": round(achieved / PEAK_INT8_TOPS, 5),
+                           "traffic": recorded_traffic(dom),
+                           "timing": "device timestamps in the timed region"}
     if args.mfma_probe_iters > 0:
         # the dense int8 matrix-core rate on this GPU (register-only MFMA chains, two waves per
         # SIMD); `peak` above stays the published figure
@@ -413,6 +547,10 @@ def main():
                                   "waves_per_simd": 2, "published_TOPs": PEAK_INT8_TOPS}
     if args.stress_reps > 0:
         out["stress_conv"] = stress_layer(args.stress_reps)
+    if not args.no_extras:
+        out["paper_nets"] = paper_nets()
+        out["inference"] = infer_bench()
+        out["preprocess"] = preprocess_bench()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)
         out["cpu_baseline"]["one_core"] = one_core

@@ -390,7 +390,8 @@ int32_t nitro_host_relu_mu(int32_t alpha_inv, int32_t round);
  * Returns 0 for fan_in < 1. */
 int32_t nitro_host_kaiming_bound(int64_t fan_in);
 
-/* Per-kernel timing for profiling. While enabled, every launch of a timed kernel class records,
+/* Per-kernel timing for profiling. enable = 1 (device timestamps): while enabled, every launch of a
+ * timed kernel class records,
  * on the device, the wall-clock time from its first workgroup's start to its last workgroup's
  * end (this also works inside a graph replayed by nitro_train_step_graph). Classes: 0 the tiled
  * int8 MFMA conv forward kernel, 1 the tiled conv input-gradient kernel, 2 the conv
@@ -399,6 +400,10 @@ int32_t nitro_host_kaiming_bound(int64_t fan_in);
  * nitro_kernel_time synchronises the context's stream and returns the summed milliseconds and
  * the number of launches: of the launches enqueued since the last read or enable, or, when a
  * graph was captured with timing on, of the last replay. */
+/* enable = 2 (events): every eager launch of a timed class (not one being captured into a graph)
+ * is bracketed by two HIP events recorded on the stream it is launched on; nitro_kernel_time
+ * then returns the summed event-to-event times of the launches since the last read (at most
+ * 1024 per class). 0 disables timing. EINVAL for other values. */
 nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable);
 nitro_status nitro_kernel_time(nitro_ctx *ctx, int32_t cls, double *ms, int64_t *launches);
 

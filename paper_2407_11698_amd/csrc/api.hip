@@ -94,8 +94,47 @@ struct nitro_ctx : public LaunchTimer {
 
     uint64_t *slot(int cls) override
     {
-        if (!tsbuf || used[cls] >= (size_t)TS_CAP) return nullptr;
+        if (by_events || !tsbuf || used[cls] >= (size_t)TS_CAP) return nullptr;
         return tsbuf + ((size_t)cls * TS_CAP + used[cls]++) * TS_WORDS;
+    }
+    // event timing: a pair of events per eager launch of a timed class (not inside a capture)
+    bool by_events = false;
+    std::vector<hipEvent_t> evpool[TIMED_CLASSES];
+    size_t evused[TIMED_CLASSES] = {0, 0, 0};
+    static bool capturing(hipStream_t s)
+    {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        return hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone;
+    }
+    hipEvent_t next_event(int cls)
+    {
+        if (evused[cls] >= 2 * (size_t)TS_CAP) return nullptr;
+        if (evused[cls] == evpool[cls].size()) {
+            hipEvent_t e = nullptr;
+            if (hipEventCreate(&e) != hipSuccess) return nullptr;
+            evpool[cls].push_back(e);
+        }
+        return evpool[cls][evused[cls]++];
+    }
+    void ev_begin(int cls, hipStream_t s) override
+    {
+        if (!by_events || capturing(s) || evused[cls] % 2 != 0) return;
+        hipEvent_t e = next_event(cls);
+        if (e) (void)hipEventRecord(e, s);
+    }
+    void ev_end(int cls, hipStream_t s) override
+    {
+        if (!by_events || evused[cls] % 2 != 1) return;
+        hipEvent_t e = next_event(cls);
+        if (e) (void)hipEventRecord(e, s);
+    }
+    void drop_events()
+    {
+        for (auto &v : evpool) {
+            for (hipEvent_t e : v) (void)hipEventDestroy(e);
+            v.clear();
+        }
+        for (auto &u : evused) u = 0;
     }
     nitro_status ensure_aux()
     {
@@ -137,7 +176,10 @@ size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 // Installs the context's launch timer for the duration of an API call.
 struct TimerScope {
     LaunchTimer *prev;
-    explicit TimerScope(nitro_ctx *ctx) : prev(g_timer) { g_timer = ctx->timing ? ctx : nullptr; }
+    explicit TimerScope(nitro_ctx *ctx) : prev(g_timer)
+    {
+        g_timer = (ctx->timing || ctx->by_events) ? ctx : nullptr;
+    }
     ~TimerScope() { g_timer = prev; }
 };
 
@@ -731,6 +773,7 @@ void nitro_destroy(nitro_ctx *ctx)
     DeviceGuard guard(ctx->device);
     (void)hipStreamSynchronize(ctx->stream);
     ctx->drop_graphs();
+    ctx->drop_events();
     if (ctx->tsbuf) (void)hipFree(ctx->tsbuf);
     if (ctx->aux_ready) {
         for (int b = 0; b < nitro_ctx::NAUX; b++) {
@@ -1299,9 +1342,13 @@ nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable)
 {
     if (!ctx) return NITRO_EINVAL;
     DeviceGuard guard(ctx->device);
+    if (enable < 0 || enable > 2) return NITRO_EINVAL;
     // graphs captured before hold the timing state and slot assignment of their capture
     ctx->drop_graphs();
-    ctx->timing = enable != 0;
+    (void)hipStreamSynchronize(ctx->stream);
+    ctx->drop_events();
+    ctx->by_events = enable == 2;
+    ctx->timing = enable == 1;
     if (ctx->timing) {
         const int64_t nslots = (int64_t)TIMED_CLASSES * nitro_ctx::TS_CAP;
         if (!ctx->tsbuf && hipMalloc((void **)&ctx->tsbuf, (size_t)nslots * TS_WORDS * 8) != hipSuccess) {
@@ -1355,6 +1402,21 @@ nitro_status nitro_kernel_time(nitro_ctx *ctx, int32_t cls, double *ms, int64_t 
     DeviceGuard guard(ctx->device);
     *ms = 0.0;
     *launches = 0;
+    if (ctx->by_events) {
+        // pairs recorded since the last read; then the pool's events are reused
+        if (hipStreamSynchronize(ctx->stream) != hipSuccess) return NITRO_EHIP;
+        const size_t pairs = ctx->evused[cls] / 2;
+        for (size_t i = 0; i < pairs; i++) {
+            float t = 0.f;
+            if (hipEventSynchronize(ctx->evpool[cls][2 * i + 1]) != hipSuccess ||
+                hipEventElapsedTime(&t, ctx->evpool[cls][2 * i], ctx->evpool[cls][2 * i + 1]) != hipSuccess)
+                return NITRO_EHIP;
+            *ms += t;
+        }
+        *launches = (int64_t)pairs;
+        ctx->evused[cls] = 0;
+        return NITRO_OK;
+    }
     if (!ctx->tsbuf || ctx->used[cls] == 0) return NITRO_OK;
     if (hipStreamSynchronize(ctx->stream) != hipSuccess) return NITRO_EHIP;
     int khz = 0;

@@ -547,10 +547,13 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
     const unsigned nwg = (unsigned)(pl.tiles_co * pl.tiles_ci * pl.nsplit);
     a.ts = timer_slot(TIMED_DW);
     const size_t lds = lds_stage > lds_red ? lds_stage : lds_red;
-    if (pl.chunk >= DWP_L3_MIN)
-        hipLaunchKernelGGL(k_conv_dw_planes<true>, dim3(nwg), dim3(256), lds, s, a);
-    else
-        hipLaunchKernelGGL(k_conv_dw_planes<false>, dim3(nwg), dim3(256), lds, s, a);
+    {
+        TimedLaunch tl(TIMED_DW, s);
+        if (pl.chunk >= DWP_L3_MIN)
+            hipLaunchKernelGGL(k_conv_dw_planes<true>, dim3(nwg), dim3(256), lds, s, a);
+        else
+            hipLaunchKernelGGL(k_conv_dw_planes<false>, dim3(nwg), dim3(256), lds, s, a);
+    }
     if (pl.nsplit > 1) launch_sum_partials(s, part, pl.nsplit, (int64_t)sh.co * 9 * sh.c, dw);
 }
 

@@ -753,6 +753,7 @@ static void launch_tile(hipStream_t s, int persist, TileArgs a)
     a.d_aseg = make_div32((uint32_t)((a.rs + 2) * a.apitch));
     const int cus = device_cu_count();
     const bool big = a.ntiles >= CT_PERSIST_TILES_PER_CU * cus;
+    TimedLaunch tl(MODE == IG_FWD ? TIMED_CONV_FWD : TIMED_CONV_DX, s);
     if (WM == 4 && (persist > 0 || (persist == 0 && big))) {
         int g = (a.ntiles + CT_PERSIST_TILES_PER_CU - 1) / CT_PERSIST_TILES_PER_CU;
         if (g > cus) g = cus;

@@ -399,10 +399,26 @@ enum { TIMED_CONV_FWD = 0, TIMED_CONV_DX = 1, TIMED_DW = 2, TIMED_CLASSES = 3 };
 constexpr int TS_SPREAD = 16, TS_WORDS = 2 * TS_SPREAD;
 struct LaunchTimer {
     virtual uint64_t *slot(int cls) = 0;
+    // event timing (eager launches only): events recorded on the launch's stream around it
+    virtual void ev_begin(int cls, hipStream_t s) {}
+    virtual void ev_end(int cls, hipStream_t s) {}
     virtual ~LaunchTimer() {}
 };
 extern thread_local LaunchTimer *g_timer;
 inline uint64_t *timer_slot(int cls) { return g_timer ? g_timer->slot(cls) : nullptr; }
+// Brackets one timed kernel launch with the installed timer's events (when it times by events).
+struct TimedLaunch {
+    int cls;
+    hipStream_t s;
+    TimedLaunch(int c, hipStream_t st) : cls(c), s(st)
+    {
+        if (g_timer) g_timer->ev_begin(cls, s);
+    }
+    ~TimedLaunch()
+    {
+        if (g_timer) g_timer->ev_end(cls, s);
+    }
+};
 
 __device__ inline unsigned ts_block_id()
 {

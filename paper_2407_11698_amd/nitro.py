@@ -390,8 +390,11 @@ class Context:
         return out.value
 
     # -- profiling ----------------------------------------------------------------------
-    def kernel_timing(self, enable: bool) -> None:
-        check(LIB.nitro_kernel_timing(self.h, 1 if enable else 0), "nitro_kernel_timing")
+    def kernel_timing(self, enable, events: bool = False) -> None:
+        """Per-kernel timing: device timestamps (enable), or HIP events around each eager launch
+        (enable and events)."""
+        mode = 0 if not enable else (2 if events else 1)
+        check(LIB.nitro_kernel_timing(self.h, mode), "nitro_kernel_timing")
 
     def kernel_time(self, cls: int):
         ms = ctypes.c_double(0)
