@@ -1146,6 +1146,23 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     if (st != NITRO_OK) return st;
     const int nuse = ctx->aux_use;
     unsigned used_aux = 0;
+    // every auxiliary stream that joined the iteration is joined back to the context's stream
+    // before returning, on error too: a capture can only end once every stream forked from the
+    // capturing one has been joined into it
+    auto join_aux = [&]() -> bool {
+        bool ok = true;
+        for (int a = 0; a < nuse; a++) {
+            if (!(used_aux & (1u << a))) continue;
+            ok &= hipEventRecord(ctx->join[a], ctx->aux[a]) == hipSuccess;
+            ok &= hipStreamWaitEvent(ctx->stream, ctx->join[a], 0) == hipSuccess;
+        }
+        used_aux = 0;
+        return ok;
+    };
+    auto fail = [&](nitro_status e) -> nitro_status {
+        (void)join_aux();
+        return e;
+    };
     auto backward = [&](int b, hipStream_t bs) -> nitro_status {
         const nitro_block_desc &d = net->block[b];
         const int8_t *xin = b == 0 ? x : (const int8_t *)at(workspace, g.aout[b - 1]);
@@ -1173,19 +1190,19 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
                      b, net->block[b].maxpool};
         st = block_forward_impl(ctx, &net->block[b], g.b[b], &bp, cur, aout, at(workspace, g.state[b]),
                                 false, true, b == 0, true, &drop);
-        if (st != NITRO_OK) return st;
+        if (st != NITRO_OK) return fail(st);
         cur = aout;
         if (b + 1 == net->n_blocks) break;
         hipStream_t bs = ctx->stream;
         if (nuse > 0) {
             const int a = b % nuse;
             bs = ctx->aux[a];
-            if (hipEventRecord(ctx->fev[b], ctx->stream) != hipSuccess) return NITRO_EHIP;
-            if (hipStreamWaitEvent(bs, ctx->fev[b], 0) != hipSuccess) return NITRO_EHIP;
+            if (hipEventRecord(ctx->fev[b], ctx->stream) != hipSuccess) return fail(NITRO_EHIP);
             used_aux |= 1u << a;
+            if (hipStreamWaitEvent(bs, ctx->fev[b], 0) != hipSuccess) return fail(NITRO_EHIP);
         }
         st = backward(b, bs);
-        if (st != NITRO_OK) return st;
+        if (st != NITRO_OK) return fail(st);
     }
     // 2. output layer: global gradient (its update comes with the others, step 4)
     const int n = net->block[0].n;
@@ -1200,12 +1217,8 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     }
     // 3. the last block's local training; the context's stream then waits for the others
     st = backward(net->n_blocks - 1, ctx->stream);
-    if (st != NITRO_OK) return st;
-    for (int a = 0; a < nuse; a++) {
-        if (!(used_aux & (1u << a))) continue;
-        if (hipEventRecord(ctx->join[a], ctx->aux[a]) != hipSuccess) return NITRO_EHIP;
-        if (hipStreamWaitEvent(ctx->stream, ctx->join[a], 0) != hipSuccess) return NITRO_EHIP;
-    }
+    if (st != NITRO_OK) return fail(st);
+    if (!join_aux()) return NITRO_EHIP;
     // 4. IntegerSGD (Alg. 1) of every weight tensor, after every gradient is complete
     if (net->head) {
         st = sgd_entry(ctx, sgd, params->w_head, hdw, (int64_t)G * g.hd, hp->gamma_inv,

@@ -1,4 +1,4 @@
-"""Write the full-size expected results of the two benchmark-sized workloads as digests.
+"""Write the full-size expected results of the benchmark-sized workloads as digests.
 
 Runs only the CPU oracle (``oracle/``) on the seeded draws of ``paper_2407_11698_amd/workloads.py``
 and stores, for every step, the SHA-256 of every tensor the oracle computes, in the dtype the
@@ -12,10 +12,13 @@ digests after every step.
     every layer's pre-activation and every weight gradient; then every weight after the update.
   * single conv layer 256 -> 256 on 256x256x32x32, twenty repeats with IntegerSGD between them:
     the activations, region codes, the gradient at the pre-activation, the weight gradient, the
-    int64 input gradient and the weights after the update.
+    int64 input gradient and the weights after the update;
+  * the paper's architectures VGG8B, VGG11B, MLP 3 and MLP 4 at their batch of 64, three training
+    iterations each (learning-layer pooling, dropout), through the whole-iteration call: every
+    tensor but delta^fw and the pre-activation gradients, and the output layer's tensors.
 
-Usage: ``python tests/golden/make_digests.py [vgg|stress|all]`` (the single conv layer takes about
-half an hour on 8 cores).
+Usage: ``python tests/golden/make_digests.py [vgg|stress|paper|all]`` (the single conv layer takes
+about half an hour on 8 cores).
 """
 from __future__ import annotations
 
@@ -80,10 +83,16 @@ def pooled_codes(zs, idx) -> np.ndarray:
     return idx + 4 * region_codes(win)
 
 
-def vgg_digests(steps: int = 10) -> dict:
-    wl = WL.VGG_CNN
+def train_digests(wl, steps: int, taps: bool) -> dict:
+    """Every tensor of `steps` training iterations of workload `wl`: per block the inner
+    activations and region codes, the block output and its codes (dropped outputs, when the
+    workload has dropout, read "saturated"), yhat, e and every weight gradient; with `taps` also
+    delta^fw and the gradient at every layer's pre-activation; the output layer's yhat, e and
+    weight gradient; every weight after the update."""
     dr = WL.draw_workload(wl, O.kaiming_bound, steps=steps)
-    hp = O.Hyper(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr, wl.alpha_inv, wl.n_classes)
+    hp = O.Hyper(wl.gamma_inv, wl.lambda_inv_fw, wl.lambda_inv_lr, wl.alpha_inv, wl.n_classes,
+                 d_lr=wl.d_lr, dropout_conv_ppm=wl.dropout_conv_ppm,
+                 dropout_lin_ppm=wl.dropout_lin_ppm, dropout_seed=wl.dropout_seed)
     net = O.OracleNet([(len(b.layers), b.maxpool, b.learning) for b in wl.blocks], wl.head,
                       dr.weights, hp)
     out = {"workload": wl.name, "batch": wl.batch, "rounding": "floor", "steps": []}
@@ -101,19 +110,34 @@ def vgg_digests(steps: int = 10) -> dict:
                 if j < J - 1:
                     put("b%d.act%d" % (b, j), ly.a, "int8")
                     put("b%d.code%d" % (b, j), region_codes(ly.zs), "uint8")
-                put("b%d.g%d" % (b, j), blk.g[j], "int32")
+                if taps:
+                    put("b%d.g%d" % (b, j), blk.g[j], "int32")
                 put("b%d.dw%d" % (b, j), blk.dw[j], "int64")
             put("b%d.out" % b, blk.out, "int8")
-            put("b%d.code%d" % (b, J - 1), pooled_codes(blk.layers[-1].zs, blk.pool_idx), "uint8")
+            pooled = blk.pool_idx is not None
+            code = (pooled_codes(blk.layers[-1].zs, blk.pool_idx) if pooled
+                    else region_codes(blk.layers[-1].zs))
+            if blk.keep is not None:
+                code = np.where(blk.keep, code, (code & 3) + 8 if pooled else 2)
+            put("b%d.code%d" % (b, J - 1), code, "uint8")
             put("b%d.yhat" % b, blk.yhat, "int32")
             put("b%d.e" % b, blk.e, "int32")
             put("b%d.dw_lr" % b, blk.dw_lr, "int64")
-            put("b%d.delta" % b, blk.delta_fw.reshape(blk.out.shape), "int32")
+            if taps:
+                put("b%d.delta" % b, blk.delta_fw.reshape(blk.f.shape), "int32")
+        if wl.head:
+            put("head.yhat", st.head_yhat, "int32")
+            put("head.e", st.head_e, "int32")
+            put("head.dw", st.head_dw, "int64")
         for k, w in enumerate(net.w):
             put("w%d" % k, w, "int32")
         out["steps"].append(rec)
-        print("vgg step %d: %.1f s" % (s, time.time() - t0), flush=True)
+        print("%s step %d: %.1f s" % (wl.name, s, time.time() - t0), flush=True)
     return out
+
+
+def vgg_digests(steps: int = 10) -> dict:
+    return train_digests(WL.VGG_CNN, steps, taps=True)
 
 
 def stress_digests(repeats: int = 20) -> dict:
@@ -151,6 +175,9 @@ def main():
         jobs.append(("digests_vgg_cnn_b256.json", vgg_digests))
     if which in ("stress", "all"):
         jobs.append(("digests_conv_stress.json", stress_digests))
+    if which in ("paper", "all"):
+        for wl in WL.PAPER_NETS:
+            jobs.append(("digests_%s.json" % wl.name, lambda wl=wl: train_digests(wl, 3, taps=False)))
     for name, fn in jobs:
         d = fn()
         with open(os.path.join(HERE, name), "w") as f:

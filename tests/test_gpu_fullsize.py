@@ -1,9 +1,10 @@
 """Parity at full size, in the configuration bench.py times: every tensor after every step.
 
-The oracle's results for the two benchmark-sized workloads are stored as per-step SHA-256 digests
-of every tensor (``tests/golden/make_digests.py``, which runs only the oracle): the VGG-style CNN
-at batch 256 over its ten training iterations, and the single 256 -> 256 conv layer on
-256x256x32x32 over its twenty repeats with IntegerSGD between them. Each GPU tensor is hashed in
+The oracle's results for the benchmark-sized workloads are stored as per-step SHA-256 digests of
+every tensor (``tests/golden/make_digests.py``, which runs only the oracle): the VGG-style CNN at
+batch 256 over its ten training iterations, the single 256 -> 256 conv layer on 256x256x32x32
+over its twenty repeats with IntegerSGD between them, and the paper's VGG8B, VGG11B, MLP 3 and
+MLP 4 at batch 64 over three iterations. Each GPU tensor is hashed in
 its storage dtype and must match; on a mismatch the stored sample values name the positions that
 differ.
 
@@ -185,3 +186,39 @@ def test_conv_stress_full_size_twenty_repeats(ctx):
         check(exp, "dw", st.dw, where)
         check(exp, "dx", st.dx, where)
         check(exp, "w", st.w, where)
+
+
+@pytest.mark.parametrize("name", [wl.name for wl in WL.PAPER_NETS])
+def test_paper_nets_full_batch_every_tensor(ctx, name):
+    """The paper's architectures at their batch of 64 (learning-layer pooling to 4096 features,
+    dropout where Tab. 6 sets it), three training iterations through nitro_train_step: every
+    tensor the iteration leaves in its workspace, the output layer's, and every weight."""
+    wl = WL.WORKLOADS[name]
+    dg = load_digests("digests_%s.json" % name)
+    assert dg["workload"] == wl.name and dg["batch"] == wl.batch
+    print("full-size case", wl.name, flush=True)
+    dr = WL.draw_workload(wl, runner.kaiming_bound, steps=len(dg["steps"]))
+    net = runner.GpuNet(wl, dr.weights, ctx=ctx)
+    for s, ((x, y), exp) in enumerate(zip(dr.batches, dg["steps"])):
+        print("step", s, flush=True)
+        net.step(dev(x), dev(y))
+        ctx.sync()
+        where = "step %d" % s
+        for b, blk in enumerate(wl.blocks):
+            v = net.view(b)
+            J = len(blk.layers)
+            for j in range(J):
+                if j < J - 1:
+                    check(exp, "b%d.act%d" % (b, j), v["act"][j], where)
+                check(exp, "b%d.code%d" % (b, j), v["code"][j], where)
+                check(exp, "b%d.dw%d" % (b, j), v["dw"][j], where)
+            check(exp, "b%d.out" % b, v["a_out"], where)
+            check(exp, "b%d.yhat" % b, v["yhat"], where)
+            check(exp, "b%d.e" % b, v["e"], where)
+            check(exp, "b%d.dw_lr" % b, v["dw_lr"], where)
+        hv = net.head_view()
+        check(exp, "head.yhat", hv["yhat"], where)
+        check(exp, "head.e", hv["e"], where)
+        check(exp, "head.dw", hv["dw"], where)
+        for k in range(len(net.w)):
+            check(exp, "w%d" % k, net.w[k], where)
