@@ -580,11 +580,12 @@ bool mul_ok(int64_t a, int64_t b, int64_t *out)
 // One IntegerSGD update as an entry of a batched launch (validation as sgd_impl). A full batch
 // is launched first: its entries' gradients are complete when later entries are added.
 nitro_status sgd_entry(nitro_ctx *ctx, SgdBatch &b, int32_t *w, const int64_t *dw, int64_t count,
-                       int64_t gamma_inv, int64_t lambda_inv, int64_t eta_override, int32_t round)
+                       int64_t gamma_inv, int64_t lambda_inv, int64_t eta_override, int32_t round,
+                       hipStream_t stream = nullptr)
 {
     if (!w || !dw || count < 0 || gamma_inv < 1 || lambda_inv < 0) return NITRO_EINVAL;
     if (b.n == SGD_MAX) {
-        launch_sgd_batch(ctx->stream, b);
+        launch_sgd_batch(stream ? stream : ctx->stream, b);
         b.n = 0;
     }
     int64_t eta = eta_override;
@@ -1125,8 +1126,9 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     DeviceGuard guard(ctx->device);
     TimerScope timer(ctx);
     // a captured iteration with timing clears its timing slots first (every replay measures
-    // afresh); every block's max slots cleared in one launch; every update applied in one
-    // launch at the end (blocks and the output layer share no weights)
+    // afresh); every block's max slots cleared in one launch; each block's updates enqueued
+    // behind its local training, the last block's and the output layer's at the end (blocks and
+    // the output layer share no weights)
     if (ctx->timing && ctx->tsbuf) {
         hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
         if (hipStreamIsCapturing(ctx->stream, &cs) == hipSuccess && cs == hipStreamCaptureStatusActive)
@@ -1161,6 +1163,23 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     };
     auto fail = [&](nitro_status e) -> nitro_status {
         (void)join_aux();
+        return e;
+    };
+    // IntegerSGD (Alg. 1) of block b's learning layer (gamma) and forward layers (AF gamma), on
+    // the stream of the block's local training, right after it: nothing later in the iteration
+    // reads these weights (the block's backward reads its packed limb planes, and no other
+    // block touches them)
+    auto block_sgd = [&](int b, hipStream_t bs) -> nitro_status {
+        const nitro_block_desc &d = net->block[b];
+        SgdBatch bb{};
+        bb.flags = ctx->flags;
+        nitro_status e = sgd_entry(ctx, bb, params->w_lr[b], (const int64_t *)at(workspace, g.dwlr[b]),
+                                   (int64_t)G * g.b[b].d, hp->gamma_inv, hp->lambda_inv_lr, eta_lr,
+                                   round, bs);
+        for (int j = 0; j < d.n_layers && e == NITRO_OK; j++)
+            e = sgd_entry(ctx, bb, params->w[b][j], (const int64_t *)at(workspace, g.dw[b][j]),
+                          weight_count(d.layer[j]), gamma_fw, hp->lambda_inv_fw, eta_fw, round, bs);
+        if (e == NITRO_OK) launch_sgd_batch(bs, bb);
         return e;
     };
     auto backward = [&](int b, hipStream_t bs) -> nitro_status {
@@ -1203,6 +1222,8 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
         }
         st = backward(b, bs);
         if (st != NITRO_OK) return fail(st);
+        st = block_sgd(b, bs);
+        if (st != NITRO_OK) return fail(st);
     }
     // 2. output layer: global gradient (its update comes with the others, step 4)
     const int n = net->block[0].n;
@@ -1219,13 +1240,15 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
     st = backward(net->n_blocks - 1, ctx->stream);
     if (st != NITRO_OK) return fail(st);
     if (!join_aux()) return NITRO_EHIP;
-    // 4. IntegerSGD (Alg. 1) of every weight tensor, after every gradient is complete
+    // 4. IntegerSGD (Alg. 1) of the output layer and of the last block (the other blocks' updates
+    // were enqueued behind their local training)
     if (net->head) {
         st = sgd_entry(ctx, sgd, params->w_head, hdw, (int64_t)G * g.hd, hp->gamma_inv,
                        hp->lambda_inv_lr, eta_lr, round);
         if (st != NITRO_OK) return st;
     }
-    for (int b = 0; b < net->n_blocks; b++) {
+    {
+        const int b = net->n_blocks - 1;
         const nitro_block_desc &d = net->block[b];
         st = sgd_entry(ctx, sgd, params->w_lr[b], (const int64_t *)at(workspace, g.dwlr[b]),
                        (int64_t)G * g.b[b].d, hp->gamma_inv, hp->lambda_inv_lr, eta_lr, round);
@@ -1236,7 +1259,6 @@ nitro_status nitro_train_step(nitro_ctx *ctx, const nitro_net_desc *net,
             if (st != NITRO_OK) return st;
         }
     }
-    // 4. IntegerSGD (Alg. 1) of every weight tensor
     launch_sgd_batch(ctx->stream, sgd);
     return hip_status();
 }
