@@ -347,6 +347,16 @@ nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
                                     const nitro_net_params *params, void *workspace,
                                     const int8_t *x, const int32_t *labels, const nitro_hparams *hp);
 
+/* The graph nitro_train_step_graph would replay for these arguments, captured and instantiated
+ * now if the context has none for their key, and not launched: nothing runs on the GPU and no
+ * weight changes. A training loop over several resident batches prepares each one's graph before
+ * its first iteration, so that no capture happens between replays. Same arguments, limits and
+ * errors as nitro_train_step_graph (preparing a 17th key replaces the least recently used). */
+nitro_status nitro_train_step_graph_prepare(nitro_ctx *ctx, const nitro_net_desc *net,
+                                            const nitro_net_params *params, void *workspace,
+                                            const int8_t *x, const int32_t *labels,
+                                            const nitro_hparams *hp);
+
 /* Device pointer, inside a workspace laid out by nitro_net_query, of block b's output a_b
  * (int8), so that callers can inspect the forward activations after nitro_train_step. */
 nitro_status nitro_net_block_output(const nitro_net_desc *net, void *workspace, int32_t b,

@@ -1313,9 +1313,12 @@ nitro_status nitro_net_infer(nitro_ctx *ctx, const nitro_net_desc *net,
     return hip_status();
 }
 
-nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
-                                    const nitro_net_params *params, void *workspace,
-                                    const int8_t *x, const int32_t *labels, const nitro_hparams *hp)
+// The graph of this key (descriptors, parameters, buffers, hyper-parameters, the context's
+// stream and settings): the one kept for it, or a new capture of one iteration.
+static nitro_status graph_for_key(nitro_ctx *ctx, const nitro_net_desc *net,
+                                  const nitro_net_params *params, void *workspace, const int8_t *x,
+                                  const int32_t *labels, const nitro_hparams *hp,
+                                  nitro_ctx::GraphEntry **out)
 {
     if (!ctx || !net || !params || !workspace || !x || !labels || !hp) return NITRO_EINVAL;
     if (!ctx->stream) return NITRO_EINVAL;           // the legacy default stream cannot capture
@@ -1369,8 +1372,29 @@ nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
         ctx->ts_graph = ctx->timing && ctx->tsbuf;
     }
     ge->last = ++ctx->gclock;
+    *out = ge;
+    return NITRO_OK;
+}
+
+nitro_status nitro_train_step_graph(nitro_ctx *ctx, const nitro_net_desc *net,
+                                    const nitro_net_params *params, void *workspace,
+                                    const int8_t *x, const int32_t *labels, const nitro_hparams *hp)
+{
+    nitro_ctx::GraphEntry *ge = nullptr;
+    const nitro_status st = graph_for_key(ctx, net, params, workspace, x, labels, hp, &ge);
+    if (st != NITRO_OK) return st;
+    DeviceGuard guard(ctx->device);
     if (hipGraphLaunch(ge->exec, ctx->stream) != hipSuccess) return NITRO_EHIP;
     return NITRO_OK;
+}
+
+nitro_status nitro_train_step_graph_prepare(nitro_ctx *ctx, const nitro_net_desc *net,
+                                            const nitro_net_params *params, void *workspace,
+                                            const int8_t *x, const int32_t *labels,
+                                            const nitro_hparams *hp)
+{
+    nitro_ctx::GraphEntry *ge = nullptr;
+    return graph_for_key(ctx, net, params, workspace, x, labels, hp, &ge);
 }
 
 nitro_status nitro_kernel_timing(nitro_ctx *ctx, int32_t enable)

@@ -117,6 +117,7 @@ def _load():
         "nitro_net_block_output": (I32, [P(NetDesc), VP, I32, P(VP)]),
         "nitro_train_step": (I32, [VP, P(NetDesc), P(NetParams), VP, VP, VP, P(HParams)]),
         "nitro_train_step_graph": (I32, [VP, P(NetDesc), P(NetParams), VP, VP, VP, P(HParams)]),
+        "nitro_train_step_graph_prepare": (I32, [VP, P(NetDesc), P(NetParams), VP, VP, VP, P(HParams)]),
         "nitro_net_infer": (I32, [VP, P(NetDesc), P(NetParams), VP, VP, VP, VP]),
         "nitro_host_div": (I64, [I64, I64, I32]),
         "nitro_host_relu_mu": (I32, [I32, I32]),
@@ -144,7 +145,8 @@ EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_set_conv_
            "nitro_head_backward", "nitro_integer_sgd_step", "nitro_block_sgd_step",
            "nitro_net_block_view", "nitro_net_head_view", "nitro_net_query",
            "nitro_preprocess_query", "nitro_preprocess",
-           "nitro_net_block_output", "nitro_train_step", "nitro_train_step_graph", "nitro_net_infer",
+           "nitro_net_block_output", "nitro_train_step", "nitro_train_step_graph",
+           "nitro_train_step_graph_prepare", "nitro_net_infer",
            "nitro_host_div", "nitro_host_relu_mu", "nitro_host_kaiming_bound",
            "nitro_kernel_timing", "nitro_kernel_time", "nitro_mfma_rate")
 
@@ -378,6 +380,12 @@ class Context:
         check(LIB.nitro_train_step_graph(self.h, ctypes.byref(nd), ctypes.byref(params),
                                          _p(workspace), _p(x), _p(labels), ctypes.byref(hp)),
               "nitro_train_step_graph")
+
+    def train_step_graph_prepare(self, nd: NetDesc, params: NetParams, workspace, x, labels,
+                                 hp: HParams) -> None:
+        check(LIB.nitro_train_step_graph_prepare(self.h, ctypes.byref(nd), ctypes.byref(params),
+                                                 _p(workspace), _p(x), _p(labels), ctypes.byref(hp)),
+              "nitro_train_step_graph_prepare")
 
     def net_infer(self, nd: NetDesc, params: NetParams, workspace, x, yhat, pred) -> None:
         check(LIB.nitro_net_infer(self.h, ctypes.byref(nd), ctypes.byref(params), _p(workspace),

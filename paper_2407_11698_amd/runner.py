@@ -46,7 +46,19 @@ class GpuNet:
         self.ctx = ctx or N.Context(device)
         self.descs = block_descs(wl, round_mode)
         self.nd = N.net_desc(self.descs, wl.head)
-        self.w = [_dev(w, self.dev) for w in weights]
+        # every weight a view of one flat int32 buffer (each at a multiple of 64 elements), so that
+        # a caller can save or restore all of them with one copy
+        sizes = [int(np.prod(np.shape(w))) for w in weights]
+        offs, o = [], 0
+        for n in sizes:
+            offs.append(o)
+            o += (n + 63) // 64 * 64
+        self.w_flat = torch.zeros(o, dtype=torch.int32, device=self.dev)
+        self.w = []
+        for w, off, n in zip(weights, offs, sizes):
+            t = self.w_flat[off:off + n].view(np.shape(w))
+            t.copy_(_dev(np.asarray(w, dtype=np.int32), self.dev))
+            self.w.append(t)
         self.params = N.NetParams()
         k = 0
         for b, blk in enumerate(wl.blocks):
@@ -79,6 +91,12 @@ class GpuNet:
             return self.step(x, y)
         self.ctx.train_step_graph(self.nd, self.params, self.workspace, x, y, self.hp)
         self.steps += 1
+
+    def prepare_graph(self, x: torch.Tensor, y: torch.Tensor) -> None:
+        """Capture (without running) the graph step_graph replays for these buffers."""
+        if self.wl.dropout_conv_ppm or self.wl.dropout_lin_ppm:
+            return
+        self.ctx.train_step_graph_prepare(self.nd, self.params, self.workspace, x, y, self.hp)
 
     def infer(self, x: torch.Tensor):
         """Inference with the current weights: (yhat [n][G] int32, predicted class [n] int32)."""

@@ -543,7 +543,7 @@ def test_train_step_aux_streams(ctx, naux):
         assert np.array_equal(a, b)
 
 
-@pytest.mark.parametrize("feed", ["copy", "resident"])
+@pytest.mark.parametrize("feed", ["copy", "resident", "prepared"])
 @pytest.mark.parametrize("wl,nbuf", [(WL.scaled(WL.SMALL_CNN, 16), 18), (WL.scaled(WL.VGG_CNN, 8), 4)],
                          ids=["small_cnn_b16", "vgg_b8"])
 def test_train_step_graph_matches_eager(wl, nbuf, feed):
@@ -552,7 +552,8 @@ def test_train_step_graph_matches_eager(wl, nbuf, feed):
     the oracle-parity tests pin. The batch changes by writing into the captured buffers (copy),
     or by passing one of nbuf resident buffer sets, each replayed from a graph of its own
     (resident; on the small network more sets than the context keeps graphs for, so that graphs
-    are replaced and captured again)."""
+    are replaced and captured again), or so with every set's graph prepared first
+    (nitro_train_step_graph_prepare, which must leave the weights untouched)."""
     import torch
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
@@ -565,12 +566,20 @@ def test_train_step_graph_matches_eager(wl, nbuf, feed):
         yb = torch.empty_like(dev(dr.batches[0][1]))
         bufs = [(dev(dr.batches[k % 4][0]), dev(dr.batches[k % 4][1])) for k in range(nbuf)]
         steps = 8 if feed == "copy" else 2 * nbuf
+        if feed == "prepared":
+            w_init = graph.weights_np()
+            for xd, yd in bufs:
+                graph.prepare_graph(xd, yd)
+            torch.cuda.synchronize()
+            gctx.sync()
+            for a, b in zip(w_init, graph.weights_np()):
+                assert np.array_equal(a, b), "preparing a graph changed the weights"
         for s in range(steps):
-            k = s % nbuf if feed == "resident" else s % 4
+            k = s % nbuf if feed != "copy" else s % 4
             print("graph replay", wl.name, feed, "step", s, "batch", k % 4, flush=True)
-            xd, yd = bufs[k] if feed == "resident" else (dev(dr.batches[k][0]), dev(dr.batches[k][1]))
+            xd, yd = bufs[k] if feed != "copy" else (dev(dr.batches[k][0]), dev(dr.batches[k][1]))
             eager.step(xd, yd)
-            if feed == "resident":
+            if feed != "copy":
                 graph.step_graph(xd, yd)
             else:
                 xb.copy_(xd)
