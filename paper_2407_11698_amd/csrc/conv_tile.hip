@@ -461,6 +461,23 @@ void k_conv_tile(TileArgs p)
                 stage_load(0);
             }
         }
+        // (input gradient: the previous layer's region codes of this thread's outputs, requested
+        // all at once before the epilogue; read one by one between its stores, each read would
+        // wait for the memory in turn)
+        uint32_t cdv[MODE == IG_DX ? TM : 1][MODE == IG_DX ? TN : 1];
+        if (MODE == IG_DX && p.prev_code) {
+            const int pxp = (tid >> 7) * 64 + (tid & 15);
+            const int cbp = ((tid >> 6) & 1) * 32 + 4 * ((tid >> 4) & 3);
+#pragma unroll
+            for (int i = 0; i < TM; i++)
+#pragma unroll
+                for (int j = 0; j < TN; j++) {
+                    const int64_t m = em0 + pxp + 16 * i;
+                    const int col = en0 + cbp + 16 * j;
+                    cdv[MODE == IG_DX ? i : 0][MODE == IG_DX ? j : 0] =
+                        m < M && col < p.no ? *(const uint32_t *)(p.prev_code + m * p.no + col) : 0u;
+                }
+        }
         __syncthreads();                          // the epilogue reuses the stages' LDS
         // ------------------------------------------------------------ epilogues
         // The MFMAs took B as the first operand: lane l of tile (i, j) holds output channels
@@ -619,7 +636,7 @@ void k_conv_tile(TileArgs p)
                         const int64_t o = m * p.no + col;
                         v4i g = acc[i][j];
                         if (p.prev_code) {
-                            const uint32_t cd = *(const uint32_t *)(p.prev_code + o);
+                            const uint32_t cd = cdv[MODE == IG_DX ? i : 0][MODE == IG_DX ? j : 0];
 #pragma unroll
                             for (int t = 0; t < 4; t++)
                                 g[t] = relu_bwd32<TR>(g[t], (cd >> (8 * t)) & 0xffu, p.rp);
