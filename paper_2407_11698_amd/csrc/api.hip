@@ -218,6 +218,7 @@ struct BlockGeom {
     size_t lwf, lwt, lft, lpart, lepad, let;   // its scratch
     size_t lf, lfc;                // learning-pooled block output and its window indices
     size_t yhat, e, delta, g0, g1;
+    size_t g16;                    // an inner layer's gradient in the escaped 16-bit form
     size_t total;
 };
 
@@ -342,6 +343,7 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     g->delta = off; off = align256(off + (size_t)(G > 0 ? g->out_elems : 0) * 4);
     g->g0 = off;    off = align256(off + (size_t)gmax * 4);
     g->g1 = off;    off = align256(off + (size_t)(g->J > 1 ? gmax : 0) * 4);
+    g->g16 = off;   off = align256(off + (size_t)(g->J > 1 ? gmax : 0) * 2);
     g->total = off;
     return NITRO_OK;
 }
@@ -515,6 +517,9 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         launch_unpool_relu_bwd(s, n, LJ.sh.h, LJ.sh.w, LJ.sh.co, desc->maxpool != 0, delta,
                                at(state, g.code[J - 1]), rp, gb[0], slots + (4 + J - 1) * SLOT_WORDS, ctx->flags);
     int cur = 0;
+    // g_j in the escaped 16-bit form (int16 at g16, the escapes in gb[cur]) when the layer above
+    // wrote it so
+    const int16_t *gj16 = nullptr;
     for (int j = J - 1; j >= 0; j--) {
         const LayerGeom &L = g.L[j];
         const int8_t *xin = j == 0 ? x : (const int8_t *)at(state, g.act[j - 1]);
@@ -527,7 +532,8 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                                       L.dx_tile && need_dx ? (int8_t *)at(state, g.gnl) : nullptr,
                                       (int64_t *)at(state, g.part), gr->dw[j], ctx->flags,
                                       j == J - 1 && rows_from_forward(g),
-                                      j == J - 1 && g_pooled ? at(state, g.code[J - 1]) : nullptr);
+                                      j == J - 1 && g_pooled ? at(state, g.code[J - 1]) : nullptr,
+                                      gj16);
             else if (mfma_conv_dw_ok(L.sh) || mfma_conv_dw_smallc_ok(L.sh))
                 launch_conv_dw_mfma(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, xin, (int8_t *)at(state, g.gt),
                                     (int64_t *)at(state, g.part), gr->dw[j], ctx->flags);
@@ -549,6 +555,16 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         } else if (taps && taps->dx) {
             dst64 = taps->dx;
         }
+        int16_t *dst16 = nullptr;
+        if (dst && L.conv && L.dx_tile) {
+            // g_{j-1} in 16 bits (with escapes) where its only reader is the weight-gradient
+            // preparation of layer j-1: no tap of it, the planes weight gradient, and that
+            // layer's own input gradient (if any) on the tile, which reads the prepared planes
+            const LayerGeom &Lp = g.L[j - 1];
+            const bool need_dx_prev = j - 1 > 0 || (taps && taps->dx);
+            if (Lp.conv && dwp_ok(Lp.sh) && (!need_dx_prev || Lp.dx_tile) && !(taps && taps->g[j - 1]))
+                dst16 = (int16_t *)at(state, g.g16);
+        }
         if (dst || dst64) {
             uint32_t *gmax_out = j > 0 ? slots + (4 + j - 1) * SLOT_WORDS : nullptr;
             if (L.conv) {
@@ -556,7 +572,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                     launch_conv_dx_tile(s, ctx->conv_tile, ctx->conv_persist, L.sh, (const int8_t *)at(state, g.gnl),
                                         slots + (4 + j) * SLOT_WORDS,
                                         (const int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS,
-                                        code, rp, dst, dst64, gmax_out, ctx->flags);
+                                        code, rp, dst, dst64, gmax_out, ctx->flags, dst16);
                 else if (mfma_conv_dx_ok(L.sh))
                     launch_conv_dx_mfma(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, (const int8_t *)at(state, g.wt[j]),
                                         slots + (j) * SLOT_WORDS, code, rp, dst, dst64, gmax_out, ctx->flags);
@@ -567,6 +583,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                                  ctx->flags);
             }
         }
+        gj16 = dst16;
         cur ^= 1;
     }
     return hip_status();

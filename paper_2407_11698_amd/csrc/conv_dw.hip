@@ -171,7 +171,8 @@ __device__ void dwp_pad_rows(int n, int h, int w, int hp, int wp, int64_t kraw, 
 // [n][h/2][w/2][C]: pixel (y, x) takes it where the pool's argmax (the code's low 2 bits) is
 // window position 2 (y & 1) + (x & 1), and zero elsewhere. Workgroup (bx, by): positions
 // 64 bx .., channels 64 by ...
-__device__ void dwp_grad_planes(const int32_t *__restrict__ g, int n, int h, int w, int c, int hp,
+__device__ void dwp_grad_planes(const int32_t *__restrict__ g, const int16_t *__restrict__ g16,
+                                int n, int h, int w, int c, int hp,
                                 int wp, int kp, const uint32_t *gmax,
                                 const uint8_t *__restrict__ pcode, int8_t *__restrict__ gp,
                                 int8_t *__restrict__ gn, int bx, int by)
@@ -199,7 +200,17 @@ __device__ void dwp_grad_planes(const int32_t *__restrict__ g, int n, int h, int
             const int ch = c0 + 16 * cq + 4 * u;
             v4i x = v4i{0, 0, 0, 0};
             if (pix >= 0 && ch < c) {
-                x = *(const v4i *)(g + (int64_t)src * c + ch);
+                if (g16) {
+                    // the escaped 16-bit form: an escape's value is in g at the same index
+                    const v2i hv = *(const v2i *)(g16 + (int64_t)src * c + ch);
+#pragma unroll
+                    for (int e = 0; e < 4; e++) {
+                        const int16_t v = (int16_t)((uint32_t)hv[e >> 1] >> (16 * (e & 1)));
+                        x[e] = v == G16_ESC ? g[(int64_t)src * c + ch + e] : (int32_t)v;
+                    }
+                } else {
+                    x = *(const v4i *)(g + (int64_t)src * c + ch);
+                }
                 if (pcode) {
                     const uint32_t cd = *(const uint32_t *)(pcode + (int64_t)src * c + ch);
 #pragma unroll
@@ -260,6 +271,7 @@ struct DwpPrep {
     int64_t kraw, xs;
     int8_t *xr;
     const int32_t *g;
+    const int16_t *g16;          // optional: g in the escaped 16-bit form (g: the escapes)
     const uint32_t *gmax;
     const uint8_t *pcode;
     int8_t *gp, *gn;
@@ -276,7 +288,7 @@ __global__ __launch_bounds__(256) void k_dwp_prep(DwpPrep a)
         return;
     }
     const int q = b - nrows;
-    dwp_grad_planes(a.g, a.n, a.h, a.w, a.co, a.hp, a.wp, a.kp, a.gmax, a.pcode, a.gp, a.gn,
+    dwp_grad_planes(a.g, a.g16, a.n, a.h, a.w, a.co, a.hp, a.wp, a.kp, a.gmax, a.pcode, a.gp, a.gn,
                     q % a.gp_gx, q / a.gp_gx);
 }
 
@@ -294,8 +306,6 @@ struct DwpArgs {
     uint32_t *flags;
     uint64_t *ts;          // timing slot (null: untimed)
 };
-
-typedef int v2i __attribute__((ext_vector_type(2)));
 
 // Transposing LDS read (gfx950 ds_read_b64_tr_b8). Within each group of 16 lanes, output lane
 // 8 h + j receives, as its byte b (b = 0..7), byte j of the 8 bytes addressed by lane 2 b + h.
@@ -517,7 +527,7 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
                            int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags,
-                           bool x_rows_ready, const uint8_t *pool_code)
+                           bool x_rows_ready, const uint8_t *pool_code, const int16_t *g16)
 {
     const DwpGeom ge = dwp_geom(sh);
     const DwpPlan pl = dwp_plan(sh);
@@ -531,7 +541,7 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
         pa.gp_gx = (int)(ge.kp / 64);
         pa.x = x; pa.n = sh.n; pa.h = sh.h; pa.w = sh.w; pa.c = sh.c; pa.co = sh.co;
         pa.hp = ge.hp; pa.wp = ge.wp; pa.kp = (int)ge.kp; pa.kraw = ge.kraw; pa.xs = ge.xs; pa.xr = xp;
-        pa.g = g; pa.gmax = gmax; pa.pcode = pool_code; pa.gp = gp; pa.gn = gn;
+        pa.g = g; pa.g16 = g16; pa.gmax = gmax; pa.pcode = pool_code; pa.gp = gp; pa.gn = gn;
         const int64_t nwg = (int64_t)pa.rows_gx * pa.rows_gy + (int64_t)pa.gp_gx * ((sh.co + 63) / 64);
         hipLaunchKernelGGL(k_dwp_prep, dim3((unsigned)nwg), dim3(256), 0, s, pa);
     }

@@ -85,6 +85,7 @@ struct TileArgs {
     const uint8_t *prev_code;
     Relu rp;
     int32_t *gout;
+    int16_t *gout16;               // optional: g in the escaped 16-bit form (gout: escapes only)
     int64_t *out64;
     uint32_t *gmax;
     uint32_t *flags;
@@ -646,7 +647,18 @@ void k_conv_tile(TileArgs p)
                             const uint32_t ag = abs_u32(g[t]);
                             mx = ag > mx ? ag : mx;
                         }
-                        *(v4i *)(p.gout + o) = g;
+                        if (p.gout16) {
+                            uint32_t h[4];
+#pragma unroll
+                            for (int t = 0; t < 4; t++) {
+                                const bool esc = g[t] < -G16_MAX || g[t] > G16_MAX;
+                                if (esc) p.gout[o + t] = g[t];
+                                h[t] = (uint32_t)(uint16_t)(esc ? G16_ESC : (int16_t)g[t]);
+                            }
+                            *(v2i *)(p.gout16 + o) = v2i{(int)(h[0] | (h[1] << 16)), (int)(h[2] | (h[3] << 16))};
+                        } else {
+                            *(v4i *)(p.gout + o) = g;
+                        }
                     }
             };
             if (p.rp.alpha.trunc) emit(std::true_type{});
@@ -802,7 +814,7 @@ void launch_conv_fwd_tile(hipStream_t s, int tile, int persist, const ConvShape 
 void launch_conv_dx_tile(hipStream_t s, int tile, int persist, const ConvShape &sh, const int8_t *gl,
                          const uint32_t *gmax_in, const int8_t *wt, const uint32_t *wmax,
                          const uint8_t *prev_code, const Relu &rp, int32_t *gout, int64_t *out64,
-                         uint32_t *gmax_out, uint32_t *flags)
+                         uint32_t *gmax_out, uint32_t *flags, int16_t *gout16)
 {
     TileArgs a{};
     a.n = sh.n; a.h = sh.h; a.w = sh.w;
@@ -811,6 +823,7 @@ void launch_conv_dx_tile(hipStream_t s, int tile, int persist, const ConvShape &
     a.b = wt; a.bplane = (int64_t)sh.c * 9 * sh.co; a.b_max = wmax;
     a.rp = rp;
     a.prev_code = prev_code; a.gout = gout; a.out64 = out64; a.gmax = gmax_out;
+    a.gout16 = gout ? gout16 : nullptr;
     a.flags = flags;
     if (use_wide_tile(tile, sh.n, sh.h, sh.w, sh.c, false)) launch_tile<IG_DX, 4>(s, persist, a);
     else launch_tile<IG_DX, 2>(s, persist, a);

@@ -7,6 +7,7 @@
 namespace nitro {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 
 __host__ __device__ inline int limbs_for(uint32_t m)
 {

@@ -593,10 +593,12 @@ constexpr int DWP_HMAX = 64;
 int64_t dwp_rows_stride(const ConvShape &sh);   // xs
 // pool_code (a pooled layer's codes, [n][h/2][w/2][co]): g is given at the pooled positions only
 // (launch_learning_mfma with g_pooled) and each window's argmax takes the value
+// g16: g in the escaped 16-bit form (g then holds the escaped values only).
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
                            int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags,
-                           bool x_rows_ready = false, const uint8_t *pool_code = nullptr);
+                           bool x_rows_ready = false, const uint8_t *pool_code = nullptr,
+                           const int16_t *g16 = nullptr);
 
 // ---- implicit-GEMM conv with the input tile staged once (conv_tile.hip)
 bool tile_conv_fwd_ok(const ConvShape &sh, bool pool, int64_t sf, int alpha_inv);
@@ -609,11 +611,19 @@ void launch_conv_fwd_tile(hipStream_t s, int tile, int persist, const ConvShape 
                           const uint32_t *wmax, int64_t sf, int alpha_inv, int round,
                           const Relu &rp, bool pool, int8_t *out, uint8_t *code, uint32_t *flags,
                           int8_t *xr = nullptr, int64_t xs = 0);
-// gl: g's NHWC limb planes [LA][P][co] (max|g| in gmax_in); otherwise as launch_conv_dx_mfma
+// gl: g's NHWC limb planes [LA][P][co] (max|g| in gmax_in); otherwise as launch_conv_dx_mfma.
+// gout16 (with gout): the result in the escaped 16-bit form below instead of int32 (gout then
+// receives only the escaped values).
 void launch_conv_dx_tile(hipStream_t s, int tile, int persist, const ConvShape &sh, const int8_t *gl,
                          const uint32_t *gmax_in, const int8_t *wt, const uint32_t *wmax,
                          const uint8_t *prev_code, const Relu &rp, int32_t *gout, int64_t *out64,
-                         uint32_t *gmax_out, uint32_t *flags);
+                         uint32_t *gmax_out, uint32_t *flags, int16_t *gout16 = nullptr);
+
+// A gradient stored in 16 bits with an escape: g16[i] = g[i] where |g[i]| <= G16_MAX, else
+// G16_ESC, and then the int32 array beside it holds g[i] at the same index (written, and read,
+// only there).
+constexpr int32_t G16_MAX = 32767;
+constexpr int16_t G16_ESC = -32768;
 void launch_conv_dx_mfma(hipStream_t s, const ConvShape &sh, const int32_t *g, const uint32_t *gmax_in,
                          const int8_t *wt, const uint32_t *wmax, const uint8_t *prev_code,
                          const Relu &rp, int32_t *gout, int64_t *out64, uint32_t *gmax_out,

@@ -39,9 +39,11 @@ def rand(rng, shape, lo, hi, dtype):
 
 
 def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dmax=1 << 15,
-              conv=True, tap_last_g=True, d_lr=0):
+              conv=True, tap_last_g=True, d_lr=0, tap_inner_g=True):
     """One nitro_block_forward + nitro_block_backward against the oracle's block functions.
-    tap_last_g=False leaves the last layer's g untapped (the library may then keep it pooled)."""
+    tap_last_g=False leaves the last layer's g untapped (the library may then keep it pooled);
+    tap_inner_g=False the other layers' (the library may then keep them in 16 bits with escapes).
+    Returns the oracle's record."""
     print("block case", dict(n=n, h=h, w=w, chans=chans, pool=maxpool, G=G, alpha=alpha,
                              mode=nm, wmax=wmax, conv=conv), flush=True)
     J = len(chans) - 1
@@ -97,7 +99,8 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
     dws = [torch.empty(a.shape, dtype=torch.int64, device=DEV) for a in ws]
     dw_lr = torch.empty((G, d), dtype=torch.int64, device=DEV) if G else None
     taps = {"g": [torch.empty(l.zs.shape, dtype=torch.int32, device=DEV)
-                  if tap_last_g or j < J - 1 else None for j, l in enumerate(rec.layers)],
+                  if (tap_last_g if j == J - 1 else tap_inner_g) else None
+                  for j, l in enumerate(rec.layers)],
             "dx": torch.empty(x.shape, dtype=torch.int64, device=DEV) if want_dx else None}
     if G:
         taps["yhat"] = torch.empty((n, G), dtype=torch.int32, device=DEV)
@@ -108,7 +111,7 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
                        taps)
     if expect_overflow:
         assert ctx.sync_status() == N.EOVERFLOW
-        return
+        return rec
     ctx.sync()
     assert np.array_equal(host(a_out), rec.out), "block output"
     if G:
@@ -122,6 +125,7 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
         assert np.array_equal(host(dws[j]), rec.dw[j]), "dW layer %d" % j
     if want_dx:
         assert np.array_equal(host(taps["dx"]), rec.dx), "dx"
+    return rec
 
 
 CONV_CASES = [
@@ -243,6 +247,35 @@ def test_conv_block_wide_weight_gradient(ctx, case):
     n, h, w, chans, pool, dmax = case
     rng = np.random.default_rng(hash((n, h, w, tuple(chans), dmax, 4242)) % (1 << 31))
     run_block(ctx, rng, n, h, w, chans, pool, 0, 10, N.ROUND_FLOOR, O.FLOOR, dmax=dmax)
+
+
+# blocks whose inner layers' gradients are not tapped, on the tiled input gradient and the planes
+# weight gradient: g_{j-1} is then kept in 16 bits with escapes for |g| > 32767 (the last flag:
+# whether the oracle's inner gradients have such values, checked); the four-layer case passes the
+# 16-bit form down twice
+G16_CASES = [
+    # n, h, w, chans, pool, G, alpha, wmax, dmax, escapes
+    (1, 32, 32, [3, 64, 64], True, 100, 10, 2, 0, False),
+    (3, 16, 16, [32, 64, 64], True, 10, 10, 3, 0, False),
+    (2, 8, 8, [64, 128, 128], True, 100, 16, 4, 0, False),
+    (3, 16, 16, [32, 64, 64], True, 10, 10, 300, 0, True),
+    (2, 16, 16, [64, 64, 64], False, 0, 10, 1, 300, False),
+    (2, 16, 16, [64, 64, 64], False, 0, 10, 2, 1000, True),
+    (2, 16, 16, [64, 64, 64], False, 0, 10, 3, 3000, True),
+    (2, 16, 16, [64, 64, 64, 64], False, 0, 10, 1, 16, False),
+    (2, 16, 16, [64, 64, 64, 64], False, 0, 10, 2, 1000, True),
+]
+
+
+@pytest.mark.parametrize("case", G16_CASES)
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_conv_block_inner_g16(ctx, case, modes):
+    n, h, w, chans, pool, G, alpha, wmax, dmax, escapes = case
+    rng = np.random.default_rng(hash((n, h, w, tuple(chans), G, wmax, 16)) % (1 << 31))
+    rec = run_block(ctx, rng, n, h, w, chans, pool, G, alpha, modes[0], modes[1], wmax=wmax,
+                    tap_inner_g=False, dmax=max(dmax, 1))
+    inner = [np.abs(np.asarray(g, dtype=np.int64)).max() for g in rec.g[:-1]]
+    assert (max(inner) > 32767) == escapes, inner
 
 
 @pytest.mark.parametrize("chans,G,wmax", [([784, 100], 10, 7), ([100, 50, 30], 10, 300),
