@@ -1378,11 +1378,17 @@ static nitro_status graph_for_key(nitro_ctx *ctx, const nitro_net_desc *net,
         hipGraph_t graph = nullptr;
         const hipError_t e = hipStreamEndCapture(ctx->stream, &graph);
         if (st == NITRO_OK && e != hipSuccess) st = NITRO_EHIP;
+        // every auxiliary stream that joined the capture must have left it with the capturing
+        // stream: one still capturing was forked and not joined back, and its graph is unusable
+        for (int a = 0; a < nitro_ctx::NAUX; a++)
+            if (ctx->aux[a] && nitro_ctx::capturing(ctx->aux[a])) st = NITRO_EHIP;
         if (st == NITRO_OK && hipGraphInstantiate(&ge->exec, graph, nullptr, nullptr, 0) != hipSuccess) {
             ge->exec = nullptr;
             st = NITRO_EHIP;
         }
-        if (graph) (void)hipGraphDestroy(graph);
+        // (a graph is handed out only by a capture that ended well; after a failed end the
+        // pointer is not one to release)
+        if (graph && e == hipSuccess) (void)hipGraphDestroy(graph);
         (void)hipGetLastError();
         if (st != NITRO_OK) return st;
         ge->key = std::move(key);
