@@ -308,38 +308,43 @@ __global__ void k_pack_learning_weights(const int32_t *__restrict__ w, uint32_t 
     block_slot_max(wmax, m);
 }
 
-// f [n][d] int8 -> fT [d][np] (zero columns n >= N): 64 x 64 tiles through LDS, tile (bx, by)
-// = features 64 bx .., samples 64 by ...
+// f [n][d] int8 -> fT [d][np] (zero columns n >= N), tile (bx, by) = features 64 bx ..,
+// samples 64 by ..: each thread transposes one 4 x 4 byte block in registers (four dword loads
+// of 4 samples' 4 features, byte permutes, four dword stores of 4 features' 4 samples; d and np
+// are multiples of 16).
 __device__ void transpose_i8_tile(const int8_t *__restrict__ f, int N, int d, int np,
                                   int8_t *__restrict__ ft, int bx, int by)
 {
-    __shared__ int8_t t[64][65];
-    const int n0 = by * 64, k0 = bx * 64;
-    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-        const int r = e / 64, c = e % 64;                 // r: sample, c: feature
-        t[r][c] = (n0 + r < N && k0 + c < d) ? f[(int64_t)(n0 + r) * d + k0 + c] : 0;
-    }
-    __syncthreads();
-    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-        const int r = e / 64, c = e % 64;                 // r: feature, c: sample
-        if (k0 + r < d && n0 + c < np) ft[(int64_t)(k0 + r) * np + n0 + c] = t[c][r];
-    }
+    const int t = threadIdx.x;
+    const int r0 = by * 64 + 4 * (t >> 4);             // first of the block's 4 samples
+    const int c0 = bx * 64 + 4 * (t & 15);             // first of its 4 features
+    if (c0 >= d || r0 >= np) return;
+    uint32_t a[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+        a[i] = r0 + i < N ? *(const uint32_t *)(f + (int64_t)(r0 + i) * d + c0) : 0u;
+    uint32_t o[4];
+    transpose4x4(a[0], a[1], a[2], a[3], o[0], o[1], o[2], o[3]);
+#pragma unroll
+    for (int j = 0; j < 4; j++) *(uint32_t *)(ft + (int64_t)(c0 + j) * np + r0) = o[j];
 }
 
-// Forward of the learning layer in one launch: workgroups 0 .. tgx tgy - 1 transpose f (for the
-// weight gradient), the rest compute the split-K partial tiles (x fastest, then y, then split).
+// Forward of the learning layer in one launch: workgroups 0 .. ngemm - 1 compute the split-K
+// partial tiles (x fastest, then y, then split), the rest transpose f (for the weight gradient);
+// the tiles come first, so that their longer chains start before the short transposes.
 __global__ __launch_bounds__(256) void k_lgemm_fwd(LgemmArgs p, const int8_t *f, int N, int d, int np,
                                                    int8_t *ft, int tgx, int tgy)
 {
     __shared__ __attribute__((aligned(16))) uint8_t smem[LG_SMEM];
     const int b = blockIdx.x;
-    if (b < tgx * tgy) {
-        transpose_i8_tile(f, N, d, np, ft, b % tgx, b / tgx);
+    const int gx = (p.M + LG_BM - 1) / LG_BM, gy = (p.N + LG_BN - 1) / LG_BN;
+    const int ngemm = (int)gridDim.x - tgx * tgy;
+    if (b < ngemm) {
+        lgemm_tile<LIN_PART>(p, smem, b % gx, (b / gx) % gy, b / (gx * gy));
         return;
     }
-    const int q = b - tgx * tgy;
-    const int gx = (p.M + LG_BM - 1) / LG_BM, gy = (p.N + LG_BN - 1) / LG_BN;
-    lgemm_tile<LIN_PART>(p, smem, q % gx, (q / gx) % gy, q / (gx * gy));
+    const int q = b - ngemm;
+    transpose_i8_tile(f, N, d, np, ft, q % tgx, q / tgx);
 }
 
 // Backward of the learning layer in one launch (both read e only): workgroups 0 .. ndw - 1 the

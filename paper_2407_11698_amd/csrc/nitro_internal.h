@@ -324,12 +324,11 @@ __device__ inline bool fits_i32(int64_t v) { return v >= INT32_MIN && v <= INT32
 
 __device__ inline void raise_flag(uint32_t *flags, uint32_t f) { atomicOr(flags, f); }
 
-// Running maximum in a device slot. The plain read first skips the atomic whenever the slot
-// already holds a value at least as large (a stale read only costs an extra atomic).
+// Running maximum in a device slot: one atomic max, its result unused (a workgroup's last act:
+// reading the slot first to skip the atomic costs the workgroup a memory round trip).
 __device__ inline void slot_max(uint32_t *slot, uint32_t m)
 {
-    if (m && m > __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-        atomicMax(slot, m);
+    if (m) atomicMax(slot, m);
 }
 
 __device__ inline uint32_t wave_max_u32(uint32_t v)
