@@ -470,41 +470,45 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 #pragma unroll
                 for (int i = 0; i < 4; i++) acc[t][i] = v4i{0, 0, 0, 0};
         }
-        // sum of the four waves (int64), each weighted 256^limb: straight into this split's
-        // tile, or (L3) into this thread's 36 values (3-tap group t0 / 3, element e = tid + 256 k
-        // of the group's 3 x 64 x 16), stored after the last pass
+        // Sum of the four waves (int64), each weighted 256^limb: straight into this split's
+        // tile, or (L3) into this thread's 36 values, stored after the last pass. Per 3-tap
+        // group, every lane stores its accumulators whole (16 bytes: output channels
+        // 16 i + 4 g4 .. + 3 of input channel j) at [wave][tap][i][g4][j][r]; then each thread
+        // takes such a run of 4 output channels for the 4 waves (16-byte reads) and adds them:
+        // run m of the thread is group q = tid + 256 m = (tap, i, g4, j).
         __syncthreads();
-        int32_t *red = (int32_t *)lds;        // [wave][3 taps][64 co][16 ci]
+        int32_t *red = (int32_t *)lds;        // [wave][3 taps][4 i][4 g4][16 j][4 r]
 #pragma unroll
         for (int t0 = 0; t0 < 9; t0 += 3) {
 #pragma unroll
             for (int tt = 0; tt < 3; tt++)
 #pragma unroll
                 for (int i = 0; i < 4; i++)
+                    *(v4i *)(red + (wave * 3 + tt) * 1024 + (i * 4 + g4) * 64 + j * 4) = acc[t0 + tt][i];
+            __syncthreads();
+#pragma unroll
+            for (int m = 0; m < 3; m++) {
+                const int q = tid + 256 * m;
+                const int tt = q >> 8, cl = 4 * ((q >> 4) & 15), ci = ci0 + (q & 15);
+                int64_t v[4] = {0, 0, 0, 0};
+#pragma unroll
+                for (int w = 0; w < 4; w++) {
+                    const v4i rv = *(const v4i *)(red + (w * 3 + tt) * 1024 + (q & 255) * 4);
+                    const int sh = 8 * (L3 ? (l3 ? l : w / Q) : w / Q);
+#pragma unroll
+                    for (int r = 0; r < 4; r++) v[r] += (int64_t)rv[r] * ((int64_t)1 << sh);
+                }
+                if (L3) {
 #pragma unroll
                     for (int r = 0; r < 4; r++)
-                        red[((wave * 3 + tt) * 64 + 16 * i + 4 * g4 + r) * 16 + j] = acc[t0 + tt][i][r];
-            __syncthreads();
-            if (L3) {
+                        tot[L3 ? t0 / 3 : 0][4 * m + r] = pass == 0 ? v[r] : tot[L3 ? t0 / 3 : 0][4 * m + r] + v[r];
+                } else {
 #pragma unroll
-                for (int k = 0; k < 12; k++) {
-                    const int e = tid + 256 * k;
-                    int64_t v = 0;
-#pragma unroll
-                    for (int w = 0; w < 4; w++)
-                        v += (int64_t)red[(w * 3 + e / 1024) * 1024 + (e & 1023)] *
-                             ((int64_t)1 << (8 * (l3 ? l : w / Q)));
-                    tot[L3 ? t0 / 3 : 0][k] = pass == 0 ? v : tot[L3 ? t0 / 3 : 0][k] + v;
-                }
-            } else {
-                for (int e = tid; e < 3 * 1024; e += 256) {
-                    const int tt = e >> 10, co = co0 + ((e >> 4) & 63), ci = ci0 + (e & 15);
-                    int64_t v = 0;
-#pragma unroll
-                    for (int w = 0; w < 4; w++)
-                        v += (int64_t)red[(w * 3 + tt) * 1024 + (e & 1023)] * ((int64_t)1 << (8 * (w / Q)));
-                    if (co < p.co && ci < p.ci_out)
-                        p.out[(((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci_out + ci] = v;
+                    for (int r = 0; r < 4; r++) {
+                        const int co = co0 + cl + r;
+                        if (co < p.co && ci < p.ci_out)
+                            p.out[(((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci_out + ci] = v[r];
+                    }
                 }
             }
             __syncthreads();
@@ -514,11 +518,16 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 #pragma unroll
         for (int t0 = 0; t0 < 9; t0 += 3)
 #pragma unroll
-            for (int k = 0; k < 12; k++) {
-                const int e = tid + 256 * k;
-                const int tt = e >> 10, co = co0 + ((e >> 4) & 63), ci = ci0 + (e & 15);
-                if (co < p.co && ci < p.ci_out)
-                    p.out[(((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci_out + ci] = tot[L3 ? t0 / 3 : 0][k];
+            for (int m = 0; m < 3; m++) {
+                const int q = tid + 256 * m;
+                const int tt = q >> 8, cl = 4 * ((q >> 4) & 15), ci = ci0 + (q & 15);
+#pragma unroll
+                for (int r = 0; r < 4; r++) {
+                    const int co = co0 + cl + r;
+                    if (co < p.co && ci < p.ci_out)
+                        p.out[(((int64_t)split * p.co + co) * 9 + t0 + tt) * p.ci_out + ci] =
+                            tot[L3 ? t0 / 3 : 0][4 * m + r];
+                }
             }
     }
     ts_end(p.ts);
