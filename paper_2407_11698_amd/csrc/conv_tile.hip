@@ -389,6 +389,29 @@ void k_conv_tile(TileArgs p)
     // Persistent (two stages, one workgroup per CU): workgroup b takes tiles b, b + G, b + 2G, ...
     // (G = the grid size), its set-up done once, and the global loads of the next tile's first
     // phase are issued before the epilogue and overlap it. Otherwise one tile per workgroup.
+    // (input gradient: the previous layer's region codes of this thread's outputs, requested
+    // all at once as the tile's last phase starts, so that they arrive under its MFMAs; read
+    // one by one between the epilogue's stores, each read would wait for the memory in turn)
+    uint32_t cdv[MODE == IG_DX ? TM : 1][MODE == IG_DX ? TN : 1];
+    // The loads are issued whether or not there are codes (then from a zero block): this loop
+    // also loads straight into LDS, and the compiler counts outstanding loads statically, so a
+    // load skipped on one path would let its wait before the next barrier count too few.
+    auto codes_load = [&](int64_t tm0, int tn0) {
+        if (MODE != IG_DX) return;
+        const int pxp = (tid >> 7) * 64 + (tid & 15);
+        const int cbp = ((tid >> 6) & 1) * 32 + 4 * ((tid >> 4) & 3);
+        const bool have = p.prev_code != nullptr;
+#pragma unroll
+        for (int i = 0; i < TM; i++)
+#pragma unroll
+            for (int j = 0; j < TN; j++) {
+                const int64_t m = tm0 + pxp + 16 * i;
+                const int col = tn0 + cbp + 16 * j;
+                const bool in = have && m < M && col < p.no;
+                const uint8_t *src = in ? p.prev_code + m * p.no + col : (const uint8_t *)ct_zero16;
+                cdv[MODE == IG_DX ? i : 0][MODE == IG_DX ? j : 0] = *(const uint32_t *)src;
+            }
+    };
     uint32_t mx = 0;                              // input gradient: max |g| over this workgroup
     bool bad = false;                             // input gradient: a sum outside int32
     int v = blockIdx.x;
@@ -423,6 +446,7 @@ void k_conv_tile(TileArgs p)
                 stage_store(0);
                 __syncthreads();
                 if (ph + 1 < nph) stage_load(ph + 1);
+                if (ph + 1 == nph) codes_load(em0, en0);
                 compute(std::false_type{}, smem, 0, nullptr, nullptr);
                 fold(ph);
                 gph++;
@@ -437,6 +461,7 @@ void k_conv_tile(TileArgs p)
             for (int ph = 0; ph < nph; ph++) {
                 __syncthreads();
                 const int cb = gph & 1;
+                if (ph + 1 == nph) codes_load(em0, en0);
                 if (ADMA) {
                     const int8_t *sa = nullptr, *sb = nullptr;
                     if (ph + 1 < nph) {
@@ -461,23 +486,6 @@ void k_conv_tile(TileArgs p)
                 set_tile(vn);
                 stage_load(0);
             }
-        }
-        // (input gradient: the previous layer's region codes of this thread's outputs, requested
-        // all at once before the epilogue; read one by one between its stores, each read would
-        // wait for the memory in turn)
-        uint32_t cdv[MODE == IG_DX ? TM : 1][MODE == IG_DX ? TN : 1];
-        if (MODE == IG_DX && p.prev_code) {
-            const int pxp = (tid >> 7) * 64 + (tid & 15);
-            const int cbp = ((tid >> 6) & 1) * 32 + 4 * ((tid >> 4) & 3);
-#pragma unroll
-            for (int i = 0; i < TM; i++)
-#pragma unroll
-                for (int j = 0; j < TN; j++) {
-                    const int64_t m = em0 + pxp + 16 * i;
-                    const int col = en0 + cbp + 16 * j;
-                    cdv[MODE == IG_DX ? i : 0][MODE == IG_DX ? j : 0] =
-                        m < M && col < p.no ? *(const uint32_t *)(p.prev_code + m * p.no + col) : 0u;
-                }
         }
         __syncthreads();                          // the epilogue reuses the stages' LDS
         // ------------------------------------------------------------ epilogues

@@ -682,7 +682,7 @@ void launch_pack_conv_tiled(hipStream_t s, const int32_t *w, int co, int ci, int
 void launch_pack_matrix(hipStream_t s, const int32_t *w, int R, int C, int Rpad, int8_t *p,
                         int8_t *t, uint32_t *wmax);
 constexpr int SGD_MAX = 24;
-constexpr int SGD_ITEMS = 8;
+constexpr int SGD_ITEMS = 2;
 struct SgdTensor {
     int32_t *w;
     const int64_t *dw;
