@@ -145,6 +145,13 @@ __device__ void lgemm_tile(const LgemmArgs &p, uint8_t *smem, int bx, int by, in
             cdp[q] = m < p.M && col < p.N ? *(const v4i *)(p.code + (int64_t)m * p.N + col) : v4i{0, 0, 0, 0};
         }
     }
+    // (the codes are consumed here, by nothing: left alone, the compiler issues their loads
+    // only in the epilogue, where each then waits for the memory; this wait coincides with the
+    // first round's own)
+    if (MODE == LIN_UNPOOL) {
+#pragma unroll
+        for (int q = 0; q < EIT; q++) asm volatile("" : "+v"(cdp[q]));
+    }
     for (int r = 0; r < nr; r++) {
         __syncthreads();                          // every wave is done with the previous round
         store(r);
