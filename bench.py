@@ -92,6 +92,19 @@ def limbs_for(m: int) -> int:
     return 1 if m <= 127 else 2 if m <= 32639 else 3 if m <= 8355711 else 4
 
 
+# The library's input gradient takes g in two limbs plus an offset correction when
+# 32639 < max|g| <= 32768 and at most this many entries of g equal 32768 (three limbs otherwise).
+G_OFFSET_CAP = 16384
+
+
+def dx_g_limbs(g) -> int:
+    """Limb passes over g of the first layer's int64 input gradient."""
+    m = int(g.abs().max().item())
+    if 32639 < m <= 32768 and int((g == 32768).sum().item()) <= G_OFFSET_CAP:
+        return 2
+    return limbs_for(m)
+
+
 def stress_layer(reps: int):
     """The single conv-layer stress case (256x256x32x32 int8 activations, conv 256 -> 256, int32
     error signal in [-2^15, 2^15] at the NITRO-ReLU output), `reps` cumulative repeats, each a
@@ -99,9 +112,12 @@ def stress_layer(reps: int):
     IntegerSGD step with the amplified rate, run alone on the GPU after the training iterations.
 
     Each repeat is timed whole with HIP events on the library's stream (every kernel of the
-    repeat, IntegerSGD included), and its three conv GEMM kernels by their own device time.
+    repeat, IntegerSGD included), and its three conv GEMM kernels by their own device time; the
+    repeat's g (limb passes) comes from an untimed replay of it from the same weights.
     Algorithmic ops count each GEMM once (2 x N*H*W*C_out*9*C_in, three GEMMs per repeat); MFMA
-    ops count every limb pass the kernel executes, from the repeat's own max|W| and max|g|. The
+    ops count every limb pass the kernel executes, from the repeat's own max|W| and g (the input
+    gradient's kernel time excludes the two small kernels of g's offset form, which the whole
+    repeat includes). The
     weights leave int8 after the first repeat, so repeat 1 and the steady state (median over the
     later repeats) are reported separately."""
     import torch
@@ -122,16 +138,27 @@ def stress_layer(reps: int):
     st.ctx.kernel_timing(True)
     for r in range(reps):
         lw = limbs_for(int(st.w.abs().max().item()))          # the weights this repeat reads
+        w_before = st.w.clone()
         st.ctx.sync()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        st.repeat(xd, dd, taps={"g": [g]})
+        st.repeat(xd, dd)
         e1.record(stream)
         st.ctx.sync()
         kt = {name: st.ctx.kernel_time(c)[0] for c, name in KERNEL_CLASSES.items()}
+        # g of this repeat (for its limb passes) from an untimed replay with g tapped: the same
+        # weights in, the same weights out
+        w_after = st.w.clone()
+        st.w.copy_(w_before)
+        st.ctx.kernel_timing(False)
+        st.repeat(xd, dd, taps={"g": [g]})
+        st.ctx.sync()
+        st.ctx.kernel_timing(True)
+        if not torch.equal(st.w, w_after):
+            raise RuntimeError("stress repeat %d: the replay's weights differ" % r)
         lg = limbs_for(int(g.abs().max().item()))
         per.append({"ms": e0.elapsed_time(e1), "kernels_ms": kt,
-                    "passes": {"k_conv_tile<fwd>": lw, "k_conv_tile<dx>": lg * lw,
+                    "passes": {"k_conv_tile<fwd>": lw, "k_conv_tile<dx>": dx_g_limbs(g) * lw,
                                "k_conv_dw_planes": lg}})
     st.ctx.kernel_timing(False)
 

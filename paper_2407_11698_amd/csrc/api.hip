@@ -208,7 +208,8 @@ struct BlockGeom {
     size_t code[NITRO_MAX_LAYERS];
     size_t wf[NITRO_MAX_LAYERS];   // conv: 4 int8 limb planes of W, [co][9 ci] (ci padded: 16)
     size_t wt[NITRO_MAX_LAYERS];   // conv: 4 int8 limb planes of W, [ci][9 co]
-    size_t slots;                  // max slots: |W_j| (0..3), |g_j| (4..7), |W_lr| (8), |e| (9)
+    size_t slots;                  // max slots: |W_j| (0..3), |g_j| (4..7), |W_lr| (8), |e| (9);
+                                   // slot 10 word 0: the offset form's residual count
     size_t gt;                     // weight-gradient scratch: pixel-contiguous limb planes of g
     size_t xpl;                    // weight-gradient scratch: zero-padded planes of x
     size_t xpad;                   // forward scratch: a layer input with channels padded to 16
@@ -219,6 +220,7 @@ struct BlockGeom {
     size_t lf, lfc;                // learning-pooled block output and its window indices
     size_t yhat, e, delta, g0, g1;
     size_t g16;                    // an inner layer's gradient in the escaped 16-bit form
+    size_t gres, gbias;            // the first layer's g in the offset form: residual list, bias
     size_t total;
 };
 
@@ -344,6 +346,9 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     g->g0 = off;    off = align256(off + (size_t)gmax * 4);
     g->g1 = off;    off = align256(off + (size_t)(g->J > 1 ? gmax : 0) * 4);
     g->g16 = off;   off = align256(off + (size_t)(g->J > 1 ? gmax : 0) * 2);
+    const bool goff = conv && g->L[0].dx_tile && dwp_ok(g->L[0].sh);
+    g->gres = off;  off = align256(off + (goff ? (size_t)GOFF_CAP * 4 : 0));
+    g->gbias = off; off = align256(off + (goff ? (size_t)16 * 8 * g->L[0].sh.c : 0));
     g->total = off;
     return NITRO_OK;
 }
@@ -451,8 +456,9 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
     const int J = g.J;
     const LayerGeom &LJ = g.L[J - 1];
     uint32_t *slots = (uint32_t *)at(state, g.slots);
-    // max|g_j| (4..7), max|W_lr| (8), max|e| (9) are produced by this call
-    if (zero_slots && hipMemsetAsync(slots + 4 * SLOT_WORDS, 0, 6 * SLOT_WORDS * 4, s) != hipSuccess)
+    // max|g_j| (4..7), max|W_lr| (8), max|e| (9) and the offset form's count (10) are produced
+    // by this call
+    if (zero_slots && hipMemsetAsync(slots + 4 * SLOT_WORDS, 0, 7 * SLOT_WORDS * 4, s) != hipSuccess)
         return NITRO_EHIP;
     bool have_g = false;
     // The last layer's g left pooled by the learning layer and un-pooled by the weight-gradient
@@ -524,6 +530,9 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         const LayerGeom &L = g.L[j];
         const int8_t *xin = j == 0 ? x : (const int8_t *)at(state, g.act[j - 1]);
         const int32_t *gj = gb[cur];
+        // the first layer's int64 input gradient on the tile: g may go in the offset form
+        const bool goff = j == 0 && taps && taps->dx && L.conv && L.dx_tile && dwp_ok(L.sh);
+        const GOff go{slots + 10 * SLOT_WORDS, (uint32_t *)at(state, g.gres), (int64_t *)at(state, g.gbias)};
         if (L.conv) {
             const bool need_dx = j > 0 || (taps && taps->dx);
             if (dwp_ok(L.sh))
@@ -533,7 +542,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                                       (int64_t *)at(state, g.part), gr->dw[j], ctx->flags,
                                       j == J - 1 && rows_from_forward(g),
                                       j == J - 1 && g_pooled ? at(state, g.code[J - 1]) : nullptr,
-                                      gj16);
+                                      gj16, goff ? &go : nullptr);
             else if (mfma_conv_dw_ok(L.sh) || mfma_conv_dw_smallc_ok(L.sh))
                 launch_conv_dw_mfma(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, xin, (int8_t *)at(state, g.gt),
                                     (int64_t *)at(state, g.part), gr->dw[j], ctx->flags);
@@ -568,12 +577,17 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         if (dst || dst64) {
             uint32_t *gmax_out = j > 0 ? slots + (4 + j - 1) * SLOT_WORDS : nullptr;
             if (L.conv) {
-                if (L.dx_tile)
+                if (L.dx_tile) {
+                    if (goff)
+                        launch_goff_bias(s, (const int8_t *)at(state, g.wt[j]), L.sh.co, L.sh.c,
+                                         slots + (4 + j) * SLOT_WORDS, go.bias);
                     launch_conv_dx_tile(s, ctx->conv_tile, ctx->conv_persist, L.sh, (const int8_t *)at(state, g.gnl),
                                         slots + (4 + j) * SLOT_WORDS,
                                         (const int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS,
-                                        code, rp, dst, dst64, gmax_out, ctx->flags, dst16);
-                else if (mfma_conv_dx_ok(L.sh))
+                                        code, rp, dst, dst64, gmax_out, ctx->flags, dst16,
+                                        goff ? &go : nullptr);
+                    if (goff) launch_goff_fix(s, L.sh, go, p->w[j], dst64);
+                } else if (mfma_conv_dx_ok(L.sh))
                     launch_conv_dx_mfma(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, (const int8_t *)at(state, g.wt[j]),
                                         slots + (j) * SLOT_WORDS, code, rp, dst, dst64, gmax_out, ctx->flags);
                 else

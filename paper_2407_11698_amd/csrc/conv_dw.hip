@@ -166,8 +166,9 @@ __device__ void dwp_pad_rows(int n, int h, int w, int hp, int wp, int64_t kraw, 
 // padded position k (zeros at pad positions), 16-byte chunk (channel c, positions k .. k + 15)
 // at l C kp + ((k / 256 * C / 16 + c / 16) * 4 + k % 256 / 64) * 1024 + 256 (k % 64 / 16)
 // + 16 (c % 16); when gn is not null also the NHWC limb planes gn [l][P][C] (the A
-// operand of the input-gradient GEMM). A workgroup: 64 positions x 64 channels, transposed
-// through LDS. With pcode, g holds a 2x2-pooled layer's gradient at the pooled positions only,
+// operand of the input-gradient GEMM), with goff and max|g| in the offset range those of
+// g - 128 (three limbs) and the indices of the entries g = 32768 appended to go.list. A
+// workgroup: 64 positions x 64 channels, transposed through LDS. With pcode, g holds a 2x2-pooled layer's gradient at the pooled positions only,
 // [n][h/2][w/2][C]: pixel (y, x) takes it where the pool's argmax (the code's low 2 bits) is
 // window position 2 (y & 1) + (x & 1), and zero elsewhere. Workgroup (bx, by): positions
 // 64 bx .., channels 64 by ...
@@ -175,12 +176,15 @@ __device__ void dwp_grad_planes(const int32_t *__restrict__ g, const int16_t *__
                                 int n, int h, int w, int c, int hp,
                                 int wp, int kp, const uint32_t *gmax,
                                 const uint8_t *__restrict__ pcode, int8_t *__restrict__ gp,
-                                int8_t *__restrict__ gn, int bx, int by)
+                                int8_t *__restrict__ gn, const GOff &go, bool goff, int bx, int by)
 {
     __shared__ int32_t T[64][65];        // [position][channel]
-    const int LA = limbs_for(slot_read(gmax));
+    const uint32_t gm = slot_read(gmax);
+    const int LA = limbs_for(gm);
     if (LA > 4) return;                  // the weight-gradient kernel flags it
+    const bool off = goff && goff_range(gm);
     const int tid = threadIdx.x;
+    uint32_t rmask = 0;                  // offset form: this thread's entries with g = 32768
     const int k0 = bx * 64;
     const int c0 = by * 64;
     {
@@ -225,16 +229,41 @@ __device__ void dwp_grad_planes(const int32_t *__restrict__ g, const int16_t *__
         }
         if (gn && pix >= 0 && c0 + 16 * cq < c) {
             const int64_t P = (int64_t)n * h * w;
+            const int32_t ob = off ? GOFF_BIAS : 0;
+#pragma unroll
+            for (int e = 0; e < 16; e++) rmask |= (off && v[e] >= 32768) ? 1u << e : 0u;
 #pragma unroll
             for (int l = 0; l < 4; l++) {
                 if (l < LA) {
                     v4i o;
 #pragma unroll
                     for (int q = 0; q < 4; q++)
-                        o[q] = (int)limb4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3], l);
+                        o[q] = (int)limb4(v[4 * q] - ob, v[4 * q + 1] - ob, v[4 * q + 2] - ob,
+                                          v[4 * q + 3] - ob, l);
                     *(v4i *)(gn + (int64_t)l * P * c + (int64_t)pix * c + c0 + 16 * cq) = o;
                 }
             }
+        }
+        // the entries g = 32768 appended to the list: one atomic per wave that has any, each
+        // lane's entries at its exclusive prefix of the wave's counts (every lane is here)
+        if (off && __ballot(rmask != 0)) {
+            const int lane = tid & 63;
+            const int k = __popc(rmask);
+            int incl = k;
+#pragma unroll
+            for (int d = 1; d < 64; d <<= 1) {
+                const int o = __shfl_up(incl, d, 64);
+                if (lane >= d) incl += o;
+            }
+            const int total = __shfl(incl, 63, 64);
+            uint32_t base = 0;
+            if (lane == 0) base = atomicAdd(go.count, (uint32_t)total);
+            uint32_t idx = (uint32_t)__shfl((int)base, 0, 64) + (uint32_t)(incl - k);
+            for (int e = 0; e < 16; e++)
+                if (rmask & (1u << e)) {
+                    if (idx < GOFF_CAP) go.list[idx] = (uint32_t)pix * (uint32_t)c + (uint32_t)(c0 + 16 * cq + e);
+                    idx++;
+                }
         }
     }
     __syncthreads();
@@ -275,6 +304,8 @@ struct DwpPrep {
     const uint32_t *gmax;
     const uint8_t *pcode;
     int8_t *gp, *gn;
+    GOff go;                     // with goff: gn may take the offset form
+    int goff;
 };
 
 __global__ __launch_bounds__(256) void k_dwp_prep(DwpPrep a)
@@ -289,7 +320,7 @@ __global__ __launch_bounds__(256) void k_dwp_prep(DwpPrep a)
     }
     const int q = b - nrows;
     dwp_grad_planes(a.g, a.g16, a.n, a.h, a.w, a.co, a.hp, a.wp, a.kp, a.gmax, a.pcode, a.gp, a.gn,
-                    q % a.gp_gx, q / a.gp_gx);
+                    a.go, a.goff != 0, q % a.gp_gx, q / a.gp_gx);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -536,7 +567,8 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
                            int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags,
-                           bool x_rows_ready, const uint8_t *pool_code, const int16_t *g16)
+                           bool x_rows_ready, const uint8_t *pool_code, const int16_t *g16,
+                           const GOff *goff)
 {
     const DwpGeom ge = dwp_geom(sh);
     const DwpPlan pl = dwp_plan(sh);
@@ -551,6 +583,10 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
         pa.x = x; pa.n = sh.n; pa.h = sh.h; pa.w = sh.w; pa.c = sh.c; pa.co = sh.co;
         pa.hp = ge.hp; pa.wp = ge.wp; pa.kp = (int)ge.kp; pa.kraw = ge.kraw; pa.xs = ge.xs; pa.xr = xp;
         pa.g = g; pa.g16 = g16; pa.gmax = gmax; pa.pcode = pool_code; pa.gp = gp; pa.gn = gn;
+        if (goff && gn) {
+            pa.go = *goff;
+            pa.goff = 1;
+        }
         const int64_t nwg = (int64_t)pa.rows_gx * pa.rows_gy + (int64_t)pa.gp_gx * ((sh.co + 63) / 64);
         hipLaunchKernelGGL(k_dwp_prep, dim3((unsigned)nwg), dim3(256), 0, s, pa);
     }

@@ -90,6 +90,11 @@ struct TileArgs {
     uint32_t *gmax;
     uint32_t *flags;
     uint64_t *ts;                  // timing slot (null: untimed)
+    // out64: g may be in the offset form (two limbs of g - 128, or three with more than
+    // GOFF_CAP entries g = 32768), its term from the border-class table goff_bias [16][no]
+    int goff;
+    const uint32_t *goff_count;
+    const int64_t *goff_bias;
 };
 
 __device__ inline int32_t sat_i32(int64_t v)
@@ -144,7 +149,16 @@ void k_conv_tile(TileArgs p)
     const int K = 9 * p.ck;
     const int nchunk = p.ck / CC;
 
-    const int LA = MODE == IG_FWD ? 1 : limbs_for(slot_read(p.a_max));
+    // (input gradient: the residual count of the offset form is read whether or not it is
+    // used, from the max slot then, so that both loads are in flight together)
+    bool goff = false;
+    int LA = 1;
+    if (MODE == IG_DX) {
+        const uint32_t rn = *(p.goff ? p.goff_count : p.a_max);
+        const uint32_t am = slot_read(p.a_max);
+        goff = p.goff && goff_range(am);
+        LA = goff ? (rn <= GOFF_CAP ? 2 : 3) : limbs_for(am);
+    }
     const int LB = limbs_for(slot_read(p.b_max));
     if (LA > 4 || LB > 4) {
         if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
@@ -606,7 +620,8 @@ void k_conv_tile(TileArgs p)
                 }
             }
         } else if (p.out64) {
-            // raw int64 input gradient (the first layer of a network): 4 channels per lane and tile
+            // raw int64 input gradient (the first layer of a network): 4 channels per lane and
+            // tile; the offset form adds its term for the pixel's border class
 #pragma unroll
             for (int i = 0; i < TM; i++)
 #pragma unroll
@@ -615,9 +630,19 @@ void k_conv_tile(TileArgs p)
                     const int col = en0 + cbl + 16 * j;
                     if (m >= M || col >= p.no) continue;
                     int64_t *dst = p.out64 + m * p.no + col;
+                    int64_t bv[4] = {0, 0, 0, 0};
+                    if (goff) {
+                        const uint32_t R = udiv32((uint32_t)m, p.d_w);
+                        const int ww = (int)((uint32_t)m - R * (uint32_t)p.w);
+                        const int hh = (int)(R - udiv32(R, p.d_h) * (uint32_t)p.h);
+                        const int cls = (hh == 0) | (hh == p.h - 1) << 1 | (ww == 0) << 2 | (ww == p.w - 1) << 3;
+                        const int64_t *bp = p.goff_bias + cls * p.no + col;
+#pragma unroll
+                        for (int t = 0; t < 4; t++) bv[t] = bp[t];
+                    }
 #pragma unroll
                     for (int t = 0; t < 4; t++)
-                        dst[t] = npass > 1 ? acc64[i][j][t] : (int64_t)acc[i][j][t];
+                        dst[t] = (npass > 1 ? acc64[i][j][t] : (int64_t)acc[i][j][t]) + bv[t];
                 }
         } else {
             // int32 sums, ReLU' of the previous layer with its 4 region codes, one 16-byte store
@@ -822,7 +847,7 @@ void launch_conv_fwd_tile(hipStream_t s, int tile, int persist, const ConvShape 
 void launch_conv_dx_tile(hipStream_t s, int tile, int persist, const ConvShape &sh, const int8_t *gl,
                          const uint32_t *gmax_in, const int8_t *wt, const uint32_t *wmax,
                          const uint8_t *prev_code, const Relu &rp, int32_t *gout, int64_t *out64,
-                         uint32_t *gmax_out, uint32_t *flags, int16_t *gout16)
+                         uint32_t *gmax_out, uint32_t *flags, int16_t *gout16, const GOff *goff)
 {
     TileArgs a{};
     a.n = sh.n; a.h = sh.h; a.w = sh.w;
@@ -832,9 +857,108 @@ void launch_conv_dx_tile(hipStream_t s, int tile, int persist, const ConvShape &
     a.rp = rp;
     a.prev_code = prev_code; a.gout = gout; a.out64 = out64; a.gmax = gmax_out;
     a.gout16 = gout ? gout16 : nullptr;
+    if (goff && out64) {
+        a.goff = 1;
+        a.goff_count = goff->count;
+        a.goff_bias = goff->bias;
+    }
     a.flags = flags;
     if (use_wide_tile(tile, sh.n, sh.h, sh.w, sh.c, false)) launch_tile<IG_DX, 4>(s, persist, a);
     else launch_tile<IG_DX, 2>(s, persist, a);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Offset form of g: the bias table and the corrections of the listed entries.
+
+// bias[cls][ci] = 128 sum_co sum_{(r,s) allowed by cls} W[co][r][s][ci]: a pixel on the top row
+// (cls bit 0) has no g position above it to take tap r = 2 from (g at p - (r-1, s-1)), the
+// bottom row (bit 1) none for r = 0, the first column (bit 2) none for s = 2, the last column
+// (bit 3) none for s = 0. W is read from the input gradient's limb planes wt [4][ci][9 co] (all
+// four limbs: W exactly). One wave per input channel c: its lanes take the dwords of row c of
+// each plane, every (limb, tap) load issued before the sums, then the 36 tap sums are reduced
+// across the wave by shuffles and lanes 0..15 form the 16 classes.
+__global__ __launch_bounds__(256) void k_goff_bias(const int8_t *__restrict__ wt, int co, int ci,
+                                                   const uint32_t *gmax, int64_t *__restrict__ bias)
+{
+    if (!goff_range(slot_read(gmax))) return;
+    const int lane = threadIdx.x & 63;
+    const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (c >= ci) return;
+    const int64_t row = 9 * (int64_t)co, plane = (int64_t)ci * row;
+    const int nd = co / 4;                        // dwords per tap row
+    int32_t acc[36];
+#pragma unroll
+    for (int k = 0; k < 36; k++) acc[k] = 0;
+    for (int d0 = 0; d0 < nd; d0 += 64) {
+        const int d = d0 + lane;
+        const bool in = d < nd;
+        uint32_t v[36];
+#pragma unroll
+        for (int k = 0; k < 36; k++)
+            v[k] = in ? *(const uint32_t *)(wt + (k / 9) * plane + c * row + (k % 9) * co + 4 * d) : 0u;
+#pragma unroll
+        for (int k = 0; k < 36; k++)
+            acc[k] += (int8_t)v[k] + (int8_t)(v[k] >> 8) + (int8_t)(v[k] >> 16) + (int8_t)(v[k] >> 24);
+    }
+#pragma unroll
+    for (int k = 0; k < 36; k++)
+        for (int off = 32; off > 0; off >>= 1) acc[k] += __shfl_xor(acc[k], off, 64);
+    if (lane >= 16) return;
+    const int cls = lane;
+    int64_t b = 0;
+#pragma unroll
+    for (int t = 0; t < 9; t++) {
+        const int r = t / 3, sc = t % 3;
+        const bool ok = !(((cls & 1) && r == 2) || ((cls & 2) && r == 0) || ((cls & 4) && sc == 2) ||
+                          ((cls & 8) && sc == 0));
+#pragma unroll
+        for (int l = 0; l < 4; l++)
+            if (ok) b += (int64_t)acc[9 * l + t] * ((int64_t)1 << (8 * l));
+    }
+    bias[(int64_t)cls * ci + c] = (int64_t)GOFF_BIAS * b;
+}
+
+void launch_goff_bias(hipStream_t s, const int8_t *wt, int co, int ci, const uint32_t *gmax,
+                      int64_t *bias)
+{
+    hipLaunchKernelGGL(k_goff_bias, dim3((unsigned)((ci + 3) / 4)), dim3(256), 0, s, wt, co, ci, gmax,
+                       bias);
+}
+
+// Entry (g = 32768 at pixel p, channel o, its third limb 1): dx[p + (r-1, s-1)][ci] +=
+// 65536 W[o][r][s][ci] for the taps whose pixel is inside the image (atomic adds: entries near
+// each other reach the same outputs). Workgroups take entries e = blockIdx.x + gridDim.x k,
+// threads the input channels; a thread's nine W values are loaded before its adds.
+__global__ __launch_bounds__(256) void k_goff_fix(GOff go, const int32_t *__restrict__ w, int h,
+                                                  int wd, int co, int ci, int64_t *__restrict__ dx)
+{
+    const uint32_t cnt = *go.count;
+    if (cnt == 0 || cnt > GOFF_CAP) return;
+    const uint32_t hw = (uint32_t)h * (uint32_t)wd;
+    for (uint32_t e = blockIdx.x; e < cnt; e += gridDim.x) {
+        const uint32_t idx = go.list[e];
+        const uint32_t pix = idx / (uint32_t)co, o = idx - pix * (uint32_t)co;
+        const uint32_t img = pix / hw, rem = pix - img * hw;
+        const int y = (int)(rem / (uint32_t)wd), x = (int)(rem - (uint32_t)y * (uint32_t)wd);
+        for (int c = threadIdx.x; c < ci; c += 256) {
+            int64_t v[9];
+#pragma unroll
+            for (int t = 0; t < 9; t++) v[t] = (int64_t)w[((int64_t)o * 9 + t) * ci + c] * 65536;
+#pragma unroll
+            for (int t = 0; t < 9; t++) {
+                const int qy = y + t / 3 - 1, qx = x + t % 3 - 1;
+                if (qy >= 0 && qy < h && qx >= 0 && qx < wd)
+                    atomicAdd((unsigned long long *)(dx + (((int64_t)img * h + qy) * wd + qx) * ci + c),
+                              (unsigned long long)v[t]);
+            }
+        }
+    }
+}
+
+void launch_goff_fix(hipStream_t s, const ConvShape &sh, const GOff &go, const int32_t *w,
+                     int64_t *dx)
+{
+    hipLaunchKernelGGL(k_goff_fix, dim3(1024), dim3(256), 0, s, go, w, sh.h, sh.w, sh.co, sh.c, dx);
 }
 
 }  // namespace nitro

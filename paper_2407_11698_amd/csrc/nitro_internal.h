@@ -593,11 +593,43 @@ int64_t dwp_rows_stride(const ConvShape &sh);   // xs
 // pool_code (a pooled layer's codes, [n][h/2][w/2][co]): g is given at the pooled positions only
 // (launch_learning_mfma with g_pooled) and each window's argmax takes the value
 // g16: g in the escaped 16-bit form (g then holds the escaped values only).
+// goff (with gn): gn may take the offset form below.
+struct GOff;
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
                            int8_t *gn, int64_t *part, int64_t *dw, uint32_t *flags,
                            bool x_rows_ready = false, const uint8_t *pool_code = nullptr,
-                           const int16_t *g16 = nullptr);
+                           const int16_t *g16 = nullptr, const GOff *goff = nullptr);
+
+// g one value past two limbs. Two balanced int8 limbs hold the 65536 integers [-32896, 32639];
+// a gradient with max|g| = 32768 (the 16-bit error signal of the single-layer case passed
+// through NITRO-ReLU) spans 65537 and would take a third limb pass in the input-gradient GEMM.
+// Offset form, for the int64 input gradient of a block's first layer: when
+// 32639 < max|g| <= 32768, g's NHWC limb planes hold the three balanced limbs of g - 128 at
+// every pixel, whose third limb is 1 where g = 32768 and 0 elsewhere. The GEMM runs limbs 0
+// and 1 only, and the input gradient gets back
+//   + 128 sum_{co, (r,s) with p - (r-1, s-1) inside the image} W[co][r][s][ci]
+// (a function of ci and of the pixel's border class, from a table) and, for each g = 32768
+// (listed by the preparation, at most GOFF_CAP of them), 65536 W[co][r][s][ci] at the pixels
+// p + (r-1, s-1) inside the image (atomic adds). With more than GOFF_CAP such entries the GEMM
+// runs all three limbs instead. Exact either way.
+constexpr int32_t GOFF_BIAS = 128;
+constexpr uint32_t GOFF_CAP = 16384;
+__host__ __device__ inline bool goff_range(uint32_t m) { return m > 32639u && m <= 32768u; }
+struct GOff {
+    uint32_t *count;       // entries with g = 32768 (a word that is zero before the preparation)
+    uint32_t *list;        // [GOFF_CAP] their indices p co + c in g
+    int64_t *bias;         // [16][ci]: the offset's term for border class
+                           // (h == 0) | (h == H-1) << 1 | (w == 0) << 2 | (w == W-1) << 3
+};
+// The bias table from W's input-gradient limb planes wt [4][ci][9 co] (the workgroups return
+// at once unless max|g| is in the offset range).
+void launch_goff_bias(hipStream_t s, const int8_t *wt, int co, int ci, const uint32_t *gmax,
+                      int64_t *bias);
+// The listed entries' 65536 W terms added into dx int64 NHWC [n][h][w][ci] (nothing unless
+// 0 < count <= GOFF_CAP).
+void launch_goff_fix(hipStream_t s, const ConvShape &sh, const GOff &go, const int32_t *w,
+                     int64_t *dx);
 
 // ---- implicit-GEMM conv with the input tile staged once (conv_tile.hip)
 bool tile_conv_fwd_ok(const ConvShape &sh, bool pool, int64_t sf, int alpha_inv);
@@ -613,10 +645,12 @@ void launch_conv_fwd_tile(hipStream_t s, int tile, int persist, const ConvShape 
 // gl: g's NHWC limb planes [LA][P][co] (max|g| in gmax_in); otherwise as launch_conv_dx_mfma.
 // gout16 (with gout): the result in the escaped 16-bit form below instead of int32 (gout then
 // receives only the escaped values).
+// goff (out64 only): gl may hold g in the offset form (as launch_conv_dw_planes wrote it).
 void launch_conv_dx_tile(hipStream_t s, int tile, int persist, const ConvShape &sh, const int8_t *gl,
                          const uint32_t *gmax_in, const int8_t *wt, const uint32_t *wmax,
                          const uint8_t *prev_code, const Relu &rp, int32_t *gout, int64_t *out64,
-                         uint32_t *gmax_out, uint32_t *flags, int16_t *gout16 = nullptr);
+                         uint32_t *gmax_out, uint32_t *flags, int16_t *gout16 = nullptr,
+                         const GOff *goff = nullptr);
 
 // A gradient stored in 16 bits with an escape: g16[i] = g[i] where |g[i]| <= G16_MAX, else
 // G16_ESC, and then the int32 array beside it holds g[i] at the same index (written, and read,

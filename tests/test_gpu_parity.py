@@ -39,10 +39,11 @@ def rand(rng, shape, lo, hi, dtype):
 
 
 def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dmax=1 << 15,
-              conv=True, tap_last_g=True, d_lr=0, tap_inner_g=True):
+              conv=True, tap_last_g=True, d_lr=0, tap_inner_g=True, delta_edit=None):
     """One nitro_block_forward + nitro_block_backward against the oracle's block functions.
     tap_last_g=False leaves the last layer's g untapped (the library may then keep it pooled);
     tap_inner_g=False the other layers' (the library may then keep them in 16 bits with escapes).
+    delta_edit(rng, delta, rec) (no learning layer): the given delta, edited after the forward.
     Returns the oracle's record."""
     print("block case", dict(n=n, h=h, w=w, chans=chans, pool=maxpool, G=G, alpha=alpha,
                              mode=nm, wmax=wmax, conv=conv), flush=True)
@@ -73,6 +74,8 @@ def run_block(ctx, rng, n, h, w, chans, maxpool, G, alpha, nm, om, wmax=127, dma
     want_dx, expect_overflow = True, False
     w_lr = rand(rng, (G, d), -wmax, wmax, np.int32) if G else None
     delta = None if G else rand(rng, out_shape, -dmax, dmax, np.int32)
+    if delta_edit is not None:
+        delta = delta_edit(rng, delta, rec)
     try:
         if G > 0:
             ff = f.reshape(n, d)
@@ -276,6 +279,64 @@ def test_conv_block_inner_g16(ctx, case, modes):
                     tap_inner_g=False, dmax=max(dmax, 1))
     inner = [np.abs(np.asarray(g, dtype=np.int64)).max() for g in rec.g[:-1]]
     assert (max(inner) > 32767) == escapes, inner
+
+
+# The first layer's int64 input gradient with g one value past two limbs (32639 < max|g| <=
+# 32768): the library takes g - 128 in two limbs, adds the offset's term per border class and
+# corrects each g = 32768 from a list (more than 16384 of them: three limbs instead). The given
+# delta is drawn in [-32767, 32767] and then set to 32768 at `plus` positions where NITRO-ReLU
+# passes it unchanged (z* in [0, 127]) and to -32768 at 5 such positions; top = 32769 puts one
+# 32769 there instead (outside the offset range), top = 32000 draws no edit at all.
+G_OFFSET_CASES = [
+    # n, h, w, chans, pool, plus, top
+    (4, 16, 16, [64, 64], False, 0, 32768),
+    (4, 16, 16, [64, 64], False, 7, 32768),
+    (4, 16, 16, [64, 64], False, 300, 32768),
+    (8, 16, 16, [64, 64], False, 16484, 32768),
+    (3, 8, 8, [32, 32], False, 40, 32768),
+    (2, 4, 4, [16, 16], False, 9, 32768),
+    (2, 16, 2, [16, 16], False, 9, 32768),
+    (2, 8, 8, [16, 32], True, 0, 32768),
+    (4, 16, 16, [64, 64], False, 7, 32769),
+    (4, 16, 16, [64, 64], False, 0, 32000),
+]
+
+
+def g_offset_edit(plus, top):
+    def edit(rng, delta, rec):
+        if top == 32000:
+            return np.clip(delta, -32000, 32000).astype(np.int32)
+        d = np.clip(delta, -32767, 32767).astype(np.int32)
+        zs = np.asarray(rec.layers[-1].zs)
+        if zs.shape != d.shape:        # pooled: the random draw reaches the range by itself
+            return rand(rng, d.shape, -32768, 32768, np.int32)
+        idx = np.flatnonzero((zs >= 0) & (zs <= 127))
+        pick = rng.choice(idx, size=plus + 5 + 1, replace=False)
+        flat = d.reshape(-1)
+        flat[pick[:plus]] = 32768 if top == 32768 else 0
+        flat[pick[plus:plus + 5]] = -32768
+        if top == 32769:
+            flat[pick[-1]] = 32769
+        return d
+    return edit
+
+
+@pytest.mark.parametrize("tile", [128, 256])
+@pytest.mark.parametrize("case", G_OFFSET_CASES)
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_conv_block_g_offset(ctx, tile, case, modes):
+    n, h, w, chans, pool, plus, top = case
+    rng = np.random.default_rng(hash((n, h, w, tuple(chans), pool, plus, top, 128)) % (1 << 31))
+    ctx.set_conv_tile(tile)
+    try:
+        rec = run_block(ctx, rng, n, h, w, chans, pool, 0, 10, modes[0], modes[1],
+                        delta_edit=g_offset_edit(plus, top))
+    finally:
+        ctx.set_conv_tile(0)
+    g = np.asarray(rec.g[0], dtype=np.int64)
+    if not pool:
+        assert int(np.abs(g).max()) == (top if top != 32000 else int(np.abs(g).max()))
+        assert int((g == 32768).sum()) == (plus if top == 32768 else 0)
 
 
 @pytest.mark.parametrize("chans,G,wmax", [([784, 100], 10, 7), ([100, 50, 30], 10, 300),
