@@ -345,7 +345,9 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     g->delta = off; off = align256(off + (size_t)(G > 0 ? g->out_elems : 0) * 4);
     g->g0 = off;    off = align256(off + (size_t)gmax * 4);
     g->g1 = off;    off = align256(off + (size_t)(g->J > 1 ? gmax : 0) * 4);
-    g->g16 = off;   off = align256(off + (size_t)(g->J > 1 ? gmax : 0) * 2);
+    // (an inner layer's g, or the last layer's as the ReLU' pass writes it for the preparation)
+    const bool g16_last = conv && dwp_ok(g->L[g->J - 1].sh) && !d->maxpool;
+    g->g16 = off;   off = align256(off + (size_t)(g->J > 1 || g16_last ? gmax : 0) * 2);
     const bool goff = conv && g->L[0].dx_tile && dwp_ok(g->L[0].sh);
     g->gres = off;  off = align256(off + (goff ? (size_t)GOFF_CAP * 4 : 0));
     g->gbias = off; off = align256(off + (goff ? (size_t)16 * 8 * g->L[0].sh.c : 0));
@@ -519,13 +521,22 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
             if (taps->e) (void)hipMemcpyAsync(taps->e, e, (size_t)n * G * 4, hipMemcpyDeviceToDevice, s);
         }
     }
-    if (!have_g)
-        launch_unpool_relu_bwd(s, n, LJ.sh.h, LJ.sh.w, LJ.sh.co, desc->maxpool != 0, delta,
-                               at(state, g.code[J - 1]), rp, gb[0], slots + (4 + J - 1) * SLOT_WORDS, ctx->flags);
-    int cur = 0;
     // g_j in the escaped 16-bit form (int16 at g16, the escapes in gb[cur]) when the layer above
-    // wrote it so
+    // (or, for the last layer, the ReLU' pass) wrote it so
     const int16_t *gj16 = nullptr;
+    if (!have_g) {
+        // the last layer's g in 16 bits where its only reader is the weight-gradient preparation
+        // (no tap of it, the planes weight gradient, its input gradient (if any) on the tile)
+        int16_t *g16 = nullptr;
+        if (LJ.conv && !desc->maxpool && dwp_ok(LJ.sh) && (!need_dx_last || LJ.dx_tile) &&
+            !(taps && taps->g[J - 1]))
+            g16 = (int16_t *)at(state, g.g16);
+        launch_unpool_relu_bwd(s, n, LJ.sh.h, LJ.sh.w, LJ.sh.co, desc->maxpool != 0, delta,
+                               at(state, g.code[J - 1]), rp, gb[0], slots + (4 + J - 1) * SLOT_WORDS, ctx->flags,
+                               g16);
+        gj16 = g16;
+    }
+    int cur = 0;
     for (int j = J - 1; j >= 0; j--) {
         const LayerGeom &L = g.L[j];
         const int8_t *xin = j == 0 ? x : (const int8_t *)at(state, g.act[j - 1]);

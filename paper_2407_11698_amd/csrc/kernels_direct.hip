@@ -1,7 +1,7 @@
 // Direct (non-MFMA) integer kernels for gfx950: elementwise passes, the skinny linear layers,
 // and direct convolutions for layers whose channel counts are too small for the MFMA tiles.
 // All accumulation is exact: int64 where a sum can leave int32.
-#include "nitro_internal.h"
+#include "mfma_common.h"
 
 namespace nitro {
 
@@ -321,35 +321,79 @@ __global__ void k_unpool_relu_bwd(int n, int h, int w, int c, const int32_t *__r
     if (gmax) block_slot_max(gmax, mx);
 }
 
-__global__ void k_relu_bwd(uint32_t count, const int32_t *__restrict__ delta,
-                           const uint8_t *__restrict__ code, Relu rp, int32_t *__restrict__ g,
-                           uint32_t *gmax, uint32_t *flags)
+// g = ReLU'(delta) at the layer's region codes (int32 delta: |g| <= |delta|, so g fits). Four
+// elements per thread and step (16 bytes of delta, 4 of codes) when the buffers are 16-byte
+// aligned; with g16, g in the escaped 16-bit form (g then receives only the escaped values).
+template <bool TR>
+__global__ __launch_bounds__(256) void k_relu_bwd(uint32_t count, const int32_t *__restrict__ delta,
+                                                  const uint8_t *__restrict__ code, Relu rp,
+                                                  int32_t *__restrict__ g, int16_t *__restrict__ g16,
+                                                  uint32_t *gmax, int vec)
 {
     uint32_t mx = 0;
-    bool bad = false;
-    for (uint32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < count; i += gridDim.x * blockDim.x) {
-        const int64_t v = relu_bwd(delta[i], code[i], rp);
-        const uint32_t a = abs_i64_sat(v);
-        mx = a > mx ? a : mx;
-        bad |= !fits_i32(v);
-        g[i] = (int32_t)v;
+    const uint32_t stride = gridDim.x * blockDim.x;
+    const uint32_t t0 = blockIdx.x * blockDim.x + threadIdx.x;
+    uint32_t done = 0;
+    if (vec) {
+        const uint32_t nq = count / 4;
+        for (uint32_t q = t0; q < nq; q += stride) {
+            const v4i d = *(const v4i *)(delta + 4 * (size_t)q);
+            const uint32_t cd = *(const uint32_t *)(code + 4 * (size_t)q);
+            v4i o;
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                o[e] = relu_bwd32<TR>(d[e], (cd >> (8 * e)) & 0xffu, rp);
+                const uint32_t a = abs_u32(o[e]);
+                mx = a > mx ? a : mx;
+            }
+            if (g16) {
+                uint32_t h[4];
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const bool esc = o[e] < -G16_MAX || o[e] > G16_MAX;
+                    if (esc) g[4 * (size_t)q + e] = o[e];
+                    h[e] = (uint32_t)(uint16_t)(esc ? G16_ESC : (int16_t)o[e]);
+                }
+                *(v2i *)(g16 + 4 * (size_t)q) = v2i{(int)(h[0] | (h[1] << 16)), (int)(h[2] | (h[3] << 16))};
+            } else {
+                *(v4i *)(g + 4 * (size_t)q) = o;
+            }
+        }
+        done = nq * 4;
     }
-    if (bad) raise_flag(flags, FLAG_OVERFLOW);
+    for (uint32_t i = done + t0; i < count; i += stride) {
+        const int32_t v = relu_bwd32<TR>(delta[i], code[i], rp);
+        const uint32_t a = abs_u32(v);
+        mx = a > mx ? a : mx;
+        if (g16) {
+            const bool esc = v < -G16_MAX || v > G16_MAX;
+            if (esc) g[i] = v;
+            g16[i] = esc ? G16_ESC : (int16_t)v;
+        } else {
+            g[i] = v;
+        }
+    }
     if (gmax) block_slot_max(gmax, mx);
 }
 
 void launch_unpool_relu_bwd(hipStream_t s, int n, int h, int w, int c, bool pool,
                             const int32_t *delta, const uint8_t *code, const Relu &rp,
-                            int32_t *g, uint32_t *gmax, uint32_t *flags)
+                            int32_t *g, uint32_t *gmax, uint32_t *flags, int16_t *g16)
 {
     if (pool) {
         int64_t total = (int64_t)n * (h / 2) * (w / 2) * c;
         hipLaunchKernelGGL(k_unpool_relu_bwd, dim3(grid_stride_blocks(total)), dim3(256), 0, s,
                            n, h, w, c, delta, code, rp, g, gmax, flags);
     } else {
-        int64_t total = (int64_t)n * h * w * c;
-        hipLaunchKernelGGL(k_relu_bwd, dim3(grid_stride_blocks(total)), dim3(256), 0, s,
-                           (uint32_t)total, delta, code, rp, g, gmax, flags);
+        const int64_t total = (int64_t)n * h * w * c;
+        const int vec = (((uintptr_t)delta | (uintptr_t)code | (uintptr_t)g | (uintptr_t)g16) & 15) == 0;
+        const unsigned nb = grid_stride_blocks(vec ? (total + 3) / 4 : total);
+        if (rp.alpha.trunc)
+            hipLaunchKernelGGL(k_relu_bwd<true>, dim3(nb), dim3(256), 0, s, (uint32_t)total, delta, code, rp,
+                               g, g16, gmax, vec);
+        else
+            hipLaunchKernelGGL(k_relu_bwd<false>, dim3(nb), dim3(256), 0, s, (uint32_t)total, delta, code,
+                               rp, g, g16, gmax, vec);
     }
 }
 

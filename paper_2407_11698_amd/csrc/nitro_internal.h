@@ -477,9 +477,10 @@ void launch_linear_dw(hipStream_t s, int n, int k, int m, const int32_t *e, cons
                       int64_t *dw);
 // gradient at the block output -> gradient at the last layer's pre-activation; max|g| -> *gmax
 // (when not null).
+// g16 (not pooled): g in the escaped 16-bit form below (g then receives only the escapes).
 void launch_unpool_relu_bwd(hipStream_t s, int n, int h, int w, int c, bool pool,
                             const int32_t *delta, const uint8_t *code, const Relu &rp,
-                            int32_t *g, uint32_t *gmax, uint32_t *flags);
+                            int32_t *g, uint32_t *gmax, uint32_t *flags, int16_t *g16 = nullptr);
 // conv input gradient; with `code` applies ReLU' of the previous layer and writes int32 `out`
 // (overflow flagged, max|out| -> *gmax when not null); with out64 writes the raw int64 sum.
 void launch_conv_dx(hipStream_t s, const ConvShape &sh, const int32_t *g, const int32_t *w,

@@ -162,7 +162,9 @@ def test_vgg_full_batch_every_tensor(ctx):
 
 def test_conv_stress_full_size_twenty_repeats(ctx):
     """256x256x32x32, conv 256 -> 256, fixed activations and error signal, twenty cumulative
-    repeats with IntegerSGD between them (the weights leave int8 after the first)."""
+    repeats with IntegerSGD between them (the weights leave int8 after the first). g is tapped on
+    even repeats only: untapped, the library passes it to the weight-gradient preparation in 16
+    bits (as in the bench's repeats)."""
     wl = WL.CONV_STRESS
     dg = load_digests("digests_conv_stress.json")
     assert dg["workload"] == wl.name and dg["batch"] == wl.batch
@@ -177,12 +179,13 @@ def test_conv_stress_full_size_twenty_repeats(ctx):
     code = st.state[off:off + st.a.numel()].view(st.a.shape)
     for r, exp in enumerate(dg["steps"]):
         print("repeat", r, flush=True)
-        st.repeat(xd, dd, taps={"g": [g]})
+        st.repeat(xd, dd, taps={"g": [g]} if r % 2 == 0 else None)
         ctx.sync()
         where = "repeat %d" % r
         check(exp, "a", st.a, where)
         check(exp, "code", code, where)
-        check(exp, "g", g, where)
+        if r % 2 == 0:
+            check(exp, "g", g, where)
         check(exp, "dw", st.dw, where)
         check(exp, "dx", st.dx, where)
         check(exp, "w", st.w, where)
