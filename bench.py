@@ -92,13 +92,14 @@ def limbs_for(m: int) -> int:
     return 1 if m <= 127 else 2 if m <= 32639 else 3 if m <= 8355711 else 4
 
 
-# The library's input gradient takes g in two limbs plus an offset correction when
-# 32639 < max|g| <= 32768 and at most this many entries of g equal 32768 (three limbs otherwise).
+# The library's input and weight gradients of the single layer take g in two limbs plus an
+# offset correction when 32639 < max|g| <= 32768 and at most this many entries of g equal 32768
+# (three limbs otherwise).
 G_OFFSET_CAP = 16384
 
 
-def dx_g_limbs(g) -> int:
-    """Limb passes over g of the first layer's int64 input gradient."""
+def offset_g_limbs(g) -> int:
+    """Limb passes over g of the single layer's input and weight gradients."""
     m = int(g.abs().max().item())
     if 32639 < m <= 32768 and int((g == 32768).sum().item()) <= G_OFFSET_CAP:
         return 2
@@ -117,7 +118,7 @@ def stress_layer(reps: int):
     Algorithmic ops count each GEMM once (2 x N*H*W*C_out*9*C_in, three GEMMs per repeat); MFMA
     ops count every limb pass the kernel executes, from the repeat's own max|W| and g (the input
     gradient's kernel time excludes the two small kernels of g's offset form, which the whole
-    repeat includes). The
+    repeat includes; the weight gradient's, the split-K sums and their offset term). The
     weights leave int8 after the first repeat, so repeat 1 and the steady state (median over the
     later repeats) are reported separately."""
     import torch
@@ -156,9 +157,9 @@ def stress_layer(reps: int):
         st.ctx.kernel_timing(True)
         if not torch.equal(st.w, w_after):
             raise RuntimeError("stress repeat %d: the replay's weights differ" % r)
-        lg = limbs_for(int(g.abs().max().item()))
+        lg = offset_g_limbs(g)
         per.append({"ms": e0.elapsed_time(e1), "kernels_ms": kt,
-                    "passes": {"k_conv_tile<fwd>": lw, "k_conv_tile<dx>": dx_g_limbs(g) * lw,
+                    "passes": {"k_conv_tile<fwd>": lw, "k_conv_tile<dx>": lg * lw,
                                "k_conv_dw_planes": lg}})
     st.ctx.kernel_timing(False)
 

@@ -220,7 +220,8 @@ struct BlockGeom {
     size_t lf, lfc;                // learning-pooled block output and its window indices
     size_t yhat, e, delta, g0, g1;
     size_t g16;                    // an inner layer's gradient in the escaped 16-bit form
-    size_t gres, gbias;            // the first layer's g in the offset form: residual list, bias
+    size_t gres, gbias, gxq;       // the first layer's g in the offset form: residual list, bias
+                                   // table, sums of x (weight gradient in the form too)
     size_t total;
 };
 
@@ -351,6 +352,7 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     const bool goff = conv && g->L[0].dx_tile && dwp_ok(g->L[0].sh);
     g->gres = off;  off = align256(off + (goff ? (size_t)GOFF_CAP * 4 : 0));
     g->gbias = off; off = align256(off + (goff ? (size_t)16 * 8 * g->L[0].sh.c : 0));
+    g->gxq = off;   off = align256(off + (goff && dwp_goff_ok(g->L[0].sh) ? (size_t)9 * 4 * g->L[0].sh.c : 0));
     g->total = off;
     return NITRO_OK;
 }
@@ -462,6 +464,14 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
     // by this call
     if (zero_slots && hipMemsetAsync(slots + 4 * SLOT_WORDS, 0, 7 * SLOT_WORDS * 4, s) != hipSuccess)
         return NITRO_EHIP;
+    // the offset form of g (the first layer's int64 input gradient on the tile, a block call):
+    // its count is slot 10's first word; the weight gradient joins where its shape allows
+    const LayerGeom &L0 = g.L[0];
+    const bool goff0 = zero_slots && taps && taps->dx && L0.conv && L0.dx_tile && dwp_ok(L0.sh);
+    const bool goff_dw0 = goff0 && dwp_goff_ok(L0.sh);
+    const GOff go{slots + 10 * SLOT_WORDS, (uint32_t *)at(state, g.gres), (int64_t *)at(state, g.gbias),
+                  goff_dw0 ? (int32_t *)at(state, g.gxq) : nullptr};
+    if (goff_dw0 && hipMemsetAsync(go.xq, 0, (size_t)9 * 4 * L0.sh.c, s) != hipSuccess) return NITRO_EHIP;
     bool have_g = false;
     // The last layer's g left pooled by the learning layer and un-pooled by the weight-gradient
     // planes, which then give every other reader its values: a pooled conv block on the MFMA
@@ -541,9 +551,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
         const LayerGeom &L = g.L[j];
         const int8_t *xin = j == 0 ? x : (const int8_t *)at(state, g.act[j - 1]);
         const int32_t *gj = gb[cur];
-        // the first layer's int64 input gradient on the tile: g may go in the offset form
-        const bool goff = j == 0 && taps && taps->dx && L.conv && L.dx_tile && dwp_ok(L.sh);
-        const GOff go{slots + 10 * SLOT_WORDS, (uint32_t *)at(state, g.gres), (int64_t *)at(state, g.gbias)};
+        const bool goff = j == 0 && goff0;
         if (L.conv) {
             const bool need_dx = j > 0 || (taps && taps->dx);
             if (dwp_ok(L.sh))
@@ -597,7 +605,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                                         (const int8_t *)at(state, g.wt[j]), slots + j * SLOT_WORDS,
                                         code, rp, dst, dst64, gmax_out, ctx->flags, dst16,
                                         goff ? &go : nullptr);
-                    if (goff) launch_goff_fix(s, L.sh, go, p->w[j], dst64);
+                    if (goff) launch_goff_fix(s, L.sh, go, p->w[j], dst64, xin, goff_dw0 ? gr->dw[j] : nullptr);
                 } else if (mfma_conv_dx_ok(L.sh))
                     launch_conv_dx_mfma(s, L.sh, gj, slots + (4 + j) * SLOT_WORDS, (const int8_t *)at(state, g.wt[j]),
                                         slots + (j) * SLOT_WORDS, code, rp, dst, dst64, gmax_out, ctx->flags);

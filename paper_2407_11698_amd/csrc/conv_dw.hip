@@ -176,13 +176,16 @@ __device__ void dwp_grad_planes(const int32_t *__restrict__ g, const int16_t *__
                                 int n, int h, int w, int c, int hp,
                                 int wp, int kp, const uint32_t *gmax,
                                 const uint8_t *__restrict__ pcode, int8_t *__restrict__ gp,
-                                int8_t *__restrict__ gn, const GOff &go, bool goff, int bx, int by)
+                                int8_t *__restrict__ gn, const GOff &go, bool goff_dx,
+                                bool goff_dw, int bx, int by)
 {
     __shared__ int32_t T[64][65];        // [position][channel]
     const uint32_t gm = slot_read(gmax);
     const int LA = limbs_for(gm);
     if (LA > 4) return;                  // the weight-gradient kernel flags it
-    const bool off = goff && goff_range(gm);
+    const bool off_n = goff_dx && goff_range(gm);   // gn in the offset form
+    const bool off_p = goff_dw && goff_range(gm);   // gp in the offset form
+    const bool off = off_n || off_p;
     const int tid = threadIdx.x;
     uint32_t rmask = 0;                  // offset form: this thread's entries with g = 32768
     const int k0 = bx * 64;
@@ -221,17 +224,21 @@ __device__ void dwp_grad_planes(const int32_t *__restrict__ g, const int16_t *__
                     for (int e = 0; e < 4; e++) x[e] = ((cd >> (8 * e)) & 3u) == win ? x[e] : 0;
                 }
             }
+            // (gp in the offset form: g - 128 at the image's pixels, pad positions stay zero)
+            const int32_t obp = off_p && pix >= 0 && ch < c ? GOFF_BIAS : 0;
 #pragma unroll
             for (int e = 0; e < 4; e++) {
                 v[4 * u + e] = x[e];
-                T[pi][16 * cq + 4 * u + e] = x[e];
+                T[pi][16 * cq + 4 * u + e] = x[e] - obp;
             }
+        }
+        if (off && pix >= 0) {
+#pragma unroll
+            for (int e = 0; e < 16; e++) rmask |= v[e] >= 32768 ? 1u << e : 0u;
         }
         if (gn && pix >= 0 && c0 + 16 * cq < c) {
             const int64_t P = (int64_t)n * h * w;
-            const int32_t ob = off ? GOFF_BIAS : 0;
-#pragma unroll
-            for (int e = 0; e < 16; e++) rmask |= (off && v[e] >= 32768) ? 1u << e : 0u;
+            const int32_t ob = off_n ? GOFF_BIAS : 0;
 #pragma unroll
             for (int l = 0; l < 4; l++) {
                 if (l < LA) {
@@ -289,8 +296,56 @@ __device__ void dwp_grad_planes(const int32_t *__restrict__ g, const int16_t *__
     }
 }
 
-// The two independent preparations of a weight-gradient launch in one launch: workgroups
-// 0 .. rows_gx rows_gy - 1 write x's rows (or zero their pad positions), the rest g's planes.
+// Sums of x for the weight gradient's offset form: workgroup (image img, channels 64 cb ..
+// 64 cb + 63) adds x over the image's pixels, its rows h = 0 and H-1, columns w = 0 and W-1 and
+// four corners into xq [9][c] (atomic adds; xq is zero before). Thread: 4 channels (tid % 16),
+// pixels tid / 16 + 16 k; the 16 pixel lanes reduced by shuffles within a wave, the waves in
+// LDS. Nothing unless max|g| is in the offset range.
+__device__ void dwp_xsums(const int8_t *__restrict__ x, int h, int w, int c, const uint32_t *gmax,
+                          int32_t *xq, int img, int cb)
+{
+    __shared__ int32_t red[4][16][36];
+    if (!goff_range(slot_read(gmax))) return;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int cq = tid & 15, pl = tid >> 4;
+    const int hw = h * w;
+    const int8_t *base = x + (int64_t)img * hw * c + 64 * cb + 4 * cq;
+    int32_t a[36];
+#pragma unroll
+    for (int k = 0; k < 36; k++) a[k] = 0;
+    for (int p = pl; p < hw; p += 16) {
+        const uint32_t v = *(const uint32_t *)(base + (int64_t)p * c);
+        const int y = p / w, xx = p - y * w;
+        const bool top = y == 0, bot = y == h - 1, lft = xx == 0, rgt = xx == w - 1;
+        const bool on[9] = {true, top, bot, lft, rgt, top && lft, top && rgt, bot && lft, bot && rgt};
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            const int32_t b = (int8_t)(v >> (8 * e));
+#pragma unroll
+            for (int qn = 0; qn < 9; qn++) a[4 * qn + e] += on[qn] ? b : 0;
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < 36; k++) {
+        a[k] += __shfl_xor(a[k], 16, 64);
+        a[k] += __shfl_xor(a[k], 32, 64);
+    }
+    if (lane < 16) {
+#pragma unroll
+        for (int k = 0; k < 36; k++) red[wave][lane][k] = a[k];
+    }
+    __syncthreads();
+    for (int o = tid; o < 9 * 64; o += 256) {
+        const int qn = o >> 6, cc = o & 63;
+        const int k = 4 * qn + (cc & 3);
+        const int32_t sum = red[0][cc >> 2][k] + red[1][cc >> 2][k] + red[2][cc >> 2][k] + red[3][cc >> 2][k];
+        if (sum) atomicAdd(xq + qn * c + 64 * cb + cc, sum);
+    }
+}
+
+// The independent preparations of a weight-gradient launch in one launch: workgroups
+// 0 .. xs_n - 1 the sums of x for the offset form (if asked for), then x's rows (or zeros at
+// their pad positions), then g's planes.
 struct DwpPrep {
     int rows;                    // 1: x rows from x; 2: zeros at the pad positions of rows
                                  //    written by the previous layer's forward
@@ -304,14 +359,21 @@ struct DwpPrep {
     const uint32_t *gmax;
     const uint8_t *pcode;
     int8_t *gp, *gn;
-    GOff go;                     // with goff: gn may take the offset form
-    int goff;
+    GOff go;                     // offset form: gn (goff_dx), gp and the sums of x (goff_dw)
+    int goff_dx, goff_dw;
+    int xs_n;                    // sum workgroups: n (C / 64)
 };
 
 __global__ __launch_bounds__(256) void k_dwp_prep(DwpPrep a)
 {
     const int nrows = a.rows_gx * a.rows_gy;
-    const int b = blockIdx.x;
+    int b = blockIdx.x;
+    if (b < a.xs_n) {
+        const int nb = a.c / 64;
+        dwp_xsums(a.x, a.h, a.w, a.c, a.gmax, a.go.xq, b / nb, b % nb);
+        return;
+    }
+    b -= a.xs_n;
     if (b < nrows) {
         const int bx = b % a.rows_gx, by = b / a.rows_gx;
         if (a.rows == 1) dwp_act_rows(a.x, a.n, a.h, a.w, a.c, a.hp, a.wp, (int)a.xs, a.xr, bx, by);
@@ -320,7 +382,7 @@ __global__ __launch_bounds__(256) void k_dwp_prep(DwpPrep a)
     }
     const int q = b - nrows;
     dwp_grad_planes(a.g, a.g16, a.n, a.h, a.w, a.co, a.hp, a.wp, a.kp, a.gmax, a.pcode, a.gp, a.gn,
-                    a.go, a.goff != 0, q % a.gp_gx, q / a.gp_gx);
+                    a.go, a.goff_dx != 0, a.goff_dw != 0, q % a.gp_gx, q / a.gp_gx);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -336,6 +398,9 @@ struct DwpArgs {
     int64_t *out;          // [nsplit][co][9][ci_out]; dW itself when there is one split
     uint32_t *flags;
     uint64_t *ts;          // timing slot (null: untimed)
+    // g's planes may be in the offset form (two limbs, or three with more than GOFF_CAP entries)
+    int goff;
+    const uint32_t *goff_count;
 };
 
 // Transposing LDS read (gfx950 ds_read_b64_tr_b8). Within each group of 16 lanes, output lane
@@ -360,7 +425,12 @@ __global__ __launch_bounds__(256) void k_conv_dw_planes(DwpArgs p)
     ts_start(p.ts);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar)
-    const int LA = limbs_for(slot_read(p.gmax));
+    // (the offset form's residual count read whether or not it is used, from the max slot then,
+    // so that both loads are in flight together)
+    const uint32_t rn = *(p.goff ? p.goff_count : p.gmax);
+    const uint32_t gm = slot_read(p.gmax);
+    const bool goff = p.goff && goff_range(gm);
+    const int LA = goff ? (rn <= GOFF_CAP ? 2 : 3) : limbs_for(gm);
     if (LA > 4) {
         if (tid == 0) raise_flag(p.flags, FLAG_OVERFLOW);
         return;
@@ -583,11 +653,12 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
         pa.x = x; pa.n = sh.n; pa.h = sh.h; pa.w = sh.w; pa.c = sh.c; pa.co = sh.co;
         pa.hp = ge.hp; pa.wp = ge.wp; pa.kp = (int)ge.kp; pa.kraw = ge.kraw; pa.xs = ge.xs; pa.xr = xp;
         pa.g = g; pa.g16 = g16; pa.gmax = gmax; pa.pcode = pool_code; pa.gp = gp; pa.gn = gn;
-        if (goff && gn) {
-            pa.go = *goff;
-            pa.goff = 1;
-        }
-        const int64_t nwg = (int64_t)pa.rows_gx * pa.rows_gy + (int64_t)pa.gp_gx * ((sh.co + 63) / 64);
+        const bool goff_dw = goff && goff->xq && dwp_goff_ok(sh);
+        if (goff) pa.go = *goff;
+        pa.goff_dx = goff && gn;
+        pa.goff_dw = goff_dw;
+        pa.xs_n = goff_dw ? sh.n * (sh.c / 64) : 0;
+        const int64_t nwg = pa.xs_n + (int64_t)pa.rows_gx * pa.rows_gy + (int64_t)pa.gp_gx * ((sh.co + 63) / 64);
         hipLaunchKernelGGL(k_dwp_prep, dim3((unsigned)nwg), dim3(256), 0, s, pa);
     }
     DwpArgs a{};
@@ -598,6 +669,11 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
     a.gmax = gmax;
     a.out = pl.nsplit > 1 ? part : dw;
     a.flags = flags;
+    const bool goff_dw = goff && goff->xq && dwp_goff_ok(sh);
+    if (goff_dw) {
+        a.goff = 1;
+        a.goff_count = goff->count;
+    }
     const size_t lds_stage = (size_t)4 * 2 * DWP_WIN * 16, lds_red = (size_t)4 * 3 * 1024 * 4;
     const unsigned nwg = (unsigned)(pl.tiles_co * pl.tiles_ci * pl.nsplit);
     a.ts = timer_slot(TIMED_DW);
@@ -609,7 +685,15 @@ void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
         else
             hipLaunchKernelGGL(k_conv_dw_planes<false>, dim3(nwg), dim3(256), lds, s, a);
     }
-    if (pl.nsplit > 1) launch_sum_partials(s, part, pl.nsplit, (int64_t)sh.co * 9 * sh.c, dw);
+    if (goff_dw)
+        launch_sum_partials_goff(s, part, pl.nsplit, (int64_t)sh.co * 9 * sh.c, dw, goff->xq, sh.c, gmax);
+    else if (pl.nsplit > 1)
+        launch_sum_partials(s, part, pl.nsplit, (int64_t)sh.co * 9 * sh.c, dw);
+}
+
+bool dwp_goff_ok(const ConvShape &sh)
+{
+    return dwp_ok(sh) && sh.c % 64 == 0 && dwp_plan(sh).nsplit > 1;
 }
 
 }  // namespace nitro

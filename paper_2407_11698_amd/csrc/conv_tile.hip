@@ -926,11 +926,13 @@ void launch_goff_bias(hipStream_t s, const int8_t *wt, int co, int ci, const uin
 }
 
 // Entry (g = 32768 at pixel p, channel o, its third limb 1): dx[p + (r-1, s-1)][ci] +=
-// 65536 W[o][r][s][ci] for the taps whose pixel is inside the image (atomic adds: entries near
-// each other reach the same outputs). Workgroups take entries e = blockIdx.x + gridDim.x k,
-// threads the input channels; a thread's nine W values are loaded before its adds.
+// 65536 W[o][r][s][ci] for the taps whose pixel is inside the image, and (dw) dW[o][r][s][ci] +=
+// 65536 x[p + (r-1, s-1)][ci] for the same taps (atomic adds: entries near each other reach the
+// same outputs). Workgroups take entries e = blockIdx.x + gridDim.x k, threads the input
+// channels; a thread's nine W (or x) values are loaded before its adds.
 __global__ __launch_bounds__(256) void k_goff_fix(GOff go, const int32_t *__restrict__ w, int h,
-                                                  int wd, int co, int ci, int64_t *__restrict__ dx)
+                                                  int wd, int co, int ci, int64_t *__restrict__ dx,
+                                                  const int8_t *__restrict__ x, int64_t *__restrict__ dw)
 {
     const uint32_t cnt = *go.count;
     if (cnt == 0 || cnt > GOFF_CAP) return;
@@ -939,26 +941,41 @@ __global__ __launch_bounds__(256) void k_goff_fix(GOff go, const int32_t *__rest
         const uint32_t idx = go.list[e];
         const uint32_t pix = idx / (uint32_t)co, o = idx - pix * (uint32_t)co;
         const uint32_t img = pix / hw, rem = pix - img * hw;
-        const int y = (int)(rem / (uint32_t)wd), x = (int)(rem - (uint32_t)y * (uint32_t)wd);
+        const int y = (int)(rem / (uint32_t)wd), xc = (int)(rem - (uint32_t)y * (uint32_t)wd);
+        bool in[9];
+        int64_t q[9];
+#pragma unroll
+        for (int t = 0; t < 9; t++) {
+            const int qy = y + t / 3 - 1, qx = xc + t % 3 - 1;
+            in[t] = qy >= 0 && qy < h && qx >= 0 && qx < wd;
+            q[t] = ((int64_t)img * h + qy) * wd + qx;
+        }
         for (int c = threadIdx.x; c < ci; c += 256) {
-            int64_t v[9];
+            if (dx) {
+                int64_t v[9];
 #pragma unroll
-            for (int t = 0; t < 9; t++) v[t] = (int64_t)w[((int64_t)o * 9 + t) * ci + c] * 65536;
+                for (int t = 0; t < 9; t++) v[t] = (int64_t)w[((int64_t)o * 9 + t) * ci + c] * 65536;
 #pragma unroll
-            for (int t = 0; t < 9; t++) {
-                const int qy = y + t / 3 - 1, qx = x + t % 3 - 1;
-                if (qy >= 0 && qy < h && qx >= 0 && qx < wd)
-                    atomicAdd((unsigned long long *)(dx + (((int64_t)img * h + qy) * wd + qx) * ci + c),
-                              (unsigned long long)v[t]);
+                for (int t = 0; t < 9; t++)
+                    if (in[t]) atomicAdd((unsigned long long *)(dx + q[t] * ci + c), (unsigned long long)v[t]);
+            }
+            if (dw) {
+                int64_t v[9];
+#pragma unroll
+                for (int t = 0; t < 9; t++) v[t] = in[t] ? (int64_t)x[q[t] * ci + c] * 65536 : 0;
+#pragma unroll
+                for (int t = 0; t < 9; t++)
+                    if (v[t]) atomicAdd((unsigned long long *)(dw + ((int64_t)o * 9 + t) * ci + c), (unsigned long long)v[t]);
             }
         }
     }
 }
 
 void launch_goff_fix(hipStream_t s, const ConvShape &sh, const GOff &go, const int32_t *w,
-                     int64_t *dx)
+                     int64_t *dx, const int8_t *x, int64_t *dw)
 {
-    hipLaunchKernelGGL(k_goff_fix, dim3(1024), dim3(256), 0, s, go, w, sh.h, sh.w, sh.co, sh.c, dx);
+    hipLaunchKernelGGL(k_goff_fix, dim3(1024), dim3(256), 0, s, go, w, sh.h, sh.w, sh.co, sh.c, dx,
+                       x, dw);
 }
 
 }  // namespace nitro

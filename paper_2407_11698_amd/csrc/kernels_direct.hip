@@ -51,6 +51,59 @@ void launch_sum_partials(hipStream_t s, const int64_t *part, int nz, int64_t cou
                        nz, count, out);
 }
 
+// Split-K sums of a conv weight gradient [co][3][3][ci] whose planes may hold g - 128 (offset
+// form, max|g| in its range): output (o, r, s, c) then adds 128 S with
+// S = sum_{p inside the image} x[p + (r-1, s-1)][c], from the sums xq [9][ci] of x over every
+// pixel, the rows h = 0 and H-1, the columns w = 0 and W-1 and the four corners by
+// inclusion-exclusion: the tap excludes row 0 when r = 2 (no p above it), row H-1 when r = 0,
+// column 0 when s = 2, column W-1 when s = 0.
+__global__ __launch_bounds__(256) void k_sum_partials_goff(const int64_t *__restrict__ part, int nz,
+                                                           int64_t count, int64_t *__restrict__ out,
+                                                           const int32_t *__restrict__ xq, int ci,
+                                                           const uint32_t *gmax)
+{
+    __shared__ int64_t red[4][64];
+    const bool off = goff_range(slot_read(gmax));
+    const int il = threadIdx.x & 63, q = threadIdx.x >> 6;
+    const int64_t i = (int64_t)blockIdx.x * 64 + il;
+    int64_t v = 0;
+    if (i < count) {
+        int z = q;
+        for (; z + 12 < nz; z += 16)
+            v += part[(int64_t)z * count + i] + part[(int64_t)(z + 4) * count + i] +
+                 part[(int64_t)(z + 8) * count + i] + part[(int64_t)(z + 12) * count + i];
+        for (; z < nz; z += 4) v += part[(int64_t)z * count + i];
+    }
+    red[q][il] = v;
+    __syncthreads();
+    if (q != 0 || i >= count) return;
+    int64_t sum = red[0][il] + red[1][il] + red[2][il] + red[3][il];
+    if (off) {
+        const int c = (int)(i % ci), t = (int)((i / ci) % 9);
+        const int r = t / 3, sc = t % 3;
+        const int32_t *Q = xq + c;
+        int64_t S = Q[0];
+        if (r == 2) S -= Q[ci];                       // row 0
+        if (r == 0) S -= Q[2 * ci];                   // row H-1
+        if (sc == 2) S -= Q[3 * ci];                  // column 0
+        if (sc == 0) S -= Q[4 * ci];                  // column W-1
+        if (r == 2 && sc == 2) S += Q[5 * ci];        // (0, 0)
+        if (r == 2 && sc == 0) S += Q[6 * ci];        // (0, W-1)
+        if (r == 0 && sc == 2) S += Q[7 * ci];        // (H-1, 0)
+        if (r == 0 && sc == 0) S += Q[8 * ci];        // (H-1, W-1)
+        sum += (int64_t)GOFF_BIAS * S;
+    }
+    out[i] = sum;
+}
+
+void launch_sum_partials_goff(hipStream_t s, const int64_t *part, int nz, int64_t count,
+                              int64_t *out, const int32_t *xq, int ci, const uint32_t *gmax)
+{
+    if (count <= 0) return;
+    hipLaunchKernelGGL(k_sum_partials_goff, dim3((unsigned)((count + 63) / 64)), dim3(256), 0, s, part,
+                       nz, count, out, xq, ci, gmax);
+}
+
 // ---------------------------------------------------------------------------------------------
 // Direct 3x3 conv, stride 1, zero padding 1: z[n][h][w][co] = sum_{r,s,ci} x[..][h+r-1][w+s-1][ci]
 // * W[co][r][s][ci], then NITRO-Scaling and NITRO-ReLU.

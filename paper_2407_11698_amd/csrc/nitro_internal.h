@@ -452,6 +452,10 @@ struct ConvShape {
 void launch_fill_i64(hipStream_t s, int64_t *p, int64_t count);
 // out[i] = sum_{z < nz} part[z * count + i]  (split-K partial sums, fixed order)
 void launch_sum_partials(hipStream_t s, const int64_t *part, int nz, int64_t count, int64_t *out);
+// The same for a conv weight gradient [co][9][ci] whose g may be in the offset form: when
+// max|g| (gmax) is in the offset range, each output adds the offset's term from xq.
+void launch_sum_partials_goff(hipStream_t s, const int64_t *part, int nz, int64_t count,
+                              int64_t *out, const int32_t *xq, int ci, const uint32_t *gmax);
 
 // forward conv + Scaling + ReLU; POOL variant writes the pooled output and per pooled element
 // code = argmax | region << 2; the plain variant writes the full-resolution output and region.
@@ -594,7 +598,8 @@ int64_t dwp_rows_stride(const ConvShape &sh);   // xs
 // pool_code (a pooled layer's codes, [n][h/2][w/2][co]): g is given at the pooled positions only
 // (launch_learning_mfma with g_pooled) and each window's argmax takes the value
 // g16: g in the escaped 16-bit form (g then holds the escaped values only).
-// goff (with gn): gn may take the offset form below.
+// goff: gn (if any) may take the offset form below, and with goff->xq (dwp_goff_ok) the weight
+// gradient too.
 struct GOff;
 void launch_conv_dw_planes(hipStream_t s, const ConvShape &sh, const int32_t *g,
                            const uint32_t *gmax, const int8_t *x, int8_t *gp, int8_t *xp,
@@ -622,15 +627,22 @@ struct GOff {
     uint32_t *list;        // [GOFF_CAP] their indices p co + c in g
     int64_t *bias;         // [16][ci]: the offset's term for border class
                            // (h == 0) | (h == H-1) << 1 | (w == 0) << 2 | (w == W-1) << 3
+    int32_t *xq;           // (weight gradient in the form too) [9][ci], zero before the
+                           // preparation: x summed over every pixel, over the rows h = 0 and
+                           // h = H-1, the columns w = 0 and w = W-1, and the four corners
 };
+// The weight gradient takes the offset form too where the layer's shape allows it (C_in a
+// multiple of 64, split-K): its planes hold g - 128, the split-K sums add
+// 128 sum_{p inside} x[p + (r-1, s-1)][ci] (from xq) and the fix adds 65536 x rows per entry.
+bool dwp_goff_ok(const ConvShape &sh);
 // The bias table from W's input-gradient limb planes wt [4][ci][9 co] (the workgroups return
 // at once unless max|g| is in the offset range).
 void launch_goff_bias(hipStream_t s, const int8_t *wt, int co, int ci, const uint32_t *gmax,
                       int64_t *bias);
-// The listed entries' 65536 W terms added into dx int64 NHWC [n][h][w][ci] (nothing unless
-// 0 < count <= GOFF_CAP).
+// The listed entries' 65536 W terms added into dx int64 NHWC [n][h][w][ci] and (dw not null)
+// their 65536 x terms into dW int64 KRSC (nothing unless 0 < count <= GOFF_CAP).
 void launch_goff_fix(hipStream_t s, const ConvShape &sh, const GOff &go, const int32_t *w,
-                     int64_t *dx);
+                     int64_t *dx, const int8_t *x = nullptr, int64_t *dw = nullptr);
 
 // ---- implicit-GEMM conv with the input tile staged once (conv_tile.hip)
 bool tile_conv_fwd_ok(const ConvShape &sh, bool pool, int64_t sf, int alpha_inv);

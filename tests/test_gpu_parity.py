@@ -283,7 +283,8 @@ def test_conv_block_inner_g16(ctx, case, modes):
 
 # The first layer's int64 input gradient with g one value past two limbs (32639 < max|g| <=
 # 32768): the library takes g - 128 in two limbs, adds the offset's term per border class and
-# corrects each g = 32768 from a list (more than 16384 of them: three limbs instead). The given
+# corrects each g = 32768 from a list (more than 16384 of them: three limbs instead); so does the
+# weight gradient where it is split (C_in a multiple of 64), with x's window sums as the term. The given
 # delta is drawn in [-32767, 32767] and then set to 32768 at `plus` positions where NITRO-ReLU
 # passes it unchanged (z* in [0, 127]) and to -32768 at 5 such positions; top = 32769 puts one
 # 32769 there instead (outside the offset range), top = 32000 draws no edit at all.
@@ -299,6 +300,11 @@ G_OFFSET_CASES = [
     (2, 8, 8, [16, 32], True, 0, 32768),
     (4, 16, 16, [64, 64], False, 7, 32769),
     (4, 16, 16, [64, 64], False, 0, 32000),
+    # split-K weight gradients with C_in % 64 == 0: the weight gradient takes the form too
+    (16, 16, 16, [64, 64], False, 0, 32768),
+    (16, 16, 16, [64, 64], False, 11, 32768),
+    (8, 32, 32, [128, 64], False, 200, 32768),
+    (16, 16, 16, [64, 64], False, 20000, 32768),
 ]
 
 
