@@ -177,19 +177,18 @@ __device__ void dwp_grad_planes(const int32_t *__restrict__ g, const int16_t *__
                                 int wp, int kp, const uint32_t *gmax,
                                 const uint8_t *__restrict__ pcode, int8_t *__restrict__ gp,
                                 int8_t *__restrict__ gn, const GOff &go, bool goff_dx,
-                                bool goff_dw, int bx, int by)
+                                bool goff_dw, int bx, int by, int32_t *lds)
 {
-    __shared__ int32_t T[64][65];        // [position][channel]
-    const uint32_t gm = slot_read(gmax);
-    const int LA = limbs_for(gm);
-    if (LA > 4) return;                  // the weight-gradient kernel flags it
-    const bool off_n = goff_dx && goff_range(gm);   // gn in the offset form
-    const bool off_p = goff_dw && goff_range(gm);   // gp in the offset form
-    const bool off = off_n || off_p;
+    int32_t(*T)[65] = (int32_t(*)[65])lds;   // [64 positions][64 channels + 1]
     const int tid = threadIdx.x;
+    // the max slot's word is requested with g's loads and reduced after them
+    const uint32_t sw = gmax[tid & 63];
     uint32_t rmask = 0;                  // offset form: this thread's entries with g = 32768
     const int k0 = bx * 64;
     const int c0 = by * 64;
+    uint32_t gm = 0;
+    int LA = 0;
+    bool off_n = false, off_p = false, off = false;
     {
         const int pi = tid >> 2, cq = tid & 3;
         const int pix = padded_pixel(k0 + pi, n, h, w, hp, wp);
@@ -224,13 +223,22 @@ __device__ void dwp_grad_planes(const int32_t *__restrict__ g, const int16_t *__
                     for (int e = 0; e < 4; e++) x[e] = ((cd >> (8 * e)) & 3u) == win ? x[e] : 0;
                 }
             }
-            // (gp in the offset form: g - 128 at the image's pixels, pad positions stay zero)
-            const int32_t obp = off_p && pix >= 0 && ch < c ? GOFF_BIAS : 0;
 #pragma unroll
-            for (int e = 0; e < 4; e++) {
-                v[4 * u + e] = x[e];
-                T[pi][16 * cq + 4 * u + e] = x[e] - obp;
-            }
+            for (int e = 0; e < 4; e++) v[4 * u + e] = x[e];
+        }
+        gm = wave_max_u32(sw);
+        LA = limbs_for(gm);
+        if (LA > 4) return;              // the weight-gradient kernel flags it
+        off_n = goff_dx && goff_range(gm);   // gn in the offset form
+        off_p = goff_dw && goff_range(gm);   // gp in the offset form
+        off = off_n || off_p;
+        // (gp in the offset form: g - 128 at the image's pixels, pad positions stay zero)
+        const int32_t obp = off_p && pix >= 0 ? GOFF_BIAS : 0;
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            const int32_t ob = c0 + 16 * cq + 4 * u < c ? obp : 0;
+#pragma unroll
+            for (int e = 0; e < 4; e++) T[pi][16 * cq + 4 * u + e] = v[4 * u + e] - ob;
         }
         if (off && pix >= 0) {
 #pragma unroll
@@ -302,9 +310,9 @@ __device__ void dwp_grad_planes(const int32_t *__restrict__ g, const int16_t *__
 // pixels tid / 16 + 16 k; the 16 pixel lanes reduced by shuffles within a wave, the waves in
 // LDS. Nothing unless max|g| is in the offset range.
 __device__ void dwp_xsums(const int8_t *__restrict__ x, int h, int w, int c, const uint32_t *gmax,
-                          int32_t *xq, int img, int cb)
+                          int32_t *xq, int img, int cb, int32_t *lds)
 {
-    __shared__ int32_t red[4][16][36];
+    int32_t(*red)[16][36] = (int32_t(*)[16][36])lds;   // [4 waves][16 lanes][36]
     if (!goff_range(slot_read(gmax))) return;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int cq = tid & 15, pl = tid >> 4;
@@ -366,11 +374,12 @@ struct DwpPrep {
 
 __global__ __launch_bounds__(256) void k_dwp_prep(DwpPrep a)
 {
+    __shared__ int32_t lds[64 * 65];     // g planes: the transpose; sums of x: the wave sums
     const int nrows = a.rows_gx * a.rows_gy;
     int b = blockIdx.x;
     if (b < a.xs_n) {
         const int nb = a.c / 64;
-        dwp_xsums(a.x, a.h, a.w, a.c, a.gmax, a.go.xq, b / nb, b % nb);
+        dwp_xsums(a.x, a.h, a.w, a.c, a.gmax, a.go.xq, b / nb, b % nb, lds);
         return;
     }
     b -= a.xs_n;
@@ -382,7 +391,7 @@ __global__ __launch_bounds__(256) void k_dwp_prep(DwpPrep a)
     }
     const int q = b - nrows;
     dwp_grad_planes(a.g, a.g16, a.n, a.h, a.w, a.co, a.hp, a.wp, a.kp, a.gmax, a.pcode, a.gp, a.gn,
-                    a.go, a.goff_dx != 0, a.goff_dw != 0, q % a.gp_gx, q / a.gp_gx);
+                    a.go, a.goff_dx != 0, a.goff_dw != 0, q % a.gp_gx, q / a.gp_gx, lds);
 }
 
 // ---------------------------------------------------------------------------------------------
