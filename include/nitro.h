@@ -208,6 +208,35 @@ nitro_status nitro_block_backward(nitro_ctx *ctx, const nitro_block_desc *desc,
                                   const int32_t *delta_out, void *state,
                                   const nitro_block_grads *grads, const nitro_block_taps *taps);
 
+/* ------------------------------------------------------------------------------------------ */
+/* One forward layer (thin wrappers over a one-layer block with no pooling and no learning     */
+/* layer: the single-layer workload and unit tests)                                             */
+/* ------------------------------------------------------------------------------------------ */
+
+typedef struct {
+    int32_t n, h, w;       /* batch; input height and width (1, 1 for linear)                  */
+    nitro_layer layer;     /* IntConv2D 3x3 (stride 1, zero padding 1) or IntLinear            */
+    int32_t alpha_inv;     /* NITRO-ReLU inverse slope, >= 2                                    */
+    int32_t round;         /* nitro_round                                                       */
+} nitro_layer_desc;
+
+/* Size in bytes of the layer's state buffer (as nitro_block_query for the one-layer block). */
+nitro_status nitro_layer_query(const nitro_layer_desc *desc, size_t *state_bytes);
+
+/* The layer's forward pass with NITRO-Scaling (SF = 2^8 fan-in, section 3.2.1) and NITRO-ReLU
+ * (section 3.2.2): w int32 (conv KRSC [c_out][3][3][c_in], linear [c_out][c_in]), x int8 NHWC,
+ * a_out int8 NHWC [n][h][w][c_out]; x stays unchanged until the matching backward call. */
+nitro_status nitro_layer_forward(nitro_ctx *ctx, const nitro_layer_desc *desc, const int32_t *w,
+                                 const int8_t *x, int8_t *a_out, void *state);
+
+/* The layer's backward pass from delta, the int32 gradient at its NITRO-ReLU output (shape of
+ * a_out): g = the gradient at z through NITRO-ReLU (section 3.2.2; written to g when not NULL),
+ * dw = the weight gradient (int64, overwritten; section 3.2.1), and, when dx is not NULL, the
+ * int64 gradient at x. EINVAL for a null w, x, a_out, delta, state or dw. */
+nitro_status nitro_layer_backward(nitro_ctx *ctx, const nitro_layer_desc *desc, const int32_t *w,
+                                  const int8_t *x, const int8_t *a_out, const int32_t *delta,
+                                  void *state, int64_t *dw, int32_t *g, int64_t *dx);
+
 /* Output layer on f [n][d] int8: yhat = floor(f W^T / (2^8 d)), e = yhat - 32*onehot(labels),
  * dW = e^T f (int64 [G][d]) -- the global loss gradient of section 3.3. yhat, e may be NULL. */
 nitro_status nitro_head_backward(nitro_ctx *ctx, int32_t n, int32_t d, int32_t n_classes,

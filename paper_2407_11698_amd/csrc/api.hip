@@ -967,6 +967,55 @@ nitro_status nitro_block_backward(nitro_ctx *ctx, const nitro_block_desc *desc,
     return block_backward_impl(ctx, desc, g, params, x, a_out, labels, delta_out, state, grads, taps);
 }
 
+// The one-layer block of a layer call (no pooling, no learning layer).
+static nitro_status layer_block(const nitro_layer_desc *d, nitro_block_desc *b)
+{
+    if (!d) return NITRO_EINVAL;
+    *b = nitro_block_desc{};
+    b->n = d->n;
+    b->h = d->h;
+    b->w = d->w;
+    b->n_layers = 1;
+    b->layer[0] = d->layer;
+    b->alpha_inv = d->alpha_inv;
+    b->round = d->round;
+    return NITRO_OK;
+}
+
+nitro_status nitro_layer_query(const nitro_layer_desc *desc, size_t *state_bytes)
+{
+    nitro_block_desc b;
+    if (layer_block(desc, &b) != NITRO_OK) return NITRO_EINVAL;
+    return nitro_block_query(&b, state_bytes);
+}
+
+nitro_status nitro_layer_forward(nitro_ctx *ctx, const nitro_layer_desc *desc, const int32_t *w,
+                                 const int8_t *x, int8_t *a_out, void *state)
+{
+    nitro_block_desc b;
+    if (layer_block(desc, &b) != NITRO_OK || !w) return NITRO_EINVAL;
+    nitro_block_params p{};
+    p.w[0] = w;
+    return nitro_block_forward(ctx, &b, &p, x, a_out, state);
+}
+
+nitro_status nitro_layer_backward(nitro_ctx *ctx, const nitro_layer_desc *desc, const int32_t *w,
+                                  const int8_t *x, const int8_t *a_out, const int32_t *delta,
+                                  void *state, int64_t *dw, int32_t *g, int64_t *dx)
+{
+    nitro_block_desc b;
+    if (layer_block(desc, &b) != NITRO_OK || !w || !delta || !dw) return NITRO_EINVAL;
+    nitro_block_params p{};
+    p.w[0] = w;
+    nitro_block_grads gr{};
+    gr.dw[0] = dw;
+    nitro_block_taps t{};
+    t.g[0] = g;
+    t.dx = dx;
+    return nitro_block_backward(ctx, &b, &p, x, a_out, nullptr, delta, state, &gr,
+                                g || dx ? &t : nullptr);
+}
+
 nitro_status nitro_head_backward(nitro_ctx *ctx, int32_t n, int32_t d, int32_t n_classes,
                                  const int8_t *f, const int32_t *w, const int32_t *labels,
                                  int32_t round, int64_t *dw, int32_t *yhat, int32_t *e)

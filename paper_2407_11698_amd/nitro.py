@@ -49,6 +49,11 @@ class BlockDesc(ctypes.Structure):
                 ("alpha_inv", I32), ("round", I32), ("d_lr", I32)]
 
 
+class LayerDesc(ctypes.Structure):
+    _fields_ = [("n", I32), ("h", I32), ("w", I32), ("layer", Layer), ("alpha_inv", I32),
+                ("round", I32)]
+
+
 class BlockParams(ctypes.Structure):
     _fields_ = [("w", VP * MAX_LAYERS), ("w_lr", VP)]
 
@@ -106,6 +111,9 @@ def _load():
         "nitro_block_forward_noalloc": (I32, [VP, P(BlockDesc), P(BlockParams), VP, VP]),
         "nitro_block_backward": (I32, [VP, P(BlockDesc), P(BlockParams), VP, VP, VP, VP, VP,
                                        P(BlockGrads), P(BlockTaps)]),
+        "nitro_layer_query": (I32, [P(LayerDesc), P(ctypes.c_size_t)]),
+        "nitro_layer_forward": (I32, [VP, P(LayerDesc), VP, VP, VP, VP]),
+        "nitro_layer_backward": (I32, [VP, P(LayerDesc), VP, VP, VP, VP, VP, VP, VP, VP]),
         "nitro_head_backward": (I32, [VP, I32, I32, I32, VP, VP, VP, I32, VP, VP, VP]),
         "nitro_integer_sgd_step": (I32, [VP, VP, VP, I64, I64, I64, I64, I32]),
         "nitro_block_sgd_step": (I32, [VP, P(BlockDesc), P(BlockWeights), P(BlockGrads), P(HParams)]),
@@ -142,6 +150,7 @@ EXPORTS = ("nitro_create", "nitro_destroy", "nitro_set_stream", "nitro_set_conv_
            "nitro_status_str", "nitro_block_query", "nitro_block_saved", "nitro_block_forward",
            "nitro_block_forward_noalloc",
            "nitro_block_backward",
+           "nitro_layer_query", "nitro_layer_forward", "nitro_layer_backward",
            "nitro_head_backward", "nitro_integer_sgd_step", "nitro_block_sgd_step",
            "nitro_net_block_view", "nitro_net_head_view", "nitro_net_query",
            "nitro_preprocess_query", "nitro_preprocess",
@@ -184,6 +193,22 @@ def block_desc(n: int, h: int, w: int, layers: Sequence[Layer], maxpool: bool, n
     d.round = round_mode
     d.d_lr = d_lr
     return d
+
+
+def layer_desc(n: int, h: int, w: int, ly: Layer, alpha_inv: int,
+               round_mode: int = ROUND_FLOOR) -> LayerDesc:
+    d = LayerDesc()
+    d.n, d.h, d.w = n, h, w
+    d.layer = ly
+    d.alpha_inv = alpha_inv
+    d.round = round_mode
+    return d
+
+
+def layer_query(desc: LayerDesc) -> int:
+    out = ctypes.c_size_t(0)
+    check(LIB.nitro_layer_query(ctypes.byref(desc), ctypes.byref(out)), "nitro_layer_query")
+    return out.value
 
 
 def block_query(desc: BlockDesc) -> int:
@@ -318,6 +343,16 @@ class Context:
             bp.w[j] = _p(w)
         check(LIB.nitro_block_forward_noalloc(self.h, ctypes.byref(desc), ctypes.byref(bp), _p(x),
                                               _p(a_out)), "nitro_block_forward_noalloc")
+
+    def layer_forward(self, desc: LayerDesc, w, x, a_out, state) -> None:
+        check(LIB.nitro_layer_forward(self.h, ctypes.byref(desc), _p(w), _p(x), _p(a_out),
+                                      _p(state)), "nitro_layer_forward")
+
+    def layer_backward(self, desc: LayerDesc, w, x, a_out, delta, state, dw, g=None,
+                       dx=None) -> None:
+        check(LIB.nitro_layer_backward(self.h, ctypes.byref(desc), _p(w), _p(x), _p(a_out),
+                                       _p(delta), _p(state), _p(dw), _p(g), _p(dx)),
+              "nitro_layer_backward")
 
     def block_backward(self, desc: BlockDesc, ws, w_lr, x, a_out, labels, delta_out, state,
                        dws, dw_lr, taps: Optional[dict] = None) -> None:

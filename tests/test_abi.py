@@ -104,6 +104,29 @@ def test_block_query_rejects(bad):
     assert ei.value.code == N.EINVAL
 
 
+def test_layer_query_is_the_one_layer_block():
+    """nitro_layer_query sizes the one-layer block (no pooling, no learning layer) and
+    rejects what nitro_block_query rejects."""
+    for ly, h, w in ((N.layer(N.CONV3X3, 256, 256), 32, 32), (N.layer(N.CONV3X3, 3, 16), 7, 5),
+                     (N.layer(N.LINEAR, 784, 100), 1, 1)):
+        ld = N.layer_desc(8, h, w, ly, 10)
+        bd = N.block_desc(8, h, w, [ly], False, 0, 10)
+        assert N.layer_query(ld) == N.block_query(bd) > 0
+    for bad in (N.layer_desc(0, 8, 8, N.layer(N.CONV3X3, 4, 8), 10),
+                N.layer_desc(2, 8, 8, N.layer(N.CONV3X3, 4, 8), 1),
+                N.layer_desc(2, 8, 8, N.layer(N.LINEAR, 4, 8), 10),
+                N.layer_desc(2, 8, 8, N.layer(N.CONV3X3, 4, 8), 10, round_mode=2)):
+        with pytest.raises(N.NitroError) as ei:
+            N.layer_query(bad)
+        assert ei.value.code == N.EINVAL
+    import ctypes
+    assert N.LIB.nitro_layer_query(None, ctypes.byref(ctypes.c_size_t(0))) == N.EINVAL
+    ld = N.layer_desc(2, 8, 8, N.layer(N.CONV3X3, 4, 8), 10)
+    assert N.LIB.nitro_layer_forward(None, ld, None, None, None, None) == N.EINVAL
+    assert N.LIB.nitro_layer_backward(None, ld, None, None, None, None, None, None, None,
+                                      None) == N.EINVAL
+
+
 def test_net_query_checks_chaining():
     descs = runner.block_descs(WL.VGG_CNN)
     assert N.net_query(N.net_desc(descs, False)) > 0

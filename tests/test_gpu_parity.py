@@ -348,6 +348,51 @@ def test_conv_block_g_offset(ctx, tile, case, modes, tap):
         assert int((g == 32768).sum()) == (plus if top == 32768 else 0)
 
 
+# nitro_layer_forward / nitro_layer_backward: one layer (a one-layer block with no pooling and
+# no learning layer) against the oracle's block functions, with and without the g and dx
+# outputs; the 64-channel conv case draws delta up to 32768 (g in the offset form when dx is
+# asked for).
+LAYER_CASES = [
+    # kind, n, h, w, c_in, c_out, dmax
+    (N.CONV3X3, 2, 8, 8, 16, 32, 1 << 15),
+    (N.CONV3X3, 3, 7, 5, 3, 16, 5000),
+    (N.CONV3X3, 16, 16, 16, 64, 64, 1 << 15),
+    (N.LINEAR, 16, 1, 1, 100, 50, 1 << 15),
+]
+
+
+@pytest.mark.parametrize("outs", ["all", "none"])
+@pytest.mark.parametrize("case", LAYER_CASES)
+@pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
+def test_layer_calls(ctx, case, modes, outs):
+    kind, n, h, w, ci, co, dmax = case
+    print("layer case", case, modes[0], outs, flush=True)
+    rng = np.random.default_rng(hash((kind, n, h, w, ci, co, dmax, 77)) % (1 << 31))
+    conv = kind == N.CONV3X3
+    xs = (n, h, w, ci) if conv else (n, ci)
+    ws = (co, 3, 3, ci) if conv else (co, ci)
+    x = rand(rng, xs, -127, 127, np.int8)
+    wt = rand(rng, ws, -127, 127, np.int32)
+    rec = O.block_forward(x, [wt], False, 10, modes[1])
+    delta = rand(rng, rec.out.shape, -dmax, dmax, np.int32)
+    O.block_backward(rec, [wt], delta, False, 10, modes[1], want_dx=True)
+    desc = N.layer_desc(n, h if conv else 1, w if conv else 1, N.layer(kind, ci, co), 10, modes[0])
+    state = torch.empty(N.layer_query(desc), dtype=torch.uint8, device=DEV)
+    xd, wd = dev(x), dev(wt)
+    a_out = torch.empty(rec.out.shape, dtype=torch.int8, device=DEV)
+    ctx.layer_forward(desc, wd, xd, a_out, state)
+    dw = torch.empty(wt.shape, dtype=torch.int64, device=DEV)
+    g = torch.empty(rec.out.shape, dtype=torch.int32, device=DEV) if outs == "all" else None
+    dx = torch.empty(x.shape, dtype=torch.int64, device=DEV) if outs == "all" else None
+    ctx.layer_backward(desc, wd, xd, a_out, dev(delta), state, dw, g, dx)
+    ctx.sync()
+    assert np.array_equal(host(a_out), rec.out), "output"
+    assert np.array_equal(host(dw), rec.dw[0]), "dW"
+    if outs == "all":
+        assert np.array_equal(host(g), rec.g[0]), "g"
+        assert np.array_equal(host(dx), rec.dx), "dx"
+
+
 @pytest.mark.parametrize("chans,G,wmax", [([784, 100], 10, 7), ([100, 50, 30], 10, 300),
                                           ([37, 5], 3, 20000), ([64, 65], 0, 127)])
 @pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
