@@ -548,11 +548,13 @@ def main():
                                              "workgroups, inside the replayed graph (blocks on "
                                              "four streams)"},
     }
-    if serial:
+    if serial_ev:
         # the dominant kernel class of the serial pass; achieved = its algorithmic ops per step /
-        # its summed launch time per step (= ops per launch / average launch duration)
-        sdom = max(serial, key=lambda k: serial[k]["ms_per_step"])
-        sd = serial[sdom]
+        # its summed launch time per step (= ops per launch / average launch duration), the
+        # launches timed by HIP events on their stream (what a kernel trace of the same command
+        # reports as their durations); the kernels' own device timestamps beside it
+        sdom = max(serial_ev, key=lambda k: serial_ev[k]["ms_per_step"])
+        sd = serial_ev[sdom]
         out["roofline"] = {"bound": "mfma", "kernel": sdom, "achieved": sd["algorithmic_TOPs"],
                            "peak": PEAK_INT8_TOPS, "unit": "TOP/s",
                            "frac": round(sd["algorithmic_TOPs"] / PEAK_INT8_TOPS, 5),
@@ -560,12 +562,13 @@ def main():
                            "launches_per_step": sd["launches_per_step"],
                            "ops_per_step": ops[sdom],
                            "traffic": recorded_traffic(sdom),
-                           "avg_launch_us_events": serial_ev.get(sdom, {}).get("avg_launch_us"),
-                           "timing": "device timestamps of each launch (first workgroup start to "
-                                     "last workgroup end), %d eager iterations of the same "
-                                     "trajectory after the timed region, every block on one "
-                                     "stream; avg_launch_us_events: HIP events around each launch "
-                                     "on its stream in the same setting" % args.serial_steps}
+                           "avg_launch_us_device_timestamps": serial.get(sdom, {}).get("avg_launch_us"),
+                           "timing": "HIP events around each launch on the stream it is launched "
+                                     "on, %d eager iterations of the same trajectory after the "
+                                     "timed region, every block on one stream; "
+                                     "avg_launch_us_device_timestamps: the launches' first "
+                                     "workgroup start to last workgroup end (s_memrealtime) in "
+                                     "the same setting" % args.serial_steps}
         out["conv_mfma"]["serial_per_kernel"] = serial
         out["conv_mfma"]["serial_per_kernel_events"] = serial_ev
     else:
