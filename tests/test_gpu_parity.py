@@ -305,6 +305,7 @@ G_OFFSET_CASES = [
     (16, 16, 16, [64, 64], False, 11, 32768),
     (8, 32, 32, [128, 64], False, 200, 32768),
     (16, 16, 16, [64, 64], False, 20000, 32768),
+    (16, 8, 32, [64, 128], False, 60, 32768),
 ]
 
 
