@@ -194,6 +194,7 @@ struct LayerGeom {
     bool pad16;               // forward on the MFMA GEMM with C_in zero-padded to 16
     bool fwd_tile;            // forward on k_conv_tile (with the padded input when pad16)
     bool dx_tile;             // input gradient on k_conv_tile (g's NHWC limb planes from dW)
+    bool lin_mfma;            // linear: forward and weight gradient on the int8 MFMA GEMM
 };
 
 struct BlockGeom {
@@ -222,6 +223,8 @@ struct BlockGeom {
     size_t g16;                    // an inner layer's gradient in the escaped 16-bit form
     size_t gres, gbias, gxq;       // the first layer's g in the offset form: residual list, bias
                                    // table, sums of x (weight gradient in the form too)
+    size_t nxpad, npart, ngt, nxt; // linear layers on the MFMA GEMM: padded input rows, forward
+                                   // split-K partials, the weight gradient's g^T planes and x^T
     size_t total;
 };
 
@@ -255,6 +258,7 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
         L.sf = 256 * (int64_t)(conv ? 9 * ly.c_in : ly.c_in);
         const bool pool = j == d->n_layers - 1 && d->maxpool;
         L.pad16 = L.fwd_tile = L.dx_tile = false;
+        L.lin_mfma = !conv && linear_mfma_ok(d->n, ly.c_in, ly.c_out);
         if (conv) {
             ConvShape s16 = L.sh;
             if (ly.c_in < 16) s16.c = 16;
@@ -296,7 +300,9 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     int64_t xpadb = 0;
     for (int j = 0; j < g->J; j++) {
         const int64_t nw = conv ? 9 * (int64_t)d->layer[j].c_in * d->layer[j].c_out : 0;
-        const int64_t nwf = g->L[j].pad16 ? 9 * 16 * (int64_t)d->layer[j].c_out : nw;
+        const int64_t nwf = g->L[j].pad16 ? 9 * 16 * (int64_t)d->layer[j].c_out
+                          : g->L[j].lin_mfma ? linear_scratch(d->n, d->layer[j].c_in, d->layer[j].c_out).wf_bytes / 4
+                          : nw;
         g->wf[j] = off; off = align256(off + (size_t)(4 * nwf));
         g->wt[j] = off; off = align256(off + (size_t)(4 * nw));
         if (g->L[j].pad16 && (int64_t)d->n * hw * 16 > xpadb) xpadb = (int64_t)d->n * hw * 16;
@@ -349,6 +355,21 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
     // (an inner layer's g, or the last layer's as the ReLU' pass writes it for the preparation)
     const bool g16_last = conv && dwp_ok(g->L[g->J - 1].sh) && !d->maxpool;
     g->g16 = off;   off = align256(off + (size_t)(g->J > 1 || g16_last ? gmax : 0) * 2);
+    {
+        int64_t xp = 0, pt = 0, gt = 0, xt = 0;
+        for (int j = 0; j < g->J; j++) {
+            if (!g->L[j].lin_mfma) continue;
+            const LinearScratch ls = linear_scratch(d->n, g->L[j].sh.c, g->L[j].sh.co);
+            if (ls.xpad_bytes > xp) xp = ls.xpad_bytes;
+            if (ls.part_bytes > pt) pt = ls.part_bytes;
+            if (ls.gt_bytes > gt) gt = ls.gt_bytes;
+            if (ls.xt_bytes > xt) xt = ls.xt_bytes;
+        }
+        g->nxpad = off; off = align256(off + (size_t)xp);
+        g->npart = off; off = align256(off + (size_t)pt);
+        g->ngt = off;   off = align256(off + (size_t)gt);
+        g->nxt = off;   off = align256(off + (size_t)xt);
+    }
     const bool goff = conv && g->L[0].dx_tile && dwp_ok(g->L[0].sh);
     g->gres = off;  off = align256(off + (goff ? (size_t)GOFF_CAP * 4 : 0));
     g->gbias = off; off = align256(off + (goff ? (size_t)16 * 8 * g->L[0].sh.c : 0));
@@ -433,6 +454,14 @@ nitro_status block_forward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, co
                 launch_conv_fwd_smallc(s, L.sh, cur, p->w[j], sf, rp, pool, out, code);
             else
                 launch_conv_fwd(s, L.sh, cur, p->w[j], sf, rp, pool, out, code);
+        } else if (L.lin_mfma) {
+            const LinearScratch ls = linear_scratch(L.sh.n, L.sh.c, L.sh.co);
+            if (!prepacked)
+                launch_pack_linear_weights(s, p->w[j], L.sh.co, L.sh.c, ls.cip, (int8_t *)at(state, g.wf[j]),
+                                           slots + j * SLOT_WORDS);
+            launch_linear_fwd_mfma(s, L.sh.n, L.sh.c, L.sh.co, cur, (int8_t *)at(state, g.nxpad),
+                                   (const int8_t *)at(state, g.wf[j]), slots + j * SLOT_WORDS, sf, rp, out,
+                                   code, (int64_t *)at(state, g.npart), ctx->flags);
         } else {
             launch_linear_fwd_relu(s, L.sh.n, L.sh.c, L.sh.co, cur, p->w[j], sf, rp, out, code);
         }
@@ -569,6 +598,10 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
                 launch_conv_dw_smallc(s, L.sh, gj, xin, (int64_t *)at(state, g.part), gr->dw[j]);
             else
                 launch_conv_dw(s, L.sh, gj, xin, gr->dw[j]);
+        } else if (L.lin_mfma) {
+            launch_linear_dw_mfma(s, n, L.sh.c, L.sh.co, gj, slots + (4 + j) * SLOT_WORDS, xin,
+                                  (int8_t *)at(state, g.ngt), (int8_t *)at(state, g.nxt), gr->dw[j],
+                                  ctx->flags);
         } else {
             launch_linear_dw(s, n, L.sh.c, L.sh.co, gj, xin, gr->dw[j]);
         }
@@ -1094,6 +1127,10 @@ void net_setup(nitro_ctx *ctx, const nitro_net_desc *net, const NetGeom &g,
             uint32_t *slots = (uint32_t *)at(state, bg.slots);
             for (int j = 0; j < bg.J; j++) {
                 const LayerGeom &L = bg.L[j];
+                if (L.lin_mfma)
+                    pl.add_conv(ctx->stream, params->w[b][j], L.sh.co, L.sh.c,
+                                linear_scratch(L.sh.n, L.sh.c, L.sh.co).cip, (int8_t *)at(state, bg.wf[j]),
+                                nullptr, slots + j * SLOT_WORDS, 1);
                 if (!L.conv) continue;
                 if (!L.pad16 && pack_conv_tiled_ok(L.sh.co, L.sh.c))
                     pl.add(ctx->stream,

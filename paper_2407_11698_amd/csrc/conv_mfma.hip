@@ -49,6 +49,15 @@ void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, i
                            (uint32_t)ci, wt);
 }
 
+void launch_pack_linear_weights(hipStream_t s, const int32_t *w, int co, int ci, int cpad,
+                                int8_t *wf, uint32_t *wmax)
+{
+    // (the element-wise pack of the conv weights with one tap: row r = output, column c < ci)
+    const uint32_t total_pad = (uint32_t)co * (uint32_t)cpad;
+    hipLaunchKernelGGL(k_pack_conv_weights, dim3(grid_stride_blocks(total_pad)), dim3(256), 0, s,
+                       w, total_pad, ci, cpad, wf, wmax);
+}
+
 // x int8 [P][c] -> [P][16] with zero channels c..15 (c < 16): the forward GEMM's K then takes
 // whole 16-channel chunks per tap.
 __global__ __launch_bounds__(256) void k_pad_channels16(const int8_t *__restrict__ x, int P, int c,

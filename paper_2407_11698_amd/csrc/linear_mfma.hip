@@ -424,6 +424,182 @@ __global__ void k_loss_from_partials(const int64_t *__restrict__ part, int nz, i
 }
 
 // ---------------------------------------------------------------------------------------------
+// IntLinear forward layers and their weight gradients on the same tile.
+
+// Split-K partial tiles of C = A B^T (grid: x fastest, then y, then split).
+__global__ __launch_bounds__(256) void k_lgemm_part(LgemmArgs p)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t smem[LG_SMEM];
+    const int gx = (p.M + LG_BM - 1) / LG_BM, gy = (p.N + LG_BN - 1) / LG_BN;
+    const int b = blockIdx.x;
+    lgemm_tile<LIN_PART>(p, smem, b % gx, (b / gx) % gy, b / (gx * gy));
+}
+
+// C = A B^T written as int64 rows (no split).
+__global__ __launch_bounds__(256) void k_lgemm_dw(LgemmArgs p)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t smem[LG_SMEM];
+    const int gx = (p.M + LG_BM - 1) / LG_BM;
+    lgemm_tile<LIN_DW>(p, smem, blockIdx.x % gx, blockIdx.x / gx, 0);
+}
+
+// x int8 [n][ci] -> xpad [n][cip] with zero columns ci..cip-1: thread = 16 bytes of one row.
+__global__ __launch_bounds__(256) void k_pad_rows(const int8_t *__restrict__ x, int n, int ci, int cip,
+                                                  int8_t *__restrict__ xpad)
+{
+    const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int per = cip / 16;
+    if (u >= (int64_t)n * per) return;
+    const int r = (int)(u / per), c0 = (int)(u - (int64_t)r * per) * 16;
+    v4i v = v4i{0, 0, 0, 0};
+    for (int e = 0; e < 16 && c0 + e < ci; e++)
+        v[e >> 2] |= (int)((uint32_t)(uint8_t)x[(int64_t)r * ci + c0 + e] << (8 * (e & 3)));
+    *(v4i *)(xpad + (int64_t)r * cip + c0) = v;
+}
+
+// NITRO-Scaling and NITRO-ReLU of z = the sum of the split partials [nz][n][co] (as the direct
+// kernel: floor or truncated z / SF, then the NITRO-ReLU map and its region code).
+__global__ __launch_bounds__(256) void k_linear_relu_from_partials(const int64_t *__restrict__ part, int nz,
+                                                                   int64_t count, Div sf, Relu rp,
+                                                                   int8_t *__restrict__ out,
+                                                                   uint8_t *__restrict__ code)
+{
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (int64_t)gridDim.x * 256) {
+        int64_t z0 = 0, z1 = 0;
+        int s = 0;
+        for (; s + 1 < nz; s += 2) {
+            z0 += part[(int64_t)s * count + i];
+            z1 += part[(int64_t)(s + 1) * count + i];
+        }
+        if (s < nz) z0 += part[(int64_t)s * count + i];
+        uint8_t reg;
+        const int32_t a = relu_fwd(idiv(z0 + z1, sf), rp, reg);
+        out[i] = (int8_t)a;
+        code[i] = reg;
+    }
+}
+
+// The weight gradient's operands: workgroups 0 .. ng - 1 write g^T's balanced limb planes
+// gt [4][co][np] (thread: one output channel, 16 samples; zero for samples >= n) and fold max|g|
+// into gmax; the rest write x^T [ci][np] (thread: one input channel, 16 samples).
+__global__ __launch_bounds__(256) void k_linear_dw_prep(const int32_t *__restrict__ g, int n, int co,
+                                                        int np, int8_t *__restrict__ gt, uint32_t *gmax,
+                                                        const int8_t *__restrict__ x, int ci,
+                                                        int8_t *__restrict__ xt, int ng)
+{
+    const int q = np / 16;
+    if ((int)blockIdx.x < ng) {
+        const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+        uint32_t mx = 0;
+        if (u < (int64_t)co * q) {
+            const int o = (int)(u % co), s0 = (int)(u / co) * 16;
+            int32_t v[16];
+#pragma unroll
+            for (int e = 0; e < 16; e++) {
+                v[e] = s0 + e < n ? g[(int64_t)(s0 + e) * co + o] : 0;
+                const uint32_t a = abs_u32(v[e]);
+                mx = a > mx ? a : mx;
+            }
+            const int64_t plane = (int64_t)co * np;
+#pragma unroll
+            for (int l = 0; l < 4; l++) {
+                v4i d;
+#pragma unroll
+                for (int k = 0; k < 4; k++) d[k] = (int)limb4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3], l);
+                *(v4i *)(gt + l * plane + (int64_t)o * np + s0) = d;
+            }
+        }
+        block_slot_max(gmax, mx);
+        return;
+    }
+    const int64_t u = (int64_t)(blockIdx.x - ng) * 256 + threadIdx.x;
+    if (u >= (int64_t)ci * q) return;
+    const int c = (int)(u % ci), s0 = (int)(u / ci) * 16;
+    v4i d = v4i{0, 0, 0, 0};
+#pragma unroll
+    for (int e = 0; e < 16; e++)
+        if (s0 + e < n) d[e >> 2] |= (int)((uint32_t)(uint8_t)x[(int64_t)(s0 + e) * ci + c] << (8 * (e & 3)));
+    *(v4i *)(xt + (int64_t)c * np + s0) = d;
+}
+
+bool linear_mfma_ok(int n, int ci, int co)
+{
+    const int64_t cip = (ci + 15) / 16 * 16, np = (n + 15) / 16 * 16;
+    const int64_t lim = (int64_t)1 << 31;
+    return n >= 1 && ci >= 1 && co >= 1 && 4 * (int64_t)co * cip < lim && (int64_t)n * cip < lim &&
+           4 * (int64_t)co * np < lim && (int64_t)ci * np < lim && (int64_t)n * co < lim;
+}
+
+LinearScratch linear_scratch(int n, int ci, int co)
+{
+    LinearScratch s{};
+    s.cip = (ci + 15) / 16 * 16;
+    s.np = (n + 15) / 16 * 16;
+    // forward split-K as the learning layer's: about 256 of K per workgroup, at most 1024
+    // workgroups
+    int splits = (s.cip + 255) / 256;
+    const int tiles = ((n + LG_BM - 1) / LG_BM) * ((co + LG_BN - 1) / LG_BN);
+    if (splits * tiles > 1024) splits = (1024 + tiles - 1) / tiles;
+    if (splits < 1) splits = 1;
+    int kchunk = (s.cip + splits - 1) / splits;
+    kchunk = (kchunk + LG_KC - 1) / LG_KC * LG_KC;
+    s.kchunk = kchunk;
+    s.splits = (s.cip + kchunk - 1) / kchunk;
+    s.wf_bytes = 4 * (int64_t)co * s.cip;
+    s.xpad_bytes = ci % 16 ? (int64_t)n * s.cip : 0;
+    s.part_bytes = 8 * (int64_t)s.splits * n * co;
+    s.gt_bytes = 4 * (int64_t)co * s.np;
+    s.xt_bytes = (int64_t)ci * s.np;
+    return s;
+}
+
+void launch_linear_fwd_mfma(hipStream_t s, int n, int ci, int co, const int8_t *x, int8_t *xpad,
+                            const int8_t *wf, const uint32_t *wmax, const Div &sf, const Relu &rp,
+                            int8_t *out, uint8_t *code, int64_t *part, uint32_t *flags)
+{
+    const LinearScratch sc = linear_scratch(n, ci, co);
+    const int8_t *a = x;
+    if (ci % 16) {
+        const int64_t units = (int64_t)n * (sc.cip / 16);
+        hipLaunchKernelGGL(k_pad_rows, dim3((unsigned)((units + 255) / 256)), dim3(256), 0, s, x, n, ci,
+                           sc.cip, xpad);
+        a = xpad;
+    }
+    LgemmArgs p{};
+    p.M = n; p.N = co; p.K = sc.cip;
+    p.a = a; p.lda = sc.cip;
+    p.b = wf; p.ldb = sc.cip; p.bplane = (int64_t)co * sc.cip; p.b_max = wmax;
+    p.kchunk = sc.kchunk;
+    p.out64 = part;
+    p.flags = flags;
+    const int64_t nwg = (int64_t)((n + LG_BM - 1) / LG_BM) * ((co + LG_BN - 1) / LG_BN) * sc.splits;
+    hipLaunchKernelGGL(k_lgemm_part, dim3((unsigned)nwg), dim3(256), 0, s, p);
+    const int64_t count = (int64_t)n * co;
+    hipLaunchKernelGGL(k_linear_relu_from_partials, dim3(grid_stride_blocks(count)), dim3(256), 0, s,
+                       part, sc.splits, count, sf, rp, out, code);
+}
+
+void launch_linear_dw_mfma(hipStream_t s, int n, int ci, int co, const int32_t *g, uint32_t *gmax,
+                           const int8_t *x, int8_t *gt, int8_t *xt, int64_t *dw, uint32_t *flags)
+{
+    const LinearScratch sc = linear_scratch(n, ci, co);
+    const int q = sc.np / 16;
+    const int ng = (int)(((int64_t)co * q + 255) / 256), nx = (int)(((int64_t)ci * q + 255) / 256);
+    hipLaunchKernelGGL(k_linear_dw_prep, dim3((unsigned)(ng + nx)), dim3(256), 0, s, g, n, co, sc.np,
+                       gt, gmax, x, ci, xt, ng);
+    // dW[o][c] = sum_k gt[o][k] xt[c][k]: M = co, N = ci, K = np (one split)
+    LgemmArgs p{};
+    p.M = co; p.N = ci; p.K = sc.np;
+    p.a = gt; p.lda = sc.np; p.aplane = (int64_t)co * sc.np; p.a_max = gmax;
+    p.b = xt; p.ldb = sc.np; p.bplane = 0; p.b_max = nullptr;
+    p.kchunk = sc.np;
+    p.out64 = dw; p.ldc = ci; p.m_valid = co;
+    p.flags = flags;
+    const int64_t nwg = (int64_t)((co + LG_BM - 1) / LG_BM) * ((ci + LG_BN - 1) / LG_BN);
+    hipLaunchKernelGGL(k_lgemm_dw, dim3((unsigned)nwg), dim3(256), 0, s, p);
+}
+
+// ---------------------------------------------------------------------------------------------
 bool mfma_learning_ok(int n, int64_t d, int G, int c)
 {
     // c: channels of the block output (its 16-column epilogue groups stay inside one pixel)

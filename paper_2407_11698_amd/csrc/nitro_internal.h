@@ -504,6 +504,26 @@ struct LearningBuffers {
     uint32_t *wmax, *emax, *gmax;  // max|W|, max|e|, max|g| slots (zeroed before the call)
 };
 bool mfma_learning_ok(int n, int64_t d, int G, int c);   // c: block output channels
+// IntLinear forward layers (section 3.2.1) on the same GEMM: z = x W^T in split-K partials, then
+// NITRO-Scaling and NITRO-ReLU; their weight gradient dW = g^T x (int64). K (c_in, and the batch
+// for dW) is zero-padded to a multiple of 16.
+struct LinearScratch {
+    int cip, np, splits, kchunk;   // c_in and n rounded up to 16; forward split-K
+    int64_t wf_bytes;              // the weight's limb planes [4][co][cip]
+    int64_t xpad_bytes;            // x with its rows padded to cip (0 when c_in % 16 == 0)
+    int64_t part_bytes;            // forward partials [splits][n][co] int64
+    int64_t gt_bytes, xt_bytes;    // weight gradient: g^T limb planes [4][co][np], x^T [ci][np]
+};
+bool linear_mfma_ok(int n, int ci, int co);
+LinearScratch linear_scratch(int n, int ci, int co);
+// out (int8 [n][co]) and code from x (int8 [n][ci]); wf / wmax from launch_pack_linear_weights.
+void launch_linear_fwd_mfma(hipStream_t s, int n, int ci, int co, const int8_t *x, int8_t *xpad,
+                            const int8_t *wf, const uint32_t *wmax, const Div &sf, const Relu &rp,
+                            int8_t *out, uint8_t *code, int64_t *part, uint32_t *flags);
+// dw (int64 [co][ci], overwritten) = g^T x for g int32 [n][co]; max|g| folded into gmax (a slot
+// that is zero, or already holds max|g|, before the call).
+void launch_linear_dw_mfma(hipStream_t s, int n, int ci, int co, const int32_t *g, uint32_t *gmax,
+                           const int8_t *x, int8_t *gt, int8_t *xt, int64_t *dw, uint32_t *flags);
 LearningScratch learning_scratch(int n, int64_t d, int G);
 // yhat, e, dW of the learning layer on f = the block output [n][d], and the gradient g at the
 // last forward layer's pre-activation (un-pool and NITRO-ReLU backward of delta = e W).
@@ -565,6 +585,9 @@ bool mfma_conv_dx_ok(const ConvShape &sh);
 // [ci][9 co] (wt, optional); max|W| -> the max slot wmax (zeroed first).
 void launch_pack_conv_weights(hipStream_t s, const int32_t *w, int co, int ci, int cpad,
                               int8_t *wf, int8_t *wt, uint32_t *wmax);
+// Linear weight W int32 [co][ci] -> 4 limb planes [co][cpad] (columns ci..cpad-1 zero), max|W|.
+void launch_pack_linear_weights(hipStream_t s, const int32_t *w, int co, int ci, int cpad,
+                                int8_t *wf, uint32_t *wmax);
 // x int8 [P][c] (c < 16) -> [P][16], channels c..15 zero.
 void launch_pad_channels16(hipStream_t s, const int8_t *x, int P, int c, int8_t *xpad);
 void launch_conv_fwd_mfma(hipStream_t s, const ConvShape &sh, const int8_t *x, const int8_t *wf,
@@ -702,6 +725,7 @@ constexpr int PACK_CONV = 4;
 struct ConvPackArgs {
     const int32_t *w;
     uint32_t co, ci, cpad;
+    uint32_t taps;                 // 9 (conv KRSC) or 1 (linear [co][ci])
     int8_t *wf, *wt;
     uint32_t *wmax;
     int nf, nt;                    // workgroups of the plain and of the swapped planes
@@ -720,7 +744,7 @@ struct PackList {
     void add(hipStream_t s, const PackArgs &a, int batches);   // batches: 9 for a conv weight
     // a conv weight packed element-wise (launch_pack_conv_weights' planes and max)
     void add_conv(hipStream_t s, const int32_t *w, int co, int ci, int cpad, int8_t *wf, int8_t *wt,
-                  uint32_t *wmax);
+                  uint32_t *wmax, int taps = 9);
     void flush(hipStream_t s);
 };
 void launch_pack_conv_tiled(hipStream_t s, const int32_t *w, int co, int ci, int8_t *wf,

@@ -79,7 +79,7 @@ __global__ __launch_bounds__(256) void k_pack_batch(PackBatch b)
         for (int k = 0; k < b.nc; k++) {
             const ConvPackArgs &c = b.c[k];
             if (wid < c.nf) {
-                pack_conv_weights_part(c.w, c.co * 9 * c.cpad, (int)c.ci, (int)c.cpad, c.wf, c.wmax,
+                pack_conv_weights_part(c.w, c.co * c.taps * c.cpad, (int)c.ci, (int)c.cpad, c.wf, c.wmax,
                                        (uint32_t)wid, (uint32_t)c.nf);
                 return;
             }
@@ -114,7 +114,7 @@ void PackList::add(hipStream_t s, const PackArgs &a, int batches)
 }
 
 void PackList::add_conv(hipStream_t s, const int32_t *w, int co, int ci, int cpad, int8_t *wf,
-                        int8_t *wt, uint32_t *wmax)
+                        int8_t *wt, uint32_t *wmax, int taps)
 {
     if (b.nc == PACK_CONV) flush(s);
     ConvPackArgs &c = b.c[b.nc++];
@@ -122,11 +122,12 @@ void PackList::add_conv(hipStream_t s, const int32_t *w, int co, int ci, int cpa
     c.co = (uint32_t)co;
     c.ci = (uint32_t)ci;
     c.cpad = (uint32_t)cpad;
+    c.taps = (uint32_t)taps;
     c.wf = wf;
-    c.wt = wt;
+    c.wt = taps == 9 ? wt : nullptr;
     c.wmax = wmax;
-    c.nf = grid_stride_blocks((int64_t)co * 9 * cpad);
-    c.nt = wt ? (int)(((int64_t)co * 9 * ci + 255) / 256) : 0;
+    c.nf = grid_stride_blocks((int64_t)co * taps * cpad);
+    c.nt = c.wt ? (int)(((int64_t)co * 9 * ci + 255) / 256) : 0;
 }
 
 void PackList::flush(hipStream_t s)

@@ -394,13 +394,16 @@ def test_layer_calls(ctx, case, modes, outs):
         assert np.array_equal(host(dx), rec.dx), "dx"
 
 
-@pytest.mark.parametrize("chans,G,wmax", [([784, 100], 10, 7), ([100, 50, 30], 10, 300),
-                                          ([37, 5], 3, 20000), ([64, 65], 0, 127)])
+# (the forward layers and their weight gradients run on the int8 MFMA GEMM with K zero-padded
+# to 16: 100, 50, 37, 3000 are ragged; 3000 and the split-K forward are MLP 4's widths)
+@pytest.mark.parametrize("chans,G,wmax,n", [([784, 100], 10, 7, 64), ([100, 50, 30], 10, 300, 5),
+                                            ([37, 5], 3, 20000, 5), ([64, 65], 0, 127, 5),
+                                            ([1024, 3000], 10, 40, 16), ([3000, 3000], 10, 3000, 7),
+                                            ([3000, 1000, 200], 0, 127, 3)])
 @pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
-def test_linear_block(ctx, chans, G, wmax, modes):
-    rng = np.random.default_rng(len(chans) * 1000 + chans[0])
-    run_block(ctx, rng, 64 if chans[0] == 784 else 5, 1, 1, chans, False, G, 10, modes[0],
-              modes[1], wmax=wmax, conv=False)
+def test_linear_block(ctx, chans, G, wmax, n, modes):
+    rng = np.random.default_rng(len(chans) * 1000 + chans[0] + chans[1])
+    run_block(ctx, rng, n, 1, 1, chans, False, G, 10, modes[0], modes[1], wmax=wmax, conv=False)
 
 
 # conv blocks whose learning layer reads the block output max-pooled to at most d_lr features
