@@ -365,6 +365,7 @@ nitro_status block_geom(const nitro_block_desc *d, BlockGeom *g)
             if (ls.gt_bytes > gt) gt = ls.gt_bytes;
             if (ls.xt_bytes > xt) xt = ls.xt_bytes;
         }
+
         g->nxpad = off; off = align256(off + (size_t)xp);
         g->npart = off; off = align256(off + (size_t)pt);
         g->ngt = off;   off = align256(off + (size_t)gt);
@@ -512,6 +513,7 @@ nitro_status block_backward_impl(nitro_ctx *ctx, const nitro_block_desc *desc, c
     if (G > 0) {
         int32_t *yhat = (int32_t *)at(state, g.yhat);
         int32_t *e = (int32_t *)at(state, g.e);
+
         const Div sf = make_div(256 * g.d, desc->round);
         if (g.lr_mfma) {
             LearningBuffers lb;

@@ -197,7 +197,18 @@ __device__ inline int64_t wave_sum_i64(int64_t v)
 __device__ inline int64_t linear_point(const int8_t *x, const int32_t *w, int k, int lane)
 {
     int64_t acc = 0;
-    for (int t = lane; t < k; t += 64) acc += (int64_t)x[t] * (int64_t)w[t];
+    if ((k & 3) == 0) {
+        // (rows of a multiple of 4: each lane takes 4 inputs per step, one dword of x and four
+        // weights in one 16-byte load)
+        for (int t = lane; t < (k >> 2); t += 64) {
+            const int xv = *(const int *)(x + 4 * t);
+            const v4i wv = *(const v4i *)(w + 4 * t);
+            acc += (int64_t)(int8_t)xv * wv[0] + (int64_t)(int8_t)(xv >> 8) * wv[1] +
+                   (int64_t)(int8_t)(xv >> 16) * wv[2] + (int64_t)(xv >> 24) * wv[3];
+        }
+    } else {
+        for (int t = lane; t < k; t += 64) acc += (int64_t)x[t] * (int64_t)w[t];
+    }
     return wave_sum_i64(acc);
 }
 
@@ -332,6 +343,8 @@ __global__ void k_linear_dw(int n, int k, int m, const int32_t *__restrict__ e,
     if (i >= (int64_t)m * k) return;
     int row = (int)(i / k), col = (int)(i % k);
     int64_t acc = 0;
+    // (unrolled: the loads of 8 samples are requested before their products)
+#pragma unroll 8
     for (int t = 0; t < n; t++) acc += (int64_t)e[(int64_t)t * m + row] * (int64_t)x[(int64_t)t * k + col];
     dw[i] = acc;
 }

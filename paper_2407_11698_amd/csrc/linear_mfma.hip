@@ -452,8 +452,16 @@ __global__ __launch_bounds__(256) void k_pad_rows(const int8_t *__restrict__ x, 
     if (u >= (int64_t)n * per) return;
     const int r = (int)(u / per), c0 = (int)(u - (int64_t)r * per) * 16;
     v4i v = v4i{0, 0, 0, 0};
-    for (int e = 0; e < 16 && c0 + e < ci; e++)
-        v[e >> 2] |= (int)((uint32_t)(uint8_t)x[(int64_t)r * ci + c0 + e] << (8 * (e & 3)));
+    const int8_t *src = x + (int64_t)r * ci + c0;
+    if ((ci & 3) == 0) {
+        // (dword loads: rows of a multiple of 4 bytes keep them aligned)
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+            if (c0 + 4 * q < ci) v[q] = *(const int *)(src + 4 * q);
+    } else {
+        for (int e = 0; e < 16 && c0 + e < ci; e++)
+            v[e >> 2] |= (int)((uint32_t)(uint8_t)src[e] << (8 * (e & 3)));
+    }
     *(v4i *)(xpad + (int64_t)r * cip + c0) = v;
 }
 

@@ -57,18 +57,35 @@ __device__ inline void pack_conv_weights_part(const int32_t *__restrict__ w, uin
                                               uint32_t bid, uint32_t nb)
 {
     uint32_t m = 0;
-    for (uint32_t i = bid * 256 + threadIdx.x; i < total; i += nb * 256) {
-        int32_t v;
-        if (cpad == ci) {
-            v = w[i];
-        } else {
+    if ((ci & 3) == 0 && (cpad & 3) == 0) {
+        // four elements of one row per step: 16-byte loads, one dword per limb plane
+        for (uint32_t i = (bid * 256 + threadIdx.x) * 4; i < total; i += nb * 256 * 4) {
             const uint32_t c = i % (uint32_t)cpad, row = i / (uint32_t)cpad;
-            v = (int)c < ci ? w[row * ci + c] : 0;
-        }
-        const uint32_t a = abs_u32(v);
-        m = a > m ? a : m;
+            v4i v = v4i{0, 0, 0, 0};
+            if ((int)c < ci) v = *(const v4i *)(w + (int64_t)row * ci + c);
 #pragma unroll
-        for (int l = 0; l < 4; l++) wf[(int64_t)l * total + i] = limb1(v, l);
+            for (int e = 0; e < 4; e++) {
+                const uint32_t a = abs_u32(v[e]);
+                m = a > m ? a : m;
+            }
+#pragma unroll
+            for (int l = 0; l < 4; l++)
+                *(uint32_t *)(wf + (int64_t)l * total + i) = limb4(v[0], v[1], v[2], v[3], l);
+        }
+    } else {
+        for (uint32_t i = bid * 256 + threadIdx.x; i < total; i += nb * 256) {
+            int32_t v;
+            if (cpad == ci) {
+                v = w[i];
+            } else {
+                const uint32_t c = i % (uint32_t)cpad, row = i / (uint32_t)cpad;
+                v = (int)c < ci ? w[row * ci + c] : 0;
+            }
+            const uint32_t a = abs_u32(v);
+            m = a > m ? a : m;
+#pragma unroll
+            for (int l = 0; l < 4; l++) wf[(int64_t)l * total + i] = limb1(v, l);
+        }
     }
     block_slot_max(wmax, m);
 }
