@@ -417,6 +417,7 @@ LR_POOL_CASES = [
     (1, 5, 6, [8, 16], False, 4, 250),
     (2, 16, 16, [32, 64, 64], True, 10, 1024),
     (2, 8, 8, [16, 32], True, 10, 100000),
+    (2, 8, 8, [16, 6], False, 10, 64),       # 6 channels: the one-channel-per-thread kernels
 ]
 
 
