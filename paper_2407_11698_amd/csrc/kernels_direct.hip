@@ -199,7 +199,8 @@ __device__ inline int64_t linear_point(const int8_t *x, const int32_t *w, int k,
     int64_t acc = 0;
     if ((k & 3) == 0) {
         // (rows of a multiple of 4: each lane takes 4 inputs per step, one dword of x and four
-        // weights in one 16-byte load)
+        // weights in one 16-byte load; four steps' loads requested together)
+#pragma unroll 4
         for (int t = lane; t < (k >> 2); t += 64) {
             const int xv = *(const int *)(x + 4 * t);
             const v4i wv = *(const v4i *)(w + 4 * t);
