@@ -182,14 +182,16 @@ nitro_status nitro_block_forward(nitro_ctx *ctx, const nitro_block_desc *desc,
  * loops, harnesses that forbid allocation): nitro_block_forward without the caller's state
  * buffer. Computes the same a_out (forward layers, NITRO-Scaling, NITRO-ReLU, pool; section 3.2).
  * Everything else the forward pass writes (inner activations, region codes, weight limb planes,
- * max slots, a channel-padded input) goes to a library-owned device array of 64 MiB per device,
+ * max slots, a channel-padded input, the split-K partial sums and padded input rows of linear
+ * layers on the int8 MFMA GEMM) goes to a library-owned device array of 64 MiB per device,
  * allocated with the library's code and held until the process ends; the call allocates and
  * frees nothing. Nothing in that array is meant for the caller, and no nitro_block_backward can
  * follow from it. NITRO_EUNSUPPORTED when the block needs more than 64 MiB of it (the forward
  * part of nitro_block_query's state: about 2 bytes per inner and last-layer activation plus the
- * weight planes), NITRO_EHIP if the array's device address could not be found when the context
- * was created. Every call on a device shares that device's array: calls that overlap on one
- * device (other streams or contexts) race on it; calls ordered on one stream do not. */
+ * weight planes, and for linear layers 8 bytes per output per K split), NITRO_EHIP if the
+ * array's device address could not be found when the context was created. Every call on a
+ * device shares that device's array: calls that overlap on one device (other streams or
+ * contexts) race on it; calls ordered on one stream do not. */
 nitro_status nitro_block_forward_noalloc(nitro_ctx *ctx, const nitro_block_desc *desc,
                                          const nitro_block_params *params, const int8_t *x,
                                          int8_t *a_out);

@@ -962,10 +962,25 @@ nitro_status nitro_block_forward_noalloc(nitro_ctx *ctx, const nitro_block_desc 
     if (st != NITRO_OK) return st;
     for (int j = 0; j < g.J; j++)
         if (!params->w[j]) return NITRO_EINVAL;
-    // the forward pass uses the front of the block state: saved activations and codes, weight
-    // limb planes, the channel-padded input and the max slots (the backward's scratch follows);
-    // the size is checked before the context, so that the limit holds whatever else is wrong
-    const size_t need = align256(g.slots + 16 * SLOT_WORDS * 4);
+    // the forward pass uses the front of the block state (saved activations and codes, weight
+    // limb planes, the channel-padded input and the max slots) and, for linear layers on the
+    // MFMA GEMM, their padded rows and split-K partials, which the block state keeps among the
+    // backward's scratch: here they move to just behind the max slots. The size is checked
+    // before the context, so that the limit holds whatever else is wrong.
+    BlockGeom gf = g;
+    size_t need = align256(g.slots + 16 * SLOT_WORDS * 4);
+    {
+        int64_t xp = 0, pt = 0;
+        for (int j = 0; j < g.J; j++) {
+            if (!g.L[j].lin_mfma) continue;
+            const LinearScratch ls = linear_scratch(desc->n, g.L[j].sh.c, g.L[j].sh.co);
+            if (ls.xpad_bytes > xp) xp = ls.xpad_bytes;
+            if (ls.part_bytes > pt) pt = ls.part_bytes;
+        }
+        gf.nxpad = need;
+        gf.npart = align256(gf.nxpad + (size_t)xp);
+        need = align256(gf.npart + (size_t)pt);
+    }
     if (need > NOALLOC_SCRATCH_BYTES) return NITRO_EUNSUPPORTED;
     if (!ctx) return NITRO_EINVAL;
     DeviceGuard guard(ctx->device);
@@ -974,10 +989,10 @@ nitro_status nitro_block_forward_noalloc(nitro_ctx *ctx, const nitro_block_desc 
     TimerScope timer(ctx);
     // the max slots start at zero: cleared by a kernel (no memset node if the caller captures)
     SlotList sl{};
-    sl.p[0] = (uint32_t *)at(state, g.slots);
+    sl.p[0] = (uint32_t *)at(state, gf.slots);
     sl.words = 8 * SLOT_WORDS;
     launch_zero_slots(ctx->stream, sl, 1);
-    return block_forward_impl(ctx, desc, g, params, x, a_out, state, false, false, false, false);
+    return block_forward_impl(ctx, desc, gf, params, x, a_out, state, false, false, false, false);
 }
 
 nitro_status nitro_block_backward(nitro_ctx *ctx, const nitro_block_desc *desc,

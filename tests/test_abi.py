@@ -163,5 +163,11 @@ def test_noalloc_forward_size_limit():
     vgg1 = N.block_desc(256, 32, 32, [N.layer(N.CONV3X3, 3, 64), N.layer(N.CONV3X3, 64, 64)],
                         True, 0, 10)
     assert N.LIB.nitro_block_forward_noalloc(None, vgg1, bp, one, one) == N.EINVAL
+    # an MLP block whose max slots end at about 14 MB but whose split-K partials of the MFMA
+    # linear forward need 67 MB more: the check counts them (their room sits behind the slots)
+    bp.w[2] = 1
+    mlp = N.block_desc(2048, 1, 1, [N.layer(N.LINEAR, 784, 1024), N.layer(N.LINEAR, 1024, 1024)],
+                       False, 0, 10)
+    assert N.LIB.nitro_block_forward_noalloc(None, mlp, bp, one, one) == N.EUNSUPPORTED
     bp.w[1] = None
     assert N.LIB.nitro_block_forward_noalloc(None, small, bp, one, one) == N.EINVAL

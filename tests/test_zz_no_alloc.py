@@ -24,10 +24,13 @@ CASES = [
     [(8, 32, 32, [3, 64, 64], True, 44), (2, 32, 32, [3, 64, 64], True, 44)],
     [(4, 16, 16, [64, 128, 128], False, 6000), (1, 8, 8, [64, 128, 128], False, 6000)],
     [(64, 1, 1, [784, 100, 50], False, 300), (5, 1, 1, [784, 100, 50], False, 300)],
+    # an MLP block whose full block state (about 80 MB) exceeds the 64 MiB array while its forward
+    # part (about 52 MB, mostly the MFMA linear forward's split-K partials) fits
+    [(4096, 1, 1, [64, 512, 512, 512, 512], False, 40), (1000, 1, 1, [64, 512, 512, 512, 512], False, 40)],
 ]
 
 
-@pytest.mark.parametrize("calls", CASES, ids=["vgg_block", "wide_weights", "mlp"])
+@pytest.mark.parametrize("calls", CASES, ids=["vgg_block", "wide_weights", "mlp", "mlp_big_state"])
 def test_noalloc_matches_block_forward(calls):
     ctx = N.Context(0)
     try:
@@ -47,6 +50,8 @@ def test_noalloc_matches_block_forward(calls):
             ref = torch.empty(shape, dtype=torch.int8, device=DEV)
             got = torch.full(shape, 77, dtype=torch.int8, device=DEV)
             state = torch.empty(N.block_query(desc), dtype=torch.uint8, device=DEV)
+            if n == 4096:
+                assert state.numel() > 64 << 20
             ctx.block_forward(desc, ws, x, ref, state)
             ctx.block_forward_noalloc(desc, ws, x, got)
             ctx.sync()
