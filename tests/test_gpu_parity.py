@@ -143,6 +143,9 @@ CONV_CASES = [
     (1, 4, 4, [128, 256], True, 100, 10, 9),
     (2, 8, 8, [64, 128, 128], True, 100, 16, 6000),
     (1, 32, 32, [3, 64, 64], True, 100, 10, 44),
+    # one-pixel-high and 1x1 images: every tap but the centre (or the centre row) in the padding
+    (3, 1, 5, [16, 16], False, 4, 10, 127),
+    (2, 1, 1, [8, 32, 16], False, 10, 10, 127),
 ]
 
 
@@ -395,11 +398,13 @@ def test_layer_calls(ctx, case, modes, outs):
 
 
 # (the forward layers and their weight gradients run on the int8 MFMA GEMM with K zero-padded
-# to 16: 100, 50, 37, 3000 are ragged; 3000 and the split-K forward are MLP 4's widths)
+# to 16: 100, 50, 37, 3000 are ragged; 3000 and the split-K forward are MLP 4's widths; a batch
+# of one with one output unit, and one input feature)
 @pytest.mark.parametrize("chans,G,wmax,n", [([784, 100], 10, 7, 64), ([100, 50, 30], 10, 300, 5),
                                             ([37, 5], 3, 20000, 5), ([64, 65], 0, 127, 5),
                                             ([1024, 3000], 10, 40, 16), ([3000, 3000], 10, 3000, 7),
-                                            ([3000, 1000, 200], 0, 127, 3)])
+                                            ([3000, 1000, 200], 0, 127, 3), ([17, 1], 2, 127, 1),
+                                            ([1, 16], 3, 127, 2)])
 @pytest.mark.parametrize("modes", MODES, ids=["floor", "trunc"])
 def test_linear_block(ctx, chans, G, wmax, n, modes):
     rng = np.random.default_rng(len(chans) * 1000 + chans[0] + chans[1])
