@@ -62,7 +62,7 @@ typedef enum {
     NITRO_ELABEL = -3,        /* a label outside [0, G)                                       */
     NITRO_EHIP = -4,          /* a HIP runtime call failed                                    */
     NITRO_ENOMEM = -5,        /* a device allocation failed                                   */
-    NITRO_EUNSUPPORTED = -6   /* valid but not supported by this build (e.g. too many blocks)*/
+    NITRO_EUNSUPPORTED = -6   /* valid but not supported by the library (e.g. too many blocks) */
 } nitro_status;
 
 typedef enum { NITRO_ROUND_FLOOR = 0, NITRO_ROUND_TRUNC = 1 } nitro_round;

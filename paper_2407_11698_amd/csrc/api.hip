@@ -803,7 +803,7 @@ const char *nitro_status_str(nitro_status s)
     case NITRO_ELABEL: return "label outside [0, G)";
     case NITRO_EHIP: return "HIP runtime error";
     case NITRO_ENOMEM: return "out of device memory";
-    case NITRO_EUNSUPPORTED: return "unsupported by this build";
+    case NITRO_EUNSUPPORTED: return "unsupported by the library";
     }
     return "unknown status";
 }
